@@ -1,0 +1,298 @@
+"""Plain CPU oracle for DynaSpec's dynamic draft head (arXiv 2510.13847).
+
+TEST INFRASTRUCTURE ONLY.  This module is the slow, obviously-correct
+definition the HIP library is checked against.  Only the test-suite, the
+smoke check and the CPU-baseline leg of the benchmark may import it; the
+library never calls it and shares no code, table or helper with it.
+
+Everything is evaluated in float64 from the exact input values: fp32 arrays
+are widened, bf16 inputs arrive as raw uint16 bit patterns and are decoded
+here (a bf16 value is the upper half of an fp32 word, so the decode is exact).
+
+The path, in the paper's order (Sec. 4.2 "Context-aware dynamic sub-vocabulary
+selection", Sec. 4.3 "Dynamic Drafting", Algorithm 1):
+
+  partition      V = disjoint union of clusters C_1..C_M          (Sec. 4.2, "Vocabulary partition")
+  router         s = r_theta(x), a small FFN                       (Sec. 4.2, "Low-cost router"; "Training the router")
+  top-k          K = TopK_k(s)                                     (Sec. 4.2)
+  shortlist      V_S = disjoint union of C_m over m in K           (Sec. 4.2)
+  logits         z = h . W_LM[:, V_S]  (gathered head)             (Sec. 4.3; Algorithm 1, FUSED_INDEX_GEMM)
+  select         log_softmax over V_S, TopK_{k_t}, remap to ids    (Algorithm 1; Sec. 5 restricted draft q_S)
+
+Readings where the paper is silent (each is listed in the design notes):
+  * the LM head is stored [V, d] row-major: paper column v is row v;
+  * ties in any top-k go to the lower id (cluster id for routing, vocabulary
+    id for tokens); NaN scores count as -inf; -0 equals +0;
+  * the shortlist is ordered by ascending cluster id, then ascending
+    vocabulary id inside a cluster;
+  * log-probabilities and sampling use softmax(z / T) over the shortlist
+    (T = 1 gives Algorithm 1's log_softmax(z)); sampling walks the CDF in
+    shortlist order and returns the first j with F_j > u, else the last j
+    with p_j > 0;
+  * the router's hidden activation is not re-rounded (fp64 here).
+
+Every function below has a pin in tests/test_oracle_pins.py.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+ACTS = ("none", "relu", "silu")
+
+
+# --------------------------------------------------------------------------
+# input decoding
+# --------------------------------------------------------------------------
+def as_f64(a) -> np.ndarray:
+    """float64 view of an input: fp32/fp64 values, or bf16 bit patterns (uint16)."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    if a.dtype in (np.float32, np.float64):
+        return a.astype(np.float64)
+    raise TypeError(f"unsupported input dtype {a.dtype}")
+
+
+# --------------------------------------------------------------------------
+# vocabulary partition (Sec. 4.2, "Vocabulary partition")
+# --------------------------------------------------------------------------
+def cluster_layout(cluster_of, M: int):
+    """Cluster-contiguous layout of a partition of the vocabulary.
+
+    The paper partitions V into M disjoint clusters with no balance
+    constraint.  Laid out cluster by cluster (ascending cluster id, ascending
+    vocabulary id inside each cluster), every cluster is one contiguous run.
+
+    Returns (sizes[M], offsets[M+1], perm[V], cap_by_k[M+1]):
+      perm[j]     vocabulary id stored at layout row j;
+      offsets[m]  first layout row of cluster m;
+      cap_by_k[k] largest possible shortlist of k clusters (sum of the k
+                  largest cluster sizes).
+    """
+    cluster_of = np.asarray(cluster_of, dtype=np.int64)
+    if cluster_of.size and (cluster_of.min() < 0 or cluster_of.max() >= M):
+        raise ValueError("cluster id out of range")
+    sizes = np.bincount(cluster_of, minlength=M).astype(np.int64)
+    offsets = np.zeros(M + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(sizes)
+    perm = np.argsort(cluster_of, kind="stable").astype(np.int64)
+    cap_by_k = np.zeros(M + 1, dtype=np.int64)
+    cap_by_k[1:] = np.cumsum(np.sort(sizes)[::-1])
+    return sizes, offsets, perm, cap_by_k
+
+
+# --------------------------------------------------------------------------
+# router (Sec. 4.2, "Low-cost router" and "Training the router")
+# --------------------------------------------------------------------------
+def activation(a: np.ndarray, act: str) -> np.ndarray:
+    if act == "none":
+        return a
+    if act == "relu":
+        return np.maximum(a, 0.0)
+    if act == "silu":
+        return a / (1.0 + np.exp(-a))
+    raise ValueError(act)
+
+
+def router_scores(x, W1, W2=None, b1=None, b2=None, act: str = "silu") -> np.ndarray:
+    """Cluster scores s[B, M] from context features x[B, d_r].
+
+    Two-layer FFN: s = W2 . act(W1 . x + b1) + b2, with W1 [H, d_r] and
+    W2 [M, H].  With W2 = None the router is one linear map s = W1 . x + b1,
+    W1 [M, d_r].  The sigmoid of the training loss is not part of scoring
+    (top-k is invariant to it).
+    """
+    x = as_f64(x)
+    W1 = as_f64(W1)
+    pre = x @ W1.T
+    if b1 is not None:
+        pre = pre + as_f64(b1)
+    if W2 is None:
+        return pre
+    a = activation(pre, act)
+    s = a @ as_f64(W2).T
+    if b2 is not None:
+        s = s + as_f64(b2)
+    return s
+
+
+# --------------------------------------------------------------------------
+# ordering rule shared by every top-k of the path (a reading, see header)
+# --------------------------------------------------------------------------
+def _canonical(values: np.ndarray) -> np.ndarray:
+    v = np.where(np.isnan(values), -np.inf, values)
+    return v + 0.0  # -0 + 0 = +0 under round-to-nearest
+
+
+def rank_order(values, ids) -> np.ndarray:
+    """Indices that sort (values desc, ids asc)."""
+    v = _canonical(np.asarray(values, dtype=np.float64))
+    return np.lexsort((np.asarray(ids), -v))
+
+
+# --------------------------------------------------------------------------
+# top-k clusters (Sec. 4.2, K(c,t) = TopK_{k_c(t)}(s))
+# --------------------------------------------------------------------------
+def topk_clusters(scores, k: int):
+    """Per row, the k clusters with the highest scores, in rank order.
+
+    Returns (ids[B, k], vals[B, k]).
+    """
+    s = np.atleast_2d(np.asarray(scores, dtype=np.float64))
+    B, M = s.shape
+    if not 1 <= k <= M:
+        raise ValueError("k out of range")
+    ids = np.empty((B, k), dtype=np.int64)
+    vals = np.empty((B, k), dtype=np.float64)
+    for b in range(B):
+        order = rank_order(s[b], np.arange(M))[:k]
+        ids[b] = order
+        vals[b] = s[b, order]
+    return ids, vals
+
+
+# --------------------------------------------------------------------------
+# shortlist (Sec. 4.2, V_S = disjoint union of the selected clusters)
+# --------------------------------------------------------------------------
+def shortlist(cluster_ids, offsets, perm):
+    """Shortlist of one context from its selected cluster ids.
+
+    Returns (sel_sorted[k], rowoff[k+1], layout_rows[n], vocab_ids[n]):
+    clusters in ascending id, the start of each cluster inside the
+    shortlist, the layout rows of the shortlist, and their vocabulary ids.
+    """
+    sel = np.sort(np.asarray(cluster_ids, dtype=np.int64))
+    offsets = np.asarray(offsets, dtype=np.int64)
+    sizes = offsets[sel + 1] - offsets[sel]
+    rowoff = np.zeros(sel.size + 1, dtype=np.int64)
+    rowoff[1:] = np.cumsum(sizes)
+    rows = np.concatenate([np.arange(offsets[m], offsets[m + 1]) for m in sel]) \
+        if sel.size else np.zeros(0, dtype=np.int64)
+    return sel, rowoff, rows, np.asarray(perm, dtype=np.int64)[rows]
+
+
+# --------------------------------------------------------------------------
+# gathered head (Sec. 4.3; Algorithm 1, FUSED_INDEX_GEMM)
+# --------------------------------------------------------------------------
+def shortlist_logits(h, W_lm, vocab_ids) -> np.ndarray:
+    """z[j] = h . W_LM[:, vocab_ids[j]] for one context row h[d].
+
+    Read from the original (vocabulary-ordered) LM head, never from the
+    permuted copy, so a layout error cannot hide in both sides.
+    """
+    Wg = as_f64(np.asarray(W_lm)[np.asarray(vocab_ids, dtype=np.int64)])
+    return Wg @ as_f64(h)
+
+
+# --------------------------------------------------------------------------
+# draft selection (Algorithm 1: log_softmax, TopK_{k_t}, remap2realid;
+# Sec. 5: the restricted, renormalised draft q_S)
+# --------------------------------------------------------------------------
+def log_softmax(z, temperature: float = 1.0) -> np.ndarray:
+    """log q_S over the shortlist: z/T - log(sum exp(z/T)), shifted by the max."""
+    t = np.asarray(z, dtype=np.float64) / float(temperature)
+    mx = np.max(t)
+    return t - (mx + np.log(np.sum(np.exp(t - mx))))
+
+
+def topk_tokens(z, vocab_ids, k_t: int):
+    """Positions of the k_t largest logits, ordered (z desc, vocabulary id asc)."""
+    order = rank_order(z, vocab_ids)
+    return order[:k_t]
+
+
+def sample_inverse_cdf(z, u: float, temperature: float = 1.0) -> int:
+    """Shortlist position drawn from softmax(z/T) by the inverse CDF at u.
+
+    The CDF runs in shortlist order; the answer is the first j with F_j > u,
+    else (when rounding leaves F_n <= u) the last j with p_j > 0.
+    """
+    t = np.asarray(z, dtype=np.float64) / float(temperature)
+    p = np.exp(t - np.max(t))
+    p = p / p.sum()
+    F = np.cumsum(p)
+    hit = np.nonzero(F > u)[0]
+    if hit.size:
+        return int(hit[0])
+    return int(np.nonzero(p > 0)[0][-1])
+
+
+def sample_cdf(z, temperature: float = 1.0) -> np.ndarray:
+    """Normalised CDF in shortlist order (used to find near-boundary uniforms)."""
+    t = np.asarray(z, dtype=np.float64) / float(temperature)
+    p = np.exp(t - np.max(t))
+    return np.cumsum(p / p.sum())
+
+
+def draft_select(z, vocab_ids, k_t: int = 1, temperature: float = 1.0, u=None):
+    """Draft outputs of one context over its shortlist.
+
+    Returns dict(ids[k_t], logprobs[k_t], positions[k_t], sample_id,
+    sample_pos, sample_logprob); ids are vocabulary ids (remap2realid).
+    """
+    vocab_ids = np.asarray(vocab_ids, dtype=np.int64)
+    lp = log_softmax(z, temperature)
+    pos = topk_tokens(z, vocab_ids, k_t)
+    out = dict(ids=vocab_ids[pos], logprobs=lp[pos], positions=pos)
+    if u is not None:
+        j = sample_inverse_cdf(z, float(u), temperature)
+        out.update(sample_id=int(vocab_ids[j]), sample_pos=j, sample_logprob=float(lp[j]))
+    return out
+
+
+# --------------------------------------------------------------------------
+# whole head and the two baselines
+# --------------------------------------------------------------------------
+def draft_head(x, h, W1, W2, act, cluster_of, M, W_lm, k, k_t=1, temperature=1.0,
+               u=None, b1=None, b2=None):
+    """The dynamic draft head for a batch: route, shortlist, logits, select.
+
+    Returns a list (one dict per context row) with the router's cluster ids,
+    the shortlist and the draft outputs.
+    """
+    sizes, offsets, perm, _ = cluster_layout(cluster_of, M)
+    s = router_scores(x, W1, W2, b1, b2, act)
+    ids, vals = topk_clusters(s, k)
+    h = np.atleast_2d(np.asarray(h))
+    out = []
+    for b in range(h.shape[0]):
+        sel, rowoff, rows, vids = shortlist(ids[b], offsets, perm)
+        z = shortlist_logits(h[b], W_lm, vids)
+        r = draft_select(z, vids, k_t, temperature, None if u is None else u[b])
+        r.update(clusters=ids[b], cluster_scores=vals[b], sel_sorted=sel, rowoff=rowoff,
+                 layout_rows=rows, vocab_ids=vids, logits=z, scores=s[b])
+        out.append(r)
+    return out
+
+
+def dense_head(h, W_lm, k_t=1, temperature=1.0, u=None, n_rows=None):
+    """Full-vocabulary head O = H W_LM (Sec. 4.1), or, with n_rows, the static
+    head over the first n_rows vocabulary ids (Sec. 4.1, the FR-Spec drafter,
+    with an id prefix standing in for the frequency ranking)."""
+    W = np.asarray(W_lm)
+    if n_rows is not None:
+        W = W[:n_rows]
+    vids = np.arange(W.shape[0])
+    h = np.atleast_2d(np.asarray(h))
+    Wf = as_f64(W)
+    out = []
+    for b in range(h.shape[0]):
+        z = Wf @ as_f64(h[b])
+        r = draft_select(z, vids, k_t, temperature, None if u is None else u[b])
+        r["logits"] = z
+        out.append(r)
+    return out
+
+
+# --------------------------------------------------------------------------
+# position-aware cluster budget (Sec. 4.2, eq. pos_schedule; Algorithm 1)
+# --------------------------------------------------------------------------
+def k_schedule(t: int, k0: int, k1: int, k_min: int = 1) -> int:
+    """Cluster budget at draft position t: k0, k1, then floor((k1 + t) / (2t)),
+    clamped below at k_min (the equation reaches 0 for large t while the
+    text bounds the budget by k_min)."""
+    if t == 0:
+        return k0
+    if t == 1:
+        return k1
+    return max(k_min, (k1 + t) // (2 * t))

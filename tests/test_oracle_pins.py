@@ -1,0 +1,311 @@
+"""Pins for the CPU oracle: each check ties it to something other than itself.
+
+Sources of truth used here: hand-worked examples (tests/golden), closed forms,
+invariants of the partition and the shortlist, special cases that reduce to a
+different library routine (torch's Linear/SiLU, Python's sorted, numpy's
+argmax, scipy's log_softmax), and brute force on tiny vocabularies by a
+different route (masking the dense head instead of gathering rows).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import dynaspec_oracle as O
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")))
+
+
+def _num(v):
+    return float("nan") if v == "nan" else float(v)
+
+
+# ---------------------------------------------------------------- decoding
+def test_bf16_decode_hand_values():
+    bits = np.array([0x3F80, 0xC000, 0x3FC0, 0x0000, 0x8000, 0x7F80, 0x0001], dtype=np.uint16)
+    got = O.as_f64(bits)
+    assert got[0] == 1.0 and got[1] == -2.0 and got[2] == 1.5
+    assert got[3] == 0.0 and np.signbit(got[4]) and got[5] == np.inf
+    assert got[6] == 2.0 ** -133  # smallest bf16 subnormal: 2^-126 * 2^-7
+
+
+def test_bf16_decode_matches_torch_conversion():
+    rng = np.random.default_rng(1)
+    bits = rng.integers(0, 1 << 16, size=4096, dtype=np.uint16)
+    bits = bits[((bits >> 7) & 0xFF) != 0xFF]  # drop inf/nan patterns
+    ref = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.as_f64(bits), ref)
+
+
+# ---------------------------------------------------------------- partition
+def test_layout_hand_example():
+    g = GOLD["layout"]
+    sizes, offsets, perm, cap = O.cluster_layout(np.array(g["cluster_of"]), g["M"])
+    assert sizes.tolist() == g["sizes"]
+    assert offsets.tolist() == g["offsets"]
+    assert perm.tolist() == g["perm"]
+    assert cap.tolist() == g["cap_by_k"]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_layout_is_disjoint_covering_and_contiguous(seed):
+    rng = np.random.default_rng(seed)
+    V, M = 997, 37
+    cluster_of = rng.integers(0, M, size=V)
+    cluster_of[cluster_of == 5] = 6  # force an empty cluster
+    sizes, offsets, perm, cap = O.cluster_layout(cluster_of, M)
+    assert sorted(perm.tolist()) == list(range(V))          # bijection
+    assert offsets[0] == 0 and offsets[-1] == V
+    assert np.all(np.diff(offsets) >= 0)
+    assert sizes[5] == 0
+    for m in range(M):                                      # each run is exactly C_m, ascending
+        run = perm[offsets[m]:offsets[m + 1]].tolist()
+        assert run == [v for v in range(V) if cluster_of[v] == m]
+    # cap_by_k[k] is the best sum of k sizes (brute force over all k-subsets for small k)
+    from itertools import combinations
+    small = sizes[:9]
+    _, _, _, cap9 = O.cluster_layout(np.repeat(np.arange(9), small), 9)
+    for k in range(1, 4):
+        assert cap9[k] == max(sum(c) for c in combinations(small.tolist(), k))
+
+
+def test_layout_rejects_bad_ids():
+    with pytest.raises(ValueError):
+        O.cluster_layout(np.array([0, 3]), 3)
+    with pytest.raises(ValueError):
+        O.cluster_layout(np.array([0, -1]), 3)
+
+
+# ---------------------------------------------------------------- router
+def test_router_relu_hand_example():
+    g = GOLD["router_relu"]
+    x, W1, W2 = np.array(g["x"]), np.array(g["W1"], float), np.array(g["W2"], float)
+    np.testing.assert_array_equal(O.router_scores(x, W1, W2, act="relu"), g["scores_no_bias"])
+    np.testing.assert_array_equal(
+        O.router_scores(x, W1, W2, b1=np.array(g["b1"]), b2=np.array(g["b2"]), act="relu"),
+        g["scores_with_bias"])
+
+
+def test_router_linear_hand_example():
+    g = GOLD["router_linear"]
+    got = O.router_scores(np.array(g["x"]), np.array(g["W1"], float), None, act="none")
+    np.testing.assert_array_equal(got, g["scores"])
+
+
+def test_silu_closed_form():
+    g = GOLD["silu"]
+    np.testing.assert_allclose(O.activation(np.array(g["a"]), "silu"), g["silu"], rtol=1e-15)
+    a = np.linspace(-20, 20, 81)
+    # silu(a) - silu(-a) = a  (sigmoid(a) + sigmoid(-a) = 1)
+    np.testing.assert_allclose(O.activation(a, "silu") - O.activation(-a, "silu"), a, atol=1e-12)
+
+
+@pytest.mark.parametrize("act", ["relu", "silu"])
+def test_router_matches_torch_modules(act):
+    rng = np.random.default_rng(3)
+    d_r, H, M, B = 24, 16, 12, 5  # non-square everywhere: a transposed operand cannot fit
+    x = rng.standard_normal((B, d_r))
+    W1, b1 = rng.standard_normal((H, d_r)), rng.standard_normal(H)
+    W2, b2 = rng.standard_normal((M, H)), rng.standard_normal(M)
+    l1, l2 = torch.nn.Linear(d_r, H).double(), torch.nn.Linear(H, M).double()
+    with torch.no_grad():
+        l1.weight.copy_(torch.from_numpy(W1)); l1.bias.copy_(torch.from_numpy(b1))
+        l2.weight.copy_(torch.from_numpy(W2)); l2.bias.copy_(torch.from_numpy(b2))
+        mod = torch.nn.Sequential(l1, torch.nn.ReLU() if act == "relu" else torch.nn.SiLU(), l2)
+        ref = mod(torch.from_numpy(x)).numpy()
+    np.testing.assert_allclose(O.router_scores(x, W1, W2, b1, b2, act), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_router_bf16_inputs_decode_exactly():
+    # a bf16 weight matrix must give the same scores as its exact fp64 values
+    rng = np.random.default_rng(4)
+    W = torch.from_numpy(rng.standard_normal((6, 8)).astype(np.float32)).to(torch.bfloat16)
+    x = torch.from_numpy(rng.standard_normal((2, 8)).astype(np.float32)).to(torch.bfloat16)
+    bits = lambda t: t.view(torch.int16).numpy().view(np.uint16)
+    ref = x.double().numpy() @ W.double().numpy().T
+    np.testing.assert_array_equal(O.router_scores(bits(x), bits(W), None, act="none"), ref)
+
+
+# ---------------------------------------------------------------- top-k
+def test_topk_hand_ties_nan():
+    g = GOLD["topk_ties"]
+    s = np.array([_num(v) for v in g["scores"]])
+    for k in (3, 4, 6):
+        assert O.topk_clusters(s, k)[0][0].tolist() == g[f"k{k}"]
+
+
+def test_topk_signed_zero_equal():
+    assert O.topk_clusters(np.array([-0.0, 0.0, -1.0]), 1)[0][0].tolist() == [0]
+    assert O.topk_clusters(np.array([0.0, -0.0, -1.0]), 2)[0][0].tolist() == [0, 1]
+    assert O.topk_clusters(np.array([np.nan, -np.inf]), 1)[0][0].tolist() == [0]
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_topk_matches_python_sorted_and_argmax(seed):
+    rng = np.random.default_rng(seed)
+    M = 23
+    s = rng.integers(-3, 4, size=(6, M)).astype(float)  # many ties
+    for k in (1, 5, M):
+        ids, vals = O.topk_clusters(s, k)
+        for b in range(s.shape[0]):
+            ref = sorted(range(M), key=lambda i: (-s[b, i], i))[:k]
+            assert ids[b].tolist() == ref
+            assert vals[b].tolist() == [s[b, i] for i in ref]
+    ids, _ = O.topk_clusters(s, 1)
+    assert ids[:, 0].tolist() == np.argmax(s, axis=1).tolist()  # numpy: first maximum
+
+
+# ---------------------------------------------------------------- shortlist
+@pytest.mark.parametrize("seed", range(4))
+def test_shortlist_is_exact_union(seed):
+    rng = np.random.default_rng(seed)
+    V, M, k = 300, 17, 5
+    cluster_of = rng.integers(0, M, size=V)
+    sizes, offsets, perm, cap = O.cluster_layout(cluster_of, M)
+    K = rng.choice(M, size=k, replace=False)
+    sel, rowoff, rows, vids = O.shortlist(K, offsets, perm)
+    members = {v for v in range(V) if cluster_of[v] in set(K.tolist())}   # brute force
+    assert set(vids.tolist()) == members and len(vids) == len(members)
+    assert sel.tolist() == sorted(K.tolist())
+    assert rowoff[-1] == len(members) <= cap[k]
+    # ascending cluster id, then ascending vocabulary id inside a cluster
+    key = [(cluster_of[v], v) for v in vids.tolist()]
+    assert key == sorted(key)
+    for i, m in enumerate(sel):
+        assert rowoff[i + 1] - rowoff[i] == sizes[m]
+        assert np.all(perm[rows[rowoff[i]:rowoff[i + 1]]] == vids[rowoff[i]:rowoff[i + 1]])
+
+
+# ---------------------------------------------------------------- logits
+def test_logits_one_hot_head_reads_back_h():
+    # W_LM rows are unit vectors e_{v mod d}: z[j] must equal h[vocab_ids[j] mod d]
+    V, d = 40, 16
+    W = np.zeros((V, d)); W[np.arange(V), np.arange(V) % d] = 1.0
+    h = np.arange(d, dtype=float) * 1.5 - 7.0
+    vids = np.array([3, 17, 39, 0, 22])
+    np.testing.assert_array_equal(O.shortlist_logits(h, W, vids), h[vids % d])
+
+
+def test_logits_rank_one_head():
+    # W_LM = a c^T  =>  z[j] = a[v_j] (c . h)
+    rng = np.random.default_rng(5)
+    a, c, h = rng.standard_normal(50), rng.standard_normal(12), rng.standard_normal(12)
+    vids = rng.choice(50, size=9, replace=False)
+    ch = sum(ci * hi for ci, hi in zip(c, h))
+    np.testing.assert_allclose(O.shortlist_logits(h, np.outer(a, c), vids), a[vids] * ch, rtol=1e-12)
+
+
+def test_logits_integer_exact():
+    rng = np.random.default_rng(6)
+    W = rng.integers(-8, 9, size=(30, 11)); h = rng.integers(-8, 9, size=11)
+    vids = np.array([29, 0, 14])
+    exact = [sum(int(W[v, i]) * int(h[i]) for i in range(11)) for v in vids]
+    assert O.shortlist_logits(h.astype(float), W.astype(float), vids).tolist() == exact
+
+
+# ---------------------------------------------------------------- select
+def test_select_hand_example():
+    g = GOLD["select"]
+    p, vids = np.array(g["probs"]), np.array(g["vocab_ids"])
+    z = np.log(p) + 3.0  # any shift gives the same q_S
+    r = O.draft_select(z, vids, k_t=2)
+    assert r["positions"].tolist() == g["top2_positions"] and r["ids"].tolist() == g["top2_ids"]
+    np.testing.assert_allclose(np.exp(O.log_softmax(z)), p, rtol=1e-14)
+    for u, pos in g["u_to_position"]:
+        assert O.sample_inverse_cdf(z, u) == pos
+        assert O.sample_inverse_cdf(2.0 * z, u, temperature=2.0) == pos  # z/T unchanged
+
+
+def test_select_tie_goes_to_lower_vocab_id():
+    g = GOLD["select_ties"]
+    assert O.topk_tokens(np.array(g["z"]), np.array(g["vocab_ids"]), 3).tolist() == g["top3_positions"]
+
+
+def test_sampling_fallback_and_zero_mass():
+    z = np.array([0.0, -np.inf])
+    assert O.sample_inverse_cdf(z, 0.5) == 0
+    assert O.sample_inverse_cdf(z, 1.0) == 0  # no F_j > u: last j with p_j > 0
+
+
+def test_sampling_grid_frequencies_equal_probabilities():
+    rng = np.random.default_rng(7)
+    z = rng.standard_normal(9)
+    p = np.exp(z - z.max()); p /= p.sum()
+    N = 20000
+    counts = np.bincount([O.sample_inverse_cdf(z, (i + 0.5) / N) for i in range(N)], minlength=9)
+    assert np.all(np.abs(counts - p * N) <= 1.0)
+
+
+def test_logprobs_normalised():
+    rng = np.random.default_rng(8)
+    z = rng.standard_normal(1000) * 4
+    lp = O.log_softmax(z, 0.7)
+    assert np.all(lp <= 0)
+    assert abs(np.exp(lp).sum() - 1.0) < 1e-12
+    from scipy.special import log_softmax as ref
+    np.testing.assert_allclose(lp, ref(z / 0.7), rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------- whole head, brute force
+def _tiny_problem(seed, V=16, M=4, d=6, B=3, H=5):
+    rng = np.random.default_rng(seed)
+    cluster_of = rng.permutation(np.arange(V) % M)
+    W = rng.standard_normal((V, d)); h = rng.standard_normal((B, d))
+    W1, W2 = rng.standard_normal((H, d)), rng.standard_normal((M, H))
+    u = rng.random(B)
+    return cluster_of, W, h, W1, W2, u
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_head_matches_masked_dense_head_every_k(seed):
+    from scipy.special import log_softmax as ref_lsm
+    V, M = 16, 4
+    cluster_of, W, h, W1, W2, u = _tiny_problem(seed, V=V, M=M)
+    s = O.router_scores(h, W1, W2, act="silu")
+    for k in range(1, M + 1):
+        out = O.draft_head(h, h, W1, W2, "silu", cluster_of, M, W, k, k_t=3, u=u)
+        for b, r in enumerate(out):
+            chosen = sorted(range(M), key=lambda m: (-s[b, m], m))[:k]      # brute force routing
+            mask = np.isin(cluster_of, chosen)
+            zfull = W @ h[b]
+            zm = np.where(mask, zfull, -np.inf)
+            top = sorted(np.nonzero(mask)[0].tolist(), key=lambda v: (-zfull[v], v))[:3]
+            assert r["ids"].tolist() == top[:min(3, mask.sum())]
+            lsm = ref_lsm(zm)
+            np.testing.assert_allclose(r["logprobs"], lsm[r["ids"]], rtol=1e-12)
+            np.testing.assert_allclose(r["logits"], zfull[r["vocab_ids"]], rtol=1e-12)
+            # sampled token: walk the masked distribution in layout order
+            order = sorted(np.nonzero(mask)[0].tolist(), key=lambda v: (cluster_of[v], v))
+            p = np.exp(lsm[order]); F = np.cumsum(p)
+            assert r["sample_id"] == order[int(np.nonzero(F > u[b])[0][0])]
+
+
+def test_k_equals_M_is_the_dense_head():
+    V, M = 64, 8
+    cluster_of, W, h, W1, W2, u = _tiny_problem(11, V=V, M=M, d=10, B=4)
+    dyn = O.draft_head(h, h, W1, W2, "silu", cluster_of, M, W, M, k_t=5)
+    dense = O.dense_head(h, W, k_t=5)
+    for i, (a, b) in enumerate(zip(dyn, dense)):
+        assert sorted(a["vocab_ids"].tolist()) == list(range(V))
+        assert a["ids"].tolist() == b["ids"].tolist()
+        np.testing.assert_allclose(a["logprobs"], b["logprobs"], rtol=1e-12)
+        np.testing.assert_allclose(a["logits"], b["logits"][a["vocab_ids"]], rtol=1e-12)
+        assert a["ids"][0] == int(np.argmax(W @ h[i]))
+
+
+def test_static_head_is_the_dense_head_on_a_prefix():
+    rng = np.random.default_rng(12)
+    W, h = rng.standard_normal((50, 7)), rng.standard_normal((2, 7))
+    st = O.dense_head(h, W, k_t=4, n_rows=20)
+    for b in range(2):
+        z = W @ h[b]
+        assert st[b]["ids"].tolist() == sorted(range(20), key=lambda v: (-z[v], v))[:4]
+
+
+def test_k_schedule_closed_form():
+    g = GOLD["k_schedule"]
+    assert [O.k_schedule(t, g["k0"], g["k1"]) for t in range(10)] == g["t_0_to_9"]
+    assert O.k_schedule(100, 64, 32) == 1  # clamped at k_min
