@@ -1,0 +1,270 @@
+"""Benchmark of the dynamic draft head on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+
+One step = one dyna_draft_head call (route -> top-k -> shortlist -> gathered
+logits -> select) for one batch of contexts.  The default workload is the
+Llama-3-8B-shaped chain step (V=128256, d=4096, bf16, M=1024 clusters, router
+4096->1024->1024, k=32, B=1, greedy).  Inputs are synthetic and resident in
+HBM before timing; every step uses a different context batch and rotates over
+replicas of the permuted LM head and router, so a step's slabs are not left in
+the 256 MB last-level cache by an earlier step.  Steps are replayed from a
+captured HIP graph (no host launch cost inside the timed region).
+
+Printed: one JSON line with steps/s, the dominant kernel's roofline (bytes it
+must move / its event-timed duration) and the CPU oracle on a bounded sample,
+plus the dense full-vocabulary head and a static fixed-shortlist head timed
+the same way on the same GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+PEAK_HBM_GBS = 8000.0
+N_REPLICAS = 4
+POOL = 64
+GRAPH_CHUNK = 256
+
+
+def mode_of(w, D):
+    m = 0
+    for name, flag in (("argmax", D.SEL_ARGMAX), ("topk", D.SEL_TOPK), ("sample", D.SEL_SAMPLE)):
+        if name in w.modes:
+            m |= flag
+    return m
+
+
+def capture(fn_steps, torch):
+    """Capture a list of step closures into one CUDA/HIP graph."""
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for f in fn_steps:  # warm the closures outside capture once
+            f()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for f in fn_steps:
+            f()
+    torch.cuda.synchronize()
+    return g
+
+
+def time_graph_steps(make_step, K, torch):
+    """Time exactly K steps replayed from graphs of up to GRAPH_CHUNK steps."""
+    full, rem = divmod(K, GRAPH_CHUNK)
+    g_full = capture([make_step(i) for i in range(GRAPH_CHUNK)], torch) if full else None
+    g_rem = capture([make_step(i) for i in range(rem)], torch) if rem else None
+    if g_full:
+        g_full.replay()
+    if g_rem:
+        g_rem.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(full):
+        g_full.replay()
+    if g_rem:
+        g_rem.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return e0.elapsed_time(e1) / 1e3, wall
+
+
+def cpu_baseline(w, cluster_of, host, budget_s=12.0, max_steps=50):
+    """The oracle, as it stands, on a bounded number of steps of the same workload."""
+    from oracle import dynaspec_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    n = 0
+    t0 = time.perf_counter()
+    while n < max_steps and (time.perf_counter() - t0) < budget_s:
+        i = n % host["x"].shape[0]
+        O.draft_head(host["x"][i], host["x"][i], host["W1"], host["W2"], w.act, cluster_of, w.M,
+                     host["W_lm"], w.k, k_t=w.k_t, u=host["u"][i])
+        n += 1
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "steps/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n} steps of {w.name} (B={w.B}) on the host, fp64 numpy oracle"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="llama3_8b_chain", choices=W.WORKLOAD_ORDER)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--no-baselines", action="store_true", help="skip dense/static heads")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the head shards by context rows with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2510_13847_amd import dynahead as D
+
+    D.lib()
+    dev = "cuda"
+    w = W.WORKLOADS[args.workload]
+    mode = mode_of(w, D)
+    k_t = w.k_t if mode & D.SEL_TOPK else 1
+    print(f"[bench] {w.name}: V={w.V} d={w.d} M={w.M} H={w.H} k={w.k} B={w.B}", file=sys.stderr,
+          flush=True)
+
+    # ---------------- inputs (device) ----------------
+    cluster_of = W.partition(w)
+    W_lm = W.lm_head(w, dev)
+    W1, W2 = W.router_weights(w, dev)
+    L0 = D.build_layout(torch.from_numpy(cluster_of).to(dev), W_lm, w.M)
+    layouts = [L0] + [L0.with_weights(L0.W_perm.clone()) for _ in range(N_REPLICAS - 1)]
+    routers = [D.Router(W1, W2, act=w.act)] + [
+        D.Router(W1.clone(), None if W2 is None else W2.clone(), act=w.act)
+        for _ in range(N_REPLICAS - 1)]
+    xs = [W.contexts(w, dev, salt=i) for i in range(POOL)]
+    us = [W.uniforms(w, dev, salt=i) for i in range(POOL)]
+    head = D.DraftHead(routers[0], L0, w.B, w.k, mode, k_t, keep_logits=False)
+    torch.cuda.synchronize()
+
+    def make_step(i):
+        L, R, x, u = layouts[i % N_REPLICAS], routers[i % N_REPLICAS], xs[i % POOL], us[i % POOL]
+        return lambda: head(x, x, u, layout=L, router=R)
+
+    # ---------------- algorithmic bytes per context set ----------------
+    sizes = np.diff(L0.offsets.cpu().numpy().astype(np.int64))
+    s_w = 2 if w.dtype == "bf16" else 4
+    router_bytes = s_w * (w.d_r * w.H + w.H * w.M) if w.H else s_w * w.d_r * w.M
+    slab_bytes, rows = [], []
+    for i in range(POOL):
+        head(xs[i], xs[i], us[i])
+        cl = head.clusters.cpu().numpy()
+        union = np.unique(cl)
+        slab_bytes.append(s_w * w.d * int(sizes[union].sum()))
+        rows.append(int(sizes[cl].sum()))
+    act_bytes = s_w * w.B * (w.d_r + w.d)
+    mean_slab = float(np.mean(slab_bytes))
+    step_bytes = router_bytes + mean_slab + act_bytes
+    mean_rows = float(np.mean(rows))  # shortlisted rows per step, summed over contexts
+
+    # ---------------- warmup + timed steps ----------------
+    for i in range(args.warmup):
+        make_step(i)()
+    torch.cuda.synchronize()
+    gpu_s, wall_s = time_graph_steps(make_step, args.steps, torch)
+    steps_per_s = args.steps / gpu_s
+
+    # ---------------- dominant kernel: gathered head, event-timed ----------------
+    n_kt = min(args.steps, 512)
+    D.set_option(D.OPT_KERNEL_TIMING, 1)
+    D.kernel_timing(reset=True)
+    for i in range(n_kt):
+        make_step(i)()
+    torch.cuda.synchronize()
+    k_ms, k_n = D.kernel_timing(reset=True)
+    D.set_option(D.OPT_KERNEL_TIMING, 0)
+    k_avg_s = k_ms / 1e3 / max(k_n, 1)
+    # bytes one launch must move: each distinct selected slab once, the
+    # contexts' h rows, and the logits it writes
+    k_bytes = float(np.mean([slab_bytes[i % POOL] for i in range(n_kt)])) + s_w * w.B * w.d \
+        + 4.0 * float(np.mean([rows[i % POOL] for i in range(n_kt)]))
+    achieved = k_bytes / k_avg_s / 1e9
+
+    rec = {
+        "metric": "draft-head steps/s (dynamic vocabulary head, 1 GPU)",
+        "value": round(steps_per_s, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(gpu_s * 1e3 / args.steps, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "V": w.V, "d": w.d, "M": w.M, "router": [w.d_r, w.H, w.M],
+                   "k": w.k, "B": w.B, "select": list(w.modes), "k_t": k_t,
+                   "replicas": N_REPLICAS, "context_pool": POOL, "timing": "hip graph replay"},
+        "rows_per_s": round(mean_rows * steps_per_s, 1),
+        "step_bytes": int(step_bytes),
+        "step_GBps": round(step_bytes * steps_per_s / 1e9, 1),
+        "step_frac_hbm_peak": round(step_bytes * steps_per_s / 1e9 / PEAK_HBM_GBS, 4),
+        "wall_s": round(wall_s, 4),
+        "roofline": {"kernel": "rowdot (gathered head)", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "bytes_per_launch": int(k_bytes), "avg_launch_us": round(k_avg_s * 1e6, 3),
+                     "launches": int(k_n)},
+    }
+
+    # ---------------- baselines on the same GPU ----------------
+    if not args.no_baselines:
+        base = {}
+        Ws = [W_lm] + [W_lm.clone() for _ in range(N_REPLICAS - 1)]
+        for label, n_rows in (("dense", w.V), ("static", min(w.static_prefix, w.V))):
+            dh = D.DenseHead(W_lm, n_rows, w.B, mode, k_t)
+
+            def mk(i, dh=dh):
+                Wi, x, u = Ws[i % N_REPLICAS], xs[i % POOL], us[i % POOL]
+                return lambda: dh(x, u, W=Wi)
+            K = max(20, min(200, args.steps // 5))
+            g_s, _ = time_graph_steps(mk, K, torch)
+            bytes_ = s_w * n_rows * w.d + s_w * w.B * w.d
+            base[label] = {"rows": n_rows, "steps_per_s": round(K / g_s, 2),
+                           "ms_per_step": round(g_s * 1e3 / K, 5),
+                           "GBps": round(bytes_ * K / g_s / 1e9, 1)}
+        # vendor GEMV/GEMM + argmax as a reference for the dense head
+        K = 50
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for i in range(5):
+            torch.argmax(xs[i % POOL] @ Ws[i % N_REPLICAS].T, dim=-1)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(K):
+            torch.argmax(xs[i % POOL] @ Ws[i % N_REPLICAS].T, dim=-1)
+        e1.record()
+        torch.cuda.synchronize()
+        base["dense_torch_matmul_argmax"] = {"ms_per_step": round(e0.elapsed_time(e1) / K, 5)}
+        dense_ms = base["dense"]["ms_per_step"]
+        dense_bytes = s_w * w.V * w.d + s_w * w.B * w.d
+        rec["baselines"] = base
+        rec["speedup_vs_dense"] = round(dense_ms / rec["ms_per_step"], 3)
+        rec["byte_ratio_dense_over_dynamic"] = round(dense_bytes / step_bytes, 3)
+
+    # ---------------- CPU oracle on a bounded sample ----------------
+    if not args.no_cpu:
+        host = {
+            "x": np.stack([W.host_array(xs[i]) for i in range(8)]),
+            "u": np.stack([us[i].cpu().numpy().astype(np.float64) for i in range(8)]),
+            "W1": W.host_array(W1),
+            "W2": None if W2 is None else W.host_array(W2),
+            "W_lm": W.host_array(W_lm),
+        }
+        rec["cpu_baseline"] = cpu_baseline(w, cluster_of, host)
+
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

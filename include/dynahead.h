@@ -1,0 +1,259 @@
+/*
+ * libdynahead -- the dynamic vocabulary draft head of DynaSpec
+ * (arXiv 2510.13847), as hand-written HIP kernels for AMD CDNA4 (gfx950).
+ *
+ * One draft step for B contexts (Sec. 4.2 and Sec. 4.3 of the paper,
+ * Algorithm 1 in its appendix):
+ *
+ *   route       s_b = r(x_b)                      scores over M token clusters
+ *   top-k       K_b = TopK_k(s_b)                 the k best clusters per context
+ *   shortlist   S_b = disjoint union of C_m, m in K_b
+ *   logits      z_b = h_b . W_LM[:, S_b]          only the shortlisted LM-head rows
+ *   select      log_softmax over S_b, top-k_t / argmax / inverse-CDF sample,
+ *               mapped back to vocabulary ids
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers are device pointers unless the argument says "host".  The
+ *    library never allocates, frees or copies caller memory on the hot calls;
+ *    scratch space comes from a caller workspace sized by dyna_workspace_bytes.
+ *  - Matrices are row-major.  The paper's LM head W_LM in R^{d x |V|} is held
+ *    as a [V, d] array: paper column v is row v (d contiguous elements).
+ *  - Every argument check runs on the host before any HIP call; a failed
+ *    check returns a status and leaves device memory untouched.
+ *  - Hot-path calls (everything except dyna_build_layout) are asynchronous
+ *    on the given stream and never synchronise; faults inside kernels surface
+ *    at the caller's next synchronisation.
+ *  - Ordering rules: every top-k breaks ties toward the lower id (cluster id
+ *    when routing, vocabulary id when selecting tokens); NaN counts as -inf;
+ *    -0 equals +0.  A context's shortlist is ordered by ascending cluster id,
+ *    then ascending vocabulary id inside each cluster (= layout order).
+ *  - Results are bit-identical from run to run (no floating-point atomics).
+ *  - Calls are thread-safe for distinct workspaces; dyna_last_error() is
+ *    per host thread.
+ */
+#ifndef DYNAHEAD_H
+#define DYNAHEAD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DYNA_ABI_VERSION 1
+#define DYNA_MAX_M 8192     /* clusters */
+#define DYNA_MAX_KT 64      /* tokens per context in top-k output */
+
+typedef enum {
+    DYNA_OK = 0,
+    DYNA_ERR_INVALID_ARG = 1,  /* null pointer, bad size, bad enum, misaligned */
+    DYNA_ERR_CAPACITY = 2,     /* cap smaller than the largest possible shortlist */
+    DYNA_ERR_WORKSPACE = 3,    /* workspace smaller than dyna_*workspace_bytes */
+    DYNA_ERR_UNSUPPORTED = 4,  /* valid request outside what the kernels handle */
+    DYNA_ERR_HIP = 5,          /* a HIP runtime call or launch failed */
+    DYNA_ERR_DEVICE_DATA = 6   /* device-resident input failed a check (build_layout) */
+} dyna_status;
+
+typedef enum { DYNA_F32 = 0, DYNA_BF16 = 1 } dyna_dtype;
+
+/* Router hidden activation.  The paper's router is a two-layer FFN with ReLU
+ * (Sec. 4.2, "Training the router"); SiLU is offered for routers trained so. */
+typedef enum { DYNA_ACT_NONE = 0, DYNA_ACT_RELU = 1, DYNA_ACT_SILU = 2 } dyna_act;
+
+/* Selection modes, combinable bit flags (Algorithm 1: TopK_{k_t} of the
+ * log-softmax over the shortlist; sampling draws from the restricted,
+ * renormalised draft q_S of Sec. 5 with tail weight beta = 0). */
+enum { DYNA_SEL_ARGMAX = 1, DYNA_SEL_TOPK = 2, DYNA_SEL_SAMPLE = 4 };
+
+/* Cluster-contiguous LM head produced once by dyna_build_layout
+ * (Sec. 4.2, "Vocabulary partition": V is the disjoint union of M clusters
+ * of unconstrained sizes).  Layout row j holds vocabulary id perm[j];
+ * cluster m occupies rows [offsets[m], offsets[m+1]). */
+typedef struct dyna_layout {
+    int32_t V, d, M;
+    int32_t wdtype;            /* dyna_dtype of W_perm */
+    const void* W_perm;        /* device [V, d], 16-byte aligned */
+    const int32_t* perm;       /* device [V] */
+    const int32_t* offsets;    /* device [M + 1] */
+    const int32_t* cap_by_k;   /* HOST [M + 1]: sum of the k largest cluster sizes */
+    int32_t max_cluster;       /* largest cluster size */
+} dyna_layout;
+
+/* Router r: R^{d_r} -> R^M (Sec. 4.2, "Low-cost router").
+ * H > 0: s = W2 . act(W1 . x + b1) + b2, W1 [H, d_r], W2 [M, H].
+ * H = 0: s = W1 . x + b1, W1 [M, d_r] (a single linear map).
+ * The hidden activation is kept in fp32 (never re-rounded to bf16). */
+typedef struct dyna_router {
+    int32_t d_r, H, M;
+    int32_t wdtype;            /* dyna_dtype of W1 and W2 */
+    int32_t act;               /* dyna_act (ignored when H == 0) */
+    const void* W1;            /* device, 16-byte aligned */
+    const float* b1;           /* device [H] (or [M] when H == 0), may be NULL */
+    const void* W2;            /* device [M, H]; NULL when H == 0 */
+    const float* b2;           /* device [M], may be NULL */
+} dyna_router;
+
+/* ------------------------------------------------------------------ */
+/* One-time layout (Sec. 4.2, "Vocabulary partition").                  */
+/* ------------------------------------------------------------------ */
+
+size_t dyna_layout_workspace_bytes(int32_t V, int32_t M);
+
+/* Permute the LM head so that every cluster is a contiguous slab.
+ *  cluster_of [V]  device int32, cluster id of each vocabulary token
+ *  W_lm [V, d]     device, dtype wdtype, row v = paper column v
+ *  W_perm [V, d]   device output, row j = W_lm row perm[j]
+ *  perm [V]        device output: ascending cluster id, then ascending vocabulary id
+ *  offsets [M+1]   device output: CSR start of each cluster (offsets[M] = V)
+ *  cap_by_k_host   HOST output [M + 1] (cap_by_k[0] = 0)
+ *  max_cluster_host HOST output, may be NULL
+ * Synchronises `stream` before returning.  A cluster id outside [0, M)
+ * gives DYNA_ERR_DEVICE_DATA (outputs are then unspecified).  Empty clusters
+ * are allowed. */
+dyna_status dyna_build_layout(const int32_t* cluster_of, int32_t V, int32_t M,
+                              const void* W_lm, int32_t wdtype, int32_t d,
+                              void* W_perm, int32_t* perm, int32_t* offsets,
+                              int32_t* cap_by_k_host, int32_t* max_cluster_host,
+                              void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ */
+/* Hot path, step by step.                                             */
+/* ------------------------------------------------------------------ */
+
+/* Workspace for any of the calls below with these sizes (router may be NULL
+ * when only shortlist_logits / draft_select are used). */
+size_t dyna_workspace_bytes(const dyna_layout* L, const dyna_router* r,
+                            int32_t B, int32_t k, int32_t cap);
+
+/* Route (Sec. 4.2: s = r(x), K = TopK_k(s)).
+ *  x [B, d_r]          device, dtype xdtype
+ *  topk_ids [B, k]     device output, cluster ids in rank order (score desc, id asc)
+ *  topk_scores [B, k]  device output, may be NULL
+ *  scores [B, M]       device output (fp32), may be NULL
+ * 1 <= k <= M.  B = 0 is a no-op. */
+dyna_status dyna_route(const dyna_router* r, const void* x, int32_t xdtype,
+                       int32_t B, int32_t k, int32_t* topk_ids, float* topk_scores,
+                       float* scores, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Shortlist (Sec. 4.2: V_S = disjoint union of C_m over m in K).
+ *  topk_ids [B, k]       device, distinct cluster ids per row (any order)
+ *  sel_sorted [B, k]     device output, the same ids ascending
+ *  sel_rowoff [B, k+1]   device output, start of each selected cluster inside
+ *                        the row's shortlist (exclusive prefix of sizes)
+ *  row_len [B]           device output, shortlist length
+ *  shortlist_ids [B, cap] device output, may be NULL: vocabulary ids of the
+ *                        shortlist in order; entries past row_len untouched
+ * An id outside [0, M) or repeated in a row is ignored (counts as an empty
+ * cluster) so that the shortlist never exceeds cap_by_k[k].
+ * Requires cap >= cap_by_k[k] when shortlist_ids is given. */
+dyna_status dyna_shortlist(const dyna_layout* L, const int32_t* topk_ids, int32_t B,
+                           int32_t k, int32_t* sel_sorted, int32_t* sel_rowoff,
+                           int32_t* row_len, int32_t* shortlist_ids, int32_t cap,
+                           hipStream_t stream);
+
+/* Shortlist logits (Sec. 4.3: one gathered GEMM over the shortlisted columns;
+ * Algorithm 1, FUSED_INDEX_GEMM): logits[b, j] = h_b . W_perm[row of slot j].
+ *  h [B, d]            device, dtype hdtype
+ *  sel_* / row_len     as written by dyna_shortlist
+ *  logits [B, cap]     device output fp32; slots past row_len untouched
+ * Each distinct selected slab is read from HBM once per call however many
+ * contexts chose it.  Requires cap >= cap_by_k[k]. */
+dyna_status dyna_shortlist_logits(const dyna_layout* L, const void* h, int32_t hdtype,
+                                  int32_t B, int32_t k, const int32_t* sel_sorted,
+                                  const int32_t* sel_rowoff, const int32_t* row_len,
+                                  float* logits, int32_t cap, void* ws, size_t ws_bytes,
+                                  hipStream_t stream);
+
+/* Draft select (Algorithm 1: p = log_softmax(z); TopK_{k_t}(p); remap2realid).
+ * Log-probabilities are those of softmax(z / temperature) over the shortlist.
+ *  mode                DYNA_SEL_* flags; ARGMAX alone means k_t = 1
+ *  out_ids [B, k_t]    device output, vocabulary ids, (z desc, id asc); -1 past row_len
+ *  out_logprobs [B, k_t] device output, may be NULL
+ *  uniforms [B]        device, u in [0, 1), required with DYNA_SEL_SAMPLE
+ *  out_sample [B]      device output (SAMPLE): first j in shortlist order whose
+ *                      CDF exceeds u, else the last j with nonzero mass
+ *  out_sample_logprob [B] device output, may be NULL
+ *  ws                  workspace of dyna_workspace_bytes(L, NULL, B, k, cap) bytes
+ * 1 <= k_t <= DYNA_MAX_KT; temperature > 0. */
+dyna_status dyna_draft_select(const dyna_layout* L, const float* logits,
+                              const int32_t* sel_sorted, const int32_t* sel_rowoff,
+                              const int32_t* row_len, int32_t B, int32_t k, int32_t cap,
+                              int32_t mode, int32_t k_t, float temperature,
+                              const float* uniforms, int32_t* out_ids, float* out_logprobs,
+                              int32_t* out_sample, float* out_sample_logprob,
+                              void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ */
+/* The whole head in one call (Algorithm 1, one draft step).           */
+/* ------------------------------------------------------------------ */
+
+/* route -> top-k -> shortlist -> logits -> select.
+ *  x [B, d_r], h [B, d]  device, both of dtype adtype (x may equal h)
+ *  out_clusters [B, k]   device output, may be NULL (rank order)
+ *  out_logits [B, cap]   device output, may be NULL
+ *  route_stream          NULL: everything runs on `stream`.  Otherwise routing
+ *                        (route, top-k, shortlist) runs on route_stream so it
+ *                        can overlap the caller's draft layer on `stream`
+ *                        (Sec. 4.2 and Sec. 4.3: the router on a parallel
+ *                        stream); the logits wait for it with an event join.
+ *  x_ready               with route_stream: event after which x is valid;
+ *                        NULL means "x is valid when this call is made
+ *                        relative to `stream`" and the library records one.
+ * Other arguments as in the step-by-step calls. */
+dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
+                            const void* x, const void* h, int32_t adtype,
+                            int32_t B, int32_t k, int32_t mode, int32_t k_t,
+                            float temperature, const float* uniforms,
+                            int32_t* out_ids, float* out_logprobs, int32_t* out_sample,
+                            float* out_sample_logprob, int32_t* out_clusters,
+                            float* out_logits, int32_t cap, void* ws, size_t ws_bytes,
+                            hipStream_t stream, hipStream_t route_stream,
+                            hipEvent_t x_ready);
+
+/* ------------------------------------------------------------------ */
+/* Baselines on the same kernels (Sec. 4.1).                           */
+/* ------------------------------------------------------------------ */
+
+size_t dyna_dense_workspace_bytes(int32_t n_rows, int32_t B);
+
+/* Head over the contiguous rows [0, n_rows) of W [>= n_rows, d]: the dense
+ * full-vocabulary head O = H W_LM when n_rows = V, and the static
+ * fixed-shortlist head (FR-Spec's W~ = W_LM[:, V_high], here the first
+ * n_rows ids) otherwise.  Token ids are row indices.  out_logits [B, n_rows]
+ * may be NULL.  Selection as in dyna_draft_select. */
+dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_rows, int32_t d,
+                            const void* h, int32_t hdtype, int32_t B, int32_t mode,
+                            int32_t k_t, float temperature, const float* uniforms,
+                            int32_t* out_ids, float* out_logprobs, int32_t* out_sample,
+                            float* out_sample_logprob, float* out_logits,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ */
+/* Diagnostics.                                                        */
+/* ------------------------------------------------------------------ */
+
+/* Kernel-path override for tests and measurement:
+ * DYNA_OPT_LOGITS_PATH: 0 automatic, 1 wave-per-row GEMV, 2 MFMA tiles.
+ * DYNA_OPT_ROUTER_PATH: 0 automatic, 1 GEMV, 2 MFMA tiles.
+ * DYNA_OPT_KERNEL_TIMING: 1 brackets every launch of the gathered-head
+ *   (logits) kernel with two events on the stream it runs on; 0 stops. */
+enum { DYNA_OPT_LOGITS_PATH = 1, DYNA_OPT_ROUTER_PATH = 2, DYNA_OPT_KERNEL_TIMING = 3 };
+dyna_status dyna_set_option(int32_t option, int32_t value);
+
+/* Waits for the events recorded under DYNA_OPT_KERNEL_TIMING and returns the
+ * summed duration (ms) and number of timed launches since the last reset.
+ * reset != 0 forgets them afterwards.  Host call; synchronises the events. */
+dyna_status dyna_kernel_timing(double* total_ms, int64_t* launches, int32_t reset);
+
+int32_t dyna_abi_version(void);
+const char* dyna_status_string(dyna_status status);
+/* Detail of the last non-OK status returned to this host thread. */
+const char* dyna_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DYNAHEAD_H */

@@ -1,0 +1,569 @@
+// C ABI of libdynahead: argument checks, workspace carving, stream joins.
+// Every check runs on the host before the first HIP call of an entry point.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <atomic>
+#include <mutex>
+#include <utility>
+#include <vector>
+
+#include "dyna_internal.h"
+
+#define DYNA_API extern "C" __attribute__((visibility("default")))
+
+namespace dyna {
+
+namespace {
+thread_local char g_last_error[512] = "";
+std::atomic<int> g_logits_path{0};
+std::atomic<int> g_router_path{0};
+std::atomic<int> g_kernel_timing{0};
+
+// event pairs around timed gathered-head launches
+std::mutex g_timing_mu;
+std::vector<std::pair<hipEvent_t, hipEvent_t>> g_timing_pairs;
+std::vector<hipEvent_t> g_timing_free;
+
+constexpr int kMaxDevices = 64;
+thread_local hipEvent_t g_ev_x[kMaxDevices];
+thread_local hipEvent_t g_ev_join[kMaxDevices];
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool valid_dtype(int32_t t) { return t == DYNA_F32 || t == DYNA_BF16; }
+int elt_size(int32_t t) { return t == DYNA_BF16 ? 2 : 4; }
+}  // namespace
+
+dyna_status set_error(dyna_status s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+dyna_status check_launch(const char* what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return set_error(DYNA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return DYNA_OK;
+}
+
+int option_logits_path() { return g_logits_path.load(); }
+
+static hipEvent_t timing_event() {
+    std::lock_guard<std::mutex> g(g_timing_mu);
+    if (!g_timing_free.empty()) {
+        hipEvent_t e = g_timing_free.back();
+        g_timing_free.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Launch the gathered-head kernel, optionally between two timing events.
+static dyna_status timed_rowdot(const RowdotArgs& a, int path, hipStream_t s) {
+    if (!g_kernel_timing.load()) return launch_rowdot(a, path, s);
+    hipEvent_t e0 = timing_event(), e1 = timing_event();
+    if (!e0 || !e1 || hipEventRecord(e0, s) != hipSuccess)
+        return set_error(DYNA_ERR_HIP, "kernel timing: event record failed");
+    dyna_status st = launch_rowdot(a, path, s);
+    if (st != DYNA_OK) return st;
+    if (hipEventRecord(e1, s) != hipSuccess) return set_error(DYNA_ERR_HIP, "kernel timing: event record failed");
+    std::lock_guard<std::mutex> g(g_timing_mu);
+    g_timing_pairs.emplace_back(e0, e1);
+    return DYNA_OK;
+}
+int option_router_path() { return g_router_path.load(); }
+
+// ------------------------------------------------------------------ workspace
+// One carving serves every hot entry point, so a single workspace can back a
+// whole step; each call only touches its own regions.
+struct Carve {
+    float* hidden = nullptr;      // [B, H]
+    float* scores = nullptr;      // [B, M]
+    int32_t* topk_ids = nullptr;  // [B, k]
+    float* topk_scores = nullptr; // [B, k]
+    int32_t* sel_sorted = nullptr;// [B, k]
+    int32_t* sel_rowoff = nullptr;// [B, k + 1]
+    int32_t* row_len = nullptr;   // [B]
+    float* logits = nullptr;      // [B, cap]
+    Plan plan{};
+    void* select_ws = nullptr;
+    size_t bytes = 0;
+};
+
+static int64_t max_chunks_for(const dyna_layout* L) {
+    return ((int64_t)L->V + kTileRows - 1) / kTileRows + L->M;
+}
+
+static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_t k, int32_t cap,
+                   void* base) {
+    Carve c;
+    char* p = static_cast<char*>(base);
+    size_t off = 0;
+    auto take = [&](size_t n) -> void* {
+        void* q = p ? p + off : nullptr;
+        off += align256(n);
+        return q;
+    };
+    const int64_t Bl = B;
+    const int32_t M = L ? L->M : (r ? r->M : 0);
+    if (r && r->H > 0) c.hidden = static_cast<float*>(take(sizeof(float) * Bl * r->H));
+    c.scores = static_cast<float*>(take(sizeof(float) * Bl * M));
+    c.topk_ids = static_cast<int32_t*>(take(sizeof(int32_t) * Bl * k));
+    c.topk_scores = static_cast<float*>(take(sizeof(float) * Bl * k));
+    c.sel_sorted = static_cast<int32_t*>(take(sizeof(int32_t) * Bl * k));
+    c.sel_rowoff = static_cast<int32_t*>(take(sizeof(int32_t) * Bl * (k + 1)));
+    c.row_len = static_cast<int32_t*>(take(sizeof(int32_t) * Bl));
+    c.logits = static_cast<float*>(take(sizeof(float) * Bl * cap));
+    if (L) {
+        c.plan.max_chunks = (int32_t)max_chunks_for(L);
+        c.plan.max_entries = (int32_t)(Bl * k);
+        c.plan.hdr = static_cast<PlanHeader*>(take(sizeof(PlanHeader)));
+        c.plan.chunks = static_cast<Chunk*>(take(sizeof(Chunk) * (size_t)c.plan.max_chunks));
+        c.plan.list = static_cast<ListEntry*>(take(sizeof(ListEntry) * (size_t)c.plan.max_entries));
+    }
+    c.select_ws = take(select_ws_bytes(B, cap, DYNA_MAX_KT));
+    c.bytes = off;
+    return c;
+}
+
+// ------------------------------------------------------------------ checks
+#define REQUIRE(cond, ...) \
+    do {                   \
+        if (!(cond)) return set_error(DYNA_ERR_INVALID_ARG, __VA_ARGS__); \
+    } while (0)
+
+static dyna_status check_layout(const dyna_layout* L) {
+    REQUIRE(L != nullptr, "layout is NULL");
+    REQUIRE(L->V >= 1 && L->d >= 8 && L->M >= 1, "layout: bad sizes V=%d d=%d M=%d", L->V, L->d, L->M);
+    REQUIRE(L->M <= L->V, "layout: M=%d > V=%d", L->M, L->V);
+    if (L->M > DYNA_MAX_M)
+        return set_error(DYNA_ERR_UNSUPPORTED, "layout: M=%d > DYNA_MAX_M=%d", L->M, DYNA_MAX_M);
+    REQUIRE(valid_dtype(L->wdtype), "layout: bad wdtype %d", L->wdtype);
+    REQUIRE(L->d % 8 == 0, "layout: d=%d is not a multiple of 8", L->d);
+    if (L->d > 8192) return set_error(DYNA_ERR_UNSUPPORTED, "layout: d=%d > 8192", L->d);
+    REQUIRE(L->W_perm && L->perm && L->offsets && L->cap_by_k, "layout: NULL array");
+    REQUIRE(aligned16(L->W_perm), "layout: W_perm not 16-byte aligned");
+    REQUIRE(L->max_cluster >= 1 && L->max_cluster <= L->V, "layout: bad max_cluster %d", L->max_cluster);
+    return DYNA_OK;
+}
+
+static dyna_status check_router(const dyna_router* r) {
+    REQUIRE(r != nullptr, "router is NULL");
+    REQUIRE(r->d_r >= 8 && r->M >= 1 && r->H >= 0, "router: bad sizes d_r=%d H=%d M=%d", r->d_r, r->H, r->M);
+    REQUIRE(r->d_r % 8 == 0, "router: d_r=%d is not a multiple of 8", r->d_r);
+    REQUIRE(r->H % 8 == 0, "router: H=%d is not a multiple of 8", r->H);
+    if (r->d_r > 8192 || r->H > 8192)
+        return set_error(DYNA_ERR_UNSUPPORTED, "router: d_r or H > 8192");
+    if (r->M > DYNA_MAX_M) return set_error(DYNA_ERR_UNSUPPORTED, "router: M > DYNA_MAX_M");
+    REQUIRE(valid_dtype(r->wdtype), "router: bad wdtype %d", r->wdtype);
+    REQUIRE(r->act == DYNA_ACT_NONE || r->act == DYNA_ACT_RELU || r->act == DYNA_ACT_SILU,
+            "router: bad act %d", r->act);
+    REQUIRE(r->W1 != nullptr && aligned16(r->W1), "router: W1 NULL or not 16-byte aligned");
+    if (r->H > 0) REQUIRE(r->W2 != nullptr && aligned16(r->W2), "router: W2 NULL or not 16-byte aligned");
+    return DYNA_OK;
+}
+
+static dyna_status check_k(const dyna_layout* L, int32_t k) {
+    REQUIRE(k >= 1 && k <= L->M, "k=%d outside [1, M=%d]", k, L->M);
+    return DYNA_OK;
+}
+
+static dyna_status check_cap(const dyna_layout* L, int32_t k, int32_t cap) {
+    if (cap < L->cap_by_k[k])
+        return set_error(DYNA_ERR_CAPACITY, "cap=%d < cap_by_k[%d]=%d", cap, k, L->cap_by_k[k]);
+    if (cap > select_max_len())
+        return set_error(DYNA_ERR_UNSUPPORTED, "cap=%d > %d", cap, select_max_len());
+    return DYNA_OK;
+}
+
+static dyna_status check_select(int32_t mode, int32_t* k_t, float temperature, const float* uniforms,
+                                const int32_t* out_ids, const int32_t* out_sample) {
+    REQUIRE(mode > 0 && (mode & ~(DYNA_SEL_ARGMAX | DYNA_SEL_TOPK | DYNA_SEL_SAMPLE)) == 0,
+            "bad select mode %d", mode);
+    if (mode & DYNA_SEL_TOPK) {
+        REQUIRE(*k_t >= 1 && *k_t <= DYNA_MAX_KT, "k_t=%d outside [1, %d]", *k_t, DYNA_MAX_KT);
+    } else {
+        *k_t = 1;  // argmax, or the max needed by sampling
+    }
+    if (mode & (DYNA_SEL_TOPK | DYNA_SEL_ARGMAX)) REQUIRE(out_ids != nullptr, "out_ids is NULL");
+    if (mode & DYNA_SEL_SAMPLE) {
+        REQUIRE(uniforms != nullptr && out_sample != nullptr, "sampling needs uniforms and out_sample");
+        REQUIRE(temperature > 0.0f && temperature < 3.0e38f, "temperature must be positive and finite");
+    }
+    return DYNA_OK;
+}
+
+#define TRY(expr)                                   \
+    do {                                            \
+        dyna_status _s = (expr);                    \
+        if (_s != DYNA_OK) return _s;               \
+    } while (0)
+
+// ------------------------------------------------------------------ pieces
+static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtype, int32_t B,
+                              float* scores, float* hidden, hipStream_t s) {
+    const int path = option_router_path();
+    RowdotArgs a{};
+    a.W = r->W1;
+    a.wdtype = r->wdtype;
+    a.K = r->d_r;
+    a.v = x;
+    a.vdtype = xdtype;
+    a.B = B;
+    if (r->H == 0) {
+        a.out = scores;
+        a.ld = r->M;
+        a.bias = r->b1;
+        a.act = DYNA_ACT_NONE;
+        a.n_rows = r->M;
+        return launch_rowdot(a, path, s);
+    }
+    a.out = hidden;
+    a.ld = r->H;
+    a.bias = r->b1;
+    a.act = r->act;
+    a.n_rows = r->H;
+    TRY(launch_rowdot(a, path, s));
+    RowdotArgs b{};
+    b.W = r->W2;
+    b.wdtype = r->wdtype;
+    b.K = r->H;
+    b.v = hidden;
+    b.vdtype = DYNA_F32;
+    b.B = B;
+    b.out = scores;
+    b.ld = r->M;
+    b.bias = r->b2;
+    b.act = DYNA_ACT_NONE;
+    b.n_rows = r->M;
+    return launch_rowdot(b, path, s);
+}
+
+static dyna_status run_logits(const dyna_layout* L, const void* h, int32_t hdtype, int32_t B, int32_t k,
+                              const int32_t* sel_sorted, const int32_t* sel_rowoff, float* logits,
+                              int32_t cap, const Plan& plan, hipStream_t s) {
+    TRY(launch_plan(L->offsets, L->M, sel_sorted, sel_rowoff, B, k, plan, s));
+    RowdotArgs a{};
+    a.W = L->W_perm;
+    a.wdtype = L->wdtype;
+    a.K = L->d;
+    a.v = h;
+    a.vdtype = hdtype;
+    a.B = B;
+    a.out = logits;
+    a.ld = cap;
+    a.bias = nullptr;
+    a.act = DYNA_ACT_NONE;
+    a.n_rows = 0;
+    a.plan = plan;
+    a.max_chunks_bound = plan.max_chunks;
+    return timed_rowdot(a, option_logits_path(), s);
+}
+
+static hipEvent_t lazy_event(hipEvent_t* table) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    if (table[dev] == nullptr) {
+        hipEvent_t e = nullptr;
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+        table[dev] = e;
+    }
+    return table[dev];
+}
+
+}  // namespace dyna
+
+using namespace dyna;
+
+// ====================================================================== ABI
+DYNA_API int32_t dyna_abi_version(void) { return DYNA_ABI_VERSION; }
+
+DYNA_API const char* dyna_status_string(dyna_status s) {
+    switch (s) {
+        case DYNA_OK: return "DYNA_OK";
+        case DYNA_ERR_INVALID_ARG: return "DYNA_ERR_INVALID_ARG";
+        case DYNA_ERR_CAPACITY: return "DYNA_ERR_CAPACITY";
+        case DYNA_ERR_WORKSPACE: return "DYNA_ERR_WORKSPACE";
+        case DYNA_ERR_UNSUPPORTED: return "DYNA_ERR_UNSUPPORTED";
+        case DYNA_ERR_HIP: return "DYNA_ERR_HIP";
+        case DYNA_ERR_DEVICE_DATA: return "DYNA_ERR_DEVICE_DATA";
+    }
+    return "unknown dyna_status";
+}
+
+DYNA_API const char* dyna_last_error(void) { return g_last_error; }
+
+DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
+    REQUIRE(value >= 0 && value <= 2, "option value %d outside [0, 2]", value);
+    if (option == DYNA_OPT_LOGITS_PATH) g_logits_path.store(value);
+    else if (option == DYNA_OPT_ROUTER_PATH) g_router_path.store(value);
+    else if (option == DYNA_OPT_KERNEL_TIMING) g_kernel_timing.store(value ? 1 : 0);
+    else return set_error(DYNA_ERR_INVALID_ARG, "unknown option %d", option);
+    return DYNA_OK;
+}
+
+DYNA_API dyna_status dyna_kernel_timing(double* total_ms, int64_t* launches, int32_t reset) {
+    REQUIRE(total_ms != nullptr && launches != nullptr, "NULL argument");
+    std::lock_guard<std::mutex> g(g_timing_mu);
+    double sum = 0.0;
+    for (auto& pr : g_timing_pairs) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(pr.second) != hipSuccess ||
+            hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess)
+            return set_error(DYNA_ERR_HIP, "kernel timing: elapsed time query failed");
+        sum += ms;
+    }
+    *total_ms = sum;
+    *launches = (int64_t)g_timing_pairs.size();
+    if (reset) {
+        for (auto& pr : g_timing_pairs) {
+            g_timing_free.push_back(pr.first);
+            g_timing_free.push_back(pr.second);
+        }
+        g_timing_pairs.clear();
+    }
+    return DYNA_OK;
+}
+
+DYNA_API size_t dyna_layout_workspace_bytes(int32_t V, int32_t M) {
+    if (V < 1 || M < 1) return 0;
+    return layout_ws_bytes(V, M);
+}
+
+DYNA_API dyna_status dyna_build_layout(const int32_t* cluster_of, int32_t V, int32_t M,
+                                       const void* W_lm, int32_t wdtype, int32_t d, void* W_perm,
+                                       int32_t* perm, int32_t* offsets, int32_t* cap_by_k_host,
+                                       int32_t* max_cluster_host, void* ws, size_t ws_bytes,
+                                       hipStream_t stream) {
+    REQUIRE(cluster_of && W_lm && W_perm && perm && offsets && cap_by_k_host && ws, "NULL argument");
+    REQUIRE(V >= 1 && M >= 1 && M <= V, "bad sizes V=%d M=%d", V, M);
+    if (M > DYNA_MAX_M) return set_error(DYNA_ERR_UNSUPPORTED, "M=%d > DYNA_MAX_M", M);
+    REQUIRE(valid_dtype(wdtype), "bad wdtype %d", wdtype);
+    REQUIRE(d >= 8 && d % 8 == 0, "d=%d must be a positive multiple of 8", d);
+    REQUIRE(aligned16(W_lm) && aligned16(W_perm), "W_lm / W_perm not 16-byte aligned");
+    REQUIRE(W_lm != W_perm, "W_perm must not alias W_lm");
+    if (ws_bytes < layout_ws_bytes(V, M))
+        return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, layout_ws_bytes(V, M));
+    std::vector<int32_t> off(M + 1);
+    TRY(launch_build_layout(cluster_of, V, M, W_lm, wdtype, d, W_perm, perm, offsets, ws, ws_bytes,
+                            off.data(), stream));
+    std::vector<int32_t> sizes(M);
+    for (int m = 0; m < M; ++m) sizes[m] = off[m + 1] - off[m];
+    std::sort(sizes.begin(), sizes.end(), [](int a, int b) { return a > b; });
+    cap_by_k_host[0] = 0;
+    for (int m = 0; m < M; ++m) cap_by_k_host[m + 1] = cap_by_k_host[m] + sizes[m];
+    if (max_cluster_host) *max_cluster_host = sizes[0];
+    return DYNA_OK;
+}
+
+DYNA_API size_t dyna_workspace_bytes(const dyna_layout* L, const dyna_router* r, int32_t B, int32_t k,
+                                     int32_t cap) {
+    if (B < 0 || k < 1 || cap < 0 || (!L && !r)) return 0;
+    return carve(L, r, B, k, cap, nullptr).bytes;
+}
+
+DYNA_API dyna_status dyna_route(const dyna_router* r, const void* x, int32_t xdtype, int32_t B, int32_t k,
+                                int32_t* topk_ids, float* topk_scores, float* scores, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+    TRY(check_router(r));
+    REQUIRE(B >= 0, "B=%d < 0", B);
+    REQUIRE(k >= 1 && k <= r->M, "k=%d outside [1, M=%d]", k, r->M);
+    REQUIRE(valid_dtype(xdtype), "bad xdtype %d", xdtype);
+    if (B == 0) return DYNA_OK;
+    REQUIRE(x != nullptr && aligned16(x) && topk_ids != nullptr, "x / topk_ids NULL or x misaligned");
+    REQUIRE(ws != nullptr, "workspace is NULL");
+    const Carve c0 = carve(nullptr, r, B, k, 0, nullptr);
+    if (ws_bytes < c0.bytes) return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, c0.bytes);
+    const Carve c = carve(nullptr, r, B, k, 0, ws);
+    float* sc = scores ? scores : c.scores;
+    TRY(run_router(r, x, xdtype, B, sc, c.hidden, stream));
+    return launch_topk_clusters(sc, B, r->M, k, topk_ids, topk_scores, nullptr, nullptr, nullptr,
+                                nullptr, stream);
+}
+
+DYNA_API dyna_status dyna_shortlist(const dyna_layout* L, const int32_t* topk_ids, int32_t B, int32_t k,
+                                    int32_t* sel_sorted, int32_t* sel_rowoff, int32_t* row_len,
+                                    int32_t* shortlist_ids, int32_t cap, hipStream_t stream) {
+    TRY(check_layout(L));
+    TRY(check_k(L, k));
+    REQUIRE(B >= 0, "B=%d < 0", B);
+    if (B == 0) return DYNA_OK;
+    REQUIRE(topk_ids && sel_sorted && sel_rowoff && row_len, "NULL argument");
+    if (shortlist_ids) TRY(check_cap(L, k, cap));
+    return launch_shortlist(L->offsets, L->perm, L->M, topk_ids, B, k, sel_sorted, sel_rowoff, row_len,
+                            shortlist_ids, cap, stream);
+}
+
+DYNA_API dyna_status dyna_shortlist_logits(const dyna_layout* L, const void* h, int32_t hdtype, int32_t B,
+                                           int32_t k, const int32_t* sel_sorted, const int32_t* sel_rowoff,
+                                           const int32_t* row_len, float* logits, int32_t cap, void* ws,
+                                           size_t ws_bytes, hipStream_t stream) {
+    TRY(check_layout(L));
+    TRY(check_k(L, k));
+    REQUIRE(B >= 0, "B=%d < 0", B);
+    REQUIRE(valid_dtype(hdtype), "bad hdtype %d", hdtype);
+    TRY(check_cap(L, k, cap));
+    if (B == 0) return DYNA_OK;
+    REQUIRE(h && aligned16(h) && sel_sorted && sel_rowoff && row_len && logits && ws,
+            "NULL argument or h misaligned");
+    const Carve c0 = carve(L, nullptr, B, k, cap, nullptr);
+    if (ws_bytes < c0.bytes) return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, c0.bytes);
+    const Carve c = carve(L, nullptr, B, k, cap, ws);
+    return run_logits(L, h, hdtype, B, k, sel_sorted, sel_rowoff, logits, cap, c.plan, stream);
+}
+
+DYNA_API dyna_status dyna_draft_select(const dyna_layout* L, const float* logits, const int32_t* sel_sorted,
+                                       const int32_t* sel_rowoff, const int32_t* row_len, int32_t B, int32_t k,
+                                       int32_t cap, int32_t mode, int32_t k_t, float temperature,
+                                       const float* uniforms, int32_t* out_ids, float* out_logprobs,
+                                       int32_t* out_sample, float* out_sample_logprob, void* ws,
+                                       size_t ws_bytes, hipStream_t stream) {
+    TRY(check_layout(L));
+    TRY(check_k(L, k));
+    TRY(check_cap(L, k, cap));
+    TRY(check_select(mode, &k_t, temperature, uniforms, out_ids, out_sample));
+    REQUIRE(B >= 0, "B=%d < 0", B);
+    if (B == 0) return DYNA_OK;
+    REQUIRE(logits && sel_sorted && sel_rowoff && row_len && ws, "NULL argument");
+    const Carve c0 = carve(L, nullptr, B, k, cap, nullptr);
+    if (ws_bytes < c0.bytes) return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, c0.bytes);
+    const Carve c = carve(L, nullptr, B, k, cap, ws);
+    const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
+    const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
+    return launch_select(logits, cap, row_len, 0, cap, sel_sorted, sel_rowoff, L->offsets, L->perm, B, k,
+                         k_t, temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
+                         want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
+                         want_sample ? out_sample_logprob : nullptr, c.select_ws, stream);
+}
+
+DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L, const void* x, const void* h,
+                                     int32_t adtype, int32_t B, int32_t k, int32_t mode, int32_t k_t,
+                                     float temperature, const float* uniforms, int32_t* out_ids,
+                                     float* out_logprobs, int32_t* out_sample, float* out_sample_logprob,
+                                     int32_t* out_clusters, float* out_logits, int32_t cap, void* ws,
+                                     size_t ws_bytes, hipStream_t stream, hipStream_t route_stream,
+                                     hipEvent_t x_ready) {
+    TRY(check_router(r));
+    TRY(check_layout(L));
+    REQUIRE(r->M == L->M, "router M=%d differs from layout M=%d", r->M, L->M);
+    REQUIRE(r->d_r > 0, "router d_r");
+    TRY(check_k(L, k));
+    TRY(check_cap(L, k, cap));
+    TRY(check_select(mode, &k_t, temperature, uniforms, out_ids, out_sample));
+    REQUIRE(valid_dtype(adtype), "bad adtype %d", adtype);
+    REQUIRE(B >= 0, "B=%d < 0", B);
+    if (B == 0) return DYNA_OK;
+    REQUIRE(x && h && aligned16(x) && aligned16(h) && ws, "NULL argument or x/h misaligned");
+    const Carve c0 = carve(L, r, B, k, cap, nullptr);
+    if (ws_bytes < c0.bytes) return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, c0.bytes);
+    const Carve c = carve(L, r, B, k, cap, ws);
+
+    hipStream_t rs = route_stream ? route_stream : stream;
+    const bool split = rs != stream;
+    if (split) {
+        hipEvent_t ready = x_ready;
+        if (ready == nullptr) {
+            ready = lazy_event(g_ev_x);
+            if (!ready || hipEventRecord(ready, stream) != hipSuccess)
+                return set_error(DYNA_ERR_HIP, "draft_head: recording the x-ready event failed");
+        }
+        if (hipStreamWaitEvent(rs, ready, 0) != hipSuccess)
+            return set_error(DYNA_ERR_HIP, "draft_head: route stream wait failed");
+    }
+    // routing: router, top-k, shortlist, plan (the router's stream)
+    int32_t* clusters = out_clusters ? out_clusters : c.topk_ids;
+    TRY(run_router(r, x, adtype, B, c.scores, c.hidden, rs));
+    TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, L->offsets, c.sel_sorted,
+                             c.sel_rowoff, c.row_len, rs));
+    TRY(launch_plan(L->offsets, L->M, c.sel_sorted, c.sel_rowoff, B, k, c.plan, rs));
+    if (split) {
+        hipEvent_t join = lazy_event(g_ev_join);
+        if (!join || hipEventRecord(join, rs) != hipSuccess || hipStreamWaitEvent(stream, join, 0) != hipSuccess)
+            return set_error(DYNA_ERR_HIP, "draft_head: stream join failed");
+    }
+    // gathered head and selection (the caller's stream)
+    float* logits = out_logits ? out_logits : c.logits;
+    RowdotArgs a{};
+    a.W = L->W_perm;
+    a.wdtype = L->wdtype;
+    a.K = L->d;
+    a.v = h;
+    a.vdtype = adtype;
+    a.B = B;
+    a.out = logits;
+    a.ld = cap;
+    a.act = DYNA_ACT_NONE;
+    a.plan = c.plan;
+    a.max_chunks_bound = c.plan.max_chunks;
+    TRY(timed_rowdot(a, option_logits_path(), stream));
+    const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
+    const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
+    return launch_select(logits, cap, c.row_len, 0, cap, c.sel_sorted, c.sel_rowoff, L->offsets, L->perm, B,
+                         k, k_t, temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
+                         want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
+                         want_sample ? out_sample_logprob : nullptr, c.select_ws, stream);
+}
+
+// ------------------------------------------------------------------ baselines
+static size_t dense_bytes(int32_t n_rows, int32_t B, float** logits, void** sel, void* base) {
+    char* p = static_cast<char*>(base);
+    size_t off = 0;
+    const size_t lb = align256(sizeof(float) * (size_t)B * (size_t)n_rows);
+    if (logits) *logits = p ? reinterpret_cast<float*>(p) : nullptr;
+    off += lb;
+    if (sel) *sel = p ? p + off : nullptr;
+    off += align256(select_ws_bytes(B, n_rows, DYNA_MAX_KT));
+    return off;
+}
+
+DYNA_API size_t dyna_dense_workspace_bytes(int32_t n_rows, int32_t B) {
+    if (n_rows < 1 || B < 0) return 0;
+    return dense_bytes(n_rows, B, nullptr, nullptr, nullptr);
+}
+
+DYNA_API dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_rows, int32_t d, const void* h,
+                                     int32_t hdtype, int32_t B, int32_t mode, int32_t k_t, float temperature,
+                                     const float* uniforms, int32_t* out_ids, float* out_logprobs,
+                                     int32_t* out_sample, float* out_sample_logprob, float* out_logits,
+                                     void* ws, size_t ws_bytes, hipStream_t stream) {
+    REQUIRE(valid_dtype(wdtype) && valid_dtype(hdtype), "bad dtype");
+    REQUIRE(n_rows >= 1 && d >= 8 && d % 8 == 0, "bad sizes n_rows=%d d=%d", n_rows, d);
+    if (d > 8192) return set_error(DYNA_ERR_UNSUPPORTED, "d=%d > 8192", d);
+    if (n_rows > select_max_len())
+        return set_error(DYNA_ERR_UNSUPPORTED, "n_rows=%d > %d", n_rows, select_max_len());
+    TRY(check_select(mode, &k_t, temperature, uniforms, out_ids, out_sample));
+    REQUIRE(B >= 0, "B=%d < 0", B);
+    if (B == 0) return DYNA_OK;
+    REQUIRE(W && h && aligned16(W) && aligned16(h) && ws, "NULL argument or W/h misaligned");
+    const size_t need = dense_bytes(n_rows, B, nullptr, nullptr, nullptr);
+    if (ws_bytes < need) return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+    float* wl = nullptr;
+    void* sel = nullptr;
+    dense_bytes(n_rows, B, &wl, &sel, ws);
+    float* logits = out_logits ? out_logits : wl;
+    RowdotArgs a{};
+    a.W = W;
+    a.wdtype = wdtype;
+    a.K = d;
+    a.v = h;
+    a.vdtype = hdtype;
+    a.B = B;
+    a.out = logits;
+    a.ld = n_rows;
+    a.act = DYNA_ACT_NONE;
+    a.n_rows = n_rows;
+    TRY(timed_rowdot(a, option_logits_path(), stream));
+    const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
+    const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
+    return launch_select(logits, n_rows, nullptr, n_rows, n_rows, nullptr, nullptr, nullptr, nullptr, B, 0, k_t,
+                         temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
+                         want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
+                         want_sample ? out_sample_logprob : nullptr, sel, stream);
+}

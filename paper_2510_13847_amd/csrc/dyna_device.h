@@ -1,0 +1,166 @@
+// Device helpers shared by the libdynahead kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dyna_internal.h"
+
+namespace dyna {
+
+// ---------------------------------------------------------------- bf16
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// Eight consecutive elements of a row as fp32, from bf16 (one 16-byte load)
+// or fp32 (two 16-byte loads).  `nt` streams the load past the caches.
+template <typename T, bool NT>
+struct Load8;
+
+template <bool NT>
+struct Load8<uint16_t, NT> {
+    __device__ __forceinline__ static void run(const uint16_t* p, float (&x)[8]) {
+        u32x4 w = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p))
+                     : *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[2 * i] = bf16_lo(w[i]);
+            x[2 * i + 1] = bf16_hi(w[i]);
+        }
+    }
+};
+
+template <bool NT>
+struct Load8<float, NT> {
+    __device__ __forceinline__ static void run(const float* p, float (&x)[8]) {
+        const u32x4* q = reinterpret_cast<const u32x4*>(p);
+        u32x4 a = NT ? __builtin_nontemporal_load(q) : q[0];
+        u32x4 b = NT ? __builtin_nontemporal_load(q + 1) : q[1];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[i] = __uint_as_float(a[i]);
+            x[4 + i] = __uint_as_float(b[i]);
+        }
+    }
+};
+
+// ---------------------------------------------------------------- ordering
+// Monotone map of a float to uint32 (larger float -> larger code).  NaN is
+// mapped like -inf and -0 like +0, the ordering rule of every top-k here.
+__device__ __forceinline__ uint32_t ord_f32(float f) {
+    if (f != f) f = -__builtin_inff();
+    if (f == 0.0f) f = 0.0f;
+    uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float ord_to_f32(uint32_t o) {
+    uint32_t u = (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o;
+    return __uint_as_float(u);
+}
+// 64-bit selection key: higher value first, then lower id first.
+__device__ __forceinline__ uint64_t sel_key(float v, uint32_t id) {
+    return (static_cast<uint64_t>(ord_f32(v)) << 32) | static_cast<uint64_t>(0xffffffffu - id);
+}
+__device__ __forceinline__ uint32_t key_id(uint64_t key) {
+    return 0xffffffffu - static_cast<uint32_t>(key & 0xffffffffu);
+}
+__device__ __forceinline__ float key_val(uint64_t key) {
+    return ord_to_f32(static_cast<uint32_t>(key >> 32));
+}
+
+// ---------------------------------------------------------------- wave ops
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// Sum over the wave; every lane gets the same value (fixed butterfly order).
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, kWave);
+    return x;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        uint64_t y = __shfl_xor(x, off, kWave);
+        x = y > x ? y : x;
+    }
+    return x;
+}
+
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        int y = __shfl_up(x, off, kWave);
+        if (lane >= off) x += y;
+    }
+    return x;
+}
+
+// Exclusive scan over a workgroup of NT threads.  `tmp` holds NT/64 + 1 ints
+// of LDS.  Returns the exclusive prefix and writes the block total.
+template <int NT>
+__device__ __forceinline__ int block_exclusive_scan(int x, int* tmp, int* total) {
+    constexpr int NW = NT / kWave;
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    int inc = wave_inclusive_scan(x);
+    if (lane == kWave - 1) tmp[w] = inc;
+    __syncthreads();
+    if (w == 0) {
+        int t = lane < NW ? tmp[lane] : 0;
+        int ti = wave_inclusive_scan(t);
+        if (lane < NW) tmp[lane] = ti - t;
+        if (lane == NW - 1) tmp[NW] = ti;
+    }
+    __syncthreads();
+    int res = inc - x + tmp[w];
+    *total = tmp[NW];
+    __syncthreads();
+    return res;
+}
+
+// Float inclusive scan over a workgroup, fixed association order.
+template <int NT>
+__device__ __forceinline__ float block_inclusive_scan_f32(float x, float* tmp, float* total) {
+    constexpr int NW = NT / kWave;
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        float y = __shfl_up(x, off, kWave);
+        if (lane >= off) x += y;
+    }
+    if (lane == kWave - 1) tmp[w] = x;
+    __syncthreads();
+    if (w == 0) {
+        float t = lane < NW ? tmp[lane] : 0.0f;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            float y = __shfl_up(t, off, kWave);
+            if (lane >= off) t += y;
+        }
+        if (lane < NW) tmp[NW + 1 + lane] = t;  // inclusive wave prefixes
+    }
+    __syncthreads();
+    float base = w > 0 ? tmp[NW + 1 + w - 1] : 0.0f;
+    *total = tmp[NW + 1 + NW - 1];
+    __syncthreads();
+    return base + x;
+}
+
+__device__ __forceinline__ float apply_act(float y, int act) {
+    if (act == DYNA_ACT_RELU) return y > 0.0f ? y : 0.0f;
+    if (act == DYNA_ACT_SILU) return y / (1.0f + expf(-y));
+    return y;
+}
+
+}  // namespace dyna

@@ -1,0 +1,113 @@
+// Internal declarations shared by the libdynahead translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "dynahead.h"
+
+namespace dyna {
+
+constexpr int kWave = 64;
+constexpr int kTileRows = 16;     // layout rows per work chunk (one MFMA A tile)
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// A work chunk of the gathered head: up to kTileRows consecutive layout rows
+// of one cluster and the list of contexts that selected that cluster.
+struct Chunk {
+    int32_t r0;        // first layout row
+    int32_t nrows;     // rows in this chunk (1..kTileRows)
+    int32_t list_off;  // first entry of the cluster's context list
+    int32_t list_cnt;  // number of contexts that selected the cluster
+};
+
+// One context that selected a cluster: its row b and the shortlist slot of
+// layout row r, which is slot_base + r.
+struct ListEntry {
+    int32_t b;
+    int32_t slot_base;
+};
+
+// Device-side header of a plan; counts are written by the plan kernels.
+struct PlanHeader {
+    int32_t n_chunks;
+    int32_t n_entries;
+    int32_t pad[62];
+};
+
+// Views into a caller workspace for the gathered head.
+struct Plan {
+    PlanHeader* hdr;
+    Chunk* chunks;       // [max_chunks]
+    ListEntry* list;     // [max_entries]
+    int32_t max_chunks;
+    int32_t max_entries;
+};
+
+// Launch error -> status with a message.
+dyna_status set_error(dyna_status s, const char* fmt, ...);
+dyna_status check_launch(const char* what);
+
+// ---------------- launchers (defined in the .hip files) ----------------
+
+// layout.hip
+dyna_status launch_build_layout(const int32_t* cluster_of, int32_t V, int32_t M,
+                                const void* W_lm, int32_t wdtype, int32_t d, void* W_perm,
+                                int32_t* perm, int32_t* offsets, void* ws, size_t ws_bytes,
+                                int32_t* host_offsets_out, hipStream_t stream);
+size_t layout_ws_bytes(int32_t V, int32_t M);
+
+// rowdot.hip: out[b * ld + base_b + row] = act(sum_k W[row, k] * v[b, k] + bias[row])
+struct RowdotArgs {
+    const void* W;          // [rows, K]
+    int32_t wdtype;
+    int32_t K;
+    const void* v;          // [B, K] (row stride K)
+    int32_t vdtype;
+    int32_t B;
+    float* out;
+    int64_t ld;             // output row stride (per context)
+    const float* bias;      // [rows] or nullptr
+    int32_t act;            // dyna_act
+    // dense mode: rows [0, n_rows), every context, base 0
+    int32_t n_rows;
+    // plan mode (when plan.hdr != nullptr): chunks and context lists
+    Plan plan;
+    int32_t max_chunks_bound;  // host-known upper bound on plan chunks
+};
+dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);
+
+// select.hip
+dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int32_t k,
+                                 int32_t* topk_ids, float* topk_scores,
+                                 // optional fused shortlist outputs (all or none)
+                                 const int32_t* offsets, int32_t* sel_sorted,
+                                 int32_t* sel_rowoff, int32_t* row_len, hipStream_t stream);
+dyna_status launch_shortlist(const int32_t* offsets, const int32_t* perm, int32_t M,
+                             const int32_t* topk_ids, int32_t B, int32_t k,
+                             int32_t* sel_sorted, int32_t* sel_rowoff, int32_t* row_len,
+                             int32_t* shortlist_ids, int32_t cap, hipStream_t stream);
+dyna_status launch_plan(const int32_t* offsets, int32_t M, const int32_t* sel_sorted,
+                        const int32_t* sel_rowoff, int32_t B, int32_t k, Plan plan,
+                        hipStream_t stream);
+dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_len,
+                          int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
+                          const int32_t* sel_rowoff, const int32_t* offsets,
+                          const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
+                          float temperature, const float* uniforms, int32_t* out_ids,
+                          float* out_logprobs, int32_t* out_sample,
+                          float* out_sample_logprob, void* ws, hipStream_t stream);
+// Workspace for launch_select with rows of at most max_len slots.
+size_t select_ws_bytes(int32_t B, int32_t max_len, int32_t k_t);
+// Longest row launch_select handles (256 segments).
+int32_t select_max_len();
+
+// Global options (dyna_set_option).
+int option_logits_path();
+int option_router_path();
+
+}  // namespace dyna

@@ -1,0 +1,328 @@
+// Row-dot kernels: out[b, base_b + row] = act(W[row, :] . v[b, :] + bias[row]).
+//
+// The same two kernels serve the router layers (every row of W against every
+// context, Sec. 4.2 "Low-cost router") and the gathered head (only the rows of
+// the selected cluster slabs, each against the contexts that selected that
+// cluster: Sec. 4.3, the gathered LM head / FUSED_INDEX_GEMM of Algorithm 1).
+//
+//  * rowdot_gemv_kernel: one wave per W row.  Each lane streams 16-byte pieces
+//    of the row (a wave covers 1 KiB of one row per load), keeps the row in
+//    registers and dots it with each context that needs it; a butterfly sum
+//    finishes each dot product.  Chosen for few contexts (B <= 4), where the
+//    kernel is a pure HBM stream.
+//  * rowdot_mfma_kernel: one wave per tile of 16 W rows; contexts are the 16
+//    columns of v_mfma_f32_16x16x32_bf16 (G column groups per pass).  Chosen
+//    for tree and serving batches, where one slab row feeds many contexts.
+//    An fp32 right operand (the router's hidden layer) is split into two bf16
+//    terms hi + lo, so the product keeps ~16 significant bits of it.
+//
+// W rows are read with non-temporal loads (each row is touched once per call);
+// v rows are small and re-read from cache.  All sums have a fixed order, so
+// results are bit-identical from run to run.
+#include "dyna_device.h"
+
+namespace dyna {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWavesPerBlock = kThreads / kWave;
+
+// ------------------------------------------------------------------ GEMV
+template <typename WT, typename VT, int NB, bool PLAN>
+__global__ __launch_bounds__(kThreads) void rowdot_gemv_kernel(RowdotArgs a) {
+    const int lane = lane_id();
+    const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
+    const int64_t n_items = PLAN ? (int64_t)a.plan.hdr->n_chunks * kTileRows : (int64_t)a.n_rows;
+    const WT* __restrict__ W = static_cast<const WT*>(a.W);
+    const VT* __restrict__ v = static_cast<const VT*>(a.v);
+    const int K = a.K;
+
+    for (int64_t it = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; it < n_items;
+         it += nwaves) {
+        int64_t row;
+        int lcnt;
+        const ListEntry* list = nullptr;
+        if constexpr (PLAN) {
+            const Chunk c = a.plan.chunks[it / kTileRows];
+            const int r = (int)(it % kTileRows);
+            if (r >= c.nrows) continue;
+            row = (int64_t)c.r0 + r;
+            lcnt = c.list_cnt;
+            list = a.plan.list + c.list_off;
+        } else {
+            row = it;
+            lcnt = a.B;
+        }
+        const WT* wr = W + row * K;
+        float w[NB][8];
+#pragma unroll
+        for (int blk = 0; blk < NB; ++blk) {
+            const int e = blk * 512 + lane * 8;
+            if (e < K) {
+                Load8<WT, true>::run(wr + e, w[blk]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) w[blk][j] = 0.0f;
+            }
+        }
+        const float bias = a.bias ? a.bias[row] : 0.0f;
+        for (int i = 0; i < lcnt; ++i) {
+            int b, base;
+            if constexpr (PLAN) {
+                const ListEntry le = list[i];
+                b = le.b;
+                base = le.slot_base;
+            } else {
+                b = i;
+                base = 0;
+            }
+            const VT* vr = v + (int64_t)b * K;
+            float acc = 0.0f;
+#pragma unroll
+            for (int blk = 0; blk < NB; ++blk) {
+                const int e = blk * 512 + lane * 8;
+                if (e < K) {
+                    float x[8];
+                    Load8<VT, false>::run(vr + e, x);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) acc = fmaf(w[blk][j], x[j], acc);
+                }
+            }
+            acc = wave_sum(acc);
+            if (lane == 0) a.out[(int64_t)b * a.ld + base + row] = apply_act(acc + bias, a.act);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ MFMA
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+// 8 consecutive fp32 values split into bf16 hi and lo terms.
+__device__ __forceinline__ void split8(const float* p, u32x4& hi, u32x4& lo) {
+    const u32x4* q = reinterpret_cast<const u32x4*>(p);
+    const u32x4 x0 = q[0], x1 = q[1];
+    float f[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[i] = __uint_as_float(x0[i]);
+        f[4 + i] = __uint_as_float(x1[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t h0 = f32_to_bf16_bits(f[2 * i]);
+        const uint32_t h1 = f32_to_bf16_bits(f[2 * i + 1]);
+        const uint32_t l0 = f32_to_bf16_bits(f[2 * i] - __uint_as_float(h0 << 16));
+        const uint32_t l1 = f32_to_bf16_bits(f[2 * i + 1] - __uint_as_float(h1 << 16));
+        hi[i] = h0 | (h1 << 16);
+        lo[i] = l0 | (l1 << 16);
+    }
+}
+
+template <int G, bool VF32, bool PLAN, int KSPLIT, int U>
+__global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
+    static_assert(KSPLIT == 1 || KSPLIT == kWavesPerBlock, "K split is per wave of a block");
+    __shared__ float red[KSPLIT > 1 ? (KSPLIT - 1) * G * 4 * kWave : 1];
+    const int lane = lane_id();
+    const int wv = threadIdx.x / kWave;
+    const int col = lane & 15;   // A row inside the tile, and B / D column
+    const int kq = lane >> 4;    // 8-element slice of each 32-wide k step
+    const int K = a.K;
+    const int nsteps = (K + 31) / 32;
+    const uint16_t* __restrict__ W = static_cast<const uint16_t*>(a.W);
+
+    const int64_t n_items =
+        PLAN ? (int64_t)a.plan.hdr->n_chunks : ((int64_t)a.n_rows + kTileRows - 1) / kTileRows;
+    const int64_t item0 = KSPLIT == 1 ? (int64_t)blockIdx.x * kWavesPerBlock + wv : blockIdx.x;
+    const int64_t istride = KSPLIT == 1 ? (int64_t)gridDim.x * kWavesPerBlock : gridDim.x;
+    const int s_begin = KSPLIT == 1 ? 0 : (wv * nsteps) / KSPLIT;
+    const int s_end = KSPLIT == 1 ? nsteps : ((wv + 1) * nsteps) / KSPLIT;
+
+    for (int64_t it = item0; it < n_items; it += istride) {
+        int r0, nrows, lcnt;
+        const ListEntry* list = nullptr;
+        if constexpr (PLAN) {
+            const Chunk c = a.plan.chunks[it];
+            r0 = c.r0;
+            nrows = c.nrows;
+            lcnt = c.list_cnt;
+            list = a.plan.list + c.list_off;
+        } else {
+            r0 = (int)(it * kTileRows);
+            nrows = min(kTileRows, a.n_rows - r0);
+            lcnt = a.B;
+        }
+        const bool rvalid = col < nrows;
+        const uint16_t* wrow = W + (int64_t)(r0 + (rvalid ? col : 0)) * K + kq * 8;
+
+        for (int gb = 0; gb < lcnt; gb += 16 * G) {
+            int cb[G], cbase[G];
+            bool cvalid[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const int e = gb + g * 16 + col;
+                cvalid[g] = e < lcnt;
+                if constexpr (PLAN) {
+                    const ListEntry le = cvalid[g] ? list[e] : ListEntry{0, 0};
+                    cb[g] = le.b;
+                    cbase[g] = le.slot_base;
+                } else {
+                    cb[g] = cvalid[g] ? e : 0;
+                    cbase[g] = 0;
+                }
+            }
+            f32x4 acc[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+            for (int s = s_begin; s < s_end; s += U) {
+                u32x4 A[U];
+                u32x4 Bh[U][G];
+                u32x4 Bl[U][G];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int k = (s + u) * 32 + kq * 8;
+                    const bool kv = (s + u) < s_end && k < K;
+                    A[u] = (rvalid && kv)
+                               ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow + (s + u) * 32))
+                               : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                    for (int g = 0; g < G; ++g) {
+                        Bh[u][g] = u32x4{0u, 0u, 0u, 0u};
+                        Bl[u][g] = u32x4{0u, 0u, 0u, 0u};
+                        if (cvalid[g] && kv) {
+                            if constexpr (VF32) {
+                                split8(static_cast<const float*>(a.v) + (int64_t)cb[g] * K + k,
+                                       Bh[u][g], Bl[u][g]);
+                            } else {
+                                Bh[u][g] = *reinterpret_cast<const u32x4*>(
+                                    static_cast<const uint16_t*>(a.v) + (int64_t)cb[g] * K + k);
+                            }
+                        }
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+#pragma unroll
+                    for (int g = 0; g < G; ++g) {
+                        if (gb + g * 16 < lcnt) {  // wave-uniform
+                            acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                as_bf16x8(A[u]), as_bf16x8(Bh[u][g]), acc[g], 0, 0, 0);
+                            if constexpr (VF32)
+                                acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    as_bf16x8(A[u]), as_bf16x8(Bl[u][g]), acc[g], 0, 0, 0);
+                        }
+                    }
+                }
+            }
+
+            if constexpr (KSPLIT > 1) {
+                if (wv > 0) {
+#pragma unroll
+                    for (int g = 0; g < G; ++g)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            red[(((wv - 1) * G + g) * 4 + r) * kWave + lane] = acc[g][r];
+                }
+                __syncthreads();
+                if (wv == 0) {
+#pragma unroll
+                    for (int w = 1; w < KSPLIT; ++w)
+#pragma unroll
+                        for (int g = 0; g < G; ++g)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r)
+                                acc[g][r] += red[(((w - 1) * G + g) * 4 + r) * kWave + lane];
+                }
+                __syncthreads();
+                if (wv != 0) continue;
+            }
+
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                if (!cvalid[g]) continue;
+                float* o = a.out + (int64_t)cb[g] * a.ld + cbase[g] + r0;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int i = kq * 4 + r;
+                    if (i < nrows) {
+                        const float bias = a.bias ? a.bias[r0 + i] : 0.0f;
+                        o[i] = apply_act(acc[g][r] + bias, a.act);
+                    }
+                }
+            }
+        }
+    }
+}
+
+int resident_blocks() { return 256 * 8; }  // 256 CUs x 8 blocks of 4 waves
+
+template <typename WT, typename VT, bool PLAN>
+dyna_status launch_gemv_nb(const RowdotArgs& a, int nb, unsigned grid, hipStream_t stream) {
+#define DYNA_GEMV_CASE(N)                                                              \
+    if (nb <= N) {                                                                     \
+        rowdot_gemv_kernel<WT, VT, N, PLAN><<<grid, kThreads, 0, stream>>>(a);         \
+        return check_launch("rowdot_gemv_kernel");                                     \
+    }
+    DYNA_GEMV_CASE(1)
+    DYNA_GEMV_CASE(2)
+    DYNA_GEMV_CASE(4)
+    DYNA_GEMV_CASE(8)
+    DYNA_GEMV_CASE(12)
+    DYNA_GEMV_CASE(16)
+#undef DYNA_GEMV_CASE
+    return set_error(DYNA_ERR_UNSUPPORTED, "rowdot: K > 8192");
+}
+
+template <bool PLAN>
+dyna_status launch_gemv(const RowdotArgs& a, hipStream_t stream) {
+    const int nb = (a.K + 511) / 512;
+    const int64_t items = PLAN ? (int64_t)a.max_chunks_bound * kTileRows : (int64_t)a.n_rows;
+    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock,
+                                                                   resident_blocks()));
+    const unsigned grid = (unsigned)blocks;
+    const bool wb = a.wdtype == DYNA_BF16, vb = a.vdtype == DYNA_BF16;
+    if (wb && vb) return launch_gemv_nb<uint16_t, uint16_t, PLAN>(a, nb, grid, stream);
+    if (wb && !vb) return launch_gemv_nb<uint16_t, float, PLAN>(a, nb, grid, stream);
+    if (!wb && vb) return launch_gemv_nb<float, uint16_t, PLAN>(a, nb, grid, stream);
+    return launch_gemv_nb<float, float, PLAN>(a, nb, grid, stream);
+}
+
+template <int G, bool VF32, bool PLAN, int KSPLIT, int U>
+dyna_status launch_mfma_t(const RowdotArgs& a, hipStream_t stream) {
+    const int64_t items = PLAN ? (int64_t)a.max_chunks_bound
+                               : ((int64_t)a.n_rows + kTileRows - 1) / kTileRows;
+    const int64_t per_block = KSPLIT == 1 ? kWavesPerBlock : 1;
+    const int64_t blocks =
+        std::max<int64_t>(1, std::min<int64_t>((items + per_block - 1) / per_block, resident_blocks()));
+    rowdot_mfma_kernel<G, VF32, PLAN, KSPLIT, U><<<(unsigned)blocks, kThreads, 0, stream>>>(a);
+    return check_launch("rowdot_mfma_kernel");
+}
+
+template <bool VF32, bool PLAN>
+dyna_status launch_mfma(const RowdotArgs& a, hipStream_t stream) {
+    if (PLAN) return launch_mfma_t<1, VF32, PLAN, 1, 8>(a, stream);
+    // dense: all contexts share every row; split K over the 4 waves of a
+    // block so that a small W still spreads over many CUs
+    const int groups = (a.B + 15) / 16;
+    if (groups <= 1) return launch_mfma_t<1, VF32, PLAN, kWavesPerBlock, 4>(a, stream);
+    if (groups <= 2) return launch_mfma_t<2, VF32, PLAN, kWavesPerBlock, 2>(a, stream);
+    if (groups <= 4) return launch_mfma_t<4, VF32, PLAN, kWavesPerBlock, 1>(a, stream);
+    return launch_mfma_t<8, VF32, PLAN, kWavesPerBlock, 1>(a, stream);
+}
+
+}  // namespace
+
+// path: 0 automatic, 1 GEMV, 2 MFMA
+dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream) {
+    const bool plan = a.plan.hdr != nullptr;
+    const bool mfma_ok = a.wdtype == DYNA_BF16;
+    if (path == 2 && !mfma_ok)
+        return set_error(DYNA_ERR_UNSUPPORTED, "rowdot: MFMA path needs bf16 weights");
+    const bool use_mfma = path == 2 || (path == 0 && mfma_ok && a.B > 4);
+    if (!use_mfma) return plan ? launch_gemv<true>(a, stream) : launch_gemv<false>(a, stream);
+    const bool vf32 = a.vdtype == DYNA_F32;
+    if (plan) return vf32 ? launch_mfma<true, true>(a, stream) : launch_mfma<false, true>(a, stream);
+    return vf32 ? launch_mfma<true, false>(a, stream) : launch_mfma<false, false>(a, stream);
+}
+
+}  // namespace dyna

@@ -1,0 +1,628 @@
+// Routing top-k, shortlist construction, the gathered-head work plan and the
+// draft selection.
+//
+//  topk_clusters_kernel  K_b = TopK_k(s_b) (Sec. 4.2): radix select of the
+//                        k-th largest score on 8-bit digits, then the ties at
+//                        that score taken lowest id first; optionally also the
+//                        row's shortlist (Sec. 4.2: V_S = disjoint union of the
+//                        selected clusters) as a prefix sum of cluster sizes.
+//  shortlist_kernel      the same shortlist from any list of cluster ids.
+//  plan_kernel           the batch's distinct selected clusters, cut into
+//                        16-row chunks, each with the contexts that chose it,
+//                        so that every selected slab is streamed once.
+//  select_partial/final  Algorithm 1's log_softmax, TopK_{k_t} and remap to
+//                        vocabulary ids, plus inverse-CDF sampling from the
+//                        restricted draft q_S (Sec. 5), split over 2048-slot
+//                        segments so long rows (the dense baseline) spread
+//                        over many workgroups.
+#include "dyna_device.h"
+
+namespace dyna {
+namespace {
+
+constexpr int kNT = 256;
+
+// ------------------------------------------------------------------ top-k
+__global__ __launch_bounds__(kNT) void topk_clusters_kernel(
+    const float* __restrict__ scores, int M, int k, int32_t* __restrict__ topk_ids,
+    float* __restrict__ topk_scores, const int32_t* __restrict__ offsets,
+    int32_t* __restrict__ sel_sorted, int32_t* __restrict__ sel_rowoff,
+    int32_t* __restrict__ row_len) {
+    extern __shared__ unsigned char smem[];
+    uint64_t* skey = reinterpret_cast<uint64_t*>(smem);       // [k], ascending id
+    int32_t* ssize = reinterpret_cast<int32_t*>(skey + k);    // [k]
+    __shared__ int hist[256];
+    __shared__ int tmp[kNT / kWave + 1];
+    __shared__ uint32_t sh_prefix;
+    __shared__ int sh_krem;
+
+    const int b = blockIdx.x;
+    const float* s = scores + (int64_t)b * M;
+    const int E = (M + kNT - 1) / kNT;
+    const int j0 = min(M, (int)threadIdx.x * E);
+    const int j1 = min(M, j0 + E);
+
+    // radix select: the ordered code T of the k-th largest score, and how
+    // many of the codes equal to T still have to be taken (krem >= 1)
+    uint32_t prefix = 0, mask = 0;
+    int krem = k;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int i = threadIdx.x; i < 256; i += kNT) hist[i] = 0;
+        __syncthreads();
+        for (int j = j0; j < j1; ++j) {
+            const uint32_t o = ord_f32(s[j]);
+            if ((o & mask) == prefix) atomicAdd(&hist[(o >> shift) & 255u], 1);
+        }
+        __syncthreads();
+        if (threadIdx.x < kWave) {
+            const int l = threadIdx.x;  // lane l holds digits 255-4l .. 252-4l
+            int c[4], sum = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                c[q] = hist[255 - 4 * l - q];
+                sum += c[q];
+            }
+            const int inc = wave_inclusive_scan(sum);
+            const int exc = inc - sum;
+            if (exc < krem && krem <= inc) {
+                int acc = exc;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (acc + c[q] >= krem) {
+                        sh_prefix = prefix | ((uint32_t)(255 - 4 * l - q) << shift);
+                        sh_krem = krem - acc;
+                        break;
+                    }
+                    acc += c[q];
+                }
+            }
+        }
+        __syncthreads();
+        prefix = sh_prefix;
+        krem = sh_krem;
+        mask |= 255u << shift;
+        __syncthreads();
+    }
+    const uint32_t T = prefix;
+
+    int n_gt = 0, n_eq = 0;
+    for (int j = j0; j < j1; ++j) {
+        const uint32_t o = ord_f32(s[j]);
+        n_gt += o > T;
+        n_eq += o == T;
+    }
+    int total;
+    const int eq_before = block_exclusive_scan<kNT>(n_eq, tmp, &total);
+    const int take_eq = max(0, min(n_eq, krem - eq_before));
+    const int sel_before = block_exclusive_scan<kNT>(n_gt + take_eq, tmp, &total);
+    int pos = sel_before, eq_seen = 0;
+    for (int j = j0; j < j1; ++j) {
+        const uint32_t o = ord_f32(s[j]);
+        bool take = o > T;
+        if (o == T) take = eq_seen++ < take_eq;
+        if (take) skey[pos++] = (static_cast<uint64_t>(o) << 32) | (0xffffffffu - (uint32_t)j);
+    }
+    __syncthreads();
+
+    // rank order (score desc, id asc) by counting larger keys
+    for (int i = threadIdx.x; i < k; i += kNT) {
+        const uint64_t key = skey[i];
+        int rank = 0;
+        for (int j = 0; j < k; ++j) rank += skey[j] > key;
+        const uint32_t id = key_id(key);
+        topk_ids[(int64_t)b * k + rank] = (int32_t)id;
+        if (topk_scores) topk_scores[(int64_t)b * k + rank] = s[id];
+    }
+
+    if (sel_sorted != nullptr) {
+        const int per = (k + kNT - 1) / kNT;
+        const int i0 = min(k, (int)threadIdx.x * per);
+        const int i1 = min(k, i0 + per);
+        int local = 0;
+        for (int i = i0; i < i1; ++i) {
+            const int m = (int)key_id(skey[i]);
+            ssize[i] = offsets[m + 1] - offsets[m];
+            local += ssize[i];
+        }
+        int len;
+        int run = block_exclusive_scan<kNT>(local, tmp, &len);
+        for (int i = i0; i < i1; ++i) {
+            sel_sorted[(int64_t)b * k + i] = (int32_t)key_id(skey[i]);
+            sel_rowoff[(int64_t)b * (k + 1) + i] = run;
+            run += ssize[i];
+        }
+        if (threadIdx.x == 0) {
+            sel_rowoff[(int64_t)b * (k + 1) + k] = len;
+            row_len[b] = len;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ shortlist
+__global__ __launch_bounds__(kNT) void shortlist_kernel(
+    const int32_t* __restrict__ offsets, const int32_t* __restrict__ perm, int M,
+    const int32_t* __restrict__ topk_ids, int k, int32_t* __restrict__ sel_sorted,
+    int32_t* __restrict__ sel_rowoff, int32_t* __restrict__ row_len,
+    int32_t* __restrict__ shortlist_ids, int64_t cap) {
+    extern __shared__ int32_t sl[];
+    int32_t* ids = sl;            // [k] input ids, -1 when dropped
+    int32_t* sid = sl + k;        // [k] kept ids ascending, then -1
+    int32_t* soff = sl + 2 * k;   // [k + 1] row offsets
+    __shared__ int tmp[kNT / kWave + 1];
+    __shared__ int sh_nkeep;
+    const int b = blockIdx.x;
+    const int32_t* in = topk_ids + (int64_t)b * k;
+
+    for (int i = threadIdx.x; i < k; i += kNT) {
+        const int m = in[i];
+        ids[i] = (m >= 0 && m < M) ? m : -1;
+    }
+    __syncthreads();
+    // drop repeats: keep the first occurrence of every id
+    for (int i = threadIdx.x; i < k; i += kNT) {
+        const int m = ids[i];
+        bool dup = false;
+        if (m >= 0)
+            for (int j = 0; j < i; ++j) dup |= ids[j] == m;
+        sid[i] = dup ? -1 : m;   // staging: kept id or -1
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < k; i += kNT) ids[i] = sid[i];
+    __syncthreads();
+    int nkeep_local = 0;
+    for (int i = threadIdx.x; i < k; i += kNT) nkeep_local += ids[i] >= 0;
+    int nkeep;
+    block_exclusive_scan<kNT>(nkeep_local, tmp, &nkeep);
+    for (int i = threadIdx.x; i < k; i += kNT) sid[i] = -1;
+    __syncthreads();
+    for (int i = threadIdx.x; i < k; i += kNT) {
+        const int m = ids[i];
+        if (m < 0) continue;
+        int rank = 0;
+        for (int j = 0; j < k; ++j) rank += (ids[j] >= 0 && ids[j] < m);
+        sid[rank] = m;
+    }
+    if (threadIdx.x == 0) sh_nkeep = nkeep;
+    __syncthreads();
+
+    const int per = (k + kNT - 1) / kNT;
+    const int i0 = min(k, (int)threadIdx.x * per);
+    const int i1 = min(k, i0 + per);
+    int local = 0;
+    for (int i = i0; i < i1; ++i) {
+        const int m = sid[i];
+        local += m >= 0 ? offsets[m + 1] - offsets[m] : 0;
+    }
+    int len;
+    int run = block_exclusive_scan<kNT>(local, tmp, &len);
+    for (int i = i0; i < i1; ++i) {
+        const int m = sid[i];
+        sel_sorted[(int64_t)b * k + i] = m;
+        sel_rowoff[(int64_t)b * (k + 1) + i] = run;
+        soff[i] = run;
+        run += m >= 0 ? offsets[m + 1] - offsets[m] : 0;
+    }
+    if (threadIdx.x == 0) {
+        sel_rowoff[(int64_t)b * (k + 1) + k] = len;
+        row_len[b] = len;
+    }
+    __syncthreads();
+    if (shortlist_ids != nullptr) {
+        for (int i = 0; i < sh_nkeep; ++i) {
+            const int m = sid[i];
+            const int o = offsets[m], n = offsets[m + 1] - o;
+            for (int t = threadIdx.x; t < n; t += kNT)
+                shortlist_ids[(int64_t)b * cap + soff[i] + t] = perm[o + t];
+        }
+    }
+}
+
+// ------------------------------------------------------------------ plan
+constexpr int kPlanThreads = 1024;
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(
+    const int32_t* __restrict__ offsets, int M, const int32_t* __restrict__ sel_sorted,
+    const int32_t* __restrict__ sel_rowoff, int B, int k, Plan plan) {
+    extern __shared__ int32_t pl[];
+    int32_t* cnt = pl;            // contexts per cluster, later the list fill counters
+    int32_t* loff = pl + M;       // first list entry per cluster
+    int32_t* coff = pl + 2 * M;   // first chunk per cluster
+    __shared__ int tmp[kPlanThreads / kWave + 1];
+    for (int m = threadIdx.x; m < M; m += kPlanThreads) cnt[m] = 0;
+    __syncthreads();
+    const int64_t n_sel = (int64_t)B * k;
+    for (int64_t e = threadIdx.x; e < n_sel; e += kPlanThreads) {
+        const int m = sel_sorted[e];
+        if (m >= 0 && m < M) atomicAdd(&cnt[m], 1);
+    }
+    __syncthreads();
+    const int per = (M + kPlanThreads - 1) / kPlanThreads;
+    const int m0 = min(M, (int)threadIdx.x * per);
+    const int m1 = min(M, m0 + per);
+    int lc = 0, lch = 0;
+    for (int m = m0; m < m1; ++m) {
+        lc += cnt[m];
+        if (cnt[m] > 0) lch += (offsets[m + 1] - offsets[m] + kTileRows - 1) / kTileRows;
+    }
+    int n_entries, n_chunks;
+    int rl = block_exclusive_scan<kPlanThreads>(lc, tmp, &n_entries);
+    int rc = block_exclusive_scan<kPlanThreads>(lch, tmp, &n_chunks);
+    for (int m = m0; m < m1; ++m) {
+        loff[m] = rl;
+        coff[m] = rc;
+        rl += cnt[m];
+        if (cnt[m] == 0) continue;
+        const int o = offsets[m], n = offsets[m + 1] - o;
+        for (int c = 0; c * kTileRows < n; ++c)
+            plan.chunks[rc + c] =
+                Chunk{o + c * kTileRows, min(kTileRows, n - c * kTileRows), loff[m], cnt[m]};
+        rc += (n + kTileRows - 1) / kTileRows;
+    }
+    __syncthreads();
+    for (int m = threadIdx.x; m < M; m += kPlanThreads) cnt[m] = 0;
+    __syncthreads();
+    for (int64_t e = threadIdx.x; e < n_sel; e += kPlanThreads) {
+        const int m = sel_sorted[e];
+        if (m < 0 || m >= M) continue;
+        const int b = (int)(e / k), i = (int)(e % k);
+        const int slot_base = sel_rowoff[(int64_t)b * (k + 1) + i] - offsets[m];
+        const int p = atomicAdd(&cnt[m], 1);
+        plan.list[loff[m] + p] = ListEntry{b, slot_base};
+    }
+    if (threadIdx.x == 0) {
+        plan.hdr->n_chunks = n_chunks;
+        plan.hdr->n_entries = n_entries;
+    }
+}
+
+// ------------------------------------------------------------------ select
+constexpr int kSeg = 2048;          // shortlist slots per partial workgroup
+constexpr int kPer = kSeg / kNT;    // 8 slots per thread
+
+struct SelectArgs {
+    const float* logits;
+    int64_t ld;
+    const int32_t* row_len;   // nullptr: every row has fixed_len
+    int32_t fixed_len;
+    const int32_t* sel_sorted;
+    const int32_t* sel_rowoff;
+    const int32_t* offsets;
+    const int32_t* perm;      // nullptr: vocabulary id = slot
+    int32_t k;
+    int32_t k_t;
+    float inv_t;
+    const float* uniforms;
+    int32_t P;                // segments per row
+    // partials, [B][P][...]
+    uint64_t* pkeys;          // [B][P][k_t]
+    float* pmax;              // [B][P]
+    float* psum;              // [B][P]
+    int32_t* out_ids;
+    float* out_logprobs;
+    int32_t* out_sample;
+    float* out_sample_logprob;
+};
+
+__device__ __forceinline__ float canon(float z) { return z != z ? -__builtin_inff() : z; }
+
+// Vocabulary ids of the slots [j0, j0 + n) of row b, written into vid[].
+__device__ __forceinline__ void slot_vids(const SelectArgs& a, int b, int j0, int n, uint32_t* vid) {
+    if (a.perm == nullptr) {
+        for (int q = 0; q < n; ++q) vid[q] = (uint32_t)(j0 + q);
+        return;
+    }
+    const int32_t* ro = a.sel_rowoff + (int64_t)b * (a.k + 1);
+    const int32_t* ss = a.sel_sorted + (int64_t)b * a.k;
+    // largest ci with ro[ci] <= j0
+    int lo = 0, hi = a.k - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (ro[mid] <= j0) lo = mid; else hi = mid - 1;
+    }
+    int ci = lo;
+    int end = ro[ci + 1];
+    for (int q = 0; q < n; ++q) {
+        const int j = j0 + q;
+        while (j >= end) {
+            ++ci;
+            end = ro[ci + 1];
+        }
+        const int m = ss[ci];
+        vid[q] = (uint32_t)a.perm[a.offsets[m] + (j - ro[ci])];
+    }
+}
+
+// Block-wide selection of the k_t largest keys from per-thread lists sorted
+// descending (list[0] largest, 0 = empty).  Thread 0 receives them in out[].
+template <int L>
+__device__ void block_topk_rounds(uint64_t (&list)[L], int k_t, uint64_t* wmax /* LDS [2][4] */,
+                                  uint64_t* out /* LDS [k_t] */) {
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    for (int r = 0; r < k_t; ++r) {
+        const uint64_t m = wave_max_u64(list[0]);
+        if (lane == 0) wmax[(r & 1) * 4 + w] = m;
+        __syncthreads();
+        uint64_t best = wmax[(r & 1) * 4];
+#pragma unroll
+        for (int q = 1; q < kNT / kWave; ++q) best = max(best, wmax[(r & 1) * 4 + q]);
+        if (best != 0 && list[0] == best) {
+#pragma unroll
+            for (int q = 0; q < L - 1; ++q) list[q] = list[q + 1];
+            list[L - 1] = 0;
+        }
+        if (threadIdx.x == 0) out[r] = best;
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(kNT) void select_partial_kernel(SelectArgs a) {
+    __shared__ uint64_t wmax[8];
+    __shared__ uint64_t top[DYNA_MAX_KT];
+    __shared__ float red[kNT / kWave];
+    const int p = blockIdx.x, b = blockIdx.y;
+    const int len = a.row_len ? a.row_len[b] : a.fixed_len;
+    const int seg0 = p * kSeg;
+    const int j0 = seg0 + threadIdx.x * kPer;
+    const int n = max(0, min(kPer, len - j0));
+    const float* z = a.logits + (int64_t)b * a.ld;
+
+    uint32_t vid[kPer];
+    float zv[kPer];
+    uint64_t list[kPer];
+    if (n > 0) slot_vids(a, b, j0, n, vid);
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        zv[q] = q < n ? canon(z[j0 + q]) : -__builtin_inff();
+        list[q] = q < n ? sel_key(zv[q], vid[q]) : 0;
+    }
+    // sort the thread's keys descending (odd-even transposition network)
+#pragma unroll
+    for (int r = 0; r < kPer; ++r)
+#pragma unroll
+        for (int q = r & 1; q + 1 < kPer; q += 2)
+            if (list[q] < list[q + 1]) {
+                const uint64_t t = list[q];
+                list[q] = list[q + 1];
+                list[q + 1] = t;
+            }
+    block_topk_rounds<kPer>(list, a.k_t, wmax, top);
+    // segment max = value of the best key (or -inf for an empty segment)
+    const float smax = top[0] != 0 ? key_val(top[0]) : -__builtin_inff();
+    float tsum = 0.0f;
+    if (smax != -__builtin_inff()) {
+#pragma unroll
+        for (int q = 0; q < kPer; ++q)
+            if (q < n) tsum += expf((zv[q] - smax) * a.inv_t);
+    }
+    tsum = wave_sum(tsum);
+    if (lane_id() == 0) red[threadIdx.x / kWave] = tsum;
+    __syncthreads();
+    const int64_t pb = (int64_t)b * a.P + p;
+    if (threadIdx.x == 0) {
+        float ssum = 0.0f;
+#pragma unroll
+        for (int q = 0; q < kNT / kWave; ++q) ssum += red[q];
+        a.pmax[pb] = smax;
+        a.psum[pb] = ssum;
+    }
+    for (int r = threadIdx.x; r < a.k_t; r += kNT) a.pkeys[pb * a.k_t + r] = top[r];
+}
+
+__global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
+    __shared__ uint64_t wmax[8];
+    __shared__ uint64_t top[DYNA_MAX_KT];
+    __shared__ float sh_mx, sh_total, sh_target, sh_base;
+    __shared__ int sh_seg;
+    __shared__ float red[2 * (kNT / kWave) + 1];
+    __shared__ int sh_pick;
+    __shared__ float incl_s[kNT];
+    const int b = blockIdx.x;
+    const int P = a.P;
+    const int len = a.row_len ? a.row_len[b] : a.fixed_len;
+    const int64_t pb0 = (int64_t)b * P;
+
+    if (threadIdx.x == 0) {
+        float mx = -__builtin_inff();
+        for (int p = 0; p < P; ++p) mx = fmaxf(mx, a.pmax[pb0 + p]);
+        float total = 0.0f;
+        if (mx != -__builtin_inff())
+            for (int p = 0; p < P; ++p) {
+                const float sm = a.pmax[pb0 + p];
+                if (sm != -__builtin_inff()) total += a.psum[pb0 + p] * expf((sm - mx) * a.inv_t);
+            }
+        sh_mx = mx;
+        sh_total = total;
+    }
+    // merge the per-segment lists: thread t walks the list of segment t
+    // (P <= 256 is guaranteed by the host)
+    uint64_t list[1];
+    int head = 0;
+    const uint64_t* mylist = a.pkeys + (pb0 + threadIdx.x) * a.k_t;
+    list[0] = (int)threadIdx.x < P ? mylist[0] : 0;
+    {
+        const int lane = lane_id(), w = threadIdx.x / kWave;
+        for (int r = 0; r < a.k_t; ++r) {
+            const uint64_t m = wave_max_u64(list[0]);
+            if (lane == 0) wmax[(r & 1) * 4 + w] = m;
+            __syncthreads();
+            uint64_t best = wmax[(r & 1) * 4];
+#pragma unroll
+            for (int q = 1; q < kNT / kWave; ++q) best = max(best, wmax[(r & 1) * 4 + q]);
+            if (best != 0 && list[0] == best) {
+                ++head;
+                list[0] = head < a.k_t ? mylist[head] : 0;
+            }
+            if (threadIdx.x == 0) top[r] = best;
+        }
+    }
+    __syncthreads();
+    const float mx = sh_mx, total = sh_total;
+    const float log_total = logf(total);
+    if (a.out_ids != nullptr) {
+        for (int r = threadIdx.x; r < a.k_t; r += kNT) {
+            const uint64_t key = top[r];
+            a.out_ids[(int64_t)b * a.k_t + r] = key != 0 ? (int32_t)key_id(key) : -1;
+            if (a.out_logprobs)
+                a.out_logprobs[(int64_t)b * a.k_t + r] =
+                    key != 0 ? (key_val(key) - mx) * a.inv_t - log_total : -__builtin_inff();
+        }
+    }
+    if (a.uniforms == nullptr || a.out_sample == nullptr) return;
+
+    // inverse CDF: first segment whose running mass passes u * total
+    if (threadIdx.x == 0) {
+        const float target = a.uniforms[b] * total;
+        float run = 0.0f;
+        int seg = -1, last_nz = -1;
+        float base = 0.0f, base_last = 0.0f;
+        for (int p = 0; p < P; ++p) {
+            const float sm = a.pmax[pb0 + p];
+            const float c = sm != -__builtin_inff() ? a.psum[pb0 + p] * expf((sm - mx) * a.inv_t) : 0.0f;
+            if (c > 0.0f) {
+                last_nz = p;
+                base_last = run;
+            }
+            if (seg < 0 && run + c > target && c > 0.0f) {
+                seg = p;
+                base = run;
+            }
+            run += c;
+        }
+        if (seg < 0) {
+            seg = last_nz;
+            base = base_last;
+        }
+        sh_seg = seg;
+        sh_base = base;
+        sh_target = target;
+        sh_pick = -1;
+    }
+    __syncthreads();
+    const int seg = sh_seg;
+    if (seg < 0) {  // empty shortlist
+        if (threadIdx.x == 0) {
+            a.out_sample[b] = -1;
+            if (a.out_sample_logprob) a.out_sample_logprob[b] = -__builtin_inff();
+        }
+        return;
+    }
+    const float* z = a.logits + (int64_t)b * a.ld;
+    const int j0 = seg * kSeg + threadIdx.x * kPer;
+    const int n = max(0, min(kPer, len - j0));
+    float e[kPer];
+    float tsum = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        e[q] = q < n ? expf((canon(z[j0 + q]) - mx) * a.inv_t) : 0.0f;
+        tsum += e[q];
+    }
+    float blk_total;
+    const float incl = block_inclusive_scan_f32<kNT>(tsum, red, &blk_total);
+    incl_s[threadIdx.x] = incl;
+    __syncthreads();
+    const float excl = threadIdx.x > 0 ? incl_s[threadIdx.x - 1] : 0.0f;
+    const float target = sh_target - sh_base;
+    // the thread whose running range holds the target picks inside its slots
+    if (tsum > 0.0f && excl <= target && target < incl) {
+        float acc = excl;
+        int pick = -1, last = -1;
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            if (e[q] > 0.0f) last = q;
+            acc += e[q];
+            if (pick < 0 && e[q] > 0.0f && acc > target) pick = q;
+        }
+        atomicMax(&sh_pick, j0 + (pick >= 0 ? pick : last));
+    }
+    __syncthreads();
+    if (sh_pick < 0) {  // rounding left the target at or past the segment mass: last slot with mass
+        int last = -1;
+#pragma unroll
+        for (int q = 0; q < kPer; ++q)
+            if (e[q] > 0.0f) last = j0 + q;
+        if (last >= 0) atomicMax(&sh_pick, last);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const int j = sh_pick;
+        uint32_t vid;
+        slot_vids(a, b, j, 1, &vid);
+        a.out_sample[b] = (int32_t)vid;
+        if (a.out_sample_logprob) a.out_sample_logprob[b] = (canon(z[j]) - mx) * a.inv_t - log_total;
+    }
+}
+
+}  // namespace
+
+dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int32_t k,
+                                 int32_t* topk_ids, float* topk_scores, const int32_t* offsets,
+                                 int32_t* sel_sorted, int32_t* sel_rowoff, int32_t* row_len,
+                                 hipStream_t stream) {
+    const size_t lds = (size_t)k * (sizeof(uint64_t) + sizeof(int32_t));
+    topk_clusters_kernel<<<B, kNT, lds, stream>>>(scores, M, k, topk_ids, topk_scores, offsets,
+                                                  sel_sorted, sel_rowoff, row_len);
+    return check_launch("topk_clusters_kernel");
+}
+
+dyna_status launch_shortlist(const int32_t* offsets, const int32_t* perm, int32_t M,
+                             const int32_t* topk_ids, int32_t B, int32_t k, int32_t* sel_sorted,
+                             int32_t* sel_rowoff, int32_t* row_len, int32_t* shortlist_ids,
+                             int32_t cap, hipStream_t stream) {
+    const size_t lds = sizeof(int32_t) * (3 * (size_t)k + 1);
+    shortlist_kernel<<<B, kNT, lds, stream>>>(offsets, perm, M, topk_ids, k, sel_sorted, sel_rowoff,
+                                              row_len, shortlist_ids, cap);
+    return check_launch("shortlist_kernel");
+}
+
+dyna_status launch_plan(const int32_t* offsets, int32_t M, const int32_t* sel_sorted,
+                        const int32_t* sel_rowoff, int32_t B, int32_t k, Plan plan,
+                        hipStream_t stream) {
+    const size_t lds = sizeof(int32_t) * 3 * (size_t)M;
+    plan_kernel<<<1, kPlanThreads, lds, stream>>>(offsets, M, sel_sorted, sel_rowoff, B, k, plan);
+    return check_launch("plan_kernel");
+}
+
+size_t select_ws_bytes(int32_t B, int32_t max_len, int32_t k_t) {
+    const int64_t P = std::max<int64_t>(1, ((int64_t)max_len + kSeg - 1) / kSeg);
+    return (size_t)B * P * ((size_t)k_t * sizeof(uint64_t) + 2 * sizeof(float)) + 512;
+}
+
+int32_t select_max_len() { return kSeg * kNT; }
+
+dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_len,
+                          int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
+                          const int32_t* sel_rowoff, const int32_t* offsets, const int32_t* perm,
+                          int32_t B, int32_t k, int32_t k_t, float temperature,
+                          const float* uniforms, int32_t* out_ids, float* out_logprobs,
+                          int32_t* out_sample, float* out_sample_logprob, void* ws,
+                          hipStream_t stream) {
+    SelectArgs a;
+    a.logits = logits;
+    a.ld = ld;
+    a.row_len = row_len;
+    a.fixed_len = fixed_len;
+    a.sel_sorted = sel_sorted;
+    a.sel_rowoff = sel_rowoff;
+    a.offsets = offsets;
+    a.perm = perm;
+    a.k = k;
+    a.k_t = k_t;
+    a.inv_t = 1.0f / temperature;
+    a.uniforms = uniforms;
+    a.P = (int32_t)std::max<int64_t>(1, ((int64_t)max_len + kSeg - 1) / kSeg);
+    char* p = static_cast<char*>(ws);
+    a.pkeys = reinterpret_cast<uint64_t*>(p);
+    p += (size_t)B * a.P * k_t * sizeof(uint64_t);
+    a.pmax = reinterpret_cast<float*>(p);
+    p += (size_t)B * a.P * sizeof(float);
+    a.psum = reinterpret_cast<float*>(p);
+    a.out_ids = out_ids;
+    a.out_logprobs = out_logprobs;
+    a.out_sample = out_sample;
+    a.out_sample_logprob = out_sample_logprob;
+    select_partial_kernel<<<dim3(a.P, B), kNT, 0, stream>>>(a);
+    if (dyna_status s = check_launch("select_partial_kernel"); s != DYNA_OK) return s;
+    select_final_kernel<<<B, kNT, 0, stream>>>(a);
+    return check_launch("select_final_kernel");
+}
+
+}  // namespace dyna

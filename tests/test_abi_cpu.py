@@ -1,0 +1,147 @@
+"""Host-side checks of the C ABI: no GPU needed (no call reaches a HIP API)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2510_13847_amd import dynahead as D
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dynahead.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dyna_[a-z_]+)\s*\(", text)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = D.lib()
+    declared = header_functions()
+    assert len(declared) >= 14
+    for name in declared:
+        assert hasattr(lib, name), f"{name} declared in dynahead.h but not exported"
+    assert set(declared) == set(D.EXPORTED), "binding and header disagree"
+    assert lib.dyna_abi_version() == 1
+
+
+def test_status_strings():
+    lib = D.lib()
+    for code, name in enumerate(["DYNA_OK", "DYNA_ERR_INVALID_ARG", "DYNA_ERR_CAPACITY",
+                                 "DYNA_ERR_WORKSPACE", "DYNA_ERR_UNSUPPORTED", "DYNA_ERR_HIP",
+                                 "DYNA_ERR_DEVICE_DATA"]):
+        assert lib.dyna_status_string(code).decode() == name
+
+
+def test_set_option_validation():
+    lib = D.lib()
+    assert lib.dyna_set_option(99, 0) == D.ERR_INVALID_ARG
+    assert b"unknown option" in lib.dyna_last_error()
+    assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 7) == D.ERR_INVALID_ARG
+    assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 0) == D.OK
+
+
+def _layout(V=1000, d=64, M=10, cap=None, W=0x1000):
+    cap_arr = (ctypes.c_int32 * (M + 1))(*([0] + [100 * (i + 1) for i in range(M)]))
+    L = D._Layout(V, d, M, D.BF16, W, 0x2000, 0x3000, ctypes.addressof(cap_arr), 100)
+    return L, cap_arr
+
+
+def test_workspace_sizes_are_host_only():
+    lib = D.lib()
+    L, keep = _layout()
+    n1 = lib.dyna_workspace_bytes(ctypes.byref(L), None, 4, 3, 300)
+    n2 = lib.dyna_workspace_bytes(ctypes.byref(L), None, 8, 3, 300)
+    assert 0 < n1 < n2
+    assert lib.dyna_workspace_bytes(None, None, 4, 3, 300) == 0
+    assert lib.dyna_dense_workspace_bytes(0, 4) == 0
+    assert lib.dyna_dense_workspace_bytes(128256, 1) > 128256 * 4
+    assert lib.dyna_layout_workspace_bytes(128256, 1024) >= 128256 * 4
+
+
+def test_shortlist_logits_argument_errors():
+    lib = D.lib()
+    L, keep = _layout()
+    s = lib.dyna_shortlist_logits
+    P = 0x10000
+    # k out of range
+    assert s(ctypes.byref(L), P, D.BF16, 2, 0, P, P, P, P, 300, P, 1 << 30, None) == D.ERR_INVALID_ARG
+    assert s(ctypes.byref(L), P, D.BF16, 2, 11, P, P, P, P, 300, P, 1 << 30, None) == D.ERR_INVALID_ARG
+    # cap below cap_by_k[k]
+    assert s(ctypes.byref(L), P, D.BF16, 2, 3, P, P, P, P, 299, P, 1 << 30, None) == D.ERR_CAPACITY
+    assert b"cap=299" in lib.dyna_last_error()
+    # workspace too small
+    assert s(ctypes.byref(L), P, D.BF16, 2, 3, P, P, P, P, 300, P, 16, None) == D.ERR_WORKSPACE
+    # misaligned h
+    assert s(ctypes.byref(L), P + 2, D.BF16, 2, 3, P, P, P, P, 300, P, 1 << 30, None) == D.ERR_INVALID_ARG
+    # bad dtype
+    assert s(ctypes.byref(L), P, 7, 2, 3, P, P, P, P, 300, P, 1 << 30, None) == D.ERR_INVALID_ARG
+    # B = 0 is a no-op even with NULL buffers
+    assert s(ctypes.byref(L), None, D.BF16, 0, 3, None, None, None, None, 300, None, 0, None) == D.OK
+
+
+def test_layout_struct_checks():
+    lib = D.lib()
+    P = 0x10000
+    for field, value in [("d", 12), ("M", 0), ("M", 2000), ("wdtype", 3), ("max_cluster", 0)]:
+        L, keep = _layout()
+        setattr(L, field, value)
+        assert lib.dyna_shortlist(ctypes.byref(L), P, 1, 1, P, P, P, None, 0, None) != D.OK
+    L, keep = _layout(M=9000, V=100000)
+    assert lib.dyna_shortlist(ctypes.byref(L), P, 1, 1, P, P, P, None, 0, None) == D.ERR_UNSUPPORTED
+
+
+def test_select_and_head_argument_errors():
+    lib = D.lib()
+    L, keep = _layout()
+    P = 0x10000
+    sel = lib.dyna_draft_select
+    # bad mode, k_t out of range, sampling without uniforms, bad temperature
+    base = dict(mode=D.SEL_TOPK, k_t=4, temp=1.0, u=P)
+    def call(mode, k_t, temp, u):
+        return sel(ctypes.byref(L), P, P, P, P, 2, 3, 300, mode, k_t, temp, u, P, P, P, P, P, 1 << 30, None)
+    assert call(0, 4, 1.0, P) == D.ERR_INVALID_ARG
+    assert call(8, 4, 1.0, P) == D.ERR_INVALID_ARG
+    assert call(D.SEL_TOPK, 0, 1.0, P) == D.ERR_INVALID_ARG
+    assert call(D.SEL_TOPK, 65, 1.0, P) == D.ERR_INVALID_ARG
+    assert call(D.SEL_SAMPLE, 1, 1.0, None) == D.ERR_INVALID_ARG
+    assert call(D.SEL_SAMPLE, 1, 0.0, P) == D.ERR_INVALID_ARG
+    assert call(D.SEL_SAMPLE, 1, float("inf"), P) == D.ERR_INVALID_ARG
+    # router/layout mismatch in the fused call
+    R = D._Router(64, 0, 11, D.BF16, 0, P, None, None, None)
+    head = lib.dyna_draft_head
+    st = head(ctypes.byref(R), ctypes.byref(L), P, P, D.BF16, 2, 3, D.SEL_ARGMAX, 1, 1.0, None,
+              P, P, None, None, None, None, 300, P, 1 << 30, None, None, None)
+    assert st == D.ERR_INVALID_ARG and b"differs" in lib.dyna_last_error()
+    R = D._Router(64, 12, 10, D.BF16, 2, P, None, P, None)  # H not a multiple of 8
+    st = head(ctypes.byref(R), ctypes.byref(L), P, P, D.BF16, 2, 3, D.SEL_ARGMAX, 1, 1.0, None,
+              P, P, None, None, None, None, 300, P, 1 << 30, None, None, None)
+    assert st == D.ERR_INVALID_ARG
+    R = D._Router(64, 0, 10, D.BF16, 9, P, None, None, None)  # bad activation
+    assert lib.dyna_route(ctypes.byref(R), P, D.BF16, 2, 3, P, None, None, P, 1 << 30, None) == D.ERR_INVALID_ARG
+
+
+def test_build_layout_argument_errors():
+    lib = D.lib()
+    P = 0x10000
+    cap = (ctypes.c_int32 * 11)()
+    b = lib.dyna_build_layout
+    assert b(None, 100, 10, P, D.BF16, 64, P + 4096, P, P, cap, None, P, 1 << 30, None) == D.ERR_INVALID_ARG
+    assert b(P, 100, 101, P, D.BF16, 64, P + 4096, P, P, cap, None, P, 1 << 30, None) == D.ERR_INVALID_ARG
+    assert b(P, 100, 10, P, D.BF16, 60, P + 4096, P, P, cap, None, P, 1 << 30, None) == D.ERR_INVALID_ARG
+    assert b(P, 100, 10, P, D.BF16, 64, P, P, P, cap, None, P, 1 << 30, None) == D.ERR_INVALID_ARG
+    assert b(P, 100, 10, P, D.BF16, 64, P + 4096, P, P, cap, None, P, 8, None) == D.ERR_WORKSPACE
+
+
+def test_dense_head_argument_errors():
+    lib = D.lib()
+    P = 0x10000
+    d = lib.dyna_dense_head
+    assert d(P, D.BF16, 0, 64, P, D.BF16, 1, D.SEL_ARGMAX, 1, 1.0, None, P, None, None, None, None,
+             P, 1 << 30, None) == D.ERR_INVALID_ARG
+    assert d(P, D.BF16, 600000, 64, P, D.BF16, 1, D.SEL_ARGMAX, 1, 1.0, None, P, None, None, None,
+             None, P, 1 << 30, None) == D.ERR_UNSUPPORTED
+    assert d(P, D.BF16, 1000, 64, P, D.BF16, 1, D.SEL_ARGMAX, 1, 1.0, None, P, None, None, None,
+             None, P, 4, None) == D.ERR_WORKSPACE

@@ -1,0 +1,92 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times (one dyna_draft_head call per step).  Inputs are generated on
+the device; the oracle recomputes sampled context rows from host copies of the
+inputs (router weights, the rows' features and the LM-head rows they need)."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import dynaspec_oracle as O
+from tests import parity as PC
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def mode_of(w, D):
+    m = 0
+    if "argmax" in w.modes:
+        m |= D.SEL_ARGMAX
+    if "topk" in w.modes:
+        m |= D.SEL_TOPK
+    if "sample" in w.modes:
+        m |= D.SEL_SAMPLE
+    return m
+
+
+@pytest.mark.parametrize("name", W.WORKLOAD_ORDER)
+def test_fullsize_workload(name):
+    from paper_2510_13847_amd import dynahead as D
+    w = W.WORKLOADS[name]
+    print(f"[fullsize] {name}: V={w.V} d={w.d} M={w.M} B={w.B} k={w.k}", flush=True)
+    cluster_of = W.partition(w)
+    W_lm = W.lm_head(w, DEV)
+    W1, W2 = W.router_weights(w, DEV)
+    h = W.contexts(w, DEV)
+    u = W.uniforms(w, DEV)
+    L = D.build_layout(torch.from_numpy(cluster_of).to(DEV), W_lm, w.M)
+    R = D.Router(W1, W2, act=w.act)
+
+    # layout: exact
+    sizes, offsets, perm, cap = O.cluster_layout(cluster_of, w.M)
+    assert L.perm.cpu().numpy().tolist() == perm.tolist()
+    assert L.offsets.cpu().numpy().tolist() == offsets.tolist()
+    assert L.cap_by_k.tolist() == cap.tolist()
+    perm_d = L.perm.long()
+    for r0 in range(0, w.V, 16384):
+        r1 = min(w.V, r0 + 16384)
+        assert torch.equal(L.W_perm[r0:r1], W_lm.index_select(0, perm_d[r0:r1])), "W_perm rows"
+
+    mode = mode_of(w, D)
+    head = D.DraftHead(R, L, w.B, w.k, mode, w.k_t if mode & D.SEL_TOPK else 1, keep_logits=True)
+    head(h, h, u)
+    torch.cuda.synchronize()
+
+    rng = np.random.default_rng(0)
+    rows = list(range(w.B)) if w.B <= 16 else sorted({0, w.B - 1, *rng.choice(w.B, 6, replace=False).tolist()})
+    h_np = W.host_array(h[rows])
+    W1_np = W.host_array(W1)
+    W2_np = None if W2 is None else W.host_array(W2)
+    ref_scores = O.router_scores(h_np, W1_np, W2_np, act=w.act)
+    clusters = head.clusters.cpu().numpy()
+    logits = head.logits.cpu().numpy().astype(np.float64)
+    u_np = u.cpu().numpy().astype(np.float64)
+    tol = PC.TOL[w.dtype]
+    strict = 0
+    max_err = 0.0
+    for i, b in enumerate(rows):
+        eq, ok = PC.cluster_check(clusters[b], ref_scores[i], w.k)
+        assert ok, f"row {b}: clusters"
+        strict += int(not eq)
+        sel, rowoff, lrows, vids = O.shortlist(clusters[b], offsets, perm)
+        n = len(vids)
+        Wrows = W.host_array(W_lm.index_select(0, torch.from_numpy(vids).to(DEV)))
+        z_ref = O.shortlist_logits(h_np[i], Wrows, np.arange(n))
+        max_err = max(max_err, PC.assert_close(logits[b, :n], z_ref, tol, f"logits row {b}"))
+        z_gpu = logits[b, :n]
+        if head.ids is not None:
+            kt = head.ids.shape[1]
+            got = head.ids[b].cpu().numpy()
+            r = O.draft_select(z_gpu, vids, min(kt, n))
+            assert got[:min(kt, n)].tolist() == r["ids"].tolist()
+            eq, ok = PC.tokens_check(got, z_ref, vids, kt)
+            assert ok, f"row {b}: tokens"
+        if head.sample is not None:
+            eq, ok = PC.sample_check(int(head.sample[b]), z_gpu, vids, u_np[b])
+            assert ok, f"row {b}: sample"
+    print(f"[fullsize] {name}: rows checked {len(rows)}, strict cluster mismatches {strict}, "
+          f"max |logit err| {max_err:.3e}", flush=True)
+    del head, L, W_lm
+    torch.cuda.empty_cache()

@@ -1,0 +1,405 @@
+"""GPU parity of libdynahead against the CPU oracle (stage-wise), small sizes.
+
+Sizes here run in seconds on the oracle but span several 16-row tiles, ragged
+cluster tails, a ragged reduction dimension (d = 200 is not a multiple of the
+32-wide MFMA step nor of the 512-wide GEMV block), both logits kernels and
+both router kernels.  Full-size workloads are in test_gpu_fullsize.py.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import dynaspec_oracle as O
+from tests import parity as PC
+
+pytestmark = pytest.mark.gpu
+
+D = None
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    global D
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2510_13847_amd import dynahead
+    D = dynahead
+    D.lib()
+    yield
+    D.set_option(D.OPT_LOGITS_PATH, 0)
+    D.set_option(D.OPT_ROUTER_PATH, 0)
+
+
+DEV = "cuda"
+BASE = W.WORKLOADS["llama3_8b_chain"]
+
+
+def case(name, **kw):
+    kw.setdefault("modes", ("topk", "sample"))
+    kw.setdefault("k_t", 6)
+    return W.scaled(BASE, name=name, **kw)
+
+
+CASES = [
+    W.WORKLOADS["tiny_fp32"],
+    case("ragged_b1", V=3001, d=200, M=37, H=24, k=5, B=1),
+    case("ragged_b3", V=3001, d=200, M=37, H=24, k=5, B=3),
+    case("ragged_b7", V=3001, d=200, M=37, H=24, k=5, B=7),
+    case("ragged_b37", V=3001, d=200, M=37, H=24, k=5, B=37),
+    case("f32_b5", V=2000, d=136, M=20, H=16, k=4, B=5, dtype="f32"),
+    case("linear_b20", V=2500, d=264, M=30, H=0, act="none", k=4, B=20),
+    case("relu_b2", V=1500, d=128, M=16, H=32, act="relu", k=3, B=2),
+    case("zipf_b9", V=6000, d=96, M=12, sizes=("zipf", 1.1, 1500), H=16, k=3, B=9),
+    case("wide_k_b4", V=4096, d=512, M=64, H=64, k=64, B=4),  # k = M: shortlist = V
+]
+
+
+class Problem:
+    def __init__(self, w, gen_device="cpu"):
+        self.w = w
+        self.cluster_of = W.partition(w)
+        self.W_lm = W.lm_head(w, gen_device)
+        self.W1, self.W2 = W.router_weights(w, gen_device)
+        self.h = W.contexts(w, gen_device)
+        self.u = W.uniforms(w, gen_device)
+        self.hd = self.h.to(DEV)
+        self.ud = self.u.to(DEV)
+        self.L = D.build_layout(torch.from_numpy(self.cluster_of).to(DEV), self.W_lm.to(DEV), w.M)
+        self.R = D.Router(self.W1.to(DEV), None if self.W2 is None else self.W2.to(DEV), act=w.act)
+        # host copies for the oracle
+        self.h_np = W.host_array(self.h)
+        self.W_np = W.host_array(self.W_lm)
+        self.W1_np = W.host_array(self.W1)
+        self.W2_np = None if self.W2 is None else W.host_array(self.W2)
+        self.u_np = self.u.numpy().astype(np.float64)
+        self.sizes, self.offsets, self.perm, self.cap = O.cluster_layout(self.cluster_of, w.M)
+        self.tol = PC.TOL[w.dtype]
+
+    def oracle_scores(self):
+        return O.router_scores(self.h_np, self.W1_np, self.W2_np, act=self.w.act)
+
+
+def _ids(tensor):
+    return tensor.cpu().numpy().astype(np.int64)
+
+
+# ---------------------------------------------------------------- layout
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_layout_exact(w):
+    p = Problem(w)
+    assert _ids(p.L.perm).tolist() == p.perm.tolist()
+    assert _ids(p.L.offsets).tolist() == p.offsets.tolist()
+    assert p.L.cap_by_k.tolist() == p.cap.tolist()
+    assert p.L.max_cluster == int(p.sizes.max())
+    got = W.host_array(p.L.W_perm.cpu())
+    np.testing.assert_array_equal(got, p.W_np[p.perm])
+
+
+def test_layout_with_empty_clusters_and_bad_ids():
+    rng = np.random.default_rng(5)
+    V, M, d = 700, 40, 64
+    cluster_of = rng.integers(0, M, size=V).astype(np.int32)
+    cluster_of[np.isin(cluster_of, [3, 17, 39])] = 0  # three empty clusters, one big
+    Wl = torch.randn(V, d).to(torch.bfloat16)
+    L = D.build_layout(torch.from_numpy(cluster_of).to(DEV), Wl.to(DEV), M)
+    sizes, offsets, perm, cap = O.cluster_layout(cluster_of, M)
+    assert _ids(L.offsets).tolist() == offsets.tolist() and _ids(L.perm).tolist() == perm.tolist()
+    assert L.cap_by_k.tolist() == cap.tolist()
+    bad = cluster_of.copy()
+    bad[123] = M  # out of range: flagged on the device, reported on the host
+    with pytest.raises(D.DynaError) as e:
+        D.build_layout(torch.from_numpy(bad).to(DEV), Wl.to(DEV), M)
+    assert e.value.status == D.ERR_DEVICE_DATA
+
+
+# ---------------------------------------------------------------- router
+@pytest.mark.parametrize("path", [0, 1, 2])
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_route_parity(w, path):
+    if path == 2 and w.dtype == "f32":
+        pytest.skip("MFMA router path needs bf16 weights")
+    p = Problem(w)
+    D.set_option(D.OPT_ROUTER_PATH, path)
+    try:
+        ids, sc, scores = D.route(p.R, p.hd, w.k, want_scores=True)
+        torch.cuda.synchronize()
+    finally:
+        D.set_option(D.OPT_ROUTER_PATH, 0)
+    ref = p.oracle_scores()
+    g_scores = scores.cpu().numpy().astype(np.float64)
+    PC.assert_close(g_scores, ref, PC.SCORE_TOL, "router scores")
+    g_ids = _ids(ids)
+    # the top-k kernel is exact on its own fp32 scores (same ordering rule)
+    ids_own, vals_own = O.topk_clusters(g_scores, w.k)
+    np.testing.assert_array_equal(g_ids, ids_own)
+    np.testing.assert_array_equal(sc.cpu().numpy().astype(np.float64), vals_own)
+    strict = 0
+    for b in range(w.B):
+        eq, ok = PC.cluster_check(g_ids[b], ref[b], w.k)
+        assert ok, f"row {b}: clusters {g_ids[b]} not a valid top-{w.k}"
+        strict += int(not eq)
+    assert strict <= max(1, w.B // 4)
+
+
+def test_route_nan_and_ties():
+    # NaN features make every score NaN: all count as -inf, ties go to lower ids
+    M, d_r = 50, 64
+    W1 = torch.randn(M, d_r).to(torch.bfloat16).to(DEV)
+    x = torch.full((3, d_r), float("nan")).to(torch.bfloat16).to(DEV)
+    R = D.Router(W1, None, act="none")
+    ids, sc, _ = D.route(R, x, 7)
+    assert _ids(ids).tolist() == [list(range(7))] * 3
+    # exact ties: zero weights give all-zero scores; +0 and -0 must compare equal
+    W0 = torch.zeros(M, d_r).to(torch.bfloat16).to(DEV)
+    xz = torch.randn(2, d_r).to(torch.bfloat16).to(DEV)
+    ids, _, _ = D.route(D.Router(W0, None, act="none"), xz, 5)
+    assert _ids(ids).tolist() == [list(range(5))] * 2
+
+
+# ---------------------------------------------------------------- shortlist
+@pytest.mark.parametrize("w", CASES[:5], ids=lambda w: w.name)
+def test_shortlist_exact_union(w):
+    p = Problem(w)
+    rng = np.random.default_rng(11)
+    B, k, M = 6, w.k, w.M
+    topk = np.stack([rng.choice(M, size=k, replace=False) for _ in range(B)]).astype(np.int32)
+    sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
+    sel, rowoff, row_len, sl = _ids(sel), _ids(rowoff), _ids(row_len), _ids(sl)
+    for b in range(B):
+        s_o, r_o, rows_o, vids_o = O.shortlist(topk[b], p.offsets, p.perm)
+        assert sel[b].tolist() == s_o.tolist()
+        assert rowoff[b].tolist() == r_o.tolist()
+        assert row_len[b] == len(vids_o)
+        assert sl[b, :row_len[b]].tolist() == vids_o.tolist()
+        assert np.all(sl[b, row_len[b]:] == -1)  # untouched past row_len
+
+
+def test_shortlist_ignores_repeats_and_out_of_range():
+    w = CASES[1]
+    p = Problem(w)
+    topk = np.array([[3, 3, 7, -1, 36], [40, 0, 0, 0, 1]], dtype=np.int32)
+    sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
+    sel, rowoff, row_len = _ids(sel), _ids(rowoff), _ids(row_len)
+    assert sel[0].tolist() == [3, 7, 36, -1, -1]
+    assert sel[1].tolist() == [0, 1, -1, -1, -1]
+    for b, valid in enumerate([[3, 7, 36], [0, 1]]):
+        assert row_len[b] == sum(p.sizes[m] for m in valid)
+        assert rowoff[b, -1] == row_len[b]
+
+
+# ---------------------------------------------------------------- logits
+def _random_selection(p, B, k, seed):
+    rng = np.random.default_rng(seed)
+    topk = np.stack([rng.choice(p.w.M, size=k, replace=False) for _ in range(B)]).astype(np.int32)
+    # make some clusters popular across the batch, like a biased router
+    if B > 2:
+        topk[: B // 2, 0] = topk[0, 0]
+        for b in range(B // 2):
+            row = topk[b]
+            if len(set(row.tolist())) < k:
+                spare = [m for m in range(p.w.M) if m not in set(row.tolist())]
+                row[1:] = rng.choice(spare, size=k - 1, replace=False)
+    return topk
+
+
+@pytest.mark.parametrize("path", [1, 2])
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_logits_parity(w, path):
+    if path == 2 and w.dtype == "f32":
+        pytest.skip("MFMA logits path needs bf16 weights")
+    p = Problem(w)
+    topk = _random_selection(p, w.B, w.k, 3)
+    sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
+    D.set_option(D.OPT_LOGITS_PATH, path)
+    try:
+        logits = D.shortlist_logits(p.L, p.hd, sel, rowoff, row_len)
+        torch.cuda.synchronize()
+    finally:
+        D.set_option(D.OPT_LOGITS_PATH, 0)
+    lg = logits.cpu().numpy().astype(np.float64)
+    row_len, sl = _ids(row_len), _ids(sl)
+    for b in range(w.B):
+        n = row_len[b]
+        ref = O.shortlist_logits(p.h_np[b], p.W_np, sl[b, :n])
+        PC.assert_close(lg[b, :n], ref, p.tol, f"logits row {b}")
+        assert np.all(np.isnan(lg[b, n:])), "slots past row_len must stay untouched"
+
+
+# ---------------------------------------------------------------- select
+def _select_problem(seed, B=5, with_ties=True):
+    w = CASES[2]
+    p = Problem(w)
+    topk = _random_selection(p, B, w.k, seed)
+    sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
+    cap = p.L.cap(w.k)
+    rng = np.random.default_rng(seed)
+    z = (rng.standard_normal((B, cap)) * 3).astype(np.float32)
+    if with_ties:
+        z[:, 5:40] = np.round(z[:, 5:40])  # many exactly equal logits
+        z[0, :] = 1.25                      # a row of all-equal logits
+    return p, sel, rowoff, row_len, sl, torch.from_numpy(z).to(DEV), z
+
+
+@pytest.mark.parametrize("k_t", [1, 4, 13, 64])
+@pytest.mark.parametrize("temperature", [1.0, 0.7])
+def test_select_exact_on_same_logits(k_t, temperature):
+    p, sel, rowoff, row_len, sl, zd, z = _select_problem(7 + k_t)
+    B = z.shape[0]
+    u = torch.rand(B, generator=torch.Generator().manual_seed(k_t)).to(DEV)
+    out = D.draft_select(p.L, zd, sel, rowoff, row_len, mode=D.SEL_TOPK | D.SEL_SAMPLE, k_t=k_t,
+                         temperature=temperature, uniforms=u)
+    torch.cuda.synchronize()
+    row_len, sl = _ids(row_len), _ids(sl)
+    ids, lps = _ids(out["ids"]), out["logprobs"].cpu().numpy()
+    smp, slp = _ids(out["sample"]), out["sample_logprob"].cpu().numpy()
+    un = u.cpu().numpy().astype(np.float64)
+    for b in range(B):
+        n = row_len[b]
+        zb = z[b, :n].astype(np.float64)
+        r = O.draft_select(zb, sl[b, :n], min(k_t, n), temperature, un[b])
+        m = min(k_t, n)
+        assert ids[b, :m].tolist() == r["ids"].tolist(), f"row {b}"
+        assert np.all(ids[b, m:] == -1)
+        PC.assert_close(lps[b, :m], r["logprobs"], PC.LOGPROB_TOL, "logprobs")
+        eq, ok = PC.sample_check(smp[b], zb, sl[b, :n], un[b], temperature)
+        assert ok, f"row {b}: sample {smp[b]}"
+        j = int(np.nonzero(sl[b, :n] == smp[b])[0][0])
+        PC.assert_close([slp[b]], [O.log_softmax(zb, temperature)[j]], PC.LOGPROB_TOL, "sample lp")
+
+
+def test_sampling_grid_matches_probabilities():
+    # a sweep of u over [0, 1) must hit every shortlist slot in proportion to q_S
+    p, sel, rowoff, row_len, sl, zd, z = _select_problem(3, B=1, with_ties=False)
+    N = 4096
+    n = int(_ids(row_len)[0])
+    zsmall = zd.clone()
+    zsmall[0, :n] = torch.linspace(-2.0, 2.0, n, device=DEV)
+    sel_r = sel.repeat(N, 1)
+    rowoff_r = rowoff.repeat(N, 1)
+    rl_r = row_len.repeat(N)
+    zr = zsmall.repeat(N, 1)
+    u = (torch.arange(N, dtype=torch.float32, device=DEV) + 0.5) / N
+    out = D.draft_select(p.L, zr, sel_r, rowoff_r, rl_r, mode=D.SEL_SAMPLE, uniforms=u)
+    smp = _ids(out["sample"])
+    sl0 = _ids(sl)[0, :n]
+    zb = zsmall[0, :n].cpu().numpy().astype(np.float64)
+    q = np.exp(O.log_softmax(zb))
+    counts = np.array([(smp == v).sum() for v in sl0])
+    assert counts.sum() == N
+    assert np.all(np.abs(counts - q * N) <= 1.0 + 1e-6 * N)
+
+
+# ---------------------------------------------------------------- whole head
+def _check_head(p, head, modes_ids=True):
+    w = p.w
+    ref_scores = p.oracle_scores()
+    clusters = _ids(head.clusters)
+    logits = head.logits.cpu().numpy().astype(np.float64)
+    for b in range(w.B):
+        eq, ok = PC.cluster_check(clusters[b], ref_scores[b], w.k)
+        assert ok, f"row {b}: clusters"
+        sel, rowoff, rows, vids = O.shortlist(clusters[b], p.offsets, p.perm)
+        n = len(vids)
+        z_ref = O.shortlist_logits(p.h_np[b], p.W_np, vids)
+        PC.assert_close(logits[b, :n], z_ref, p.tol, f"head logits row {b}")
+        z_gpu = logits[b, :n]
+        if head.ids is not None:
+            kt = head.ids.shape[1]
+            got = _ids(head.ids)[b]
+            r = O.draft_select(z_gpu, vids, min(kt, n))
+            assert got[:min(kt, n)].tolist() == r["ids"].tolist()     # exact on own logits
+            eq, ok = PC.tokens_check(got, z_ref, vids, kt)             # vs oracle logits
+            assert ok
+        if head.sample is not None:
+            eq, ok = PC.sample_check(_ids(head.sample)[b], z_gpu, vids, p.u_np[b], head.temperature)
+            assert ok
+
+
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_draft_head_chain(w):
+    p = Problem(w)
+    mode = D.SEL_TOPK | D.SEL_SAMPLE
+    head = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode, k_t=w.k_t, uniforms=p.ud)
+    torch.cuda.synchronize()
+    _check_head(p, head)
+    # the fused call equals the step-by-step calls exactly
+    ids, _, _ = D.route(p.R, p.hd, w.k)
+    assert torch.equal(ids, head.clusters)
+    sel, rowoff, row_len, _ = D.shortlist(p.L, ids, with_ids=False)
+    logits = D.shortlist_logits(p.L, p.hd, sel, rowoff, row_len)
+    mask = ~torch.isnan(logits)
+    assert torch.equal(logits[mask], head.logits[mask])
+    out = D.draft_select(p.L, logits, sel, rowoff, row_len, mode=mode, k_t=w.k_t, uniforms=p.ud)
+    assert torch.equal(out["ids"], head.ids) and torch.equal(out["sample"], head.sample)
+
+
+def test_k_equals_M_is_the_dense_head():
+    w = CASES[-1]  # k = M = 64: the shortlist is the whole vocabulary
+    p = Problem(w)
+    mode = D.SEL_TOPK
+    head = D.draft_head(p.R, p.L, p.hd, p.hd, w.M, mode=mode, k_t=8)
+    dense = D.DenseHead(p.W_lm.to(DEV), w.V, w.B, mode, 8, keep_logits=True)(p.hd)
+    torch.cuda.synchronize()
+    assert torch.equal(head.ids, dense.ids)
+    PC.assert_close(head.logprobs.cpu().numpy(), dense.logprobs.cpu().numpy(), PC.LOGPROB_TOL, "lp")
+    # and the dense head itself against the oracle
+    for b in range(w.B):
+        r = O.dense_head(p.h_np[b:b + 1], p.W_np, k_t=8)[0]
+        PC.assert_close(dense.logits[b].cpu().numpy(), r["logits"], p.tol, "dense logits")
+        eq, ok = PC.tokens_check(_ids(dense.ids)[b], r["logits"], np.arange(w.V), 8)
+        assert ok
+
+
+@pytest.mark.parametrize("B", [1, 6])
+def test_static_head_prefix(B):
+    w = CASES[4]
+    p = Problem(w)
+    n = 777
+    hd = p.hd[:B].contiguous()
+    st = D.DenseHead(p.W_lm.to(DEV), n, B, D.SEL_TOPK | D.SEL_SAMPLE, 5, keep_logits=True)
+    u = p.ud[:B].contiguous()
+    st(hd, u)
+    torch.cuda.synchronize()
+    for b in range(B):
+        r = O.dense_head(p.h_np[b:b + 1], p.W_np, k_t=5, n_rows=n)[0]
+        PC.assert_close(st.logits[b].cpu().numpy(), r["logits"], p.tol, "static logits")
+        eq, ok = PC.tokens_check(_ids(st.ids)[b], r["logits"], np.arange(n), 5)
+        assert ok
+        zg = st.logits[b].cpu().numpy().astype(np.float64)
+        eq, ok = PC.sample_check(_ids(st.sample)[b], zg, np.arange(n), p.u_np[b])
+        assert ok
+
+
+def test_determinism_and_stream_overlap():
+    w = CASES[4]
+    p = Problem(w)
+    mode = D.SEL_TOPK | D.SEL_SAMPLE
+    a = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode, k_t=w.k_t, uniforms=p.ud)
+    outs = [(a.ids.clone(), a.logits.clone(), a.sample.clone())]
+    side = torch.cuda.Stream()
+    for route_stream in [None, side, None, side]:
+        a(p.hd, p.hd, p.ud, route_stream=route_stream)
+        torch.cuda.synchronize()
+        outs.append((a.ids.clone(), a.logits.clone(), a.sample.clone()))
+    for o in outs[1:]:
+        assert torch.equal(o[0], outs[0][0]) and torch.equal(o[2], outs[0][2])
+        assert torch.equal(torch.nan_to_num(o[1], nan=7.0), torch.nan_to_num(outs[0][1], nan=7.0))
+
+
+def test_empty_batch_is_a_no_op():
+    w = CASES[1]
+    p = Problem(w)
+    x = p.hd[:0]
+    ids, _, _ = D.route(p.R, x, w.k)
+    assert ids.shape == (0, w.k)
+
+
+def test_tiny_vocab_every_k():
+    # brute-force scale: V = 64, M = 8, every k, B = 3
+    for k in range(1, 9):
+        w = case(f"tiny_k{k}", V=64, d=32, M=8, H=16, k=k, B=3, k_t=4)
+        p = Problem(w)
+        head = D.draft_head(p.R, p.L, p.hd, p.hd, k, mode=D.SEL_TOPK | D.SEL_SAMPLE, k_t=4,
+                            uniforms=p.ud)
+        torch.cuda.synchronize()
+        _check_head(p, head)
