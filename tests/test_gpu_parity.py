@@ -189,17 +189,19 @@ def test_shortlist_ignores_repeats_and_out_of_range():
 
 # ---------------------------------------------------------------- logits
 def _random_selection(p, B, k, seed):
+    """Random distinct clusters per context; half the batch shares one cluster,
+    like a router biased toward a popular cluster."""
     rng = np.random.default_rng(seed)
-    topk = np.stack([rng.choice(p.w.M, size=k, replace=False) for _ in range(B)]).astype(np.int32)
-    # make some clusters popular across the batch, like a biased router
-    if B > 2:
-        topk[: B // 2, 0] = topk[0, 0]
-        for b in range(B // 2):
-            row = topk[b]
-            if len(set(row.tolist())) < k:
-                spare = [m for m in range(p.w.M) if m not in set(row.tolist())]
-                row[1:] = rng.choice(spare, size=k - 1, replace=False)
-    return topk
+    M = p.w.M
+    common = int(rng.integers(M))
+    others = np.array([m for m in range(M) if m != common])
+    rows = []
+    for b in range(B):
+        if B > 2 and b < B // 2:
+            rows.append([common] + rng.choice(others, size=k - 1, replace=False).tolist())
+        else:
+            rows.append(rng.choice(M, size=k, replace=False).tolist())
+    return np.array(rows, dtype=np.int32)
 
 
 @pytest.mark.parametrize("path", [1, 2])
