@@ -21,6 +21,7 @@ thread_local char g_last_error[512] = "";
 std::atomic<int> g_logits_path{0};
 std::atomic<int> g_router_path{0};
 std::atomic<int> g_kernel_timing{0};
+std::atomic<int> g_gemv_rows{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -79,6 +80,7 @@ static dyna_status timed_rowdot(const RowdotArgs& a, int path, hipStream_t s) {
     return DYNA_OK;
 }
 int option_router_path() { return g_router_path.load(); }
+int option_gemv_rows() { return g_gemv_rows.load(); }
 
 // ------------------------------------------------------------------ workspace
 // One carving serves every hot entry point, so a single workspace can back a
@@ -92,6 +94,7 @@ struct Carve {
     int32_t* sel_rowoff = nullptr;// [B, k + 1]
     int32_t* row_len = nullptr;   // [B]
     float* logits = nullptr;      // [B, cap]
+    int32_t* slot_vid = nullptr;  // [B, cap]
     Plan plan{};
     void* select_ws = nullptr;
     size_t bytes = 0;
@@ -99,6 +102,15 @@ struct Carve {
 
 static int64_t max_chunks_for(const dyna_layout* L) {
     return ((int64_t)L->V + kTileRows - 1) / kTileRows + L->M;
+}
+
+// Chunks a step can produce: the union of the selected slabs holds at most
+// min(V, B * cap_by_k[k]) rows in at most min(M, B * k) clusters, and each
+// cluster adds at most one partial chunk.
+static int32_t chunk_bound(const dyna_layout* L, int32_t B, int32_t k) {
+    const int64_t rows = std::min<int64_t>(L->V, (int64_t)B * L->cap_by_k[k]);
+    const int64_t clusters = std::min<int64_t>(L->M, (int64_t)B * k);
+    return (int32_t)std::min<int64_t>(max_chunks_for(L), rows / kTileRows + clusters + 1);
 }
 
 static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_t k, int32_t cap,
@@ -121,6 +133,7 @@ static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_
     c.sel_rowoff = static_cast<int32_t*>(take(sizeof(int32_t) * Bl * (k + 1)));
     c.row_len = static_cast<int32_t*>(take(sizeof(int32_t) * Bl));
     c.logits = static_cast<float*>(take(sizeof(float) * Bl * cap));
+    c.slot_vid = static_cast<int32_t*>(take(sizeof(int32_t) * Bl * cap));
     if (L) {
         c.plan.max_chunks = (int32_t)max_chunks_for(L);
         c.plan.max_entries = (int32_t)(Bl * k);
@@ -263,7 +276,7 @@ static dyna_status run_logits(const dyna_layout* L, const void* h, int32_t hdtyp
     a.act = DYNA_ACT_NONE;
     a.n_rows = 0;
     a.plan = plan;
-    a.max_chunks_bound = plan.max_chunks;
+    a.max_chunks_bound = chunk_bound(L, B, k);
     return timed_rowdot(a, option_logits_path(), s);
 }
 
@@ -301,6 +314,11 @@ DYNA_API const char* dyna_status_string(dyna_status s) {
 DYNA_API const char* dyna_last_error(void) { return g_last_error; }
 
 DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
+    if (option == DYNA_OPT_GEMV_ROWS) {
+        REQUIRE(value == 0 || value == 1 || value == 2 || value == 4, "GEMV rows %d not in {0,1,2,4}", value);
+        g_gemv_rows.store(value);
+        return DYNA_OK;
+    }
     REQUIRE(value >= 0 && value <= 2, "option value %d outside [0, 2]", value);
     if (option == DYNA_OPT_LOGITS_PATH) g_logits_path.store(value);
     else if (option == DYNA_OPT_ROUTER_PATH) g_router_path.store(value);
@@ -385,7 +403,7 @@ DYNA_API dyna_status dyna_route(const dyna_router* r, const void* x, int32_t xdt
     float* sc = scores ? scores : c.scores;
     TRY(run_router(r, x, xdtype, B, sc, c.hidden, stream));
     return launch_topk_clusters(sc, B, r->M, k, topk_ids, topk_scores, nullptr, nullptr, nullptr,
-                                nullptr, stream);
+                                nullptr, nullptr, stream);
 }
 
 DYNA_API dyna_status dyna_shortlist(const dyna_layout* L, const int32_t* topk_ids, int32_t B, int32_t k,
@@ -481,8 +499,8 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     int32_t* clusters = out_clusters ? out_clusters : c.topk_ids;
     TRY(run_router(r, x, adtype, B, c.scores, c.hidden, rs));
     TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, L->offsets, c.sel_sorted,
-                             c.sel_rowoff, c.row_len, rs));
-    TRY(launch_plan(L->offsets, L->M, c.sel_sorted, c.sel_rowoff, B, k, c.plan, rs));
+                             c.sel_rowoff, c.row_len, &c.plan, rs));
+    if (B > 1) TRY(launch_plan(L->offsets, L->M, c.sel_sorted, c.sel_rowoff, B, k, c.plan, rs));
     if (split) {
         hipEvent_t join = lazy_event(g_ev_join);
         if (!join || hipEventRecord(join, rs) != hipSuccess || hipStreamWaitEvent(stream, join, 0) != hipSuccess)
@@ -501,14 +519,16 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     a.ld = cap;
     a.act = DYNA_ACT_NONE;
     a.plan = c.plan;
-    a.max_chunks_bound = c.plan.max_chunks;
+    a.max_chunks_bound = chunk_bound(L, B, k);
+    a.perm = L->perm;
+    a.vid_out = c.slot_vid;
     TRY(timed_rowdot(a, option_logits_path(), stream));
     const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
     const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     return launch_select(logits, cap, c.row_len, 0, cap, c.sel_sorted, c.sel_rowoff, L->offsets, L->perm, B,
                          k, k_t, temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
-                         want_sample ? out_sample_logprob : nullptr, c.select_ws, stream);
+                         want_sample ? out_sample_logprob : nullptr, c.select_ws, stream, c.slot_vid);
 }
 
 // ------------------------------------------------------------------ baselines

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "dyna_internal.h"
 
 namespace dyna {
@@ -77,32 +79,75 @@ __device__ __forceinline__ float key_val(uint64_t key) {
 }
 
 // ---------------------------------------------------------------- wave ops
+// Cross-lane steps use DPP row shifts and row broadcasts (ALU latency)
+// instead of LDS permutes.  Source lanes outside a row read the identity.
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
-// Sum over the wave; every lane gets the same value (fixed butterfly order).
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, kWave);
-    return x;
+template <int CTRL, int ROW_MASK = 0xf, int BANK_MASK = 0xf>
+__device__ __forceinline__ uint32_t dpp(uint32_t identity, uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)identity, (int)x, CTRL, ROW_MASK, BANK_MASK, true);
 }
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        uint64_t y = __shfl_xor(x, off, kWave);
-        x = y > x ? y : x;
-    }
+// Inclusive scan over the 64 lanes: Hillis-Steele inside each 16-lane row,
+// then the row totals are carried across rows with two row broadcasts.
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_scan_dpp(T x, Op op, uint32_t identity) {
+    auto step = [&](auto ctrl_tag, auto rmask_tag) {
+        constexpr int CTRL = decltype(ctrl_tag)::value;
+        constexpr int RM = decltype(rmask_tag)::value;
+        T y;
+        if constexpr (sizeof(T) == 4) {
+            y = __builtin_bit_cast(T, dpp<CTRL, RM>(identity, __builtin_bit_cast(uint32_t, x)));
+        }
+        x = op(x, y);
+    };
+    using I = std::integral_constant<int, 0>;
+    step(std::integral_constant<int, kRowShr1>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr2>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr4>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr8>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowBcast15>{}, std::integral_constant<int, 0xa>{});
+    step(std::integral_constant<int, kRowBcast31>{}, std::integral_constant<int, 0xc>{});
+    (void)sizeof(I);
     return x;
 }
 
 __device__ __forceinline__ int wave_inclusive_scan(int x) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        int y = __shfl_up(x, off, kWave);
-        if (lane >= off) x += y;
-    }
-    return x;
+    return wave_scan_dpp<int>(x, [](int a, int b) { return a + b; }, 0u);
+}
+__device__ __forceinline__ float wave_inclusive_scan_f32(float x) {
+    return wave_scan_dpp<float>(x, [](float a, float b) { return a + b; }, 0u);
+}
+__device__ __forceinline__ float readlane_f32(float x, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+
+// Sum over the wave; every lane gets the same value (fixed order).
+__device__ __forceinline__ float wave_sum(float x) {
+    return readlane_f32(wave_inclusive_scan_f32(x), kWave - 1);
+}
+
+// Largest 64-bit value over the wave, on every lane.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+    auto step = [&](auto ctrl_tag, auto rmask_tag) {
+        constexpr int CTRL = decltype(ctrl_tag)::value;
+        constexpr int RM = decltype(rmask_tag)::value;
+        const uint32_t lo = dpp<CTRL, RM>(0u, (uint32_t)x);
+        const uint32_t hi = dpp<CTRL, RM>(0u, (uint32_t)(x >> 32));
+        const uint64_t y = ((uint64_t)hi << 32) | lo;
+        x = y > x ? y : x;
+    };
+    step(std::integral_constant<int, kRowShr1>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr2>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr4>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr8>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowBcast15>{}, std::integral_constant<int, 0xa>{});
+    step(std::integral_constant<int, kRowBcast31>{}, std::integral_constant<int, 0xc>{});
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, kWave - 1);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), kWave - 1);
+    return ((uint64_t)hi << 32) | lo;
 }
 
 // Exclusive scan over a workgroup of NT threads.  `tmp` holds NT/64 + 1 ints
@@ -134,20 +179,12 @@ __device__ __forceinline__ float block_inclusive_scan_f32(float x, float* tmp, f
     constexpr int NW = NT / kWave;
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        float y = __shfl_up(x, off, kWave);
-        if (lane >= off) x += y;
-    }
+    x = wave_inclusive_scan_f32(x);
     if (lane == kWave - 1) tmp[w] = x;
     __syncthreads();
     if (w == 0) {
         float t = lane < NW ? tmp[lane] : 0.0f;
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            float y = __shfl_up(t, off, kWave);
-            if (lane >= off) t += y;
-        }
+        t = wave_inclusive_scan_f32(t);
         if (lane < NW) tmp[NW + 1 + lane] = t;  // inclusive wave prefixes
     }
     __syncthreads();

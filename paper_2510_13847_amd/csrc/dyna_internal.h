@@ -78,6 +78,9 @@ struct RowdotArgs {
     // plan mode (when plan.hdr != nullptr): chunks and context lists
     Plan plan;
     int32_t max_chunks_bound;  // host-known upper bound on plan chunks
+    // plan mode, optional: vid_out[b * ld + slot] = perm[layout row of slot]
+    const int32_t* perm;
+    int32_t* vid_out;
 };
 dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);
 
@@ -86,7 +89,9 @@ dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int3
                                  int32_t* topk_ids, float* topk_scores,
                                  // optional fused shortlist outputs (all or none)
                                  const int32_t* offsets, int32_t* sel_sorted,
-                                 int32_t* sel_rowoff, int32_t* row_len, hipStream_t stream);
+                                 int32_t* sel_rowoff, int32_t* row_len,
+                                 // with one context, also write the gathered-head plan
+                                 const Plan* plan, hipStream_t stream);
 dyna_status launch_shortlist(const int32_t* offsets, const int32_t* perm, int32_t M,
                              const int32_t* topk_ids, int32_t B, int32_t k,
                              int32_t* sel_sorted, int32_t* sel_rowoff, int32_t* row_len,
@@ -100,7 +105,10 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
                           const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
                           float temperature, const float* uniforms, int32_t* out_ids,
                           float* out_logprobs, int32_t* out_sample,
-                          float* out_sample_logprob, void* ws, hipStream_t stream);
+                          float* out_sample_logprob, void* ws, hipStream_t stream,
+                          // optional [B, ld]: vocabulary id of every slot (written
+                          // by the gathered head); saves the layout walk
+                          const int32_t* slot_vid = nullptr);
 // Workspace for launch_select with rows of at most max_len slots.
 size_t select_ws_bytes(int32_t B, int32_t max_len, int32_t k_t);
 // Longest row launch_select handles (256 segments).
@@ -109,5 +117,6 @@ int32_t select_max_len();
 // Global options (dyna_set_option).
 int option_logits_path();
 int option_router_path();
+int option_gemv_rows();
 
 }  // namespace dyna

@@ -28,44 +28,111 @@ constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / kWave;
 
 // ------------------------------------------------------------------ GEMV
-template <typename WT, typename VT, int NB, bool PLAN>
+// Raw 16-byte pieces of a row: bf16 rows need one u32x4 per 8 elements,
+// fp32 rows two.  Rows stay raw in registers and are widened inside the FMA
+// loop, which halves the registers a bf16 row needs.
+template <typename T>
+struct Raw8;
+template <>
+struct Raw8<uint16_t> {
+    u32x4 q;
+    template <bool NT>
+    __device__ __forceinline__ void load(const uint16_t* p) {
+        q = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p))
+               : *reinterpret_cast<const u32x4*>(p);
+    }
+    __device__ __forceinline__ void zero() { q = u32x4{0u, 0u, 0u, 0u}; }
+    __device__ __forceinline__ float at(int j) const {
+        return (j & 1) ? bf16_hi(q[j >> 1]) : bf16_lo(q[j >> 1]);
+    }
+};
+template <>
+struct Raw8<float> {
+    u32x4 q0, q1;
+    template <bool NT>
+    __device__ __forceinline__ void load(const float* p) {
+        const u32x4* r = reinterpret_cast<const u32x4*>(p);
+        q0 = NT ? __builtin_nontemporal_load(r) : r[0];
+        q1 = NT ? __builtin_nontemporal_load(r + 1) : r[1];
+    }
+    __device__ __forceinline__ void zero() { q0 = q1 = u32x4{0u, 0u, 0u, 0u}; }
+    __device__ __forceinline__ float at(int j) const {
+        return __uint_as_float(j < 4 ? q0[j] : q1[j - 4]);
+    }
+};
+
+// One wave computes R consecutive rows per iteration.  With SINGLE (one
+// context: B = 1) the context row is loaded into registers once per wave.
+template <typename WT, typename VT, int NB, bool PLAN, int R, bool SINGLE>
 __global__ __launch_bounds__(kThreads) void rowdot_gemv_kernel(RowdotArgs a) {
+    static_assert(kTileRows % R == 0, "row groups must tile a chunk");
+    constexpr int kGroups = kTileRows / R;  // row groups per plan chunk
     const int lane = lane_id();
     const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
-    const int64_t n_items = PLAN ? (int64_t)a.plan.hdr->n_chunks * kTileRows : (int64_t)a.n_rows;
     const WT* __restrict__ W = static_cast<const WT*>(a.W);
     const VT* __restrict__ v = static_cast<const VT*>(a.v);
     const int K = a.K;
+    const int64_t it0 = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
 
-    for (int64_t it = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; it < n_items;
-         it += nwaves) {
-        int64_t row;
-        int lcnt;
-        const ListEntry* list = nullptr;
-        if constexpr (PLAN) {
-            const Chunk c = a.plan.chunks[it / kTileRows];
-            const int r = (int)(it % kTileRows);
-            if (r >= c.nrows) continue;
-            row = (int64_t)c.r0 + r;
-            lcnt = c.list_cnt;
-            list = a.plan.list + c.list_off;
-        } else {
-            row = it;
-            lcnt = a.B;
-        }
-        const WT* wr = W + row * K;
-        float w[NB][8];
+    Raw8<VT> hv[SINGLE ? NB : 1];
+    if constexpr (SINGLE) {
 #pragma unroll
         for (int blk = 0; blk < NB; ++blk) {
             const int e = blk * 512 + lane * 8;
-            if (e < K) {
-                Load8<WT, true>::run(wr + e, w[blk]);
-            } else {
+            if (e < K) hv[blk].template load<false>(v + e);
+            else hv[blk].zero();
+        }
+    }
+
+    int64_t n_items;
+    Chunk pre{0, 0, 0, 0};
+    if constexpr (PLAN) {
+        // the first chunk descriptor is fetched together with the count
+        // (in bounds: the grid never exceeds the allocated chunk table)
+        const int64_t c0 = it0 / kGroups;
+        if (c0 < a.plan.max_chunks) pre = a.plan.chunks[c0];
+        n_items = (int64_t)a.plan.hdr->n_chunks * kGroups;
+    } else {
+        n_items = ((int64_t)a.n_rows + R - 1) / R;
+    }
+
+    for (int64_t it = it0; it < n_items; it += nwaves) {
+        int64_t row0;
+        int nrow;  // valid rows of this group
+        int lcnt;
+        const ListEntry* list = nullptr;
+        if constexpr (PLAN) {
+            const Chunk c = it == it0 ? pre : a.plan.chunks[it / kGroups];
+            const int sub = (int)(it % kGroups) * R;
+            if (sub >= c.nrows) continue;
+            row0 = (int64_t)c.r0 + sub;
+            nrow = min(R, c.nrows - sub);
+            lcnt = c.list_cnt;
+            list = a.plan.list + c.list_off;
+        } else {
+            row0 = it * R;
+            nrow = (int)min<int64_t>(R, (int64_t)a.n_rows - row0);
+            lcnt = a.B;
+        }
+        Raw8<WT> w[R][NB];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) w[blk][j] = 0.0f;
+        for (int r = 0; r < R; ++r) {
+            const WT* wr = W + (row0 + r) * K;
+#pragma unroll
+            for (int blk = 0; blk < NB; ++blk) {
+                const int e = blk * 512 + lane * 8;
+                if (r < nrow && e < K) w[r][blk].template load<true>(wr + e);
+                else w[r][blk].zero();
             }
         }
-        const float bias = a.bias ? a.bias[row] : 0.0f;
+        // lane r < nrow owns row r of the group in the epilogue
+        const bool own = lane < nrow;
+        const float bias = (a.bias && own) ? a.bias[row0 + lane] : 0.0f;
+        int32_t vid = 0;
+        if constexpr (PLAN) {
+            if (a.vid_out && own) vid = a.perm[row0 + lane];
+        }
+
         for (int i = 0; i < lcnt; ++i) {
             int b, base;
             if constexpr (PLAN) {
@@ -76,20 +143,39 @@ __global__ __launch_bounds__(kThreads) void rowdot_gemv_kernel(RowdotArgs a) {
                 b = i;
                 base = 0;
             }
-            const VT* vr = v + (int64_t)b * K;
-            float acc = 0.0f;
+            float acc[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r] = 0.0f;
 #pragma unroll
             for (int blk = 0; blk < NB; ++blk) {
-                const int e = blk * 512 + lane * 8;
-                if (e < K) {
-                    float x[8];
-                    Load8<VT, false>::run(vr + e, x);
+                Raw8<VT> x;
+                if constexpr (SINGLE) {
+                    x = hv[blk];
+                } else {
+                    const int e = blk * 512 + lane * 8;
+                    if (e < K) x.template load<false>(v + (int64_t)b * K + e);
+                    else x.zero();
+                }
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) acc = fmaf(w[blk][j], x[j], acc);
+                for (int j = 0; j < 8; ++j) {
+                    const float xj = x.at(j);
+#pragma unroll
+                    for (int r = 0; r < R; ++r) acc[r] = fmaf(w[r][blk].at(j), xj, acc[r]);
                 }
             }
-            acc = wave_sum(acc);
-            if (lane == 0) a.out[(int64_t)b * a.ld + base + row] = apply_act(acc + bias, a.act);
+            float mine = 0.0f;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const float t = wave_sum(acc[r]);
+                if (lane == r) mine = t;
+            }
+            if (own) {
+                const int64_t o = (int64_t)b * a.ld + base + row0 + lane;
+                a.out[o] = apply_act(mine + bias, a.act);
+                if constexpr (PLAN) {
+                    if (a.vid_out) a.vid_out[o] = vid;
+                }
+            }
         }
     }
 }
@@ -153,6 +239,14 @@ __global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
         }
         const bool rvalid = col < nrows;
         const uint16_t* wrow = W + (int64_t)(r0 + (rvalid ? col : 0)) * K + kq * 8;
+        int32_t pv[4] = {0, 0, 0, 0};
+        if constexpr (PLAN) {
+            if (a.vid_out) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (kq * 4 + r < nrows) pv[r] = a.perm[r0 + kq * 4 + r];
+            }
+        }
 
         for (int gb = 0; gb < lcnt; gb += 16 * G) {
             int cb[G], cbase[G];
@@ -247,6 +341,9 @@ __global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
                     if (i < nrows) {
                         const float bias = a.bias ? a.bias[r0 + i] : 0.0f;
                         o[i] = apply_act(acc[g][r] + bias, a.act);
+                        if constexpr (PLAN) {
+                            if (a.vid_out) a.vid_out[(o - a.out) + i] = pv[r];
+                        }
                     }
                 }
             }
@@ -256,13 +353,42 @@ __global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
 
 int resident_blocks() { return 256 * 8; }  // 256 CUs x 8 blocks of 4 waves
 
+// Rows in flight per wave: up to 4 where the registers allow it (a
+// 4096-wide bf16 row takes 32 VGPRs raw), fewer for long or fp32 rows.
+template <typename WT, int NB>
+constexpr int gemv_max_rows() {
+    return (sizeof(WT) == 2 ? NB : 2 * NB) <= 8 ? 4 : ((sizeof(WT) == 2 ? NB : 2 * NB) <= 16 ? 2 : 1);
+}
+
+template <typename WT, typename VT, bool PLAN, int NB, int R>
+dyna_status launch_gemv_r(const RowdotArgs& a, bool single, hipStream_t stream) {
+    const int64_t items = PLAN ? (int64_t)a.max_chunks_bound * (kTileRows / R)
+                               : ((int64_t)a.n_rows + R - 1) / R;
+    const int64_t blocks = std::max<int64_t>(
+        1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock, 4096));
+    if (single)
+        rowdot_gemv_kernel<WT, VT, NB, PLAN, R, true><<<(unsigned)blocks, kThreads, 0, stream>>>(a);
+    else
+        rowdot_gemv_kernel<WT, VT, NB, PLAN, R, false><<<(unsigned)blocks, kThreads, 0, stream>>>(a);
+    return check_launch("rowdot_gemv_kernel");
+}
+
+template <typename WT, typename VT, bool PLAN, int NB>
+dyna_status launch_gemv_t(const RowdotArgs& a, bool single, int rows_opt, hipStream_t stream) {
+    constexpr int RMAX = gemv_max_rows<WT, NB>();
+    int R = rows_opt > 0 ? std::min(rows_opt, RMAX) : RMAX;
+    // a small dense matrix (a router layer) spreads one row per wave so that
+    // every CU takes part
+    if (rows_opt == 0 && !PLAN && (int64_t)a.n_rows < 4 * 256 * 16) R = 1;
+    if (R >= 4 && RMAX >= 4) return launch_gemv_r<WT, VT, PLAN, NB, (RMAX >= 4 ? 4 : 1)>(a, single, stream);
+    if (R >= 2 && RMAX >= 2) return launch_gemv_r<WT, VT, PLAN, NB, (RMAX >= 2 ? 2 : 1)>(a, single, stream);
+    return launch_gemv_r<WT, VT, PLAN, NB, 1>(a, single, stream);
+}
+
 template <typename WT, typename VT, bool PLAN>
-dyna_status launch_gemv_nb(const RowdotArgs& a, int nb, unsigned grid, hipStream_t stream) {
-#define DYNA_GEMV_CASE(N)                                                              \
-    if (nb <= N) {                                                                     \
-        rowdot_gemv_kernel<WT, VT, N, PLAN><<<grid, kThreads, 0, stream>>>(a);         \
-        return check_launch("rowdot_gemv_kernel");                                     \
-    }
+dyna_status launch_gemv_nb(const RowdotArgs& a, int nb, bool single, int rows_opt, hipStream_t stream) {
+#define DYNA_GEMV_CASE(N) \
+    if (nb <= N) return launch_gemv_t<WT, VT, PLAN, N>(a, single, rows_opt, stream);
     DYNA_GEMV_CASE(1)
     DYNA_GEMV_CASE(2)
     DYNA_GEMV_CASE(4)
@@ -276,15 +402,13 @@ dyna_status launch_gemv_nb(const RowdotArgs& a, int nb, unsigned grid, hipStream
 template <bool PLAN>
 dyna_status launch_gemv(const RowdotArgs& a, hipStream_t stream) {
     const int nb = (a.K + 511) / 512;
-    const int64_t items = PLAN ? (int64_t)a.max_chunks_bound * kTileRows : (int64_t)a.n_rows;
-    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock,
-                                                                   resident_blocks()));
-    const unsigned grid = (unsigned)blocks;
+    const bool single = a.B == 1;
+    const int rows_opt = option_gemv_rows();
     const bool wb = a.wdtype == DYNA_BF16, vb = a.vdtype == DYNA_BF16;
-    if (wb && vb) return launch_gemv_nb<uint16_t, uint16_t, PLAN>(a, nb, grid, stream);
-    if (wb && !vb) return launch_gemv_nb<uint16_t, float, PLAN>(a, nb, grid, stream);
-    if (!wb && vb) return launch_gemv_nb<float, uint16_t, PLAN>(a, nb, grid, stream);
-    return launch_gemv_nb<float, float, PLAN>(a, nb, grid, stream);
+    if (wb && vb) return launch_gemv_nb<uint16_t, uint16_t, PLAN>(a, nb, single, rows_opt, stream);
+    if (wb && !vb) return launch_gemv_nb<uint16_t, float, PLAN>(a, nb, single, rows_opt, stream);
+    if (!wb && vb) return launch_gemv_nb<float, uint16_t, PLAN>(a, nb, single, rows_opt, stream);
+    return launch_gemv_nb<float, float, PLAN>(a, nb, single, rows_opt, stream);
 }
 
 template <int G, bool VF32, bool PLAN, int KSPLIT, int U>

@@ -23,117 +23,157 @@ namespace {
 constexpr int kNT = 256;
 
 // ------------------------------------------------------------------ top-k
+// One workgroup per context.  Scores (and, for the shortlist, the CSR
+// offsets) are staged in LDS in one round trip.  Two 8-bit radix passes over
+// the ordered score codes find the 16-bit prefix P of the k-th largest score:
+// every code above P is selected, and the few codes sharing P are ranked
+// exactly by (score desc, id asc) to fill the remaining places.  The k keys
+// are then put in rank order and in ascending id order; with `plan` set (one
+// context) the workgroup also writes the gathered-head work plan, so no
+// separate plan launch is needed for a single context.
+__device__ __forceinline__ void radix_digit(const int* hist, int krem, uint32_t prefix, int shift,
+                                            uint32_t* sh_prefix, int* sh_krem) {
+    // wave 0: lane l holds digits 255-4l .. 252-4l (descending)
+    const int l = lane_id();
+    int c[4], sum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        c[q] = hist[255 - 4 * l - q];
+        sum += c[q];
+    }
+    const int inc = wave_inclusive_scan(sum);
+    const int exc = inc - sum;
+    if (exc < krem && krem <= inc) {
+        int acc = exc;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (acc + c[q] >= krem) {
+                *sh_prefix = prefix | ((uint32_t)(255 - 4 * l - q) << shift);
+                *sh_krem = krem - acc;
+                break;
+            }
+            acc += c[q];
+        }
+    }
+}
+
 __global__ __launch_bounds__(kNT) void topk_clusters_kernel(
     const float* __restrict__ scores, int M, int k, int32_t* __restrict__ topk_ids,
     float* __restrict__ topk_scores, const int32_t* __restrict__ offsets,
     int32_t* __restrict__ sel_sorted, int32_t* __restrict__ sel_rowoff,
-    int32_t* __restrict__ row_len) {
+    int32_t* __restrict__ row_len, Plan plan) {
     extern __shared__ unsigned char smem[];
-    uint64_t* skey = reinterpret_cast<uint64_t*>(smem);       // [k], ascending id
-    int32_t* ssize = reinterpret_cast<int32_t*>(skey + k);    // [k]
+    float* sv = reinterpret_cast<float*>(smem);                       // [M] raw scores
+    int32_t* offs = reinterpret_cast<int32_t*>(sv + M);                // [M + 1]
+    uint64_t* sel = reinterpret_cast<uint64_t*>(smem + ((size_t)(2 * M + 1) * 4 + 7) / 8 * 8);  // [k]
+    uint64_t* cand = sel + k;                                          // [M] tie candidates
+    int32_t* sid = reinterpret_cast<int32_t*>(cand + M);               // [k] ids ascending
+    int32_t* ssize = sid + k;                                          // [k]
     __shared__ int hist[256];
     __shared__ int tmp[kNT / kWave + 1];
     __shared__ uint32_t sh_prefix;
-    __shared__ int sh_krem;
+    __shared__ int sh_krem, sh_nsel, sh_ncand;
 
     const int b = blockIdx.x;
     const float* s = scores + (int64_t)b * M;
-    const int E = (M + kNT - 1) / kNT;
-    const int j0 = min(M, (int)threadIdx.x * E);
-    const int j1 = min(M, j0 + E);
-
-    // radix select: the ordered code T of the k-th largest score, and how
-    // many of the codes equal to T still have to be taken (krem >= 1)
-    uint32_t prefix = 0, mask = 0;
-    int krem = k;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int i = threadIdx.x; i < 256; i += kNT) hist[i] = 0;
-        __syncthreads();
-        for (int j = j0; j < j1; ++j) {
-            const uint32_t o = ord_f32(s[j]);
-            if ((o & mask) == prefix) atomicAdd(&hist[(o >> shift) & 255u], 1);
-        }
-        __syncthreads();
-        if (threadIdx.x < kWave) {
-            const int l = threadIdx.x;  // lane l holds digits 255-4l .. 252-4l
-            int c[4], sum = 0;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                c[q] = hist[255 - 4 * l - q];
-                sum += c[q];
-            }
-            const int inc = wave_inclusive_scan(sum);
-            const int exc = inc - sum;
-            if (exc < krem && krem <= inc) {
-                int acc = exc;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    if (acc + c[q] >= krem) {
-                        sh_prefix = prefix | ((uint32_t)(255 - 4 * l - q) << shift);
-                        sh_krem = krem - acc;
-                        break;
-                    }
-                    acc += c[q];
-                }
-            }
-        }
-        __syncthreads();
-        prefix = sh_prefix;
-        krem = sh_krem;
-        mask |= 255u << shift;
-        __syncthreads();
-    }
-    const uint32_t T = prefix;
-
-    int n_gt = 0, n_eq = 0;
-    for (int j = j0; j < j1; ++j) {
-        const uint32_t o = ord_f32(s[j]);
-        n_gt += o > T;
-        n_eq += o == T;
-    }
-    int total;
-    const int eq_before = block_exclusive_scan<kNT>(n_eq, tmp, &total);
-    const int take_eq = max(0, min(n_eq, krem - eq_before));
-    const int sel_before = block_exclusive_scan<kNT>(n_gt + take_eq, tmp, &total);
-    int pos = sel_before, eq_seen = 0;
-    for (int j = j0; j < j1; ++j) {
-        const uint32_t o = ord_f32(s[j]);
-        bool take = o > T;
-        if (o == T) take = eq_seen++ < take_eq;
-        if (take) skey[pos++] = (static_cast<uint64_t>(o) << 32) | (0xffffffffu - (uint32_t)j);
+    for (int j = threadIdx.x; j < M; j += kNT) sv[j] = s[j];
+    if (sel_sorted != nullptr)
+        for (int j = threadIdx.x; j <= M; j += kNT) offs[j] = offsets[j];
+    hist[threadIdx.x] = 0;
+    if (threadIdx.x == 0) {
+        sh_nsel = 0;
+        sh_ncand = 0;
     }
     __syncthreads();
 
-    // rank order (score desc, id asc) by counting larger keys
-    for (int i = threadIdx.x; i < k; i += kNT) {
-        const uint64_t key = skey[i];
-        int rank = 0;
-        for (int j = 0; j < k; ++j) rank += skey[j] > key;
-        const uint32_t id = key_id(key);
-        topk_ids[(int64_t)b * k + rank] = (int32_t)id;
-        if (topk_scores) topk_scores[(int64_t)b * k + rank] = s[id];
+    // pass 1: top byte
+    for (int j = threadIdx.x; j < M; j += kNT) atomicAdd(&hist[ord_f32(sv[j]) >> 24], 1);
+    __syncthreads();
+    if (threadIdx.x < kWave) radix_digit(hist, k, 0u, 24, &sh_prefix, &sh_krem);
+    __syncthreads();
+    const uint32_t p1 = sh_prefix;
+    hist[threadIdx.x] = 0;
+    __syncthreads();
+    // pass 2: second byte inside the chosen top byte
+    for (int j = threadIdx.x; j < M; j += kNT) {
+        const uint32_t o = ord_f32(sv[j]);
+        if ((o & 0xff000000u) == p1) atomicAdd(&hist[(o >> 16) & 255u], 1);
     }
+    __syncthreads();
+    if (threadIdx.x < kWave) radix_digit(hist, sh_krem, p1, 16, &sh_prefix, &sh_krem);
+    __syncthreads();
+    const uint32_t P = sh_prefix >> 16;  // 16-bit prefix of the k-th largest code
+    const int need = sh_krem;             // places left for codes with prefix P
 
-    if (sel_sorted != nullptr) {
-        const int per = (k + kNT - 1) / kNT;
-        const int i0 = min(k, (int)threadIdx.x * per);
-        const int i1 = min(k, i0 + per);
-        int local = 0;
-        for (int i = i0; i < i1; ++i) {
-            const int m = (int)key_id(skey[i]);
-            ssize[i] = offsets[m + 1] - offsets[m];
-            local += ssize[i];
+    // codes above P are in; codes with prefix P are ranked below
+    for (int j = threadIdx.x; j < M; j += kNT) {
+        const uint32_t o = ord_f32(sv[j]);
+        const uint64_t key = (static_cast<uint64_t>(o) << 32) | (0xffffffffu - (uint32_t)j);
+        if ((o >> 16) > P) sel[atomicAdd(&sh_nsel, 1)] = key;
+        else if ((o >> 16) == P) cand[atomicAdd(&sh_ncand, 1)] = key;
+    }
+    __syncthreads();
+    const int nsel0 = sh_nsel, ncand = sh_ncand;
+    for (int c = threadIdx.x; c < ncand; c += kNT) {
+        const uint64_t key = cand[c];
+        int rank = 0;
+        for (int j = 0; j < ncand; ++j) rank += cand[j] > key;
+        if (rank < need) sel[nsel0 + rank] = key;
+    }
+    __syncthreads();
+
+    // rank order (score desc, id asc) and ascending-id order by counting
+    for (int i = threadIdx.x; i < k; i += kNT) {
+        const uint64_t key = sel[i];
+        const uint32_t id = key_id(key);
+        int rank = 0, idrank = 0;
+        for (int j = 0; j < k; ++j) {
+            const uint64_t o = sel[j];
+            rank += o > key;
+            idrank += key_id(o) < id;
         }
-        int len;
-        int run = block_exclusive_scan<kNT>(local, tmp, &len);
-        for (int i = i0; i < i1; ++i) {
-            sel_sorted[(int64_t)b * k + i] = (int32_t)key_id(skey[i]);
-            sel_rowoff[(int64_t)b * (k + 1) + i] = run;
-            run += ssize[i];
+        topk_ids[(int64_t)b * k + rank] = (int32_t)id;
+        if (topk_scores) topk_scores[(int64_t)b * k + rank] = sv[id];
+        if (sel_sorted != nullptr) {
+            sid[idrank] = (int32_t)id;
+            ssize[idrank] = offs[id + 1] - offs[id];
         }
-        if (threadIdx.x == 0) {
-            sel_rowoff[(int64_t)b * (k + 1) + k] = len;
-            row_len[b] = len;
+    }
+    if (sel_sorted == nullptr) return;
+    __syncthreads();
+
+    // shortlist: exclusive prefix of the sizes in ascending id order
+    const int per = (k + kNT - 1) / kNT;
+    const int i0 = min(k, (int)threadIdx.x * per);
+    const int i1 = min(k, i0 + per);
+    int local = 0, lchunks = 0;
+    for (int i = i0; i < i1; ++i) {
+        local += ssize[i];
+        lchunks += (ssize[i] + kTileRows - 1) / kTileRows;
+    }
+    int len, n_chunks = 0;
+    int run = block_exclusive_scan<kNT>(local, tmp, &len);
+    int crun = plan.hdr ? block_exclusive_scan<kNT>(lchunks, tmp, &n_chunks) : 0;
+    for (int i = i0; i < i1; ++i) {
+        const int m = sid[i];
+        sel_sorted[(int64_t)b * k + i] = m;
+        sel_rowoff[(int64_t)b * (k + 1) + i] = run;
+        if (plan.hdr) {
+            const int o = offs[m];
+            plan.list[i] = ListEntry{b, run - o};
+            for (int c = 0; c * kTileRows < ssize[i]; ++c)
+                plan.chunks[crun + c] =
+                    Chunk{o + c * kTileRows, min(kTileRows, ssize[i] - c * kTileRows), i, 1};
+            crun += (ssize[i] + kTileRows - 1) / kTileRows;
+        }
+        run += ssize[i];
+    }
+    if (threadIdx.x == 0) {
+        sel_rowoff[(int64_t)b * (k + 1) + k] = len;
+        row_len[b] = len;
+        if (plan.hdr) {
+            plan.hdr->n_chunks = n_chunks;
+            plan.hdr->n_entries = k;
         }
     }
 }
@@ -277,6 +317,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 // ------------------------------------------------------------------ select
 constexpr int kSeg = 2048;          // shortlist slots per partial workgroup
 constexpr int kPer = kSeg / kNT;    // 8 slots per thread
+constexpr int kRowMax = 32768;      // longest row the one-launch select takes
 
 struct SelectArgs {
     const float* logits;
@@ -287,6 +328,7 @@ struct SelectArgs {
     const int32_t* sel_rowoff;
     const int32_t* offsets;
     const int32_t* perm;      // nullptr: vocabulary id = slot
+    const int32_t* slot_vid;  // optional [B][ld]: vocabulary id per slot
     int32_t k;
     int32_t k_t;
     float inv_t;
@@ -306,6 +348,10 @@ __device__ __forceinline__ float canon(float z) { return z != z ? -__builtin_inf
 
 // Vocabulary ids of the slots [j0, j0 + n) of row b, written into vid[].
 __device__ __forceinline__ void slot_vids(const SelectArgs& a, int b, int j0, int n, uint32_t* vid) {
+    if (a.slot_vid != nullptr) {
+        for (int q = 0; q < n; ++q) vid[q] = (uint32_t)a.slot_vid[(int64_t)b * a.ld + j0 + q];
+        return;
+    }
     if (a.perm == nullptr) {
         for (int q = 0; q < n; ++q) vid[q] = (uint32_t)(j0 + q);
         return;
@@ -551,15 +597,156 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     }
 }
 
+// Whole-row selection in one workgroup (shortlist-sized rows, k_t <= KT).
+// Max, top-k_t and the softmax sum read the row with coalesced strided loads;
+// only the sampling walk uses contiguous per-thread ranges, so that the CDF
+// runs in shortlist order.  Vocabulary ids come from the gathered head's
+// per-slot ids when present, else from the shortlist's cluster table staged
+// in LDS.
+constexpr int kRowTable = 1024;  // clusters per row the LDS table holds
+
+template <int KT>
+__global__ __launch_bounds__(kNT) void select_row_kernel(SelectArgs a) {
+    __shared__ uint64_t wmax[8];
+    __shared__ uint64_t top[DYNA_MAX_KT];
+    __shared__ float red[2 * (kNT / kWave) + 1];
+    __shared__ float incl_s[kNT];
+    __shared__ int sh_pick;
+    __shared__ int32_t t_ro[kRowTable + 1];
+    __shared__ int32_t t_base[kRowTable];
+    const int b = blockIdx.x;
+    const int len = a.row_len ? a.row_len[b] : a.fixed_len;
+    const float* z = a.logits + (int64_t)b * a.ld;
+    const int32_t* sv = a.slot_vid ? a.slot_vid + (int64_t)b * a.ld : nullptr;
+    const bool table = sv == nullptr && a.perm != nullptr;
+    if (table) {  // slot -> layout row: rows of cluster ci start at t_base[ci] + slot
+        const int32_t* ro = a.sel_rowoff + (int64_t)b * (a.k + 1);
+        const int32_t* ss = a.sel_sorted + (int64_t)b * a.k;
+        for (int c = threadIdx.x; c <= a.k; c += kNT) {
+            t_ro[c] = ro[c];
+            if (c < a.k) t_base[c] = ss[c] >= 0 ? a.offsets[ss[c]] - ro[c] : 0;
+        }
+        __syncthreads();
+    }
+    auto vid_of = [&](int j) -> uint32_t {
+        if (sv != nullptr) return (uint32_t)sv[j];
+        if (a.perm == nullptr) return (uint32_t)j;
+        int lo = 0, hi = a.k - 1;  // largest ci with ro[ci] <= j
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (t_ro[mid] <= j) lo = mid; else hi = mid - 1;
+        }
+        return (uint32_t)a.perm[t_base[lo] + j];
+    };
+
+    uint64_t list[KT];
+#pragma unroll
+    for (int q = 0; q < KT; ++q) list[q] = 0;
+#pragma unroll 4
+    for (int j = threadIdx.x; j < len; j += kNT) {
+        const uint64_t key = sel_key(canon(z[j]), vid_of(j));
+        if (key > list[KT - 1]) {
+            list[KT - 1] = key;
+#pragma unroll
+            for (int q = KT - 1; q > 0; --q)
+                if (list[q] > list[q - 1]) {
+                    const uint64_t t = list[q];
+                    list[q] = list[q - 1];
+                    list[q - 1] = t;
+                }
+        }
+    }
+    block_topk_rounds<KT>(list, a.k_t, wmax, top);
+    const float mx = top[0] != 0 ? key_val(top[0]) : -__builtin_inff();
+    const bool sampling = a.uniforms != nullptr && a.out_sample != nullptr;
+
+    // softmax mass: strided when only top-k is asked, contiguous ranges
+    // (shortlist order) when a sample must be drawn from the same sums
+    const int E = (len + kNT - 1) / kNT;
+    const int j0 = min(len, (int)threadIdx.x * E);
+    const int j1 = min(len, j0 + E);
+    float tsum = 0.0f;
+    if (mx != -__builtin_inff()) {
+        if (sampling) {
+            for (int j = j0; j < j1; ++j) tsum += expf((canon(z[j]) - mx) * a.inv_t);
+        } else {
+#pragma unroll 4
+            for (int j = threadIdx.x; j < len; j += kNT) tsum += expf((canon(z[j]) - mx) * a.inv_t);
+        }
+    }
+    float total;
+    const float incl = block_inclusive_scan_f32<kNT>(tsum, red, &total);
+    const float log_total = logf(total);
+    if (a.out_ids != nullptr) {
+        for (int r = threadIdx.x; r < a.k_t; r += kNT) {
+            const uint64_t key = top[r];
+            a.out_ids[(int64_t)b * a.k_t + r] = key != 0 ? (int32_t)key_id(key) : -1;
+            if (a.out_logprobs)
+                a.out_logprobs[(int64_t)b * a.k_t + r] =
+                    key != 0 ? (key_val(key) - mx) * a.inv_t - log_total : -__builtin_inff();
+        }
+    }
+    if (!sampling) return;
+
+    incl_s[threadIdx.x] = incl;
+    if (threadIdx.x == 0) sh_pick = -1;
+    __syncthreads();
+    const float excl = threadIdx.x > 0 ? incl_s[threadIdx.x - 1] : 0.0f;
+    const float target = a.uniforms[b] * total;
+    if (tsum > 0.0f && excl <= target && target < incl) {
+        float acc = excl;
+        int pick = -1, last = -1;
+        for (int j = j0; j < j1; ++j) {
+            const float e = expf((canon(z[j]) - mx) * a.inv_t);
+            if (e > 0.0f) last = j;
+            acc += e;
+            if (e > 0.0f && acc > target) {
+                pick = j;
+                break;
+            }
+        }
+        atomicMax(&sh_pick, pick >= 0 ? pick : last);
+    }
+    __syncthreads();
+    if (sh_pick < 0 && tsum > 0.0f) {  // rounding: the last slot with mass
+        int last = -1;
+        for (int j = j0; j < j1; ++j)
+            if (expf((canon(z[j]) - mx) * a.inv_t) > 0.0f) last = j;
+        atomicMax(&sh_pick, last);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int j = sh_pick;
+        if (j < 0) {
+            a.out_sample[b] = -1;
+            if (a.out_sample_logprob) a.out_sample_logprob[b] = -__builtin_inff();
+        } else {
+            a.out_sample[b] = (int32_t)vid_of(j);
+            if (a.out_sample_logprob) a.out_sample_logprob[b] = (canon(z[j]) - mx) * a.inv_t - log_total;
+        }
+    }
+}
+
 }  // namespace
 
 dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int32_t k,
                                  int32_t* topk_ids, float* topk_scores, const int32_t* offsets,
                                  int32_t* sel_sorted, int32_t* sel_rowoff, int32_t* row_len,
-                                 hipStream_t stream) {
-    const size_t lds = (size_t)k * (sizeof(uint64_t) + sizeof(int32_t));
+                                 const Plan* plan, hipStream_t stream) {
+    const size_t lds = ((size_t)(2 * M + 1) * 4 + 7) / 8 * 8 + (size_t)(k + M) * sizeof(uint64_t) +
+                       (size_t)2 * k * sizeof(int32_t);
+    if (lds > 65536) {
+        static bool raised = false;
+        if (!raised &&
+            hipFuncSetAttribute(reinterpret_cast<const void*>(topk_clusters_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+            return set_error(DYNA_ERR_UNSUPPORTED, "top-k needs %zu bytes of LDS", lds);
+        raised = true;
+    }
+    Plan p{};
+    if (plan != nullptr && B == 1) p = *plan;
     topk_clusters_kernel<<<B, kNT, lds, stream>>>(scores, M, k, topk_ids, topk_scores, offsets,
-                                                  sel_sorted, sel_rowoff, row_len);
+                                                  sel_sorted, sel_rowoff, row_len, p);
     return check_launch("topk_clusters_kernel");
 }
 
@@ -594,8 +781,9 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
                           int32_t B, int32_t k, int32_t k_t, float temperature,
                           const float* uniforms, int32_t* out_ids, float* out_logprobs,
                           int32_t* out_sample, float* out_sample_logprob, void* ws,
-                          hipStream_t stream) {
+                          hipStream_t stream, const int32_t* slot_vid) {
     SelectArgs a;
+    a.slot_vid = slot_vid;
     a.logits = logits;
     a.ld = ld;
     a.row_len = row_len;
@@ -619,6 +807,12 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
     a.out_logprobs = out_logprobs;
     a.out_sample = out_sample;
     a.out_sample_logprob = out_sample_logprob;
+    // shortlist-sized rows: one workgroup per row, one launch
+    if (max_len <= (row_len ? kRowMax : kRowMax / 4) && k_t <= 16 && (perm == nullptr || k <= kRowTable)) {
+        if (k_t == 1) select_row_kernel<1><<<B, kNT, 0, stream>>>(a);
+        else select_row_kernel<16><<<B, kNT, 0, stream>>>(a);
+        return check_launch("select_row_kernel");
+    }
     select_partial_kernel<<<dim3(a.P, B), kNT, 0, stream>>>(a);
     if (dyna_status s = check_launch("select_partial_kernel"); s != DYNA_OK) return s;
     select_final_kernel<<<B, kNT, 0, stream>>>(a);
