@@ -22,6 +22,7 @@ std::atomic<int> g_logits_path{0};
 std::atomic<int> g_router_path{0};
 std::atomic<int> g_kernel_timing{0};
 std::atomic<int> g_gemv_rows{0};
+std::atomic<int> g_fused_off{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -67,17 +68,22 @@ static hipEvent_t timing_event() {
 }
 
 // Launch the gathered-head kernel, optionally between two timing events.
-static dyna_status timed_rowdot(const RowdotArgs& a, int path, hipStream_t s) {
-    if (!g_kernel_timing.load()) return launch_rowdot(a, path, s);
+template <typename F>
+static dyna_status timed(F launch, hipStream_t s) {
+    if (!g_kernel_timing.load()) return launch();
     hipEvent_t e0 = timing_event(), e1 = timing_event();
     if (!e0 || !e1 || hipEventRecord(e0, s) != hipSuccess)
         return set_error(DYNA_ERR_HIP, "kernel timing: event record failed");
-    dyna_status st = launch_rowdot(a, path, s);
+    dyna_status st = launch();
     if (st != DYNA_OK) return st;
     if (hipEventRecord(e1, s) != hipSuccess) return set_error(DYNA_ERR_HIP, "kernel timing: event record failed");
     std::lock_guard<std::mutex> g(g_timing_mu);
     g_timing_pairs.emplace_back(e0, e1);
     return DYNA_OK;
+}
+
+static dyna_status timed_rowdot(const RowdotArgs& a, int path, hipStream_t s) {
+    return timed([&] { return launch_rowdot(a, path, s); }, s);
 }
 int option_router_path() { return g_router_path.load(); }
 int option_gemv_rows() { return g_gemv_rows.load(); }
@@ -95,6 +101,8 @@ struct Carve {
     int32_t* row_len = nullptr;   // [B]
     float* logits = nullptr;      // [B, cap]
     int32_t* slot_vid = nullptr;  // [B, cap]
+    int32_t* counters = nullptr;  // [2] arrival counters of the fused one-context kernels
+    void* partials = nullptr;     // partials of the fused one-context head
     Plan plan{};
     void* select_ws = nullptr;
     size_t bytes = 0;
@@ -134,6 +142,8 @@ static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_
     c.row_len = static_cast<int32_t*>(take(sizeof(int32_t) * Bl));
     c.logits = static_cast<float*>(take(sizeof(float) * Bl * cap));
     c.slot_vid = static_cast<int32_t*>(take(sizeof(int32_t) * Bl * cap));
+    c.counters = static_cast<int32_t*>(take(2 * sizeof(int32_t)));
+    if (B == 1) c.partials = take(greedy_partials_bytes());
     if (L) {
         c.plan.max_chunks = (int32_t)max_chunks_for(L);
         c.plan.max_entries = (int32_t)(Bl * k);
@@ -221,9 +231,11 @@ static dyna_status check_select(int32_t mode, int32_t* k_t, float temperature, c
 
 // ------------------------------------------------------------------ pieces
 static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtype, int32_t B,
-                              float* scores, float* hidden, hipStream_t s) {
+                              float* scores, float* hidden, hipStream_t s, int32_t* zero_words = nullptr) {
     const int path = option_router_path();
     RowdotArgs a{};
+    a.zero_words = zero_words;  // cleared by block 0 of the first router kernel
+    a.n_zero_words = zero_words ? 2 : 0;
     a.W = r->W1;
     a.wdtype = r->wdtype;
     a.K = r->d_r;
@@ -314,6 +326,11 @@ DYNA_API const char* dyna_status_string(dyna_status s) {
 DYNA_API const char* dyna_last_error(void) { return g_last_error; }
 
 DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
+    if (option == DYNA_OPT_FUSED_B1) {
+        REQUIRE(value == 0 || value == 1, "fused option %d not in {0, 1}", value);
+        g_fused_off.store(value);
+        return DYNA_OK;
+    }
     if (option == DYNA_OPT_GEMV_ROWS) {
         REQUIRE(value == 0 || value == 1 || value == 2 || value == 4, "GEMV rows %d not in {0,1,2,4}", value);
         g_gemv_rows.store(value);
@@ -495,9 +512,16 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
         if (hipStreamWaitEvent(rs, ready, 0) != hipSuccess)
             return set_error(DYNA_ERR_HIP, "draft_head: route stream wait failed");
     }
-    // routing: router, top-k, shortlist, plan (the router's stream)
+    const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
+    const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     int32_t* clusters = out_clusters ? out_clusters : c.topk_ids;
-    TRY(run_router(r, x, adtype, B, c.scores, c.hidden, rs));
+    float* logits = out_logits ? out_logits : c.logits;
+    // one greedy context: the gathered head carries the selection (4 launches)
+    const bool fused = B == 1 && !g_fused_off.load() && option_logits_path() != 2 && k_t == 1 &&
+                       !want_sample;
+
+    // routing (the router's stream)
+    TRY(run_router(r, x, adtype, B, c.scores, c.hidden, rs, fused ? c.counters : nullptr));
     TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, L->offsets, c.sel_sorted,
                              c.sel_rowoff, c.row_len, &c.plan, rs));
     if (B > 1) TRY(launch_plan(L->offsets, L->M, c.sel_sorted, c.sel_rowoff, B, k, c.plan, rs));
@@ -507,7 +531,6 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
             return set_error(DYNA_ERR_HIP, "draft_head: stream join failed");
     }
     // gathered head and selection (the caller's stream)
-    float* logits = out_logits ? out_logits : c.logits;
     RowdotArgs a{};
     a.W = L->W_perm;
     a.wdtype = L->wdtype;
@@ -522,9 +545,13 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     a.max_chunks_bound = chunk_bound(L, B, k);
     a.perm = L->perm;
     a.vid_out = c.slot_vid;
+    const SelectArgs sa = make_select_args(
+        logits, cap, c.row_len, 0, cap, c.sel_sorted, c.sel_rowoff, L->offsets, L->perm, B, k, k_t,
+        temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
+        want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
+        want_sample ? out_sample_logprob : nullptr, c.select_ws, c.slot_vid);
+    if (fused) return timed([&] { return launch_logits_greedy(a, sa, c.partials, c.counters, stream); }, stream);
     TRY(timed_rowdot(a, option_logits_path(), stream));
-    const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
-    const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     return launch_select(logits, cap, c.row_len, 0, cap, c.sel_sorted, c.sel_rowoff, L->offsets, L->perm, B,
                          k, k_t, temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,

@@ -10,6 +10,8 @@
 
 namespace dyna {
 
+constexpr int kNT = 256;  // threads of the per-context (select, top-k) workgroups
+
 // ---------------------------------------------------------------- bf16
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -85,7 +87,8 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
 template <int CTRL, int ROW_MASK = 0xf, int BANK_MASK = 0xf>
 __device__ __forceinline__ uint32_t dpp(uint32_t identity, uint32_t x) {
-    return (uint32_t)__builtin_amdgcn_update_dpp((int)identity, (int)x, CTRL, ROW_MASK, BANK_MASK, true);
+    // bound_ctrl off: lanes whose source is outside the row keep `identity`
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)identity, (int)x, CTRL, ROW_MASK, BANK_MASK, false);
 }
 constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
 constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
@@ -122,6 +125,11 @@ __device__ __forceinline__ float wave_inclusive_scan_f32(float x) {
 }
 __device__ __forceinline__ float readlane_f32(float x, int l) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+
+__device__ __forceinline__ float wave_max_f32(float x) {
+    return wave_scan_dpp<float>(x, [](float a, float b) { return fmaxf(a, b); },
+                                __float_as_uint(-__builtin_inff()));
 }
 
 // Sum over the wave; every lane gets the same value (fixed order).
@@ -194,6 +202,18 @@ __device__ __forceinline__ float block_inclusive_scan_f32(float x, float* tmp, f
     return base + x;
 }
 
+// Device-coherent (agent scope) store / load: written through to, and read
+// from, the point where every XCD sees the same value, without an L2
+// write-back or invalidate.  Used for the few words one workgroup hands to
+// another inside a kernel.
+template <typename T>
+__device__ __forceinline__ void store_coherent(T* p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ T load_coherent(const T* p) {
+    return __hip_atomic_load(const_cast<T*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ float apply_act(float y, int act) {
     if (act == DYNA_ACT_RELU) return y > 0.0f ? y : 0.0f;
     if (act == DYNA_ACT_SILU) return y / (1.0f + expf(-y));

@@ -81,8 +81,51 @@ struct RowdotArgs {
     // plan mode, optional: vid_out[b * ld + slot] = perm[layout row of slot]
     const int32_t* perm;
     int32_t* vid_out;
+    // optional: block 0 clears these words first (arrival counters that the
+    // next kernels of the step use)
+    int32_t* zero_words;
+    int32_t n_zero_words;
 };
 dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);
+
+// Arguments of the per-context top-k (Sec. 4.2) and of the draft selection
+// (Algorithm 1), shared by the separate and the fused launches.
+struct TopkArgs {
+    const float* scores;   // [B, M]
+    int M, k;
+    int32_t* topk_ids;     // [B, k] rank order
+    float* topk_scores;    // [B, k] or nullptr
+    const int32_t* offsets;  // [M + 1] (shortlist)
+    int32_t* sel_sorted;   // [B, k] or nullptr: no shortlist
+    int32_t* sel_rowoff;   // [B, k + 1]
+    int32_t* row_len;      // [B]
+    Plan plan;             // hdr == nullptr: no plan (one context only)
+};
+
+struct SelectArgs {
+    const float* logits;
+    int64_t ld;
+    const int32_t* row_len;   // nullptr: every row has fixed_len
+    int32_t fixed_len;
+    const int32_t* sel_sorted;
+    const int32_t* sel_rowoff;
+    const int32_t* offsets;
+    const int32_t* perm;      // nullptr: vocabulary id = slot
+    const int32_t* slot_vid;  // optional [B][ld]: vocabulary id per slot
+    int32_t k;
+    int32_t k_t;
+    float inv_t;
+    const float* uniforms;
+    int32_t P;                // segments per row
+    // partials, [B][P][...]
+    uint64_t* pkeys;          // [B][P][k_t]
+    float* pmax;              // [B][P]
+    float* psum;              // [B][P]
+    int32_t* out_ids;
+    float* out_logprobs;
+    int32_t* out_sample;
+    float* out_sample_logprob;
+};
 
 // select.hip
 dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int32_t k,
@@ -113,6 +156,23 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
 size_t select_ws_bytes(int32_t B, int32_t max_len, int32_t k_t);
 // Longest row launch_select handles (256 segments).
 int32_t select_max_len();
+// Fill SelectArgs for rows of at most max_len slots; ws as for launch_select.
+SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_len,
+                            int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
+                            const int32_t* sel_rowoff, const int32_t* offsets,
+                            const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
+                            float temperature, const float* uniforms, int32_t* out_ids,
+                            float* out_logprobs, int32_t* out_sample,
+                            float* out_sample_logprob, void* ws, const int32_t* slot_vid);
+// True when the one-workgroup select handles rows of max_len slots.
+bool select_row_fits(int32_t max_len, bool fixed, int32_t k_t, int32_t k);
+
+// fused.hip (one context, greedy): gathered head + argmax selection with
+// per-workgroup online-softmax partials; `counter` is zero on entry.
+constexpr int kGreedyMaxBlocks = 4096;
+size_t greedy_partials_bytes();
+dyna_status launch_logits_greedy(const RowdotArgs& lg, const SelectArgs& sa, void* partials,
+                                 int32_t* counter, hipStream_t s);
 
 // Global options (dyna_set_option).
 int option_logits_path();

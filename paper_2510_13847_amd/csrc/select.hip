@@ -15,167 +15,16 @@
 //                        restricted draft q_S (Sec. 5), split over 2048-slot
 //                        segments so long rows (the dense baseline) spread
 //                        over many workgroups.
-#include "dyna_device.h"
+#include "topk.h"
+#include "select_row.h"
 
 namespace dyna {
 namespace {
 
-constexpr int kNT = 256;
-
 // ------------------------------------------------------------------ top-k
-// One workgroup per context.  Scores (and, for the shortlist, the CSR
-// offsets) are staged in LDS in one round trip.  Two 8-bit radix passes over
-// the ordered score codes find the 16-bit prefix P of the k-th largest score:
-// every code above P is selected, and the few codes sharing P are ranked
-// exactly by (score desc, id asc) to fill the remaining places.  The k keys
-// are then put in rank order and in ascending id order; with `plan` set (one
-// context) the workgroup also writes the gathered-head work plan, so no
-// separate plan launch is needed for a single context.
-__device__ __forceinline__ void radix_digit(const int* hist, int krem, uint32_t prefix, int shift,
-                                            uint32_t* sh_prefix, int* sh_krem) {
-    // wave 0: lane l holds digits 255-4l .. 252-4l (descending)
-    const int l = lane_id();
-    int c[4], sum = 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        c[q] = hist[255 - 4 * l - q];
-        sum += c[q];
-    }
-    const int inc = wave_inclusive_scan(sum);
-    const int exc = inc - sum;
-    if (exc < krem && krem <= inc) {
-        int acc = exc;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            if (acc + c[q] >= krem) {
-                *sh_prefix = prefix | ((uint32_t)(255 - 4 * l - q) << shift);
-                *sh_krem = krem - acc;
-                break;
-            }
-            acc += c[q];
-        }
-    }
-}
-
-__global__ __launch_bounds__(kNT) void topk_clusters_kernel(
-    const float* __restrict__ scores, int M, int k, int32_t* __restrict__ topk_ids,
-    float* __restrict__ topk_scores, const int32_t* __restrict__ offsets,
-    int32_t* __restrict__ sel_sorted, int32_t* __restrict__ sel_rowoff,
-    int32_t* __restrict__ row_len, Plan plan) {
+__global__ __launch_bounds__(kNT) void topk_clusters_kernel(TopkArgs A) {
     extern __shared__ unsigned char smem[];
-    float* sv = reinterpret_cast<float*>(smem);                       // [M] raw scores
-    int32_t* offs = reinterpret_cast<int32_t*>(sv + M);                // [M + 1]
-    uint64_t* sel = reinterpret_cast<uint64_t*>(smem + ((size_t)(2 * M + 1) * 4 + 7) / 8 * 8);  // [k]
-    uint64_t* cand = sel + k;                                          // [M] tie candidates
-    int32_t* sid = reinterpret_cast<int32_t*>(cand + M);               // [k] ids ascending
-    int32_t* ssize = sid + k;                                          // [k]
-    __shared__ int hist[256];
-    __shared__ int tmp[kNT / kWave + 1];
-    __shared__ uint32_t sh_prefix;
-    __shared__ int sh_krem, sh_nsel, sh_ncand;
-
-    const int b = blockIdx.x;
-    const float* s = scores + (int64_t)b * M;
-    for (int j = threadIdx.x; j < M; j += kNT) sv[j] = s[j];
-    if (sel_sorted != nullptr)
-        for (int j = threadIdx.x; j <= M; j += kNT) offs[j] = offsets[j];
-    hist[threadIdx.x] = 0;
-    if (threadIdx.x == 0) {
-        sh_nsel = 0;
-        sh_ncand = 0;
-    }
-    __syncthreads();
-
-    // pass 1: top byte
-    for (int j = threadIdx.x; j < M; j += kNT) atomicAdd(&hist[ord_f32(sv[j]) >> 24], 1);
-    __syncthreads();
-    if (threadIdx.x < kWave) radix_digit(hist, k, 0u, 24, &sh_prefix, &sh_krem);
-    __syncthreads();
-    const uint32_t p1 = sh_prefix;
-    hist[threadIdx.x] = 0;
-    __syncthreads();
-    // pass 2: second byte inside the chosen top byte
-    for (int j = threadIdx.x; j < M; j += kNT) {
-        const uint32_t o = ord_f32(sv[j]);
-        if ((o & 0xff000000u) == p1) atomicAdd(&hist[(o >> 16) & 255u], 1);
-    }
-    __syncthreads();
-    if (threadIdx.x < kWave) radix_digit(hist, sh_krem, p1, 16, &sh_prefix, &sh_krem);
-    __syncthreads();
-    const uint32_t P = sh_prefix >> 16;  // 16-bit prefix of the k-th largest code
-    const int need = sh_krem;             // places left for codes with prefix P
-
-    // codes above P are in; codes with prefix P are ranked below
-    for (int j = threadIdx.x; j < M; j += kNT) {
-        const uint32_t o = ord_f32(sv[j]);
-        const uint64_t key = (static_cast<uint64_t>(o) << 32) | (0xffffffffu - (uint32_t)j);
-        if ((o >> 16) > P) sel[atomicAdd(&sh_nsel, 1)] = key;
-        else if ((o >> 16) == P) cand[atomicAdd(&sh_ncand, 1)] = key;
-    }
-    __syncthreads();
-    const int nsel0 = sh_nsel, ncand = sh_ncand;
-    for (int c = threadIdx.x; c < ncand; c += kNT) {
-        const uint64_t key = cand[c];
-        int rank = 0;
-        for (int j = 0; j < ncand; ++j) rank += cand[j] > key;
-        if (rank < need) sel[nsel0 + rank] = key;
-    }
-    __syncthreads();
-
-    // rank order (score desc, id asc) and ascending-id order by counting
-    for (int i = threadIdx.x; i < k; i += kNT) {
-        const uint64_t key = sel[i];
-        const uint32_t id = key_id(key);
-        int rank = 0, idrank = 0;
-        for (int j = 0; j < k; ++j) {
-            const uint64_t o = sel[j];
-            rank += o > key;
-            idrank += key_id(o) < id;
-        }
-        topk_ids[(int64_t)b * k + rank] = (int32_t)id;
-        if (topk_scores) topk_scores[(int64_t)b * k + rank] = sv[id];
-        if (sel_sorted != nullptr) {
-            sid[idrank] = (int32_t)id;
-            ssize[idrank] = offs[id + 1] - offs[id];
-        }
-    }
-    if (sel_sorted == nullptr) return;
-    __syncthreads();
-
-    // shortlist: exclusive prefix of the sizes in ascending id order
-    const int per = (k + kNT - 1) / kNT;
-    const int i0 = min(k, (int)threadIdx.x * per);
-    const int i1 = min(k, i0 + per);
-    int local = 0, lchunks = 0;
-    for (int i = i0; i < i1; ++i) {
-        local += ssize[i];
-        lchunks += (ssize[i] + kTileRows - 1) / kTileRows;
-    }
-    int len, n_chunks = 0;
-    int run = block_exclusive_scan<kNT>(local, tmp, &len);
-    int crun = plan.hdr ? block_exclusive_scan<kNT>(lchunks, tmp, &n_chunks) : 0;
-    for (int i = i0; i < i1; ++i) {
-        const int m = sid[i];
-        sel_sorted[(int64_t)b * k + i] = m;
-        sel_rowoff[(int64_t)b * (k + 1) + i] = run;
-        if (plan.hdr) {
-            const int o = offs[m];
-            plan.list[i] = ListEntry{b, run - o};
-            for (int c = 0; c * kTileRows < ssize[i]; ++c)
-                plan.chunks[crun + c] =
-                    Chunk{o + c * kTileRows, min(kTileRows, ssize[i] - c * kTileRows), i, 1};
-            crun += (ssize[i] + kTileRows - 1) / kTileRows;
-        }
-        run += ssize[i];
-    }
-    if (threadIdx.x == 0) {
-        sel_rowoff[(int64_t)b * (k + 1) + k] = len;
-        row_len[b] = len;
-        if (plan.hdr) {
-            plan.hdr->n_chunks = n_chunks;
-            plan.hdr->n_entries = k;
-        }
-    }
+    topk_row(A, blockIdx.x, smem);
 }
 
 // ------------------------------------------------------------------ shortlist
@@ -315,91 +164,6 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 }
 
 // ------------------------------------------------------------------ select
-constexpr int kSeg = 2048;          // shortlist slots per partial workgroup
-constexpr int kPer = kSeg / kNT;    // 8 slots per thread
-constexpr int kRowMax = 32768;      // longest row the one-launch select takes
-
-struct SelectArgs {
-    const float* logits;
-    int64_t ld;
-    const int32_t* row_len;   // nullptr: every row has fixed_len
-    int32_t fixed_len;
-    const int32_t* sel_sorted;
-    const int32_t* sel_rowoff;
-    const int32_t* offsets;
-    const int32_t* perm;      // nullptr: vocabulary id = slot
-    const int32_t* slot_vid;  // optional [B][ld]: vocabulary id per slot
-    int32_t k;
-    int32_t k_t;
-    float inv_t;
-    const float* uniforms;
-    int32_t P;                // segments per row
-    // partials, [B][P][...]
-    uint64_t* pkeys;          // [B][P][k_t]
-    float* pmax;              // [B][P]
-    float* psum;              // [B][P]
-    int32_t* out_ids;
-    float* out_logprobs;
-    int32_t* out_sample;
-    float* out_sample_logprob;
-};
-
-__device__ __forceinline__ float canon(float z) { return z != z ? -__builtin_inff() : z; }
-
-// Vocabulary ids of the slots [j0, j0 + n) of row b, written into vid[].
-__device__ __forceinline__ void slot_vids(const SelectArgs& a, int b, int j0, int n, uint32_t* vid) {
-    if (a.slot_vid != nullptr) {
-        for (int q = 0; q < n; ++q) vid[q] = (uint32_t)a.slot_vid[(int64_t)b * a.ld + j0 + q];
-        return;
-    }
-    if (a.perm == nullptr) {
-        for (int q = 0; q < n; ++q) vid[q] = (uint32_t)(j0 + q);
-        return;
-    }
-    const int32_t* ro = a.sel_rowoff + (int64_t)b * (a.k + 1);
-    const int32_t* ss = a.sel_sorted + (int64_t)b * a.k;
-    // largest ci with ro[ci] <= j0
-    int lo = 0, hi = a.k - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (ro[mid] <= j0) lo = mid; else hi = mid - 1;
-    }
-    int ci = lo;
-    int end = ro[ci + 1];
-    for (int q = 0; q < n; ++q) {
-        const int j = j0 + q;
-        while (j >= end) {
-            ++ci;
-            end = ro[ci + 1];
-        }
-        const int m = ss[ci];
-        vid[q] = (uint32_t)a.perm[a.offsets[m] + (j - ro[ci])];
-    }
-}
-
-// Block-wide selection of the k_t largest keys from per-thread lists sorted
-// descending (list[0] largest, 0 = empty).  Thread 0 receives them in out[].
-template <int L>
-__device__ void block_topk_rounds(uint64_t (&list)[L], int k_t, uint64_t* wmax /* LDS [2][4] */,
-                                  uint64_t* out /* LDS [k_t] */) {
-    const int lane = lane_id(), w = threadIdx.x / kWave;
-    for (int r = 0; r < k_t; ++r) {
-        const uint64_t m = wave_max_u64(list[0]);
-        if (lane == 0) wmax[(r & 1) * 4 + w] = m;
-        __syncthreads();
-        uint64_t best = wmax[(r & 1) * 4];
-#pragma unroll
-        for (int q = 1; q < kNT / kWave; ++q) best = max(best, wmax[(r & 1) * 4 + q]);
-        if (best != 0 && list[0] == best) {
-#pragma unroll
-            for (int q = 0; q < L - 1; ++q) list[q] = list[q + 1];
-            list[L - 1] = 0;
-        }
-        if (threadIdx.x == 0) out[r] = best;
-    }
-    __syncthreads();
-}
-
 __global__ __launch_bounds__(kNT) void select_partial_kernel(SelectArgs a) {
     __shared__ uint64_t wmax[8];
     __shared__ uint64_t top[DYNA_MAX_KT];
@@ -597,134 +361,9 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     }
 }
 
-// Whole-row selection in one workgroup (shortlist-sized rows, k_t <= KT).
-// Max, top-k_t and the softmax sum read the row with coalesced strided loads;
-// only the sampling walk uses contiguous per-thread ranges, so that the CDF
-// runs in shortlist order.  Vocabulary ids come from the gathered head's
-// per-slot ids when present, else from the shortlist's cluster table staged
-// in LDS.
-constexpr int kRowTable = 1024;  // clusters per row the LDS table holds
-
 template <int KT>
 __global__ __launch_bounds__(kNT) void select_row_kernel(SelectArgs a) {
-    __shared__ uint64_t wmax[8];
-    __shared__ uint64_t top[DYNA_MAX_KT];
-    __shared__ float red[2 * (kNT / kWave) + 1];
-    __shared__ float incl_s[kNT];
-    __shared__ int sh_pick;
-    __shared__ int32_t t_ro[kRowTable + 1];
-    __shared__ int32_t t_base[kRowTable];
-    const int b = blockIdx.x;
-    const int len = a.row_len ? a.row_len[b] : a.fixed_len;
-    const float* z = a.logits + (int64_t)b * a.ld;
-    const int32_t* sv = a.slot_vid ? a.slot_vid + (int64_t)b * a.ld : nullptr;
-    const bool table = sv == nullptr && a.perm != nullptr;
-    if (table) {  // slot -> layout row: rows of cluster ci start at t_base[ci] + slot
-        const int32_t* ro = a.sel_rowoff + (int64_t)b * (a.k + 1);
-        const int32_t* ss = a.sel_sorted + (int64_t)b * a.k;
-        for (int c = threadIdx.x; c <= a.k; c += kNT) {
-            t_ro[c] = ro[c];
-            if (c < a.k) t_base[c] = ss[c] >= 0 ? a.offsets[ss[c]] - ro[c] : 0;
-        }
-        __syncthreads();
-    }
-    auto vid_of = [&](int j) -> uint32_t {
-        if (sv != nullptr) return (uint32_t)sv[j];
-        if (a.perm == nullptr) return (uint32_t)j;
-        int lo = 0, hi = a.k - 1;  // largest ci with ro[ci] <= j
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (t_ro[mid] <= j) lo = mid; else hi = mid - 1;
-        }
-        return (uint32_t)a.perm[t_base[lo] + j];
-    };
-
-    uint64_t list[KT];
-#pragma unroll
-    for (int q = 0; q < KT; ++q) list[q] = 0;
-#pragma unroll 4
-    for (int j = threadIdx.x; j < len; j += kNT) {
-        const uint64_t key = sel_key(canon(z[j]), vid_of(j));
-        if (key > list[KT - 1]) {
-            list[KT - 1] = key;
-#pragma unroll
-            for (int q = KT - 1; q > 0; --q)
-                if (list[q] > list[q - 1]) {
-                    const uint64_t t = list[q];
-                    list[q] = list[q - 1];
-                    list[q - 1] = t;
-                }
-        }
-    }
-    block_topk_rounds<KT>(list, a.k_t, wmax, top);
-    const float mx = top[0] != 0 ? key_val(top[0]) : -__builtin_inff();
-    const bool sampling = a.uniforms != nullptr && a.out_sample != nullptr;
-
-    // softmax mass: strided when only top-k is asked, contiguous ranges
-    // (shortlist order) when a sample must be drawn from the same sums
-    const int E = (len + kNT - 1) / kNT;
-    const int j0 = min(len, (int)threadIdx.x * E);
-    const int j1 = min(len, j0 + E);
-    float tsum = 0.0f;
-    if (mx != -__builtin_inff()) {
-        if (sampling) {
-            for (int j = j0; j < j1; ++j) tsum += expf((canon(z[j]) - mx) * a.inv_t);
-        } else {
-#pragma unroll 4
-            for (int j = threadIdx.x; j < len; j += kNT) tsum += expf((canon(z[j]) - mx) * a.inv_t);
-        }
-    }
-    float total;
-    const float incl = block_inclusive_scan_f32<kNT>(tsum, red, &total);
-    const float log_total = logf(total);
-    if (a.out_ids != nullptr) {
-        for (int r = threadIdx.x; r < a.k_t; r += kNT) {
-            const uint64_t key = top[r];
-            a.out_ids[(int64_t)b * a.k_t + r] = key != 0 ? (int32_t)key_id(key) : -1;
-            if (a.out_logprobs)
-                a.out_logprobs[(int64_t)b * a.k_t + r] =
-                    key != 0 ? (key_val(key) - mx) * a.inv_t - log_total : -__builtin_inff();
-        }
-    }
-    if (!sampling) return;
-
-    incl_s[threadIdx.x] = incl;
-    if (threadIdx.x == 0) sh_pick = -1;
-    __syncthreads();
-    const float excl = threadIdx.x > 0 ? incl_s[threadIdx.x - 1] : 0.0f;
-    const float target = a.uniforms[b] * total;
-    if (tsum > 0.0f && excl <= target && target < incl) {
-        float acc = excl;
-        int pick = -1, last = -1;
-        for (int j = j0; j < j1; ++j) {
-            const float e = expf((canon(z[j]) - mx) * a.inv_t);
-            if (e > 0.0f) last = j;
-            acc += e;
-            if (e > 0.0f && acc > target) {
-                pick = j;
-                break;
-            }
-        }
-        atomicMax(&sh_pick, pick >= 0 ? pick : last);
-    }
-    __syncthreads();
-    if (sh_pick < 0 && tsum > 0.0f) {  // rounding: the last slot with mass
-        int last = -1;
-        for (int j = j0; j < j1; ++j)
-            if (expf((canon(z[j]) - mx) * a.inv_t) > 0.0f) last = j;
-        atomicMax(&sh_pick, last);
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const int j = sh_pick;
-        if (j < 0) {
-            a.out_sample[b] = -1;
-            if (a.out_sample_logprob) a.out_sample_logprob[b] = -__builtin_inff();
-        } else {
-            a.out_sample[b] = (int32_t)vid_of(j);
-            if (a.out_sample_logprob) a.out_sample_logprob[b] = (canon(z[j]) - mx) * a.inv_t - log_total;
-        }
-    }
+    select_row<KT>(a, blockIdx.x);
 }
 
 }  // namespace
@@ -733,8 +372,7 @@ dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int3
                                  int32_t* topk_ids, float* topk_scores, const int32_t* offsets,
                                  int32_t* sel_sorted, int32_t* sel_rowoff, int32_t* row_len,
                                  const Plan* plan, hipStream_t stream) {
-    const size_t lds = ((size_t)(2 * M + 1) * 4 + 7) / 8 * 8 + (size_t)(k + M) * sizeof(uint64_t) +
-                       (size_t)2 * k * sizeof(int32_t);
+    const size_t lds = topk_lds_bytes(M, k);
     if (lds > 65536) {
         static bool raised = false;
         if (!raised &&
@@ -745,8 +383,8 @@ dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int3
     }
     Plan p{};
     if (plan != nullptr && B == 1) p = *plan;
-    topk_clusters_kernel<<<B, kNT, lds, stream>>>(scores, M, k, topk_ids, topk_scores, offsets,
-                                                  sel_sorted, sel_rowoff, row_len, p);
+    TopkArgs A{scores, M, k, topk_ids, topk_scores, offsets, sel_sorted, sel_rowoff, row_len, p};
+    topk_clusters_kernel<<<B, kNT, lds, stream>>>(A);
     return check_launch("topk_clusters_kernel");
 }
 
@@ -775,15 +413,14 @@ size_t select_ws_bytes(int32_t B, int32_t max_len, int32_t k_t) {
 
 int32_t select_max_len() { return kSeg * kNT; }
 
-dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_len,
-                          int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
-                          const int32_t* sel_rowoff, const int32_t* offsets, const int32_t* perm,
-                          int32_t B, int32_t k, int32_t k_t, float temperature,
-                          const float* uniforms, int32_t* out_ids, float* out_logprobs,
-                          int32_t* out_sample, float* out_sample_logprob, void* ws,
-                          hipStream_t stream, const int32_t* slot_vid) {
+SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_len,
+                            int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
+                            const int32_t* sel_rowoff, const int32_t* offsets,
+                            const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
+                            float temperature, const float* uniforms, int32_t* out_ids,
+                            float* out_logprobs, int32_t* out_sample,
+                            float* out_sample_logprob, void* ws, const int32_t* slot_vid) {
     SelectArgs a;
-    a.slot_vid = slot_vid;
     a.logits = logits;
     a.ld = ld;
     a.row_len = row_len;
@@ -792,6 +429,7 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
     a.sel_rowoff = sel_rowoff;
     a.offsets = offsets;
     a.perm = perm;
+    a.slot_vid = slot_vid;
     a.k = k;
     a.k_t = k_t;
     a.inv_t = 1.0f / temperature;
@@ -807,8 +445,26 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
     a.out_logprobs = out_logprobs;
     a.out_sample = out_sample;
     a.out_sample_logprob = out_sample_logprob;
+    return a;
+}
+
+bool select_row_fits(int32_t max_len, bool fixed, int32_t k_t, int32_t k) {
+    return max_len <= (fixed ? kRowMax / 4 : kRowMax) && k_t <= 16 && (fixed || k <= kRowTable);
+}
+
+dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_len,
+                          int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
+                          const int32_t* sel_rowoff, const int32_t* offsets, const int32_t* perm,
+                          int32_t B, int32_t k, int32_t k_t, float temperature,
+                          const float* uniforms, int32_t* out_ids, float* out_logprobs,
+                          int32_t* out_sample, float* out_sample_logprob, void* ws,
+                          hipStream_t stream, const int32_t* slot_vid) {
+    const SelectArgs a = make_select_args(logits, ld, row_len, fixed_len, max_len, sel_sorted,
+                                          sel_rowoff, offsets, perm, B, k, k_t, temperature,
+                                          uniforms, out_ids, out_logprobs, out_sample,
+                                          out_sample_logprob, ws, slot_vid);
     // shortlist-sized rows: one workgroup per row, one launch
-    if (max_len <= (row_len ? kRowMax : kRowMax / 4) && k_t <= 16 && (perm == nullptr || k <= kRowTable)) {
+    if (select_row_fits(max_len, row_len == nullptr, k_t, perm == nullptr ? 0 : k)) {
         if (k_t == 1) select_row_kernel<1><<<B, kNT, 0, stream>>>(a);
         else select_row_kernel<16><<<B, kNT, 0, stream>>>(a);
         return check_launch("select_row_kernel");

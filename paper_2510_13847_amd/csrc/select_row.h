@@ -1,0 +1,201 @@
+// Draft selection over one context's shortlist logits (Algorithm 1:
+// log_softmax, TopK_{k_t}, remap2realid; Sec. 5: inverse-CDF sampling from
+// the restricted, renormalised draft q_S).
+#pragma once
+#include "dyna_device.h"
+
+namespace dyna {
+namespace {
+
+constexpr int kSeg = 2048;          // shortlist slots per partial workgroup
+constexpr int kPer = kSeg / kNT;    // 8 slots per thread
+constexpr int kRowMax = 32768;      // longest row the one-launch select takes
+
+
+__device__ __forceinline__ float canon(float z) { return z != z ? -__builtin_inff() : z; }
+
+// Vocabulary ids of the slots [j0, j0 + n) of row b, written into vid[].
+__device__ __forceinline__ void slot_vids(const SelectArgs& a, int b, int j0, int n, uint32_t* vid) {
+    if (a.slot_vid != nullptr) {
+        for (int q = 0; q < n; ++q) vid[q] = (uint32_t)a.slot_vid[(int64_t)b * a.ld + j0 + q];
+        return;
+    }
+    if (a.perm == nullptr) {
+        for (int q = 0; q < n; ++q) vid[q] = (uint32_t)(j0 + q);
+        return;
+    }
+    const int32_t* ro = a.sel_rowoff + (int64_t)b * (a.k + 1);
+    const int32_t* ss = a.sel_sorted + (int64_t)b * a.k;
+    // largest ci with ro[ci] <= j0
+    int lo = 0, hi = a.k - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (ro[mid] <= j0) lo = mid; else hi = mid - 1;
+    }
+    int ci = lo;
+    int end = ro[ci + 1];
+    for (int q = 0; q < n; ++q) {
+        const int j = j0 + q;
+        while (j >= end) {
+            ++ci;
+            end = ro[ci + 1];
+        }
+        const int m = ss[ci];
+        vid[q] = (uint32_t)a.perm[a.offsets[m] + (j - ro[ci])];
+    }
+}
+
+// Block-wide selection of the k_t largest keys from per-thread lists sorted
+// descending (list[0] largest, 0 = empty).  Thread 0 receives them in out[].
+template <int L>
+__device__ void block_topk_rounds(uint64_t (&list)[L], int k_t, uint64_t* wmax /* LDS [2][4] */,
+                                  uint64_t* out /* LDS [k_t] */) {
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    for (int r = 0; r < k_t; ++r) {
+        const uint64_t m = wave_max_u64(list[0]);
+        if (lane == 0) wmax[(r & 1) * 4 + w] = m;
+        __syncthreads();
+        uint64_t best = wmax[(r & 1) * 4];
+#pragma unroll
+        for (int q = 1; q < kNT / kWave; ++q) best = max(best, wmax[(r & 1) * 4 + q]);
+        if (best != 0 && list[0] == best) {
+#pragma unroll
+            for (int q = 0; q < L - 1; ++q) list[q] = list[q + 1];
+            list[L - 1] = 0;
+        }
+        if (threadIdx.x == 0) out[r] = best;
+    }
+    __syncthreads();
+}
+
+// Whole-row selection in one workgroup (shortlist-sized rows, k_t <= KT).
+// Max, top-k_t and the softmax sum read the row with coalesced strided loads;
+// only the sampling walk uses contiguous per-thread ranges, so that the CDF
+// runs in shortlist order.  Vocabulary ids come from the gathered head's
+// per-slot ids when present, else from the shortlist's cluster table staged
+// in LDS.
+constexpr int kRowTable = 1024;  // clusters per row the LDS table holds
+
+template <int KT>
+__device__ void select_row(const SelectArgs& a, int b) {
+    __shared__ uint64_t wmax[8];
+    __shared__ uint64_t top[DYNA_MAX_KT];
+    __shared__ float red[2 * (kNT / kWave) + 1];
+    __shared__ float incl_s[kNT];
+    __shared__ int sh_pick;
+    __shared__ int32_t t_ro[kRowTable + 1];
+    __shared__ int32_t t_base[kRowTable];
+    const int len = a.row_len ? a.row_len[b] : a.fixed_len;
+    const float* z = a.logits + (int64_t)b * a.ld;
+    const int32_t* sv = a.slot_vid ? a.slot_vid + (int64_t)b * a.ld : nullptr;
+    const bool table = sv == nullptr && a.perm != nullptr;
+    if (table) {  // slot -> layout row: rows of cluster ci start at t_base[ci] + slot
+        const int32_t* ro = a.sel_rowoff + (int64_t)b * (a.k + 1);
+        const int32_t* ss = a.sel_sorted + (int64_t)b * a.k;
+        for (int c = threadIdx.x; c <= a.k; c += kNT) {
+            t_ro[c] = ro[c];
+            if (c < a.k) t_base[c] = ss[c] >= 0 ? a.offsets[ss[c]] - ro[c] : 0;
+        }
+        __syncthreads();
+    }
+    auto vid_of = [&](int j) -> uint32_t {
+        if (sv != nullptr) return (uint32_t)sv[j];
+        if (a.perm == nullptr) return (uint32_t)j;
+        int lo = 0, hi = a.k - 1;  // largest ci with ro[ci] <= j
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (t_ro[mid] <= j) lo = mid; else hi = mid - 1;
+        }
+        return (uint32_t)a.perm[t_base[lo] + j];
+    };
+
+    uint64_t list[KT];
+#pragma unroll
+    for (int q = 0; q < KT; ++q) list[q] = 0;
+#pragma unroll 4
+    for (int j = threadIdx.x; j < len; j += kNT) {
+        const uint64_t key = sel_key(canon(z[j]), vid_of(j));
+        if (key > list[KT - 1]) {
+            list[KT - 1] = key;
+#pragma unroll
+            for (int q = KT - 1; q > 0; --q)
+                if (list[q] > list[q - 1]) {
+                    const uint64_t t = list[q];
+                    list[q] = list[q - 1];
+                    list[q - 1] = t;
+                }
+        }
+    }
+    block_topk_rounds<KT>(list, a.k_t, wmax, top);
+    const float mx = top[0] != 0 ? key_val(top[0]) : -__builtin_inff();
+    const bool sampling = a.uniforms != nullptr && a.out_sample != nullptr;
+
+    // softmax mass: strided when only top-k is asked, contiguous ranges
+    // (shortlist order) when a sample must be drawn from the same sums
+    const int E = (len + kNT - 1) / kNT;
+    const int j0 = min(len, (int)threadIdx.x * E);
+    const int j1 = min(len, j0 + E);
+    float tsum = 0.0f;
+    if (mx != -__builtin_inff()) {
+        if (sampling) {
+            for (int j = j0; j < j1; ++j) tsum += expf((canon(z[j]) - mx) * a.inv_t);
+        } else {
+#pragma unroll 4
+            for (int j = threadIdx.x; j < len; j += kNT) tsum += expf((canon(z[j]) - mx) * a.inv_t);
+        }
+    }
+    float total;
+    const float incl = block_inclusive_scan_f32<kNT>(tsum, red, &total);
+    const float log_total = logf(total);
+    if (a.out_ids != nullptr) {
+        for (int r = threadIdx.x; r < a.k_t; r += kNT) {
+            const uint64_t key = top[r];
+            a.out_ids[(int64_t)b * a.k_t + r] = key != 0 ? (int32_t)key_id(key) : -1;
+            if (a.out_logprobs)
+                a.out_logprobs[(int64_t)b * a.k_t + r] =
+                    key != 0 ? (key_val(key) - mx) * a.inv_t - log_total : -__builtin_inff();
+        }
+    }
+    if (!sampling) return;
+
+    incl_s[threadIdx.x] = incl;
+    if (threadIdx.x == 0) sh_pick = -1;
+    __syncthreads();
+    const float excl = threadIdx.x > 0 ? incl_s[threadIdx.x - 1] : 0.0f;
+    const float target = a.uniforms[b] * total;
+    if (tsum > 0.0f && excl <= target && target < incl) {
+        float acc = excl;
+        int pick = -1, last = -1;
+        for (int j = j0; j < j1; ++j) {
+            const float e = expf((canon(z[j]) - mx) * a.inv_t);
+            if (e > 0.0f) last = j;
+            acc += e;
+            if (e > 0.0f && acc > target) {
+                pick = j;
+                break;
+            }
+        }
+        atomicMax(&sh_pick, pick >= 0 ? pick : last);
+    }
+    __syncthreads();
+    if (sh_pick < 0 && tsum > 0.0f) {  // rounding: the last slot with mass
+        int last = -1;
+        for (int j = j0; j < j1; ++j)
+            if (expf((canon(z[j]) - mx) * a.inv_t) > 0.0f) last = j;
+        atomicMax(&sh_pick, last);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int j = sh_pick;
+        if (j < 0) {
+            a.out_sample[b] = -1;
+            if (a.out_sample_logprob) a.out_sample_logprob[b] = -__builtin_inff();
+        } else {
+            a.out_sample[b] = (int32_t)vid_of(j);
+            if (a.out_sample_logprob) a.out_sample_logprob[b] = (canon(z[j]) - mx) * a.inv_t - log_total;
+        }
+    }
+}
+
+}  // namespace
+}  // namespace dyna

@@ -405,3 +405,42 @@ def test_tiny_vocab_every_k():
                             uniforms=p.ud)
         torch.cuda.synchronize()
         _check_head(p, head)
+
+
+FUSED_CASES = [c for c in CASES if c.B == 1] + [
+    case("fused_big", V=20000, d=1024, M=100, H=64, k=12, B=1),
+    case("fused_f32", V=3000, d=128, M=24, H=16, k=5, B=1, dtype="f32"),
+]
+
+
+@pytest.mark.parametrize("temperature", [1.0, 0.6])
+@pytest.mark.parametrize("w", FUSED_CASES, ids=lambda w: w.name)
+def test_fused_greedy_matches_separate_kernels(w, temperature):
+    """A greedy one-context step folds the selection into the gathered head;
+    its token must equal the separate kernels' exactly and its log-probability
+    within rounding, call after call (the arrival counter resets itself)."""
+    p = Problem(w)
+    mode = D.SEL_ARGMAX
+    fused = D.DraftHead(p.R, p.L, 1, w.k, mode, 1, temperature, keep_logits=True)
+    sep = D.DraftHead(p.R, p.L, 1, w.k, mode, 1, temperature, keep_logits=True)
+    side = torch.cuda.Stream()
+    for it, rs in enumerate([None, None, side, None, None]):
+        x = W.contexts(w, "cpu", salt=it).to(DEV)
+        fused(x, x, route_stream=rs)
+        D.set_option(D.OPT_FUSED_B1, 1)
+        try:
+            sep(x, x, route_stream=rs)
+        finally:
+            D.set_option(D.OPT_FUSED_B1, 0)
+        torch.cuda.synchronize()
+        assert torch.equal(fused.clusters, sep.clusters)
+        assert torch.equal(fused.ids, sep.ids)
+        PC.assert_close(fused.logprobs.cpu().numpy(), sep.logprobs.cpu().numpy(), (2e-6, 2e-6), "lp")
+        vids = O.shortlist(fused.clusters[0].cpu().numpy(), p.offsets, p.perm)[3]
+        n = len(vids)
+        assert torch.equal(fused.logits[:, :n], sep.logits[:, :n])
+        # against the oracle on the GPU's own logits
+        z = fused.logits[0, :n].cpu().numpy().astype(np.float64)
+        r = O.draft_select(z, vids, 1, temperature)
+        assert int(fused.ids[0, 0]) == int(r["ids"][0])
+        PC.assert_close(fused.logprobs[0].cpu().numpy(), r["logprobs"], PC.LOGPROB_TOL, "lp oracle")
