@@ -23,6 +23,7 @@ std::atomic<int> g_router_path{0};
 std::atomic<int> g_kernel_timing{0};
 std::atomic<int> g_gemv_rows{0};
 std::atomic<int> g_fused_off{0};
+std::atomic<int> g_mfma_unroll{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -55,6 +56,11 @@ dyna_status check_launch(const char* what) {
 
 int option_logits_path() { return g_logits_path.load(); }
 
+LaunchEvents& pending_launch_events() {
+    static thread_local LaunchEvents ev;
+    return ev;
+}
+
 static hipEvent_t timing_event() {
     std::lock_guard<std::mutex> g(g_timing_mu);
     if (!g_timing_free.empty()) {
@@ -70,13 +76,24 @@ static hipEvent_t timing_event() {
 // Launch the gathered-head kernel, optionally between two timing events.
 template <typename F>
 static dyna_status timed(F launch, hipStream_t s) {
+    (void)s;
     if (!g_kernel_timing.load()) return launch();
     hipEvent_t e0 = timing_event(), e1 = timing_event();
-    if (!e0 || !e1 || hipEventRecord(e0, s) != hipSuccess)
-        return set_error(DYNA_ERR_HIP, "kernel timing: event record failed");
-    dyna_status st = launch();
-    if (st != DYNA_OK) return st;
-    if (hipEventRecord(e1, s) != hipSuccess) return set_error(DYNA_ERR_HIP, "kernel timing: event record failed");
+    if (!e0 || !e1) return set_error(DYNA_ERR_HIP, "kernel timing: event creation failed");
+    if (g_kernel_timing.load() == 2) {
+        // start/stop events handed to the gathered-head dispatch itself
+        pending_launch_events() = LaunchEvents{e0, e1};
+        dyna_status st = launch();
+        const bool taken = pending_launch_events().start == nullptr;
+        pending_launch_events() = LaunchEvents{};
+        if (st != DYNA_OK) return st;
+        if (!taken) return set_error(DYNA_ERR_HIP, "kernel timing: launch did not take the events");
+    } else {
+        if (hipEventRecord(e0, s) != hipSuccess) return set_error(DYNA_ERR_HIP, "kernel timing: event record failed");
+        dyna_status st = launch();
+        if (st != DYNA_OK) return st;
+        if (hipEventRecord(e1, s) != hipSuccess) return set_error(DYNA_ERR_HIP, "kernel timing: event record failed");
+    }
     std::lock_guard<std::mutex> g(g_timing_mu);
     g_timing_pairs.emplace_back(e0, e1);
     return DYNA_OK;
@@ -87,6 +104,7 @@ static dyna_status timed_rowdot(const RowdotArgs& a, int path, hipStream_t s) {
 }
 int option_router_path() { return g_router_path.load(); }
 int option_gemv_rows() { return g_gemv_rows.load(); }
+int option_mfma_unroll() { return g_mfma_unroll.load(); }
 
 // ------------------------------------------------------------------ workspace
 // One carving serves every hot entry point, so a single workspace can back a
@@ -109,7 +127,7 @@ struct Carve {
 };
 
 static int64_t max_chunks_for(const dyna_layout* L) {
-    return ((int64_t)L->V + kTileRows - 1) / kTileRows + L->M;
+    return ((int64_t)L->V + kChunkRows - 1) / kChunkRows + L->M;
 }
 
 // Chunks a step can produce: the union of the selected slabs holds at most
@@ -118,7 +136,7 @@ static int64_t max_chunks_for(const dyna_layout* L) {
 static int32_t chunk_bound(const dyna_layout* L, int32_t B, int32_t k) {
     const int64_t rows = std::min<int64_t>(L->V, (int64_t)B * L->cap_by_k[k]);
     const int64_t clusters = std::min<int64_t>(L->M, (int64_t)B * k);
-    return (int32_t)std::min<int64_t>(max_chunks_for(L), rows / kTileRows + clusters + 1);
+    return (int32_t)std::min<int64_t>(max_chunks_for(L), rows / kChunkRows + clusters + 1);
 }
 
 static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_t k, int32_t cap,
@@ -326,6 +344,11 @@ DYNA_API const char* dyna_status_string(dyna_status s) {
 DYNA_API const char* dyna_last_error(void) { return g_last_error; }
 
 DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
+    if (option == DYNA_OPT_MFMA_UNROLL) {
+        REQUIRE(value == 0 || value == 4 || value == 8 || value == 16, "MFMA unroll %d not in {0, 4, 8, 16}", value);
+        g_mfma_unroll.store(value);
+        return DYNA_OK;
+    }
     if (option == DYNA_OPT_FUSED_B1) {
         REQUIRE(value == 0 || value == 1, "fused option %d not in {0, 1}", value);
         g_fused_off.store(value);
@@ -339,7 +362,7 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
     REQUIRE(value >= 0 && value <= 2, "option value %d outside [0, 2]", value);
     if (option == DYNA_OPT_LOGITS_PATH) g_logits_path.store(value);
     else if (option == DYNA_OPT_ROUTER_PATH) g_router_path.store(value);
-    else if (option == DYNA_OPT_KERNEL_TIMING) g_kernel_timing.store(value ? 1 : 0);
+    else if (option == DYNA_OPT_KERNEL_TIMING) g_kernel_timing.store(value);
     else return set_error(DYNA_ERR_INVALID_ARG, "unknown option %d", option);
     return DYNA_OK;
 }
@@ -348,15 +371,19 @@ DYNA_API dyna_status dyna_kernel_timing(double* total_ms, int64_t* launches, int
     REQUIRE(total_ms != nullptr && launches != nullptr, "NULL argument");
     std::lock_guard<std::mutex> g(g_timing_mu);
     double sum = 0.0;
+    dyna_status st = DYNA_OK;
     for (auto& pr : g_timing_pairs) {
         float ms = 0.0f;
         if (hipEventSynchronize(pr.second) != hipSuccess ||
-            hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess)
-            return set_error(DYNA_ERR_HIP, "kernel timing: elapsed time query failed");
+            hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess) {
+            (void)hipGetLastError();
+            st = set_error(DYNA_ERR_HIP, "kernel timing: elapsed time query failed");
+            break;
+        }
         sum += ms;
     }
-    *total_ms = sum;
-    *launches = (int64_t)g_timing_pairs.size();
+    *total_ms = st == DYNA_OK ? sum : 0.0;
+    *launches = st == DYNA_OK ? (int64_t)g_timing_pairs.size() : 0;
     if (reset) {
         for (auto& pr : g_timing_pairs) {
             g_timing_free.push_back(pr.first);
@@ -364,7 +391,7 @@ DYNA_API dyna_status dyna_kernel_timing(double* total_ms, int64_t* launches, int
         }
         g_timing_pairs.clear();
     }
-    return DYNA_OK;
+    return st;
 }
 
 DYNA_API size_t dyna_layout_workspace_bytes(int32_t V, int32_t M) {

@@ -1,6 +1,7 @@
 // Internal declarations shared by the libdynahead translation units.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <stddef.h>
@@ -10,17 +11,18 @@
 namespace dyna {
 
 constexpr int kWave = 64;
-constexpr int kTileRows = 16;     // layout rows per work chunk (one MFMA A tile)
+constexpr int kChunkRows = 64;    // layout rows per work chunk of the gathered head
+constexpr int kMfmaRows = 16;     // rows of one MFMA A tile (a chunk holds 4)
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-// A work chunk of the gathered head: up to kTileRows consecutive layout rows
+// A work chunk of the gathered head: up to kChunkRows consecutive layout rows
 // of one cluster and the list of contexts that selected that cluster.
 struct Chunk {
     int32_t r0;        // first layout row
-    int32_t nrows;     // rows in this chunk (1..kTileRows)
+    int32_t nrows;     // rows in this chunk (1..kChunkRows)
     int32_t list_off;  // first entry of the cluster's context list
     int32_t list_cnt;  // number of contexts that selected the cluster
 };
@@ -47,6 +49,26 @@ struct Plan {
     int32_t max_chunks;
     int32_t max_entries;
 };
+
+// Events for the next gathered-head launch on this host thread (kernel
+// timing): stamped by the dispatch itself, so they bracket the kernel only.
+struct LaunchEvents {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+LaunchEvents& pending_launch_events();
+
+template <typename K, typename... Args>
+void launch_timed_kernel(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t stream,
+                         Args... args) {
+    LaunchEvents& ev = pending_launch_events();
+    if (ev.start != nullptr) {
+        hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ev.start, ev.stop, 0u, args...);
+        ev = LaunchEvents{};
+    } else {
+        kernel<<<grid, block, shmem, stream>>>(args...);
+    }
+}
 
 // Launch error -> status with a message.
 dyna_status set_error(dyna_status s, const char* fmt, ...);
@@ -178,5 +200,6 @@ dyna_status launch_logits_greedy(const RowdotArgs& lg, const SelectArgs& sa, voi
 int option_logits_path();
 int option_router_path();
 int option_gemv_rows();
+int option_mfma_unroll();
 
 }  // namespace dyna

@@ -59,7 +59,7 @@ __global__ __launch_bounds__(kThreads) void logits_greedy_kernel(RowdotArgs lg, 
     __shared__ uint64_t w_best[kWavesPerBlock];
     __shared__ float w_m[kWavesPerBlock], w_s[kWavesPerBlock];
     __shared__ int last;
-    const int64_t n_items = (int64_t)lg.plan.hdr->n_chunks * (kTileRows / R);
+    const int64_t n_items = (int64_t)lg.plan.hdr->n_chunks * (kChunkRows / R);
     // workgroups whose first wave has an item take part (at least workgroup 0)
     const int64_t n_part = std::max<int64_t>(
         1, std::min<int64_t>(gridDim.x, (n_items + kWavesPerBlock - 1) / kWavesPerBlock));
@@ -135,11 +135,11 @@ __global__ __launch_bounds__(kThreads) void logits_greedy_kernel(RowdotArgs lg, 
 template <typename WT, typename VT, int NB, int R>
 dyna_status launch_lg_r(const RowdotArgs& lg, const SelectArgs& sa, void* part, int32_t* counter,
                         hipStream_t s) {
-    const int64_t items = (int64_t)lg.max_chunks_bound * (kTileRows / R);
+    const int64_t items = (int64_t)lg.max_chunks_bound * (kChunkRows / R);
     const unsigned grid = (unsigned)std::max<int64_t>(
         1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock, kGreedyGrid));
-    logits_greedy_kernel<WT, VT, NB, R><<<grid, kThreads, 0, s>>>(
-        lg, sa, static_cast<GreedyPartial*>(part), counter);
+    launch_timed_kernel(logits_greedy_kernel<WT, VT, NB, R>, dim3(grid), dim3(kThreads), 0, s, lg, sa,
+                        static_cast<GreedyPartial*>(part), counter);
     return check_launch("logits_greedy_kernel");
 }
 

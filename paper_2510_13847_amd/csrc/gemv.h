@@ -61,8 +61,8 @@ struct StoreEpi {
 
 template <typename WT, typename VT, int NB, bool PLAN, int R, bool SINGLE, typename Epi = StoreEpi<PLAN>>
 __device__ __forceinline__ void gemv_rows(const RowdotArgs& a, Epi& epi) {
-    static_assert(kTileRows % R == 0, "row groups must tile a chunk");
-    constexpr int kGroups = kTileRows / R;  // row groups per plan chunk
+    static_assert(kChunkRows % R == 0, "row groups must tile a chunk");
+    constexpr int kGroups = kChunkRows / R;  // row groups per plan chunk
     const int lane = lane_id();
     const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
     const WT* __restrict__ W = static_cast<const WT*>(a.W);

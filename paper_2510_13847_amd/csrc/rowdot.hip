@@ -57,51 +57,61 @@ __device__ __forceinline__ void split8(const float* p, u32x4& hi, u32x4& lo) {
     }
 }
 
-template <int G, bool VF32, bool PLAN, int KSPLIT, int U>
-__global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
-    static_assert(KSPLIT == 1 || KSPLIT == kWavesPerBlock, "K split is per wave of a block");
-    __shared__ float red[KSPLIT > 1 ? (KSPLIT - 1) * G * 4 * kWave : 1];
+// One item = T tiles of 16 W rows (T * 16 consecutive rows) against the
+// contexts of the item, G groups of 16 contexts at a time: every B-operand
+// load feeds T MFMAs and every A-operand load feeds G.  KS > 1 splits the
+// k steps over the KS waves of a block (reduced through LDS in a fixed
+// order); KS = 1 lets every wave take its own items.  U k-steps are loaded
+// before their MFMAs are issued.
+template <int T, int G, bool VF32, bool PLAN, int KS, int U>
+__global__ __launch_bounds__(KS > 1 ? KS * kWave : kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
+    constexpr int NW = KS > 1 ? KS : kWavesPerBlock;  // waves per block
+    constexpr int kItemRows = T * kMfmaRows;
+    __shared__ float red[KS > 1 ? (KS - 1) * T * G * 4 * kWave : 1];
     if (a.zero_words != nullptr && blockIdx.x == 0 && (int)threadIdx.x < a.n_zero_words)
         a.zero_words[threadIdx.x] = 0;
     const int lane = lane_id();
     const int wv = threadIdx.x / kWave;
-    const int col = lane & 15;   // A row inside the tile, and B / D column
+    const int col = lane & 15;   // A row inside a tile, and B / D column
     const int kq = lane >> 4;    // 8-element slice of each 32-wide k step
     const int K = a.K;
     const int nsteps = (K + 31) / 32;
     const uint16_t* __restrict__ W = static_cast<const uint16_t*>(a.W);
 
-    const int64_t n_items =
-        PLAN ? (int64_t)a.plan.hdr->n_chunks : ((int64_t)a.n_rows + kTileRows - 1) / kTileRows;
-    const int64_t item0 = KSPLIT == 1 ? (int64_t)blockIdx.x * kWavesPerBlock + wv : blockIdx.x;
-    const int64_t istride = KSPLIT == 1 ? (int64_t)gridDim.x * kWavesPerBlock : gridDim.x;
-    const int s_begin = KSPLIT == 1 ? 0 : (wv * nsteps) / KSPLIT;
-    const int s_end = KSPLIT == 1 ? nsteps : ((wv + 1) * nsteps) / KSPLIT;
+    // plan mode: a chunk of up to 64 rows gives 64 / kItemRows wave items
+    constexpr int kSub = kChunkRows / kItemRows;
+    const int64_t n_items = PLAN ? (int64_t)a.plan.hdr->n_chunks * kSub
+                                 : ((int64_t)a.n_rows + kItemRows - 1) / kItemRows;
+    const int64_t item0 = KS == 1 ? (int64_t)blockIdx.x * NW + wv : blockIdx.x;
+    const int64_t istride = KS == 1 ? (int64_t)gridDim.x * NW : gridDim.x;
+    const int s_begin = KS == 1 ? 0 : (wv * nsteps) / KS;
+    const int s_end = KS == 1 ? nsteps : ((wv + 1) * nsteps) / KS;
 
     for (int64_t it = item0; it < n_items; it += istride) {
         int r0, nrows, lcnt;
         const ListEntry* list = nullptr;
         if constexpr (PLAN) {
-            const Chunk c = a.plan.chunks[it];
-            r0 = c.r0;
-            nrows = c.nrows;
+            const Chunk c = a.plan.chunks[it / kSub];
+            const int sub = (int)(it % kSub) * kItemRows;
+            if (sub >= c.nrows) continue;  // wave-uniform
+            r0 = c.r0 + sub;
+            nrows = min(kItemRows, c.nrows - sub);
             lcnt = c.list_cnt;
             list = a.plan.list + c.list_off;
         } else {
-            r0 = (int)(it * kTileRows);
-            nrows = min(kTileRows, a.n_rows - r0);
+            r0 = (int)(it * kItemRows);
+            nrows = min(kItemRows, a.n_rows - r0);
             lcnt = a.B;
         }
-        const bool rvalid = col < nrows;
-        const uint16_t* wrow = W + (int64_t)(r0 + (rvalid ? col : 0)) * K + kq * 8;
-        int32_t pv[4] = {0, 0, 0, 0};
-        if constexpr (PLAN) {
-            if (a.vid_out) {
+        // rows past nrows (and contexts past lcnt) read a valid row whose
+        // results are never stored, so every load below is unconditional
+        const uint16_t* wrow[T];
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (kq * 4 + r < nrows) pv[r] = a.perm[r0 + kq * 4 + r];
-            }
+        for (int t = 0; t < T; ++t) {
+            const bool rvalid = t * kMfmaRows + col < nrows;
+            wrow[t] = W + (int64_t)(r0 + (rvalid ? t * kMfmaRows + col : 0)) * K;
         }
+        const int tiles = (nrows + kMfmaRows - 1) / kMfmaRows;  // wave-uniform
 
         for (int gb = 0; gb < lcnt; gb += 16 * G) {
             int cb[G], cbase[G];
@@ -111,7 +121,7 @@ __global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
                 const int e = gb + g * 16 + col;
                 cvalid[g] = e < lcnt;
                 if constexpr (PLAN) {
-                    const ListEntry le = cvalid[g] ? list[e] : ListEntry{0, 0};
+                    const ListEntry le = list[cvalid[g] ? e : 0];
                     cb[g] = le.b;
                     cbase[g] = le.slot_base;
                 } else {
@@ -119,29 +129,38 @@ __global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
                     cbase[g] = 0;
                 }
             }
-            f32x4 acc[G];
+            f32x4 acc[T][G];
 #pragma unroll
-            for (int g = 0; g < G; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int t = 0; t < T; ++t)
+#pragma unroll
+                for (int g = 0; g < G; ++g) acc[t][g] = f32x4{0.f, 0.f, 0.f, 0.f};
 
             for (int s = s_begin; s < s_end; s += U) {
-                u32x4 A[U];
+                u32x4 A[U][T];
                 u32x4 Bh[U][G];
-                u32x4 Bl[U][G];
+                u32x4 Bl[U][VF32 ? G : 1];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
+                    // k steps past the range (or the k tail) load element 0 and
+                    // are zeroed, so they add nothing
                     const int k = (s + u) * 32 + kq * 8;
                     const bool kv = (s + u) < s_end && k < K;
-                    A[u] = (rvalid && kv)
-                               ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow + (s + u) * 32))
-                               : u32x4{0u, 0u, 0u, 0u};
+                    const int ko = kv ? k : 0;
+#pragma unroll
+                    for (int t = 0; t < T; ++t) {
+                        const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow[t] + ko));
+                        A[u][t] = kv ? x : u32x4{0u, 0u, 0u, 0u};
+                    }
 #pragma unroll
                     for (int g = 0; g < G; ++g) {
+                        // context columns are often sparse (a few contexts per
+                        // cluster): only valid columns load
                         Bh[u][g] = u32x4{0u, 0u, 0u, 0u};
-                        Bl[u][g] = u32x4{0u, 0u, 0u, 0u};
+                        if constexpr (VF32) Bl[u][g] = u32x4{0u, 0u, 0u, 0u};
                         if (cvalid[g] && kv) {
                             if constexpr (VF32) {
-                                split8(static_cast<const float*>(a.v) + (int64_t)cb[g] * K + k,
-                                       Bh[u][g], Bl[u][g]);
+                                split8(static_cast<const float*>(a.v) + (int64_t)cb[g] * K + k, Bh[u][g],
+                                       Bl[u][g]);
                             } else {
                                 Bh[u][g] = *reinterpret_cast<const u32x4*>(
                                     static_cast<const uint16_t*>(a.v) + (int64_t)cb[g] * K + k);
@@ -150,37 +169,43 @@ __global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
                     }
                 }
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
+                for (int u = 0; u < U; ++u)
 #pragma unroll
-                    for (int g = 0; g < G; ++g) {
-                        if (gb + g * 16 < lcnt) {  // wave-uniform
-                            acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                as_bf16x8(A[u]), as_bf16x8(Bh[u][g]), acc[g], 0, 0, 0);
+                    for (int t = 0; t < T; ++t) {
+                        if (t >= tiles) continue;  // wave-uniform
+#pragma unroll
+                        for (int g = 0; g < G; ++g) {
+                            if (gb + g * 16 >= lcnt) continue;  // wave-uniform
+                            acc[t][g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                as_bf16x8(A[u][t]), as_bf16x8(Bh[u][g]), acc[t][g], 0, 0, 0);
                             if constexpr (VF32)
-                                acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                    as_bf16x8(A[u]), as_bf16x8(Bl[u][g]), acc[g], 0, 0, 0);
+                                acc[t][g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    as_bf16x8(A[u][t]), as_bf16x8(Bl[u][g]), acc[t][g], 0, 0, 0);
                         }
                     }
-                }
             }
 
-            if constexpr (KSPLIT > 1) {
+            if constexpr (KS > 1) {
                 if (wv > 0) {
 #pragma unroll
-                    for (int g = 0; g < G; ++g)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            red[(((wv - 1) * G + g) * 4 + r) * kWave + lane] = acc[g][r];
-                }
-                __syncthreads();
-                if (wv == 0) {
-#pragma unroll
-                    for (int w = 1; w < KSPLIT; ++w)
+                    for (int t = 0; t < T; ++t)
 #pragma unroll
                         for (int g = 0; g < G; ++g)
 #pragma unroll
                             for (int r = 0; r < 4; ++r)
-                                acc[g][r] += red[(((w - 1) * G + g) * 4 + r) * kWave + lane];
+                                red[((((wv - 1) * T + t) * G + g) * 4 + r) * kWave + lane] = acc[t][g][r];
+                }
+                __syncthreads();
+                if (wv == 0) {
+#pragma unroll
+                    for (int w = 1; w < KS; ++w)
+#pragma unroll
+                        for (int t = 0; t < T; ++t)
+#pragma unroll
+                            for (int g = 0; g < G; ++g)
+#pragma unroll
+                                for (int r = 0; r < 4; ++r)
+                                    acc[t][g][r] += red[((((w - 1) * T + t) * G + g) * 4 + r) * kWave + lane];
                 }
                 __syncthreads();
                 if (wv != 0) continue;
@@ -191,16 +216,18 @@ __global__ __launch_bounds__(kThreads) void rowdot_mfma_kernel(RowdotArgs a) {
                 if (!cvalid[g]) continue;
                 float* o = a.out + (int64_t)cb[g] * a.ld + cbase[g] + r0;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int i = kq * 4 + r;
-                    if (i < nrows) {
-                        const float bias = a.bias ? a.bias[r0 + i] : 0.0f;
-                        o[i] = apply_act(acc[g][r] + bias, a.act);
-                        if constexpr (PLAN) {
-                            if (a.vid_out) a.vid_out[(o - a.out) + i] = pv[r];
+                for (int t = 0; t < T; ++t)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int i = t * kMfmaRows + kq * 4 + r;
+                        if (i < nrows) {
+                            const float bias = a.bias ? a.bias[r0 + i] : 0.0f;
+                            o[i] = apply_act(acc[t][g][r] + bias, a.act);
+                            if constexpr (PLAN) {
+                                if (a.vid_out) a.vid_out[(o - a.out) + i] = a.perm[r0 + i];
+                            }
                         }
                     }
-                }
             }
         }
     }
@@ -217,14 +244,16 @@ constexpr int gemv_max_rows() {
 
 template <typename WT, typename VT, bool PLAN, int NB, int R>
 dyna_status launch_gemv_r(const RowdotArgs& a, bool single, hipStream_t stream) {
-    const int64_t items = PLAN ? (int64_t)a.max_chunks_bound * (kTileRows / R)
+    const int64_t items = PLAN ? (int64_t)a.max_chunks_bound * (kChunkRows / R)
                                : ((int64_t)a.n_rows + R - 1) / R;
     const int64_t blocks = std::max<int64_t>(
         1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock, 4096));
     if (single)
-        rowdot_gemv_kernel<WT, VT, NB, PLAN, R, true><<<(unsigned)blocks, kThreads, 0, stream>>>(a);
+        launch_timed_kernel(rowdot_gemv_kernel<WT, VT, NB, PLAN, R, true>, dim3((unsigned)blocks),
+                            dim3(kThreads), 0, stream, a);
     else
-        rowdot_gemv_kernel<WT, VT, NB, PLAN, R, false><<<(unsigned)blocks, kThreads, 0, stream>>>(a);
+        launch_timed_kernel(rowdot_gemv_kernel<WT, VT, NB, PLAN, R, false>, dim3((unsigned)blocks),
+                            dim3(kThreads), 0, stream, a);
     return check_launch("rowdot_gemv_kernel");
 }
 
@@ -266,27 +295,34 @@ dyna_status launch_gemv(const RowdotArgs& a, hipStream_t stream) {
     return launch_gemv_nb<float, float, PLAN>(a, nb, single, rows_opt, stream);
 }
 
-template <int G, bool VF32, bool PLAN, int KSPLIT, int U>
+template <int T, int G, bool VF32, bool PLAN, int KS, int U>
 dyna_status launch_mfma_t(const RowdotArgs& a, hipStream_t stream) {
-    const int64_t items = PLAN ? (int64_t)a.max_chunks_bound
-                               : ((int64_t)a.n_rows + kTileRows - 1) / kTileRows;
-    const int64_t per_block = KSPLIT == 1 ? kWavesPerBlock : 1;
+    constexpr int kItemRows = T * kMfmaRows;
+    const int64_t items = PLAN ? (int64_t)a.max_chunks_bound * (kChunkRows / kItemRows)
+                               : ((int64_t)a.n_rows + kItemRows - 1) / kItemRows;
+    const int64_t per_block = KS == 1 ? kWavesPerBlock : 1;
     const int64_t blocks =
         std::max<int64_t>(1, std::min<int64_t>((items + per_block - 1) / per_block, resident_blocks()));
-    rowdot_mfma_kernel<G, VF32, PLAN, KSPLIT, U><<<(unsigned)blocks, kThreads, 0, stream>>>(a);
+    launch_timed_kernel(rowdot_mfma_kernel<T, G, VF32, PLAN, KS, U>, dim3((unsigned)blocks),
+                        dim3(KS > 1 ? KS * kWave : kThreads), 0, stream, a);
     return check_launch("rowdot_mfma_kernel");
 }
 
 template <bool VF32, bool PLAN>
 dyna_status launch_mfma(const RowdotArgs& a, hipStream_t stream) {
-    if (PLAN) return launch_mfma_t<1, VF32, PLAN, 1, 8>(a, stream);
-    // dense: all contexts share every row; split K over the 4 waves of a
-    // block so that a small W still spreads over many CUs
+    if (PLAN) {
+        // one 16-row tile per wave, U k steps loaded ahead
+        if (option_mfma_unroll() == 4) return launch_mfma_t<1, 1, VF32, PLAN, 1, 4>(a, stream);
+        if (option_mfma_unroll() == 16) return launch_mfma_t<1, 1, VF32, PLAN, 1, 16>(a, stream);
+        return launch_mfma_t<1, 1, VF32, PLAN, 1, 8>(a, stream);
+    }
+    // dense (router layers, dense head): all contexts share every row; the
+    // k steps of a 16-row tile are split over the 8 waves of a block
     const int groups = (a.B + 15) / 16;
-    if (groups <= 1) return launch_mfma_t<1, VF32, PLAN, kWavesPerBlock, 4>(a, stream);
-    if (groups <= 2) return launch_mfma_t<2, VF32, PLAN, kWavesPerBlock, 2>(a, stream);
-    if (groups <= 4) return launch_mfma_t<4, VF32, PLAN, kWavesPerBlock, 1>(a, stream);
-    return launch_mfma_t<8, VF32, PLAN, kWavesPerBlock, 1>(a, stream);
+    if (groups <= 1) return launch_mfma_t<1, 1, VF32, PLAN, 8, 4>(a, stream);
+    if (groups <= 2) return launch_mfma_t<1, 2, VF32, PLAN, 8, 4>(a, stream);
+    if (groups <= 4) return launch_mfma_t<1, 4, VF32, PLAN, 8, 4>(a, stream);
+    return launch_mfma_t<1, 8, VF32, PLAN, 8, 2>(a, stream);
 }
 
 }  // namespace

@@ -130,7 +130,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     int lc = 0, lch = 0;
     for (int m = m0; m < m1; ++m) {
         lc += cnt[m];
-        if (cnt[m] > 0) lch += (offsets[m + 1] - offsets[m] + kTileRows - 1) / kTileRows;
+        if (cnt[m] > 0) lch += (offsets[m + 1] - offsets[m] + kChunkRows - 1) / kChunkRows;
     }
     int n_entries, n_chunks;
     int rl = block_exclusive_scan<kPlanThreads>(lc, tmp, &n_entries);
@@ -141,10 +141,10 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         rl += cnt[m];
         if (cnt[m] == 0) continue;
         const int o = offsets[m], n = offsets[m + 1] - o;
-        for (int c = 0; c * kTileRows < n; ++c)
+        for (int c = 0; c * kChunkRows < n; ++c)
             plan.chunks[rc + c] =
-                Chunk{o + c * kTileRows, min(kTileRows, n - c * kTileRows), loff[m], cnt[m]};
-        rc += (n + kTileRows - 1) / kTileRows;
+                Chunk{o + c * kChunkRows, min(kChunkRows, n - c * kChunkRows), loff[m], cnt[m]};
+        rc += (n + kChunkRows - 1) / kChunkRows;
     }
     __syncthreads();
     for (int m = threadIdx.x; m < M; m += kPlanThreads) cnt[m] = 0;

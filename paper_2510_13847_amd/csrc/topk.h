@@ -145,7 +145,7 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
     int local = 0, lchunks = 0;
     for (int i = i0; i < i1; ++i) {
         local += ssize[i];
-        lchunks += (ssize[i] + kTileRows - 1) / kTileRows;
+        lchunks += (ssize[i] + kChunkRows - 1) / kChunkRows;
     }
     int len, n_chunks = 0;
     int run = block_exclusive_scan<kNT>(local, tmp, &len);
@@ -157,10 +157,10 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
         if (plan.hdr) {
             const int o = offs[m];
             plan.list[i] = ListEntry{b, run - o};
-            for (int c = 0; c * kTileRows < ssize[i]; ++c)
+            for (int c = 0; c * kChunkRows < ssize[i]; ++c)
                 plan.chunks[crun + c] =
-                    Chunk{o + c * kTileRows, min(kTileRows, ssize[i] - c * kTileRows), i, 1};
-            crun += (ssize[i] + kTileRows - 1) / kTileRows;
+                    Chunk{o + c * kChunkRows, min(kChunkRows, ssize[i] - c * kChunkRows), i, 1};
+            crun += (ssize[i] + kChunkRows - 1) / kChunkRows;
         }
         run += ssize[i];
     }
