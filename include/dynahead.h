@@ -236,7 +236,9 @@ dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_rows, int32
 /* ------------------------------------------------------------------ */
 
 /* Kernel-path override for tests and measurement:
- * DYNA_OPT_LOGITS_PATH: 0 automatic, 1 wave-per-row GEMV, 2 MFMA tiles.
+ * DYNA_OPT_LOGITS_PATH: 0 automatic, 1 wave-per-row GEMV, 2 MFMA tiles with
+ *   the slab rows staged through LDS (bf16 weights and contexts; other types
+ *   fall back to 3), 3 MFMA tiles loaded straight from HBM.
  * DYNA_OPT_ROUTER_PATH: 0 automatic, 1 GEMV, 2 MFMA tiles.
  * DYNA_OPT_KERNEL_TIMING: 1 brackets every launch of the gathered-head
  *   (logits) kernel with two (default) events recorded on the stream it runs
@@ -244,15 +246,19 @@ dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_rows, int32
  *   0 stops.
  * DYNA_OPT_GEMV_ROWS: rows each wave of the GEMV kernel keeps in flight:
  *   0 automatic, else 1, 2 or 4 (capped by the register budget).
- * DYNA_OPT_FUSED_B1: 0 (default) lets dyna_draft_head run a one-context step
- *   as three launches (router layer 1; layer 2 fused with top-k, shortlist
- *   and plan; gathered head fused with selection); 1 uses the separate
- *   kernels.  Both give bit-identical results.  Under kernel timing the
- *   fused gathered-head + selection launch is what is timed.
- * DYNA_OPT_MFMA_UNROLL: k steps the batched gathered-head MFMA kernel loads
- *   ahead: 0 automatic (8), 4, 8 or 16. */
+ * DYNA_OPT_FUSED_B1: 0 (default) lets dyna_draft_head run a one-context
+ *   greedy step as four launches (router layer 1; router layer 2; top-k with
+ *   shortlist and plan; gathered head fused with selection); 1 uses the
+ *   separate kernels.  Both give bit-identical results.  Under kernel timing
+ *   the fused gathered-head + selection launch is what is timed.
+ * DYNA_OPT_MFMA_UNROLL: k steps the direct-load MFMA kernel (path 3) loads
+ *   ahead: 0 automatic (8), 4, 8 or 16.
+ * DYNA_OPT_GATHER_CFG: shape of the LDS-staged MFMA kernel (path 2): 0
+ *   automatic, 1..6 fixed (waves per block, ring stages, k columns per
+ *   stage, context columns per pass). */
 enum { DYNA_OPT_LOGITS_PATH = 1, DYNA_OPT_ROUTER_PATH = 2, DYNA_OPT_KERNEL_TIMING = 3,
-       DYNA_OPT_GEMV_ROWS = 4, DYNA_OPT_FUSED_B1 = 5, DYNA_OPT_MFMA_UNROLL = 6 };
+       DYNA_OPT_GEMV_ROWS = 4, DYNA_OPT_FUSED_B1 = 5, DYNA_OPT_MFMA_UNROLL = 6,
+       DYNA_OPT_GATHER_CFG = 7 };
 dyna_status dyna_set_option(int32_t option, int32_t value);
 
 /* Waits for the events recorded under DYNA_OPT_KERNEL_TIMING and returns the

@@ -24,6 +24,7 @@ std::atomic<int> g_kernel_timing{0};
 std::atomic<int> g_gemv_rows{0};
 std::atomic<int> g_fused_off{0};
 std::atomic<int> g_mfma_unroll{0};
+std::atomic<int> g_gather_cfg{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -105,6 +106,7 @@ static dyna_status timed_rowdot(const RowdotArgs& a, int path, hipStream_t s) {
 int option_router_path() { return g_router_path.load(); }
 int option_gemv_rows() { return g_gemv_rows.load(); }
 int option_mfma_unroll() { return g_mfma_unroll.load(); }
+int option_gather_cfg() { return g_gather_cfg.load(); }
 
 // ------------------------------------------------------------------ workspace
 // One carving serves every hot entry point, so a single workspace can back a
@@ -349,6 +351,16 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         g_mfma_unroll.store(value);
         return DYNA_OK;
     }
+    if (option == DYNA_OPT_GATHER_CFG) {
+        REQUIRE(value >= 0 && value <= 6, "gather shape %d outside [0, 6]", value);
+        g_gather_cfg.store(value);
+        return DYNA_OK;
+    }
+    if (option == DYNA_OPT_LOGITS_PATH) {
+        REQUIRE(value >= 0 && value <= 3, "logits path %d outside [0, 3]", value);
+        g_logits_path.store(value);
+        return DYNA_OK;
+    }
     if (option == DYNA_OPT_FUSED_B1) {
         REQUIRE(value == 0 || value == 1, "fused option %d not in {0, 1}", value);
         g_fused_off.store(value);
@@ -360,8 +372,7 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         return DYNA_OK;
     }
     REQUIRE(value >= 0 && value <= 2, "option value %d outside [0, 2]", value);
-    if (option == DYNA_OPT_LOGITS_PATH) g_logits_path.store(value);
-    else if (option == DYNA_OPT_ROUTER_PATH) g_router_path.store(value);
+    if (option == DYNA_OPT_ROUTER_PATH) g_router_path.store(value);
     else if (option == DYNA_OPT_KERNEL_TIMING) g_kernel_timing.store(value);
     else return set_error(DYNA_ERR_INVALID_ARG, "unknown option %d", option);
     return DYNA_OK;
@@ -544,7 +555,7 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     int32_t* clusters = out_clusters ? out_clusters : c.topk_ids;
     float* logits = out_logits ? out_logits : c.logits;
     // one greedy context: the gathered head carries the selection (4 launches)
-    const bool fused = B == 1 && !g_fused_off.load() && option_logits_path() != 2 && k_t == 1 &&
+    const bool fused = B == 1 && !g_fused_off.load() && option_logits_path() <= 1 && k_t == 1 &&
                        !want_sample;
 
     // routing (the router's stream)

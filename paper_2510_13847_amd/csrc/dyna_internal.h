@@ -11,8 +11,10 @@
 namespace dyna {
 
 constexpr int kWave = 64;
-constexpr int kChunkRows = 64;    // layout rows per work chunk of the gathered head
-constexpr int kMfmaRows = 16;     // rows of one MFMA A tile (a chunk holds 4)
+constexpr int kMfmaRows = 16;     // rows of one MFMA A tile
+// Layout rows per work chunk of the gathered head: one MFMA tile, so every
+// chunk is a full work item of equal cost (partial only at a cluster's end).
+constexpr int kChunkRows = kMfmaRows;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -110,6 +112,11 @@ struct RowdotArgs {
 };
 dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);
 
+// gather.hip: plan mode with bf16 weights and contexts, slab rows staged
+// through LDS (MFMA tiles)
+bool gather_lds_eligible(const RowdotArgs& a);
+dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream);
+
 // Arguments of the per-context top-k (Sec. 4.2) and of the draft selection
 // (Algorithm 1), shared by the separate and the fused launches.
 struct TopkArgs {
@@ -201,5 +208,6 @@ int option_logits_path();
 int option_router_path();
 int option_gemv_rows();
 int option_mfma_unroll();
+int option_gather_cfg();
 
 }  // namespace dyna

@@ -1,0 +1,330 @@
+// Gathered head for several contexts on the matrix cores, with the slab rows
+// staged through LDS (Sec. 4.3: the shortlist logits of a batch are one
+// gathered GEMM over the selected cluster slabs; Algorithm 1, FUSED_INDEX_GEMM).
+//
+// Work unit: one plan chunk (up to 16 rows of one selected cluster: one MFMA
+// tile) against up to NC of the contexts that selected that cluster.  All
+// chunks cost the same, and waves take them in a fixed stride, so every wave
+// gets the same number of units (to one).  The tile rows
+// are the A operand of v_mfma_f32_16x16x32_bf16, the contexts its B columns.
+//
+// Why LDS: the MFMA operand layout puts 16 different rows in one register, so
+// loading A straight from HBM reads 64 bytes of each of 16 rows per wave
+// instruction, a pattern HBM serves far below its streaming rate.  Here each
+// wave instruction is a direct-to-LDS load (global_load_lds_dwordx4) of whole
+// 256- or 512-byte row pieces, and the MFMA operands are read back from LDS.
+// Each wave keeps a private ring of S stages (a stage = KB columns of the 16
+// tile rows plus the same KB columns of its context rows), so S - 1 stages of
+// loads are always in flight without holding any registers; the wave waits on
+// its own load counter only, never on a barrier.
+//
+// Every other memory read inside the loop (chunk descriptors, context lists,
+// the vocabulary ids of the tile rows) goes through the scalar unit, so the
+// vector-memory counter only ever holds the staged loads and the output
+// stores, and waiting on it never drains the ring.
+//
+// LDS layout of a stage: A [16 rows][KB/8 pieces of 16 B], then B [NC
+// contexts][KB/8 pieces].  Piece p of row r is stored at position p ^ r (the
+// writer picks which global piece each lane fetches), so the 16 lanes that
+// read one piece index from 16 rows hit 16 different bank groups.
+#include <atomic>
+
+#include "dyna_device.h"
+
+namespace dyna {
+namespace {
+
+template <typename T>
+using sptr = const __attribute__((address_space(4))) T*;  // read through the scalar unit
+typedef __attribute__((address_space(3))) void* lds_ptr;
+typedef __attribute__((address_space(1))) void* glb_ptr;
+
+// Wait until at most N vector-memory instructions of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// A work unit of one wave: plan chunk `it` and context group g (list entries
+// g * NC ..).
+struct Unit {
+    int64_t it;
+    int g;
+    int kb;        // k block of the next stage of this unit
+    int r0;        // first layout row of the tile
+    int nrows;     // valid tile rows (1..16)
+    int list_off;  // first context-list entry of the chunk
+    int lcnt;      // contexts that selected the chunk's cluster
+    bool valid;
+};
+
+static_assert(kChunkRows == kMfmaRows, "a plan chunk is one MFMA tile");
+
+// Move u to the first chunk at or after u.it (stride `stride`) with rows and contexts.
+__device__ __forceinline__ void find_tile(Unit& u, const Plan& plan, int64_t n_items, int64_t stride) {
+    sptr<int32_t> ch = (sptr<int32_t>)plan.chunks;
+    while (u.it < n_items) {
+        const int64_t c = u.it;
+        const int r0 = ch[4 * c + 0], nr = ch[4 * c + 1], lo = ch[4 * c + 2], lc = ch[4 * c + 3];
+        if (nr > 0 && lc > 0) {
+            u.r0 = r0;
+            u.nrows = min(kMfmaRows, nr);
+            u.list_off = lo;
+            u.lcnt = lc;
+            u.g = 0;
+            u.kb = 0;
+            u.valid = true;
+            return;
+        }
+        u.it += stride;
+    }
+    u.valid = false;
+}
+
+// Next stage of a unit: next k block, else next context group, else next tile.
+template <int NC>
+__device__ __forceinline__ bool advance(Unit& u, int nkb, const Plan& plan, int64_t n_items, int64_t stride) {
+    if (++u.kb < nkb) return false;
+    u.kb = 0;
+    if (++u.g * NC < u.lcnt) return true;  // same tile, next group
+    u.it += stride;
+    find_tile(u, plan, n_items, stride);
+    return true;
+}
+
+// Lane j of v becomes x (x and j uniform).  x passes through readfirstlane
+// so that the chain of selects cannot be folded back into a per-lane load.
+__device__ __forceinline__ int set_lane(int v, int x, int j) {
+    const int xs = __builtin_amdgcn_readfirstlane(x);
+    return lane_id() == j ? xs : v;
+}
+
+__device__ __forceinline__ int from_lane(int v, int src_lane) {
+    return __builtin_amdgcn_ds_bpermute(src_lane << 2, v);
+}
+
+// Context ids and slot bases of the unit's group, read through the scalar
+// unit and spread over lanes: lane j of (vb, vs) holds entry j of the group
+// (entries past the group repeat its first entry).  Lanes fetch the entry
+// they need with ds_bpermute, which leaves the vector-memory counter alone.
+template <int NC>
+__device__ __forceinline__ int group_entries(const Unit& u, const Plan& plan, int& vb, int& vs) {
+    sptr<int32_t> L = (sptr<int32_t>)plan.list + 2 * ((int64_t)u.list_off + (int64_t)u.g * NC);
+    const int n = min(NC, u.lcnt - u.g * NC);
+    const int b0 = L[0], s0 = L[1];
+    vb = b0;
+    vs = s0;
+#pragma unroll
+    for (int j = 1; j < NC; ++j) {
+        if (j < n) {
+            vb = set_lane(vb, L[2 * j], j);
+            vs = set_lane(vs, L[2 * j + 1], j);
+        }
+    }
+    return n;
+}
+
+// NW waves per block, S ring stages per wave, KB k-columns per stage, NC context columns.
+template <int NW, int S, int KB, int NC>
+__global__ __launch_bounds__(NW * kWave) void gather_lds_kernel(RowdotArgs a) {
+    constexpr int ROWB = KB * 2;         // bytes of one row per stage
+    constexpr int PIECES = ROWB / 16;    // 16-byte pieces per row per stage
+    constexpr int RPI = kWave / PIECES;  // rows per direct-to-LDS instruction
+    constexpr int NA = kMfmaRows / RPI;  // A instructions per stage
+    constexpr int NBI = (NC + RPI - 1) / RPI;  // B instructions per stage (at most)
+    constexpr int A_BYTES = kMfmaRows * ROWB;
+    constexpr int STAGE = A_BYTES + NBI * RPI * ROWB;
+    constexpr int STEPS = KB / 32;       // MFMA k steps per stage
+    static_assert(PIECES <= kWave && kWave % PIECES == 0 && kMfmaRows % RPI == 0, "stage shape");
+    static_assert(NC <= 16 && (NC & (NC - 1)) == 0, "context columns");
+
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int lane = lane_id();
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    char* ring = smem + wv * (S * STAGE);
+    const int K = a.K;
+    const int nkb = (K + KB - 1) / KB;
+    const uint16_t* __restrict__ W = static_cast<const uint16_t*>(a.W);
+    const uint16_t* __restrict__ v = static_cast<const uint16_t*>(a.v);
+    const int64_t n_items = (int64_t)((sptr<int32_t>)a.plan.hdr)[0];
+    const int64_t stride = (int64_t)gridDim.x * NW;
+
+    // loader lanes: row (or context) RPI * i + lsub, stored piece lpc
+    const int lsub = lane / PIECES, lpc = lane % PIECES;
+    // MFMA lanes: tile row / context column `col`, k slice kq
+    const int col = lane & 15, kq = lane >> 4;
+    const int ccol = col & (NC - 1);
+
+    Unit iu;  // issue cursor
+    iu.it = (int64_t)blockIdx.x * NW + wv;
+    find_tile(iu, a.plan, n_items, stride);
+    if (!iu.valid) return;
+    Unit cu = iu;  // consume cursor
+
+    // issue-side group state: per B instruction, this lane's context row
+    const uint16_t* bsrc[NBI];
+    int nbi = 0;
+    auto issue_group = [&]() {
+        int vb, vs;
+        const int n = group_entries<NC>(iu, a.plan, vb, vs);
+        nbi = (n + RPI - 1) / RPI;
+#pragma unroll
+        for (int i = 0; i < NBI; ++i) bsrc[i] = v + (int64_t)from_lane(vb, min(RPI * i + lsub, n - 1)) * K;
+    };
+    // consume-side group state: this lane's output row base, and tile vocabulary ids
+    int ncols = 0;
+    int64_t obase = 0;
+    int32_t vid[4] = {0, 0, 0, 0};
+    auto consume_group = [&]() {
+        int vb, vs;
+        ncols = group_entries<NC>(cu, a.plan, vb, vs);
+        obase = (int64_t)from_lane(vb, ccol) * a.ld + from_lane(vs, ccol) + cu.r0;
+        if (a.vid_out != nullptr && cu.g == 0) {
+            // lane j < 16 of vp holds the vocabulary id of tile row j
+            sptr<int32_t> P = (sptr<int32_t>)a.perm + cu.r0;
+            int vp = P[0];
+            if (cu.nrows == kMfmaRows) {
+#pragma unroll
+                for (int j = 1; j < kMfmaRows; ++j) vp = set_lane(vp, P[j], j);
+            } else {
+#pragma unroll
+                for (int j = 1; j < kMfmaRows; ++j)
+                    if (j < cu.nrows) vp = set_lane(vp, P[j], j);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) vid[r] = from_lane(vp, 4 * kq + r);
+        }
+    };
+
+    auto issue = [&](int slot) {
+        char* dst = ring + slot * STAGE;
+        const int kb = iu.kb;
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int row = RPI * i + lsub;
+            const int piece = lpc ^ (row % PIECES);
+            int e = kb * KB + piece * 8;
+            e = e < K ? e : 0;  // k tail: any in-bounds piece; zeroed when read
+            const uint16_t* src = W + (int64_t)(iu.r0 + min(row, iu.nrows - 1)) * K + e;
+            __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < NBI; ++i) {
+            if (i < nbi) {
+                const int c = RPI * i + lsub;
+                const int piece = lpc ^ (c % PIECES);
+                int e = kb * KB + piece * 8;
+                e = e < K ? e : 0;
+                __builtin_amdgcn_global_load_lds((glb_ptr)(bsrc[i] + e),
+                                                 (lds_ptr)(dst + A_BYTES + i * (RPI * ROWB)), 16, 0, 0);
+            }
+        }
+    };
+
+    issue_group();
+    consume_group();
+    int issued = 0;
+#pragma unroll
+    for (int s = 0; s < S - 1; ++s) {
+        if (iu.valid) {
+            issue(issued % S);
+            ++issued;
+            if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) issue_group();
+        }
+    }
+
+    int consumed = 0;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    while (true) {
+        if (iu.valid) {
+            issue(issued % S);
+            ++issued;
+            if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) issue_group();
+            wait_vmem<(S - 1) * NA>();  // the S - 1 later stages may stay in flight
+        } else {
+            wait_vmem<0>();
+        }
+        const char* st = ring + (consumed % S) * STAGE;
+        const int k0 = cu.kb * KB;
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s) {
+            const int p = s * 4 + kq;
+            u32x4 av = *reinterpret_cast<const u32x4*>(st + col * ROWB + (p ^ (col % PIECES)) * 16);
+            u32x4 bv = *reinterpret_cast<const u32x4*>(st + A_BYTES + ccol * ROWB + (p ^ (ccol % PIECES)) * 16);
+            if (col >= ncols) bv = u32x4{0u, 0u, 0u, 0u};
+            if (k0 + p * 8 >= K) {
+                av = u32x4{0u, 0u, 0u, 0u};
+                bv = u32x4{0u, 0u, 0u, 0u};
+            }
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
+                                                          __builtin_bit_cast(bf16x8, bv), acc, 0, 0, 0);
+        }
+        ++consumed;
+        if (cu.kb == nkb - 1) {
+            // D rows 4 * kq + r, column col
+            if (col < ncols) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = 4 * kq + r;
+                    if (row < cu.nrows) {
+                        a.out[obase + row] = acc[r];
+                        if (a.vid_out != nullptr) a.vid_out[obase + row] = vid[r];
+                    }
+                }
+            }
+            acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        if (advance<NC>(cu, nkb, a.plan, n_items, stride)) {
+            if (!cu.valid) break;
+            consume_group();
+        }
+    }
+}
+
+template <int NW, int S, int KB, int NC>
+dyna_status launch_cfg(const RowdotArgs& a, hipStream_t stream) {
+    constexpr int ROWB = KB * 2, PIECES = ROWB / 16, RPI = kWave / PIECES;
+    constexpr int NBI = (NC + RPI - 1) / RPI;
+    constexpr int STAGE = kMfmaRows * ROWB + NBI * RPI * ROWB;
+    constexpr int LDS = NW * S * STAGE;
+    static_assert(LDS <= 160 * 1024, "LDS per block");
+    // more than 64 KiB of dynamic LDS must be allowed, once per kernel and
+    // device (the first launch is eager: a captured graph never sees this call)
+    static std::atomic<uint64_t> allowed{0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "gather: device");
+    if (!(allowed.load() & (1ull << dev))) {
+        if (hipFuncSetAttribute((const void*)gather_lds_kernel<NW, S, KB, NC>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, LDS) != hipSuccess)
+            return set_error(DYNA_ERR_HIP, "gather: LDS attribute");
+        allowed.fetch_or(1ull << dev);
+    }
+    const int per_cu = (160 * 1024) / LDS;
+    const int64_t items = (int64_t)a.max_chunks_bound;
+    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + NW - 1) / NW, 256 * per_cu));
+    launch_timed_kernel(gather_lds_kernel<NW, S, KB, NC>, dim3((unsigned)blocks), dim3(NW * kWave), LDS, stream,
+                        a);
+    return check_launch("gather_lds_kernel");
+}
+
+}  // namespace
+
+bool gather_lds_eligible(const RowdotArgs& a) {
+    return a.plan.hdr != nullptr && a.wdtype == DYNA_BF16 && a.vdtype == DYNA_BF16 && a.K % 8 == 0 &&
+           a.bias == nullptr && a.act == DYNA_ACT_NONE && (a.vid_out == nullptr || a.perm != nullptr);
+}
+
+dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
+    if (!gather_lds_eligible(a)) return set_error(DYNA_ERR_UNSUPPORTED, "gather: needs bf16 plan mode");
+    switch (option_gather_cfg()) {
+        case 2: return launch_cfg<4, 3, 256, 8>(a, stream);
+        case 3: return launch_cfg<4, 3, 128, 8>(a, stream);
+        case 4: return launch_cfg<2, 8, 128, 16>(a, stream);
+        case 5: return launch_cfg<4, 5, 64, 16>(a, stream);
+        case 6: return launch_cfg<8, 3, 64, 16>(a, stream);
+        default: return launch_cfg<4, 4, 128, 16>(a, stream);
+    }
+}
+
+}  // namespace dyna

@@ -327,14 +327,15 @@ dyna_status launch_mfma(const RowdotArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-// path: 0 automatic, 1 GEMV, 2 MFMA
+// path: 0 automatic, 1 GEMV, 2 MFMA (LDS-staged where eligible), 3 MFMA (direct loads)
 dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream) {
     const bool plan = a.plan.hdr != nullptr;
     const bool mfma_ok = a.wdtype == DYNA_BF16;
-    if (path == 2 && !mfma_ok)
+    if (path >= 2 && !mfma_ok)
         return set_error(DYNA_ERR_UNSUPPORTED, "rowdot: MFMA path needs bf16 weights");
-    const bool use_mfma = path == 2 || (path == 0 && mfma_ok && a.B > 4);
+    const bool use_mfma = path >= 2 || (path == 0 && mfma_ok && a.B > 4);
     if (!use_mfma) return plan ? launch_gemv<true>(a, stream) : launch_gemv<false>(a, stream);
+    if (plan && path != 3 && gather_lds_eligible(a)) return launch_gather_lds(a, stream);
     const bool vf32 = a.vdtype == DYNA_F32;
     if (plan) return vf32 ? launch_mfma<true, true>(a, stream) : launch_mfma<false, true>(a, stream);
     return vf32 ? launch_mfma<true, false>(a, stream) : launch_mfma<false, false>(a, stream);

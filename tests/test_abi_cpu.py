@@ -41,6 +41,8 @@ def test_set_option_validation():
     assert b"unknown option" in lib.dyna_last_error()
     assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 7) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 0) == D.OK
+    assert lib.dyna_set_option(D.OPT_GATHER_CFG, 7) == D.ERR_INVALID_ARG
+    assert lib.dyna_set_option(D.OPT_GATHER_CFG, 0) == D.OK
 
 
 def _layout(V=1000, d=64, M=10, cap=None, W=0x1000):

@@ -204,11 +204,12 @@ def _random_selection(p, B, k, seed):
     return np.array(rows, dtype=np.int32)
 
 
-@pytest.mark.parametrize("path", [1, 2])
+@pytest.mark.parametrize("path", [1, 2, 3])
 @pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
 def test_logits_parity(w, path):
-    if path == 2 and w.dtype == "f32":
-        pytest.skip("MFMA logits path needs bf16 weights")
+    """Paths: 1 GEMV, 2 MFMA with LDS-staged slabs, 3 MFMA with direct loads."""
+    if path >= 2 and w.dtype == "f32":
+        pytest.skip("MFMA logits paths need bf16 weights")
     p = Problem(w)
     topk = _random_selection(p, w.B, w.k, 3)
     sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
