@@ -239,7 +239,9 @@ dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_rows, int32
  * DYNA_OPT_LOGITS_PATH: 0 automatic, 1 wave-per-row GEMV, 2 MFMA tiles with
  *   the slab rows staged through LDS (bf16 weights and contexts; other types
  *   fall back to 3), 3 MFMA tiles loaded straight from HBM.
- * DYNA_OPT_ROUTER_PATH: 0 automatic, 1 GEMV, 2 MFMA tiles.
+ * DYNA_OPT_ROUTER_PATH: 0 automatic, 1 GEMV, 2 split-K MFMA with the contexts
+ *   staged in LDS (bf16 weights, up to 128 contexts; else 3), 3 MFMA tiles
+ *   loaded straight from HBM.
  * DYNA_OPT_KERNEL_TIMING: 1 brackets every launch of the gathered-head
  *   (logits) kernel with two (default) events recorded on the stream it runs
  *   on; 2 hands the two events to the dispatch itself (hipExtLaunchKernelGGL);

@@ -124,6 +124,8 @@ struct Carve {
     int32_t* counters = nullptr;  // [2] arrival counters of the fused one-context kernels
     void* partials = nullptr;     // partials of the fused one-context head
     Plan plan{};
+    float* rpart = nullptr;  // split-K partial sums of the router layers
+    size_t rpart_floats = 0;
     void* select_ws = nullptr;
     size_t bytes = 0;
 };
@@ -154,6 +156,14 @@ static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_
     const int64_t Bl = B;
     const int32_t M = L ? L->M : (r ? r->M : 0);
     if (r && r->H > 0) c.hidden = static_cast<float*>(take(sizeof(float) * Bl * r->H));
+    if (r) {
+        // either input type of layer 1 (fp32 inputs use shorter slices)
+        const int32_t n1 = r->H > 0 ? r->H : r->M;
+        size_t f = std::max(splitk_part_floats(n1, r->d_r, B, false), splitk_part_floats(n1, r->d_r, B, true));
+        if (r->H > 0) f = std::max(f, splitk_part_floats(r->M, r->H, B, true));
+        c.rpart_floats = f;
+        if (f > 0) c.rpart = static_cast<float*>(take(sizeof(float) * f));
+    }
     c.scores = static_cast<float*>(take(sizeof(float) * Bl * M));
     c.topk_ids = static_cast<int32_t*>(take(sizeof(int32_t) * Bl * k));
     c.topk_scores = static_cast<float*>(take(sizeof(float) * Bl * k));
@@ -250,8 +260,18 @@ static dyna_status check_select(int32_t mode, int32_t* k_t, float temperature, c
     } while (0)
 
 // ------------------------------------------------------------------ pieces
+// One router layer.  Path: 0 automatic (GEMV for up to 4 contexts, else
+// split-K MFMA), 1 GEMV, 2 split-K MFMA, 3 MFMA tiles with direct loads.
+static dyna_status run_layer(const RowdotArgs& a, int path, float* part, size_t part_floats, hipStream_t s) {
+    const bool splitk = (path == 2 || (path == 0 && a.B > 4)) && a.wdtype == DYNA_BF16 && part != nullptr &&
+                        splitk_part_floats(a.n_rows, a.K, a.B, a.vdtype == DYNA_F32) > 0;
+    if (splitk) return launch_dense_splitk(a, part, part_floats, s);
+    return launch_rowdot(a, path >= 2 ? 3 : path, s);
+}
+
 static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtype, int32_t B,
-                              float* scores, float* hidden, hipStream_t s, int32_t* zero_words = nullptr) {
+                              float* scores, float* hidden, float* part, size_t part_floats, hipStream_t s,
+                              int32_t* zero_words = nullptr) {
     const int path = option_router_path();
     RowdotArgs a{};
     a.zero_words = zero_words;  // cleared by block 0 of the first router kernel
@@ -268,14 +288,14 @@ static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtyp
         a.bias = r->b1;
         a.act = DYNA_ACT_NONE;
         a.n_rows = r->M;
-        return launch_rowdot(a, path, s);
+        return run_layer(a, path, part, part_floats, s);
     }
     a.out = hidden;
     a.ld = r->H;
     a.bias = r->b1;
     a.act = r->act;
     a.n_rows = r->H;
-    TRY(launch_rowdot(a, path, s));
+    TRY(run_layer(a, path, part, part_floats, s));
     RowdotArgs b{};
     b.W = r->W2;
     b.wdtype = r->wdtype;
@@ -288,7 +308,7 @@ static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtyp
     b.bias = r->b2;
     b.act = DYNA_ACT_NONE;
     b.n_rows = r->M;
-    return launch_rowdot(b, path, s);
+    return run_layer(b, path, part, part_floats, s);
 }
 
 static dyna_status run_logits(const dyna_layout* L, const void* h, int32_t hdtype, int32_t B, int32_t k,
@@ -371,9 +391,13 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         g_gemv_rows.store(value);
         return DYNA_OK;
     }
+    if (option == DYNA_OPT_ROUTER_PATH) {
+        REQUIRE(value >= 0 && value <= 3, "router path %d outside [0, 3]", value);
+        g_router_path.store(value);
+        return DYNA_OK;
+    }
     REQUIRE(value >= 0 && value <= 2, "option value %d outside [0, 2]", value);
-    if (option == DYNA_OPT_ROUTER_PATH) g_router_path.store(value);
-    else if (option == DYNA_OPT_KERNEL_TIMING) g_kernel_timing.store(value);
+    if (option == DYNA_OPT_KERNEL_TIMING) g_kernel_timing.store(value);
     else return set_error(DYNA_ERR_INVALID_ARG, "unknown option %d", option);
     return DYNA_OK;
 }
@@ -456,7 +480,7 @@ DYNA_API dyna_status dyna_route(const dyna_router* r, const void* x, int32_t xdt
     if (ws_bytes < c0.bytes) return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, c0.bytes);
     const Carve c = carve(nullptr, r, B, k, 0, ws);
     float* sc = scores ? scores : c.scores;
-    TRY(run_router(r, x, xdtype, B, sc, c.hidden, stream));
+    TRY(run_router(r, x, xdtype, B, sc, c.hidden, c.rpart, c.rpart_floats, stream));
     return launch_topk_clusters(sc, B, r->M, k, topk_ids, topk_scores, nullptr, nullptr, nullptr,
                                 nullptr, nullptr, stream);
 }
@@ -559,7 +583,7 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
                        !want_sample;
 
     // routing (the router's stream)
-    TRY(run_router(r, x, adtype, B, c.scores, c.hidden, rs, fused ? c.counters : nullptr));
+    TRY(run_router(r, x, adtype, B, c.scores, c.hidden, c.rpart, c.rpart_floats, rs, fused ? c.counters : nullptr));
     TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, L->offsets, c.sel_sorted,
                              c.sel_rowoff, c.row_len, &c.plan, rs));
     if (B > 1) TRY(launch_plan(L->offsets, L->M, c.sel_sorted, c.sel_rowoff, B, k, c.plan, rs));

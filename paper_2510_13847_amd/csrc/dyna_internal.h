@@ -112,6 +112,21 @@ struct RowdotArgs {
 };
 dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);
 
+// router.hip: dense layers for 1..128 contexts as split-K MFMA workgroups
+// (contexts staged in LDS) plus a fixed-order reduction with bias and
+// activation; `part` holds the per-slice partial sums.
+struct SplitShape {
+    int nw;         // waves (16 rows each) per workgroup
+    int groups;     // 16-context MFMA column groups
+    int row_tiles;  // workgroups along the rows
+    int ksl;        // k-slice length
+    int slices;     // workgroups along k
+    size_t lds;     // staged contexts, bytes
+};
+bool splitk_shape(int32_t n_rows, int32_t K, int32_t B, bool vf32, SplitShape* out);
+size_t splitk_part_floats(int32_t n_rows, int32_t K, int32_t B, bool vf32);
+dyna_status launch_dense_splitk(const RowdotArgs& a, float* part, size_t part_floats, hipStream_t stream);
+
 // gather.hip: plan mode with bf16 weights and contexts, slab rows staged
 // through LDS (MFMA tiles)
 bool gather_lds_eligible(const RowdotArgs& a);

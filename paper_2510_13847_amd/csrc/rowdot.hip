@@ -36,27 +36,6 @@ __global__ __launch_bounds__(kThreads) void rowdot_gemv_kernel(RowdotArgs a) {
 // ------------------------------------------------------------------ MFMA
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
 
-// 8 consecutive fp32 values split into bf16 hi and lo terms.
-__device__ __forceinline__ void split8(const float* p, u32x4& hi, u32x4& lo) {
-    const u32x4* q = reinterpret_cast<const u32x4*>(p);
-    const u32x4 x0 = q[0], x1 = q[1];
-    float f[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        f[i] = __uint_as_float(x0[i]);
-        f[4 + i] = __uint_as_float(x1[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const uint32_t h0 = f32_to_bf16_bits(f[2 * i]);
-        const uint32_t h1 = f32_to_bf16_bits(f[2 * i + 1]);
-        const uint32_t l0 = f32_to_bf16_bits(f[2 * i] - __uint_as_float(h0 << 16));
-        const uint32_t l1 = f32_to_bf16_bits(f[2 * i + 1] - __uint_as_float(h1 << 16));
-        hi[i] = h0 | (h1 << 16);
-        lo[i] = l0 | (l1 << 16);
-    }
-}
-
 // One item = T tiles of 16 W rows (T * 16 consecutive rows) against the
 // contexts of the item, G groups of 16 contexts at a time: every B-operand
 // load feeds T MFMAs and every A-operand load feeds G.  KS > 1 splits the

@@ -15,6 +15,8 @@
 //                        restricted draft q_S (Sec. 5), split over 2048-slot
 //                        segments so long rows (the dense baseline) spread
 //                        over many workgroups.
+#include <atomic>
+
 #include "topk.h"
 #include "select_row.h"
 
@@ -107,7 +109,11 @@ __global__ __launch_bounds__(kNT) void shortlist_kernel(
 }
 
 // ------------------------------------------------------------------ plan
+// One workgroup.  Global reads are issued kPlanPer at a time per thread so
+// that their latencies overlap (the loops below are latency-bound, not
+// bandwidth-bound); the layout offsets are copied to LDS once.
 constexpr int kPlanThreads = 1024;
+constexpr int kPlanPer = 8;
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int32_t* __restrict__ offsets, int M, const int32_t* __restrict__ sel_sorted,
     const int32_t* __restrict__ sel_rowoff, int B, int k, Plan plan) {
@@ -115,22 +121,44 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     int32_t* cnt = pl;            // contexts per cluster, later the list fill counters
     int32_t* loff = pl + M;       // first list entry per cluster
     int32_t* coff = pl + 2 * M;   // first chunk per cluster
+    int32_t* offs = pl + 3 * M;   // layout offsets [M + 1]
     __shared__ int tmp[kPlanThreads / kWave + 1];
-    for (int m = threadIdx.x; m < M; m += kPlanThreads) cnt[m] = 0;
+    const int t = threadIdx.x;
+    for (int m0 = 0; m0 <= M; m0 += kPlanThreads * kPlanPer) {
+        int v[kPlanPer];
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q) {
+            const int m = m0 + q * kPlanThreads + t;
+            v[q] = m <= M ? offsets[m] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q) {
+            const int m = m0 + q * kPlanThreads + t;
+            if (m <= M) offs[m] = v[q];
+            if (m < M) cnt[m] = 0;
+        }
+    }
     __syncthreads();
     const int64_t n_sel = (int64_t)B * k;
-    for (int64_t e = threadIdx.x; e < n_sel; e += kPlanThreads) {
-        const int m = sel_sorted[e];
-        if (m >= 0 && m < M) atomicAdd(&cnt[m], 1);
+    for (int64_t e0 = 0; e0 < n_sel; e0 += kPlanThreads * kPlanPer) {
+        int mv[kPlanPer];
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q) {
+            const int64_t e = e0 + q * kPlanThreads + t;
+            mv[q] = e < n_sel ? sel_sorted[e] : -1;
+        }
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q)
+            if (mv[q] >= 0 && mv[q] < M) atomicAdd(&cnt[mv[q]], 1);
     }
     __syncthreads();
     const int per = (M + kPlanThreads - 1) / kPlanThreads;
-    const int m0 = min(M, (int)threadIdx.x * per);
+    const int m0 = min(M, t * per);
     const int m1 = min(M, m0 + per);
     int lc = 0, lch = 0;
     for (int m = m0; m < m1; ++m) {
         lc += cnt[m];
-        if (cnt[m] > 0) lch += (offsets[m + 1] - offsets[m] + kChunkRows - 1) / kChunkRows;
+        if (cnt[m] > 0) lch += (offs[m + 1] - offs[m] + kChunkRows - 1) / kChunkRows;
     }
     int n_entries, n_chunks;
     int rl = block_exclusive_scan<kPlanThreads>(lc, tmp, &n_entries);
@@ -139,25 +167,48 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         loff[m] = rl;
         coff[m] = rc;
         rl += cnt[m];
-        if (cnt[m] == 0) continue;
-        const int o = offsets[m], n = offsets[m + 1] - o;
-        for (int c = 0; c * kChunkRows < n; ++c)
-            plan.chunks[rc + c] =
-                Chunk{o + c * kChunkRows, min(kChunkRows, n - c * kChunkRows), loff[m], cnt[m]};
-        rc += (n + kChunkRows - 1) / kChunkRows;
+        if (cnt[m] > 0) rc += (offs[m + 1] - offs[m] + kChunkRows - 1) / kChunkRows;
     }
     __syncthreads();
-    for (int m = threadIdx.x; m < M; m += kPlanThreads) cnt[m] = 0;
-    __syncthreads();
-    for (int64_t e = threadIdx.x; e < n_sel; e += kPlanThreads) {
-        const int m = sel_sorted[e];
-        if (m < 0 || m >= M) continue;
-        const int b = (int)(e / k), i = (int)(e % k);
-        const int slot_base = sel_rowoff[(int64_t)b * (k + 1) + i] - offsets[m];
-        const int p = atomicAdd(&cnt[m], 1);
-        plan.list[loff[m] + p] = ListEntry{b, slot_base};
+    // chunk descriptors, all threads together: chunk c belongs to the last
+    // cluster whose first chunk is <= c (clusters without contexts have none)
+    for (int c = t; c < n_chunks; c += kPlanThreads) {
+        int lo = 0, hi = M - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (coff[mid] <= c) lo = mid; else hi = mid - 1;
+        }
+        while (lo > 0 && cnt[lo] == 0) --lo;  // equal offsets: the cluster that owns the chunks
+        const int ci = c - coff[lo];
+        const int o = offs[lo], n = offs[lo + 1] - o;
+        plan.chunks[c] = Chunk{o + ci * kChunkRows, min(kChunkRows, n - ci * kChunkRows), loff[lo], cnt[lo]};
     }
-    if (threadIdx.x == 0) {
+    __syncthreads();
+    for (int m = t; m < M; m += kPlanThreads) cnt[m] = 0;
+    __syncthreads();
+    for (int64_t e0 = 0; e0 < n_sel; e0 += kPlanThreads * kPlanPer) {
+        int mv[kPlanPer], ro[kPlanPer];
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q) {
+            const int64_t e = e0 + q * kPlanThreads + t;
+            mv[q] = e < n_sel ? sel_sorted[e] : -1;
+        }
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q) {
+            const int64_t e = e0 + q * kPlanThreads + t;
+            const int64_t b = e / k, i = e - b * k;
+            ro[q] = (mv[q] >= 0 && mv[q] < M) ? sel_rowoff[b * (k + 1) + i] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q) {
+            const int m = mv[q];
+            if (m < 0 || m >= M) continue;
+            const int64_t e = e0 + q * kPlanThreads + t;
+            const int p = atomicAdd(&cnt[m], 1);
+            plan.list[loff[m] + p] = ListEntry{(int32_t)(e / k), ro[q] - offs[m]};
+        }
+    }
+    if (t == 0) {
         plan.hdr->n_chunks = n_chunks;
         plan.hdr->n_entries = n_entries;
     }
@@ -165,7 +216,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 
 // ------------------------------------------------------------------ select
 __global__ __launch_bounds__(kNT) void select_partial_kernel(SelectArgs a) {
-    __shared__ uint64_t wmax[8];
+    __shared__ uint64_t cand[kNT / kWave * DYNA_MAX_KT];
     __shared__ uint64_t top[DYNA_MAX_KT];
     __shared__ float red[kNT / kWave];
     const int p = blockIdx.x, b = blockIdx.y;
@@ -194,7 +245,7 @@ __global__ __launch_bounds__(kNT) void select_partial_kernel(SelectArgs a) {
                 list[q] = list[q + 1];
                 list[q + 1] = t;
             }
-    block_topk_rounds<kPer>(list, a.k_t, wmax, top);
+    block_topk_rounds<kPer, kNT, DYNA_MAX_KT>(list, a.k_t, cand, top);
     // segment max = value of the best key (or -inf for an empty segment)
     const float smax = top[0] != 0 ? key_val(top[0]) : -__builtin_inff();
     float tsum = 0.0f;
@@ -362,8 +413,8 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
 }
 
 template <int KT>
-__global__ __launch_bounds__(kNT) void select_row_kernel(SelectArgs a) {
-    select_row<KT>(a, blockIdx.x);
+__global__ __launch_bounds__(kRowThreads) void select_row_kernel(SelectArgs a) {
+    select_row<KT, kRowThreads>(a, blockIdx.x);
 }
 
 }  // namespace
@@ -401,7 +452,19 @@ dyna_status launch_shortlist(const int32_t* offsets, const int32_t* perm, int32_
 dyna_status launch_plan(const int32_t* offsets, int32_t M, const int32_t* sel_sorted,
                         const int32_t* sel_rowoff, int32_t B, int32_t k, Plan plan,
                         hipStream_t stream) {
-    const size_t lds = sizeof(int32_t) * 3 * (size_t)M;
+    const size_t lds = sizeof(int32_t) * (4 * (size_t)M + 1);
+    if (lds > 64 * 1024) {
+        // above 64 KiB the dynamic LDS size must be allowed, once per device
+        static std::atomic<uint64_t> allowed{0};
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "plan: device");
+        if (!(allowed.load() & (1ull << dev))) {
+            if (hipFuncSetAttribute((const void*)plan_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)(sizeof(int32_t) * (4 * (size_t)DYNA_MAX_M + 1))) != hipSuccess)
+                return set_error(DYNA_ERR_HIP, "plan: LDS attribute");
+            allowed.fetch_or(1ull << dev);
+        }
+    }
     plan_kernel<<<1, kPlanThreads, lds, stream>>>(offsets, M, sel_sorted, sel_rowoff, B, k, plan);
     return check_launch("plan_kernel");
 }
@@ -449,7 +512,8 @@ SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_
 }
 
 bool select_row_fits(int32_t max_len, bool fixed, int32_t k_t, int32_t k) {
-    return max_len <= (fixed ? kRowMax / 4 : kRowMax) && k_t <= 16 && (fixed || k <= kRowTable);
+    // full-vocabulary rows (fixed length) spread over many workgroups beyond 8192
+    return max_len <= (fixed ? 8192 : kRowMax) && k_t <= 16 && (fixed || k <= kRowTable);
 }
 
 dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_len,
@@ -465,8 +529,8 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
                                           out_sample_logprob, ws, slot_vid);
     // shortlist-sized rows: one workgroup per row, one launch
     if (select_row_fits(max_len, row_len == nullptr, k_t, perm == nullptr ? 0 : k)) {
-        if (k_t == 1) select_row_kernel<1><<<B, kNT, 0, stream>>>(a);
-        else select_row_kernel<16><<<B, kNT, 0, stream>>>(a);
+        if (k_t == 1) select_row_kernel<1><<<B, kRowThreads, 0, stream>>>(a);
+        else select_row_kernel<16><<<B, kRowThreads, 0, stream>>>(a);
         return check_launch("select_row_kernel");
     }
     select_partial_kernel<<<dim3(a.P, B), kNT, 0, stream>>>(a);

@@ -9,7 +9,7 @@ namespace {
 
 constexpr int kSeg = 2048;          // shortlist slots per partial workgroup
 constexpr int kPer = kSeg / kNT;    // 8 slots per thread
-constexpr int kRowMax = 32768;      // longest row the one-launch select takes
+constexpr int kRowMax = 1 << 17;    // longest shortlist row the one-launch select takes
 
 
 __device__ __forceinline__ float canon(float z) { return z != z ? -__builtin_inff() : z; }
@@ -45,25 +45,54 @@ __device__ __forceinline__ void slot_vids(const SelectArgs& a, int b, int j0, in
     }
 }
 
-// Block-wide selection of the k_t largest keys from per-thread lists sorted
-// descending (list[0] largest, 0 = empty).  Thread 0 receives them in out[].
-template <int L>
-__device__ void block_topk_rounds(uint64_t (&list)[L], int k_t, uint64_t* wmax /* LDS [2][4] */,
+// Block-wide selection of the k_t largest keys (k_t <= KTMAX) from per-thread
+// lists sorted descending (list[0] largest, 0 = empty).  Each wave first takes
+// its own k_t best keys in k_t rounds of a wave max (no barrier), then wave 0
+// takes the k_t best of the waves' candidates.  Thread 0 writes them to out[].
+// Keys are unique (they carry the vocabulary id), so a round's winner is one lane.
+template <int L, int NT, int KTMAX>
+__device__ void block_topk_rounds(uint64_t (&list)[L], int k_t, uint64_t* cand /* LDS [NT / kWave * KTMAX] */,
                                   uint64_t* out /* LDS [k_t] */) {
+    constexpr int NW = NT / kWave;
+    constexpr int C = (NW * KTMAX + kWave - 1) / kWave;  // candidates per lane of wave 0
     const int lane = lane_id(), w = threadIdx.x / kWave;
     for (int r = 0; r < k_t; ++r) {
         const uint64_t m = wave_max_u64(list[0]);
-        if (lane == 0) wmax[(r & 1) * 4 + w] = m;
-        __syncthreads();
-        uint64_t best = wmax[(r & 1) * 4];
-#pragma unroll
-        for (int q = 1; q < kNT / kWave; ++q) best = max(best, wmax[(r & 1) * 4 + q]);
-        if (best != 0 && list[0] == best) {
+        if (m != 0 && list[0] == m) {
 #pragma unroll
             for (int q = 0; q < L - 1; ++q) list[q] = list[q + 1];
             list[L - 1] = 0;
         }
-        if (threadIdx.x == 0) out[r] = best;
+        if (lane == 0) cand[w * k_t + r] = m;
+    }
+    __syncthreads();
+    if (w == 0) {
+        const int nc = NW * k_t;
+        uint64_t c[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            const int i = lane + q * kWave;
+            c[q] = i < nc ? cand[i] : 0;
+        }
+        // sort the lane's few candidates descending
+#pragma unroll
+        for (int r = 0; r < C; ++r)
+#pragma unroll
+            for (int q = r & 1; q + 1 < C; q += 2)
+                if (c[q] < c[q + 1]) {
+                    const uint64_t t = c[q];
+                    c[q] = c[q + 1];
+                    c[q + 1] = t;
+                }
+        for (int r = 0; r < k_t; ++r) {
+            const uint64_t m = wave_max_u64(c[0]);
+            if (m != 0 && c[0] == m) {
+#pragma unroll
+                for (int q = 0; q < C - 1; ++q) c[q] = c[q + 1];
+                c[C - 1] = 0;
+            }
+            if (lane == 0) out[r] = m;
+        }
     }
     __syncthreads();
 }
@@ -75,13 +104,14 @@ __device__ void block_topk_rounds(uint64_t (&list)[L], int k_t, uint64_t* wmax /
 // per-slot ids when present, else from the shortlist's cluster table staged
 // in LDS.
 constexpr int kRowTable = 1024;  // clusters per row the LDS table holds
+constexpr int kRowThreads = 1024;  // threads per row: a few slots each
 
-template <int KT>
+template <int KT, int NT>
 __device__ void select_row(const SelectArgs& a, int b) {
-    __shared__ uint64_t wmax[8];
-    __shared__ uint64_t top[DYNA_MAX_KT];
-    __shared__ float red[2 * (kNT / kWave) + 1];
-    __shared__ float incl_s[kNT];
+    __shared__ uint64_t cand[NT / kWave * KT];
+    __shared__ uint64_t top[KT];
+    __shared__ float red[2 * (NT / kWave) + 1];
+    __shared__ float incl_s[NT];
     __shared__ int sh_pick;
     __shared__ int32_t t_ro[kRowTable + 1];
     __shared__ int32_t t_base[kRowTable];
@@ -92,7 +122,7 @@ __device__ void select_row(const SelectArgs& a, int b) {
     if (table) {  // slot -> layout row: rows of cluster ci start at t_base[ci] + slot
         const int32_t* ro = a.sel_rowoff + (int64_t)b * (a.k + 1);
         const int32_t* ss = a.sel_sorted + (int64_t)b * a.k;
-        for (int c = threadIdx.x; c <= a.k; c += kNT) {
+        for (int c = threadIdx.x; c <= a.k; c += NT) {
             t_ro[c] = ro[c];
             if (c < a.k) t_base[c] = ss[c] >= 0 ? a.offsets[ss[c]] - ro[c] : 0;
         }
@@ -113,7 +143,7 @@ __device__ void select_row(const SelectArgs& a, int b) {
 #pragma unroll
     for (int q = 0; q < KT; ++q) list[q] = 0;
 #pragma unroll 4
-    for (int j = threadIdx.x; j < len; j += kNT) {
+    for (int j = threadIdx.x; j < len; j += NT) {
         const uint64_t key = sel_key(canon(z[j]), vid_of(j));
         if (key > list[KT - 1]) {
             list[KT - 1] = key;
@@ -126,13 +156,13 @@ __device__ void select_row(const SelectArgs& a, int b) {
                 }
         }
     }
-    block_topk_rounds<KT>(list, a.k_t, wmax, top);
+    block_topk_rounds<KT, NT, KT>(list, a.k_t, cand, top);
     const float mx = top[0] != 0 ? key_val(top[0]) : -__builtin_inff();
     const bool sampling = a.uniforms != nullptr && a.out_sample != nullptr;
 
     // softmax mass: strided when only top-k is asked, contiguous ranges
     // (shortlist order) when a sample must be drawn from the same sums
-    const int E = (len + kNT - 1) / kNT;
+    const int E = (len + NT - 1) / NT;
     const int j0 = min(len, (int)threadIdx.x * E);
     const int j1 = min(len, j0 + E);
     float tsum = 0.0f;
@@ -141,14 +171,14 @@ __device__ void select_row(const SelectArgs& a, int b) {
             for (int j = j0; j < j1; ++j) tsum += expf((canon(z[j]) - mx) * a.inv_t);
         } else {
 #pragma unroll 4
-            for (int j = threadIdx.x; j < len; j += kNT) tsum += expf((canon(z[j]) - mx) * a.inv_t);
+            for (int j = threadIdx.x; j < len; j += NT) tsum += expf((canon(z[j]) - mx) * a.inv_t);
         }
     }
     float total;
-    const float incl = block_inclusive_scan_f32<kNT>(tsum, red, &total);
+    const float incl = block_inclusive_scan_f32<NT>(tsum, red, &total);
     const float log_total = logf(total);
     if (a.out_ids != nullptr) {
-        for (int r = threadIdx.x; r < a.k_t; r += kNT) {
+        for (int r = threadIdx.x; r < a.k_t; r += NT) {
             const uint64_t key = top[r];
             a.out_ids[(int64_t)b * a.k_t + r] = key != 0 ? (int32_t)key_id(key) : -1;
             if (a.out_logprobs)

@@ -113,10 +113,10 @@ def test_layout_with_empty_clusters_and_bad_ids():
 
 
 # ---------------------------------------------------------------- router
-@pytest.mark.parametrize("path", [0, 1, 2])
+@pytest.mark.parametrize("path", [0, 1, 2, 3])
 @pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
 def test_route_parity(w, path):
-    if path == 2 and w.dtype == "f32":
+    if path >= 2 and w.dtype == "f32":
         pytest.skip("MFMA router path needs bf16 weights")
     p = Problem(w)
     D.set_option(D.OPT_ROUTER_PATH, path)
