@@ -33,7 +33,7 @@ sys.path.insert(0, ROOT)
 import workloads as W  # noqa: E402
 
 PEAK_HBM_GBS = 8000.0
-KERNEL_SOURCES = ["gemv.h", "rowdot.hip", "fused.hip", "dyna_device.h", "dyna_internal.h"]
+CSRC = os.path.join(ROOT, "paper_2510_13847_amd", "csrc")
 N_REPLICAS = 4
 POOL = 64
 GRAPH_CHUNK = 256
@@ -138,25 +138,138 @@ def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20):
             "routing_hidden_frac": round(max(0.0, t_s - t_o) / t_r, 3) if t_r > 0 else None}
 
 
-def kernel_source_hash():
-    """Hash of the sources the gathered-head kernels are built from."""
+KERNEL_UNITS = {"logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip",
+                "rowdot_gemv_kernel": "rowdot.hip"}
+
+
+def kernel_source_hash(symbol):
+    """Hash of the translation unit that defines `symbol` and of every library
+    header it includes, transitively (a change to the kernel invalidates the
+    counter summary taken from it)."""
     import hashlib
+    import re
+    seen, todo = [], [KERNEL_UNITS[symbol]]
+    while todo:
+        name = todo.pop()
+        if name in seen or not os.path.exists(os.path.join(CSRC, name)):
+            continue
+        seen.append(name)
+        with open(os.path.join(CSRC, name)) as f:
+            todo += re.findall(r'#include "([^"]+)"', f.read())
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2510_13847_amd", "csrc", name), "rb") as f:
+    for name in sorted(seen):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode())
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload):
+def dominant_kernel(w):
+    """Symbol (substring) and description of the gathered-head kernel a step of w launches."""
+    if w.B == 1 and w.modes == ("argmax",):
+        return "logits_greedy_kernel", "gathered head fused with argmax selection (one context)"
+    if w.dtype == "bf16" and w.B > 4:
+        return "gather_lds_kernel", "gathered head, LDS-staged MFMA tiles"
+    return "rowdot_gemv_kernel", "gathered head, wave-per-row GEMV"
+
+
+# ---------------------------------------------------------------- profile summaries
+# These read rocprofv3 CSV output (no GPU, no torch) and write the summaries
+# kept under profiles/.
+
+def _read_csv(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def summarize_trace(trace_dir, bench_json, plain_json, command):
+    """profiles/<kernel>_<workload>_kernel_trace.md from a --kernel-trace --stats run of bench.py."""
+    with open(bench_json) as f:
+        prof = json.loads(f.read().strip().splitlines()[-1])
+    plain = None
+    if plain_json:
+        with open(plain_json) as f:
+            plain = json.loads(f.read().strip().splitlines()[-1])
+    wl = prof["config"]["workload"]
+    sym = prof["roofline"]["kernel_symbol"]
+    stats = _read_csv(os.path.join(trace_dir, "run_kernel_stats.csv"))
+    trace = _read_csv(os.path.join(trace_dir, "run_kernel_trace.csv"))
+    mine = sorted((r for r in trace if sym in r["Kernel_Name"]), key=lambda r: int(r["Start_Timestamp"]))
+    n = prof["roofline"]["launches"]
+    timed = mine[-n:] if n else []
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in timed]
+    avg = sum(dur) / len(dur) if dur else float("nan")
+    lines = [f"# Kernel trace: {sym}, {wl}", "",
+             "Command (from any directory on the GPU host; `<repo>` is the repository root, `<out>` any directory):",
+             "", "```", command, "```", "",
+             "| kernel | calls | avg us | min us | max us | share |", "|---|---|---|---|---|---|"]
+    for r in stats[:14]:
+        name = r["Name"].replace("dyna::(anonymous namespace)::", "")
+        name = name if len(name) <= 90 else name[:87] + "..."
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['Percentage']):.1f}% |")
+    lines += ["", f"Dominant kernel `{sym}` over the {len(dur)} launches that bench.py brackets with events "
+              f"(the last {n} of the run): rocprofv3 average **{avg:.2f} us**.",
+              f"bench.py in the same (profiled) run: bracket {prof['roofline']['bracket_us']} us, empty bracket "
+              f"{prof['roofline']['empty_bracket_us']} us, kernel {prof['roofline']['avg_launch_us']} us "
+              "(the profiler's completion signals delay the closing event, so brackets read longer under it)."]
+    if plain:
+        lines.append(f"bench.py without the profiler (same command minus rocprofv3): kernel "
+                     f"{plain['roofline']['avg_launch_us']} us (bracket {plain['roofline']['bracket_us']} us, "
+                     f"empty bracket {plain['roofline']['empty_bracket_us']} us), "
+                     f"{plain['roofline']['achieved']} GB/s = {plain['roofline']['frac']} of peak; "
+                     f"{plain['value']} steps/s.")
+    lines.append("rocprofv3 times a kernel from dispatch to completion signal; an empty kernel reads about "
+                 "1.5 us that way, which the event figure minus an empty bracket does not contain.")
+    out = os.path.join(ROOT, "profiles", f"{sym}_{wl}_kernel_trace.md")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(out)
+
+
+def summarize_counters(fetch_dir, write_dir, counters_json, commands):
+    """profiles/traffic_<workload>.json from FETCH_SIZE and WRITE_SIZE runs of bench.py --counters."""
+    with open(counters_json) as f:
+        meta = json.loads(f.read().strip().splitlines()[-1])
+    wl, sym = meta["counters_run"], meta["kernel_symbol"]
+
+    def per_kernel(d, counter):
+        rows = [r for r in _read_csv(os.path.join(d, "run_counter_collection.csv")) if r["Counter_Name"] == counter]
+        k = [float(r["Counter_Value"]) for r in rows if sym in r["Kernel_Name"]]
+        cal = [float(r["Counter_Value"]) for r in rows if "layout_copy_rows_kernel" in r["Kernel_Name"]]
+        return sum(k) / len(k), len(k), cal[0]
+    fk, nk, fcal = per_kernel(fetch_dir, "FETCH_SIZE")
+    wk, _, wcal = per_kernel(write_dir, "WRITE_SIZE")
+    copy = meta["copy_bytes_each_way"]
+    fscale, wscale = copy / (fcal * 1024.0), copy / (wcal * 1024.0)
+    traffic = fk * 1024.0 * fscale + wk * 1024.0 * wscale
+    rec = {"workload": wl, "kernel": sym, "bytes_per_launch": int(round(traffic)),
+           "fetch_kib_per_dispatch": round(fk, 1), "write_kib_per_dispatch": round(wk, 1), "dispatches": nk,
+           "algorithmic_bytes_per_launch": meta.get("algorithmic_bytes_per_launch"),
+           "calibration": {"kernel": "layout_copy_rows_kernel", "bytes_each_way": copy,
+                           "fetch_kib": round(fcal, 1), "write_kib": round(wcal, 1),
+                           "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4)},
+           "source_hash": meta["source_hash"], "commands": commands,
+           "note": "each counter is scaled by what it reads for the layout build's row copy, "
+                   "whose byte count is known exactly"}
+    out = os.path.join(ROOT, "profiles", f"traffic_{wl}.json")
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(out)
+
+
+def measured_traffic(workload, symbol):
     """HBM bytes per gathered-head launch from the committed counter summary,
-    or None when there is none or the kernel sources changed since."""
+    or None when there is none or the kernel's sources changed since."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("source_hash") != kernel_source_hash():
+    if t.get("kernel") != symbol or t.get("source_hash") != kernel_source_hash(symbol):
         return None
     return t.get("bytes_per_launch")
 
@@ -189,10 +302,22 @@ def main():
     ap.add_argument("--workload", default="llama3_8b_chain", choices=W.WORKLOAD_ORDER)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-baselines", action="store_true", help="skip dense/static heads")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
+                    help="write the profiles/ kernel-trace summary from a rocprofv3 run of this script")
+    ap.add_argument("--plain-json", help="with --summarize-trace: the same bench command run without the profiler")
+    ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "COUNTERS_JSON"),
+                    help="write profiles/traffic_<workload>.json from FETCH_SIZE / WRITE_SIZE runs of --counters")
+    ap.add_argument("--command", action="append", default=[], help="command line(s) recorded in a summary")
     ap.add_argument("--counters", action="store_true",
                     help="hardware-counter pass: build the layout (a row copy of known size) "
                          "and run 20 eager steps; no timing")
     args = ap.parse_args()
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace, args.plain_json, "\n".join(args.command))
+        return
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters, args.command)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the head shards by context rows with no exchange; see the design notes)",
@@ -224,11 +349,18 @@ def main():
     head = D.DraftHead(routers[0], L0, w.B, w.k, mode, k_t, keep_logits=False)
     torch.cuda.synchronize()
     if args.counters:
+        sizes = np.diff(L0.offsets.cpu().numpy().astype(np.int64))
+        s_w = 2 if w.dtype == "bf16" else 4
+        alg = []
         for i in range(20):
             head(xs[i], xs[i], us[i], layout=layouts[i % N_REPLICAS], router=routers[i % N_REPLICAS])
+            cl = head.clusters.cpu().numpy()
+            alg.append(s_w * w.d * int(sizes[np.unique(cl)].sum()) + s_w * w.B * w.d + 4 * int(sizes[cl].sum()))
         torch.cuda.synchronize()
-        print(json.dumps({"counters_run": w.name, "copy_bytes_each_way": w.V * w.d * (2 if w.dtype == "bf16" else 4),
-                          "source_hash": kernel_source_hash()}), flush=True)
+        print(json.dumps({"counters_run": w.name, "kernel_symbol": dominant_kernel(w)[0],
+                          "copy_bytes_each_way": w.V * w.d * (2 if w.dtype == "bf16" else 4),
+                          "algorithmic_bytes_per_launch": int(np.mean(alg)),
+                          "source_hash": kernel_source_hash(dominant_kernel(w)[0])}), flush=True)
         return
 
     def make_step(i):
@@ -311,9 +443,9 @@ def main():
         "step_GBps": round(step_bytes * steps_per_s / 1e9, 1),
         "step_frac_hbm_peak": round(step_bytes * steps_per_s / 1e9 / PEAK_HBM_GBS, 4),
         "wall_s": round(wall_s, 4),
-        "roofline": {"kernel": "rowdot (gathered head)", "bound": "hbm",
+        "roofline": {"kernel": dominant_kernel(w)[1], "kernel_symbol": dominant_kernel(w)[0], "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": measured_traffic(w.name),
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": measured_traffic(w.name, dominant_kernel(w)[0]),
                      "bytes_per_launch": int(k_bytes), "avg_launch_us": round(k_avg_s * 1e6, 3),
                      "launches": int(k_n),
                      "timing": "event bracket on the kernel's stream minus an empty bracket",
@@ -348,10 +480,12 @@ def main():
         e1.record()
         torch.cuda.synchronize()
         base["dense_torch_matmul_argmax"] = {"ms_per_step": round(e0.elapsed_time(e1) / K, 5)}
-        dense_ms = base["dense"]["ms_per_step"]
+        # the faster of the two dense heads on this GPU is the one to beat
+        dense_ms = min(base["dense"]["ms_per_step"], base["dense_torch_matmul_argmax"]["ms_per_step"])
         dense_bytes = s_w * w.V * w.d + s_w * w.B * w.d
         rec["baselines"] = base
         rec["speedup_vs_dense"] = round(dense_ms / rec["ms_per_step"], 3)
+        rec["speedup_vs_static"] = round(base["static"]["ms_per_step"] / rec["ms_per_step"], 3)
         rec["byte_ratio_dense_over_dynamic"] = round(dense_bytes / step_bytes, 3)
 
     # ---------------- second-stream routing (workloads with a draft-layer stand-in)

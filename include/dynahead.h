@@ -257,10 +257,12 @@ dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_rows, int32
  *   ahead: 0 automatic (8), 4, 8 or 16.
  * DYNA_OPT_GATHER_CFG: shape of the LDS-staged MFMA kernel (path 2): 0
  *   automatic, 1..6 fixed (waves per block, ring stages, k columns per
- *   stage, context columns per pass). */
+ *   stage, context columns per pass).
+ * DYNA_OPT_GREEDY_GRID: workgroups of the fused one-context gathered head:
+ *   0 automatic (256), else 1..4096. */
 enum { DYNA_OPT_LOGITS_PATH = 1, DYNA_OPT_ROUTER_PATH = 2, DYNA_OPT_KERNEL_TIMING = 3,
        DYNA_OPT_GEMV_ROWS = 4, DYNA_OPT_FUSED_B1 = 5, DYNA_OPT_MFMA_UNROLL = 6,
-       DYNA_OPT_GATHER_CFG = 7 };
+       DYNA_OPT_GATHER_CFG = 7, DYNA_OPT_GREEDY_GRID = 8 };
 dyna_status dyna_set_option(int32_t option, int32_t value);
 
 /* Waits for the events recorded under DYNA_OPT_KERNEL_TIMING and returns the

@@ -25,6 +25,7 @@ std::atomic<int> g_gemv_rows{0};
 std::atomic<int> g_fused_off{0};
 std::atomic<int> g_mfma_unroll{0};
 std::atomic<int> g_gather_cfg{0};
+std::atomic<int> g_greedy_grid{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -107,6 +108,7 @@ int option_router_path() { return g_router_path.load(); }
 int option_gemv_rows() { return g_gemv_rows.load(); }
 int option_mfma_unroll() { return g_mfma_unroll.load(); }
 int option_gather_cfg() { return g_gather_cfg.load(); }
+int option_greedy_grid() { return g_greedy_grid.load(); }
 
 // ------------------------------------------------------------------ workspace
 // One carving serves every hot entry point, so a single workspace can back a
@@ -369,6 +371,11 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
     if (option == DYNA_OPT_MFMA_UNROLL) {
         REQUIRE(value == 0 || value == 4 || value == 8 || value == 16, "MFMA unroll %d not in {0, 4, 8, 16}", value);
         g_mfma_unroll.store(value);
+        return DYNA_OK;
+    }
+    if (option == DYNA_OPT_GREEDY_GRID) {
+        REQUIRE(value >= 0 && value <= kGreedyMaxBlocks, "greedy grid %d outside [0, %d]", value, kGreedyMaxBlocks);
+        g_greedy_grid.store(value);
         return DYNA_OK;
     }
     if (option == DYNA_OPT_GATHER_CFG) {

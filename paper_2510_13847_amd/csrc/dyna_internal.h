@@ -224,5 +224,6 @@ int option_router_path();
 int option_gemv_rows();
 int option_mfma_unroll();
 int option_gather_cfg();
+int option_greedy_grid();
 
 }  // namespace dyna

@@ -17,7 +17,7 @@
 namespace dyna {
 namespace {
 
-constexpr int kGreedyGrid = 256;  // workgroups of the fused head (one arrival each)
+constexpr int kGreedyGrid = 256;  // default workgroups of the fused head (one arrival each)
 
 struct GreedyPartial {
     uint64_t key;  // best (ordered logit, inverted vocabulary id)
@@ -136,8 +136,9 @@ template <typename WT, typename VT, int NB, int R>
 dyna_status launch_lg_r(const RowdotArgs& lg, const SelectArgs& sa, void* part, int32_t* counter,
                         hipStream_t s) {
     const int64_t items = (int64_t)lg.max_chunks_bound * (kChunkRows / R);
+    const int cap = option_greedy_grid() > 0 ? std::min(option_greedy_grid(), kGreedyMaxBlocks) : kGreedyGrid;
     const unsigned grid = (unsigned)std::max<int64_t>(
-        1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock, kGreedyGrid));
+        1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock, cap));
     launch_timed_kernel(logits_greedy_kernel<WT, VT, NB, R>, dim3(grid), dim3(kThreads), 0, s, lg, sa,
                         static_cast<GreedyPartial*>(part), counter);
     return check_launch("logits_greedy_kernel");
