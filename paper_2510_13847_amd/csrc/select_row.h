@@ -142,18 +142,31 @@ __device__ void select_row(const SelectArgs& a, int b) {
     uint64_t list[KT];
 #pragma unroll
     for (int q = 0; q < KT; ++q) list[q] = 0;
-#pragma unroll 4
-    for (int j = threadIdx.x; j < len; j += NT) {
-        const uint64_t key = sel_key(canon(z[j]), vid_of(j));
-        if (key > list[KT - 1]) {
-            list[KT - 1] = key;
+    // kLoadPer slots per thread per batch, their loads issued together
+    constexpr int kLoadPer = 4;
+    for (int j0 = 0; j0 < len; j0 += NT * kLoadPer) {
+        float zq[kLoadPer];
+        uint32_t vq[kLoadPer];
 #pragma unroll
-            for (int q = KT - 1; q > 0; --q)
-                if (list[q] > list[q - 1]) {
-                    const uint64_t t = list[q];
-                    list[q] = list[q - 1];
-                    list[q - 1] = t;
-                }
+        for (int q = 0; q < kLoadPer; ++q) {
+            const int j = j0 + q * NT + threadIdx.x;
+            zq[q] = j < len ? z[j] : 0.0f;
+            vq[q] = j < len ? vid_of(j) : 0u;
+        }
+#pragma unroll
+        for (int q = 0; q < kLoadPer; ++q) {
+            if (j0 + q * NT + (int)threadIdx.x >= len) continue;
+            const uint64_t key = sel_key(canon(zq[q]), vq[q]);
+            if (key > list[KT - 1]) {
+                list[KT - 1] = key;
+#pragma unroll
+                for (int r = KT - 1; r > 0; --r)
+                    if (list[r] > list[r - 1]) {
+                        const uint64_t t = list[r];
+                        list[r] = list[r - 1];
+                        list[r - 1] = t;
+                    }
+            }
         }
     }
     block_topk_rounds<KT, NT, KT>(list, a.k_t, cand, top);

@@ -15,6 +15,8 @@ namespace {
 // are then put in rank order and in ascending id order; with `plan` set (one
 // context) the workgroup also writes the gathered-head work plan, so no
 // separate plan launch is needed for a single context.
+constexpr int kStagePer = 8;  // staged loads in flight per thread
+
 __device__ __forceinline__ void radix_digit(const int* hist, int krem, uint32_t prefix, int shift,
                                             uint32_t* sh_prefix, int* sh_krem) {
     // wave 0: lane l holds digits 255-4l .. 252-4l (descending)
@@ -71,10 +73,36 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
     __shared__ uint32_t sh_prefix;
     __shared__ int sh_krem, sh_nsel, sh_ncand;
 
+    // stage scores (and offsets) with kStagePer loads in flight per thread
     const float* s = scores + (int64_t)b * M;
-    for (int j = threadIdx.x; j < M; j += kNT) sv[j] = s[j];
-    if (sel_sorted != nullptr)
-        for (int j = threadIdx.x; j <= M; j += kNT) offs[j] = offsets[j];
+    for (int j0 = 0; j0 < M; j0 += kNT * kStagePer) {
+        float x[kStagePer];
+#pragma unroll
+        for (int q = 0; q < kStagePer; ++q) {
+            const int j = j0 + q * kNT + threadIdx.x;
+            x[q] = j < M ? s[j] : 0.0f;
+        }
+#pragma unroll
+        for (int q = 0; q < kStagePer; ++q) {
+            const int j = j0 + q * kNT + threadIdx.x;
+            if (j < M) sv[j] = x[q];
+        }
+    }
+    if (sel_sorted != nullptr) {
+        for (int j0 = 0; j0 <= M; j0 += kNT * kStagePer) {
+            int x[kStagePer];
+#pragma unroll
+            for (int q = 0; q < kStagePer; ++q) {
+                const int j = j0 + q * kNT + threadIdx.x;
+                x[q] = j <= M ? offsets[j] : 0;
+            }
+#pragma unroll
+            for (int q = 0; q < kStagePer; ++q) {
+                const int j = j0 + q * kNT + threadIdx.x;
+                if (j <= M) offs[j] = x[q];
+            }
+        }
+    }
     hist[threadIdx.x] = 0;
     if (threadIdx.x == 0) {
         sh_nsel = 0;

@@ -51,6 +51,8 @@ CASES = [
     case("relu_b2", V=1500, d=128, M=16, H=32, act="relu", k=3, B=2),
     case("zipf_b9", V=6000, d=96, M=12, sizes=("zipf", 1.1, 1500), H=16, k=3, B=9),
     case("wide_k_b4", V=4096, d=512, M=64, H=64, k=64, B=4),  # k = M: shortlist = V
+    # more contexts than one MFMA column pass (and than the split-K router takes)
+    case("many_b130", V=3000, d=136, M=24, H=32, k=3, B=130),
 ]
 
 
@@ -226,6 +228,30 @@ def test_logits_parity(w, path):
         ref = O.shortlist_logits(p.h_np[b], p.W_np, sl[b, :n])
         PC.assert_close(lg[b, :n], ref, p.tol, f"logits row {b}")
         assert np.all(np.isnan(lg[b, n:])), "slots past row_len must stay untouched"
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("name", ["ragged_b37", "zipf_b9", "many_b130"])
+def test_logits_gather_shapes(name, cfg):
+    """Every workgroup shape of the LDS-staged MFMA gathered head."""
+    w = next(c for c in CASES if c.name == name)
+    p = Problem(w)
+    topk = _random_selection(p, w.B, w.k, 5)
+    sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
+    D.set_option(D.OPT_LOGITS_PATH, 2)
+    D.set_option(D.OPT_GATHER_CFG, cfg)
+    try:
+        logits = D.shortlist_logits(p.L, p.hd, sel, rowoff, row_len)
+        torch.cuda.synchronize()
+    finally:
+        D.set_option(D.OPT_LOGITS_PATH, 0)
+        D.set_option(D.OPT_GATHER_CFG, 0)
+    lg = logits.cpu().numpy().astype(np.float64)
+    row_len, sl = _ids(row_len), _ids(sl)
+    for b in range(w.B):
+        n = row_len[b]
+        ref = O.shortlist_logits(p.h_np[b], p.W_np, sl[b, :n])
+        PC.assert_close(lg[b, :n], ref, p.tol, f"cfg {cfg} logits row {b}")
 
 
 # ---------------------------------------------------------------- select
