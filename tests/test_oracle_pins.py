@@ -230,6 +230,13 @@ def test_sampling_fallback_and_zero_mass():
     assert O.sample_inverse_cdf(z, 1.0) == 0  # no F_j > u: last j with p_j > 0
 
 
+def test_sampling_boundary_uniform_goes_to_next_token():
+    # equal logits give exactly representable p_j = 1/4 and F = 1/4, 1/2, 3/4, 1:
+    # a uniform equal to F_j picks token j + 1 (first F_j > u)
+    z = np.zeros(4)
+    assert [O.sample_inverse_cdf(z, u) for u in (0.0, 0.25, 0.5, 0.75, 0.99)] == [0, 1, 2, 3, 3]
+
+
 def test_sampling_grid_frequencies_equal_probabilities():
     rng = np.random.default_rng(7)
     z = rng.standard_normal(9)
