@@ -118,6 +118,7 @@ dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);
 struct SplitShape {
     int nw;         // waves (16 rows each) per workgroup
     int groups;     // 16-context MFMA column groups
+    int tiles;      // 16-row tiles per wave
     int row_tiles;  // workgroups along the rows
     int ksl;        // k-slice length
     int slices;     // workgroups along k

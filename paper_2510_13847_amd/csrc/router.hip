@@ -29,11 +29,15 @@ constexpr int kSliceQuantum = 128;  // k-slice lengths are multiples of this
 constexpr int kMaxCols = 128;       // contexts per launch (8 MFMA column groups)
 constexpr int kLdsBudget = 128 * 1024;
 
-constexpr int kMaxSteps = 16;  // 32-wide k steps per slice (slices up to 512)
-constexpr int kStageBatch = 4; // staged pieces in flight per thread
+// 32-wide k steps per slice: up to 512 with one row tile per wave, 256 with two
+constexpr int max_steps(int tt) { return tt == 1 ? 16 : 8; }
+// staged pieces in flight per thread (fp32 pieces take twice the registers)
+template <bool VF32>
+constexpr int stage_batch() { return VF32 ? 8 : 16; }
 
-template <int NW, int G, bool VF32>
+template <int NW, int G, bool VF32, int TT>
 __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, int ksl, float* part) {
+    constexpr int MAXS = max_steps(TT);
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [G*16][ksl] hi, then lo
     constexpr int NCOL = G * 16;
     const int K = a.K, B = a.B, n = a.n_rows;
@@ -47,17 +51,22 @@ __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, 
     // HBM latency overlaps the staging of the contexts below
     const int lane = lane_id(), wv = threadIdx.x / kWave;
     const int col = lane & 15, kq = lane >> 4;
-    const int r0 = (blockIdx.x * NW + wv) * kMfmaRows;
+    const int r0 = (blockIdx.x * NW + wv) * kMfmaRows * TT;
     const int nsteps = (kn + 31) / 32;
-    u32x4 A[kMaxSteps];
+    u32x4 A[TT][MAXS];
     if (r0 < n) {
-        // rows past n read row n - 1 and are never stored
-        const uint16_t* __restrict__ wr = static_cast<const uint16_t*>(a.W) + (int64_t)min(r0 + col, n - 1) * K + k0;
 #pragma unroll
-        for (int s = 0; s < kMaxSteps; ++s) {
-            const int k = s * 32 + kq * 8;
-            A[s] = u32x4{0u, 0u, 0u, 0u};
-            if (s < nsteps && k < kn) A[s] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wr + k));
+        for (int t = 0; t < TT; ++t) {
+            // rows past n read row n - 1 and are never stored
+            const uint16_t* __restrict__ wr =
+                static_cast<const uint16_t*>(a.W) + (int64_t)min(r0 + t * kMfmaRows + col, n - 1) * K + k0;
+#pragma unroll
+            for (int s = 0; s < MAXS; ++s) {
+                const int k = s * 32 + kq * 8;
+                A[t][s] = u32x4{0u, 0u, 0u, 0u};
+                if (s < nsteps && k < kn)
+                    A[t][s] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wr + k));
+            }
         }
     }
 
@@ -67,6 +76,7 @@ __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, 
     constexpr int T = NW * kWave;
     const int dc = T / npc, dp = T - dc * npc;
     int c = threadIdx.x / npc, p = threadIdx.x - c * npc;
+    constexpr int kStageBatch = stage_batch<VF32>();
     for (int idx0 = threadIdx.x; idx0 < npieces; idx0 += T * kStageBatch) {
         u32x4 hi[kStageBatch], lo[kStageBatch];
         int cq[kStageBatch], pq[kStageBatch];
@@ -103,54 +113,61 @@ __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, 
     __syncthreads();
     if (r0 >= n) return;  // no barrier follows
 
-    f32x4 acc[G];
+    // every context piece read from LDS feeds the TT row tiles of the wave
+    f32x4 acc[TT][G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < TT; ++t)
 #pragma unroll
-    for (int s = 0; s < kMaxSteps; ++s) {
+        for (int g = 0; g < G; ++g) acc[t][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s) {
         if (s >= nsteps) continue;  // wave-uniform
         const int p = s * 4 + kq;
 #pragma unroll
         for (int g = 0; g < G; ++g) {
             const int pos = (g * 16 + col) * ksl + (p ^ col) * 8;
             const u32x4 bh = *reinterpret_cast<const u32x4*>(xs + pos);
-            acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, A[s]),
-                                                             __builtin_bit_cast(bf16x8, bh), acc[g], 0, 0, 0);
-            if constexpr (VF32) {
-                const u32x4 bl = *reinterpret_cast<const u32x4*>(xs + NCOL * ksl + pos);
-                acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, A[s]),
-                                                                 __builtin_bit_cast(bf16x8, bl), acc[g], 0, 0, 0);
+            u32x4 bl{0u, 0u, 0u, 0u};
+            if constexpr (VF32) bl = *reinterpret_cast<const u32x4*>(xs + NCOL * ksl + pos);
+#pragma unroll
+            for (int t = 0; t < TT; ++t) {
+                acc[t][g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, A[t][s]),
+                                                                    __builtin_bit_cast(bf16x8, bh), acc[t][g], 0, 0, 0);
+                if constexpr (VF32)
+                    acc[t][g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, A[t][s]), __builtin_bit_cast(bf16x8, bl), acc[t][g], 0, 0, 0);
             }
         }
     }
     // partial sums of this slice: part[slice][b][row]; D row 4 * kq + r, column col
     float* pp = part + (int64_t)blockIdx.y * B * n;
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-        const int b = g * 16 + col;
-        if (b >= B) continue;
+    for (int t = 0; t < TT; ++t)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = r0 + 4 * kq + r;
-            if (row < n) pp[(int64_t)b * n + row] = acc[g][r];
+        for (int g = 0; g < G; ++g) {
+            const int b = g * 16 + col;
+            if (b >= B) continue;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = r0 + t * kMfmaRows + 4 * kq + r;
+                if (row < n) pp[(int64_t)b * n + row] = acc[t][g][r];
+            }
         }
-    }
 }
 
 // out[b * ld + r] = act(sum over slices, in slice order, + bias[r])
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int slices, int B, int n,
                                                             float* __restrict__ out, int64_t ld,
                                                             const float* __restrict__ bias, int act) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= (int64_t)B * n) return;
-    const int b = (int)(i / n), r = (int)(i - (int64_t)b * n);
+    const int r = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+    if (r >= n) return;
     float s = 0.0f;
 #pragma unroll 8
     for (int q = 0; q < slices; ++q) s += part[((int64_t)q * B + b) * n + r];
     out[(int64_t)b * ld + r] = apply_act(s + (bias ? bias[r] : 0.0f), act);
 }
 
-template <int NW, int G, bool VF32>
+template <int NW, int G, bool VF32, int TT>
 dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* part, hipStream_t stream) {
     const dim3 grid((unsigned)sh.row_tiles, (unsigned)sh.slices);
     const uint32_t lds = (uint32_t)sh.lds;
@@ -160,29 +177,32 @@ dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* pa
         int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "router: device");
         if (!(allowed.load() & (1ull << dev))) {
-            if (hipFuncSetAttribute((const void*)dense_splitk_kernel<NW, G, VF32>,
+            if (hipFuncSetAttribute((const void*)dense_splitk_kernel<NW, G, VF32, TT>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget) != hipSuccess)
                 return set_error(DYNA_ERR_HIP, "router: LDS attribute");
             allowed.fetch_or(1ull << dev);
         }
     }
-    dense_splitk_kernel<NW, G, VF32><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
+    dense_splitk_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
     const dyna_status st = check_launch("dense_splitk_kernel");
     if (st != DYNA_OK) return st;
-    const int64_t outs = (int64_t)a.B * a.n_rows;
-    splitk_reduce_kernel<<<dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, stream>>>(
+    splitk_reduce_kernel<<<dim3((unsigned)((a.n_rows + 255) / 256), (unsigned)a.B), dim3(256), 0, stream>>>(
         part, sh.slices, a.B, a.n_rows, a.out, a.ld, a.bias, a.act);
     return check_launch("splitk_reduce_kernel");
 }
 
 template <int NW, bool VF32>
 dyna_status launch_splitk_g(const RowdotArgs& a, const SplitShape& sh, float* part, hipStream_t stream) {
+    // the kernel's row tiles per wave must be the shape's (they bound the slice length)
+    if (sh.tiles == 2) {
+        if (sh.groups == 4) return launch_splitk_t<NW, 4, VF32, 2>(a, sh, part, stream);
+        return launch_splitk_t<NW, 8, VF32, 2>(a, sh, part, stream);
+    }
     switch (sh.groups) {
-        case 1: return launch_splitk_t<NW, 1, VF32>(a, sh, part, stream);
-        case 2: return launch_splitk_t<NW, 2, VF32>(a, sh, part, stream);
-        case 3:
-        case 4: return launch_splitk_t<NW, 4, VF32>(a, sh, part, stream);
-        default: return launch_splitk_t<NW, 8, VF32>(a, sh, part, stream);
+        case 1: return launch_splitk_t<NW, 1, VF32, 1>(a, sh, part, stream);
+        case 2: return launch_splitk_t<NW, 2, VF32, 1>(a, sh, part, stream);
+        case 4: return launch_splitk_t<NW, 4, VF32, 1>(a, sh, part, stream);
+        default: return launch_splitk_t<NW, 8, VF32, 1>(a, sh, part, stream);
     }
 }
 
@@ -194,13 +214,15 @@ bool splitk_shape(int32_t n_rows, int32_t K, int32_t B, bool vf32, SplitShape* o
     s.groups = (B + 15) / 16;
     if (s.groups == 3) s.groups = 4;
     if (s.groups > 4) s.groups = 8;
-    s.nw = n_rows >= 2048 ? 8 : 4;
-    s.row_tiles = (n_rows + 16 * s.nw - 1) / (16 * s.nw);
+    s.tiles = 1;  // row tiles per wave (two measured slower: fewer waves hide less latency)
+    s.nw = n_rows >= 2048 * s.tiles ? 8 : 4;
+    const int rows_per_block = 16 * s.nw * s.tiles;
+    s.row_tiles = (n_rows + rows_per_block - 1) / rows_per_block;
     // about 256 workgroups in all, slices of at least one quantum, and the
     // staged slice within the LDS budget
     const int bytes_per_k = s.groups * 16 * 2 * (vf32 ? 2 : 1);
-    const int ksl_max = std::min(kMaxSteps * 32, std::max(kSliceQuantum, (kLdsBudget / bytes_per_k) / kSliceQuantum *
-                                                                         kSliceQuantum));
+    const int ksl_max = std::min(max_steps(s.tiles) * 32,
+                                 std::max(kSliceQuantum, (kLdsBudget / bytes_per_k) / kSliceQuantum * kSliceQuantum));
     const int want_slices = std::max(1, (256 + s.row_tiles - 1) / s.row_tiles);
     int ksl = (K + want_slices - 1) / want_slices;
     ksl = (ksl + kSliceQuantum - 1) / kSliceQuantum * kSliceQuantum;

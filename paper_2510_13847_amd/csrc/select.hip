@@ -170,18 +170,29 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         if (cnt[m] > 0) rc += (offs[m + 1] - offs[m] + kChunkRows - 1) / kChunkRows;
     }
     __syncthreads();
-    // chunk descriptors, all threads together: chunk c belongs to the last
-    // cluster whose first chunk is <= c (clusters without contexts have none)
-    for (int c = t; c < n_chunks; c += kPlanThreads) {
+    // chunk descriptors, all threads together: thread t writes an equal range
+    // of chunk indices; one binary search finds the cluster of its first chunk
+    // (the last cluster whose first chunk is <= c), then it walks forward
+    const int per_c = (n_chunks + kPlanThreads - 1) / kPlanThreads;
+    const int c0 = min(n_chunks, t * per_c), c1 = min(n_chunks, c0 + per_c);
+    if (c0 < c1) {
         int lo = 0, hi = M - 1;
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
-            if (coff[mid] <= c) lo = mid; else hi = mid - 1;
+            if (coff[mid] <= c0) lo = mid; else hi = mid - 1;
         }
         while (lo > 0 && cnt[lo] == 0) --lo;  // equal offsets: the cluster that owns the chunks
-        const int ci = c - coff[lo];
-        const int o = offs[lo], n = offs[lo + 1] - o;
-        plan.chunks[c] = Chunk{o + ci * kChunkRows, min(kChunkRows, n - ci * kChunkRows), loff[lo], cnt[lo]};
+        int m = lo;  // cluster 0 may have no contexts (then it owns no chunks)
+        int mend = coff[m] + (cnt[m] > 0 ? (offs[m + 1] - offs[m] + kChunkRows - 1) / kChunkRows : 0);
+        for (int c = c0; c < c1; ++c) {
+            while (c >= mend) {  // next cluster with contexts
+                ++m;
+                if (cnt[m] > 0) mend = coff[m] + (offs[m + 1] - offs[m] + kChunkRows - 1) / kChunkRows;
+            }
+            const int ci = c - coff[m];
+            const int o = offs[m], n = offs[m + 1] - o;
+            plan.chunks[c] = Chunk{o + ci * kChunkRows, min(kChunkRows, n - ci * kChunkRows), loff[m], cnt[m]};
+        }
     }
     __syncthreads();
     for (int m = t; m < M; m += kPlanThreads) cnt[m] = 0;
@@ -193,19 +204,20 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
             const int64_t e = e0 + q * kPlanThreads + t;
             mv[q] = e < n_sel ? sel_sorted[e] : -1;
         }
+        int bq[kPlanPer];
 #pragma unroll
         for (int q = 0; q < kPlanPer; ++q) {
-            const int64_t e = e0 + q * kPlanThreads + t;
-            const int64_t b = e / k, i = e - b * k;
-            ro[q] = (mv[q] >= 0 && mv[q] < M) ? sel_rowoff[b * (k + 1) + i] : 0;
+            const uint32_t e = (uint32_t)(e0 + q * kPlanThreads + t);  // B * k < 2^31
+            const uint32_t b = e / (uint32_t)k, i = e - b * (uint32_t)k;
+            bq[q] = (int)b;
+            ro[q] = (mv[q] >= 0 && mv[q] < M) ? sel_rowoff[(size_t)b * (k + 1) + i] : 0;
         }
 #pragma unroll
         for (int q = 0; q < kPlanPer; ++q) {
             const int m = mv[q];
             if (m < 0 || m >= M) continue;
-            const int64_t e = e0 + q * kPlanThreads + t;
             const int p = atomicAdd(&cnt[m], 1);
-            plan.list[loff[m] + p] = ListEntry{(int32_t)(e / k), ro[q] - offs[m]};
+            plan.list[loff[m] + p] = ListEntry{bq[q], ro[q] - offs[m]};
         }
     }
     if (t == 0) {

@@ -97,6 +97,87 @@ __device__ void block_topk_rounds(uint64_t (&list)[L], int k_t, uint64_t* cand /
     __syncthreads();
 }
 
+// Exact top-k_t of per-thread keys held in registers (P per thread, 0 =
+// empty; valid keys are distinct and nonzero), by radix selection from the
+// most significant byte: each pass counts, among the keys that share the
+// prefix fixed so far, the values of the next byte, and fixes the byte that
+// holds the k_t-th largest key.  The search stops as soon as the keys sharing
+// the prefix are exactly the ones still needed.  The selected keys, sorted
+// descending, go to out[0..k_t); missing ones (short rows) are 0.
+template <int NT, int P>
+__device__ void block_radix_topk(const uint64_t (&kk)[P], int k_t, int n_valid, int* hist /* LDS [256] */,
+                                 uint64_t* sel /* LDS [k_t] */, uint64_t* out /* LDS [k_t] */) {
+    __shared__ uint64_t sh_prefix;
+    __shared__ int sh_need, sh_done, sh_n;
+    uint64_t prefix = 0;
+    int shift = 64;
+    if (n_valid > k_t) {
+        uint64_t mask = 0;
+        int need = k_t;
+        for (int byte = 7; byte >= 0; --byte) {
+            for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0;
+            __syncthreads();
+            const int sh = 8 * byte;
+#pragma unroll
+            for (int q = 0; q < P; ++q)
+                if (kk[q] != 0 && (kk[q] & mask) == prefix) atomicAdd(&hist[(int)((kk[q] >> sh) & 255u)], 1);
+            __syncthreads();
+            if (threadIdx.x < kWave) {
+                // lane l holds digits 255-4l .. 252-4l (descending)
+                const int l = lane_id();
+                int c[4], sum = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    c[q] = hist[255 - 4 * l - q];
+                    sum += c[q];
+                }
+                const int inc = wave_inclusive_scan(sum);
+                const int exc = inc - sum;
+                if (exc < need && need <= inc) {
+                    int acc = exc;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (acc + c[q] >= need) {
+                            sh_prefix = prefix | ((uint64_t)(255 - 4 * l - q) << sh);
+                            sh_need = need - acc;
+                            sh_done = c[q] == need - acc;
+                            break;
+                        }
+                        acc += c[q];
+                    }
+                }
+            }
+            __syncthreads();
+            prefix = sh_prefix;
+            need = sh_need;
+            mask |= (uint64_t)255u << sh;
+            shift = sh;
+            const int done = sh_done;
+            __syncthreads();  // every thread has read the shared values
+            if (done) break;
+        }
+    }
+    if (threadIdx.x == 0) sh_n = 0;
+    __syncthreads();
+    // selected: the keys whose bits from `shift` up are at least the prefix's
+#pragma unroll
+    for (int q = 0; q < P; ++q)
+        if (kk[q] != 0 && (shift == 64 || (kk[q] >> shift) >= (prefix >> shift))) sel[atomicAdd(&sh_n, 1)] = kk[q];
+    __syncthreads();
+    const int n = sh_n;  // k_t, or fewer for a short row
+    for (int i = threadIdx.x; i < k_t; i += NT) {
+        if (i >= n) {
+            out[i] = 0;
+            continue;
+        }
+        const uint64_t key = sel[i];
+        int rank = 0;
+        for (int j = 0; j < n; ++j) rank += sel[j] > key;
+        out[rank] = key;
+    }
+    __syncthreads();
+}
+
 // Whole-row selection in one workgroup (shortlist-sized rows, k_t <= KT).
 // Max, top-k_t and the softmax sum read the row with coalesced strided loads;
 // only the sampling walk uses contiguous per-thread ranges, so that the CDF
@@ -139,37 +220,50 @@ __device__ void select_row(const SelectArgs& a, int b) {
         return (uint32_t)a.perm[t_base[lo] + j];
     };
 
-    uint64_t list[KT];
+    constexpr int kRegPer = 8;  // rows up to NT * kRegPer slots keep their keys in registers
+    if (KT > 1 && len <= NT * kRegPer) {
+        __shared__ int rhist[256];
+        __shared__ uint64_t rsel[KT];
+        uint64_t kk[kRegPer];
 #pragma unroll
-    for (int q = 0; q < KT; ++q) list[q] = 0;
-    // kLoadPer slots per thread per batch, their loads issued together
-    constexpr int kLoadPer = 4;
-    for (int j0 = 0; j0 < len; j0 += NT * kLoadPer) {
-        float zq[kLoadPer];
-        uint32_t vq[kLoadPer];
-#pragma unroll
-        for (int q = 0; q < kLoadPer; ++q) {
-            const int j = j0 + q * NT + threadIdx.x;
-            zq[q] = j < len ? z[j] : 0.0f;
-            vq[q] = j < len ? vid_of(j) : 0u;
+        for (int q = 0; q < kRegPer; ++q) {
+            const int j = q * NT + threadIdx.x;
+            kk[q] = j < len ? sel_key(canon(z[j]), vid_of(j)) : 0;
         }
+        block_radix_topk<NT, kRegPer>(kk, a.k_t, len, rhist, rsel, top);
+    } else {
+        uint64_t list[KT];
 #pragma unroll
-        for (int q = 0; q < kLoadPer; ++q) {
-            if (j0 + q * NT + (int)threadIdx.x >= len) continue;
-            const uint64_t key = sel_key(canon(zq[q]), vq[q]);
-            if (key > list[KT - 1]) {
-                list[KT - 1] = key;
+        for (int q = 0; q < KT; ++q) list[q] = 0;
+        // kLoadPer slots per thread per batch, their loads issued together
+        constexpr int kLoadPer = 4;
+        for (int j0 = 0; j0 < len; j0 += NT * kLoadPer) {
+            float zq[kLoadPer];
+            uint32_t vq[kLoadPer];
 #pragma unroll
-                for (int r = KT - 1; r > 0; --r)
-                    if (list[r] > list[r - 1]) {
-                        const uint64_t t = list[r];
-                        list[r] = list[r - 1];
-                        list[r - 1] = t;
-                    }
+            for (int q = 0; q < kLoadPer; ++q) {
+                const int j = j0 + q * NT + threadIdx.x;
+                zq[q] = j < len ? z[j] : 0.0f;
+                vq[q] = j < len ? vid_of(j) : 0u;
+            }
+#pragma unroll
+            for (int q = 0; q < kLoadPer; ++q) {
+                if (j0 + q * NT + (int)threadIdx.x >= len) continue;
+                const uint64_t key = sel_key(canon(zq[q]), vq[q]);
+                if (key > list[KT - 1]) {
+                    list[KT - 1] = key;
+#pragma unroll
+                    for (int r = KT - 1; r > 0; --r)
+                        if (list[r] > list[r - 1]) {
+                            const uint64_t t = list[r];
+                            list[r] = list[r - 1];
+                            list[r - 1] = t;
+                        }
+                }
             }
         }
+        block_topk_rounds<KT, NT, KT>(list, a.k_t, cand, top);
     }
-    block_topk_rounds<KT, NT, KT>(list, a.k_t, cand, top);
     const float mx = top[0] != 0 ? key_val(top[0]) : -__builtin_inff();
     const bool sampling = a.uniforms != nullptr && a.out_sample != nullptr;
 

@@ -51,6 +51,8 @@ CASES = [
     case("relu_b2", V=1500, d=128, M=16, H=32, act="relu", k=3, B=2),
     case("zipf_b9", V=6000, d=96, M=12, sizes=("zipf", 1.1, 1500), H=16, k=3, B=9),
     case("wide_k_b4", V=4096, d=512, M=64, H=64, k=64, B=4),  # k = M: shortlist = V
+    # split-K router with four column groups and several k slices
+    case("wide_b64", V=4000, d=520, M=40, H=48, k=4, B=64),
     # more contexts than one MFMA column pass (and than the split-K router takes)
     case("many_b130", V=3000, d=136, M=24, H=32, k=3, B=130),
 ]
