@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define DYNA_ABI_VERSION 1
+#define DYNA_ABI_VERSION 2
 #define DYNA_MAX_M 8192     /* clusters */
 #define DYNA_MAX_KT 64      /* tokens per context in top-k output */
 
@@ -176,12 +176,20 @@ dyna_status dyna_shortlist_logits(const dyna_layout* L, const void* h, int32_t h
  *  out_sample [B]      device output (SAMPLE): first j in shortlist order whose
  *                      CDF exceeds u, else the last j with nonzero mass
  *  out_sample_logprob [B] device output, may be NULL
+ *  tail_beta           weight beta in [0, 1) of the tail mixture proposal
+ *                      q~ = (1 - beta) q_S + beta omega (Sec. 5), omega uniform
+ *                      on the row's complement V \ S; 0 gives q_S.  Top-k ids
+ *                      stay in the shortlist and their log-probabilities are
+ *                      those of q~.  The sample takes the shortlist branch when
+ *                      u < 1 - beta (at u / (1 - beta)), else complement entry
+ *                      floor((u - (1 - beta)) / beta * |V \ S|), the complement
+ *                      in layout order; an empty complement (k = M) has no tail.
  *  ws                  workspace of dyna_workspace_bytes(L, NULL, B, k, cap) bytes
  * 1 <= k_t <= DYNA_MAX_KT; temperature > 0. */
 dyna_status dyna_draft_select(const dyna_layout* L, const float* logits,
                               const int32_t* sel_sorted, const int32_t* sel_rowoff,
                               const int32_t* row_len, int32_t B, int32_t k, int32_t cap,
-                              int32_t mode, int32_t k_t, float temperature,
+                              int32_t mode, int32_t k_t, float temperature, float tail_beta,
                               const float* uniforms, int32_t* out_ids, float* out_logprobs,
                               int32_t* out_sample, float* out_sample_logprob,
                               void* ws, size_t ws_bytes, hipStream_t stream);
@@ -206,7 +214,7 @@ dyna_status dyna_draft_select(const dyna_layout* L, const float* logits,
 dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
                             const void* x, const void* h, int32_t adtype,
                             int32_t B, int32_t k, int32_t mode, int32_t k_t,
-                            float temperature, const float* uniforms,
+                            float temperature, float tail_beta, const float* uniforms,
                             int32_t* out_ids, float* out_logprobs, int32_t* out_sample,
                             float* out_sample_logprob, int32_t* out_clusters,
                             float* out_logits, int32_t cap, void* ws, size_t ws_bytes,
@@ -230,6 +238,25 @@ dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_rows, int32
                             int32_t* out_ids, float* out_logprobs, int32_t* out_sample,
                             float* out_sample_logprob, float* out_logits,
                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ */
+/* Position-aware budgets (host functions, no GPU work).               */
+/* ------------------------------------------------------------------ */
+
+/* Cluster budget k_c(t) at draft position t (Sec. 4.2, eq. pos_schedule):
+ * k0 at t = 0, k1 at t = 1, then floor((k1 + t) / (2t)) (form 0), or the
+ * appendix algorithm's floor(k1 / (2t)) (form 1, its loop index read as the
+ * draft position).  The result is clamped below at k_min: the text bounds
+ * k_c(t) by k_min while both formulas reach 0 for large t.  Returns -1 for
+ * t < 0, k0 < 1, k1 < 1, k_min < 1 or another form.  The value is the k a
+ * caller passes to dyna_draft_head for that position. */
+int32_t dyna_cluster_budget(int32_t t, int32_t k0, int32_t k1, int32_t k_min, int32_t form);
+
+/* Shortlist size K_fr(t) of the position-aware frequency-ranked static head
+ * (appendix, PA-FR): k_max for t in {0, 1}, then floor(k_max / (t + 1)).
+ * Returns -1 for t < 0 or k_max < 1.  The value is the n_rows a caller
+ * passes to dyna_dense_head for the static head at that position. */
+int32_t dyna_static_budget(int32_t t, int32_t k_max);
 
 /* ------------------------------------------------------------------ */
 /* Diagnostics.                                                        */

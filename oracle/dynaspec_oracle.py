@@ -224,27 +224,53 @@ def sample_cdf(z, temperature: float = 1.0) -> np.ndarray:
     return np.cumsum(p / p.sum())
 
 
-def draft_select(z, vocab_ids, k_t: int = 1, temperature: float = 1.0, u=None):
+def draft_select(z, vocab_ids, k_t: int = 1, temperature: float = 1.0, u=None, beta: float = 0.0,
+                 complement_ids=None):
     """Draft outputs of one context over its shortlist.
 
     Returns dict(ids[k_t], logprobs[k_t], positions[k_t], sample_id,
     sample_pos, sample_logprob); ids are vocabulary ids (remap2realid).
+
+    With beta > 0 the proposal is the tail mixture of Sec. 5,
+    q~ = (1 - beta) q_S + beta * omega, omega uniform on the complement
+    V \ S given by complement_ids (in layout order).  Top-k positions stay in
+    the shortlist, with log-probabilities under q~.  The sample takes the
+    shortlist branch when u < 1 - beta (at u / (1 - beta)), else complement
+    entry floor((u - (1 - beta)) / beta * |V \ S|) (sample_pos = -1).  An empty
+    complement leaves q~ = q_S.
     """
     vocab_ids = np.asarray(vocab_ids, dtype=np.int64)
-    lp = log_softmax(z, temperature)
+    C = 0 if complement_ids is None else len(complement_ids)
+    b = float(beta) if (beta > 0.0 and C > 0) else 0.0
+    lp = log_softmax(z, temperature) + (np.log1p(-b) if b > 0.0 else 0.0)
     pos = topk_tokens(z, vocab_ids, k_t)
     out = dict(ids=vocab_ids[pos], logprobs=lp[pos], positions=pos)
     if u is not None:
-        j = sample_inverse_cdf(z, float(u), temperature)
-        out.update(sample_id=int(vocab_ids[j]), sample_pos=j, sample_logprob=float(lp[j]))
+        u = float(u)
+        if u < 1.0 - b:
+            j = sample_inverse_cdf(z, u / (1.0 - b), temperature)
+            out.update(sample_id=int(vocab_ids[j]), sample_pos=j, sample_logprob=float(lp[j]))
+        else:
+            jj = min(C - 1, int(np.floor((u - (1.0 - b)) / b * C)))
+            out.update(sample_id=int(complement_ids[jj]), sample_pos=-1,
+                       sample_logprob=float(np.log(b) - np.log(C)))
     return out
+
+
+def complement(offsets, perm, sel_sorted):
+    """Vocabulary ids outside the shortlist of clusters sel_sorted, in layout order."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    keep = np.ones(int(offsets[-1]), dtype=bool)
+    for m in np.asarray(sel_sorted, dtype=np.int64):
+        keep[offsets[m]:offsets[m + 1]] = False
+    return np.asarray(perm, dtype=np.int64)[np.nonzero(keep)[0]]
 
 
 # --------------------------------------------------------------------------
 # whole head and the two baselines
 # --------------------------------------------------------------------------
 def draft_head(x, h, W1, W2, act, cluster_of, M, W_lm, k, k_t=1, temperature=1.0,
-               u=None, b1=None, b2=None):
+               u=None, b1=None, b2=None, beta: float = 0.0):
     """The dynamic draft head for a batch: route, shortlist, logits, select.
 
     Returns a list (one dict per context row) with the router's cluster ids,
@@ -258,7 +284,8 @@ def draft_head(x, h, W1, W2, act, cluster_of, M, W_lm, k, k_t=1, temperature=1.0
     for b in range(h.shape[0]):
         sel, rowoff, rows, vids = shortlist(ids[b], offsets, perm)
         z = shortlist_logits(h[b], W_lm, vids)
-        r = draft_select(z, vids, k_t, temperature, None if u is None else u[b])
+        comp = complement(offsets, perm, sel) if beta > 0.0 else None
+        r = draft_select(z, vids, k_t, temperature, None if u is None else u[b], beta, comp)
         r.update(clusters=ids[b], cluster_scores=vals[b], sel_sorted=sel, rowoff=rowoff,
                  layout_rows=rows, vocab_ids=vids, logits=z, scores=s[b])
         out.append(r)
@@ -287,12 +314,30 @@ def dense_head(h, W_lm, k_t=1, temperature=1.0, u=None, n_rows=None):
 # --------------------------------------------------------------------------
 # position-aware cluster budget (Sec. 4.2, eq. pos_schedule; Algorithm 1)
 # --------------------------------------------------------------------------
-def k_schedule(t: int, k0: int, k1: int, k_min: int = 1) -> int:
+def k_schedule(t: int, k0: int, k1: int, k_min: int = 1, form: str = "equation") -> int:
     """Cluster budget at draft position t: k0, k1, then floor((k1 + t) / (2t)),
     clamped below at k_min (the equation reaches 0 for large t while the
-    text bounds the budget by k_min)."""
+    text bounds the budget by k_min).  form="algorithm1" takes the appendix
+    algorithm's floor(k1 / (2t)) for t >= 2 instead (its undefined index read
+    as the draft position)."""
     if t == 0:
         return k0
     if t == 1:
         return k1
-    return max(k_min, (k1 + t) // (2 * t))
+    if form == "equation":
+        return max(k_min, (k1 + t) // (2 * t))
+    if form == "algorithm1":
+        return max(k_min, k1 // (2 * t))
+    raise ValueError(form)
+
+
+# --------------------------------------------------------------------------
+# position-aware frequency-ranked static shortlist (appendix, PA-FR)
+# --------------------------------------------------------------------------
+def pa_fr_budget(t: int, k_max: int) -> int:
+    """Static shortlist size at draft position t: k_max for t in {0, 1}, then
+    floor(k_max / (t + 1)); the shortlist is the K most frequent ids (here the
+    first K ids of the vocabulary, see dense_head)."""
+    if t < 2:
+        return k_max
+    return k_max // (t + 1)

@@ -526,13 +526,15 @@ DYNA_API dyna_status dyna_shortlist_logits(const dyna_layout* L, const void* h, 
 DYNA_API dyna_status dyna_draft_select(const dyna_layout* L, const float* logits, const int32_t* sel_sorted,
                                        const int32_t* sel_rowoff, const int32_t* row_len, int32_t B, int32_t k,
                                        int32_t cap, int32_t mode, int32_t k_t, float temperature,
-                                       const float* uniforms, int32_t* out_ids, float* out_logprobs,
+                                       float tail_beta, const float* uniforms, int32_t* out_ids,
+                                       float* out_logprobs,
                                        int32_t* out_sample, float* out_sample_logprob, void* ws,
                                        size_t ws_bytes, hipStream_t stream) {
     TRY(check_layout(L));
     TRY(check_k(L, k));
     TRY(check_cap(L, k, cap));
     TRY(check_select(mode, &k_t, temperature, uniforms, out_ids, out_sample));
+    REQUIRE(tail_beta >= 0.0f && tail_beta < 1.0f, "tail_beta must lie in [0, 1)");
     REQUIRE(B >= 0, "B=%d < 0", B);
     if (B == 0) return DYNA_OK;
     REQUIRE(logits && sel_sorted && sel_rowoff && row_len && ws, "NULL argument");
@@ -542,14 +544,15 @@ DYNA_API dyna_status dyna_draft_select(const dyna_layout* L, const float* logits
     const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
     const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     return launch_select(logits, cap, row_len, 0, cap, sel_sorted, sel_rowoff, L->offsets, L->perm, B, k,
-                         k_t, temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
+                         k_t, temperature, tail_beta, L->V, want_sample ? uniforms : nullptr,
+                         want_ids ? out_ids : nullptr,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
                          want_sample ? out_sample_logprob : nullptr, c.select_ws, stream);
 }
 
 DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L, const void* x, const void* h,
                                      int32_t adtype, int32_t B, int32_t k, int32_t mode, int32_t k_t,
-                                     float temperature, const float* uniforms, int32_t* out_ids,
+                                     float temperature, float tail_beta, const float* uniforms, int32_t* out_ids,
                                      float* out_logprobs, int32_t* out_sample, float* out_sample_logprob,
                                      int32_t* out_clusters, float* out_logits, int32_t cap, void* ws,
                                      size_t ws_bytes, hipStream_t stream, hipStream_t route_stream,
@@ -561,6 +564,7 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     TRY(check_k(L, k));
     TRY(check_cap(L, k, cap));
     TRY(check_select(mode, &k_t, temperature, uniforms, out_ids, out_sample));
+    REQUIRE(tail_beta >= 0.0f && tail_beta < 1.0f, "tail_beta must lie in [0, 1)");
     REQUIRE(valid_dtype(adtype), "bad adtype %d", adtype);
     REQUIRE(B >= 0, "B=%d < 0", B);
     if (B == 0) return DYNA_OK;
@@ -616,15 +620,30 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     a.vid_out = c.slot_vid;
     const SelectArgs sa = make_select_args(
         logits, cap, c.row_len, 0, cap, c.sel_sorted, c.sel_rowoff, L->offsets, L->perm, B, k, k_t,
-        temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
+        temperature, tail_beta, L->V, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
         want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
         want_sample ? out_sample_logprob : nullptr, c.select_ws, c.slot_vid);
     if (fused) return timed([&] { return launch_logits_greedy(a, sa, c.partials, c.counters, stream); }, stream);
     TRY(timed_rowdot(a, option_logits_path(), stream));
     return launch_select(logits, cap, c.row_len, 0, cap, c.sel_sorted, c.sel_rowoff, L->offsets, L->perm, B,
-                         k, k_t, temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
+                         k, k_t, temperature, tail_beta, L->V, want_sample ? uniforms : nullptr,
+                         want_ids ? out_ids : nullptr,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
                          want_sample ? out_sample_logprob : nullptr, c.select_ws, stream, c.slot_vid);
+}
+
+// ------------------------------------------------------------------ budgets
+DYNA_API int32_t dyna_cluster_budget(int32_t t, int32_t k0, int32_t k1, int32_t k_min, int32_t form) {
+    if (t < 0 || k0 < 1 || k1 < 1 || k_min < 1 || (form != 0 && form != 1)) return -1;
+    if (t == 0) return k0;
+    if (t == 1) return k1;
+    const int64_t num = form == 0 ? (int64_t)k1 + t : (int64_t)k1;
+    return (int32_t)std::max<int64_t>(k_min, num / (2 * (int64_t)t));
+}
+
+DYNA_API int32_t dyna_static_budget(int32_t t, int32_t k_max) {
+    if (t < 0 || k_max < 1) return -1;
+    return t < 2 ? k_max : (int32_t)((int64_t)k_max / ((int64_t)t + 1));
 }
 
 // ------------------------------------------------------------------ baselines
@@ -679,7 +698,7 @@ DYNA_API dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_ro
     const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
     const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     return launch_select(logits, n_rows, nullptr, n_rows, n_rows, nullptr, nullptr, nullptr, nullptr, B, 0, k_t,
-                         temperature, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
+                         temperature, 0.0f, n_rows, want_sample ? uniforms : nullptr, want_ids ? out_ids : nullptr,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
                          want_sample ? out_sample_logprob : nullptr, sel, stream);
 }

@@ -161,6 +161,8 @@ struct SelectArgs {
     int32_t k_t;
     float inv_t;
     const float* uniforms;
+    float beta;               // tail weight of the mixture proposal (0: none)
+    int32_t V;                // vocabulary rows (the complement is V - row length)
     int32_t P;                // segments per row
     // partials, [B][P][...]
     uint64_t* pkeys;          // [B][P][k_t]
@@ -191,7 +193,7 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
                           int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
                           const int32_t* sel_rowoff, const int32_t* offsets,
                           const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
-                          float temperature, const float* uniforms, int32_t* out_ids,
+                          float temperature, float beta, int32_t V, const float* uniforms, int32_t* out_ids,
                           float* out_logprobs, int32_t* out_sample,
                           float* out_sample_logprob, void* ws, hipStream_t stream,
                           // optional [B, ld]: vocabulary id of every slot (written
@@ -206,7 +208,7 @@ SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_
                             int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
                             const int32_t* sel_rowoff, const int32_t* offsets,
                             const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
-                            float temperature, const float* uniforms, int32_t* out_ids,
+                            float temperature, float beta, int32_t V, const float* uniforms, int32_t* out_ids,
                             float* out_logprobs, int32_t* out_sample,
                             float* out_sample_logprob, void* ws, const int32_t* slot_vid);
 // True when the one-workgroup select handles rows of max_len slots.

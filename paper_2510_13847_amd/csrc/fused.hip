@@ -127,8 +127,11 @@ __global__ __launch_bounds__(kThreads) void logits_greedy_kernel(RowdotArgs lg, 
             softmax_merge(fm, fs, w_m[q], w_s[q], sa.inv_t);
         }
         if (sa.out_ids) sa.out_ids[0] = fb != 0 ? (int32_t)key_id(fb) : -1;
-        if (sa.out_logprobs)
-            sa.out_logprobs[0] = fb != 0 ? (key_val(fb) - fm) * sa.inv_t - logf(fs) : -__builtin_inff();
+        if (sa.out_logprobs) {
+            const TailMix tail = tail_of(sa, sa.row_len ? sa.row_len[0] : sa.fixed_len);
+            sa.out_logprobs[0] =
+                fb != 0 ? (key_val(fb) - fm) * sa.inv_t - logf(fs) + tail.lshift : -__builtin_inff();
+        }
     }
 }
 

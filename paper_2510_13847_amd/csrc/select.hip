@@ -329,7 +329,8 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     }
     __syncthreads();
     const float mx = sh_mx, total = sh_total;
-    const float log_total = logf(total);
+    const TailMix tail = tail_of(a, len);
+    const float log_total = logf(total) - tail.lshift;
     if (a.out_ids != nullptr) {
         for (int r = threadIdx.x; r < a.k_t; r += kNT) {
             const uint64_t key = top[r];
@@ -340,10 +341,12 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
         }
     }
     if (a.uniforms == nullptr || a.out_sample == nullptr) return;
+    float u_s;
+    if (tail_sample(a, b, tail, &u_s)) return;  // uniform decision for the block
 
     // inverse CDF: first segment whose running mass passes u * total
     if (threadIdx.x == 0) {
-        const float target = a.uniforms[b] * total;
+        const float target = u_s * total;
         float run = 0.0f;
         int seg = -1, last_nz = -1;
         float base = 0.0f, base_last = 0.0f;
@@ -492,7 +495,7 @@ SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_
                             int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
                             const int32_t* sel_rowoff, const int32_t* offsets,
                             const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
-                            float temperature, const float* uniforms, int32_t* out_ids,
+                            float temperature, float beta, int32_t V, const float* uniforms, int32_t* out_ids,
                             float* out_logprobs, int32_t* out_sample,
                             float* out_sample_logprob, void* ws, const int32_t* slot_vid) {
     SelectArgs a;
@@ -509,6 +512,8 @@ SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_
     a.k_t = k_t;
     a.inv_t = 1.0f / temperature;
     a.uniforms = uniforms;
+    a.beta = beta;
+    a.V = V;
     a.P = (int32_t)std::max<int64_t>(1, ((int64_t)max_len + kSeg - 1) / kSeg);
     char* p = static_cast<char*>(ws);
     a.pkeys = reinterpret_cast<uint64_t*>(p);
@@ -531,12 +536,12 @@ bool select_row_fits(int32_t max_len, bool fixed, int32_t k_t, int32_t k) {
 dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_len,
                           int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
                           const int32_t* sel_rowoff, const int32_t* offsets, const int32_t* perm,
-                          int32_t B, int32_t k, int32_t k_t, float temperature,
+                          int32_t B, int32_t k, int32_t k_t, float temperature, float beta, int32_t V,
                           const float* uniforms, int32_t* out_ids, float* out_logprobs,
                           int32_t* out_sample, float* out_sample_logprob, void* ws,
                           hipStream_t stream, const int32_t* slot_vid) {
     const SelectArgs a = make_select_args(logits, ld, row_len, fixed_len, max_len, sel_sorted,
-                                          sel_rowoff, offsets, perm, B, k, k_t, temperature,
+                                          sel_rowoff, offsets, perm, B, k, k_t, temperature, beta, V,
                                           uniforms, out_ids, out_logprobs, out_sample,
                                           out_sample_logprob, ws, slot_vid);
     // shortlist-sized rows: one workgroup per row, one launch

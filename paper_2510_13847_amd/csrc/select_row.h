@@ -14,6 +14,63 @@ constexpr int kRowMax = 1 << 17;    // longest shortlist row the one-launch sele
 
 __device__ __forceinline__ float canon(float z) { return z != z ? -__builtin_inff() : z; }
 
+// Tail mixture proposal (Sec. 5): q~ = (1 - beta) q_S + beta * omega, omega
+// uniform on the complement V \ S of the row's shortlist.  An empty
+// complement (the shortlist is the whole vocabulary) leaves q~ = q_S.
+struct TailMix {
+    float beta;    // weight in effect (0: none)
+    int64_t comp;  // complement size
+    float lshift;  // log(1 - beta), added to shortlist log-probabilities
+};
+__device__ __forceinline__ TailMix tail_of(const SelectArgs& a, int len) {
+    TailMix t{0.0f, 0, 0.0f};
+    if (a.beta > 0.0f && a.perm != nullptr && (int64_t)a.V > len) {
+        t.beta = a.beta;
+        t.comp = (int64_t)a.V - len;
+        t.lshift = log1pf(-a.beta);
+    }
+    return t;
+}
+
+// Vocabulary id of complement entry j of row b: layout rows in ascending
+// order, skipping the row's selected slabs (sel_sorted is ascending; dropped
+// entries are -1 at its end).
+__device__ __forceinline__ int32_t complement_vid(const SelectArgs& a, int b, int64_t j) {
+    const int32_t* ss = a.sel_sorted + (int64_t)b * a.k;
+    int64_t end_prev = 0;
+    for (int i = 0; i < a.k; ++i) {
+        const int m = ss[i];
+        if (m < 0) break;
+        const int64_t gap = (int64_t)a.offsets[m] - end_prev;
+        if (j < gap) break;
+        j -= gap;
+        end_prev = a.offsets[m + 1];
+    }
+    return a.perm[end_prev + j];
+}
+
+// Sample draw of row b under the tail mixture: true (and the outputs
+// written, by the calling thread) when u falls in the tail branch; else *u_s
+// is the uniform for the shortlist branch.
+__device__ __forceinline__ bool tail_sample(const SelectArgs& a, int b, const TailMix& t, float* u_s) {
+    const float u = a.uniforms[b];
+    if (t.beta <= 0.0f) {
+        *u_s = u;
+        return false;
+    }
+    if (u < 1.0f - t.beta) {
+        *u_s = u / (1.0f - t.beta);
+        return false;
+    }
+    int64_t j = (int64_t)floorf((u - (1.0f - t.beta)) / t.beta * (float)t.comp);
+    j = j < 0 ? 0 : (j >= t.comp ? t.comp - 1 : j);
+    if (threadIdx.x == 0) {
+        a.out_sample[b] = complement_vid(a, b, j);
+        if (a.out_sample_logprob) a.out_sample_logprob[b] = logf(t.beta) - logf((float)t.comp);
+    }
+    return true;
+}
+
 // Vocabulary ids of the slots [j0, j0 + n) of row b, written into vid[].
 __device__ __forceinline__ void slot_vids(const SelectArgs& a, int b, int j0, int n, uint32_t* vid) {
     if (a.slot_vid != nullptr) {
@@ -283,7 +340,8 @@ __device__ void select_row(const SelectArgs& a, int b) {
     }
     float total;
     const float incl = block_inclusive_scan_f32<NT>(tsum, red, &total);
-    const float log_total = logf(total);
+    const TailMix tail = tail_of(a, len);
+    const float log_total = logf(total) - tail.lshift;
     if (a.out_ids != nullptr) {
         for (int r = threadIdx.x; r < a.k_t; r += NT) {
             const uint64_t key = top[r];
@@ -294,12 +352,14 @@ __device__ void select_row(const SelectArgs& a, int b) {
         }
     }
     if (!sampling) return;
+    float u_s;
+    if (tail_sample(a, b, tail, &u_s)) return;  // uniform decision for the block
 
     incl_s[threadIdx.x] = incl;
     if (threadIdx.x == 0) sh_pick = -1;
     __syncthreads();
     const float excl = threadIdx.x > 0 ? incl_s[threadIdx.x - 1] : 0.0f;
-    const float target = a.uniforms[b] * total;
+    const float target = u_s * total;
     if (tsum > 0.0f && excl <= target && target < incl) {
         float acc = excl;
         int pick = -1, last = -1;

@@ -45,6 +45,7 @@ class _Router(ctypes.Structure):
 
 
 _lib = None
+ABI_VERSION = 2  # DYNA_ABI_VERSION of include/dynahead.h
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
@@ -63,11 +64,13 @@ _SIGNATURES = {
     "dyna_route": (_I, [_P, _P, _I, _I, _I, _P, _P, _P, _P, _Z, _P]),
     "dyna_shortlist": (_I, [_P, _P, _I, _I, _P, _P, _P, _P, _I, _P]),
     "dyna_shortlist_logits": (_I, [_P, _P, _I, _I, _I, _P, _P, _P, _P, _I, _P, _Z, _P]),
-    "dyna_draft_select": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P,
+    "dyna_draft_select": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _F, _P, _P, _P, _P, _P,
                                _P, _Z, _P]),
-    "dyna_draft_head": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P,
+    "dyna_draft_head": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _F, _P, _P, _P, _P, _P, _P, _P,
                              _I, _P, _Z, _P, _P, _P]),
     "dyna_dense_workspace_bytes": (_Z, [_I, _I]),
+    "dyna_cluster_budget": (_I, [_I, _I, _I, _I, _I]),
+    "dyna_static_budget": (_I, [_I, _I]),
     "dyna_dense_head": (_I, [_P, _I, _I, _I, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P,
                              _Z, _P]),
 }
@@ -86,7 +89,7 @@ def lib():
             f = getattr(L, name)
             f.restype = res
             f.argtypes = args
-        if L.dyna_abi_version() != 1:
+        if L.dyna_abi_version() != ABI_VERSION:
             raise RuntimeError("libdynahead ABI version mismatch")
         _lib = L
     return _lib
@@ -288,7 +291,7 @@ def _select_outputs(B, k_t, mode, dev):
 
 
 def draft_select(layout: Layout, logits, sel_sorted, sel_rowoff, row_len, mode=SEL_TOPK, k_t=1,
-                 temperature=1.0, uniforms=None, cap=None, ws=None, stream=None):
+                 temperature=1.0, uniforms=None, cap=None, ws=None, stream=None, tail_beta=0.0):
     """dyna_draft_select -> dict(ids, logprobs, sample, sample_logprob)."""
     B, k = sel_sorted.shape
     cap = logits.shape[1] if cap is None else cap
@@ -297,7 +300,7 @@ def draft_select(layout: Layout, logits, sel_sorted, sel_rowoff, row_len, mode=S
     if ws is None:
         ws = workspace(layout, None, B, k, cap, dev)
     _check(lib().dyna_draft_select(layout.c, _ptr(logits), _ptr(sel_sorted), _ptr(sel_rowoff),
-                                   _ptr(row_len), B, k, cap, mode, k_t, temperature,
+                                   _ptr(row_len), B, k, cap, mode, k_t, temperature, tail_beta,
                                    _ptr(uniforms), _ptr(ids), _ptr(lps), _ptr(smp), _ptr(slp),
                                    _ptr(ws), ws.numel(), _stream(stream)))
     return dict(ids=ids, logprobs=lps, sample=smp, sample_logprob=slp)
@@ -307,10 +310,11 @@ class DraftHead:
     """Preallocated outputs + workspace for repeated dyna_draft_head calls."""
 
     def __init__(self, router: Router, layout: Layout, B: int, k: int, mode: int, k_t: int = 1,
-                 temperature: float = 1.0, keep_logits=False, keep_clusters=True, device="cuda"):
+                 temperature: float = 1.0, keep_logits=False, keep_clusters=True, device="cuda",
+                 tail_beta: float = 0.0):
         import torch
         self.router, self.layout, self.B, self.k = router, layout, B, k
-        self.mode, self.k_t, self.temperature = mode, k_t, temperature
+        self.mode, self.k_t, self.temperature, self.tail_beta = mode, k_t, temperature, tail_beta
         self.cap = layout.cap(k)
         self.ids, self.logprobs, self.sample, self.sample_logprob = _select_outputs(B, k_t, mode, device)
         self.clusters = torch.empty((B, k), dtype=torch.int32, device=device) if keep_clusters else None
@@ -325,7 +329,7 @@ class DraftHead:
         rs = None if route_stream is None else route_stream.cuda_stream
         ev = None if x_ready is None else x_ready.cuda_event
         _check(lib().dyna_draft_head(R.c, L.c, _ptr(x), _ptr(h), _dtype_code(h), self.B, self.k,
-                                     self.mode, self.k_t, self.temperature, _ptr(uniforms),
+                                     self.mode, self.k_t, self.temperature, self.tail_beta, _ptr(uniforms),
                                      _ptr(self.ids), _ptr(self.logprobs), _ptr(self.sample),
                                      _ptr(self.sample_logprob), _ptr(self.clusters),
                                      _ptr(self.logits), self.cap, _ptr(self.ws), self.ws.numel(),
@@ -334,10 +338,11 @@ class DraftHead:
 
 
 def draft_head(router: Router, layout: Layout, x, h, k: int, mode=SEL_ARGMAX, k_t=1,
-               temperature=1.0, uniforms=None, keep_logits=True, stream=None, route_stream=None):
+               temperature=1.0, uniforms=None, keep_logits=True, stream=None, route_stream=None,
+               tail_beta=0.0):
     """One dyna_draft_head call with fresh outputs (see DraftHead for repeated calls)."""
     head = DraftHead(router, layout, h.shape[0], k, mode, k_t, temperature, keep_logits=keep_logits,
-                     device=h.device)
+                     device=h.device, tail_beta=tail_beta)
     head(x, h, uniforms, stream=stream, route_stream=route_stream)
     return head
 
@@ -367,3 +372,19 @@ class DenseHead:
                                      _ptr(self.sample), _ptr(self.sample_logprob), _ptr(self.logits),
                                      _ptr(self.ws), self.ws.numel(), _stream(stream)))
         return self
+
+
+def cluster_budget(t, k0, k1, k_min=1, form=0):
+    """Cluster budget k_c(t) (form 0: the paper's equation, 1: the appendix algorithm's)."""
+    v = lib().dyna_cluster_budget(t, k0, k1, k_min, form)
+    if v < 0:
+        raise ValueError("invalid cluster budget arguments")
+    return v
+
+
+def static_budget(t, k_max):
+    """PA-FR static shortlist size K_fr(t)."""
+    v = lib().dyna_static_budget(t, k_max)
+    if v < 0:
+        raise ValueError("invalid static budget arguments")
+    return v

@@ -24,7 +24,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     for name in declared:
         assert hasattr(lib, name), f"{name} declared in dynahead.h but not exported"
     assert set(declared) == set(D.EXPORTED), "binding and header disagree"
-    assert lib.dyna_abi_version() == 1
+    assert lib.dyna_abi_version() == D.ABI_VERSION == 2
 
 
 def test_status_strings():
@@ -102,8 +102,8 @@ def test_select_and_head_argument_errors():
     sel = lib.dyna_draft_select
     # bad mode, k_t out of range, sampling without uniforms, bad temperature
     base = dict(mode=D.SEL_TOPK, k_t=4, temp=1.0, u=P)
-    def call(mode, k_t, temp, u):
-        return sel(ctypes.byref(L), P, P, P, P, 2, 3, 300, mode, k_t, temp, u, P, P, P, P, P, 1 << 30, None)
+    def call(mode, k_t, temp, u, beta=0.0):
+        return sel(ctypes.byref(L), P, P, P, P, 2, 3, 300, mode, k_t, temp, beta, u, P, P, P, P, P, 1 << 30, None)
     assert call(0, 4, 1.0, P) == D.ERR_INVALID_ARG
     assert call(8, 4, 1.0, P) == D.ERR_INVALID_ARG
     assert call(D.SEL_TOPK, 0, 1.0, P) == D.ERR_INVALID_ARG
@@ -111,14 +111,16 @@ def test_select_and_head_argument_errors():
     assert call(D.SEL_SAMPLE, 1, 1.0, None) == D.ERR_INVALID_ARG
     assert call(D.SEL_SAMPLE, 1, 0.0, P) == D.ERR_INVALID_ARG
     assert call(D.SEL_SAMPLE, 1, float("inf"), P) == D.ERR_INVALID_ARG
+    assert call(D.SEL_SAMPLE, 1, 1.0, P, beta=1.0) == D.ERR_INVALID_ARG   # tail weight in [0, 1)
+    assert call(D.SEL_SAMPLE, 1, 1.0, P, beta=-0.1) == D.ERR_INVALID_ARG
     # router/layout mismatch in the fused call
     R = D._Router(64, 0, 11, D.BF16, 0, P, None, None, None)
     head = lib.dyna_draft_head
-    st = head(ctypes.byref(R), ctypes.byref(L), P, P, D.BF16, 2, 3, D.SEL_ARGMAX, 1, 1.0, None,
+    st = head(ctypes.byref(R), ctypes.byref(L), P, P, D.BF16, 2, 3, D.SEL_ARGMAX, 1, 1.0, 0.0, None,
               P, P, None, None, None, None, 300, P, 1 << 30, None, None, None)
     assert st == D.ERR_INVALID_ARG and b"differs" in lib.dyna_last_error()
     R = D._Router(64, 12, 10, D.BF16, 2, P, None, P, None)  # H not a multiple of 8
-    st = head(ctypes.byref(R), ctypes.byref(L), P, P, D.BF16, 2, 3, D.SEL_ARGMAX, 1, 1.0, None,
+    st = head(ctypes.byref(R), ctypes.byref(L), P, P, D.BF16, 2, 3, D.SEL_ARGMAX, 1, 1.0, 0.0, None,
               P, P, None, None, None, None, 300, P, 1 << 30, None, None, None)
     assert st == D.ERR_INVALID_ARG
     R = D._Router(64, 0, 10, D.BF16, 9, P, None, None, None)  # bad activation
@@ -147,3 +149,20 @@ def test_dense_head_argument_errors():
              None, P, 1 << 30, None) == D.ERR_UNSUPPORTED
     assert d(P, D.BF16, 1000, 64, P, D.BF16, 1, D.SEL_ARGMAX, 1, 1.0, None, P, None, None, None,
              None, P, 4, None) == D.ERR_WORKSPACE
+
+
+def test_position_budgets_match_the_oracle():
+    from oracle import dynaspec_oracle as O
+    lib = D.lib()
+    for form, name in ((0, "equation"), (1, "algorithm1")):
+        for k0, k1, k_min in ((64, 32, 1), (40, 16, 2), (8, 8, 1), (100, 63, 3)):
+            for t in range(40):
+                assert lib.dyna_cluster_budget(t, k0, k1, k_min, form) == O.k_schedule(t, k0, k1, k_min, form=name)
+    for k_max in (1, 32, 1000, 32768):
+        for t in range(40):
+            assert lib.dyna_static_budget(t, k_max) == O.pa_fr_budget(t, k_max)
+    assert lib.dyna_cluster_budget(-1, 64, 32, 1, 0) == -1
+    assert lib.dyna_cluster_budget(3, 64, 32, 0, 0) == -1
+    assert lib.dyna_cluster_budget(3, 64, 32, 1, 2) == -1
+    assert lib.dyna_static_budget(3, 0) == -1
+    assert D.cluster_budget(2, 64, 32) == 8 and D.static_budget(2, 32) == 10

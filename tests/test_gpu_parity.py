@@ -321,13 +321,14 @@ def test_sampling_grid_matches_probabilities():
 
 
 # ---------------------------------------------------------------- whole head
-def _check_head(p, head, modes_ids=True):
+def _check_head(p, head, modes_ids=True, k=None):
     w = p.w
+    k = w.k if k is None else k
     ref_scores = p.oracle_scores()
     clusters = _ids(head.clusters)
     logits = head.logits.cpu().numpy().astype(np.float64)
     for b in range(w.B):
-        eq, ok = PC.cluster_check(clusters[b], ref_scores[b], w.k)
+        eq, ok = PC.cluster_check(clusters[b], ref_scores[b], k)
         assert ok, f"row {b}: clusters"
         sel, rowoff, rows, vids = O.shortlist(clusters[b], p.offsets, p.perm)
         n = len(vids)
@@ -344,6 +345,85 @@ def _check_head(p, head, modes_ids=True):
         if head.sample is not None:
             eq, ok = PC.sample_check(_ids(head.sample)[b], z_gpu, vids, p.u_np[b], head.temperature)
             assert ok
+
+
+@pytest.mark.parametrize("form", [0, 1])
+def test_position_aware_chain(form):
+    """Draft positions t = 0..5, each routed with its cluster budget k_c(t)
+    (Sec. 4.2, eq. pos_schedule; form 1: the appendix algorithm's variant)."""
+    w = next(c for c in CASES if c.name == "ragged_b7")
+    p = Problem(w)
+    k0, k1 = min(w.M, 12), min(w.M, 6)
+    mode = D.SEL_TOPK | D.SEL_SAMPLE
+    for t in range(6):
+        k = D.cluster_budget(t, k0, k1, 1, form)
+        assert k == O.k_schedule(t, k0, k1, form=("equation", "algorithm1")[form])
+        head = D.draft_head(p.R, p.L, p.hd, p.hd, k, mode=mode, k_t=w.k_t, uniforms=p.ud)
+        torch.cuda.synchronize()
+        _check_head(p, head, k=k)
+
+
+@pytest.mark.parametrize("beta", [0.25, 0.6])
+@pytest.mark.parametrize("name", ["ragged_b37", "ragged_b1"])
+def test_tail_mixture(name, beta):
+    """Tail mixture proposal of Sec. 5: q~ = (1 - beta) q_S + beta * uniform(V minus S).
+    Shortlist ids are unchanged, log-probabilities shift by log(1 - beta), and a
+    uniform past 1 - beta picks complement entry floor((u - (1 - beta)) / beta * |V minus S|)
+    in layout order."""
+    w = next(c for c in CASES if c.name == name)
+    p = Problem(w)
+    u = torch.linspace(0.0, 0.999, w.B, dtype=torch.float32) if w.B > 1 else torch.tensor([0.9])
+    ud = u.to(DEV)
+    modes = [D.SEL_TOPK | D.SEL_SAMPLE] + ([D.SEL_ARGMAX] if w.B == 1 else [])  # argmax alone: fused path
+    for mode in modes:
+        kt = w.k_t if mode & D.SEL_TOPK else 1
+        base = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode, k_t=kt, uniforms=ud)
+        tail = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode, k_t=kt, uniforms=ud, tail_beta=beta)
+        torch.cuda.synchronize()
+        assert torch.equal(base.clusters, tail.clusters) and torch.equal(base.ids, tail.ids)
+        lb, lt = base.logprobs.cpu().numpy(), tail.logprobs.cpu().numpy()
+        fin = np.isfinite(lb)
+        np.testing.assert_allclose(lt[fin], lb[fin] + np.log1p(-beta), rtol=0, atol=2e-5)
+        if not mode & D.SEL_SAMPLE:
+            continue
+        clusters = _ids(tail.clusters)
+        logits = tail.logits.cpu().numpy().astype(np.float64)
+        for b in range(w.B):
+            sel, rowoff, rows, vids = O.shortlist(clusters[b], p.offsets, p.perm)
+            comp = O.complement(p.offsets, p.perm, sel)
+            ub = float(u[b])
+            got = int(_ids(tail.sample)[b])
+            if abs(ub - (1.0 - beta)) < 1e-6:
+                continue  # branch decided at the fp32 boundary
+            if ub < 1.0 - beta:
+                eq, ok = PC.sample_check(got, logits[b, :len(vids)], vids, ub / (1.0 - beta), 1.0)
+                assert ok, f"row {b}: shortlist branch"
+            else:
+                x = (ub - (1.0 - beta)) / beta * len(comp)
+                jj = min(len(comp) - 1, int(np.floor(x)))
+                ok = got == comp[jj] or (abs(x - round(x)) < 1e-4 and got in comp[max(0, jj - 1):jj + 2])
+                assert ok, f"row {b}: tail branch"
+                lp = float(tail.sample_logprob.cpu().numpy()[b])
+                assert abs(lp - (np.log(beta) - np.log(len(comp)))) < 1e-5
+
+
+@pytest.mark.parametrize("t", [0, 2, 5])
+def test_pa_fr_static_head(t):
+    """The position-aware frequency-ranked static head (appendix, PA-FR):
+    the first K_fr(t) ids of the vocabulary."""
+    w = CASES[4]
+    p = Problem(w)
+    n = D.static_budget(t, 2048)
+    assert n == O.pa_fr_budget(t, 2048)
+    B = w.B
+    st = D.DenseHead(p.W_lm.to(DEV), n, B, D.SEL_TOPK, 5, keep_logits=True)
+    st(p.hd)
+    torch.cuda.synchronize()
+    for b in range(B):
+        r = O.dense_head(p.h_np[b:b + 1], p.W_np, k_t=5, n_rows=n)[0]
+        PC.assert_close(st.logits[b].cpu().numpy(), r["logits"], p.tol, "PA-FR logits")
+        eq, ok = PC.tokens_check(_ids(st.ids)[b], r["logits"], np.arange(n), 5)
+        assert ok
 
 
 @pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)

@@ -246,6 +246,58 @@ def test_sampling_grid_frequencies_equal_probabilities():
     assert np.all(np.abs(counts - p * N) <= 1.0)
 
 
+def test_tail_mixture_hand_example():
+    # S = two equal tokens, complement = two tokens, beta = 1/2 (Sec. 5):
+    # q~ = 1/4 on every token; u in [0, 1/2) picks inside S by u / (1/2)
+    z, vids, comp = np.zeros(2), np.array([7, 9]), np.array([3, 4])
+    picks = [O.draft_select(z, vids, 1, u=u, beta=0.5, complement_ids=comp)["sample_id"]
+             for u in (0.0, 0.2, 0.3, 0.5, 0.6, 0.75, 0.9)]
+    assert picks == [7, 7, 9, 3, 3, 4, 4]
+    r = O.draft_select(z, vids, 2, u=0.9, beta=0.5, complement_ids=comp)
+    np.testing.assert_allclose(np.exp(r["logprobs"]), [0.25, 0.25], rtol=1e-15)
+    assert abs(np.exp(r["sample_logprob"]) - 0.25) < 1e-15
+
+
+def test_tail_mixture_is_a_full_support_distribution():
+    # grid of u: every token's frequency is its q~ probability, and q~ sums to one
+    rng = np.random.default_rng(13)
+    z = rng.standard_normal(5)
+    vids, comp, beta = np.arange(5), np.arange(5, 12), 0.3
+    p = np.exp(z - z.max()); p /= p.sum()
+    N = 70000
+    ids = [O.draft_select(z, vids, 1, u=(i + 0.5) / N, beta=beta, complement_ids=comp)["sample_id"]
+           for i in range(N)]
+    freq = np.bincount(ids, minlength=12) / N
+    q = np.concatenate([(1 - beta) * p, np.full(7, beta / 7)])
+    assert np.all(np.abs(freq - q) <= 2.0 / N)
+    r = O.draft_select(z, vids, 5, beta=beta, complement_ids=comp)
+    assert abs(np.exp(r["logprobs"]).sum() + beta - 1.0) < 1e-12
+
+
+def test_tail_mixture_reduces_to_the_shortlist_draft():
+    rng = np.random.default_rng(14)
+    z = rng.standard_normal(9)
+    for u in (0.0, 0.31, 0.77, 0.999):
+        a = O.draft_select(z, np.arange(9), 3, u=u)
+        b = O.draft_select(z, np.arange(9), 3, u=u, beta=0.0, complement_ids=np.arange(9, 20))
+        c = O.draft_select(z, np.arange(9), 3, u=u, beta=0.4, complement_ids=np.zeros(0, dtype=int))
+        for x in (b, c):  # beta = 0, or an empty complement (k = M)
+            assert x["ids"].tolist() == a["ids"].tolist() and x["sample_id"] == a["sample_id"]
+            np.testing.assert_allclose(x["logprobs"], a["logprobs"], rtol=1e-15)
+
+
+def test_complement_is_the_rest_of_the_vocabulary_in_layout_order():
+    rng = np.random.default_rng(15)
+    V, M = 200, 11
+    cluster_of = rng.integers(0, M, size=V)
+    sizes, offsets, perm, _ = O.cluster_layout(cluster_of, M)
+    K = np.array([2, 5, 9])
+    comp = O.complement(offsets, perm, K)
+    assert set(comp.tolist()) == {v for v in range(V) if cluster_of[v] not in (2, 5, 9)}
+    key = [(cluster_of[v], v) for v in comp.tolist()]
+    assert key == sorted(key)
+
+
 def test_logprobs_normalised():
     rng = np.random.default_rng(8)
     z = rng.standard_normal(1000) * 4
@@ -316,3 +368,21 @@ def test_k_schedule_closed_form():
     g = GOLD["k_schedule"]
     assert [O.k_schedule(t, g["k0"], g["k1"]) for t in range(10)] == g["t_0_to_9"]
     assert O.k_schedule(100, 64, 32) == 1  # clamped at k_min
+    g = GOLD["k_schedule_algorithm1"]
+    assert [O.k_schedule(t, g["k0"], g["k1"], form="algorithm1") for t in range(10)] == g["t_0_to_9"]
+
+
+def test_k_schedule_is_non_increasing_after_the_first_two_positions():
+    for k1 in (1, 7, 32, 64, 100):
+        for form in ("equation", "algorithm1"):
+            ks = [O.k_schedule(t, 200, k1, form=form) for t in range(1, 300)]
+            assert all(a >= b for a, b in zip(ks[1:], ks[2:])) and min(ks) >= 1
+    # the closed form is round-half-up of k1 / (2t): within 1/2 of it
+    for t in range(2, 50):
+        assert abs(O.k_schedule(t, 64, 32, k_min=0) - 32 / (2 * t)) <= 0.5 + 1e-12
+
+
+def test_pa_fr_budget_hand_values():
+    g = GOLD["pa_fr"]
+    assert [O.pa_fr_budget(t, 32) for t in range(10)] == g["k_max_32"]
+    assert [O.pa_fr_budget(t, 32768) for t in range(10)] == g["k_max_32768"]
