@@ -66,7 +66,7 @@ typedef enum { DYNA_ACT_NONE = 0, DYNA_ACT_RELU = 1, DYNA_ACT_SILU = 2 } dyna_ac
 /* Selection modes, combinable bit flags (Algorithm 1: TopK_{k_t} of the
  * log-softmax over the shortlist; sampling draws from the restricted,
  * renormalised draft q_S of Sec. 5 with tail weight beta = 0). */
-enum { DYNA_SEL_ARGMAX = 1, DYNA_SEL_TOPK = 2, DYNA_SEL_SAMPLE = 4 };
+enum { DYNA_SEL_ARGMAX = 1, DYNA_SEL_TOPK = 2, DYNA_SEL_SAMPLE = 4, DYNA_SEL_UNION = 8 };
 
 /* Cluster-contiguous LM head produced once by dyna_build_layout
  * (Sec. 4.2, "Vocabulary partition": V is the disjoint union of M clusters
@@ -210,6 +210,13 @@ dyna_status dyna_draft_select(const dyna_layout* L, const float* logits,
  *  x_ready               with route_stream: event after which x is valid;
  *                        NULL means "x is valid when this call is made
  *                        relative to `stream`" and the library records one.
+ *  mode | DYNA_SEL_UNION the B rows of the step share one shortlist, the
+ *                        union of their selected clusters (Sec. 4.2: with
+ *                        several tokens at a step, the union of the clusters
+ *                        predicted for each), in ascending cluster id.  Every
+ *                        row's logits and selection run over the union;
+ *                        out_clusters stays per row.  cap must be at least
+ *                        min(V, B * cap_by_k[k]); tail_beta must be 0.
  * Other arguments as in the step-by-step calls. */
 dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
                             const void* x, const void* h, int32_t adtype,
@@ -238,6 +245,24 @@ dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_rows, int32
                             int32_t* out_ids, float* out_logprobs, int32_t* out_sample,
                             float* out_sample_logprob, float* out_logits,
                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ */
+/* Beam expansion (Algorithm 1: cu_scores, TopK_{k_t}).                */
+/* ------------------------------------------------------------------ */
+
+/* Cumulative scores cu[b, r] = logprobs[b, r] + last_scores[b] of the B x k_t
+ * candidates of a step (the draft selection's outputs), and the n_out
+ * largest of them, ordered (cu desc, b asc, r asc): the next beam.
+ *  logprobs [B, k_t], ids [B, k_t]  device, as written by the draft head
+ *                                   (a candidate with id < 0 is never chosen)
+ *  last_scores [B]                  device, may be NULL (zeros: the first step)
+ *  out_scores, out_parent, out_ids [n_out]  device outputs: cu, the row b the
+ *                                   candidate extends, its token id; -inf, -1,
+ *                                   -1 past the number of candidates
+ * 1 <= k_t, n_out <= DYNA_MAX_KT; B * k_t <= 8192.  One workgroup. */
+dyna_status dyna_beam_expand(const float* logprobs, const int32_t* ids, const float* last_scores,
+                             int32_t B, int32_t k_t, int32_t n_out, float* out_scores,
+                             int32_t* out_parent, int32_t* out_ids, hipStream_t stream);
 
 /* ------------------------------------------------------------------ */
 /* Position-aware budgets (host functions, no GPU work).               */

@@ -226,7 +226,7 @@ def sample_cdf(z, temperature: float = 1.0) -> np.ndarray:
 
 def draft_select(z, vocab_ids, k_t: int = 1, temperature: float = 1.0, u=None, beta: float = 0.0,
                  complement_ids=None):
-    """Draft outputs of one context over its shortlist.
+    r"""Draft outputs of one context over its shortlist.
 
     Returns dict(ids[k_t], logprobs[k_t], positions[k_t], sample_id,
     sample_pos, sample_logprob); ids are vocabulary ids (remap2realid).
@@ -269,10 +269,18 @@ def complement(offsets, perm, sel_sorted):
 # --------------------------------------------------------------------------
 # whole head and the two baselines
 # --------------------------------------------------------------------------
+def union_clusters(cluster_ids) -> np.ndarray:
+    """Clusters selected by any row of a step, ascending (Sec. 4.2: with
+    several tokens at a step, the union of their predicted clusters)."""
+    return np.unique(np.asarray(cluster_ids, dtype=np.int64).ravel())
+
+
 def draft_head(x, h, W1, W2, act, cluster_of, M, W_lm, k, k_t=1, temperature=1.0,
-               u=None, b1=None, b2=None, beta: float = 0.0):
+               u=None, b1=None, b2=None, beta: float = 0.0, union: bool = False):
     """The dynamic draft head for a batch: route, shortlist, logits, select.
 
+    With union=True every row of the step shares one shortlist, the union of
+    the rows' selected clusters (Sec. 4.2); otherwise each row has its own.
     Returns a list (one dict per context row) with the router's cluster ids,
     the shortlist and the draft outputs.
     """
@@ -280,9 +288,10 @@ def draft_head(x, h, W1, W2, act, cluster_of, M, W_lm, k, k_t=1, temperature=1.0
     s = router_scores(x, W1, W2, b1, b2, act)
     ids, vals = topk_clusters(s, k)
     h = np.atleast_2d(np.asarray(h))
+    shared = union_clusters(ids) if union else None
     out = []
     for b in range(h.shape[0]):
-        sel, rowoff, rows, vids = shortlist(ids[b], offsets, perm)
+        sel, rowoff, rows, vids = shortlist(shared if union else ids[b], offsets, perm)
         z = shortlist_logits(h[b], W_lm, vids)
         comp = complement(offsets, perm, sel) if beta > 0.0 else None
         r = draft_select(z, vids, k_t, temperature, None if u is None else u[b], beta, comp)
@@ -290,6 +299,24 @@ def draft_head(x, h, W1, W2, act, cluster_of, M, W_lm, k, k_t=1, temperature=1.0
                  layout_rows=rows, vocab_ids=vids, logits=z, scores=s[b])
         out.append(r)
     return out
+
+
+def beam_expand(logprobs, ids, last_scores, n_out: int):
+    """EAGLE-2 style expansion (Algorithm 1): cumulative scores
+    cu[b, r] = logprobs[b, r] + last_scores[b] over the B x k_t candidates of a
+    step; the n_out largest, ordered (cu desc, b asc, r asc), give the next
+    beam: (scores[n_out], parent rows[n_out], token ids[n_out]).  Candidates
+    with no token (id < 0) are never chosen."""
+    lp = np.asarray(logprobs, dtype=np.float64)
+    ids = np.asarray(ids, dtype=np.int64)
+    B, kt = lp.shape
+    last = np.zeros(B) if last_scores is None else np.asarray(last_scores, dtype=np.float64)
+    cu = lp + last[:, None]
+    cand = [(cu[b, r], b, r) for b in range(B) for r in range(kt) if ids[b, r] >= 0]
+    cand.sort(key=lambda c: (-_canonical(np.array([c[0]]))[0], c[1], c[2]))
+    cand = cand[:n_out]
+    return (np.array([c[0] for c in cand]), np.array([c[1] for c in cand], dtype=np.int64),
+            np.array([ids[c[1], c[2]] for c in cand], dtype=np.int64))
 
 
 def dense_head(h, W_lm, k_t=1, temperature=1.0, u=None, n_rows=None):

@@ -178,7 +178,9 @@ static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_
     if (B == 1) c.partials = take(greedy_partials_bytes());
     if (L) {
         c.plan.max_chunks = (int32_t)max_chunks_for(L);
-        c.plan.max_entries = (int32_t)(Bl * k);
+        // per-row lists (B * k entries) or the union's (every row in each
+        // of at most min(M, B * k) clusters)
+        c.plan.max_entries = (int32_t)std::max<int64_t>(Bl * k, std::min<int64_t>(L->M, Bl * k) * Bl);
         c.plan.hdr = static_cast<PlanHeader*>(take(sizeof(PlanHeader)));
         c.plan.chunks = static_cast<Chunk*>(take(sizeof(Chunk) * (size_t)c.plan.max_chunks));
         c.plan.list = static_cast<ListEntry*>(take(sizeof(ListEntry) * (size_t)c.plan.max_entries));
@@ -562,7 +564,18 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     REQUIRE(r->M == L->M, "router M=%d differs from layout M=%d", r->M, L->M);
     REQUIRE(r->d_r > 0, "router d_r");
     TRY(check_k(L, k));
-    TRY(check_cap(L, k, cap));
+    const bool union_mode = (mode & DYNA_SEL_UNION) != 0 && B > 1;  // one row: its own shortlist
+    mode &= ~DYNA_SEL_UNION;
+    if (union_mode) {
+        const int64_t bound = std::min<int64_t>(L->V, (int64_t)B * L->cap_by_k[k]);
+        if (cap < bound)
+            return set_error(DYNA_ERR_CAPACITY, "union: cap=%d < min(V, B * cap_by_k[k])=%lld", cap,
+                             (long long)bound);
+        if (cap > select_max_len()) return set_error(DYNA_ERR_UNSUPPORTED, "union: cap=%d > %d", cap, select_max_len());
+        if (tail_beta > 0.0f) return set_error(DYNA_ERR_UNSUPPORTED, "union: no tail mixture");
+    } else {
+        TRY(check_cap(L, k, cap));
+    }
     TRY(check_select(mode, &k_t, temperature, uniforms, out_ids, out_sample));
     REQUIRE(tail_beta >= 0.0f && tail_beta < 1.0f, "tail_beta must lie in [0, 1)");
     REQUIRE(valid_dtype(adtype), "bad adtype %d", adtype);
@@ -595,9 +608,17 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
 
     // routing (the router's stream)
     TRY(run_router(r, x, adtype, B, c.scores, c.hidden, c.rpart, c.rpart_floats, rs, fused ? c.counters : nullptr));
-    TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, L->offsets, c.sel_sorted,
-                             c.sel_rowoff, c.row_len, &c.plan, rs));
-    if (B > 1) TRY(launch_plan(L->offsets, L->M, c.sel_sorted, c.sel_rowoff, B, k, c.plan, rs));
+    if (union_mode) {
+        // per-row clusters, then one shared shortlist (its ids go to sel_sorted)
+        TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, nullptr, nullptr, nullptr, nullptr,
+                                 nullptr, rs));
+        TRY(launch_union_plan(L->offsets, L->M, clusters, B, k, c.row_len, c.sel_sorted,
+                              (int32_t)std::min<int64_t>(L->M, (int64_t)B * k), c.plan, rs));
+    } else {
+        TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, L->offsets, c.sel_sorted,
+                                 c.sel_rowoff, c.row_len, &c.plan, rs));
+        if (B > 1) TRY(launch_plan(L->offsets, L->M, c.sel_sorted, c.sel_rowoff, B, k, c.plan, rs));
+    }
     if (split) {
         hipEvent_t join = lazy_event(g_ev_join);
         if (!join || hipEventRecord(join, rs) != hipSuccess || hipStreamWaitEvent(stream, join, 0) != hipSuccess)
@@ -630,6 +651,16 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
                          want_ids ? out_ids : nullptr,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
                          want_sample ? out_sample_logprob : nullptr, c.select_ws, stream, c.slot_vid);
+}
+
+// ------------------------------------------------------------------ beam expansion
+DYNA_API dyna_status dyna_beam_expand(const float* logprobs, const int32_t* ids, const float* last_scores,
+                                      int32_t B, int32_t k_t, int32_t n_out, float* out_scores,
+                                      int32_t* out_parent, int32_t* out_ids, hipStream_t stream) {
+    REQUIRE(B >= 1 && k_t >= 1 && k_t <= DYNA_MAX_KT, "B=%d, k_t=%d", B, k_t);
+    REQUIRE(n_out >= 1 && n_out <= DYNA_MAX_KT, "n_out=%d outside [1, %d]", n_out, DYNA_MAX_KT);
+    REQUIRE(logprobs && ids && out_scores && out_parent && out_ids, "NULL argument");
+    return launch_beam_expand(logprobs, ids, last_scores, B, k_t, n_out, out_scores, out_parent, out_ids, stream);
 }
 
 // ------------------------------------------------------------------ budgets

@@ -204,6 +204,11 @@ size_t select_ws_bytes(int32_t B, int32_t max_len, int32_t k_t);
 // Longest row launch_select handles (256 segments).
 int32_t select_max_len();
 // Fill SelectArgs for rows of at most max_len slots; ws as for launch_select.
+dyna_status launch_union_plan(const int32_t* offsets, int32_t M, const int32_t* topk_ids, int32_t B, int32_t k,
+                              int32_t* row_len, int32_t* sel_u, int32_t u_cap, Plan plan, hipStream_t stream);
+dyna_status launch_beam_expand(const float* logprobs, const int32_t* ids, const float* last, int32_t B, int32_t k_t,
+                               int32_t n_out, float* out_scores, int32_t* out_parent, int32_t* out_ids,
+                               hipStream_t stream);
 SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_len,
                             int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
                             const int32_t* sel_rowoff, const int32_t* offsets,

@@ -226,6 +226,157 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
 }
 
+// ------------------------------------------------------------------ union plan
+// One workgroup.  The step's rows share one shortlist, the union of their
+// selected clusters (Sec. 4.2: several tokens at a step take the union of
+// their predicted clusters).  Union clusters are marked in an LDS bitmap and
+// compacted in ascending id; each is cut into chunks whose context list is
+// every row (entries i * B .. i * B + B - 1 of the list for union cluster i).
+// Writes the plan, row_len[b] = |union| for every row, and the union itself
+// (ascending ids, -1 past its end) to sel_u[0 .. min(M, B * k)).
+__global__ __launch_bounds__(kPlanThreads) void union_plan_kernel(
+    const int32_t* __restrict__ offsets, int M, const int32_t* __restrict__ topk_ids, int B, int k,
+    int32_t* __restrict__ row_len, int32_t* __restrict__ sel_u, int u_cap, Plan plan) {
+    extern __shared__ int32_t ul[];
+    uint32_t* bits = reinterpret_cast<uint32_t*>(ul);  // [W] cluster bitmap
+    const int W = (M + 31) / 32;
+    int32_t* wpos = ul + W;                               // [W] union ids before each word
+    int32_t* uid = ul + 2 * W;                            // [M] union ids, ascending
+    int32_t* coff = uid + M;                              // [M] first chunk of union cluster i
+    int32_t* roff = coff + M;                             // [M + 1] first shortlist slot of union cluster i
+    __shared__ int tmp[kPlanThreads / kWave + 1];
+    const int t = threadIdx.x;
+    for (int i = t; i < W; i += kPlanThreads) bits[i] = 0u;
+    __syncthreads();
+    const int64_t n_sel = (int64_t)B * k;
+    for (int64_t e0 = 0; e0 < n_sel; e0 += kPlanThreads * kPlanPer) {
+        int mv[kPlanPer];
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q) {
+            const int64_t e = e0 + q * kPlanThreads + t;
+            mv[q] = e < n_sel ? topk_ids[e] : -1;
+        }
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q)
+            if (mv[q] >= 0 && mv[q] < M) atomicOr(&bits[mv[q] >> 5], 1u << (mv[q] & 31));
+    }
+    __syncthreads();
+    // compact: word w's set bits take union positions wpos[w] ..
+    const int per_w = (W + kPlanThreads - 1) / kPlanThreads;
+    const int w0 = min(W, t * per_w), w1 = min(W, w0 + per_w);
+    int cnt = 0;
+    for (int w = w0; w < w1; ++w) cnt += __popc(bits[w]);
+    int U;
+    int run = block_exclusive_scan<kPlanThreads>(cnt, tmp, &U);
+    for (int w = w0; w < w1; ++w) {
+        wpos[w] = run;
+        uint32_t x = bits[w];
+        while (x) {
+            const int bit = __builtin_ctz(x);
+            uid[run++] = w * 32 + bit;
+            x &= x - 1;
+        }
+    }
+    __syncthreads();
+    // union slots and chunks, in ascending id
+    const int per_u = (U + kPlanThreads - 1) / kPlanThreads;
+    const int i0 = min(U, t * per_u), i1 = min(U, i0 + per_u);
+    int lrows = 0, lch = 0;
+    for (int i = i0; i < i1; ++i) {
+        const int n = offsets[uid[i] + 1] - offsets[uid[i]];
+        lrows += n;
+        lch += (n + kChunkRows - 1) / kChunkRows;
+    }
+    int len, n_chunks;
+    int rr = block_exclusive_scan<kPlanThreads>(lrows, tmp, &len);
+    int rc = block_exclusive_scan<kPlanThreads>(lch, tmp, &n_chunks);
+    for (int i = i0; i < i1; ++i) {
+        const int n = offsets[uid[i] + 1] - offsets[uid[i]];
+        roff[i] = rr;
+        coff[i] = rc;
+        rr += n;
+        rc += (n + kChunkRows - 1) / kChunkRows;
+    }
+    __syncthreads();
+    // chunks: equal ranges per thread, one binary search, then a forward walk
+    const int per_c = (n_chunks + kPlanThreads - 1) / kPlanThreads;
+    const int c0 = min(n_chunks, t * per_c), c1 = min(n_chunks, c0 + per_c);
+    if (c0 < c1) {
+        int lo = 0, hi = U - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (coff[mid] <= c0) lo = mid; else hi = mid - 1;
+        }
+        int i = lo;
+        for (int c = c0; c < c1; ++c) {
+            while (i + 1 < U && coff[i + 1] <= c) ++i;
+            const int m = uid[i];
+            const int ci = c - coff[i];
+            const int o = offsets[m], n = offsets[m + 1] - o;
+            plan.chunks[c] = Chunk{o + ci * kChunkRows, min(kChunkRows, n - ci * kChunkRows), i * B, B};
+        }
+    }
+    // every row in every union cluster's list
+    for (int64_t e = t; e < (int64_t)U * B; e += kPlanThreads) {
+        const int i = (int)(e / B), b = (int)(e - (int64_t)i * B);
+        plan.list[e] = ListEntry{b, roff[i] - offsets[uid[i]]};
+    }
+    for (int b = t; b < B; b += kPlanThreads) row_len[b] = len;
+    for (int i = t; i < u_cap; i += kPlanThreads) sel_u[i] = i < U ? uid[i] : -1;
+    if (t == 0) {
+        plan.hdr->n_chunks = n_chunks;
+        plan.hdr->n_entries = U * B;
+    }
+}
+
+// ------------------------------------------------------------------ beam expansion
+// One workgroup: the n_out best cumulative scores cu[b, r] = logprobs[b, r] +
+// last[b] among the B x k_t candidates with a token (Algorithm 1's
+// cu_scores and TopK_{k_t}), ordered (cu desc, b asc, r asc) by the key
+// (ordered cu << 32) | ~(b * k_t + r).
+constexpr int kBeamPer = 8;
+__global__ __launch_bounds__(kRowThreads) void beam_expand_kernel(const float* __restrict__ logprobs,
+                                                                  const int32_t* __restrict__ ids,
+                                                                  const float* __restrict__ last, int B, int k_t,
+                                                                  int n_out, float* out_scores, int32_t* out_parent,
+                                                                  int32_t* out_ids) {
+    __shared__ int hist[256];
+    __shared__ uint64_t sel[DYNA_MAX_KT], top[DYNA_MAX_KT];
+    const int n = B * k_t;
+    uint64_t kk[kBeamPer];
+    int n_valid = 0;
+#pragma unroll
+    for (int q = 0; q < kBeamPer; ++q) {
+        const int e = q * kRowThreads + threadIdx.x;
+        kk[q] = 0;
+        if (e < n && ids[e] >= 0) {
+            const int b = e / k_t;
+            const float cu = canon(logprobs[e]) + (last ? last[b] : 0.0f);
+            kk[q] = sel_key(canon(cu), (uint32_t)e);
+            ++n_valid;
+        }
+    }
+    __shared__ int sh_valid;
+    if (threadIdx.x == 0) sh_valid = 0;
+    __syncthreads();
+    atomicAdd(&sh_valid, n_valid);
+    __syncthreads();
+    block_radix_topk<kRowThreads, kBeamPer>(kk, n_out, sh_valid, hist, sel, top);
+    for (int r = threadIdx.x; r < n_out; r += kRowThreads) {
+        const uint64_t key = top[r];
+        if (key == 0) {
+            out_scores[r] = -__builtin_inff();
+            out_parent[r] = -1;
+            out_ids[r] = -1;
+        } else {
+            const int e = (int)key_id(key);
+            out_scores[r] = key_val(key);
+            out_parent[r] = e / k_t;
+            out_ids[r] = ids[e];
+        }
+    }
+}
+
 // ------------------------------------------------------------------ select
 __global__ __launch_bounds__(kNT) void select_partial_kernel(SelectArgs a) {
     __shared__ uint64_t cand[kNT / kWave * DYNA_MAX_KT];
@@ -482,6 +633,36 @@ dyna_status launch_plan(const int32_t* offsets, int32_t M, const int32_t* sel_so
     }
     plan_kernel<<<1, kPlanThreads, lds, stream>>>(offsets, M, sel_sorted, sel_rowoff, B, k, plan);
     return check_launch("plan_kernel");
+}
+
+dyna_status launch_union_plan(const int32_t* offsets, int32_t M, const int32_t* topk_ids, int32_t B, int32_t k,
+                              int32_t* row_len, int32_t* sel_u, int32_t u_cap, Plan plan, hipStream_t stream) {
+    const size_t lds = sizeof(int32_t) * (2 * (size_t)((M + 31) / 32) + 3 * (size_t)M + 1);
+    if (lds > 64 * 1024) {
+        static std::atomic<uint64_t> allowed{0};
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "union: device");
+        if (!(allowed.load() & (1ull << dev))) {
+            const int most = (int)(sizeof(int32_t) * (2 * (size_t)((DYNA_MAX_M + 31) / 32) + 3 * (size_t)DYNA_MAX_M + 1));
+            if (hipFuncSetAttribute((const void*)union_plan_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, most) !=
+                hipSuccess)
+                return set_error(DYNA_ERR_HIP, "union: LDS attribute");
+            allowed.fetch_or(1ull << dev);
+        }
+    }
+    union_plan_kernel<<<1, kPlanThreads, lds, stream>>>(offsets, M, topk_ids, B, k, row_len, sel_u, u_cap, plan);
+    return check_launch("union_plan_kernel");
+}
+
+dyna_status launch_beam_expand(const float* logprobs, const int32_t* ids, const float* last, int32_t B, int32_t k_t,
+                               int32_t n_out, float* out_scores, int32_t* out_parent, int32_t* out_ids,
+                               hipStream_t stream) {
+    if ((int64_t)B * k_t > (int64_t)kRowThreads * kBeamPer)
+        return set_error(DYNA_ERR_UNSUPPORTED, "beam expansion: B * k_t = %lld > %d", (long long)B * k_t,
+                         kRowThreads * kBeamPer);
+    beam_expand_kernel<<<1, kRowThreads, 0, stream>>>(logprobs, ids, last, B, k_t, n_out, out_scores, out_parent,
+                                                     out_ids);
+    return check_launch("beam_expand_kernel");
 }
 
 size_t select_ws_bytes(int32_t B, int32_t max_len, int32_t k_t) {

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libdynahead.so")
 OK, ERR_INVALID_ARG, ERR_CAPACITY, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP, ERR_DEVICE_DATA = range(7)
 F32, BF16 = 0, 1
 ACT = {"none": 0, "relu": 1, "silu": 2}
-SEL_ARGMAX, SEL_TOPK, SEL_SAMPLE = 1, 2, 4
+SEL_ARGMAX, SEL_TOPK, SEL_SAMPLE, SEL_UNION = 1, 2, 4, 8
 OPT_LOGITS_PATH, OPT_ROUTER_PATH, OPT_KERNEL_TIMING, OPT_GEMV_ROWS, OPT_FUSED_B1, OPT_MFMA_UNROLL = 1, 2, 3, 4, 5, 6
 OPT_GATHER_CFG, OPT_GREEDY_GRID = 7, 8
 MAX_KT = 64
@@ -70,6 +70,7 @@ _SIGNATURES = {
                              _I, _P, _Z, _P, _P, _P]),
     "dyna_dense_workspace_bytes": (_Z, [_I, _I]),
     "dyna_cluster_budget": (_I, [_I, _I, _I, _I, _I]),
+    "dyna_beam_expand": (_I, [_P, _P, _P, _I, _I, _I, _P, _P, _P, _P]),
     "dyna_static_budget": (_I, [_I, _I]),
     "dyna_dense_head": (_I, [_P, _I, _I, _I, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P,
                              _Z, _P]),
@@ -315,7 +316,8 @@ class DraftHead:
         import torch
         self.router, self.layout, self.B, self.k = router, layout, B, k
         self.mode, self.k_t, self.temperature, self.tail_beta = mode, k_t, temperature, tail_beta
-        self.cap = layout.cap(k)
+        # DYNA_SEL_UNION: every row's logits span the step's shared shortlist
+        self.cap = union_cap(layout, B, k) if (mode & SEL_UNION) and B > 1 else layout.cap(k)
         self.ids, self.logprobs, self.sample, self.sample_logprob = _select_outputs(B, k_t, mode, device)
         self.clusters = torch.empty((B, k), dtype=torch.int32, device=device) if keep_clusters else None
         self.logits = torch.full((B, self.cap), float("nan"), dtype=torch.float32,
@@ -388,3 +390,22 @@ def static_budget(t, k_max):
     if v < 0:
         raise ValueError("invalid static budget arguments")
     return v
+
+
+def union_cap(layout: "Layout", B: int, k: int) -> int:
+    """Logits row stride a DYNA_SEL_UNION step of B rows needs: min(V, B * cap_by_k[k])."""
+    return min(layout.V, B * layout.cap(k))
+
+
+def beam_expand(logprobs, ids, last_scores=None, n_out=None, stream=None):
+    """dyna_beam_expand -> (scores[n_out], parent[n_out], ids[n_out])."""
+    import torch
+    B, k_t = logprobs.shape
+    n_out = k_t if n_out is None else n_out
+    dev = logprobs.device
+    sc = torch.empty(n_out, dtype=torch.float32, device=dev)
+    par = torch.empty(n_out, dtype=torch.int32, device=dev)
+    tok = torch.empty(n_out, dtype=torch.int32, device=dev)
+    _check(lib().dyna_beam_expand(_ptr(logprobs), _ptr(ids), _ptr(last_scores), B, k_t, n_out, _ptr(sc),
+                                  _ptr(par), _ptr(tok), _stream(stream)))
+    return sc, par, tok

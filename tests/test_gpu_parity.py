@@ -407,6 +407,117 @@ def test_tail_mixture(name, beta):
                 assert abs(lp - (np.log(beta) - np.log(len(comp)))) < 1e-5
 
 
+@pytest.mark.parametrize("name", ["ragged_b3", "ragged_b37", "zipf_b9", "wide_b64", "many_b130"])
+def test_union_shortlist_head(name):
+    """Union routing (Sec. 4.2): the rows of a step share one shortlist, the
+    union of their selected clusters; every row's logits, tokens and sample
+    are over that union (the oracle's draft_head(union=True) on the same
+    clusters)."""
+    w = next(c for c in CASES if c.name == name)
+    p = Problem(w)
+    mode = D.SEL_TOPK | D.SEL_SAMPLE
+    head = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode | D.SEL_UNION, k_t=w.k_t, uniforms=p.ud)
+    torch.cuda.synchronize()
+    assert head.cap == min(w.V, w.B * int(p.cap[w.k]))
+    ref_scores = p.oracle_scores()
+    clusters = _ids(head.clusters)
+    for b in range(w.B):
+        eq, ok = PC.cluster_check(clusters[b], ref_scores[b], w.k)
+        assert ok, f"row {b}: clusters"
+    union = O.union_clusters(clusters)
+    sel, rowoff, rows, vids = O.shortlist(union, p.offsets, p.perm)
+    n = len(vids)
+    logits = head.logits.cpu().numpy().astype(np.float64)
+    ids, smp = _ids(head.ids), _ids(head.sample)
+    kt = min(w.k_t, n)
+    for b in range(w.B):
+        z_ref = O.shortlist_logits(p.h_np[b], p.W_np, vids)
+        PC.assert_close(logits[b, :n], z_ref, p.tol, f"union logits row {b}")
+        r = O.draft_select(logits[b, :n], vids, kt)
+        assert ids[b, :kt].tolist() == r["ids"].tolist()  # exact on own logits
+        eq, ok = PC.tokens_check(ids[b], z_ref, vids, w.k_t)
+        assert ok, f"row {b}: tokens"
+        eq, ok = PC.sample_check(smp[b], logits[b, :n], vids, p.u_np[b], head.temperature)
+        assert ok, f"row {b}: sample"
+    # the oracle's union head agrees wherever its routing equals the kernels'
+    ref = O.draft_head(p.h_np, p.h_np, p.W1_np, p.W2_np, w.act, p.cluster_of, w.M, p.W_np, w.k,
+                       k_t=w.k_t, union=True)
+    if O.union_clusters(np.stack([r["clusters"] for r in ref])).tolist() == union.tolist():
+        for b in range(w.B):
+            assert ref[b]["vocab_ids"].tolist() == vids.tolist()
+            eq, ok = PC.tokens_check(ids[b], ref[b]["logits"], vids, w.k_t)
+            assert ok
+    # the per-row head on the same step is a different (smaller) shortlist
+    own = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode, k_t=w.k_t, uniforms=p.ud)
+    torch.cuda.synchronize()
+    assert torch.equal(own.clusters, head.clusters)
+
+
+def test_union_one_row_is_the_per_row_head():
+    w = next(c for c in CASES if c.name == "ragged_b1")
+    p = Problem(w)
+    mode = D.SEL_TOPK | D.SEL_SAMPLE
+    a = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode | D.SEL_UNION, k_t=w.k_t, uniforms=p.ud)
+    b = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode, k_t=w.k_t, uniforms=p.ud)
+    torch.cuda.synchronize()
+    assert torch.equal(a.ids, b.ids) and torch.equal(a.sample, b.sample)
+    assert torch.equal(a.logprobs, b.logprobs)
+
+
+def test_union_rejects_small_cap_and_tail():
+    w = next(c for c in CASES if c.name == "ragged_b7")
+    p = Problem(w)
+    head = D.DraftHead(p.R, p.L, w.B, w.k, D.SEL_TOPK | D.SEL_UNION, w.k_t, device=DEV)
+    head.cap = p.L.cap(w.k)  # the per-row bound is too small for a union
+    if head.cap < head.layout.V:
+        with pytest.raises(D.DynaError) as e:
+            head(p.hd, p.hd)
+        assert e.value.status == D.ERR_CAPACITY
+    t = D.DraftHead(p.R, p.L, w.B, w.k, D.SEL_TOPK | D.SEL_UNION, w.k_t, device=DEV, tail_beta=0.3)
+    with pytest.raises(D.DynaError) as e:
+        t(p.hd, p.hd)
+    assert e.value.status == D.ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("B,k_t,n_out", [(1, 1, 1), (1, 8, 8), (6, 8, 8), (37, 13, 20), (130, 63, 64),
+                                         (128, 64, 64)])
+def test_beam_expand(B, k_t, n_out):
+    """EAGLE-2 expansion (Algorithm 1): the n_out best cumulative scores over the
+    B x k_t candidates, ordered (score desc, row asc, rank asc); missing tokens
+    (id -1) are never chosen."""
+    rng = np.random.default_rng(B * 1000 + k_t)
+    lp = -rng.exponential(3.0, size=(B, k_t)).astype(np.float32)
+    lp[:, ::3] = np.round(lp[:, ::3] * 4) / 4  # exact ties across rows
+    ids = rng.integers(0, 50000, size=(B, k_t)).astype(np.int32)
+    ids[rng.random((B, k_t)) < 0.1] = -1
+    last = (-rng.exponential(2.0, size=B)).astype(np.float32)
+    last[::2] = np.round(last[::2] * 2) / 2
+    for lst in (None, last):
+        sc, par, tok = D.beam_expand(torch.from_numpy(lp).to(DEV), torch.from_numpy(ids).to(DEV),
+                                     None if lst is None else torch.from_numpy(lst).to(DEV), n_out)
+        torch.cuda.synchronize()
+        cu32 = lp if lst is None else (lp + lst[:, None]).astype(np.float32)  # the kernel's fp32 sums
+        r_sc, r_par, r_tok = O.beam_expand(cu32, ids, None, n_out)
+        m = len(r_sc)
+        assert sc.cpu().numpy()[:m].tolist() == r_sc.astype(np.float32).tolist()
+        assert _ids(par)[:m].tolist() == r_par.tolist()
+        assert _ids(tok)[:m].tolist() == r_tok.tolist()
+        assert np.all(_ids(par)[m:] == -1) and np.all(_ids(tok)[m:] == -1)
+        assert np.all(np.isneginf(sc.cpu().numpy()[m:]))
+
+
+def test_beam_expand_rejects_bad_sizes():
+    lp = torch.zeros((2, 4), device=DEV)
+    ids = torch.zeros((2, 4), dtype=torch.int32, device=DEV)
+    with pytest.raises(D.DynaError):
+        D.beam_expand(lp, ids, None, 0)
+    with pytest.raises(D.DynaError):
+        D.beam_expand(lp, ids, None, 65)
+    big = torch.zeros((200, 64), device=DEV)
+    with pytest.raises(D.DynaError):
+        D.beam_expand(big, torch.zeros((200, 64), dtype=torch.int32, device=DEV), None, 8)
+
+
 @pytest.mark.parametrize("t", [0, 2, 5])
 def test_pa_fr_static_head(t):
     """The position-aware frequency-ranked static head (appendix, PA-FR):

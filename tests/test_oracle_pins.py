@@ -342,6 +342,41 @@ def test_head_matches_masked_dense_head_every_k(seed):
             assert r["sample_id"] == order[int(np.nonzero(F > u[b])[0][0])]
 
 
+def test_union_head_is_the_masked_dense_head_on_the_union():
+    from scipy.special import log_softmax as ref_lsm
+    V, M = 24, 6
+    cluster_of, W, h, W1, W2, u = _tiny_problem(21, V=V, M=M, B=4)
+    s = O.router_scores(h, W1, W2, act="silu")
+    for k in (1, 2, 3):
+        out = O.draft_head(h, h, W1, W2, "silu", cluster_of, M, W, k, k_t=3, union=True)
+        chosen = {m for b in range(4) for m in sorted(range(M), key=lambda m: (-s[b, m], m))[:k]}
+        mask = np.isin(cluster_of, sorted(chosen))                      # brute-force union
+        for b, r in enumerate(out):
+            assert set(r["vocab_ids"].tolist()) == set(np.nonzero(mask)[0].tolist())
+            zfull = W @ h[b]
+            top = sorted(np.nonzero(mask)[0].tolist(), key=lambda v: (-zfull[v], v))[:3]
+            assert r["ids"].tolist() == top
+            np.testing.assert_allclose(r["logprobs"], ref_lsm(np.where(mask, zfull, -np.inf))[top], rtol=1e-12)
+    # one row: the union is that row's own shortlist
+    a = O.draft_head(h[:1], h[:1], W1, W2, "silu", cluster_of, M, W, 2, k_t=3, union=True)[0]
+    b = O.draft_head(h[:1], h[:1], W1, W2, "silu", cluster_of, M, W, 2, k_t=3)[0]
+    assert a["vocab_ids"].tolist() == b["vocab_ids"].tolist() and a["ids"].tolist() == b["ids"].tolist()
+
+
+def test_beam_expand_hand_example():
+    # two beams, three candidates each: cumulative = row log-prob + parent score
+    lp = np.log(np.array([[0.5, 0.3, 0.2], [0.6, 0.25, 0.15]]))
+    ids = np.array([[10, 11, 12], [20, 21, 22]])
+    last = np.log(np.array([0.4, 0.6]))
+    scores, parent, tok = O.beam_expand(lp, ids, last, 3)
+    # products: 0.2, 0.12, 0.08 | 0.36, 0.15, 0.09
+    assert parent.tolist() == [1, 0, 1] and tok.tolist() == [20, 10, 21]
+    np.testing.assert_allclose(np.exp(scores), [0.36, 0.2, 0.15], rtol=1e-14)
+    # ties go to the lower parent row, then the lower rank
+    s2, p2, t2 = O.beam_expand(np.zeros((2, 2)), np.array([[1, 2], [3, -1]]), None, 4)
+    assert p2.tolist() == [0, 0, 1] and t2.tolist() == [1, 2, 3]  # the empty candidate is never chosen
+
+
 def test_k_equals_M_is_the_dense_head():
     V, M = 64, 8
     cluster_of, W, h, W1, W2, u = _tiny_problem(11, V=V, M=M, d=10, B=4)
