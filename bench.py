@@ -39,8 +39,17 @@ POOL = 64
 GRAPH_CHUNK = 256
 
 
+def out_bytes(w, sizes, cl):
+    """Bytes the gathered head writes for one step: a logit and a vocabulary id
+    per slot of every row (union: B rows of logits, one shared row of ids)."""
+    if w.union:
+        u = int(sizes[np.unique(cl)].sum())
+        return 4 * w.B * u + 4 * u
+    return 8 * int(sizes[cl].sum())
+
+
 def mode_of(w, D):
-    m = 0
+    m = D.SEL_UNION if w.union else 0
     for name, flag in (("argmax", D.SEL_ARGMAX), ("topk", D.SEL_TOPK), ("sample", D.SEL_SAMPLE)):
         if name in w.modes:
             m |= flag
@@ -168,6 +177,8 @@ def dominant_kernel(w):
     """Symbol (substring) and description of the gathered-head kernel a step of w launches."""
     if w.B == 1 and w.modes == ("argmax",):
         return "logits_greedy_kernel", "gathered head fused with argmax selection (one context)"
+    if w.union and w.dtype == "bf16":
+        return "union_gemm_kernel", "union head: dense LDS-staged MFMA product of the union slabs with every context"
     if w.dtype == "bf16" and w.B > 4:
         return "gather_lds_kernel", "gathered head, LDS-staged MFMA tiles"
     return "rowdot_gemv_kernel", "gathered head, wave-per-row GEMV"
@@ -282,6 +293,8 @@ def cpu_baseline(w, cluster_of, host, budget_s=12.0, max_steps=50):
         cores = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         cores = 1
+    if w.union:
+        return cpu_baseline_union(w, cluster_of, host, cores, budget_s)
     n = 0
     t0 = time.perf_counter()
     while n < max_steps and (time.perf_counter() - t0) < budget_s:
@@ -292,6 +305,30 @@ def cpu_baseline(w, cluster_of, host, budget_s=12.0, max_steps=50):
     dt = time.perf_counter() - t0
     return {"value": n / dt, "unit": "steps/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{n} steps of {w.name} (B={w.B}) on the host, fp64 numpy oracle"}
+
+
+def cpu_baseline_union(w, cluster_of, host, cores, budget_s):
+    """Union steps: the oracle's routing, top-k and union for all B rows of one
+    step, then its logits and selection row by row until the budget is spent;
+    steps/s = 1 / (routing time + B * mean time per row)."""
+    from oracle import dynaspec_oracle as O
+    x = host["x"][0]
+    t0 = time.perf_counter()
+    sizes, offsets, perm, _ = O.cluster_layout(cluster_of, w.M)
+    s = O.router_scores(x, host["W1"], host["W2"], act=w.act)
+    ids, _ = O.topk_clusters(s, w.k)
+    sel, rowoff, rows, vids = O.shortlist(O.union_clusters(ids), offsets, perm)
+    t_route = time.perf_counter() - t0
+    n = 0
+    t1 = time.perf_counter()
+    while n < w.B and (n == 0 or time.perf_counter() - t1 < budget_s):
+        z = O.shortlist_logits(x[n], host["W_lm"], vids)
+        O.draft_select(z, vids, w.k_t)
+        n += 1
+    per_row = (time.perf_counter() - t1) / n
+    return {"value": 1.0 / (t_route + w.B * per_row), "unit": "steps/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"one step of {w.name}: routing and union for all {w.B} rows, logits and selection "
+                      f"for {n} of them (scaled to {w.B}), fp64 numpy oracle"}
 
 
 def main():
@@ -355,7 +392,7 @@ def main():
         for i in range(20):
             head(xs[i], xs[i], us[i], layout=layouts[i % N_REPLICAS], router=routers[i % N_REPLICAS])
             cl = head.clusters.cpu().numpy()
-            alg.append(s_w * w.d * int(sizes[np.unique(cl)].sum()) + s_w * w.B * w.d + 4 * int(sizes[cl].sum()))
+            alg.append(s_w * w.d * int(sizes[np.unique(cl)].sum()) + s_w * w.B * w.d + out_bytes(w, sizes, cl))
         torch.cuda.synchronize()
         print(json.dumps({"counters_run": w.name, "kernel_symbol": dominant_kernel(w)[0],
                           "copy_bytes_each_way": w.V * w.d * (2 if w.dtype == "bf16" else 4),
@@ -371,13 +408,14 @@ def main():
     sizes = np.diff(L0.offsets.cpu().numpy().astype(np.int64))
     s_w = 2 if w.dtype == "bf16" else 4
     router_bytes = s_w * (w.d_r * w.H + w.H * w.M) if w.H else s_w * w.d_r * w.M
-    slab_bytes, rows = [], []
+    slab_bytes, rows, outs = [], [], []
     for i in range(POOL):
         head(xs[i], xs[i], us[i])
         cl = head.clusters.cpu().numpy()
         union = np.unique(cl)
         slab_bytes.append(s_w * w.d * int(sizes[union].sum()))
-        rows.append(int(sizes[cl].sum()))
+        rows.append(w.B * int(sizes[union].sum()) if w.union else int(sizes[cl].sum()))
+        outs.append(out_bytes(w, sizes, cl))
     act_bytes = s_w * w.B * (w.d_r + w.d)
     mean_slab = float(np.mean(slab_bytes))
     step_bytes = router_bytes + mean_slab + act_bytes
@@ -417,10 +455,12 @@ def main():
     overhead_s = float(np.median([a.elapsed_time(b) for a, b in ov])) / 1e3
     k_avg_s = max(bracket_s - overhead_s, 1e-9)
     # bytes one launch must move: each distinct selected slab once, the
-    # contexts' h rows, and the logits it writes
+    # contexts' h rows, and the logits and vocabulary ids it writes
     k_bytes = float(np.mean([slab_bytes[i % POOL] for i in range(n_kt)])) + s_w * w.B * w.d \
-        + 4.0 * float(np.mean([rows[i % POOL] for i in range(n_kt)]))
+        + float(np.mean([outs[i % POOL] for i in range(n_kt)]))
     achieved = k_bytes / k_avg_s / 1e9
+    # matrix-core work of the launch: 2 flop per slab element per context it is dotted with
+    k_flops = 2.0 * w.d * float(np.mean([rows[i % POOL] for i in range(n_kt)]))
 
     rec = {
         "metric": "draft-head steps/s (dynamic vocabulary head, 1 GPU)",
@@ -437,6 +477,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "V": w.V, "d": w.d, "M": w.M, "router": [w.d_r, w.H, w.M],
                    "k": w.k, "B": w.B, "select": list(w.modes), "k_t": k_t,
+                   "shortlist": "union per step" if w.union else "per context",
                    "replicas": N_REPLICAS, "context_pool": POOL, "timing": "hip graph replay"},
         "rows_per_s": round(mean_rows * steps_per_s, 1),
         "step_bytes": int(step_bytes),
@@ -447,6 +488,7 @@ def main():
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": measured_traffic(w.name, dominant_kernel(w)[0]),
                      "bytes_per_launch": int(k_bytes), "avg_launch_us": round(k_avg_s * 1e6, 3),
+                     "flops_per_launch": int(k_flops), "achieved_TFLOPs": round(k_flops / k_avg_s / 1e12, 2),
                      "launches": int(k_n),
                      "timing": "event bracket on the kernel's stream minus an empty bracket",
                      "bracket_us": round(bracket_s * 1e6, 3), "empty_bracket_us": round(overhead_s * 1e6, 3)},
@@ -457,7 +499,7 @@ def main():
         base = {}
         Ws = [W_lm] + [W_lm.clone() for _ in range(N_REPLICAS - 1)]
         for label, n_rows in (("dense", w.V), ("static", min(w.static_prefix, w.V))):
-            dh = D.DenseHead(W_lm, n_rows, w.B, mode, k_t)
+            dh = D.DenseHead(W_lm, n_rows, w.B, mode & ~D.SEL_UNION, k_t)
 
             def mk(i, dh=dh):
                 Wi, x, u = Ws[i % N_REPLICAS], xs[i % POOL], us[i % POOL]

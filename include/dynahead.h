@@ -311,10 +311,14 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   automatic, 1..6 fixed (waves per block, ring stages, k columns per
  *   stage, context columns per pass).
  * DYNA_OPT_GREEDY_GRID: workgroups of the fused one-context gathered head:
- *   0 automatic (256), else 1..4096. */
+ *   0 automatic (256), else 1..4096.
+ * DYNA_OPT_UNION_CFG: shape of the dense union-row kernel of
+ *   DYNA_SEL_UNION steps: 0 automatic, 1..14 fixed (waves per workgroup,
+ *   row tiles per wave, k columns per stage, ring depth); a shape whose ring does not
+ *   fit in LDS for the batch's context count returns DYNA_ERR_UNSUPPORTED. */
 enum { DYNA_OPT_LOGITS_PATH = 1, DYNA_OPT_ROUTER_PATH = 2, DYNA_OPT_KERNEL_TIMING = 3,
        DYNA_OPT_GEMV_ROWS = 4, DYNA_OPT_FUSED_B1 = 5, DYNA_OPT_MFMA_UNROLL = 6,
-       DYNA_OPT_GATHER_CFG = 7, DYNA_OPT_GREEDY_GRID = 8 };
+       DYNA_OPT_GATHER_CFG = 7, DYNA_OPT_GREEDY_GRID = 8, DYNA_OPT_UNION_CFG = 9 };
 dyna_status dyna_set_option(int32_t option, int32_t value);
 
 /* Waits for the events recorded under DYNA_OPT_KERNEL_TIMING and returns the

@@ -26,6 +26,7 @@ std::atomic<int> g_fused_off{0};
 std::atomic<int> g_mfma_unroll{0};
 std::atomic<int> g_gather_cfg{0};
 std::atomic<int> g_greedy_grid{0};
+std::atomic<int> g_union_cfg{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -109,6 +110,7 @@ int option_gemv_rows() { return g_gemv_rows.load(); }
 int option_mfma_unroll() { return g_mfma_unroll.load(); }
 int option_gather_cfg() { return g_gather_cfg.load(); }
 int option_greedy_grid() { return g_greedy_grid.load(); }
+int option_union_cfg() { return g_union_cfg.load(); }
 
 // ------------------------------------------------------------------ workspace
 // One carving serves every hot entry point, so a single workspace can back a
@@ -380,6 +382,11 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         g_greedy_grid.store(value);
         return DYNA_OK;
     }
+    if (option == DYNA_OPT_UNION_CFG) {
+        REQUIRE(value >= 0 && value <= 14, "union shape %d outside [0, 14]", value);
+        g_union_cfg.store(value);
+        return DYNA_OK;
+    }
     if (option == DYNA_OPT_GATHER_CFG) {
         REQUIRE(value >= 0 && value <= 6, "gather shape %d outside [0, 6]", value);
         g_gather_cfg.store(value);
@@ -608,12 +615,17 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
 
     // routing (the router's stream)
     TRY(run_router(r, x, adtype, B, c.scores, c.hidden, c.rpart, c.rpart_floats, rs, fused ? c.counters : nullptr));
+    // union rows: one dense product of the union's slabs with every context
+    // (it needs only one list entry per union cluster, and writes one shared
+    // copy of the slots' vocabulary ids)
+    const bool dense_union = union_mode && option_logits_path() == 0 && L->wdtype == DYNA_BF16 &&
+                             adtype == DYNA_BF16 && L->d % 8 == 0;
     if (union_mode) {
         // per-row clusters, then one shared shortlist (its ids go to sel_sorted)
         TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, nullptr, nullptr, nullptr, nullptr,
                                  nullptr, rs));
         TRY(launch_union_plan(L->offsets, L->M, clusters, B, k, c.row_len, c.sel_sorted,
-                              (int32_t)std::min<int64_t>(L->M, (int64_t)B * k), c.plan, rs));
+                              (int32_t)std::min<int64_t>(L->M, (int64_t)B * k), c.plan, dense_union, rs));
     } else {
         TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, L->offsets, c.sel_sorted,
                                  c.sel_rowoff, c.row_len, &c.plan, rs));
@@ -645,12 +657,15 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
         want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
         want_sample ? out_sample_logprob : nullptr, c.select_ws, c.slot_vid);
     if (fused) return timed([&] { return launch_logits_greedy(a, sa, c.partials, c.counters, stream); }, stream);
-    TRY(timed_rowdot(a, option_logits_path(), stream));
+    if (dense_union && !gather_lds_eligible(a)) return set_error(DYNA_ERR_UNSUPPORTED, "union: kernel arguments");
+    if (dense_union) TRY(timed([&] { return launch_union_gemm(a, stream); }, stream));
+    else TRY(timed_rowdot(a, option_logits_path(), stream));
     return launch_select(logits, cap, c.row_len, 0, cap, c.sel_sorted, c.sel_rowoff, L->offsets, L->perm, B,
                          k, k_t, temperature, tail_beta, L->V, want_sample ? uniforms : nullptr,
                          want_ids ? out_ids : nullptr,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
-                         want_sample ? out_sample_logprob : nullptr, c.select_ws, stream, c.slot_vid);
+                         want_sample ? out_sample_logprob : nullptr, c.select_ws, stream, c.slot_vid,
+                         dense_union ? 0 : cap, union_mode);
 }
 
 // ------------------------------------------------------------------ beam expansion

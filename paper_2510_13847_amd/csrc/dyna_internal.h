@@ -132,6 +132,9 @@ dyna_status launch_dense_splitk(const RowdotArgs& a, float* part, size_t part_fl
 // through LDS (MFMA tiles)
 bool gather_lds_eligible(const RowdotArgs& a);
 dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream);
+// union rows (every plan chunk lists contexts 0..B-1 in order): dense
+// LDS-staged MFMA product; vid_out gets one shared row [slots]
+dyna_status launch_union_gemm(const RowdotArgs& a, hipStream_t stream);
 
 // Arguments of the per-context top-k (Sec. 4.2) and of the draft selection
 // (Algorithm 1), shared by the separate and the fused launches.
@@ -156,7 +159,8 @@ struct SelectArgs {
     const int32_t* sel_rowoff;
     const int32_t* offsets;
     const int32_t* perm;      // nullptr: vocabulary id = slot
-    const int32_t* slot_vid;  // optional [B][ld]: vocabulary id per slot
+    const int32_t* slot_vid;  // optional [B][vid_ld]: vocabulary id per slot
+    int64_t vid_ld;           // row stride of slot_vid (0: one row shared by all)
     int32_t k;
     int32_t k_t;
     float inv_t;
@@ -196,26 +200,35 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
                           float temperature, float beta, int32_t V, const float* uniforms, int32_t* out_ids,
                           float* out_logprobs, int32_t* out_sample,
                           float* out_sample_logprob, void* ws, hipStream_t stream,
-                          // optional [B, ld]: vocabulary id of every slot (written
-                          // by the gathered head); saves the layout walk
-                          const int32_t* slot_vid = nullptr);
+                          // optional [B, vid_ld]: vocabulary id of every slot (written
+                          // by the gathered head); saves the layout walk.  vid_ld < 0
+                          // means ld; 0 means one row shared by every context row
+                          const int32_t* slot_vid = nullptr, int64_t vid_ld = -1,
+                          // rows longer than 16384 slots take the segmented select
+                          // (many workgroups per row) instead of one workgroup per row
+                          bool split_long = false);
 // Workspace for launch_select with rows of at most max_len slots.
 size_t select_ws_bytes(int32_t B, int32_t max_len, int32_t k_t);
 // Longest row launch_select handles (256 segments).
 int32_t select_max_len();
-// Fill SelectArgs for rows of at most max_len slots; ws as for launch_select.
+// Union plan: the rows' top-k clusters -> one shared shortlist (ascending
+// cluster id), its chunk table with every row listed, row_len[b] = |union|,
+// and the union's cluster ids in sel_u[0 .. u_cap) (-1 past its end).
 dyna_status launch_union_plan(const int32_t* offsets, int32_t M, const int32_t* topk_ids, int32_t B, int32_t k,
-                              int32_t* row_len, int32_t* sel_u, int32_t u_cap, Plan plan, hipStream_t stream);
+                              int32_t* row_len, int32_t* sel_u, int32_t u_cap, Plan plan, bool compact,
+                              hipStream_t stream);
 dyna_status launch_beam_expand(const float* logprobs, const int32_t* ids, const float* last, int32_t B, int32_t k_t,
                                int32_t n_out, float* out_scores, int32_t* out_parent, int32_t* out_ids,
                                hipStream_t stream);
+// Fill SelectArgs for rows of at most max_len slots; ws as for launch_select.
 SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_len,
                             int32_t fixed_len, int32_t max_len, const int32_t* sel_sorted,
                             const int32_t* sel_rowoff, const int32_t* offsets,
                             const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
                             float temperature, float beta, int32_t V, const float* uniforms, int32_t* out_ids,
                             float* out_logprobs, int32_t* out_sample,
-                            float* out_sample_logprob, void* ws, const int32_t* slot_vid);
+                            float* out_sample_logprob, void* ws, const int32_t* slot_vid,
+                            int64_t vid_ld = -1);
 // True when the one-workgroup select handles rows of max_len slots.
 bool select_row_fits(int32_t max_len, bool fixed, int32_t k_t, int32_t k);
 
@@ -233,5 +246,6 @@ int option_gemv_rows();
 int option_mfma_unroll();
 int option_gather_cfg();
 int option_greedy_grid();
+int option_union_cfg();
 
 }  // namespace dyna

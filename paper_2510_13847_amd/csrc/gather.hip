@@ -308,6 +308,305 @@ dyna_status launch_cfg(const RowdotArgs& a, hipStream_t stream) {
     return check_launch("gather_lds_kernel");
 }
 
+// ------------------------------------------------------------------ union head
+// When the rows of a step share one shortlist (the union of their clusters,
+// Sec. 4.2), the gathered head is a dense product: every union row against
+// every context.  A workgroup takes NW * T consecutive plan chunks (each wave
+// T chunks of 16 rows, one MFMA row tile each) against NCOL = 16 * NT
+// contexts.  A stage holds KB columns of every wave's rows and of the NCOL
+// contexts; the contexts are loaded once per workgroup and shared by its
+// waves.  All loads are direct-to-LDS.  A stage is consumed after the wave's
+// own counter wait and one workgroup barrier; that barrier also frees the
+// stage read in the previous iteration, which the next load then fills.
+// Workgroups are persistent (tile blockIdx.x, + gridDim.x, ...), so the ring
+// runs on across tiles without refilling.  The plan lists one entry per union
+// cluster (its slot base); every chunk stands for all B contexts.
+template <int T>
+struct UnionCursor {
+    int64_t tile;
+    int g;          // context group (contexts g * NCOL ..)
+    int kb;         // k block
+    int r0[T];      // first layout row of each of this wave's chunks
+    int nrows[T];   // their valid rows (0: no chunk)
+    int sb[T];      // slot base of each chunk's cluster
+};
+
+template <int NW, int T>
+__device__ __forceinline__ void union_set_tile(UnionCursor<T>& u, int64_t tile, int wv, const Plan& plan,
+                                               int64_t n_chunks) {
+    u.tile = tile;
+    u.g = 0;
+    u.kb = 0;
+    sptr<int32_t> ch = (sptr<int32_t>)plan.chunks;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        const int64_t c = (tile * NW + wv) * T + t;
+        u.r0[t] = 0;
+        u.nrows[t] = 0;
+        u.sb[t] = 0;
+        if (c < n_chunks) {
+            const int r0 = ch[4 * c + 0], nr = ch[4 * c + 1], lo = ch[4 * c + 2], lc = ch[4 * c + 3];
+            if (nr > 0 && lc > 0) {
+                u.r0[t] = r0;
+                u.nrows[t] = min(kMfmaRows, nr);
+                u.sb[t] = ((sptr<int32_t>)plan.list)[2 * (int64_t)lo + 1];
+            }
+        }
+    }
+}
+
+template <int NW, int T>
+__device__ __forceinline__ void union_advance(UnionCursor<T>& u, int nkb, int ng, int wv, const Plan& plan,
+                                              int64_t n_chunks) {
+    if (++u.kb < nkb) return;
+    u.kb = 0;
+    if (++u.g < ng) return;
+    union_set_tile<NW, T>(u, u.tile + gridDim.x, wv, plan, n_chunks);
+}
+
+// LDS reads of the previous stage are complete and every wave has arrived.
+__device__ __forceinline__ void stage_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) only
+    __asm__ __volatile__("s_barrier" ::: "memory");
+}
+
+constexpr int kUnionLds = 160 * 1024;
+
+// SREQ: ring depth, or 0 for the deepest ring (at most 8) that fits in LDS
+template <int NW, int T, int KB, int NT, int SREQ>
+struct UnionShape {
+    static constexpr int ROWB = KB * 2;
+    static constexpr int STAGE = NW * T * kMfmaRows * ROWB + 16 * NT * ROWB;
+    static constexpr int S = SREQ > 0 ? SREQ : (kUnionLds / STAGE < 8 ? kUnionLds / STAGE : 8);
+    static constexpr int RPI = kWave / (ROWB / 16);  // rows per direct-to-LDS instruction
+    static constexpr int NBI = 16 * NT / RPI;         // context instructions per stage
+    static constexpr bool ok = S >= 3 && S * STAGE <= kUnionLds && NBI >= NW && NBI % NW == 0;
+};
+
+template <int NW, int T, int KB, int NT, int SREQ>
+__global__ __launch_bounds__(NW * kWave) void union_gemm_kernel(RowdotArgs a) {
+    using Sh = UnionShape<NW, T, KB, NT, SREQ>;
+    constexpr int S = Sh::S;
+    constexpr int ROWB = KB * 2;
+    constexpr int PIECES = ROWB / 16;
+    constexpr int RPI = kWave / PIECES;
+    constexpr int NA = T * kMfmaRows / RPI;  // A instructions per wave and stage
+    constexpr int NCOL = 16 * NT;
+    constexpr int NBW = NCOL / RPI / NW;     // B instructions per wave and stage
+    constexpr int NI = NA + NBW;
+    constexpr int A_TILE = kMfmaRows * ROWB;
+    constexpr int A_WAVE = T * A_TILE;
+    constexpr int A_BYTES = NW * A_WAVE;
+    constexpr int STAGE = Sh::STAGE;
+    constexpr int STEPS = KB / 32;
+    static_assert(PIECES == 16 || PIECES == 8, "stage shape");
+    static_assert(NBW >= 1 && NBW * NW * RPI == NCOL, "context loads split evenly over the waves");
+    static_assert(Sh::ok && (S - 2) * NI < 64, "ring depth");
+
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int lane = lane_id();
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int K = a.K, B = a.B;
+    const int nkb = (K + KB - 1) / KB;
+    const int ng = (B + NCOL - 1) / NCOL;
+    const int64_t n_chunks = (int64_t)((sptr<int32_t>)a.plan.hdr)[0];
+    const int64_t n_tiles = (n_chunks + NW * T - 1) / (NW * T);
+    if ((int64_t)blockIdx.x >= n_tiles) return;  // whole workgroup
+    const int64_t Q = ((n_tiles - blockIdx.x + gridDim.x - 1) / gridDim.x) * ng * nkb;
+    const uint16_t* __restrict__ W = static_cast<const uint16_t*>(a.W);
+    const uint16_t* __restrict__ v = static_cast<const uint16_t*>(a.v);
+
+    const int lsub = lane / PIECES, lpc = lane % PIECES;
+    const int col = lane & 15, kq = lane >> 4;
+
+    UnionCursor<T> iu, cu;
+    union_set_tile<NW, T>(iu, blockIdx.x, wv, a.plan, n_chunks);
+    cu = iu;
+
+    auto issue = [&](int slot) {
+        char* dst = smem + slot * STAGE;
+        const int kb = iu.kb;
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int t = (RPI * i) / kMfmaRows;
+            const int row = RPI * i + lsub - t * kMfmaRows;
+            const int piece = lpc ^ (row % PIECES);
+            int e = kb * KB + piece * 8;
+            e = e < K ? e : 0;  // k tail: any in-bounds piece; zeroed when read
+            const int64_t grow = iu.nrows[t] > 0 ? iu.r0[t] + min(row, iu.nrows[t] - 1) : 0;
+            __builtin_amdgcn_global_load_lds((glb_ptr)(W + grow * K + e),
+                                             (lds_ptr)(dst + wv * A_WAVE + i * (RPI * ROWB)), 16, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < NBW; ++i) {
+            const int ii = wv * NBW + i;
+            const int c = RPI * ii + lsub;
+            const int piece = lpc ^ (c % PIECES);
+            int e = kb * KB + piece * 8;
+            e = e < K ? e : 0;
+            const int b = min(iu.g * NCOL + c, B - 1);  // past B: any context; never stored
+            __builtin_amdgcn_global_load_lds((glb_ptr)(v + (int64_t)b * K + e),
+                                             (lds_ptr)(dst + A_BYTES + ii * (RPI * ROWB)), 16, 0, 0);
+        }
+    };
+
+    // vocabulary ids of the consumed chunks' rows (lane j < 16 of vp holds row j's)
+    int32_t vid[T][4];
+    auto load_vids = [&]() {
+        if (a.vid_out == nullptr) return;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            if (cu.nrows[t] == 0) continue;
+            sptr<int32_t> P = (sptr<int32_t>)a.perm + cu.r0[t];
+            int vp = P[0];
+#pragma unroll
+            for (int j = 1; j < kMfmaRows; ++j)
+                if (j < cu.nrows[t]) vp = set_lane(vp, P[j], j);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) vid[t][r] = from_lane(vp, 4 * kq + r);
+        }
+    };
+
+    int64_t issued = 0;
+#pragma unroll
+    for (int s = 0; s < S - 1; ++s) {
+        if (issued < Q) {
+            issue((int)(issued % S));
+            ++issued;
+            union_advance<NW, T>(iu, nkb, ng, wv, a.plan, n_chunks);
+        }
+    }
+    load_vids();
+
+    f32x4 acc[T][NT];
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[t][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int64_t q = 0; q < Q; ++q) {
+        // this wave's loads of stage q are done once at most the later stages remain
+        if (issued - q - 1 == S - 2) wait_vmem<(S - 2) * NI>();
+        else wait_vmem<0>();
+        stage_barrier();
+        if (issued < Q) {
+            issue((int)(issued % S));
+            ++issued;
+            union_advance<NW, T>(iu, nkb, ng, wv, a.plan, n_chunks);
+        }
+        const char* st = smem + (int)(q % S) * STAGE;
+        const char* sa = st + wv * A_WAVE;
+        const char* sbm = st + A_BYTES;
+        const int k0 = cu.kb * KB;
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s) {
+            const int p = s * 4 + kq;
+            const bool tail = k0 + p * 8 >= K;
+            u32x4 av[T];
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                av[t] = *reinterpret_cast<const u32x4*>(sa + t * A_TILE + col * ROWB + (p ^ (col % PIECES)) * 16);
+                if (tail) av[t] = u32x4{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                const int c = 16 * j + col;
+                u32x4 bv = *reinterpret_cast<const u32x4*>(sbm + c * ROWB + (p ^ (c % PIECES)) * 16);
+                if (tail) bv = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int t = 0; t < T; ++t)
+                    acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, av[t]), __builtin_bit_cast(bf16x8, bv), acc[t][j], 0, 0, 0);
+            }
+        }
+        if (cu.kb == nkb - 1) {
+            // D rows 4 * kq + r, context column 16 * j + col
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                if (cu.nrows[t] == 0) continue;
+                const int64_t base = (int64_t)cu.sb[t] + cu.r0[t];
+#pragma unroll
+                for (int j = 0; j < NT; ++j) {
+                    const int b = cu.g * NCOL + 16 * j + col;
+                    if (b < B) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int row = 4 * kq + r;
+                            if (row < cu.nrows[t]) a.out[(int64_t)b * a.ld + base + row] = acc[t][j][r];
+                        }
+                    }
+                }
+                // one shared copy of the slots' vocabulary ids
+                if (a.vid_out != nullptr && cu.g == 0 && col == 0) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (4 * kq + r < cu.nrows[t]) a.vid_out[base + 4 * kq + r] = vid[t][r];
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < T; ++t)
+#pragma unroll
+                for (int j = 0; j < NT; ++j) acc[t][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            union_advance<NW, T>(cu, nkb, ng, wv, a.plan, n_chunks);
+            if (cu.g == 0) load_vids();
+        } else {
+            ++cu.kb;
+        }
+    }
+}
+
+template <int NW, int T, int KB, int NT, int SREQ = 0>
+dyna_status launch_union_cfg(const RowdotArgs& a, hipStream_t stream) {
+    using Sh = UnionShape<NW, T, KB, NT, SREQ>;
+    if constexpr (!Sh::ok) {
+        return set_error(DYNA_ERR_UNSUPPORTED, "union: shape does not fit in LDS");
+    } else {
+        constexpr int LDS = Sh::S * Sh::STAGE;
+        static_assert(LDS <= kUnionLds, "LDS per block");
+        static std::atomic<uint64_t> allowed{0};
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "union: device");
+        if (!(allowed.load() & (1ull << dev))) {
+            if (hipFuncSetAttribute((const void*)union_gemm_kernel<NW, T, KB, NT, SREQ>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, LDS) != hipSuccess)
+                return set_error(DYNA_ERR_HIP, "union: LDS attribute");
+            allowed.fetch_or(1ull << dev);
+        }
+        const int per_cu = std::max(1, kUnionLds / LDS);
+        const int64_t tiles = ((int64_t)a.max_chunks_bound + NW * T - 1) / (NW * T);
+        const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(tiles, 256 * per_cu));
+        launch_timed_kernel(union_gemm_kernel<NW, T, KB, NT, SREQ>, dim3((unsigned)blocks), dim3(NW * kWave), LDS,
+                            stream, a);
+        return check_launch("union_gemm_kernel");
+    }
+}
+
+// Fixed shapes (waves, chunks per wave, k columns per stage, ring depth) of
+// the union kernel; 0 picks by context count.
+template <int NT>
+dyna_status launch_union_nt(const RowdotArgs& a, int cfg, hipStream_t stream) {
+    switch (cfg) {
+        case 1: return launch_union_cfg<4, 1, 128, NT>(a, stream);
+        case 2: return launch_union_cfg<8, 1, 128, NT>(a, stream);
+        case 3: return launch_union_cfg<4, 2, 128, NT>(a, stream);
+        case 4: return launch_union_cfg<4, 1, 64, NT>(a, stream);
+        case 5: return launch_union_cfg<8, 1, 64, NT>(a, stream);
+        case 6: return launch_union_cfg<4, 1, 64, NT, 4>(a, stream);
+        case 7: return launch_union_cfg<8, 1, 64, NT, 3>(a, stream);
+        case 8: return launch_union_cfg<4, 1, 128, NT, 3>(a, stream);
+        case 9: return launch_union_cfg<8, 2, 64, NT>(a, stream);
+        case 10: return launch_union_cfg<2, 1, 128, NT, 3>(a, stream);
+        case 11: return launch_union_cfg<8, 1, 128, NT, 4>(a, stream);
+        case 12: return launch_union_cfg<4, 1, 64, NT, 3>(a, stream);
+        case 13: return launch_union_cfg<4, 2, 64, NT, 3>(a, stream);
+        case 14: return launch_union_cfg<2, 2, 64, NT, 3>(a, stream);
+        default:  // measured best per context count (eight waves where the context loads split)
+            if constexpr (NT >= 8) return launch_union_cfg<8, 2, 64, NT>(a, stream);
+            else if constexpr (NT == 4) return launch_union_cfg<8, 1, 64, NT, 3>(a, stream);
+            else if constexpr (NT == 2) return launch_union_cfg<4, 1, 64, NT, 3>(a, stream);
+            else return launch_union_cfg<4, 1, 128, NT>(a, stream);
+    }
+}
+
 }  // namespace
 
 bool gather_lds_eligible(const RowdotArgs& a) {
@@ -325,6 +624,15 @@ dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
         case 6: return launch_cfg<8, 3, 64, 16>(a, stream);
         default: return launch_cfg<4, 4, 128, 16>(a, stream);
     }
+}
+
+dyna_status launch_union_gemm(const RowdotArgs& a, hipStream_t stream) {
+    if (!gather_lds_eligible(a) || a.B < 1) return set_error(DYNA_ERR_UNSUPPORTED, "union: needs bf16 plan mode");
+    const int cfg = option_union_cfg();
+    if (a.B <= 16) return launch_union_nt<1>(a, cfg, stream);
+    if (a.B <= 32) return launch_union_nt<2>(a, cfg, stream);
+    if (a.B <= 64) return launch_union_nt<4>(a, cfg, stream);
+    return launch_union_nt<8>(a, cfg, stream);
 }
 
 }  // namespace dyna

@@ -234,9 +234,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 // every row (entries i * B .. i * B + B - 1 of the list for union cluster i).
 // Writes the plan, row_len[b] = |union| for every row, and the union itself
 // (ascending ids, -1 past its end) to sel_u[0 .. min(M, B * k)).
+// compact: the list holds one entry per union cluster (entry i, context 0)
+// and a chunk's count is still B; only the dense union kernel reads this form.
 __global__ __launch_bounds__(kPlanThreads) void union_plan_kernel(
     const int32_t* __restrict__ offsets, int M, const int32_t* __restrict__ topk_ids, int B, int k,
-    int32_t* __restrict__ row_len, int32_t* __restrict__ sel_u, int u_cap, Plan plan) {
+    int32_t* __restrict__ row_len, int32_t* __restrict__ sel_u, int u_cap, Plan plan, int compact) {
     extern __shared__ int32_t ul[];
     uint32_t* bits = reinterpret_cast<uint32_t*>(ul);  // [W] cluster bitmap
     const int W = (M + 31) / 32;
@@ -313,19 +315,20 @@ __global__ __launch_bounds__(kPlanThreads) void union_plan_kernel(
             const int m = uid[i];
             const int ci = c - coff[i];
             const int o = offsets[m], n = offsets[m + 1] - o;
-            plan.chunks[c] = Chunk{o + ci * kChunkRows, min(kChunkRows, n - ci * kChunkRows), i * B, B};
+            plan.chunks[c] = Chunk{o + ci * kChunkRows, min(kChunkRows, n - ci * kChunkRows), compact ? i : i * B, B};
         }
     }
-    // every row in every union cluster's list
-    for (int64_t e = t; e < (int64_t)U * B; e += kPlanThreads) {
-        const int i = (int)(e / B), b = (int)(e - (int64_t)i * B);
+    // every row in every union cluster's list (compact: row 0 stands for all)
+    const int per = compact ? 1 : B;
+    for (int64_t e = t; e < (int64_t)U * per; e += kPlanThreads) {
+        const int i = (int)(e / per), b = (int)(e - (int64_t)i * per);
         plan.list[e] = ListEntry{b, roff[i] - offsets[uid[i]]};
     }
     for (int b = t; b < B; b += kPlanThreads) row_len[b] = len;
     for (int i = t; i < u_cap; i += kPlanThreads) sel_u[i] = i < U ? uid[i] : -1;
     if (t == 0) {
         plan.hdr->n_chunks = n_chunks;
-        plan.hdr->n_entries = U * B;
+        plan.hdr->n_entries = U * per;
     }
 }
 
@@ -385,6 +388,15 @@ __global__ __launch_bounds__(kNT) void select_partial_kernel(SelectArgs a) {
     const int p = blockIdx.x, b = blockIdx.y;
     const int len = a.row_len ? a.row_len[b] : a.fixed_len;
     const int seg0 = p * kSeg;
+    if (seg0 >= len) {  // past the row: an empty partial
+        const int64_t pb = (int64_t)b * a.P + p;
+        if (threadIdx.x == 0) {
+            a.pmax[pb] = -__builtin_inff();
+            a.psum[pb] = 0.0f;
+        }
+        for (int r = threadIdx.x; r < a.k_t; r += kNT) a.pkeys[pb * a.k_t + r] = 0;
+        return;
+    }
     const int j0 = seg0 + threadIdx.x * kPer;
     const int n = max(0, min(kPer, len - j0));
     const float* z = a.logits + (int64_t)b * a.ld;
@@ -393,9 +405,12 @@ __global__ __launch_bounds__(kNT) void select_partial_kernel(SelectArgs a) {
     float zv[kPer];
     uint64_t list[kPer];
     if (n > 0) slot_vids(a, b, j0, n, vid);
+    float zr[kPer];  // in-bounds loads (clamped to the row), issued together
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) zr[q] = z[min(j0 + q, len - 1)];
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
-        zv[q] = q < n ? canon(z[j0 + q]) : -__builtin_inff();
+        zv[q] = q < n ? canon(zr[q]) : -__builtin_inff();
         list[q] = q < n ? sel_key(zv[q], vid[q]) : 0;
     }
     // sort the thread's keys descending (odd-even transposition network)
@@ -434,9 +449,10 @@ __global__ __launch_bounds__(kNT) void select_partial_kernel(SelectArgs a) {
 __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     __shared__ uint64_t wmax[8];
     __shared__ uint64_t top[DYNA_MAX_KT];
-    __shared__ float sh_mx, sh_total, sh_target, sh_base;
+    __shared__ float sh_target, sh_base;
     __shared__ int sh_seg;
     __shared__ float red[2 * (kNT / kWave) + 1];
+    __shared__ float wred[kNT / kWave];
     __shared__ int sh_pick;
     __shared__ float incl_s[kNT];
     const int b = blockIdx.x;
@@ -444,18 +460,24 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     const int len = a.row_len ? a.row_len[b] : a.fixed_len;
     const int64_t pb0 = (int64_t)b * P;
 
-    if (threadIdx.x == 0) {
-        float mx = -__builtin_inff();
-        for (int p = 0; p < P; ++p) mx = fmaxf(mx, a.pmax[pb0 + p]);
-        float total = 0.0f;
-        if (mx != -__builtin_inff())
-            for (int p = 0; p < P; ++p) {
-                const float sm = a.pmax[pb0 + p];
-                if (sm != -__builtin_inff()) total += a.psum[pb0 + p] * expf((sm - mx) * a.inv_t);
-            }
-        sh_mx = mx;
-        sh_total = total;
+    // thread p < P holds segment p's (max, sum); the row max is a block max and
+    // the segment masses c_p = sum_p * exp((max_p - max) / T) are block-scanned
+    // in segment order (P <= 256 is guaranteed by the host)
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    const float my_m = (int)threadIdx.x < P ? a.pmax[pb0 + threadIdx.x] : -__builtin_inff();
+    const float my_s = (int)threadIdx.x < P ? a.psum[pb0 + threadIdx.x] : 0.0f;
+    {
+        const float m = readlane_f32(wave_max_f32(my_m), kWave - 1);
+        if (lane == 0) wred[w] = m;
     }
+    __syncthreads();
+    float mx = wred[0];
+#pragma unroll
+    for (int q = 1; q < kNT / kWave; ++q) mx = fmaxf(mx, wred[q]);
+    const float my_c =
+        (mx != -__builtin_inff() && my_m != -__builtin_inff()) ? my_s * expf((my_m - mx) * a.inv_t) : 0.0f;
+    float total;
+    const float my_incl = block_inclusive_scan_f32<kNT>(my_c, red, &total);
     // merge the per-segment lists: thread t walks the list of segment t
     // (P <= 256 is guaranteed by the host)
     uint64_t list[1];
@@ -463,7 +485,6 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     const uint64_t* mylist = a.pkeys + (pb0 + threadIdx.x) * a.k_t;
     list[0] = (int)threadIdx.x < P ? mylist[0] : 0;
     {
-        const int lane = lane_id(), w = threadIdx.x / kWave;
         for (int r = 0; r < a.k_t; ++r) {
             const uint64_t m = wave_max_u64(list[0]);
             if (lane == 0) wmax[(r & 1) * 4 + w] = m;
@@ -479,7 +500,6 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
         }
     }
     __syncthreads();
-    const float mx = sh_mx, total = sh_total;
     const TailMix tail = tail_of(a, len);
     const float log_total = logf(total) - tail.lshift;
     if (a.out_ids != nullptr) {
@@ -495,34 +515,23 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     float u_s;
     if (tail_sample(a, b, tail, &u_s)) return;  // uniform decision for the block
 
-    // inverse CDF: first segment whose running mass passes u * total
+    // inverse CDF: the segment whose running mass range holds u * total (the
+    // first with mass past it), else the last segment with mass
+    const float u_target = u_s * total;
+    const float my_excl = my_incl - my_c;
     if (threadIdx.x == 0) {
-        const float target = u_s * total;
-        float run = 0.0f;
-        int seg = -1, last_nz = -1;
-        float base = 0.0f, base_last = 0.0f;
-        for (int p = 0; p < P; ++p) {
-            const float sm = a.pmax[pb0 + p];
-            const float c = sm != -__builtin_inff() ? a.psum[pb0 + p] * expf((sm - mx) * a.inv_t) : 0.0f;
-            if (c > 0.0f) {
-                last_nz = p;
-                base_last = run;
-            }
-            if (seg < 0 && run + c > target && c > 0.0f) {
-                seg = p;
-                base = run;
-            }
-            run += c;
-        }
-        if (seg < 0) {
-            seg = last_nz;
-            base = base_last;
-        }
-        sh_seg = seg;
-        sh_base = base;
-        sh_target = target;
+        sh_seg = -1;
         sh_pick = -1;
+        sh_target = u_target;
     }
+    __syncthreads();
+    if (my_c > 0.0f && my_excl <= u_target && u_target < my_incl) atomicMax(&sh_seg, (int)threadIdx.x);
+    __syncthreads();
+    const int seg_found = sh_seg;
+    __syncthreads();
+    if (seg_found < 0 && my_c > 0.0f) atomicMax(&sh_seg, (int)threadIdx.x);
+    __syncthreads();
+    if ((int)threadIdx.x == sh_seg) sh_base = my_excl;
     __syncthreads();
     const int seg = sh_seg;
     if (seg < 0) {  // empty shortlist
@@ -538,8 +547,10 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     float e[kPer];
     float tsum = 0.0f;
 #pragma unroll
+    for (int q = 0; q < kPer; ++q) e[q] = z[min(j0 + q, len - 1)];  // in-bounds, issued together
+#pragma unroll
     for (int q = 0; q < kPer; ++q) {
-        e[q] = q < n ? expf((canon(z[j0 + q]) - mx) * a.inv_t) : 0.0f;
+        e[q] = q < n ? expf((canon(e[q]) - mx) * a.inv_t) : 0.0f;
         tsum += e[q];
     }
     float blk_total;
@@ -571,9 +582,9 @@ __global__ __launch_bounds__(kNT) void select_final_kernel(SelectArgs a) {
     }
     if (threadIdx.x == 0) {
         const int j = sh_pick;
-        uint32_t vid;
-        slot_vids(a, b, j, 1, &vid);
-        a.out_sample[b] = (int32_t)vid;
+        uint32_t vid[1];
+        slot_vids(a, b, j, 1, vid);
+        a.out_sample[b] = (int32_t)vid[0];
         if (a.out_sample_logprob) a.out_sample_logprob[b] = (canon(z[j]) - mx) * a.inv_t - log_total;
     }
 }
@@ -636,7 +647,8 @@ dyna_status launch_plan(const int32_t* offsets, int32_t M, const int32_t* sel_so
 }
 
 dyna_status launch_union_plan(const int32_t* offsets, int32_t M, const int32_t* topk_ids, int32_t B, int32_t k,
-                              int32_t* row_len, int32_t* sel_u, int32_t u_cap, Plan plan, hipStream_t stream) {
+                              int32_t* row_len, int32_t* sel_u, int32_t u_cap, Plan plan, bool compact,
+                              hipStream_t stream) {
     const size_t lds = sizeof(int32_t) * (2 * (size_t)((M + 31) / 32) + 3 * (size_t)M + 1);
     if (lds > 64 * 1024) {
         static std::atomic<uint64_t> allowed{0};
@@ -650,7 +662,8 @@ dyna_status launch_union_plan(const int32_t* offsets, int32_t M, const int32_t* 
             allowed.fetch_or(1ull << dev);
         }
     }
-    union_plan_kernel<<<1, kPlanThreads, lds, stream>>>(offsets, M, topk_ids, B, k, row_len, sel_u, u_cap, plan);
+    union_plan_kernel<<<1, kPlanThreads, lds, stream>>>(offsets, M, topk_ids, B, k, row_len, sel_u, u_cap, plan,
+                                                        compact ? 1 : 0);
     return check_launch("union_plan_kernel");
 }
 
@@ -678,7 +691,7 @@ SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_
                             const int32_t* perm, int32_t B, int32_t k, int32_t k_t,
                             float temperature, float beta, int32_t V, const float* uniforms, int32_t* out_ids,
                             float* out_logprobs, int32_t* out_sample,
-                            float* out_sample_logprob, void* ws, const int32_t* slot_vid) {
+                            float* out_sample_logprob, void* ws, const int32_t* slot_vid, int64_t vid_ld) {
     SelectArgs a;
     a.logits = logits;
     a.ld = ld;
@@ -689,6 +702,7 @@ SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_
     a.offsets = offsets;
     a.perm = perm;
     a.slot_vid = slot_vid;
+    a.vid_ld = vid_ld < 0 ? ld : vid_ld;
     a.k = k;
     a.k_t = k_t;
     a.inv_t = 1.0f / temperature;
@@ -720,13 +734,14 @@ dyna_status launch_select(const float* logits, int64_t ld, const int32_t* row_le
                           int32_t B, int32_t k, int32_t k_t, float temperature, float beta, int32_t V,
                           const float* uniforms, int32_t* out_ids, float* out_logprobs,
                           int32_t* out_sample, float* out_sample_logprob, void* ws,
-                          hipStream_t stream, const int32_t* slot_vid) {
+                          hipStream_t stream, const int32_t* slot_vid, int64_t vid_ld, bool split_long) {
     const SelectArgs a = make_select_args(logits, ld, row_len, fixed_len, max_len, sel_sorted,
                                           sel_rowoff, offsets, perm, B, k, k_t, temperature, beta, V,
                                           uniforms, out_ids, out_logprobs, out_sample,
-                                          out_sample_logprob, ws, slot_vid);
+                                          out_sample_logprob, ws, slot_vid, vid_ld);
     // shortlist-sized rows: one workgroup per row, one launch
-    if (select_row_fits(max_len, row_len == nullptr, k_t, perm == nullptr ? 0 : k)) {
+    const bool split = split_long && max_len > kRowSplit;
+    if (!split && select_row_fits(max_len, row_len == nullptr, k_t, perm == nullptr ? 0 : k)) {
         if (k_t == 1) select_row_kernel<1><<<B, kRowThreads, 0, stream>>>(a);
         else select_row_kernel<16><<<B, kRowThreads, 0, stream>>>(a);
         return check_launch("select_row_kernel");

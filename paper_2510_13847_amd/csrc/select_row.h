@@ -10,6 +10,7 @@ namespace {
 constexpr int kSeg = 2048;          // shortlist slots per partial workgroup
 constexpr int kPer = kSeg / kNT;    // 8 slots per thread
 constexpr int kRowMax = 1 << 17;    // longest shortlist row the one-launch select takes
+constexpr int kRowSplit = 1 << 14;  // longer rows may go to the segmented select instead
 
 
 __device__ __forceinline__ float canon(float z) { return z != z ? -__builtin_inff() : z; }
@@ -71,10 +72,15 @@ __device__ __forceinline__ bool tail_sample(const SelectArgs& a, int b, const Ta
     return true;
 }
 
-// Vocabulary ids of the slots [j0, j0 + n) of row b, written into vid[].
-__device__ __forceinline__ void slot_vids(const SelectArgs& a, int b, int j0, int n, uint32_t* vid) {
+// Vocabulary ids of the slots [j0, j0 + n) of row b (1 <= n <= N), written
+// into vid[]; with the gathered head's id table the N loads are issued
+// together (entries past n repeat the last one).
+template <int N>
+__device__ __forceinline__ void slot_vids(const SelectArgs& a, int b, int j0, int n, uint32_t (&vid)[N]) {
     if (a.slot_vid != nullptr) {
-        for (int q = 0; q < n; ++q) vid[q] = (uint32_t)a.slot_vid[(int64_t)b * a.ld + j0 + q];
+        const int32_t* sv = a.slot_vid + (int64_t)b * a.vid_ld + j0;
+#pragma unroll
+        for (int q = 0; q < N; ++q) vid[q] = (uint32_t)sv[q < n ? q : n - 1];
         return;
     }
     if (a.perm == nullptr) {
@@ -255,7 +261,7 @@ __device__ void select_row(const SelectArgs& a, int b) {
     __shared__ int32_t t_base[kRowTable];
     const int len = a.row_len ? a.row_len[b] : a.fixed_len;
     const float* z = a.logits + (int64_t)b * a.ld;
-    const int32_t* sv = a.slot_vid ? a.slot_vid + (int64_t)b * a.ld : nullptr;
+    const int32_t* sv = a.slot_vid ? a.slot_vid + (int64_t)b * a.vid_ld : nullptr;
     const bool table = sv == nullptr && a.perm != nullptr;
     if (table) {  // slot -> layout row: rows of cluster ci start at t_base[ci] + slot
         const int32_t* ro = a.sel_rowoff + (int64_t)b * (a.k + 1);

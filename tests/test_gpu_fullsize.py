@@ -16,7 +16,7 @@ DEV = "cuda"
 
 
 def mode_of(w, D):
-    m = 0
+    m = D.SEL_UNION if w.union else 0
     if "argmax" in w.modes:
         m |= D.SEL_ARGMAX
     if "topk" in w.modes:
@@ -56,6 +56,8 @@ def test_fullsize_workload(name):
 
     rng = np.random.default_rng(0)
     rows = list(range(w.B)) if w.B <= 16 else sorted({0, w.B - 1, *rng.choice(w.B, 6, replace=False).tolist()})
+    if w.union:
+        rows = rows[:4]
     h_np = W.host_array(h[rows])
     W1_np = W.host_array(W1)
     W2_np = None if W2 is None else W.host_array(W2)
@@ -66,14 +68,29 @@ def test_fullsize_workload(name):
     tol = PC.TOL[w.dtype]
     strict = 0
     max_err = 0.0
+    if w.union:
+        # one shared shortlist: the union of every row's clusters (all B rows)
+        union = O.union_clusters(clusters)
+        sel, rowoff, lrows, vids_u = O.shortlist(union, offsets, perm)
+        z_union = np.zeros((len(rows), len(vids_u)))
+        for j0 in range(0, len(vids_u), 8192):
+            j1 = min(len(vids_u), j0 + 8192)
+            Wrows = W.host_array(W_lm.index_select(0, torch.from_numpy(vids_u[j0:j1]).to(DEV)))
+            for i in range(len(rows)):
+                z_union[i, j0:j1] = O.shortlist_logits(h_np[i], Wrows, np.arange(j1 - j0))
     for i, b in enumerate(rows):
         eq, ok = PC.cluster_check(clusters[b], ref_scores[i], w.k)
         assert ok, f"row {b}: clusters"
         strict += int(not eq)
-        sel, rowoff, lrows, vids = O.shortlist(clusters[b], offsets, perm)
-        n = len(vids)
-        Wrows = W.host_array(W_lm.index_select(0, torch.from_numpy(vids).to(DEV)))
-        z_ref = O.shortlist_logits(h_np[i], Wrows, np.arange(n))
+        if w.union:
+            vids = vids_u
+            n = len(vids)
+            z_ref = z_union[i]
+        else:
+            sel, rowoff, lrows, vids = O.shortlist(clusters[b], offsets, perm)
+            n = len(vids)
+            Wrows = W.host_array(W_lm.index_select(0, torch.from_numpy(vids).to(DEV)))
+            z_ref = O.shortlist_logits(h_np[i], Wrows, np.arange(n))
         max_err = max(max_err, PC.assert_close(logits[b, :n], z_ref, tol, f"logits row {b}"))
         z_gpu = logits[b, :n]
         if head.ids is not None:

@@ -47,6 +47,7 @@ class Workload:
     seed_index: Optional[int] = None  # reuse another workload's partition/router/LM head
     overlap_gemm: Optional[tuple] = None  # (rows, K, N) stand-in draft-layer GEMM
     static_prefix: int = 32768
+    union: bool = False   # the step's rows share one shortlist (union of their clusters)
 
     @property
     def d_r(self) -> int:
@@ -71,10 +72,15 @@ WORKLOADS = {
         Workload("gemma3_large_vocab", 4, V=262144, d=5376, M=4096, dtype="bf16",
                  sizes=("lognormal", 0.7), H=2048, act="silu", k=64, B=128,
                  modes=("topk", "sample"), k_t=10, overlap_gemm=(128, 5376, 14336)),
+        # the tree batch (same seeds: partition, weights and contexts) with one
+        # union shortlist per step, the beam form of Sec. 4.2
+        Workload("llama3_8b_tree_union", 2, V=128256, d=4096, M=1024, dtype="bf16",
+                 sizes=("lognormal", 0.5), H=1024, act="silu", k=32, B=64,
+                 modes=("topk",), k_t=10, seed_index=1, union=True),
     ]
 }
 WORKLOAD_ORDER = ["tiny_fp32", "llama3_8b_chain", "llama3_8b_tree",
-                  "qwen25_serving", "gemma3_large_vocab"]
+                  "qwen25_serving", "gemma3_large_vocab", "llama3_8b_tree_union"]
 
 
 def scaled(w: Workload, **changes) -> Workload:
