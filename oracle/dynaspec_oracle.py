@@ -29,7 +29,13 @@ Readings where the paper is silent (each is listed in the design notes):
     (T = 1 gives Algorithm 1's log_softmax(z)); sampling walks the CDF in
     shortlist order and returns the first j with F_j > u, else the last j
     with p_j > 0;
-  * the router's hidden activation is not re-rounded (fp64 here).
+  * the router's hidden activation is not re-rounded (fp64 here);
+  * the partition itself comes from spherical k-means on the unit LM-head
+    rows (Sec. 4.2): centroids start at caller-chosen points, each round
+    assigns every point to its most similar centroid (ties to the lower id;
+    the similarity is taken with centroids in bf16, the kernel's operand
+    precision) and then sets each centroid to the mean direction of its
+    points; an empty cluster keeps its centroid.
 
 Every function below has a pin in tests/test_oracle_pins.py.
 """
@@ -368,3 +374,80 @@ def pa_fr_budget(t: int, k_max: int) -> int:
     if t < 2:
         return k_max
     return k_max // (t + 1)
+
+
+# --------------------------------------------------------------------------
+# building the partition: spherical k-means (Sec. 4.2, "Vocabulary partition")
+# --------------------------------------------------------------------------
+def round_bf16(a) -> np.ndarray:
+    """Values rounded to bf16 (round to nearest, ties to even), returned as
+    float64.  Used only where a decision is taken in the kernel's operand
+    precision: a float32 value keeps its upper 16 bits after adding half an
+    ulp of bf16 plus the parity bit of the kept part."""
+    f = np.asarray(a, dtype=np.float64).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    keep = ((u >> np.uint64(16)) & np.uint64(1))
+    r = ((u + np.uint64(0x7FFF) + keep) >> np.uint64(16)) << np.uint64(16)
+    r = np.where(np.isnan(f), u, r)  # NaN stays NaN
+    return (r.astype(np.uint32)).view(np.float32).astype(np.float64)
+
+
+def unit_rows(W) -> np.ndarray:
+    """The paper's points: every LM-head column (here row) divided by its
+    2-norm; an all-zero row stays zero (it has no direction)."""
+    X = as_f64(W)
+    n = np.sqrt((X * X).sum(axis=1))
+    out = np.zeros_like(X)
+    nz = n > 0
+    out[nz] = X[nz] / n[nz, None]
+    return out
+
+
+def kmeans_assign(W, centroids):
+    """Assignment step: each point goes to the centroid of largest cosine
+    similarity, x_v . mu_m for unit mu_m; ties go to the lower cluster id.
+    The centroids enter in the kernel's operand precision (bf16); the
+    similarities are formed in float64.  Returns (assign[V], S[V, M])."""
+    X = unit_rows(W)
+    S = X @ round_bf16(centroids).T
+    return np.argmax(_canonical(S), axis=1).astype(np.int64), S
+
+
+def kmeans_update(W, assign, M: int, prev):
+    """Update step: mu_m = sum of the unit points assigned to m, divided by
+    its norm (the mean direction).  A cluster with no points (or a zero sum)
+    keeps its previous centroid."""
+    X = unit_rows(W)
+    assign = np.asarray(assign, dtype=np.int64)
+    mu = np.array(np.asarray(prev, dtype=np.float64), copy=True)
+    for m in range(M):
+        members = np.nonzero(assign == m)[0]
+        if len(members) == 0:
+            continue
+        s = X[members].sum(axis=0)
+        n = np.sqrt((s * s).sum())
+        if n > 0:
+            mu[m] = s / n
+    return mu
+
+
+def spherical_kmeans(W, M: int, init_ids, iters: int):
+    """Spherical k-means on the unit LM-head rows: centroids start at the
+    points init_ids (M distinct vocabulary ids, drawn by the caller), then
+    `iters` rounds of assignment followed by update.  Returns the last
+    assignment (the partition, cluster_of[V]) and the centroids after the
+    last update."""
+    X = unit_rows(W)
+    mu = X[np.asarray(init_ids, dtype=np.int64)]
+    assign = np.zeros(X.shape[0], dtype=np.int64)
+    for _ in range(iters):
+        assign, _ = kmeans_assign(W, mu)
+        mu = kmeans_update(W, assign, M, mu)
+    return assign, mu
+
+
+def kmeans_objective(W, assign, centroids) -> float:
+    """Sum over points of the cosine similarity to their own centroid."""
+    X = unit_rows(W)
+    mu = np.asarray(centroids, dtype=np.float64)
+    return float((X * mu[np.asarray(assign, dtype=np.int64)]).sum())

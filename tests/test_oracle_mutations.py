@@ -140,6 +140,42 @@ def schedule_eq_without_t(t, k0, k1, k_min=1):
     return max(k_min, k1 // (2 * t))
 
 
+def kmeans_update_raw_rows(W, assign, M, prev):
+    Wf = O.as_f64(W)
+    mu = np.array(np.asarray(prev, dtype=np.float64), copy=True)
+    assign = np.asarray(assign)
+    for m in range(M):
+        mem = np.nonzero(assign == m)[0]
+        if len(mem):
+            s = Wf[mem].sum(axis=0)  # rows not normalised first
+            mu[m] = s / np.linalg.norm(s)
+    return mu
+
+
+def kmeans_ties_high(W, centroids):
+    a, S = ORIG["kmeans_assign"](W, centroids)
+    M = S.shape[1]
+    return (M - 1 - np.argmax(O._canonical(S)[:, ::-1], axis=1)).astype(np.int64), S
+
+
+def kmeans_empty_to_zero(W, assign, M, prev):
+    mu = ORIG["kmeans_update"](W, assign, M, prev)
+    counts = np.bincount(np.asarray(assign, dtype=np.int64), minlength=M)
+    mu[counts == 0] = 0.0
+    return mu
+
+
+def kmeans_argmin(W, centroids):
+    a, S = ORIG["kmeans_assign"](W, centroids)
+    return np.argmin(S, axis=1).astype(np.int64), S
+
+
+def round_bf16_truncates(a):
+    f = np.asarray(a, dtype=np.float64).astype(np.float32)
+    u = f.view(np.uint32) & np.uint32(0xFFFF0000)
+    return u.view(np.float32).astype(np.float64)
+
+
 MUTANTS = {
     "layout: descending ids inside a cluster": ("cluster_layout", layout_desc_within_cluster,
         [P.test_layout_hand_example, lambda: P.test_layout_is_disjoint_covering_and_contiguous(0)]),
@@ -182,6 +218,16 @@ MUTANTS = {
         [P.test_static_head_is_the_dense_head_on_a_prefix]),
     "schedule: floor(k1 / 2t)": ("k_schedule", schedule_eq_without_t,
         [P.test_k_schedule_closed_form]),
+    "k-means: update sums the raw rows": ("kmeans_update", kmeans_update_raw_rows,
+        [P.test_kmeans_mean_direction_hand_example, P.test_kmeans_is_invariant_to_positive_row_scales]),
+    "k-means: ties to the higher cluster": ("kmeans_assign", kmeans_ties_high,
+        [P.test_kmeans_ties_go_to_the_lower_cluster_and_empty_clusters_keep_their_centroid]),
+    "k-means: empty cluster reset to zero": ("kmeans_update", kmeans_empty_to_zero,
+        [P.test_kmeans_ties_go_to_the_lower_cluster_and_empty_clusters_keep_their_centroid]),
+    "k-means: least similar centroid": ("kmeans_assign", kmeans_argmin,
+        [P.test_kmeans_assignment_is_euclidean_argmin_on_the_sphere, P.test_kmeans_planted_directions_are_recovered]),
+    "k-means: bf16 rounding truncates": ("round_bf16", round_bf16_truncates,
+        [P.test_round_bf16_matches_torch_conversion]),
 }
 
 

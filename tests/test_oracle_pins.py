@@ -421,3 +421,111 @@ def test_pa_fr_budget_hand_values():
     g = GOLD["pa_fr"]
     assert [O.pa_fr_budget(t, 32) for t in range(10)] == g["k_max_32"]
     assert [O.pa_fr_budget(t, 32768) for t in range(10)] == g["k_max_32768"]
+
+
+# ---------------------------------------------------------------- spherical k-means (Sec. 4.2, "Vocabulary partition")
+def test_round_bf16_matches_torch_conversion():
+    rng = np.random.default_rng(7)
+    v = np.concatenate([rng.standard_normal(4096) * 10.0 ** rng.integers(-30, 30, 4096),
+                        [1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -8), 0.0, -0.0, 3.0e38]])
+    ref = torch.tensor(v, dtype=torch.float32).to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(O.round_bf16(v), ref)
+
+
+def test_kmeans_mean_direction_hand_example():
+    # unit points at 0 and 90 degrees, and a long vector at 0 degrees: the
+    # points are normalised first, so the resultant is (2, 1), not (6, 1)
+    W = np.array([[1.0, 0.0], [0.0, 1.0], [5.0, 0.0]], dtype=np.float32)
+    mu = O.kmeans_update(W, [0, 0, 0], 1, np.zeros((1, 2)))
+    np.testing.assert_allclose(mu[0], np.array([2.0, 1.0]) / math.sqrt(5.0), rtol=0, atol=1e-15)
+
+
+def test_kmeans_planted_directions_are_recovered():
+    # points are positive multiples of four orthogonal directions (plus a
+    # small orthogonal wobble); one point of each group seeds the centroids
+    rng = np.random.default_rng(3)
+    M, d, per = 4, 8, 25
+    E = np.eye(d)[:M]
+    rows, truth = [], []
+    for m in range(M):
+        for _ in range(per):
+            wob = np.zeros(d)
+            wob[M:] = rng.standard_normal(d - M) * 0.05
+            rows.append(E[m] * rng.uniform(0.5, 4.0) + wob)
+            truth.append(m)
+    W = np.array(rows, dtype=np.float32)
+    truth = np.array(truth)
+    init = [m * per for m in range(M)]
+    assign, mu = O.spherical_kmeans(W, M, init, iters=3)
+    np.testing.assert_array_equal(assign, truth)
+    for m in range(M):
+        assert mu[m, m] > 0.99 and abs(np.linalg.norm(mu[m]) - 1.0) < 1e-12
+
+
+def test_kmeans_assignment_is_euclidean_argmin_on_the_sphere():
+    # with unit centroids, max cosine = min euclidean distance between unit
+    # vectors; centroids are rows of a normalised Hadamard matrix (exact in bf16)
+    from sklearn.metrics import pairwise_distances_argmin
+    H = 0.5 * np.array([[1, 1, 1, 1], [1, -1, 1, -1], [1, 1, -1, -1], [1, -1, -1, 1]], dtype=np.float64)
+    C = np.vstack([H, -H])
+    rng = np.random.default_rng(5)
+    W = rng.standard_normal((500, 4)).astype(np.float32)
+    assign, _ = O.kmeans_assign(W, C)
+    X = W.astype(np.float64) / np.linalg.norm(W.astype(np.float64), axis=1, keepdims=True)
+    np.testing.assert_array_equal(assign, pairwise_distances_argmin(X, C))
+
+
+def test_kmeans_ties_go_to_the_lower_cluster_and_empty_clusters_keep_their_centroid():
+    W = np.array([[1.0, 0.0], [1.0, 0.1], [0.0, 1.0]], dtype=np.float32)
+    C = np.array([[1.0, 0.0], [1.0, 0.0], [0.0, 1.0]])  # clusters 0 and 1 coincide
+    assign, _ = O.kmeans_assign(W, C)
+    assert assign.tolist() == [0, 0, 2]
+    mu = O.kmeans_update(W, assign, 3, C)
+    np.testing.assert_array_equal(mu[1], C[1])  # empty: unchanged
+    assert mu[0, 1] > 0  # moved toward the second point
+
+
+def test_kmeans_is_invariant_to_positive_row_scales():
+    rng = np.random.default_rng(11)
+    W = rng.standard_normal((300, 16)).astype(np.float32)
+    scale = rng.uniform(0.1, 10.0, size=(300, 1)).astype(np.float32)
+    init = rng.choice(300, size=6, replace=False)
+    a1, mu1 = O.spherical_kmeans(W, 6, init, iters=4)
+    a2, mu2 = O.spherical_kmeans(W * scale, 6, init, iters=4)
+    np.testing.assert_array_equal(a1, a2)
+    np.testing.assert_allclose(mu1, mu2, rtol=0, atol=1e-6)
+
+
+def test_kmeans_steps_each_maximise_the_objective_and_end_at_a_fixed_point():
+    # the assignment maximises the summed similarity to the (bf16) centroids
+    # given them, the update maximises it over unit centroids given the
+    # assignment; brute force over all centroids confirms every final choice
+    rng = np.random.default_rng(2)
+    W = rng.standard_normal((60, 5)).astype(np.float32)
+    M = 4
+    init = rng.choice(60, size=M, replace=False)
+    X = O.unit_rows(W)
+    mu = X[init]
+    a = np.zeros(60, dtype=np.int64)
+    for it in range(30):
+        Cb = O.round_bf16(mu)
+        a_new, _ = O.kmeans_assign(W, mu)
+        if it:
+            assert O.kmeans_objective(W, a_new, Cb) >= O.kmeans_objective(W, a, Cb) - 1e-12
+        a = a_new
+        mu_new = O.kmeans_update(W, a, M, mu)
+        assert O.kmeans_objective(W, a, mu_new) >= O.kmeans_objective(W, a, mu) - 1e-12
+        # no other unit vector does better for one cluster (random probes)
+        for m in range(M):
+            mem = X[a == m]
+            if len(mem):
+                best = float(mem.sum(0) @ mu_new[m])
+                probes = rng.standard_normal((50, 5))
+                probes /= np.linalg.norm(probes, axis=1, keepdims=True)
+                assert np.all(mem.sum(0) @ probes.T <= best + 1e-12)
+        mu = mu_new
+    a, _ = O.kmeans_assign(W, mu)
+    Cb = O.round_bf16(mu)
+    for v in range(60):
+        sims = [float(np.dot(X[v], Cb[m])) for m in range(M)]
+        assert a[v] == min(m for m in range(M) if sims[m] == max(sims))
