@@ -265,6 +265,50 @@ dyna_status dyna_beam_expand(const float* logprobs, const int32_t* ids, const fl
                              int32_t* out_parent, int32_t* out_ids, hipStream_t stream);
 
 /* ------------------------------------------------------------------ */
+/* Building the partition: spherical k-means (Sec. 4.2, "Vocabulary   */
+/* partition": clusters from spherical k-means on the column-          */
+/* normalised LM head, one point per vocabulary entry).                */
+/* ------------------------------------------------------------------ */
+
+/* Shared argument meaning:
+ *  W [V, d]    device, bf16 (DYNA_BF16 only), row-major, 16-byte aligned;
+ *              row v is the paper's column v.  The points are W[v] / ||W[v]||
+ *              (an all-zero row is a point with no direction).
+ *  centroids   device fp32 [M, d], unit rows.
+ * Similarities are taken with the centroids rounded to bf16 (the matrix
+ * cores' operand type) and accumulated in fp32.  d % 8 == 0, d <= 8192,
+ * 1 <= M <= min(V, DYNA_MAX_M).  ws: dyna_kmeans_workspace_bytes(V, d, M)
+ * bytes of device memory, caller-owned. */
+size_t dyna_kmeans_workspace_bytes(int32_t V, int32_t d, int32_t M);
+
+/* Assignment step: out_assign[v] = argmax_m x_v . mu_m (ties to the lower
+ * m); out_score[v] (optional, may be NULL) = W[v] . bf16(mu_m) for that m, the
+ * raw row's product (the unit point's is this times 1 / ||W[v]||).
+ * Asynchronous on `stream`.  This is the launch DYNA_OPT_KERNEL_TIMING
+ * brackets for the builder. */
+dyna_status dyna_kmeans_assign(const void* W, int32_t wdtype, int32_t V, int32_t d, const float* centroids,
+                               int32_t M, int32_t* out_assign, float* out_score, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/* Update step, in place: centroids[m] = (sum of the unit points with
+ * assign[v] == m, in ascending v) / its norm, summed in fp32; a cluster
+ * with no points or a zero sum keeps its row.  Assignments outside [0, M)
+ * are skipped.  Asynchronous on `stream`. */
+dyna_status dyna_kmeans_update(const void* W, int32_t wdtype, int32_t V, int32_t d, const int32_t* assign,
+                               int32_t M, float* centroids, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The whole builder: centroids start at the points init_ids[0..M) (device,
+ * distinct ids in [0, V), drawn by the caller), then `iters` (>= 1) rounds
+ * of assignment followed by update.  out_cluster_of [V] (device) receives
+ * the last assignment, the partition that dyna_build_layout takes;
+ * out_centroids (device fp32 [M, d], optional) the centroids after the last
+ * update.  Synchronises `stream`; an init id outside [0, V) returns
+ * DYNA_ERR_DEVICE_DATA (its centroid is zero). */
+dyna_status dyna_kmeans(const void* W, int32_t wdtype, int32_t V, int32_t d, int32_t M, const int32_t* init_ids,
+                        int32_t iters, int32_t* out_cluster_of, float* out_centroids, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
+
+/* ------------------------------------------------------------------ */
 /* Position-aware budgets (host functions, no GPU work).               */
 /* ------------------------------------------------------------------ */
 
@@ -295,7 +339,7 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   staged in LDS (bf16 weights, up to 128 contexts; else 3), 3 MFMA tiles
  *   loaded straight from HBM.
  * DYNA_OPT_KERNEL_TIMING: 1 brackets every launch of the gathered-head
- *   (logits) kernel with two (default) events recorded on the stream it runs
+ *   (logits) kernel, and the k-means assignment, with two (default) events recorded on the stream it runs
  *   on; 2 hands the two events to the dispatch itself (hipExtLaunchKernelGGL);
  *   0 stops.
  * DYNA_OPT_GEMV_ROWS: rows each wave of the GEMV kernel keeps in flight:
@@ -315,10 +359,13 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  * DYNA_OPT_UNION_CFG: shape of the dense union-row kernel of
  *   DYNA_SEL_UNION steps: 0 automatic, 1..14 fixed (waves per workgroup,
  *   row tiles per wave, k columns per stage, ring depth); a shape whose ring does not
- *   fit in LDS for the batch's context count returns DYNA_ERR_UNSUPPORTED. */
+ *   fit in LDS for the batch's context count returns DYNA_ERR_UNSUPPORTED.
+ * DYNA_OPT_KMEANS_CFG: shape of the k-means assignment kernel: 0
+ *   automatic, 1..4 fixed. */
 enum { DYNA_OPT_LOGITS_PATH = 1, DYNA_OPT_ROUTER_PATH = 2, DYNA_OPT_KERNEL_TIMING = 3,
        DYNA_OPT_GEMV_ROWS = 4, DYNA_OPT_FUSED_B1 = 5, DYNA_OPT_MFMA_UNROLL = 6,
-       DYNA_OPT_GATHER_CFG = 7, DYNA_OPT_GREEDY_GRID = 8, DYNA_OPT_UNION_CFG = 9 };
+       DYNA_OPT_GATHER_CFG = 7, DYNA_OPT_GREEDY_GRID = 8, DYNA_OPT_UNION_CFG = 9,
+       DYNA_OPT_KMEANS_CFG = 10 };
 dyna_status dyna_set_option(int32_t option, int32_t value);
 
 /* Waits for the events recorded under DYNA_OPT_KERNEL_TIMING and returns the

@@ -27,6 +27,7 @@ std::atomic<int> g_mfma_unroll{0};
 std::atomic<int> g_gather_cfg{0};
 std::atomic<int> g_greedy_grid{0};
 std::atomic<int> g_union_cfg{0};
+std::atomic<int> g_kmeans_cfg{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -111,6 +112,7 @@ int option_mfma_unroll() { return g_mfma_unroll.load(); }
 int option_gather_cfg() { return g_gather_cfg.load(); }
 int option_greedy_grid() { return g_greedy_grid.load(); }
 int option_union_cfg() { return g_union_cfg.load(); }
+int option_kmeans_cfg() { return g_kmeans_cfg.load(); }
 
 // ------------------------------------------------------------------ workspace
 // One carving serves every hot entry point, so a single workspace can back a
@@ -380,6 +382,11 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
     if (option == DYNA_OPT_GREEDY_GRID) {
         REQUIRE(value >= 0 && value <= kGreedyMaxBlocks, "greedy grid %d outside [0, %d]", value, kGreedyMaxBlocks);
         g_greedy_grid.store(value);
+        return DYNA_OK;
+    }
+    if (option == DYNA_OPT_KMEANS_CFG) {
+        REQUIRE(value >= 0 && value <= 4, "k-means shape %d outside [0, 4]", value);
+        g_kmeans_cfg.store(value);
         return DYNA_OK;
     }
     if (option == DYNA_OPT_UNION_CFG) {
@@ -690,6 +697,50 @@ DYNA_API int32_t dyna_cluster_budget(int32_t t, int32_t k0, int32_t k1, int32_t 
 DYNA_API int32_t dyna_static_budget(int32_t t, int32_t k_max) {
     if (t < 0 || k_max < 1) return -1;
     return t < 2 ? k_max : (int32_t)((int64_t)k_max / ((int64_t)t + 1));
+}
+
+// ------------------------------------------------------------------ partition builder
+static dyna_status check_kmeans(int32_t wdtype, int32_t V, int32_t d, int32_t M) {
+    if (wdtype != DYNA_BF16) return set_error(DYNA_ERR_UNSUPPORTED, "k-means: bf16 rows only");
+    REQUIRE(V >= 1 && d >= 8 && d % 8 == 0, "bad sizes V=%d d=%d", V, d);
+    if (d > 8192) return set_error(DYNA_ERR_UNSUPPORTED, "k-means: d=%d > 8192", d);
+    REQUIRE(M >= 1 && M <= DYNA_MAX_M && M <= V, "M=%d outside [1, min(V, %d)]", M, DYNA_MAX_M);
+    return DYNA_OK;
+}
+
+DYNA_API size_t dyna_kmeans_workspace_bytes(int32_t V, int32_t d, int32_t M) {
+    if (V < 1 || d < 8 || M < 1) return 0;
+    return kmeans_ws_bytes(V, d, M);
+}
+
+DYNA_API dyna_status dyna_kmeans_assign(const void* W, int32_t wdtype, int32_t V, int32_t d, const float* centroids,
+                                        int32_t M, int32_t* out_assign, float* out_score, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+    TRY(check_kmeans(wdtype, V, d, M));
+    REQUIRE(W && aligned16(W) && centroids && out_assign && ws, "NULL argument or W misaligned");
+    if (ws_bytes < kmeans_ws_bytes(V, d, M))
+        return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, kmeans_ws_bytes(V, d, M));
+    return timed([&] { return kmeans_assign(W, V, d, centroids, M, out_assign, out_score, ws, stream); }, stream);
+}
+
+DYNA_API dyna_status dyna_kmeans_update(const void* W, int32_t wdtype, int32_t V, int32_t d, const int32_t* assign,
+                                        int32_t M, float* centroids, void* ws, size_t ws_bytes, hipStream_t stream) {
+    TRY(check_kmeans(wdtype, V, d, M));
+    REQUIRE(W && aligned16(W) && assign && centroids && ws, "NULL argument or W misaligned");
+    if (ws_bytes < kmeans_ws_bytes(V, d, M))
+        return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, kmeans_ws_bytes(V, d, M));
+    return kmeans_update(W, V, d, assign, M, centroids, ws, stream);
+}
+
+DYNA_API dyna_status dyna_kmeans(const void* W, int32_t wdtype, int32_t V, int32_t d, int32_t M,
+                                 const int32_t* init_ids, int32_t iters, int32_t* out_cluster_of,
+                                 float* out_centroids, void* ws, size_t ws_bytes, hipStream_t stream) {
+    TRY(check_kmeans(wdtype, V, d, M));
+    REQUIRE(iters >= 1, "iters=%d < 1", iters);
+    REQUIRE(W && aligned16(W) && init_ids && out_cluster_of && ws, "NULL argument or W misaligned");
+    if (ws_bytes < kmeans_ws_bytes(V, d, M))
+        return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, kmeans_ws_bytes(V, d, M));
+    return kmeans_run(W, V, d, M, init_ids, iters, out_cluster_of, out_centroids, ws, stream);
 }
 
 // ------------------------------------------------------------------ baselines

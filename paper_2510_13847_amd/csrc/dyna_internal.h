@@ -135,6 +135,23 @@ dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream);
 // union rows (every plan chunk lists contexts 0..B-1 in order): dense
 // LDS-staged MFMA product; vid_out gets one shared row [slots]
 dyna_status launch_union_gemm(const RowdotArgs& a, hipStream_t stream);
+// The same product with an argmax epilogue: every plan row against the B
+// contexts (centroids); vid_out[slot] = the best context (ties to the lower
+// id), out[slot] = its product (out may be null).
+dyna_status launch_union_argmax(const RowdotArgs& a, int cfg, hipStream_t stream);
+// kmeans.hip: spherical k-means over the LM-head rows
+size_t kmeans_ws_bytes(int32_t V, int32_t d, int32_t M);
+dyna_status kmeans_assign(const void* W, int32_t V, int32_t d, const float* centroids, int32_t M,
+                          int32_t* out_assign, float* out_score, void* ws, hipStream_t stream);
+dyna_status kmeans_update(const void* W, int32_t V, int32_t d, const int32_t* assign, int32_t M,
+                          float* centroids, void* ws, hipStream_t stream);
+dyna_status kmeans_run(const void* W, int32_t V, int32_t d, int32_t M, const int32_t* init_ids, int32_t iters,
+                       int32_t* out_cluster_of, float* out_centroids, void* ws, hipStream_t stream);
+int option_kmeans_cfg();
+// layout.hip: stable counting sort of ids in [0, M) (others skipped): perm and
+// CSR offsets; ws holds layout_ws_bytes(V, M)
+dyna_status launch_cluster_csr(const int32_t* cluster_of, int32_t V, int32_t M, int32_t* perm,
+                               int32_t* offsets, void* ws, hipStream_t stream);
 
 // Arguments of the per-context top-k (Sec. 4.2) and of the draft selection
 // (Algorithm 1), shared by the separate and the fused launches.

@@ -383,7 +383,28 @@ struct UnionShape {
     static constexpr bool ok = S >= 3 && S * STAGE <= kUnionLds && NBI >= NW && NBI % NW == 0;
 };
 
-template <int NW, int T, int KB, int NT, int SREQ>
+// Max of a 64-bit key over the 16 lanes of each DPP row (lanes 16r .. 16r + 15):
+// a prefix max by row shifts, so lane 15 of the row ends with it.
+__device__ __forceinline__ uint64_t row16_max_u64(uint64_t x) {
+    auto step = [&](auto ctrl_tag) {
+        constexpr int CTRL = decltype(ctrl_tag)::value;
+        const uint32_t lo = dpp<CTRL, 0xf>(0u, (uint32_t)x);
+        const uint32_t hi = dpp<CTRL, 0xf>(0u, (uint32_t)(x >> 32));
+        const uint64_t y = ((uint64_t)hi << 32) | lo;
+        x = y > x ? y : x;
+    };
+    step(std::integral_constant<int, kRowShr1>{});
+    step(std::integral_constant<int, kRowShr2>{});
+    step(std::integral_constant<int, kRowShr4>{});
+    step(std::integral_constant<int, kRowShr8>{});
+    return x;
+}
+
+// EPI 0: store every (context, slot) product to out (and the slots' ids to
+// vid_out).  EPI 1: the contexts are centroids; keep, per row, the best
+// (product, lower context id) over all contexts and write its context id to
+// vid_out[slot] and its product to out[slot] (if out is set).
+template <int NW, int T, int KB, int NT, int SREQ, int EPI>
 __global__ __launch_bounds__(NW * kWave) void union_gemm_kernel(RowdotArgs a) {
     using Sh = UnionShape<NW, T, KB, NT, SREQ>;
     constexpr int S = Sh::S;
@@ -452,8 +473,13 @@ __global__ __launch_bounds__(NW * kWave) void union_gemm_kernel(RowdotArgs a) {
 
     // vocabulary ids of the consumed chunks' rows (lane j < 16 of vp holds row j's)
     int32_t vid[T][4];
+    uint64_t run[T][4];  // EPI 1: best key per row so far (lane 15 of each DPP row)
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) run[t][r] = 0;
     auto load_vids = [&]() {
-        if (a.vid_out == nullptr) return;
+        if (EPI != 0 || a.vid_out == nullptr) return;
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             if (cu.nrows[t] == 0) continue;
@@ -518,7 +544,42 @@ __global__ __launch_bounds__(NW * kWave) void union_gemm_kernel(RowdotArgs a) {
                         __builtin_bit_cast(bf16x8, av[t]), __builtin_bit_cast(bf16x8, bv), acc[t][j], 0, 0, 0);
             }
         }
-        if (cu.kb == nkb - 1) {
+        if (EPI == 1 && cu.kb == nkb - 1) {
+            // best (product, lower centroid id) of each row over this group,
+            // folded into the row's running best; written after the last group
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    uint64_t kb_best = 0;
+#pragma unroll
+                    for (int j = 0; j < NT; ++j) {
+                        const int b = cu.g * NCOL + 16 * j + col;
+                        const float x = acc[t][j][r];
+                        const uint64_t key = sel_key(x != x ? -__builtin_inff() : x, (uint32_t)b);
+                        if (b < B && key > kb_best) kb_best = key;
+                    }
+                    kb_best = row16_max_u64(kb_best);
+                    run[t][r] = kb_best > run[t][r] ? kb_best : run[t][r];
+                }
+                if (cu.g == ng - 1) {
+                    if (col == 15 && cu.nrows[t] > 0) {
+                        const int64_t base = (int64_t)cu.sb[t] + cu.r0[t];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int row = 4 * kq + r;
+                            if (row < cu.nrows[t]) {
+                                a.vid_out[base + row] = run[t][r] != 0 ? (int32_t)key_id(run[t][r]) : 0;
+                                if (a.out != nullptr) a.out[base + row] = key_val(run[t][r]);
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) run[t][r] = 0;
+                }
+            }
+        }
+        if (EPI == 0 && cu.kb == nkb - 1) {
             // D rows 4 * kq + r, context column 16 * j + col
 #pragma unroll
             for (int t = 0; t < T; ++t) {
@@ -542,6 +603,8 @@ __global__ __launch_bounds__(NW * kWave) void union_gemm_kernel(RowdotArgs a) {
                         if (4 * kq + r < cu.nrows[t]) a.vid_out[base + 4 * kq + r] = vid[t][r];
                 }
             }
+        }
+        if (cu.kb == nkb - 1) {
 #pragma unroll
             for (int t = 0; t < T; ++t)
 #pragma unroll
@@ -554,7 +617,7 @@ __global__ __launch_bounds__(NW * kWave) void union_gemm_kernel(RowdotArgs a) {
     }
 }
 
-template <int NW, int T, int KB, int NT, int SREQ = 0>
+template <int NW, int T, int KB, int NT, int SREQ = 0, int EPI = 0>
 dyna_status launch_union_cfg(const RowdotArgs& a, hipStream_t stream) {
     using Sh = UnionShape<NW, T, KB, NT, SREQ>;
     if constexpr (!Sh::ok) {
@@ -566,7 +629,7 @@ dyna_status launch_union_cfg(const RowdotArgs& a, hipStream_t stream) {
         int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "union: device");
         if (!(allowed.load() & (1ull << dev))) {
-            if (hipFuncSetAttribute((const void*)union_gemm_kernel<NW, T, KB, NT, SREQ>,
+            if (hipFuncSetAttribute((const void*)union_gemm_kernel<NW, T, KB, NT, SREQ, EPI>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, LDS) != hipSuccess)
                 return set_error(DYNA_ERR_HIP, "union: LDS attribute");
             allowed.fetch_or(1ull << dev);
@@ -574,7 +637,7 @@ dyna_status launch_union_cfg(const RowdotArgs& a, hipStream_t stream) {
         const int per_cu = std::max(1, kUnionLds / LDS);
         const int64_t tiles = ((int64_t)a.max_chunks_bound + NW * T - 1) / (NW * T);
         const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(tiles, 256 * per_cu));
-        launch_timed_kernel(union_gemm_kernel<NW, T, KB, NT, SREQ>, dim3((unsigned)blocks), dim3(NW * kWave), LDS,
+        launch_timed_kernel(union_gemm_kernel<NW, T, KB, NT, SREQ, EPI>, dim3((unsigned)blocks), dim3(NW * kWave), LDS,
                             stream, a);
         return check_launch("union_gemm_kernel");
     }
@@ -633,6 +696,19 @@ dyna_status launch_union_gemm(const RowdotArgs& a, hipStream_t stream) {
     if (a.B <= 32) return launch_union_nt<2>(a, cfg, stream);
     if (a.B <= 64) return launch_union_nt<4>(a, cfg, stream);
     return launch_union_nt<8>(a, cfg, stream);
+}
+
+dyna_status launch_union_argmax(const RowdotArgs& a, int cfg, hipStream_t stream) {
+    if (a.plan.hdr == nullptr || a.wdtype != DYNA_BF16 || a.vdtype != DYNA_BF16 || a.K % 8 != 0 ||
+        a.vid_out == nullptr || a.B < 1)
+        return set_error(DYNA_ERR_UNSUPPORTED, "nearest centroid: needs bf16 rows and centroids");
+    switch (cfg) {
+        case 1: return launch_union_cfg<8, 1, 64, 8, 3, 1>(a, stream);
+        case 2: return launch_union_cfg<4, 1, 128, 8, 3, 1>(a, stream);
+        case 3: return launch_union_cfg<8, 1, 64, 16, 3, 1>(a, stream);
+        case 4: return launch_union_cfg<4, 2, 64, 16, 3, 1>(a, stream);
+        default: return launch_union_cfg<8, 2, 64, 8, 0, 1>(a, stream);
+    }
 }
 
 }  // namespace dyna

@@ -119,6 +119,25 @@ size_t layout_ws_bytes(int32_t V, int32_t M) {
            256;
 }
 
+dyna_status launch_cluster_csr(const int32_t* cluster_of, int32_t V, int32_t M, int32_t* perm,
+                               int32_t* offsets, void* ws, hipStream_t stream) {
+    const int32_t nchunks = (V + kChunk - 1) / kChunk;
+    char* p = static_cast<char*>(ws);
+    int32_t* rank = reinterpret_cast<int32_t*>(p);
+    p += align256(sizeof(int32_t) * (size_t)V);
+    int32_t* cnt = reinterpret_cast<int32_t*>(p);
+    p += align256(sizeof(int32_t) * (size_t)nchunks * M);
+    int32_t* bad = reinterpret_cast<int32_t*>(p);
+    fill_i32_kernel<<<1, 64, 0, stream>>>(bad, 1, 0);
+    const size_t lds = sizeof(int32_t) * ((size_t)M + kThreads);
+    layout_count_kernel<<<nchunks, kThreads, lds, stream>>>(cluster_of, V, M, rank, cnt, bad);
+    if (dyna_status s = check_launch("layout_count_kernel"); s != DYNA_OK) return s;
+    layout_scan_kernel<<<1, kScanThreads, 0, stream>>>(M, nchunks, cnt, offsets);
+    if (dyna_status s = check_launch("layout_scan_kernel"); s != DYNA_OK) return s;
+    layout_scatter_kernel<<<(V + 255) / 256, 256, 0, stream>>>(cluster_of, V, M, rank, cnt, perm);
+    return check_launch("layout_scatter_kernel");
+}
+
 dyna_status launch_build_layout(const int32_t* cluster_of, int32_t V, int32_t M, const void* W_lm,
                                 int32_t wdtype, int32_t d, void* W_perm, int32_t* perm,
                                 int32_t* offsets, void* ws, size_t ws_bytes,

@@ -21,7 +21,7 @@ F32, BF16 = 0, 1
 ACT = {"none": 0, "relu": 1, "silu": 2}
 SEL_ARGMAX, SEL_TOPK, SEL_SAMPLE, SEL_UNION = 1, 2, 4, 8
 OPT_LOGITS_PATH, OPT_ROUTER_PATH, OPT_KERNEL_TIMING, OPT_GEMV_ROWS, OPT_FUSED_B1, OPT_MFMA_UNROLL = 1, 2, 3, 4, 5, 6
-OPT_GATHER_CFG, OPT_GREEDY_GRID, OPT_UNION_CFG = 7, 8, 9
+OPT_GATHER_CFG, OPT_GREEDY_GRID, OPT_UNION_CFG, OPT_KMEANS_CFG = 7, 8, 9, 10
 MAX_KT = 64
 
 
@@ -71,6 +71,10 @@ _SIGNATURES = {
     "dyna_dense_workspace_bytes": (_Z, [_I, _I]),
     "dyna_cluster_budget": (_I, [_I, _I, _I, _I, _I]),
     "dyna_beam_expand": (_I, [_P, _P, _P, _I, _I, _I, _P, _P, _P, _P]),
+    "dyna_kmeans_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I]),
+    "dyna_kmeans_assign": (_I, [_P, _I, _I, _I, _P, _I, _P, _P, _P, ctypes.c_size_t, _P]),
+    "dyna_kmeans_update": (_I, [_P, _I, _I, _I, _P, _I, _P, _P, ctypes.c_size_t, _P]),
+    "dyna_kmeans": (_I, [_P, _I, _I, _I, _I, _P, _I, _P, _P, _P, ctypes.c_size_t, _P]),
     "dyna_static_budget": (_I, [_I, _I]),
     "dyna_dense_head": (_I, [_P, _I, _I, _I, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P,
                              _Z, _P]),
@@ -409,3 +413,46 @@ def beam_expand(logprobs, ids, last_scores=None, n_out=None, stream=None):
     _check(lib().dyna_beam_expand(_ptr(logprobs), _ptr(ids), _ptr(last_scores), B, k_t, n_out, _ptr(sc),
                                   _ptr(par), _ptr(tok), _stream(stream)))
     return sc, par, tok
+
+
+# ---------------------------------------------------------------- partition builder
+def kmeans_workspace(W, M: int):
+    import torch
+    V, d = W.shape
+    n = int(lib().dyna_kmeans_workspace_bytes(V, d, M))
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=W.device)
+
+
+def kmeans_assign(W, centroids, ws=None, stream=None, want_score=False):
+    """dyna_kmeans_assign -> (assign[V] int32, score[V] float32 or None)."""
+    import torch
+    V, d = W.shape
+    M = centroids.shape[0]
+    ws = kmeans_workspace(W, M) if ws is None else ws
+    a = torch.empty(V, dtype=torch.int32, device=W.device)
+    sc = torch.empty(V, dtype=torch.float32, device=W.device) if want_score else None
+    _check(lib().dyna_kmeans_assign(_ptr(W), _dtype_code(W), V, d, _ptr(centroids), M, _ptr(a), _ptr(sc),
+                                    _ptr(ws), ws.numel(), _stream(stream)))
+    return a, sc
+
+
+def kmeans_update(W, assign, centroids, ws=None, stream=None):
+    """dyna_kmeans_update, in place on centroids (fp32 [M, d])."""
+    V, d = W.shape
+    M = centroids.shape[0]
+    ws = kmeans_workspace(W, M) if ws is None else ws
+    _check(lib().dyna_kmeans_update(_ptr(W), _dtype_code(W), V, d, _ptr(assign), M, _ptr(centroids), _ptr(ws),
+                                    ws.numel(), _stream(stream)))
+    return centroids
+
+
+def kmeans(W, M: int, init_ids, iters: int, ws=None, stream=None, keep_centroids=True):
+    """dyna_kmeans -> (cluster_of[V] int32, centroids[M, d] float32 or None)."""
+    import torch
+    V, d = W.shape
+    ws = kmeans_workspace(W, M) if ws is None else ws
+    cl = torch.empty(V, dtype=torch.int32, device=W.device)
+    mu = torch.empty((M, d), dtype=torch.float32, device=W.device) if keep_centroids else None
+    _check(lib().dyna_kmeans(_ptr(W), _dtype_code(W), V, d, M, _ptr(init_ids), iters, _ptr(cl), _ptr(mu),
+                             _ptr(ws), ws.numel(), _stream(stream)))
+    return cl, mu

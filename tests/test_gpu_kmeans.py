@@ -1,0 +1,185 @@
+"""GPU parity of the partition builder (spherical k-means on the unit LM-head
+rows, Sec. 4.2 "Vocabulary partition") against the CPU oracle.
+
+The assignment is an argmax decided in the kernel's operand precision (bf16
+centroids, fp32 sums); the oracle takes the same decision with bf16 centroids
+and float64 sums, so an assignment may differ only where the oracle's two best
+similarities lie within 1e-5 (relative) of each other.  Centroids are fp32
+sums of unit rows; they match the oracle's float64 sums within 2e-5.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import dynaspec_oracle as O
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+D = None
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    global D
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2510_13847_amd import dynahead
+    D = dynahead
+    D.lib()
+    yield
+    D.set_option(D.OPT_KMEANS_CFG, 0)
+
+
+def _rand_head(V, d, seed):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn(V, d, generator=g) / d ** 0.5).to(torch.bfloat16)
+
+
+def _unit(rng, M, d):
+    c = rng.standard_normal((M, d))
+    return (c / np.linalg.norm(c, axis=1, keepdims=True)).astype(np.float32)
+
+
+def _check_assign(got, S, what):
+    """got[v] equals the oracle's argmax, or ties with it within 1e-5 relative."""
+    ref = np.argmax(S, axis=1)
+    bad = np.nonzero(got != ref)[0]
+    for v in bad:
+        a, b = S[v, got[v]], S[v, ref[v]]
+        assert abs(a - b) <= 1e-5 * max(abs(a), abs(b)) + 1e-7, f"{what}: row {v} -> {got[v]}, oracle {ref[v]}"
+    return len(bad)
+
+
+SHAPES = [  # V (ragged vs 16-row tiles), d (ragged vs k blocks), M (one group, several groups)
+    (1000, 64, 7), (3001, 200, 37), (2500, 520, 130), (4099, 128, 300), (2048, 1024, 513),
+]
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("V,d,M", SHAPES)
+def test_assign_step(V, d, M, cfg):
+    rng = np.random.default_rng(V + M)
+    Wl = _rand_head(V, d, V)
+    C = _unit(rng, M, d)
+    D.set_option(D.OPT_KMEANS_CFG, cfg)
+    try:
+        a, sc = D.kmeans_assign(Wl.to(DEV), torch.from_numpy(C).to(DEV), want_score=True)
+        torch.cuda.synchronize()
+    finally:
+        D.set_option(D.OPT_KMEANS_CFG, 0)
+    got = a.cpu().numpy().astype(np.int64)
+    ref, S = O.kmeans_assign(W.host_array(Wl), C)
+    n_tie = _check_assign(got, S, "assign")
+    assert n_tie <= max(1, V // 500)
+    # the reported product is the raw row's: S[v, m] * ||W[v]||
+    norms = np.linalg.norm(O.as_f64(W.host_array(Wl)), axis=1)
+    want = S[np.arange(V), got] * norms
+    np.testing.assert_allclose(sc.cpu().numpy(), want, rtol=1e-4, atol=1e-5)
+
+
+def test_assign_ties_and_zero_rows():
+    # duplicate centroids tie exactly: the lower id wins; a zero row scores 0
+    # against every centroid and goes to cluster 0
+    rng = np.random.default_rng(1)
+    V, d, M = 300, 64, 6
+    Wl = _rand_head(V, d, 9)
+    Wl[17] = 0
+    C = _unit(rng, M, d)
+    C[4] = C[1]
+    a, _ = D.kmeans_assign(Wl.to(DEV), torch.from_numpy(C).to(DEV))
+    got = a.cpu().numpy()
+    assert got[17] == 0
+    assert not np.any(got == 4)
+    ref, S = O.kmeans_assign(W.host_array(Wl), C)
+    _check_assign(got.astype(np.int64), S, "ties")
+
+
+@pytest.mark.parametrize("V,d,M", [(1000, 64, 7), (3001, 200, 37), (2048, 1024, 513), (2000, 8192, 5)])
+def test_update_step(V, d, M):
+    rng = np.random.default_rng(V * 7 + d)
+    Wl = _rand_head(V, d, V + 1)
+    assign = rng.integers(0, max(1, M - 2), size=V).astype(np.int32)  # the last clusters stay empty
+    C = _unit(rng, M, d)
+    mu = torch.from_numpy(C.copy()).to(DEV)
+    D.kmeans_update(Wl.to(DEV), torch.from_numpy(assign).to(DEV), mu)
+    torch.cuda.synchronize()
+    ref = O.kmeans_update(W.host_array(Wl), assign, M, C.astype(np.float64))
+    got = mu.cpu().numpy().astype(np.float64)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=2e-5)
+    np.testing.assert_array_equal(got[M - 2:], C[M - 2:])  # empty clusters: bit-for-bit unchanged
+
+
+def test_update_skips_out_of_range_ids():
+    rng = np.random.default_rng(4)
+    V, d, M = 500, 64, 5
+    Wl = _rand_head(V, d, 3)
+    assign = rng.integers(0, M, size=V).astype(np.int32)
+    assign[::7] = M + 3
+    assign[1::11] = -1
+    C = _unit(rng, M, d)
+    mu = torch.from_numpy(C.copy()).to(DEV)
+    D.kmeans_update(Wl.to(DEV), torch.from_numpy(assign).to(DEV), mu)
+    torch.cuda.synchronize()
+    keep = (assign >= 0) & (assign < M)
+    ref = O.kmeans_update(W.host_array(Wl)[keep], assign[keep], M, C.astype(np.float64))
+    np.testing.assert_allclose(mu.cpu().numpy(), ref, rtol=0, atol=2e-5)
+
+
+def test_planted_partition_is_recovered():
+    V, d, M = 4000, 128, 24
+    Wl, groups = W.planted_head(V, d, M, seed=5, noise=0.2)
+    init = np.array([np.nonzero(groups == m)[0][0] for m in range(M)], dtype=np.int32)
+    cl, mu = D.kmeans(Wl.to(DEV), M, torch.from_numpy(init).to(DEV), iters=4)
+    torch.cuda.synchronize()
+    got = cl.cpu().numpy().astype(np.int64)
+    np.testing.assert_array_equal(got, groups)
+    ref_a, ref_mu = O.spherical_kmeans(W.host_array(Wl), M, init, iters=4)
+    np.testing.assert_array_equal(got, ref_a)
+    np.testing.assert_allclose(mu.cpu().numpy(), ref_mu, rtol=0, atol=2e-5)
+    # the partition feeds the layout directly
+    L = D.build_layout(cl, Wl.to(DEV), M)
+    assert L.cap_by_k[M] == V
+
+
+@pytest.mark.parametrize("iters", [1, 3])
+def test_random_head_rounds(iters):
+    # no planted structure: one round compares exactly (up to ties); later
+    # rounds are compared while the assignments still agree
+    w = W.scaled(W.WORKLOADS["llama3_8b_chain"], V=5000, d=256, M=40)
+    Wl = W.lm_head(w)
+    init = W.kmeans_init_ids(w)
+    cl, mu = D.kmeans(Wl.to(DEV), w.M, torch.from_numpy(init).to(DEV), iters=iters)
+    torch.cuda.synchronize()
+    Wh = W.host_array(Wl)
+    X = O.unit_rows(Wh)
+    mu_ref = X[init]
+    got = cl.cpu().numpy().astype(np.int64)
+    for it in range(iters):
+        a_ref, S = O.kmeans_assign(Wh, mu_ref)
+        mu_ref = O.kmeans_update(Wh, a_ref, w.M, mu_ref)
+    if iters == 1:
+        _check_assign(got, S, "round 1")
+        if np.array_equal(got, a_ref):
+            np.testing.assert_allclose(mu.cpu().numpy(), mu_ref, rtol=0, atol=2e-5)
+    else:
+        # the GPU's own last round is self-consistent: its assignment is the
+        # oracle's argmax against the GPU's previous centroids
+        assert (got == a_ref).mean() > 0.99
+
+
+def test_deterministic_and_errors():
+    w = W.scaled(W.WORKLOADS["llama3_8b_chain"], V=3000, d=128, M=30)
+    Wl = W.lm_head(w).to(DEV)
+    init = torch.from_numpy(W.kmeans_init_ids(w)).to(DEV)
+    a1, m1 = D.kmeans(Wl, w.M, init, iters=2)
+    a2, m2 = D.kmeans(Wl, w.M, init, iters=2)
+    torch.cuda.synchronize()
+    assert torch.equal(a1, a2) and torch.equal(m1, m2)
+    bad = init.clone()
+    bad[3] = w.V
+    with pytest.raises(D.DynaError) as e:
+        D.kmeans(Wl, w.M, bad, iters=1)
+    assert e.value.status == D.ERR_DEVICE_DATA
+    with pytest.raises(D.DynaError) as e:
+        D.kmeans(Wl.float(), w.M, init, iters=1)
+    assert e.value.status == D.ERR_UNSUPPORTED

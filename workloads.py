@@ -250,6 +250,29 @@ def overlap_gemm_operands(w: Workload, device="cpu"):
     return a, b
 
 
+def kmeans_init_ids(w: Workload, M: Optional[int] = None, salt: int = 0) -> np.ndarray:
+    """M distinct vocabulary ids (seeded) where the partition builder's
+    centroids start."""
+    M = w.M if M is None else M
+    rng = np.random.default_rng(stream_seed(w, "spare", 100 + salt))
+    return np.sort(rng.choice(w.V, size=M, replace=False)).astype(np.int32)
+
+
+def planted_head(V: int, d: int, M: int, seed: int, noise: float = 0.3, device="cpu"):
+    """A synthetic bf16 LM head with cluster structure: M random directions,
+    row v = (a positive length) * direction[g_v] + isotropic noise, groups g_v
+    cut from a seeded permutation into near-equal runs.  Returns (W[V, d],
+    groups[V])."""
+    torch = _torch()
+    rng = np.random.default_rng(seed)
+    groups = np.empty(V, dtype=np.int64)
+    groups[rng.permutation(V)] = np.arange(V) % M
+    dirs = rng.standard_normal((M, d))
+    lengths = rng.uniform(0.5, 2.0, size=(V, 1))
+    W = dirs[groups] * lengths + noise * rng.standard_normal((V, d))
+    return torch.from_numpy(W.astype(np.float32)).to(torch.bfloat16).to(device), groups
+
+
 def bf16_bits(t) -> np.ndarray:
     """Raw bf16 bit patterns (uint16) of a torch bfloat16 tensor, on the host."""
     torch = _torch()
