@@ -221,20 +221,27 @@ def summarize_trace(trace_dir, bench_json, plain_json, command):
         lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                      f"{float(r['Percentage']):.1f}% |")
-    lines += ["", f"Dominant kernel `{sym}` over the {len(dur)} launches that bench.py brackets with events "
-              f"(the last {n} of the run): rocprofv3 average **{avg:.2f} us**.",
-              f"bench.py in the same (profiled) run: bracket {prof['roofline']['bracket_us']} us, empty bracket "
-              f"{prof['roofline']['empty_bracket_us']} us, kernel {prof['roofline']['avg_launch_us']} us "
-              "(the profiler's completion signals delay the closing event, so brackets read longer under it)."]
+    rf = prof["roofline"]
+    lines += ["", f"Dominant kernel `{sym}` over the {len(dur)} launches that bench.py times with events "
+              f"(the last {n} of the run): rocprofv3 average **{avg:.2f} us**."]
+    if "bracket_us" in rf:
+        lines.append(f"bench.py in the same (profiled) run: bracket {rf['bracket_us']} us, empty bracket "
+                     f"{rf['empty_bracket_us']} us, kernel {rf['avg_launch_us']} us "
+                     "(the profiler's completion signals delay the closing event, so brackets read longer under it).")
+    else:
+        lines.append(f"bench.py in the same (profiled) run, events handed to the dispatch: kernel "
+                     f"{rf['avg_launch_us']} us.")
     if plain:
+        pr = plain["roofline"]
+        extra = (f" (bracket {pr['bracket_us']} us, empty bracket {pr['empty_bracket_us']} us)"
+                 if "bracket_us" in pr else "")
         lines.append(f"bench.py without the profiler (same command minus rocprofv3): kernel "
-                     f"{plain['roofline']['avg_launch_us']} us (bracket {plain['roofline']['bracket_us']} us, "
-                     f"empty bracket {plain['roofline']['empty_bracket_us']} us), "
-                     f"{plain['roofline']['achieved']} GB/s = {plain['roofline']['frac']} of peak; "
-                     f"{plain['value']} steps/s.")
+                     f"{pr['avg_launch_us']} us{extra}, {pr['achieved']} {pr['unit']} = {pr['frac']} of peak; "
+                     f"{plain['value']} {plain['unit']}.")
     lines.append("rocprofv3 times a kernel from dispatch to completion signal; an empty kernel reads about "
                  "1.5 us that way, which the event figure minus an empty bracket does not contain.")
-    out = os.path.join(ROOT, "profiles", f"{sym}_{wl}_kernel_trace.md")
+    tag = wl.split()[0] + ("_kmeans" if "k-means" in wl else "")
+    out = os.path.join(ROOT, "profiles", f"{sym}_{tag}_kernel_trace.md")
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print(out)
@@ -331,6 +338,85 @@ def cpu_baseline_union(w, cluster_of, host, cores, budget_s):
                       f"for {n} of them (scaled to {w.B}), fp64 numpy oracle"}
 
 
+def bench_kmeans(w, args, D, torch):
+    """The partition builder on the workload's LM head: rounds/s of
+    dyna_kmeans, and the assignment kernel (the dominant one) against the
+    bf16 matrix-core peak."""
+    dev = "cuda"
+    print(f"[bench] k-means on {w.name}: V={w.V} d={w.d} M={w.M}", file=sys.stderr, flush=True)
+    Wl = W.lm_head(w, dev)
+    init = torch.from_numpy(W.kmeans_init_ids(w)).to(dev)
+    ws = D.kmeans_workspace(Wl, w.M)
+    R = max(1, args.kmeans_rounds)
+    D.kmeans(Wl, w.M, init, 1, ws=ws)  # warm
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    cl, mu = D.kmeans(Wl, w.M, init, R, ws=ws)
+    torch.cuda.synchronize()
+    total_s = time.perf_counter() - t0
+    # the assignment kernel alone, event-timed on its dispatch
+    n_kt = 20
+    D.set_option(D.OPT_KERNEL_TIMING, 2)
+    D.kernel_timing(reset=True)
+    for _ in range(n_kt):
+        D.kmeans_assign(Wl, mu, ws=ws)
+    torch.cuda.synchronize()
+    D.set_option(D.OPT_KERNEL_TIMING, 0)
+    k_ms, k_n = D.kernel_timing(reset=True)
+    k_s = k_ms / 1e3 / max(k_n, 1)
+    flops = 2.0 * w.V * w.M * w.d
+    a_bytes = 2.0 * w.V * w.d + 2.0 * w.M * w.d + 4.0 * w.V
+    sizes = np.bincount(cl.cpu().numpy(), minlength=w.M)
+    rec = {
+        "metric": "partition-builder rounds/s (spherical k-means on the LM head, 1 GPU)",
+        "value": round(R / total_s, 3),
+        "unit": "rounds/s",
+        "n_gpus": 1, "steps": R, "warmup": 1,
+        "ms_per_step": round(total_s * 1e3 / R, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name} LM head, spherical k-means", "V": w.V, "d": w.d, "M": w.M,
+                   "rounds": R, "timing": "one dyna_kmeans call (row norms, initial centroids, rounds, final sync)"},
+        "cluster_sizes": {"min": int(sizes.min()), "max": int(sizes.max()), "empty": int((sizes == 0).sum())},
+        "roofline": {"kernel": "k-means assignment: every row against every centroid on the matrix cores, argmax epilogue",
+                     "kernel_symbol": "union_gemm_kernel", "bound": "mfma",
+                     "achieved": round(flops / k_s / 1e12, 2), "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": round(flops / k_s / 1e12 / 2500.0, 4), "traffic": None,
+                     "flops_per_launch": int(flops), "avg_launch_us": round(k_s * 1e6, 2), "launches": int(k_n),
+                     "algorithmic_bytes_per_launch": int(a_bytes),
+                     "achieved_GBps_algorithmic": round(a_bytes / k_s / 1e9, 1),
+                     "timing": "events handed to the kernel dispatch"},
+    }
+    if not args.no_cpu:
+        rec["cpu_baseline"] = cpu_baseline_kmeans(w, Wl, init.cpu().numpy())
+    print(json.dumps(rec), flush=True)
+
+
+def cpu_baseline_kmeans(w, Wl, init, rows=2048):
+    """The oracle's assignment and update on the first `rows` rows (all M
+    centroids), scaled to the full vocabulary."""
+    from oracle import dynaspec_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    Wh = W.host_array(Wl[:rows])
+    mu = O.unit_rows(W.host_array(Wl[torch_index(init)]))
+    t0 = time.perf_counter()
+    a, _ = O.kmeans_assign(Wh, mu)
+    O.kmeans_update(Wh, a, w.M, mu)
+    dt = (time.perf_counter() - t0) * w.V / rows
+    return {"value": 1.0 / dt, "unit": "rounds/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"one round on {rows} of the {w.V} rows with all {w.M} centroids, scaled by {w.V}/{rows}; "
+                      "fp64 numpy oracle"}
+
+
+def torch_index(ids):
+    import torch
+    return torch.from_numpy(np.asarray(ids, dtype=np.int64))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -345,6 +431,10 @@ def main():
     ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "COUNTERS_JSON"),
                     help="write profiles/traffic_<workload>.json from FETCH_SIZE / WRITE_SIZE runs of --counters")
     ap.add_argument("--command", action="append", default=[], help="command line(s) recorded in a summary")
+    ap.add_argument("--kmeans", action="store_true",
+                    help="measure the partition builder (spherical k-means on the workload's LM head) instead "
+                         "of the draft head")
+    ap.add_argument("--kmeans-rounds", type=int, default=5)
     ap.add_argument("--counters", action="store_true",
                     help="hardware-counter pass: build the layout (a row copy of known size) "
                          "and run 20 eager steps; no timing")
@@ -367,6 +457,9 @@ def main():
     D.lib()
     dev = "cuda"
     w = W.WORKLOADS[args.workload]
+    if args.kmeans:
+        bench_kmeans(w, args, D, torch)
+        return
     mode = mode_of(w, D)
     k_t = w.k_t if mode & D.SEL_TOPK else 1
     print(f"[bench] {w.name}: V={w.V} d={w.d} M={w.M} H={w.H} k={w.k} B={w.B}", file=sys.stderr,
