@@ -147,7 +147,7 @@ def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20):
             "routing_hidden_frac": round(max(0.0, t_s - t_o) / t_r, 3) if t_r > 0 else None}
 
 
-KERNEL_UNITS = {"logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip",
+KERNEL_UNITS = {"logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip", "union_gemm_kernel": "gather.hip",
                 "rowdot_gemv_kernel": "rowdot.hip"}
 
 

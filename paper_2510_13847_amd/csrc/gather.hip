@@ -685,6 +685,9 @@ dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
         case 4: return launch_cfg<2, 8, 128, 16>(a, stream);
         case 5: return launch_cfg<4, 5, 64, 16>(a, stream);
         case 6: return launch_cfg<8, 3, 64, 16>(a, stream);
+        case 7: return launch_cfg<8, 3, 128, 8>(a, stream);
+        case 8: return launch_cfg<4, 2, 512, 4>(a, stream);
+        case 9: return launch_cfg<3, 2, 512, 8>(a, stream);
         default: return launch_cfg<4, 4, 128, 16>(a, stream);
     }
 }
