@@ -41,8 +41,12 @@ def test_set_option_validation():
     assert b"unknown option" in lib.dyna_last_error()
     assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 7) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 0) == D.OK
-    assert lib.dyna_set_option(D.OPT_GATHER_CFG, 7) == D.ERR_INVALID_ARG
+    assert lib.dyna_set_option(D.OPT_GATHER_CFG, 10) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_GATHER_CFG, 0) == D.OK
+    assert lib.dyna_set_option(D.OPT_UNION_CFG, 15) == D.ERR_INVALID_ARG
+    assert lib.dyna_set_option(D.OPT_UNION_CFG, 0) == D.OK
+    assert lib.dyna_set_option(D.OPT_KMEANS_CFG, 5) == D.ERR_INVALID_ARG
+    assert lib.dyna_set_option(D.OPT_KMEANS_CFG, 0) == D.OK
 
 
 def _layout(V=1000, d=64, M=10, cap=None, W=0x1000):
@@ -166,3 +170,40 @@ def test_position_budgets_match_the_oracle():
     assert lib.dyna_cluster_budget(3, 64, 32, 1, 2) == -1
     assert lib.dyna_static_budget(3, 0) == -1
     assert D.cluster_budget(2, 64, 32) == 8 and D.static_budget(2, 32) == 10
+
+
+def test_union_beam_and_kmeans_argument_errors():
+    lib = D.lib()
+    L, keep = _layout()
+    P = 0x10000
+    R = D._Router(64, 0, 10, D.BF16, 0, P, None, None, None)
+    head = lib.dyna_draft_head
+
+    def call(cap, beta=0.0, mode=D.SEL_TOPK | D.SEL_UNION):
+        return head(ctypes.byref(R), ctypes.byref(L), P, P, D.BF16, 3, 3, mode, 4, 1.0, beta, None,
+                    P, P, None, None, None, None, cap, P, 1 << 30, None, None, None)
+    # a union of 3 rows x 3 clusters needs min(V, 3 * cap_by_k[3]) = 900 slots per row
+    assert call(300) == D.ERR_CAPACITY
+    assert call(900, beta=0.3) == D.ERR_UNSUPPORTED
+    assert call(900, mode=D.SEL_UNION) == D.ERR_INVALID_ARG  # no selection asked for
+    assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 0) == D.OK
+    # beam expansion: sizes are checked before any device work
+    be = lib.dyna_beam_expand
+    assert be(P, P, None, 2, 4, 0, P, P, P, None) == D.ERR_INVALID_ARG
+    assert be(P, P, None, 2, 4, 65, P, P, P, None) == D.ERR_INVALID_ARG
+    assert be(P, P, None, 2, 0, 4, P, P, P, None) == D.ERR_INVALID_ARG
+    assert be(P, P, None, 200, 64, 8, P, P, P, None) == D.ERR_UNSUPPORTED  # B * k_t > 8192
+    assert be(None, P, None, 2, 4, 4, P, P, P, None) == D.ERR_INVALID_ARG
+    # partition builder
+    assert lib.dyna_kmeans_workspace_bytes(1000, 64, 10) > 0
+    km = lib.dyna_kmeans
+    big = 1 << 34
+    assert km(P, D.F32, 1000, 64, 10, P, 3, P, None, P, big, None) == D.ERR_UNSUPPORTED
+    assert km(P, D.BF16, 1000, 60, 10, P, 3, P, None, P, big, None) == D.ERR_INVALID_ARG
+    assert km(P, D.BF16, 1000, 64, 1001, P, 3, P, None, P, big, None) == D.ERR_INVALID_ARG
+    assert km(P, D.BF16, 1000, 64, 10, P, 0, P, None, P, big, None) == D.ERR_INVALID_ARG
+    assert km(P, D.BF16, 1000, 64, 10, None, 3, P, None, P, big, None) == D.ERR_INVALID_ARG
+    assert km(P, D.BF16, 1000, 64, 10, P, 3, P, None, P, 16, None) == D.ERR_WORKSPACE
+    assert km(P, D.BF16, 1000, 16384, 10, P, 3, P, None, P, big, None) == D.ERR_UNSUPPORTED
+    assert lib.dyna_kmeans_assign(P, D.BF16, 1000, 64, None, 10, P, None, P, big, None) == D.ERR_INVALID_ARG
+    assert lib.dyna_kmeans_update(P, D.BF16, 1000, 64, P, 10, None, P, big, None) == D.ERR_INVALID_ARG
