@@ -68,7 +68,7 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
     uint64_t* cand = sel + k;                                          // [M] tie candidates
     int32_t* sid = reinterpret_cast<int32_t*>(cand + M);               // [k] ids ascending
     int32_t* ssize = sid + k;                                          // [k]
-    __shared__ int hist[256];
+    __shared__ int hist[256], hist2[256];
     __shared__ int tmp[kNT / kWave + 1];
     __shared__ uint32_t sh_prefix;
     __shared__ int sh_krem, sh_nsel, sh_ncand;
@@ -104,6 +104,7 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
         }
     }
     hist[threadIdx.x] = 0;
+    hist2[threadIdx.x] = 0;
     if (threadIdx.x == 0) {
         sh_nsel = 0;
         sh_ncand = 0;
@@ -116,15 +117,14 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
     if (threadIdx.x < kWave) radix_digit(hist, k, 0u, 24, &sh_prefix, &sh_krem);
     __syncthreads();
     const uint32_t p1 = sh_prefix;
-    hist[threadIdx.x] = 0;
-    __syncthreads();
+    const int krem1 = sh_krem;
     // pass 2: second byte inside the chosen top byte
     for (int j = threadIdx.x; j < M; j += kNT) {
         const uint32_t o = ord_f32(sv[j]);
-        if ((o & 0xff000000u) == p1) atomicAdd(&hist[(o >> 16) & 255u], 1);
+        if ((o & 0xff000000u) == p1) atomicAdd(&hist2[(o >> 16) & 255u], 1);
     }
     __syncthreads();
-    if (threadIdx.x < kWave) radix_digit(hist, sh_krem, p1, 16, &sh_prefix, &sh_krem);
+    if (threadIdx.x < kWave) radix_digit(hist2, krem1, p1, 16, &sh_prefix, &sh_krem);
     __syncthreads();
     const uint32_t P = sh_prefix >> 16;  // 16-bit prefix of the k-th largest code
     const int need = sh_krem;             // places left for codes with prefix P
@@ -146,16 +146,38 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
     }
     __syncthreads();
 
-    // rank order (score desc, id asc) and ascending-id order by counting
+    // rank order (score desc, id asc) and ascending-id order by counting:
+    // key i is compared with S slices of the k keys by S threads at once
+    // (the tie-candidate array is free again and holds the two counts)
+    int32_t* rk = reinterpret_cast<int32_t*>(cand);  // [k]
+    int32_t* ik = rk + k;                             // [k]
     for (int i = threadIdx.x; i < k; i += kNT) {
-        const uint64_t key = sel[i];
-        const uint32_t id = key_id(key);
-        int rank = 0, idrank = 0;
-        for (int j = 0; j < k; ++j) {
-            const uint64_t o = sel[j];
-            rank += o > key;
-            idrank += key_id(o) < id;
+        rk[i] = 0;
+        ik[i] = 0;
+    }
+    __syncthreads();
+    {
+        const int S = max(1, kNT / k);
+        const int span = (k + S - 1) / S;
+        for (int wi = threadIdx.x; wi < k * S; wi += kNT) {
+            const int i = wi % k, sl = wi / k;
+            const uint64_t key = sel[i];
+            const uint32_t id = key_id(key);
+            const int j0 = sl * span, j1 = min(k, j0 + span);
+            int r = 0, q = 0;
+            for (int j = j0; j < j1; ++j) {
+                const uint64_t o = sel[j];
+                r += o > key;
+                q += key_id(o) < id;
+            }
+            if (r) atomicAdd(&rk[i], r);
+            if (q) atomicAdd(&ik[i], q);
         }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < k; i += kNT) {
+        const uint32_t id = key_id(sel[i]);
+        const int rank = rk[i], idrank = ik[i];
         topk_ids[(int64_t)b * k + rank] = (int32_t)id;
         if (topk_scores) topk_scores[(int64_t)b * k + rank] = sv[id];
         if (sel_sorted != nullptr) {
