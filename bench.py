@@ -48,6 +48,18 @@ def out_bytes(w, sizes, cl):
     return 8 * int(sizes[cl].sum())
 
 
+def launch_bytes(w, slab, outs):
+    """Algorithmic bytes of one launch of the dominant kernel: each distinct
+    selected slab once, the contexts' h rows and the per-slot outputs; the
+    one-launch step also reads the router weights and x, and writes no
+    per-slot outputs unless logits are requested."""
+    s_w = 2 if w.dtype == "bf16" else 4
+    if dominant_kernel(w)[0] == "chain_step_kernel":
+        router = s_w * (w.d_r * w.H + w.H * w.M) if w.H else s_w * w.d_r * w.M
+        return router + slab + s_w * (w.d_r + w.d)
+    return slab + s_w * w.B * w.d + outs
+
+
 def mode_of(w, D):
     m = D.SEL_UNION if w.union else 0
     for name, flag in (("argmax", D.SEL_ARGMAX), ("topk", D.SEL_TOPK), ("sample", D.SEL_SAMPLE)):
@@ -147,7 +159,7 @@ def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20):
             "routing_hidden_frac": round(max(0.0, t_s - t_o) / t_r, 3) if t_r > 0 else None}
 
 
-KERNEL_UNITS = {"logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip", "union_gemm_kernel": "gather.hip",
+KERNEL_UNITS = {"chain_step_kernel": "chain.hip", "logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip", "union_gemm_kernel": "gather.hip",
                 "rowdot_gemv_kernel": "rowdot.hip"}
 
 
@@ -175,6 +187,8 @@ def kernel_source_hash(symbol):
 
 def dominant_kernel(w):
     """Symbol (substring) and description of the gathered-head kernel a step of w launches."""
+    if w.B == 1 and w.modes == ("argmax",) and w.dtype == "bf16":
+        return "chain_step_kernel", "whole one-context step in one launch (router, top-k, gathered head, argmax)"
     if w.B == 1 and w.modes == ("argmax",):
         return "logits_greedy_kernel", "gathered head fused with argmax selection (one context)"
     if w.union and w.dtype == "bf16":
@@ -485,7 +499,7 @@ def main():
         for i in range(20):
             head(xs[i], xs[i], us[i], layout=layouts[i % N_REPLICAS], router=routers[i % N_REPLICAS])
             cl = head.clusters.cpu().numpy()
-            alg.append(s_w * w.d * int(sizes[np.unique(cl)].sum()) + s_w * w.B * w.d + out_bytes(w, sizes, cl))
+            alg.append(launch_bytes(w, s_w * w.d * int(sizes[np.unique(cl)].sum()), out_bytes(w, sizes, cl)))
         torch.cuda.synchronize()
         print(json.dumps({"counters_run": w.name, "kernel_symbol": dominant_kernel(w)[0],
                           "copy_bytes_each_way": w.V * w.d * (2 if w.dtype == "bf16" else 4),
@@ -548,9 +562,9 @@ def main():
     overhead_s = float(np.median([a.elapsed_time(b) for a, b in ov])) / 1e3
     k_avg_s = max(bracket_s - overhead_s, 1e-9)
     # bytes one launch must move: each distinct selected slab once, the
-    # contexts' h rows, and the logits and vocabulary ids it writes
-    k_bytes = float(np.mean([slab_bytes[i % POOL] for i in range(n_kt)])) + s_w * w.B * w.d \
-        + float(np.mean([outs[i % POOL] for i in range(n_kt)]))
+    # contexts' h rows, and the logits and vocabulary ids it writes (the
+    # one-launch step: also the router weights and x)
+    k_bytes = float(np.mean([launch_bytes(w, slab_bytes[i % POOL], outs[i % POOL]) for i in range(n_kt)]))
     achieved = k_bytes / k_avg_s / 1e9
     # matrix-core work of the launch: 2 flop per slab element per context it is dotted with
     k_flops = 2.0 * w.d * float(np.mean([rows[i % POOL] for i in range(n_kt)]))

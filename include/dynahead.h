@@ -124,7 +124,11 @@ dyna_status dyna_build_layout(const int32_t* cluster_of, int32_t V, int32_t M,
 /* ------------------------------------------------------------------ */
 
 /* Workspace for any of the calls below with these sizes (router may be NULL
- * when only shortlist_logits / draft_select are used). */
+ * when only shortlist_logits / draft_select are used).  A new workspace must
+ * be zero-filled once before its first dyna_draft_head call: it holds the
+ * arrival counters of the one-context kernels, which every call leaves at
+ * zero.  (A one-launch step that finds them nonzero does not hang: its
+ * bounded waits run out and it reports out_ids = -1.) */
 size_t dyna_workspace_bytes(const dyna_layout* L, const dyna_router* r,
                             int32_t B, int32_t k, int32_t cap);
 
@@ -344,11 +348,15 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   0 stops.
  * DYNA_OPT_GEMV_ROWS: rows each wave of the GEMV kernel keeps in flight:
  *   0 automatic, else 1, 2 or 4 (capped by the register budget).
- * DYNA_OPT_FUSED_B1: 0 (default) lets dyna_draft_head run a one-context
- *   greedy step as four launches (router layer 1; router layer 2; top-k with
- *   shortlist and plan; gathered head fused with selection); 1 uses the
- *   separate kernels.  Both give bit-identical results.  Under kernel timing
- *   the fused gathered-head + selection launch is what is timed.
+ * DYNA_OPT_FUSED_B1: how dyna_draft_head runs a one-context greedy step.
+ *   0 (default): one launch (router, top-k, shortlist, gathered logits and
+ *   selection with two grid-wide hand-offs) when the router, LM head and
+ *   activations are all bf16, d, d_r, H <= 8192 and routing stays on
+ *   `stream`; otherwise as 2.  2: four launches (router layer 1; router
+ *   layer 2; top-k with shortlist and plan; gathered head fused with
+ *   selection).  1: the separate kernels.  All give bit-identical results.
+ *   Under kernel timing the one-launch step, or the fused gathered-head +
+ *   selection launch, is what is timed.
  * DYNA_OPT_MFMA_UNROLL: k steps the direct-load MFMA kernel (path 3) loads
  *   ahead: 0 automatic (8), 4, 8 or 16.
  * DYNA_OPT_GATHER_CFG: shape of the LDS-staged MFMA kernel (path 2): 0

@@ -34,7 +34,6 @@ std::mutex g_timing_mu;
 std::vector<std::pair<hipEvent_t, hipEvent_t>> g_timing_pairs;
 std::vector<hipEvent_t> g_timing_free;
 
-constexpr int kMaxDevices = 64;
 thread_local hipEvent_t g_ev_x[kMaxDevices];
 thread_local hipEvent_t g_ev_join[kMaxDevices];
 
@@ -127,8 +126,9 @@ struct Carve {
     int32_t* row_len = nullptr;   // [B]
     float* logits = nullptr;      // [B, cap]
     int32_t* slot_vid = nullptr;  // [B, cap]
-    int32_t* counters = nullptr;  // [2] arrival counters of the fused one-context kernels
+    int32_t* counters = nullptr;  // [4] arrival counters (and error word) of the fused one-context kernels
     void* partials = nullptr;     // partials of the fused one-context head
+    void* chain = nullptr;        // tagged hand-off region of the one-launch step
     Plan plan{};
     float* rpart = nullptr;  // split-K partial sums of the router layers
     size_t rpart_floats = 0;
@@ -178,8 +178,9 @@ static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_
     c.row_len = static_cast<int32_t*>(take(sizeof(int32_t) * Bl));
     c.logits = static_cast<float*>(take(sizeof(float) * Bl * cap));
     c.slot_vid = static_cast<int32_t*>(take(sizeof(int32_t) * Bl * cap));
-    c.counters = static_cast<int32_t*>(take(2 * sizeof(int32_t)));
+    c.counters = static_cast<int32_t*>(take(4 * sizeof(int32_t)));
     if (B == 1) c.partials = take(greedy_partials_bytes());
+    if (B == 1 && r) c.chain = take(chain_region_bytes(r->H, r->M));
     if (L) {
         c.plan.max_chunks = (int32_t)max_chunks_for(L);
         // per-row lists (B * k entries) or the union's (every row in each
@@ -283,7 +284,7 @@ static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtyp
     const int path = option_router_path();
     RowdotArgs a{};
     a.zero_words = zero_words;  // cleared by block 0 of the first router kernel
-    a.n_zero_words = zero_words ? 2 : 0;
+    a.n_zero_words = zero_words ? 4 : 0;
     a.W = r->W1;
     a.wdtype = r->wdtype;
     a.K = r->d_r;
@@ -405,7 +406,7 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         return DYNA_OK;
     }
     if (option == DYNA_OPT_FUSED_B1) {
-        REQUIRE(value == 0 || value == 1, "fused option %d not in {0, 1}", value);
+        REQUIRE(value >= 0 && value <= 2, "fused option %d not in {0, 1, 2}", value);
         g_fused_off.store(value);
         return DYNA_OK;
     }
@@ -616,9 +617,43 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     int32_t* clusters = out_clusters ? out_clusters : c.topk_ids;
     float* logits = out_logits ? out_logits : c.logits;
-    // one greedy context: the gathered head carries the selection (4 launches)
-    const bool fused = B == 1 && !g_fused_off.load() && option_logits_path() <= 1 && k_t == 1 &&
-                       !want_sample;
+    // one greedy context: the gathered head carries the selection (4 launches),
+    // or the whole step is one launch
+    const int fused_opt = g_fused_off.load();
+    const bool fused = B == 1 && fused_opt != 1 && option_logits_path() <= 1 && k_t == 1 && !want_sample;
+    if (fused && fused_opt == 0 && !split && option_router_path() <= 1) {
+        ChainRequest q{};
+        q.all_bf16 = r->wdtype == DYNA_BF16 && L->wdtype == DYNA_BF16 && adtype == DYNA_BF16;
+        q.W1 = r->W1;
+        q.b1 = r->b1;
+        q.W2 = r->W2;
+        q.b2 = r->b2;
+        q.d_r = r->d_r;
+        q.H = r->H;
+        q.M = r->M;
+        q.act = r->act;
+        q.x = x;
+        q.W = L->W_perm;
+        q.perm = L->perm;
+        q.offsets = L->offsets;
+        q.d = L->d;
+        q.V = L->V;
+        q.h = h;
+        q.k = k;
+        q.region = c.chain;
+        q.out_clusters = clusters;
+        q.topk_scores = c.topk_scores;
+        q.sel_sorted = c.sel_sorted;
+        q.sel_rowoff = c.sel_rowoff;
+        q.row_len = c.row_len;
+        q.out_logits = out_logits;
+        q.out_ids = want_ids ? out_ids : nullptr;
+        q.out_logprobs = want_ids ? out_logprobs : nullptr;
+        q.inv_t = 1.0f / temperature;
+        q.beta = tail_beta;
+        if (chain_step_eligible(q) && q.out_ids != nullptr)
+            return timed([&] { return launch_chain_step(q, stream); }, stream);
+    }
 
     // routing (the router's stream)
     TRY(run_router(r, x, adtype, B, c.scores, c.hidden, c.rpart, c.rpart_floats, rs, fused ? c.counters : nullptr));

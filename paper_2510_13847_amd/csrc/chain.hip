@@ -1,0 +1,732 @@
+// One-context greedy draft step in a single launch (B = 1): router layer 1,
+// router layer 2, top-k clusters and shortlist, gathered logits and argmax
+// selection (Sec. 4.2 and Sec. 4.3; Algorithm 1, one draft step).
+//
+// With one context every stage is small (the chain workload moves 8 MB,
+// 2 MB, 4 KB and 33 MB), so as separate kernels the step is dominated by
+// launch gaps and by each kernel's cold start.  Here one grid of G
+// workgroups runs all of them, with two grid-wide hand-offs:
+//
+//   1. every wave dots its rows of W1 with x (x in registers) and writes
+//      the hidden units with device-coherent stores; its W2 rows for stage 2
+//      are already loading;
+//   2. after all workgroups arrived, each stages the hidden layer in LDS and
+//      dots its prefetched W2 rows with it, writing the scores;
+//   3. after all arrived again, every workgroup reads the M scores into LDS
+//      and takes the top-k itself (the same deterministic selection in every
+//      workgroup, so no further hand-off), sorts the k ids ascending and
+//      forms the shortlist offsets;
+//   4. the shortlist rows are split evenly over all waves as contiguous
+//      ranges (a range may cross slab boundaries), streamed with
+//      non-temporal 16-byte loads and dotted with h (in registers);
+//   5. each workgroup publishes its greedy partial and the last one merges
+//      them (greedy.h) and writes the token.
+//
+// Hand-off protocol: every handed-off word is 64 bits, a 32-bit epoch tag
+// above the 32-bit value, written with one device-coherent store; readers
+// poll the words themselves with coherent loads until every tag equals the
+// launch's epoch, so the data carries its own ready signal (one store and
+// one load round trip, no counter).  The epoch is one more than the value a
+// workspace word holds at launch; workgroup 0 stores it back after the
+// merge, when every workgroup has read it.  A zero-filled workspace starts
+// at epoch 1, above the tags of its zero words.  Every poll is bounded in
+// time: a word that never turns current (the grid is not co-resident, or a
+// workspace that was not zero-filled) sets an error word, the poll gives up
+// and the launch reports no token (out_ids = -1) but still terminates.
+#include <atomic>
+
+#include "dyna_internal.h"
+#include "gemv.h"
+#include "greedy.h"
+#include "topk.h"
+
+namespace dyna {
+namespace {
+
+constexpr int kChainThreads = kThreads;  // 4 waves per workgroup
+constexpr int kChainWaves = kChainThreads / kWave;
+
+// words of the chain region of the workspace: epoch, error, then tagged
+// hidden [H], scores [M] and partials [G][4]
+constexpr int kPartWords = 4;
+constexpr int kChainMaxGrid = 1024;  // workgroups at most (twice the compute units, capped)
+
+struct ChainArgs {
+    // router: H == 0 is a single linear layer W1 [M, d_r]
+    const uint16_t* W1;
+    const float* b1;
+    const uint16_t* W2;
+    const float* b2;
+    int32_t d_r, H, M, act;
+    const uint16_t* x;  // [d_r]
+    // layout
+    const uint16_t* W;  // [V, d] permuted LM head
+    const int32_t* perm;
+    const int32_t* offsets;
+    int32_t d, V;
+    const uint16_t* h;  // [d]
+    int32_t k;
+    // workspace (chain region)
+    uint32_t* epoch;     // [1]
+    uint32_t* err;       // [1]
+    uint64_t* thidden;   // [H] tagged
+    uint64_t* tscores;   // [M] tagged
+    uint64_t* tpart;     // [G][kPartWords] tagged
+    // outputs (each may be null except out_ids)
+    int32_t* out_clusters;  // [k] rank order
+    float* topk_scores;     // [k]
+    int32_t* sel_sorted;    // [k]
+    int32_t* sel_rowoff;    // [k + 1]
+    int32_t* row_len;       // [1]
+    float* out_logits;      // [cap], shortlist order
+    int32_t* out_ids;       // [1]
+    float* out_logprobs;    // [1]
+    float inv_t, beta;
+    uint64_t spin_ticks;  // bound of every wait, in wall-clock ticks
+};
+
+// Bytes of dynamic LDS: scores [M], offsets [M + 1], candidate keys [M],
+// shortlist ids [k] and offsets [k + 1], hidden [H], the G partials' words.
+__host__ __device__ inline size_t chain_lds_bytes(int M, int k, int H, int G) {
+    size_t b = (size_t)M * 4 + (size_t)(M + 1) * 4;
+    b = (b + 15) / 16 * 16;
+    b += (size_t)M * 8;
+    b += (size_t)k * 4 + (size_t)(k + 1) * 4;
+    b = (b + 15) / 16 * 16;
+    b += (size_t)H * 4;
+    b += (size_t)G * kPartWords * 4;
+    return b;
+}
+
+__device__ __forceinline__ uint64_t tagged(uint32_t e, uint32_t v) { return ((uint64_t)e << 32) | v; }
+
+// Reads n tagged words src[0..n) into dst (as raw 32-bit values), workgroup
+// wide: each thread issues its loads together, then re-polls all of its
+// stale words together (one round trip per poll, however many are stale)
+// until they carry epoch e or the time bound runs out.
+template <int NT>
+__device__ __forceinline__ void poll_words(const ChainArgs& A, const uint64_t* src, int n, uint32_t e,
+                                           uint32_t* dst) {
+    constexpr int Q = 8;
+    const uint64_t t0 = wall_clock64();
+    for (int base = 0; base < n; base += NT * Q) {
+        uint64_t v[Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int j = base + q * NT + (int)threadIdx.x;
+            v[q] = j < n ? load_coherent(src + j) : tagged(e, 0u);
+        }
+        for (;;) {
+            bool stale = false;
+#pragma unroll
+            for (int q = 0; q < Q; ++q) stale |= (uint32_t)(v[q] >> 32) != e;
+            if (!stale) break;
+            if (wall_clock64() - t0 > A.spin_ticks) {
+                store_coherent(A.err, 1u);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+            for (int q = 0; q < Q; ++q)
+                if ((uint32_t)(v[q] >> 32) != e) v[q] = load_coherent(src + base + q * NT + (int)threadIdx.x);
+        }
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int j = base + q * NT + (int)threadIdx.x;
+            if (j < n) dst[j] = (uint32_t)v[q];
+        }
+    }
+}
+
+// Thread t reads the tagged words src[t + NT q], q < Q (those below n), into
+// raw[q], re-polling its stale ones together until they carry epoch e or
+// the time bound runs out.
+template <int NT, int Q>
+__device__ __forceinline__ void poll_own(const ChainArgs& A, const uint64_t* src, int n, uint32_t e,
+                                         uint32_t (&raw)[Q]) {
+    const uint64_t t0 = wall_clock64();
+    uint64_t v[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int j = (int)threadIdx.x + NT * q;
+        v[q] = j < n ? load_coherent(src + j) : tagged(e, 0u);
+    }
+    for (;;) {
+        bool stale = false;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) stale |= (uint32_t)(v[q] >> 32) != e;
+        if (!stale) break;
+        if (wall_clock64() - t0 > A.spin_ticks) {
+            store_coherent(A.err, 1u);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+            if ((uint32_t)(v[q] >> 32) != e) v[q] = load_coherent(src + (int)threadIdx.x + NT * q);
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) raw[q] = (uint32_t)v[q];
+}
+
+template <int NB>
+__device__ __forceinline__ void load_bf16_row(Raw8<uint16_t> (&w)[NB], const uint16_t* row, int K, int lane) {
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk) {
+        const int e = blk * 512 + lane * 8;
+        if (e < K) w[blk].template load<true>(row + e);
+        else w[blk].zero();
+    }
+}
+
+template <int NB>
+__device__ __forceinline__ float dot_bf16(const Raw8<uint16_t> (&w)[NB], const Raw8<uint16_t> (&v)[NB]) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = fmaf(w[blk].at(j), v[blk].at(j), acc);
+    return wave_sum(acc);
+}
+
+// Row . hidden, the hidden layer (fp32) in LDS.
+template <int NB>
+__device__ __forceinline__ float dot_lds(const Raw8<uint16_t> (&w)[NB], const float* hid, int K, int lane) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk) {
+        const int e = blk * 512 + lane * 8;
+        if (e < K) {
+            const f32x4 a = *reinterpret_cast<const f32x4*>(hid + e);
+            const f32x4 b = *reinterpret_cast<const f32x4*>(hid + e + 4);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc = fmaf(w[blk].at(j), a[j], acc);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc = fmaf(w[blk].at(4 + j), b[j], acc);
+        }
+    }
+    return wave_sum(acc);
+}
+
+// Scores per thread in the selection: thread t holds ids t + NT q, q < kSelQ.
+constexpr int kSelQ = 4;
+constexpr int kChainMaxM = kChainThreads * kSelQ;
+
+// The k best of the M <= NT * kSelQ scores v[] (registers; thread t holds
+// ids t + NT q) by (score desc, id asc), as the shortlist in ascending
+// cluster id: sid[0..k) the ids, rowoff[0..k] the exclusive prefix of their
+// slab sizes.  Returns the shortlist length.
+//
+// Each score gets a class that is monotone in the score: 0 for -inf and
+// NaN, 255 for +inf, and for finite scores 1 + one of 254 equal-width bins
+// between the finite minimum and maximum (so the bins follow the values,
+// whatever their scale).  One histogram, scanned from the top by every wave,
+// gives the class c* of the k-th best and the number `need` of places left
+// in it; classes above c* are members, and the few scores in class c* are
+// ranked exactly by their (score, id) keys.  Counts and sizes of the members
+// are then scanned in id order (q major, thread minor) to lay out the
+// shortlist.
+template <int NT>
+__device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32_t* offs, int M, int k,
+                                            uint64_t* cand, int32_t* sid, int32_t* rowoff, uint32_t* err) {
+    static_assert(NT == 256, "one histogram bin per thread");
+    constexpr int NW = NT / kWave;
+    constexpr int Q = kSelQ;
+    __shared__ __attribute__((aligned(16))) int hist[256];
+    __shared__ float s_lo[NW], s_hi[NW];
+    __shared__ int s_nc[NW];
+    __shared__ int s_cnt[Q][NW], s_len[Q][NW];
+    const float inf = __builtin_inff();
+    const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+    bool valid[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) valid[q] = t + NT * q < M;
+
+    // range of the finite scores
+    float lo = inf, hi = -inf;
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+        if (valid[q] && v[q] - v[q] == 0.0f) {
+            lo = fminf(lo, v[q]);
+            hi = fmaxf(hi, v[q]);
+        }
+    hist[t] = 0;
+    {
+        const float wl = -readlane_f32(wave_max_f32(-lo), kWave - 1);
+        const float wh = readlane_f32(wave_max_f32(hi), kWave - 1);
+        if (lane == 0) {
+            s_lo[w] = wl;
+            s_hi[w] = wh;
+        }
+    }
+    __syncthreads();
+    lo = s_lo[0];
+    hi = s_hi[0];
+#pragma unroll
+    for (int q = 1; q < NW; ++q) {
+        lo = fminf(lo, s_lo[q]);
+        hi = fmaxf(hi, s_hi[q]);
+    }
+    const float span = hi - lo;
+    const float scale = (hi > lo && span < inf) ? 254.0f / span : 0.0f;
+    int c[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const float x = v[q];
+        int cl;
+        if (x != x || x == -inf) cl = 0;
+        else if (x == inf) cl = 255;
+        else cl = 1 + min((int)((x - lo) * scale), 253);
+        c[q] = valid[q] ? cl : -1;
+        if (valid[q]) atomicAdd(&hist[cl], 1);
+    }
+    __syncthreads();
+
+    // every wave scans the histogram from the top (lane l: classes 255 - 4l
+    // down to 252 - 4l) and finds the class of the k-th best and the places
+    // left in it, on every lane
+    int cstar, need;
+    {
+        const int4 h4 = *reinterpret_cast<const int4*>(hist + 252 - 4 * lane);
+        const int cc[4] = {h4.w, h4.z, h4.y, h4.x};
+        const int sum = cc[0] + cc[1] + cc[2] + cc[3];
+        const int inc = wave_inclusive_scan(sum);
+        const int exc = inc - sum;
+        const bool mine = exc < k && k <= inc;
+        int cs = 0, nd = 0, acc = exc;
+        bool found = false;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (!found && acc + cc[q] >= k) {
+                cs = 255 - 4 * lane - q;
+                nd = k - acc;
+                found = true;
+            }
+            acc += cc[q];
+        }
+        const uint64_t bal = __ballot(mine);
+        const int src = bal ? (int)__builtin_ctzll(bal) : 0;
+        cstar = __builtin_amdgcn_readlane(cs, src);
+        need = __builtin_amdgcn_readlane(nd, src);
+    }
+
+    // members above c*; the scores in c* are collected per wave and ranked
+    // by their owners
+    bool mem[Q], isc[Q];
+    uint64_t key[Q];
+    uint64_t* seg = cand + (int64_t)w * kWave * Q;
+    int nc = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        mem[q] = c[q] > cstar;
+        isc[q] = c[q] == cstar;
+        key[q] = sel_key(v[q], (uint32_t)(t + NT * q));
+        const uint64_t bal = __ballot(isc[q]);
+        if (isc[q])
+            seg[nc + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))] = key[q];
+        nc += __popcll(bal);
+    }
+    if (lane == 0) s_nc[w] = nc;
+    __syncthreads();
+    int ntot = 0;
+#pragma unroll
+    for (int g = 0; g < NW; ++g) ntot += s_nc[g];
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+        if (isc[q]) {
+            int rank = 0;
+            if (ntot != need)
+                for (int g = 0; g < NW; ++g) {
+                    const uint64_t* sg = cand + (int64_t)g * kWave * Q;
+                    for (int j = 0; j < s_nc[g]; ++j) rank += sg[j] > key[q];
+                }
+            mem[q] = rank < need;
+        }
+
+    // the shortlist in ascending id: (q, thread) order
+    int sz[Q], pcnt[Q], plen[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int j = t + NT * q;
+        sz[q] = mem[q] ? offs[j + 1] - offs[j] : 0;
+        const uint64_t bal = __ballot(mem[q]);
+        pcnt[q] = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+        const int inc = wave_inclusive_scan(sz[q]);
+        plen[q] = inc - sz[q];
+        if (lane == kWave - 1) {
+            s_cnt[q][w] = __popcll(bal);
+            s_len[q][w] = inc;
+        }
+    }
+    __syncthreads();
+    int total_cnt = 0, total_len = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int g = 0; g < NW; ++g) {
+            const int cq = s_cnt[q][g], lq = s_len[q][g];
+            // this (q, wave) block follows every block (q', g') before it
+#pragma unroll
+            for (int qq = 0; qq < Q; ++qq)
+                if (qq == q) {
+                    if (g < w) {
+                        pcnt[qq] += cq;
+                        plen[qq] += lq;
+                    }
+                } else if (q < qq) {
+                    pcnt[qq] += cq;
+                    plen[qq] += lq;
+                }
+            total_cnt += cq;
+            total_len += lq;
+        }
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+        if (mem[q] && pcnt[q] < k) {
+            sid[pcnt[q]] = t + NT * q;
+            rowoff[pcnt[q]] = plen[q];
+        }
+    if (t == 0) {
+        rowoff[k] = total_len;
+        if (total_cnt != k) store_coherent(err, 1u);
+    }
+    __syncthreads();
+    return total_len;
+}
+
+template <int NB, int R>
+__global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    const int M = A.M, k = A.k, H = A.H;
+    float* sv = reinterpret_cast<float*>(smem);              // [M]
+    int32_t* offs = reinterpret_cast<int32_t*>(sv + M);       // [M + 1]
+    size_t o = ((size_t)M * 4 + (size_t)(M + 1) * 4 + 15) / 16 * 16;
+    uint64_t* cand = reinterpret_cast<uint64_t*>(smem + o);   // [M]
+    o += (size_t)M * 8;
+    int32_t* sid = reinterpret_cast<int32_t*>(smem + o);      // [k] ids ascending
+    int32_t* rowoff = sid + k;                                // [k + 1]
+    o = (o + (size_t)k * 4 + (size_t)(k + 1) * 4 + 15) / 16 * 16;
+    float* hid = reinterpret_cast<float*>(smem + o);          // [H]
+    uint32_t* pv = reinterpret_cast<uint32_t*>(hid + H);      // [G][kPartWords]
+
+    const int G = gridDim.x;
+    const uint32_t e = __builtin_amdgcn_readfirstlane(load_coherent(A.epoch)) + 1u;
+    const int lane = lane_id();
+    const int wv = threadIdx.x / kWave;
+    const int nw = G * kChainWaves;
+    const int gw = blockIdx.x * kChainWaves + wv;
+
+    // ---- loads that depend on nothing: x, h, the first W1 and W2 rows,
+    // offsets (h and the W2 row only while the registers allow: d <= 4096)
+    constexpr bool kEarly = NB <= 8;
+    Raw8<uint16_t> xv[NB], hv[NB], w2[NB];
+    auto load_h = [&]() {
+#pragma unroll
+        for (int blk = 0; blk < NB; ++blk) {
+            const int e = blk * 512 + lane * 8;
+            if (e < A.d) hv[blk].template load<false>(A.h + e);
+            else hv[blk].zero();
+        }
+    };
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk) {
+        const int e = blk * 512 + lane * 8;
+        if (e < A.d_r) xv[blk].template load<false>(A.x + e);
+        else xv[blk].zero();
+    }
+    if constexpr (kEarly) load_h();
+    const int n1 = H > 0 ? H : M;
+    Raw8<uint16_t> w1[NB];
+    if (gw < n1) load_bf16_row<NB>(w1, A.W1 + (int64_t)gw * A.d_r, A.d_r, lane);
+    if (kEarly && H > 0 && gw < M) load_bf16_row<NB>(w2, A.W2 + (int64_t)gw * H, H, lane);
+    for (int j = threadIdx.x; j <= M; j += kChainThreads) offs[j] = A.offsets[j];
+
+    // ---- stage 1: layer 1 (hidden units, or the scores of a linear router)
+    {
+        uint64_t* out = H > 0 ? A.thidden : A.tscores;
+        const int act = H > 0 ? A.act : DYNA_ACT_NONE;
+        for (int j = gw; j < n1; j += nw) {
+            if (j != gw) load_bf16_row<NB>(w1, A.W1 + (int64_t)j * A.d_r, A.d_r, lane);
+            const float s = dot_bf16<NB>(w1, xv);
+            if (lane == 0)
+                store_coherent(out + j, tagged(e, __float_as_uint(apply_act(s + (A.b1 ? A.b1[j] : 0.0f), act))));
+        }
+    }
+
+    // ---- stage 2: layer 2 over the hidden layer, polled into LDS
+    if (H > 0) {
+        poll_words<kChainThreads>(A, A.thidden, H, e, reinterpret_cast<uint32_t*>(hid));
+        __syncthreads();
+        for (int j = gw; j < M; j += nw) {
+            if (!kEarly || j != gw) load_bf16_row<NB>(w2, A.W2 + (int64_t)j * H, H, lane);
+            const float s = dot_lds<NB>(w2, hid, H, lane);
+            if (lane == 0) store_coherent(A.tscores + j, tagged(e, __float_as_uint(s + (A.b2 ? A.b2[j] : 0.0f))));
+        }
+    }
+
+    // ---- stage 3: top-k clusters and the shortlist, in every workgroup
+    float v[kSelQ];
+    {
+        uint32_t raw[kSelQ];
+        poll_own<kChainThreads, kSelQ>(A, A.tscores, M, e, raw);
+#pragma unroll
+        for (int q = 0; q < kSelQ; ++q) {
+            v[q] = __uint_as_float(raw[q]);
+            if ((int)threadIdx.x + kChainThreads * q < M) sv[threadIdx.x + kChainThreads * q] = v[q];
+        }
+    }
+    const int L = chain_select<kChainThreads>(v, offs, M, k, cand, sid, rowoff, A.err);
+    if (blockIdx.x == 0 && (A.out_clusters || A.topk_scores)) {
+        // rank order (score desc, id asc) by counting, for the outputs only
+        for (int i = threadIdx.x; i < k; i += kChainThreads) {
+            const int id = sid[i];
+            const uint64_t key = sel_key(sv[id], (uint32_t)id);
+            int rank = 0;
+            for (int j = 0; j < k; ++j) rank += sel_key(sv[sid[j]], (uint32_t)sid[j]) > key;
+            if (A.out_clusters) A.out_clusters[rank] = id;
+            if (A.topk_scores) A.topk_scores[rank] = sv[id];
+        }
+    }
+    if (blockIdx.x == 0) {
+        for (int i = threadIdx.x; i <= k; i += kChainThreads) {
+            if (i < k && A.sel_sorted) A.sel_sorted[i] = sid[i];
+            if (A.sel_rowoff) A.sel_rowoff[i] = rowoff[i];
+        }
+        if (threadIdx.x == 0 && A.row_len) A.row_len[0] = L;
+    }
+
+    // ---- stage 4: logits over the wave's contiguous range of shortlist slots
+    if constexpr (!kEarly) load_h();
+    GreedyState st;
+    {
+        const int64_t p0 = (int64_t)gw * L / nw, p1 = (int64_t)(gw + 1) * L / nw;
+        // cluster position of slot p0: the first i with rowoff[i + 1] > p0
+        int ci = 0;
+        if (p0 < p1) {
+            int lo = 0, hi = k - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (rowoff[mid + 1] > p0) hi = mid;
+                else lo = mid + 1;
+            }
+            ci = lo;
+        }
+        for (int64_t p = p0; p < p1; p += R) {
+            const int nrow = (int)min<int64_t>(R, p1 - p);
+            int64_t lrow[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int q = (int)p + min(r, nrow - 1);
+                while (q >= rowoff[ci + 1]) ++ci;
+                lrow[r] = (int64_t)offs[sid[ci]] + (q - rowoff[ci]);
+            }
+            Raw8<uint16_t> w[R][NB];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                if (r < nrow) load_bf16_row<NB>(w[r], A.W + lrow[r] * A.d, A.d, lane);
+                else
+#pragma unroll
+                    for (int blk = 0; blk < NB; ++blk) w[r][blk].zero();
+            }
+            int64_t my_row = lrow[0];
+#pragma unroll
+            for (int r = 1; r < R; ++r)
+                if (lane == r) my_row = lrow[r];
+            const bool own = lane < nrow;
+            const int32_t vid = own ? A.perm[my_row] : 0;
+            float acc[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r] = 0.0f;
+#pragma unroll
+            for (int blk = 0; blk < NB; ++blk)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float hj = hv[blk].at(j);
+#pragma unroll
+                    for (int r = 0; r < R; ++r) acc[r] = fmaf(w[r][blk].at(j), hj, acc[r]);
+                }
+            float mine = 0.0f;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const float t = wave_sum(acc[r]);
+                if (lane == r) mine = t;
+            }
+            if (own) {
+                if (A.out_logits) A.out_logits[p + lane] = mine;
+                st.add(mine, vid, A.inv_t);
+            }
+        }
+    }
+
+    // ---- stage 5: greedy partials; workgroup 0 polls and merges them
+    {
+        constexpr int NW = kChainWaves;
+        __shared__ uint64_t w_best[NW];
+        __shared__ float w_m[NW], w_s[NW];
+        const uint64_t wb = wave_max_u64(st.best);
+        const float wm = readlane_f32(wave_max_f32(st.m), kWave - 1);
+        const float wsum = wave_sum(st.m == -__builtin_inff() ? 0.0f : st.s * expf((st.m - wm) * A.inv_t));
+        if (lane == 0) {
+            w_best[wv] = wb;
+            w_m[wv] = wm;
+            w_s[wv] = wsum;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint64_t bb = w_best[0];
+            float bm = w_m[0], bs = w_s[0];
+            for (int q = 1; q < NW; ++q) {
+                bb = w_best[q] > bb ? w_best[q] : bb;
+                softmax_merge(bm, bs, w_m[q], w_s[q], A.inv_t);
+            }
+            uint64_t* pw = A.tpart + (int64_t)blockIdx.x * kPartWords;
+            store_coherent(pw + 0, tagged(e, (uint32_t)(bb >> 32)));
+            store_coherent(pw + 1, tagged(e, (uint32_t)bb));
+            store_coherent(pw + 2, tagged(e, __float_as_uint(bm)));
+            store_coherent(pw + 3, tagged(e, __float_as_uint(bs)));
+        }
+        if (blockIdx.x != 0) return;
+
+        // workgroup 0: thread t merges partials t, t + NT, ... in order, then a
+        // fixed-order wave and workgroup reduction
+        __syncthreads();
+        poll_words<kChainThreads>(A, A.tpart, G * kPartWords, e, pv);
+        __syncthreads();
+        uint64_t bb = 0;
+        float bm = -__builtin_inff(), bs = 0.0f;
+        for (int g = threadIdx.x; g < G; g += kChainThreads) {
+            const uint32_t* q = pv + g * kPartWords;
+            const uint64_t k2 = ((uint64_t)q[0] << 32) | q[1];
+            bb = k2 > bb ? k2 : bb;
+            softmax_merge(bm, bs, __uint_as_float(q[2]), __uint_as_float(q[3]), A.inv_t);
+        }
+        const uint64_t gb = wave_max_u64(bb);
+        const float gm = readlane_f32(wave_max_f32(bm), kWave - 1);
+        const float gs = wave_sum(bm == -__builtin_inff() ? 0.0f : bs * expf((bm - gm) * A.inv_t));
+        __syncthreads();
+        if (lane == 0) {
+            w_best[wv] = gb;
+            w_m[wv] = gm;
+            w_s[wv] = gs;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint64_t fb = w_best[0];
+            float fm = w_m[0], fs = w_s[0];
+            for (int q = 1; q < NW; ++q) {
+                fb = w_best[q] > fb ? w_best[q] : fb;
+                softmax_merge(fm, fs, w_m[q], w_s[q], A.inv_t);
+            }
+            // every workgroup has read the epoch (its partial carries it)
+            const bool err = load_coherent(A.err) != 0u;
+            if (err) {
+                store_coherent(A.err, 0u);
+                fb = 0;
+            }
+            store_coherent(A.epoch, e);
+            A.out_ids[0] = fb != 0 ? (int32_t)key_id(fb) : -1;
+            if (A.out_logprobs) {
+                const float lshift = (A.beta > 0.0f && (int64_t)A.V > L) ? log1pf(-A.beta) : 0.0f;
+                A.out_logprobs[0] = fb != 0 ? (key_val(fb) - fm) * A.inv_t - logf(fs) + lshift : -__builtin_inff();
+            }
+        }
+    }
+}
+
+template <int NB, int R>
+dyna_status launch_chain_nb(const ChainArgs& a, int grid, size_t lds, hipStream_t s) {
+    static std::atomic<bool> raised[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return set_error(DYNA_ERR_HIP, "one-launch step: no current device");
+    if (lds > 64 * 1024 && !raised[dev]) {
+        if (hipFuncSetAttribute(reinterpret_cast<const void*>(chain_step_kernel<NB, R>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+            return set_error(DYNA_ERR_UNSUPPORTED, "one-launch step needs %zu bytes of LDS", lds);
+        raised[dev] = true;
+    }
+    launch_timed_kernel(chain_step_kernel<NB, R>, dim3(grid), dim3(kChainThreads), (uint32_t)lds, s, a);
+    return check_launch("chain_step_kernel");
+}
+
+}  // namespace
+
+size_t chain_region_bytes(int32_t H, int32_t M) {
+    return 256 + (size_t)8 * (H + M) + (size_t)8 * kPartWords * kChainMaxGrid;
+}
+
+bool chain_step_eligible(const ChainRequest& q) {
+    const int kmax = std::max(q.d_r, std::max(q.H, q.d));
+    return q.all_bf16 && q.region != nullptr && kmax <= 8192 && q.M <= kChainMaxM &&
+           chain_lds_bytes(q.M, q.k, q.H, kChainMaxGrid) <= 160 * 1024;
+}
+
+dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
+    if (!chain_step_eligible(q)) return set_error(DYNA_ERR_UNSUPPORTED, "one-launch step: shape");
+    static std::atomic<int> cus[kMaxDevices] = {};
+    static std::atomic<int64_t> tick_khz[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return set_error(DYNA_ERR_HIP, "one-launch step: no current device");
+    if (cus[dev] == 0) {
+        int n = 0, khz = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0 ||
+            hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0)
+            return set_error(DYNA_ERR_HIP, "one-launch step: device attributes");
+        tick_khz[dev].store(khz);
+        cus[dev].store(n);
+    }
+    // one workgroup per compute unit by default: the hand-offs need every
+    // workgroup resident at once
+    const int opt = option_greedy_grid();
+    const int n_cu = cus[dev].load();
+    const int grid = std::max(1, std::min(opt > 0 ? opt : n_cu, std::min(2 * n_cu, kChainMaxGrid)));
+    ChainArgs a{};
+    a.W1 = static_cast<const uint16_t*>(q.W1);
+    a.b1 = q.b1;
+    a.W2 = static_cast<const uint16_t*>(q.W2);
+    a.b2 = q.b2;
+    a.d_r = q.d_r;
+    a.H = q.H;
+    a.M = q.M;
+    a.act = q.act;
+    a.x = static_cast<const uint16_t*>(q.x);
+    a.W = static_cast<const uint16_t*>(q.W);
+    a.perm = q.perm;
+    a.offsets = q.offsets;
+    a.d = q.d;
+    a.V = q.V;
+    a.h = static_cast<const uint16_t*>(q.h);
+    a.k = q.k;
+    {
+        char* r = static_cast<char*>(q.region);
+        a.epoch = reinterpret_cast<uint32_t*>(r);
+        a.err = reinterpret_cast<uint32_t*>(r + 4);
+        a.thidden = reinterpret_cast<uint64_t*>(r + 256);
+        a.tscores = a.thidden + q.H;
+        a.tpart = a.tscores + q.M;
+    }
+    a.out_clusters = q.out_clusters;
+    a.topk_scores = q.topk_scores;
+    a.sel_sorted = q.sel_sorted;
+    a.sel_rowoff = q.sel_rowoff;
+    a.row_len = q.row_len;
+    a.out_logits = q.out_logits;
+    a.out_ids = q.out_ids;
+    a.out_logprobs = q.out_logprobs;
+    a.inv_t = q.inv_t;
+    a.beta = q.beta;
+    // every wait is bounded by 0.2 s of wall clock
+    a.spin_ticks = (uint64_t)tick_khz[dev].load() * 200;
+    const size_t lds = chain_lds_bytes(q.M, q.k, q.H, grid);
+    const int nb = (std::max(q.d_r, std::max(q.H, q.d)) + 511) / 512;
+    if (nb <= 1) return launch_chain_nb<1, 4>(a, grid, lds, s);
+    if (nb <= 2) return launch_chain_nb<2, 4>(a, grid, lds, s);
+    if (nb <= 4) return launch_chain_nb<4, 4>(a, grid, lds, s);
+    if (nb <= 8) return launch_chain_nb<8, 4>(a, grid, lds, s);
+    if (nb <= 12) return launch_chain_nb<12, 2>(a, grid, lds, s);
+    return launch_chain_nb<16, 2>(a, grid, lds, s);
+}
+
+}  // namespace dyna

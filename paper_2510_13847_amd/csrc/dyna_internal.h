@@ -11,6 +11,7 @@
 namespace dyna {
 
 constexpr int kWave = 64;
+constexpr int kMaxDevices = 64;   // per-device tables of the library
 constexpr int kMfmaRows = 16;     // rows of one MFMA A tile
 // Layout rows per work chunk of the gathered head: one MFMA tile, so every
 // chunk is a full work item of equal cost (partial only at a cluster's end).
@@ -255,6 +256,37 @@ constexpr int kGreedyMaxBlocks = 4096;
 size_t greedy_partials_bytes();
 dyna_status launch_logits_greedy(const RowdotArgs& lg, const SelectArgs& sa, void* partials,
                                  int32_t* counter, hipStream_t s);
+
+// chain.hip (one context, greedy, bf16 throughout): the whole step in one
+// launch, handing words between workgroups through an epoch-tagged region.
+struct ChainRequest {
+    bool all_bf16;  // router weights, LM head, x and h all bf16
+    const void* W1;
+    const float* b1;
+    const void* W2;
+    const float* b2;
+    int32_t d_r, H, M, act;
+    const void* x;
+    const void* W;
+    const int32_t* perm;
+    const int32_t* offsets;
+    int32_t d, V;
+    const void* h;
+    int32_t k;
+    void* region;  // chain_region_bytes(H, M) of workspace, zero-filled before first use
+    int32_t* out_clusters;
+    float* topk_scores;
+    int32_t* sel_sorted;
+    int32_t* sel_rowoff;
+    int32_t* row_len;
+    float* out_logits;
+    int32_t* out_ids;
+    float* out_logprobs;
+    float inv_t, beta;
+};
+size_t chain_region_bytes(int32_t H, int32_t M);
+bool chain_step_eligible(const ChainRequest& q);
+dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s);
 
 // Global options (dyna_set_option).
 int option_logits_path();

@@ -12,53 +12,27 @@
 // grid-wide wait and no L2 write-back is involved.  The arrival counter is
 // cleared by the step's first kernel and by the last workgroup after use.
 #include "gemv.h"
+#include "greedy.h"
 #include "select_row.h"
 
 namespace dyna {
 namespace {
 
-constexpr int kGreedyGrid = 256;  // default workgroups of the fused head (one arrival each)
-
-struct GreedyPartial {
-    uint64_t key;  // best (ordered logit, inverted vocabulary id)
-    float m;       // max logit
-    float s;       // sum of exp((z - m) / T)
-};
-
-// Online softmax pair merge (m, s) <- (m, s) (+) (m2, s2).
-__device__ __forceinline__ void softmax_merge(float& m, float& s, float m2, float s2, float inv_t) {
-    if (m2 == -__builtin_inff()) return;
-    if (m == -__builtin_inff()) {
-        m = m2;
-        s = s2;
-        return;
-    }
-    const float M = fmaxf(m, m2);
-    s = s * expf((m - M) * inv_t) + s2 * expf((m2 - M) * inv_t);
-    m = M;
-}
+constexpr int kGreedyGrid = 256;  // default workgroups of the fused one-context head (one arrival each)
 
 struct GreedyEpi {
     float inv_t;
-    uint64_t best = 0;
-    float m = -__builtin_inff();
-    float s = 0.0f;
+    GreedyState st;
     __device__ __forceinline__ void put(const RowdotArgs& a, int64_t o, float value, int32_t vid) {
         a.out[o] = value;
         if (a.vid_out) a.vid_out[o] = vid;
-        const float z = value != value ? -__builtin_inff() : value;
-        const uint64_t key = sel_key(z, (uint32_t)vid);
-        best = key > best ? key : best;
-        softmax_merge(m, s, z, 1.0f, inv_t);
+        st.add(value, vid, inv_t);
     }
 };
 
 template <typename WT, typename VT, int NB, int R>
 __global__ __launch_bounds__(kThreads) void logits_greedy_kernel(RowdotArgs lg, SelectArgs sa,
                                                                  GreedyPartial* part, int32_t* counter) {
-    __shared__ uint64_t w_best[kWavesPerBlock];
-    __shared__ float w_m[kWavesPerBlock], w_s[kWavesPerBlock];
-    __shared__ int last;
     const int64_t n_items = (int64_t)lg.plan.hdr->n_chunks * (kChunkRows / R);
     // workgroups whose first wave has an item take part (at least workgroup 0)
     const int64_t n_part = std::max<int64_t>(
@@ -68,69 +42,15 @@ __global__ __launch_bounds__(kThreads) void logits_greedy_kernel(RowdotArgs lg, 
     GreedyEpi epi{sa.inv_t};
     gemv_rows<WT, VT, NB, true, R, true, GreedyEpi>(lg, epi);
 
-    // wave, then workgroup reduction in a fixed order
-    const int lane = lane_id(), w = threadIdx.x / kWave;
-    const uint64_t wb = wave_max_u64(epi.best);
-    float m = epi.m, s = epi.s;
-    const float wm = readlane_f32(wave_max_f32(m), kWave - 1);
-    const float ws = wave_sum(m == -__builtin_inff() ? 0.0f : s * expf((m - wm) * sa.inv_t));
-    if (lane == 0) {
-        w_best[w] = wb;
-        w_m[w] = wm;
-        w_s[w] = ws;
-    }
-    __syncthreads();
+    GreedyState f;
+    if (!greedy_publish_merge<kThreads>(epi.st, sa.inv_t, part, blockIdx.x, (int)n_part, counter, &f)) return;
     if (threadIdx.x == 0) {
-        uint64_t bb = w_best[0];
-        float bm = w_m[0], bs = w_s[0];
-        for (int q = 1; q < kWavesPerBlock; ++q) {
-            bb = w_best[q] > bb ? w_best[q] : bb;
-            softmax_merge(bm, bs, w_m[q], w_s[q], sa.inv_t);
-        }
-        store_coherent(&part[blockIdx.x].key, bb);
-        store_coherent(&part[blockIdx.x].m, bm);
-        store_coherent(&part[blockIdx.x].s, bs);
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        __builtin_amdgcn_s_waitcnt(0);
-        last = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-               (int)n_part - 1;
-    }
-    __syncthreads();
-    if (!last) return;
-
-    // last workgroup: thread t merges partials t, t + 256, ... in order, then
-    // a fixed-order wave and workgroup reduction
-    if (threadIdx.x == 0) store_coherent(counter, 0);
-    uint64_t bb = 0;
-    float bm = -__builtin_inff(), bs = 0.0f;
-    for (int64_t g = threadIdx.x; g < n_part; g += kThreads) {
-        const uint64_t k2 = load_coherent(&part[g].key);
-        const float m2 = load_coherent(&part[g].m), s2 = load_coherent(&part[g].s);
-        bb = k2 > bb ? k2 : bb;
-        softmax_merge(bm, bs, m2, s2, sa.inv_t);
-    }
-    const uint64_t gb = wave_max_u64(bb);
-    const float gm = readlane_f32(wave_max_f32(bm), kWave - 1);
-    const float gs = wave_sum(bm == -__builtin_inff() ? 0.0f : bs * expf((bm - gm) * sa.inv_t));
-    __syncthreads();
-    if (lane == 0) {
-        w_best[w] = gb;
-        w_m[w] = gm;
-        w_s[w] = gs;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint64_t fb = w_best[0];
-        float fm = w_m[0], fs = w_s[0];
-        for (int q = 1; q < kWavesPerBlock; ++q) {
-            fb = w_best[q] > fb ? w_best[q] : fb;
-            softmax_merge(fm, fs, w_m[q], w_s[q], sa.inv_t);
-        }
+        const uint64_t fb = f.best;
         if (sa.out_ids) sa.out_ids[0] = fb != 0 ? (int32_t)key_id(fb) : -1;
         if (sa.out_logprobs) {
             const TailMix tail = tail_of(sa, sa.row_len ? sa.row_len[0] : sa.fixed_len);
             sa.out_logprobs[0] =
-                fb != 0 ? (key_val(fb) - fm) * sa.inv_t - logf(fs) + tail.lshift : -__builtin_inff();
+                fb != 0 ? (key_val(fb) - f.m) * sa.inv_t - logf(f.s) + tail.lshift : -__builtin_inff();
         }
     }
 }

@@ -50,59 +50,15 @@ __host__ __device__ inline size_t topk_lds_bytes(int M, int k) {
            (size_t)2 * k * sizeof(int32_t);
 }
 
-// Row b of the selection, by one workgroup of kTopkThreads threads; `smem`
-// holds topk_lds_bytes(M, k) bytes of LDS.
-__device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
-    const int M = A.M, k = A.k;
-    const float* __restrict__ scores = A.scores;
-    int32_t* __restrict__ topk_ids = A.topk_ids;
-    float* __restrict__ topk_scores = A.topk_scores;
-    const int32_t* __restrict__ offsets = A.offsets;
-    int32_t* __restrict__ sel_sorted = A.sel_sorted;
-    int32_t* __restrict__ sel_rowoff = A.sel_rowoff;
-    int32_t* __restrict__ row_len = A.row_len;
-    const Plan& plan = A.plan;
-    float* sv = reinterpret_cast<float*>(smem);                       // [M] raw scores
-    int32_t* offs = reinterpret_cast<int32_t*>(sv + M);                // [M + 1]
-    uint64_t* sel = reinterpret_cast<uint64_t*>(smem + ((size_t)(2 * M + 1) * 4 + 7) / 8 * 8);  // [k]
-    uint64_t* cand = sel + k;                                          // [M] tie candidates
-    int32_t* sid = reinterpret_cast<int32_t*>(cand + M);               // [k] ids ascending
-    int32_t* ssize = sid + k;                                          // [k]
+// The k best of the M scores sv[] (LDS) by (score desc, id asc), by one
+// workgroup of kNT threads.  On return (after a barrier) sel[0..k) holds the
+// k selection keys in no particular order, and the int32 arrays rk = (int32_t*)cand
+// and ik = rk + k hold, for each key, its rank and its position in ascending
+// id order.  `cand` is LDS scratch of M keys.
+__device__ void topk_core(const float* sv, int M, int k, uint64_t* sel, uint64_t* cand) {
     __shared__ int hist[256], hist2[256];
-    __shared__ int tmp[kNT / kWave + 1];
     __shared__ uint32_t sh_prefix;
     __shared__ int sh_krem, sh_nsel, sh_ncand;
-
-    // stage scores (and offsets) with kStagePer loads in flight per thread
-    const float* s = scores + (int64_t)b * M;
-    for (int j0 = 0; j0 < M; j0 += kNT * kStagePer) {
-        float x[kStagePer];
-#pragma unroll
-        for (int q = 0; q < kStagePer; ++q) {
-            const int j = j0 + q * kNT + threadIdx.x;
-            x[q] = j < M ? s[j] : 0.0f;
-        }
-#pragma unroll
-        for (int q = 0; q < kStagePer; ++q) {
-            const int j = j0 + q * kNT + threadIdx.x;
-            if (j < M) sv[j] = x[q];
-        }
-    }
-    if (sel_sorted != nullptr) {
-        for (int j0 = 0; j0 <= M; j0 += kNT * kStagePer) {
-            int x[kStagePer];
-#pragma unroll
-            for (int q = 0; q < kStagePer; ++q) {
-                const int j = j0 + q * kNT + threadIdx.x;
-                x[q] = j <= M ? offsets[j] : 0;
-            }
-#pragma unroll
-            for (int q = 0; q < kStagePer; ++q) {
-                const int j = j0 + q * kNT + threadIdx.x;
-                if (j <= M) offs[j] = x[q];
-            }
-        }
-    }
     hist[threadIdx.x] = 0;
     hist2[threadIdx.x] = 0;
     if (threadIdx.x == 0) {
@@ -175,6 +131,61 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
         }
     }
     __syncthreads();
+}
+
+// Row b of the selection, by one workgroup of kTopkThreads threads; `smem`
+// holds topk_lds_bytes(M, k) bytes of LDS.
+__device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
+    const int M = A.M, k = A.k;
+    const float* __restrict__ scores = A.scores;
+    int32_t* __restrict__ topk_ids = A.topk_ids;
+    float* __restrict__ topk_scores = A.topk_scores;
+    const int32_t* __restrict__ offsets = A.offsets;
+    int32_t* __restrict__ sel_sorted = A.sel_sorted;
+    int32_t* __restrict__ sel_rowoff = A.sel_rowoff;
+    int32_t* __restrict__ row_len = A.row_len;
+    const Plan& plan = A.plan;
+    float* sv = reinterpret_cast<float*>(smem);                       // [M] raw scores
+    int32_t* offs = reinterpret_cast<int32_t*>(sv + M);                // [M + 1]
+    uint64_t* sel = reinterpret_cast<uint64_t*>(smem + ((size_t)(2 * M + 1) * 4 + 7) / 8 * 8);  // [k]
+    uint64_t* cand = sel + k;                                          // [M] tie candidates
+    int32_t* sid = reinterpret_cast<int32_t*>(cand + M);               // [k] ids ascending
+    int32_t* ssize = sid + k;                                          // [k]
+    __shared__ int tmp[kNT / kWave + 1];
+
+    // stage scores (and offsets) with kStagePer loads in flight per thread
+    const float* s = scores + (int64_t)b * M;
+    for (int j0 = 0; j0 < M; j0 += kNT * kStagePer) {
+        float x[kStagePer];
+#pragma unroll
+        for (int q = 0; q < kStagePer; ++q) {
+            const int j = j0 + q * kNT + threadIdx.x;
+            x[q] = j < M ? s[j] : 0.0f;
+        }
+#pragma unroll
+        for (int q = 0; q < kStagePer; ++q) {
+            const int j = j0 + q * kNT + threadIdx.x;
+            if (j < M) sv[j] = x[q];
+        }
+    }
+    if (sel_sorted != nullptr) {
+        for (int j0 = 0; j0 <= M; j0 += kNT * kStagePer) {
+            int x[kStagePer];
+#pragma unroll
+            for (int q = 0; q < kStagePer; ++q) {
+                const int j = j0 + q * kNT + threadIdx.x;
+                x[q] = j <= M ? offsets[j] : 0;
+            }
+#pragma unroll
+            for (int q = 0; q < kStagePer; ++q) {
+                const int j = j0 + q * kNT + threadIdx.x;
+                if (j <= M) offs[j] = x[q];
+            }
+        }
+    }
+    topk_core(sv, M, k, sel, cand);
+    const int32_t* rk = reinterpret_cast<const int32_t*>(cand);
+    const int32_t* ik = rk + k;
     for (int i = threadIdx.x; i < k; i += kNT) {
         const uint32_t id = key_id(sel[i]);
         const int rank = rk[i], idrank = ik[i];

@@ -229,9 +229,10 @@ def workspace_bytes(layout: Optional[Layout], router: Optional[Router], B: int, 
 
 
 def workspace(layout, router, B, k, cap, device="cuda"):
+    """Zero-filled workspace (the one-context kernels' counters start at zero)."""
     import torch
     n = workspace_bytes(layout, router, B, k, cap)
-    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
 
 
 def route(router: Router, x, k: int, ws=None, want_scores=False, stream=None):

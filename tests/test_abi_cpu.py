@@ -47,6 +47,9 @@ def test_set_option_validation():
     assert lib.dyna_set_option(D.OPT_UNION_CFG, 0) == D.OK
     assert lib.dyna_set_option(D.OPT_KMEANS_CFG, 5) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_KMEANS_CFG, 0) == D.OK
+    assert lib.dyna_set_option(D.OPT_FUSED_B1, 3) == D.ERR_INVALID_ARG
+    for v in (2, 1, 0):
+        assert lib.dyna_set_option(D.OPT_FUSED_B1, v) == D.OK
 
 
 def _layout(V=1000, d=64, M=10, cap=None, W=0x1000):

@@ -681,11 +681,15 @@ FUSED_CASES = [c for c in CASES if c.B == 1] + [
 
 
 @pytest.mark.parametrize("temperature", [1.0, 0.6])
+@pytest.mark.parametrize("fused_opt", [0, 2], ids=["one_launch", "four_launches"])
 @pytest.mark.parametrize("w", FUSED_CASES, ids=lambda w: w.name)
-def test_fused_greedy_matches_separate_kernels(w, temperature):
-    """A greedy one-context step folds the selection into the gathered head;
-    its token must equal the separate kernels' exactly and its log-probability
-    within rounding, call after call (the arrival counter resets itself)."""
+def test_fused_greedy_matches_separate_kernels(w, temperature, fused_opt):
+    """A greedy one-context step folds the selection into the gathered head
+    (four launches), or runs the whole step as one launch; its clusters,
+    logits and token must equal the separate kernels' exactly and its
+    log-probability within rounding, call after call (the arrival counters
+    reset themselves).  The call with a second routing stream takes the
+    four-launch form."""
     p = Problem(w)
     mode = D.SEL_ARGMAX
     fused = D.DraftHead(p.R, p.L, 1, w.k, mode, 1, temperature, keep_logits=True)
@@ -693,9 +697,10 @@ def test_fused_greedy_matches_separate_kernels(w, temperature):
     side = torch.cuda.Stream()
     for it, rs in enumerate([None, None, side, None, None]):
         x = W.contexts(w, "cpu", salt=it).to(DEV)
-        fused(x, x, route_stream=rs)
-        D.set_option(D.OPT_FUSED_B1, 1)
+        D.set_option(D.OPT_FUSED_B1, fused_opt)
         try:
+            fused(x, x, route_stream=rs)
+            D.set_option(D.OPT_FUSED_B1, 1)
             sep(x, x, route_stream=rs)
         finally:
             D.set_option(D.OPT_FUSED_B1, 0)
@@ -711,3 +716,44 @@ def test_fused_greedy_matches_separate_kernels(w, temperature):
         r = O.draft_select(z, vids, 1, temperature)
         assert int(fused.ids[0, 0]) == int(r["ids"][0])
         PC.assert_close(fused.logprobs[0].cpu().numpy(), r["logprobs"], PC.LOGPROB_TOL, "lp oracle")
+
+
+@pytest.mark.parametrize("variant", ["tied_rows", "zero_router"])
+def test_one_launch_step_ties(variant):
+    """Router scores with exact ties across the k-th place (layer-2 rows 3..M-1
+    all equal, so 61 clusters tie and k = 7 always cuts into them), or all
+    equal (a zero router): the one-launch step's selection must break them
+    toward the lower cluster id exactly as the separate kernels do."""
+    w = case("ties_b1", V=4000, d=256, M=64, H=32, k=7, B=1)
+    p = Problem(w)
+    W2 = p.W2.clone()
+    if variant == "tied_rows":
+        W2[3:] = W2[3]
+    else:
+        W2.zero_()
+    R = D.Router(p.W1.to(DEV), W2.to(DEV), act=w.act)
+    mode = D.SEL_ARGMAX
+    one = D.DraftHead(R, p.L, 1, w.k, mode, 1, keep_logits=True)
+    sep = D.DraftHead(R, p.L, 1, w.k, mode, 1, keep_logits=True)
+    for it in range(4):
+        x = W.contexts(w, "cpu", salt=it).to(DEV)
+        D.set_option(D.OPT_FUSED_B1, 0)
+        try:
+            one(x, x)
+            D.set_option(D.OPT_FUSED_B1, 1)
+            sep(x, x)
+        finally:
+            D.set_option(D.OPT_FUSED_B1, 0)
+        torch.cuda.synchronize()
+        assert torch.equal(one.clusters, sep.clusters)
+        assert torch.equal(one.ids, sep.ids)
+        vids = O.shortlist(one.clusters[0].cpu().numpy(), p.offsets, p.perm)[3]
+        assert torch.equal(one.logits[:, :len(vids)], sep.logits[:, :len(vids)])
+        got = one.clusters[0].cpu().tolist()
+        if variant == "zero_router":
+            # every score is 0: the k lowest cluster ids, in id order
+            assert got == list(range(w.k))
+        else:
+            # the tied clusters taken are the lowest ids of the tied run
+            tied = sorted(c for c in got if c >= 3)
+            assert tied == list(range(3, 3 + len(tied)))
