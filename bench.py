@@ -159,7 +159,7 @@ def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20):
             "routing_hidden_frac": round(max(0.0, t_s - t_o) / t_r, 3) if t_r > 0 else None}
 
 
-KERNEL_UNITS = {"chain_step_kernel": "chain.hip", "logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip", "union_gemm_kernel": "gather.hip",
+KERNEL_UNITS = {"chain_step_kernel": "chain.hip", "logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip", "gather_ring_kernel": "gather.hip", "union_gemm_kernel": "gather.hip",
                 "rowdot_gemv_kernel": "rowdot.hip"}
 
 
@@ -194,7 +194,7 @@ def dominant_kernel(w):
     if w.union and w.dtype == "bf16":
         return "union_gemm_kernel", "union head: dense LDS-staged MFMA product of the union slabs with every context"
     if w.dtype == "bf16" and w.B > 4:
-        return "gather_lds_kernel", "gathered head, LDS-staged MFMA tiles"
+        return "gather_ring_kernel", "gathered head, MFMA tiles with the slab rows staged through LDS"
     return "rowdot_gemv_kernel", "gathered head, wave-per-row GEMV"
 
 

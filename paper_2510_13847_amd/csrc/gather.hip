@@ -282,6 +282,183 @@ __global__ __launch_bounds__(NW * kWave) void gather_lds_kernel(RowdotArgs a) {
     }
 }
 
+// The same work units with only the slab rows (A) in the LDS ring and the
+// context columns (B) loaded straight into registers: the contexts of a
+// step stay in L2, and keeping them out of LDS leaves the whole ring to the
+// slab rows, so each wave keeps more HBM bytes in flight.  Every stage
+// issues exactly NA direct-to-LDS loads and STEPS register loads (lanes
+// whose column has no context read context 0 and are zeroed when used), so
+// the wave can wait for a stage with one counter value; the loop is unrolled
+// by the ring depth so that a stage's B registers have fixed names.
+template <int NW, int S, int KB>
+__global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
+    constexpr int NC = 16;
+    constexpr int ROWB = KB * 2;
+    constexpr int PIECES = ROWB / 16;
+    constexpr int RPI = kWave / PIECES;
+    constexpr int NA = kMfmaRows / RPI;
+    constexpr int STAGE = kMfmaRows * ROWB;
+    constexpr int STEPS = KB / 32;
+    constexpr int PER_STAGE = NA + STEPS;  // vector-memory instructions per stage
+    static_assert(PIECES <= kWave && kWave % PIECES == 0 && kMfmaRows % RPI == 0, "stage shape");
+    static_assert((S - 1) * PER_STAGE <= 63, "ring depth beyond the load counter");
+
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int lane = lane_id();
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    char* ring = smem + wv * (S * STAGE);
+    const int K = a.K;
+    const int nkb = (K + KB - 1) / KB;
+    const uint16_t* __restrict__ W = static_cast<const uint16_t*>(a.W);
+    const uint16_t* __restrict__ v = static_cast<const uint16_t*>(a.v);
+    const int64_t n_items = (int64_t)((sptr<int32_t>)a.plan.hdr)[0];
+    const int64_t stride = (int64_t)gridDim.x * NW;
+
+    const int lsub = lane / PIECES, lpc = lane % PIECES;
+    const int col = lane & 15, kq = lane >> 4;
+
+    Unit iu;
+    iu.it = (int64_t)blockIdx.x * NW + wv;
+    find_tile(iu, a.plan, n_items, stride);
+    if (!iu.valid) return;
+    Unit cu = iu;
+
+    // issue side: this lane's context row (context 0 for an empty column)
+    const uint16_t* bsrc = v;
+    auto issue_group = [&]() {
+        int vb, vs;
+        const int n = group_entries<NC>(iu, a.plan, vb, vs);
+        const int b = from_lane(vb, col);
+        bsrc = v + (int64_t)(col < n ? b : 0) * K;
+    };
+    // consume side
+    int ncols = 0;
+    int64_t obase = 0;
+    int32_t vid[4] = {0, 0, 0, 0};
+    auto consume_group = [&]() {
+        int vb, vs;
+        ncols = group_entries<NC>(cu, a.plan, vb, vs);
+        obase = (int64_t)from_lane(vb, col) * a.ld + from_lane(vs, col) + cu.r0;
+        if (a.vid_out != nullptr && cu.g == 0) {
+            sptr<int32_t> P = (sptr<int32_t>)a.perm + cu.r0;
+            int vp = P[0];
+            if (cu.nrows == kMfmaRows) {
+#pragma unroll
+                for (int j = 1; j < kMfmaRows; ++j) vp = set_lane(vp, P[j], j);
+            } else {
+#pragma unroll
+                for (int j = 1; j < kMfmaRows; ++j)
+                    if (j < cu.nrows) vp = set_lane(vp, P[j], j);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) vid[r] = from_lane(vp, 4 * kq + r);
+        }
+    };
+
+    u32x4 bq[S][STEPS];
+    auto issue = [&](int slot, u32x4 (&bs)[STEPS]) {
+        char* dst = ring + slot * STAGE;
+        const int kb = iu.kb;
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int row = RPI * i + lsub;
+            const int piece = lpc ^ (row % PIECES);
+            int e = kb * KB + piece * 8;
+            e = e < K ? e : 0;  // k tail: any in-bounds piece; zeroed when read
+            const uint16_t* src = W + (int64_t)(iu.r0 + min(row, iu.nrows - 1)) * K + e;
+            __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0, 0);
+        }
+#pragma unroll
+        for (int st = 0; st < STEPS; ++st) {
+            int e = kb * KB + (st * 4 + kq) * 8;
+            e = e < K ? e : 0;
+            bs[st] = *reinterpret_cast<const u32x4*>(bsrc + e);
+        }
+    };
+
+    issue_group();
+    consume_group();
+#pragma unroll
+    for (int st = 0; st < S - 1; ++st) {
+        if (iu.valid) {
+            issue(st, bq[st]);
+            if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) issue_group();
+        }
+    }
+
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    bool done = false;
+    while (!done) {
+#pragma unroll
+        for (int u = 0; u < S; ++u) {
+            if (iu.valid) {
+                issue((u + S - 1) % S, bq[(u + S - 1) % S]);
+                if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) issue_group();
+                // the stage's loads are done once at most the S - 1 later
+                // stages are outstanding
+                wait_vmem<(S - 1) * PER_STAGE>();
+            } else {
+                wait_vmem<0>();
+            }
+            const char* st = ring + u * STAGE;
+            const int k0 = cu.kb * KB;
+#pragma unroll
+            for (int s2 = 0; s2 < STEPS; ++s2) {
+                const int p = s2 * 4 + kq;
+                u32x4 av = *reinterpret_cast<const u32x4*>(st + col * ROWB + (p ^ (col % PIECES)) * 16);
+                u32x4 bv = bq[u][s2];
+                if (col >= ncols) bv = u32x4{0u, 0u, 0u, 0u};
+                if (k0 + p * 8 >= K) {
+                    av = u32x4{0u, 0u, 0u, 0u};
+                    bv = u32x4{0u, 0u, 0u, 0u};
+                }
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
+                                                              __builtin_bit_cast(bf16x8, bv), acc, 0, 0, 0);
+            }
+            if (cu.kb == nkb - 1) {
+                if (col < ncols) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int row = 4 * kq + r;
+                        if (row < cu.nrows) {
+                            a.out[obase + row] = acc[r];
+                            if (a.vid_out != nullptr) a.vid_out[obase + row] = vid[r];
+                        }
+                    }
+                }
+                acc = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+            if (advance<NC>(cu, nkb, a.plan, n_items, stride)) {
+                if (!cu.valid) {
+                    done = true;
+                    break;
+                }
+                consume_group();
+            }
+        }
+    }
+}
+
+template <int NW, int S, int KB>
+dyna_status launch_ring_cfg(const RowdotArgs& a, hipStream_t stream) {
+    constexpr int LDS = NW * S * kMfmaRows * KB * 2;
+    static_assert(LDS <= 160 * 1024, "LDS per block");
+    static std::atomic<uint64_t> allowed{0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "gather: device");
+    if (!(allowed.load() & (1ull << dev))) {
+        if (hipFuncSetAttribute((const void*)gather_ring_kernel<NW, S, KB>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, LDS) != hipSuccess)
+            return set_error(DYNA_ERR_HIP, "gather: LDS attribute");
+        allowed.fetch_or(1ull << dev);
+    }
+    const int per_cu = (160 * 1024) / LDS;
+    const int64_t items = (int64_t)a.max_chunks_bound;
+    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + NW - 1) / NW, 256 * per_cu));
+    launch_timed_kernel(gather_ring_kernel<NW, S, KB>, dim3((unsigned)blocks), dim3(NW * kWave), LDS, stream, a);
+    return check_launch("gather_ring_kernel");
+}
+
 template <int NW, int S, int KB, int NC>
 dyna_status launch_cfg(const RowdotArgs& a, hipStream_t stream) {
     constexpr int ROWB = KB * 2, PIECES = ROWB / 16, RPI = kWave / PIECES;
@@ -680,6 +857,7 @@ bool gather_lds_eligible(const RowdotArgs& a) {
 dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
     if (!gather_lds_eligible(a)) return set_error(DYNA_ERR_UNSUPPORTED, "gather: needs bf16 plan mode");
     switch (option_gather_cfg()) {
+        case 1: return launch_cfg<4, 4, 128, 16>(a, stream);
         case 2: return launch_cfg<4, 3, 256, 8>(a, stream);
         case 3: return launch_cfg<4, 3, 128, 8>(a, stream);
         case 4: return launch_cfg<2, 8, 128, 16>(a, stream);
@@ -688,7 +866,11 @@ dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
         case 7: return launch_cfg<8, 3, 128, 8>(a, stream);
         case 8: return launch_cfg<4, 2, 512, 4>(a, stream);
         case 9: return launch_cfg<3, 2, 512, 8>(a, stream);
-        default: return launch_cfg<4, 4, 128, 16>(a, stream);
+        case 10: return launch_ring_cfg<4, 2, 512>(a, stream);
+        case 11: return launch_ring_cfg<2, 4, 256>(a, stream);
+        case 12: return launch_ring_cfg<4, 8, 128>(a, stream);
+        case 13: return launch_ring_cfg<8, 8, 64>(a, stream);
+        default: return launch_ring_cfg<4, 4, 256>(a, stream);
     }
 }
 
