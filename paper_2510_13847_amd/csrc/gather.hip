@@ -323,13 +323,27 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
     if (!iu.valid) return;
     Unit cu = iu;
 
-    // issue side: this lane's context row (context 0 for an empty column)
+    // issue side: this lane's context row; lanes whose column has no context
+    // load nothing (their output column is never stored, so whatever their
+    // registers hold is harmless), which keeps L2 traffic to the used columns
     const uint16_t* bsrc = v;
+    bool bcol = false;
     auto issue_group = [&]() {
         int vb, vs;
         const int n = group_entries<NC>(iu, a.plan, vb, vs);
         const int b = from_lane(vb, col);
-        bsrc = v + (int64_t)(col < n ? b : 0) * K;
+        bcol = col < n;
+        bsrc = v + (int64_t)(bcol ? b : 0) * K + kq * 8;
+    };
+    // issue side: this lane's source of each A instruction of a stage, at k 0
+    const uint16_t* arow[NA];
+    auto set_rows = [&]() {
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int row = RPI * i + lsub;
+            const int piece = lpc ^ (row % PIECES);
+            arow[i] = W + (int64_t)(iu.r0 + min(row, iu.nrows - 1)) * K + piece * 8;
+        }
     };
     // consume side
     int ncols = 0;
@@ -358,42 +372,67 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
     u32x4 bq[S][STEPS];
     auto issue = [&](int slot, u32x4 (&bs)[STEPS]) {
         char* dst = ring + slot * STAGE;
-        const int kb = iu.kb;
+        const int k0 = iu.kb * KB;
+        if (k0 + KB <= K) {
 #pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            const int row = RPI * i + lsub;
-            const int piece = lpc ^ (row % PIECES);
-            int e = kb * KB + piece * 8;
-            e = e < K ? e : 0;  // k tail: any in-bounds piece; zeroed when read
-            const uint16_t* src = W + (int64_t)(iu.r0 + min(row, iu.nrows - 1)) * K + e;
-            __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0, 0);
+            for (int i = 0; i < NA; ++i)
+                __builtin_amdgcn_global_load_lds((glb_ptr)(arow[i] + k0), (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0, 0);
+            if (bcol) {
+#pragma unroll
+                for (int st = 0; st < STEPS; ++st)
+                    bs[st] = *reinterpret_cast<const u32x4*>(bsrc + k0 + st * 32);
+            }
+        } else {
+            // k tail: pieces past K read an in-bounds piece; both operands of
+            // those pieces are zeroed when the stage is consumed
+#pragma unroll
+            for (int i = 0; i < NA; ++i) {
+                const int row = RPI * i + lsub;
+                const int piece = lpc ^ (row % PIECES);
+                const int off = k0 + piece * 8 < K ? k0 : -piece * 8;
+                __builtin_amdgcn_global_load_lds((glb_ptr)(arow[i] + off), (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0,
+                                                 0);
+            }
+            if (bcol) {
+#pragma unroll
+                for (int st = 0; st < STEPS; ++st) {
+                    const bool in = k0 + st * 32 + kq * 8 < K;
+                    bs[st] = *reinterpret_cast<const u32x4*>(bsrc + (in ? k0 + st * 32 : -kq * 8));
+                }
+            }
         }
-#pragma unroll
-        for (int st = 0; st < STEPS; ++st) {
-            int e = kb * KB + (st * 4 + kq) * 8;
-            e = e < K ? e : 0;
-            bs[st] = *reinterpret_cast<const u32x4*>(bsrc + e);
+    };
+
+    // next stage of the issue side: the context group (and, on a new chunk,
+    // the rows) follow the cursor
+    auto advance_issue = [&]() {
+        if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) {
+            issue_group();
+            if (iu.g == 0) set_rows();
         }
     };
 
     issue_group();
+    set_rows();
     consume_group();
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) {
         if (iu.valid) {
             issue(st, bq[st]);
-            if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) issue_group();
+            advance_issue();
         }
     }
 
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    // two accumulators take alternate k steps, so consecutive MFMAs do not
+    // wait on each other
+    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
     bool done = false;
     while (!done) {
 #pragma unroll
         for (int u = 0; u < S; ++u) {
             if (iu.valid) {
                 issue((u + S - 1) % S, bq[(u + S - 1) % S]);
-                if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) issue_group();
+                advance_issue();
                 // the stage's loads are done once at most the S - 1 later
                 // stages are outstanding
                 wait_vmem<(S - 1) * PER_STAGE>();
@@ -402,18 +441,22 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
             }
             const char* st = ring + u * STAGE;
             const int k0 = cu.kb * KB;
+            const bool tail = k0 + KB > K;
 #pragma unroll
             for (int s2 = 0; s2 < STEPS; ++s2) {
                 const int p = s2 * 4 + kq;
                 u32x4 av = *reinterpret_cast<const u32x4*>(st + col * ROWB + (p ^ (col % PIECES)) * 16);
                 u32x4 bv = bq[u][s2];
-                if (col >= ncols) bv = u32x4{0u, 0u, 0u, 0u};
-                if (k0 + p * 8 >= K) {
+                if (tail && k0 + p * 8 >= K) {
                     av = u32x4{0u, 0u, 0u, 0u};
                     bv = u32x4{0u, 0u, 0u, 0u};
                 }
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
-                                                              __builtin_bit_cast(bf16x8, bv), acc, 0, 0, 0);
+                if (s2 & 1)
+                    acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
+                                                                   __builtin_bit_cast(bf16x8, bv), acc1, 0, 0, 0);
+                else
+                    acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
+                                                                   __builtin_bit_cast(bf16x8, bv), acc0, 0, 0, 0);
             }
             if (cu.kb == nkb - 1) {
                 if (col < ncols) {
@@ -421,12 +464,13 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
                     for (int r = 0; r < 4; ++r) {
                         const int row = 4 * kq + r;
                         if (row < cu.nrows) {
-                            a.out[obase + row] = acc[r];
+                            a.out[obase + row] = acc0[r] + acc1[r];
                             if (a.vid_out != nullptr) a.vid_out[obase + row] = vid[r];
                         }
                     }
                 }
-                acc = f32x4{0.f, 0.f, 0.f, 0.f};
+                acc0 = f32x4{0.f, 0.f, 0.f, 0.f};
+                acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
             }
             if (advance<NC>(cu, nkb, a.plan, n_items, stride)) {
                 if (!cu.valid) {
