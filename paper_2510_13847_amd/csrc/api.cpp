@@ -271,16 +271,27 @@ static dyna_status check_select(int32_t mode, int32_t* k_t, float temperature, c
 // ------------------------------------------------------------------ pieces
 // One router layer.  Path: 0 automatic (GEMV for up to 4 contexts, else
 // split-K MFMA), 1 GEMV, 2 split-K MFMA, 3 MFMA tiles with direct loads.
-static dyna_status run_layer(const RowdotArgs& a, int path, float* part, size_t part_floats, hipStream_t s) {
+// With `defer` set, a split-K layer leaves its partial sums for the top-k
+// to add (defer->part stays null when the layer runs another way).
+static dyna_status run_layer(const RowdotArgs& a, int path, float* part, size_t part_floats, hipStream_t s,
+                             ScoreSlices* defer = nullptr) {
     const bool splitk = (path == 2 || (path == 0 && a.B > 4)) && a.wdtype == DYNA_BF16 && part != nullptr &&
                         splitk_part_floats(a.n_rows, a.K, a.B, a.vdtype == DYNA_F32) > 0;
+    if (splitk && defer != nullptr && a.act == DYNA_ACT_NONE) {
+        int slices = 0;
+        TRY(launch_dense_splitk(a, part, part_floats, s, &slices));
+        defer->part = part;
+        defer->slices = slices;
+        defer->bias = a.bias;
+        return DYNA_OK;
+    }
     if (splitk) return launch_dense_splitk(a, part, part_floats, s);
     return launch_rowdot(a, path >= 2 ? 3 : path, s);
 }
 
 static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtype, int32_t B,
                               float* scores, float* hidden, float* part, size_t part_floats, hipStream_t s,
-                              int32_t* zero_words = nullptr) {
+                              int32_t* zero_words = nullptr, ScoreSlices* defer = nullptr) {
     const int path = option_router_path();
     RowdotArgs a{};
     a.zero_words = zero_words;  // cleared by block 0 of the first router kernel
@@ -297,7 +308,7 @@ static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtyp
         a.bias = r->b1;
         a.act = DYNA_ACT_NONE;
         a.n_rows = r->M;
-        return run_layer(a, path, part, part_floats, s);
+        return run_layer(a, path, part, part_floats, s, defer);
     }
     a.out = hidden;
     a.ld = r->H;
@@ -317,7 +328,7 @@ static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtyp
     b.bias = r->b2;
     b.act = DYNA_ACT_NONE;
     b.n_rows = r->M;
-    return run_layer(b, path, part, part_floats, s);
+    return run_layer(b, path, part, part_floats, s, defer);
 }
 
 static dyna_status run_logits(const dyna_layout* L, const void* h, int32_t hdtype, int32_t B, int32_t k,
@@ -655,8 +666,11 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
             return timed([&] { return launch_chain_step(q, stream); }, stream);
     }
 
-    // routing (the router's stream)
-    TRY(run_router(r, x, adtype, B, c.scores, c.hidden, c.rpart, c.rpart_floats, rs, fused ? c.counters : nullptr));
+    // routing (the router's stream); with several contexts a split-K last
+    // layer leaves its partial sums to the top-k
+    ScoreSlices slices;
+    TRY(run_router(r, x, adtype, B, c.scores, c.hidden, c.rpart, c.rpart_floats, rs, fused ? c.counters : nullptr,
+                   B > 1 ? &slices : nullptr));
     // union rows: one dense product of the union's slabs with every context
     // (it needs only one list entry per union cluster, and writes one shared
     // copy of the slots' vocabulary ids)
@@ -665,12 +679,12 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     if (union_mode) {
         // per-row clusters, then one shared shortlist (its ids go to sel_sorted)
         TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, nullptr, nullptr, nullptr, nullptr,
-                                 nullptr, rs));
+                                 nullptr, rs, slices));
         TRY(launch_union_plan(L->offsets, L->M, clusters, B, k, c.row_len, c.sel_sorted,
                               (int32_t)std::min<int64_t>(L->M, (int64_t)B * k), c.plan, dense_union, rs));
     } else {
         TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, L->offsets, c.sel_sorted,
-                                 c.sel_rowoff, c.row_len, &c.plan, rs));
+                                 c.sel_rowoff, c.row_len, &c.plan, rs, slices));
         if (B > 1) TRY(launch_plan(L->offsets, L->M, c.sel_sorted, c.sel_rowoff, B, k, c.plan, rs));
     }
     if (split) {

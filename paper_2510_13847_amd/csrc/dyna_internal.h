@@ -127,7 +127,11 @@ struct SplitShape {
 };
 bool splitk_shape(int32_t n_rows, int32_t K, int32_t B, bool vf32, SplitShape* out);
 size_t splitk_part_floats(int32_t n_rows, int32_t K, int32_t B, bool vf32);
-dyna_status launch_dense_splitk(const RowdotArgs& a, float* part, size_t part_floats, hipStream_t stream);
+// deferred_slices != nullptr: the slices' partial sums stay in `part`
+// ([slices][B][n_rows]) and *deferred_slices receives the slice count; the
+// consumer adds them in slice order and then the bias (no activation).
+dyna_status launch_dense_splitk(const RowdotArgs& a, float* part, size_t part_floats, hipStream_t stream,
+                                int* deferred_slices = nullptr);
 
 // gather.hip: plan mode with bf16 weights and contexts, slab rows staged
 // through LDS (MFMA tiles)
@@ -158,6 +162,11 @@ dyna_status launch_cluster_csr(const int32_t* cluster_of, int32_t V, int32_t M, 
 // (Algorithm 1), shared by the separate and the fused launches.
 struct TopkArgs {
     const float* scores;   // [B, M]
+    // part set: the scores are the sum of `slices` split-K partial sums
+    // part[slice][B][M] in slice order, plus bias[M] (if set)
+    const float* part;
+    int slices;
+    const float* bias;
     int M, k;
     int32_t* topk_ids;     // [B, k] rank order
     float* topk_scores;    // [B, k] or nullptr
@@ -197,13 +206,19 @@ struct SelectArgs {
 };
 
 // select.hip
+struct ScoreSlices {  // split-K partial sums the top-k adds up itself
+    const float* part = nullptr;
+    int slices = 0;
+    const float* bias = nullptr;
+};
 dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int32_t k,
                                  int32_t* topk_ids, float* topk_scores,
                                  // optional fused shortlist outputs (all or none)
                                  const int32_t* offsets, int32_t* sel_sorted,
                                  int32_t* sel_rowoff, int32_t* row_len,
                                  // with one context, also write the gathered-head plan
-                                 const Plan* plan, hipStream_t stream);
+                                 const Plan* plan, hipStream_t stream,
+                                 const ScoreSlices& slices = ScoreSlices{});
 dyna_status launch_shortlist(const int32_t* offsets, const int32_t* perm, int32_t M,
                              const int32_t* topk_ids, int32_t B, int32_t k,
                              int32_t* sel_sorted, int32_t* sel_rowoff, int32_t* row_len,

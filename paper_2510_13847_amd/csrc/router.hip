@@ -168,7 +168,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 }
 
 template <int NW, int G, bool VF32, int TT>
-dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* part, hipStream_t stream) {
+dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* part, bool reduce, hipStream_t stream) {
     const dim3 grid((unsigned)sh.row_tiles, (unsigned)sh.slices);
     const uint32_t lds = (uint32_t)sh.lds;
     if (lds > 64 * 1024) {
@@ -185,24 +185,24 @@ dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* pa
     }
     dense_splitk_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
     const dyna_status st = check_launch("dense_splitk_kernel");
-    if (st != DYNA_OK) return st;
+    if (st != DYNA_OK || !reduce) return st;
     splitk_reduce_kernel<<<dim3((unsigned)((a.n_rows + 255) / 256), (unsigned)a.B), dim3(256), 0, stream>>>(
         part, sh.slices, a.B, a.n_rows, a.out, a.ld, a.bias, a.act);
     return check_launch("splitk_reduce_kernel");
 }
 
 template <int NW, bool VF32>
-dyna_status launch_splitk_g(const RowdotArgs& a, const SplitShape& sh, float* part, hipStream_t stream) {
+dyna_status launch_splitk_g(const RowdotArgs& a, const SplitShape& sh, float* part, bool reduce, hipStream_t stream) {
     // the kernel's row tiles per wave must be the shape's (they bound the slice length)
     if (sh.tiles == 2) {
-        if (sh.groups == 4) return launch_splitk_t<NW, 4, VF32, 2>(a, sh, part, stream);
-        return launch_splitk_t<NW, 8, VF32, 2>(a, sh, part, stream);
+        if (sh.groups == 4) return launch_splitk_t<NW, 4, VF32, 2>(a, sh, part, reduce, stream);
+        return launch_splitk_t<NW, 8, VF32, 2>(a, sh, part, reduce, stream);
     }
     switch (sh.groups) {
-        case 1: return launch_splitk_t<NW, 1, VF32, 1>(a, sh, part, stream);
-        case 2: return launch_splitk_t<NW, 2, VF32, 1>(a, sh, part, stream);
-        case 4: return launch_splitk_t<NW, 4, VF32, 1>(a, sh, part, stream);
-        default: return launch_splitk_t<NW, 8, VF32, 1>(a, sh, part, stream);
+        case 1: return launch_splitk_t<NW, 1, VF32, 1>(a, sh, part, reduce, stream);
+        case 2: return launch_splitk_t<NW, 2, VF32, 1>(a, sh, part, reduce, stream);
+        case 4: return launch_splitk_t<NW, 4, VF32, 1>(a, sh, part, reduce, stream);
+        default: return launch_splitk_t<NW, 8, VF32, 1>(a, sh, part, reduce, stream);
     }
 }
 
@@ -239,16 +239,26 @@ size_t splitk_part_floats(int32_t n_rows, int32_t K, int32_t B, bool vf32) {
     return (size_t)s.slices * (size_t)B * (size_t)n_rows;
 }
 
-dyna_status launch_dense_splitk(const RowdotArgs& a, float* part, size_t part_floats, hipStream_t stream) {
+dyna_status launch_dense_splitk(const RowdotArgs& a, float* part, size_t part_floats, hipStream_t stream,
+                                int* deferred_slices) {
+    // deferred_slices set: leave the slices' partial sums in `part` for the
+    // consumer to add (in slice order, then the bias; no activation)
+    const bool reduce = deferred_slices == nullptr;
     const bool vf32 = a.vdtype == DYNA_F32;
     SplitShape sh;
     if (a.wdtype != DYNA_BF16 || a.plan.hdr != nullptr || !splitk_shape(a.n_rows, a.K, a.B, vf32, &sh))
         return set_error(DYNA_ERR_UNSUPPORTED, "split-K router: needs bf16 weights, 1..128 contexts");
     if (part == nullptr || (size_t)sh.slices * (size_t)a.B * (size_t)a.n_rows > part_floats)
         return set_error(DYNA_ERR_WORKSPACE, "split-K router: partial-sum buffer too small");
+    if (!reduce) {
+        if (a.act != DYNA_ACT_NONE) return set_error(DYNA_ERR_UNSUPPORTED, "split-K router: deferred sum with activation");
+        *deferred_slices = sh.slices;
+    }
     if (sh.nw == 8)
-        return vf32 ? launch_splitk_g<8, true>(a, sh, part, stream) : launch_splitk_g<8, false>(a, sh, part, stream);
-    return vf32 ? launch_splitk_g<4, true>(a, sh, part, stream) : launch_splitk_g<4, false>(a, sh, part, stream);
+        return vf32 ? launch_splitk_g<8, true>(a, sh, part, reduce, stream)
+                    : launch_splitk_g<8, false>(a, sh, part, reduce, stream);
+    return vf32 ? launch_splitk_g<4, true>(a, sh, part, reduce, stream)
+                : launch_splitk_g<4, false>(a, sh, part, reduce, stream);
 }
 
 }  // namespace dyna

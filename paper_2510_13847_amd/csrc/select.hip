@@ -124,6 +124,21 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     int32_t* offs = pl + 3 * M;   // layout offsets [M + 1]
     __shared__ int tmp[kPlanThreads / kWave + 1];
     const int t = threadIdx.x;
+    const int64_t n_sel = (int64_t)B * k;
+    // with at most kPlanThreads * kPlanPer selections (every workload) each
+    // thread loads its selections and their shortlist offsets once, in the
+    // same round trip as the layout offsets, and keeps them in registers
+    const bool one_round = n_sel <= (int64_t)kPlanThreads * kPlanPer;
+    int mr[kPlanPer], rr[kPlanPer];
+    if (one_round) {
+#pragma unroll
+        for (int q = 0; q < kPlanPer; ++q) {
+            const int64_t e = (int64_t)q * kPlanThreads + t;
+            mr[q] = e < n_sel ? sel_sorted[e] : -1;
+            const uint32_t b = (uint32_t)e / (uint32_t)k, i = (uint32_t)e - b * (uint32_t)k;
+            rr[q] = e < n_sel ? sel_rowoff[(size_t)b * (k + 1) + i] : 0;
+        }
+    }
     for (int m0 = 0; m0 <= M; m0 += kPlanThreads * kPlanPer) {
         int v[kPlanPer];
 #pragma unroll
@@ -139,17 +154,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         }
     }
     __syncthreads();
-    const int64_t n_sel = (int64_t)B * k;
-    for (int64_t e0 = 0; e0 < n_sel; e0 += kPlanThreads * kPlanPer) {
-        int mv[kPlanPer];
-#pragma unroll
-        for (int q = 0; q < kPlanPer; ++q) {
-            const int64_t e = e0 + q * kPlanThreads + t;
-            mv[q] = e < n_sel ? sel_sorted[e] : -1;
-        }
+    if (one_round) {
 #pragma unroll
         for (int q = 0; q < kPlanPer; ++q)
-            if (mv[q] >= 0 && mv[q] < M) atomicAdd(&cnt[mv[q]], 1);
+            if (mr[q] >= 0 && mr[q] < M) atomicAdd(&cnt[mr[q]], 1);
+    } else {
+        for (int64_t e0 = 0; e0 < n_sel; e0 += kPlanThreads * kPlanPer) {
+            int mv[kPlanPer];
+#pragma unroll
+            for (int q = 0; q < kPlanPer; ++q) {
+                const int64_t e = e0 + q * kPlanThreads + t;
+                mv[q] = e < n_sel ? sel_sorted[e] : -1;
+            }
+#pragma unroll
+            for (int q = 0; q < kPlanPer; ++q)
+                if (mv[q] >= 0 && mv[q] < M) atomicAdd(&cnt[mv[q]], 1);
+        }
     }
     __syncthreads();
     const int per = (M + kPlanThreads - 1) / kPlanThreads;
@@ -199,18 +219,30 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     __syncthreads();
     for (int64_t e0 = 0; e0 < n_sel; e0 += kPlanThreads * kPlanPer) {
         int mv[kPlanPer], ro[kPlanPer];
+        if (one_round) {
 #pragma unroll
-        for (int q = 0; q < kPlanPer; ++q) {
-            const int64_t e = e0 + q * kPlanThreads + t;
-            mv[q] = e < n_sel ? sel_sorted[e] : -1;
+            for (int q = 0; q < kPlanPer; ++q) {
+                mv[q] = mr[q];
+                ro[q] = rr[q];
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < kPlanPer; ++q) {
+                const int64_t e = e0 + q * kPlanThreads + t;
+                mv[q] = e < n_sel ? sel_sorted[e] : -1;
+            }
+#pragma unroll
+            for (int q = 0; q < kPlanPer; ++q) {
+                const uint32_t e = (uint32_t)(e0 + q * kPlanThreads + t);  // B * k < 2^31
+                const uint32_t b = e / (uint32_t)k, i = e - b * (uint32_t)k;
+                ro[q] = (mv[q] >= 0 && mv[q] < M) ? sel_rowoff[(size_t)b * (k + 1) + i] : 0;
+            }
         }
         int bq[kPlanPer];
 #pragma unroll
         for (int q = 0; q < kPlanPer; ++q) {
             const uint32_t e = (uint32_t)(e0 + q * kPlanThreads + t);  // B * k < 2^31
-            const uint32_t b = e / (uint32_t)k, i = e - b * (uint32_t)k;
-            bq[q] = (int)b;
-            ro[q] = (mv[q] >= 0 && mv[q] < M) ? sel_rowoff[(size_t)b * (k + 1) + i] : 0;
+            bq[q] = (int)(e / (uint32_t)k);
         }
 #pragma unroll
         for (int q = 0; q < kPlanPer; ++q) {
@@ -599,7 +631,7 @@ __global__ __launch_bounds__(kRowThreads) void select_row_kernel(SelectArgs a) {
 dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int32_t k,
                                  int32_t* topk_ids, float* topk_scores, const int32_t* offsets,
                                  int32_t* sel_sorted, int32_t* sel_rowoff, int32_t* row_len,
-                                 const Plan* plan, hipStream_t stream) {
+                                 const Plan* plan, hipStream_t stream, const ScoreSlices& slices) {
     const size_t lds = topk_lds_bytes(M, k);
     if (lds > 65536) {
         static bool raised = false;
@@ -611,7 +643,8 @@ dyna_status launch_topk_clusters(const float* scores, int32_t B, int32_t M, int3
     }
     Plan p{};
     if (plan != nullptr && B == 1) p = *plan;
-    TopkArgs A{scores, M, k, topk_ids, topk_scores, offsets, sel_sorted, sel_rowoff, row_len, p};
+    TopkArgs A{scores, slices.part, slices.slices, slices.bias, M, k, topk_ids, topk_scores, offsets,
+               sel_sorted, sel_rowoff, row_len, p};
     topk_clusters_kernel<<<B, kNT, lds, stream>>>(A);
     return check_launch("topk_clusters_kernel");
 }

@@ -153,14 +153,43 @@ __device__ void topk_row(const TopkArgs& A, int b, unsigned char* smem) {
     int32_t* ssize = sid + k;                                          // [k]
     __shared__ int tmp[kNT / kWave + 1];
 
-    // stage scores (and offsets) with kStagePer loads in flight per thread
+    // stage scores (and offsets) with kStagePer loads in flight per thread;
+    // split-K partial sums are added here in slice order, then the bias
     const float* s = scores + (int64_t)b * M;
     for (int j0 = 0; j0 < M; j0 += kNT * kStagePer) {
         float x[kStagePer];
+        if (A.part != nullptr) {
+            // eight slices' loads are issued together, then added in order
 #pragma unroll
-        for (int q = 0; q < kStagePer; ++q) {
-            const int j = j0 + q * kNT + threadIdx.x;
-            x[q] = j < M ? s[j] : 0.0f;
+            for (int q = 0; q < kStagePer; ++q) x[q] = 0.0f;
+            for (int sl0 = 0; sl0 < A.slices; sl0 += 8) {
+                float y[8][kStagePer];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const float* ps = A.part + ((int64_t)(sl0 + u) * gridDim.x + b) * M;
+#pragma unroll
+                    for (int q = 0; q < kStagePer; ++q) {
+                        const int j = j0 + q * kNT + threadIdx.x;
+                        y[u][q] = (sl0 + u < A.slices && j < M) ? ps[j] : 0.0f;
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+#pragma unroll
+                    for (int q = 0; q < kStagePer; ++q)
+                        if (sl0 + u < A.slices) x[q] += y[u][q];
+            }
+#pragma unroll
+            for (int q = 0; q < kStagePer; ++q) {
+                const int j = j0 + q * kNT + threadIdx.x;
+                if (j < M) x[q] = x[q] + (A.bias ? A.bias[j] : 0.0f);
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < kStagePer; ++q) {
+                const int j = j0 + q * kNT + threadIdx.x;
+                x[q] = j < M ? s[j] : 0.0f;
+            }
         }
 #pragma unroll
         for (int q = 0; q < kStagePer; ++q) {
