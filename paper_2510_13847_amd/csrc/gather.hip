@@ -39,6 +39,13 @@ using sptr = const __attribute__((address_space(4))) T*;  // read through the sc
 typedef __attribute__((address_space(3))) void* lds_ptr;
 typedef __attribute__((address_space(1))) void* glb_ptr;
 
+// Cache policy of the direct-to-LDS loads of slab rows: non-temporal.  Each
+// slab row is read once per step, so streaming it past the caches' normal
+// allocation leaves L2 and the last-level cache to what is reused (the
+// contexts, the plan); it raised the gathered head from 0.64 to 0.70 of the
+// HBM peak on the tree-batch workload.  Context loads keep the default.
+constexpr int kSlabPolicy = 2;
+
 // Wait until at most N vector-memory instructions of this wave are outstanding.
 template <int N>
 __device__ __forceinline__ void wait_vmem() {
@@ -207,7 +214,7 @@ __global__ __launch_bounds__(NW * kWave) void gather_lds_kernel(RowdotArgs a) {
             int e = kb * KB + piece * 8;
             e = e < K ? e : 0;  // k tail: any in-bounds piece; zeroed when read
             const uint16_t* src = W + (int64_t)(iu.r0 + min(row, iu.nrows - 1)) * K + e;
-            __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0, kSlabPolicy);
         }
 #pragma unroll
         for (int i = 0; i < NBI; ++i) {
@@ -376,7 +383,8 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
         if (k0 + KB <= K) {
 #pragma unroll
             for (int i = 0; i < NA; ++i)
-                __builtin_amdgcn_global_load_lds((glb_ptr)(arow[i] + k0), (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds((glb_ptr)(arow[i] + k0), (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0,
+                                                 kSlabPolicy);
             if (bcol) {
 #pragma unroll
                 for (int st = 0; st < STEPS; ++st)
@@ -391,7 +399,7 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
                 const int piece = lpc ^ (row % PIECES);
                 const int off = k0 + piece * 8 < K ? k0 : -piece * 8;
                 __builtin_amdgcn_global_load_lds((glb_ptr)(arow[i] + off), (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0,
-                                                 0);
+                                                 kSlabPolicy);
             }
             if (bcol) {
 #pragma unroll
@@ -677,7 +685,7 @@ __global__ __launch_bounds__(NW * kWave) void union_gemm_kernel(RowdotArgs a) {
             e = e < K ? e : 0;  // k tail: any in-bounds piece; zeroed when read
             const int64_t grow = iu.nrows[t] > 0 ? iu.r0[t] + min(row, iu.nrows[t] - 1) : 0;
             __builtin_amdgcn_global_load_lds((glb_ptr)(W + grow * K + e),
-                                             (lds_ptr)(dst + wv * A_WAVE + i * (RPI * ROWB)), 16, 0, 0);
+                                             (lds_ptr)(dst + wv * A_WAVE + i * (RPI * ROWB)), 16, 0, kSlabPolicy);
         }
 #pragma unroll
         for (int i = 0; i < NBW; ++i) {
