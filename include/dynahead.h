@@ -360,8 +360,11 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  * DYNA_OPT_MFMA_UNROLL: k steps the direct-load MFMA kernel (path 3) loads
  *   ahead: 0 automatic (8), 4, 8 or 16.
  * DYNA_OPT_GATHER_CFG: shape of the LDS-staged MFMA kernel (path 2): 0
- *   automatic, 1..9 fixed (waves per block, ring stages, k columns per
- *   stage, context columns per pass).
+ *   automatic (slab rows staged through LDS, contexts loaded into
+ *   registers, two workgroups of two waves per compute unit); 1..9 the
+ *   older kernel that stages the contexts through LDS too (waves per block,
+ *   ring stages, k columns per stage, context columns per pass); 10..13
+ *   other shapes of the automatic kernel.
  * DYNA_OPT_GREEDY_GRID: workgroups of the fused one-context gathered head:
  *   0 automatic (256), else 1..4096.
  * DYNA_OPT_UNION_CFG: shape of the dense union-row kernel of

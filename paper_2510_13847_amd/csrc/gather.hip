@@ -919,10 +919,10 @@ dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
         case 8: return launch_cfg<4, 2, 512, 4>(a, stream);
         case 9: return launch_cfg<3, 2, 512, 8>(a, stream);
         case 10: return launch_ring_cfg<4, 2, 512>(a, stream);
-        case 11: return launch_ring_cfg<2, 4, 256>(a, stream);
+        case 11: return launch_ring_cfg<4, 4, 256>(a, stream);
         case 12: return launch_ring_cfg<4, 8, 128>(a, stream);
         case 13: return launch_ring_cfg<8, 8, 64>(a, stream);
-        default: return launch_ring_cfg<4, 4, 256>(a, stream);
+        default: return launch_ring_cfg<2, 4, 256>(a, stream);  // two workgroups of two waves per CU
     }
 }
 
