@@ -5,11 +5,12 @@
 // With one context every stage is small (the chain workload moves 8 MB,
 // 2 MB, 4 KB and 33 MB), so as separate kernels the step is dominated by
 // launch gaps and by each kernel's cold start.  Here one grid of G
-// workgroups runs all of them, with two grid-wide hand-offs:
+// workgroups runs all of them, with two grid-wide hand-offs and a final
+// gather of per-workgroup partials:
 //
-//   1. every wave dots its rows of W1 with x (x in registers) and writes
-//      the hidden units with device-coherent stores; its W2 rows for stage 2
-//      are already loading;
+//   1. every wave dots its rows of W1 with x (x in registers), writes the
+//      hidden units with device-coherent stores and starts loading its W2
+//      row for stage 2;
 //   2. after all workgroups arrived, each stages the hidden layer in LDS and
 //      dots its prefetched W2 rows with it, writing the scores;
 //   3. after all arrived again, every workgroup reads the M scores into LDS
@@ -19,8 +20,9 @@
 //   4. the shortlist rows are split evenly over all waves as contiguous
 //      ranges (a range may cross slab boundaries), streamed with
 //      non-temporal 16-byte loads and dotted with h (in registers);
-//   5. each workgroup publishes its greedy partial and the last one merges
-//      them (greedy.h) and writes the token.
+//   5. each workgroup publishes its greedy partial; workgroup 0 polls them,
+//      merges them in workgroup order and writes the token, and the last
+//      workgroup writes the selection outputs.
 //
 // Hand-off protocol: every handed-off word is 64 bits, a 32-bit epoch tag
 // above the 32-bit value, written with one device-coherent store; readers
@@ -31,8 +33,9 @@
 // merge, when every workgroup has read it.  A zero-filled workspace starts
 // at epoch 1, above the tags of its zero words.  Every poll is bounded in
 // time: a word that never turns current (the grid is not co-resident, or a
-// workspace that was not zero-filled) sets an error word, the poll gives up
-// and the launch reports no token (out_ids = -1) but still terminates.
+// workspace that was not zero-filled) sets an error word and marks the
+// workgroup's partial, the poll gives up, and the launch reports no token
+// (out_ids = -1) but still terminates.
 #include <atomic>
 
 #include "dyna_internal.h"
@@ -100,50 +103,13 @@ __host__ __device__ inline size_t chain_lds_bytes(int M, int k, int H, int G) {
 
 __device__ __forceinline__ uint64_t tagged(uint32_t e, uint32_t v) { return ((uint64_t)e << 32) | v; }
 
-// Reads n tagged words src[0..n) into dst (as raw 32-bit values), workgroup
-// wide: each thread issues its loads together, then re-polls all of its
-// stale words together (one round trip per poll, however many are stale)
-// until they carry epoch e or the time bound runs out.
-template <int NT>
-__device__ __forceinline__ void poll_words(const ChainArgs& A, const uint64_t* src, int n, uint32_t e,
-                                           uint32_t* dst) {
-    constexpr int Q = 8;
-    const uint64_t t0 = wall_clock64();
-    for (int base = 0; base < n; base += NT * Q) {
-        uint64_t v[Q];
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-            const int j = base + q * NT + (int)threadIdx.x;
-            v[q] = j < n ? load_coherent(src + j) : tagged(e, 0u);
-        }
-        for (;;) {
-            bool stale = false;
-#pragma unroll
-            for (int q = 0; q < Q; ++q) stale |= (uint32_t)(v[q] >> 32) != e;
-            if (!stale) break;
-            if (wall_clock64() - t0 > A.spin_ticks) {
-                store_coherent(A.err, 1u);
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-            for (int q = 0; q < Q; ++q)
-                if ((uint32_t)(v[q] >> 32) != e) v[q] = load_coherent(src + base + q * NT + (int)threadIdx.x);
-        }
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-            const int j = base + q * NT + (int)threadIdx.x;
-            if (j < n) dst[j] = (uint32_t)v[q];
-        }
-    }
-}
-
 // Thread t reads the tagged words src[t + NT q], q < Q (those below n), into
 // raw[q], re-polling its stale ones together until they carry epoch e or
-// the time bound runs out.
+// the time bound runs out.  Returns true if it gave up.
 template <int NT, int Q>
-__device__ __forceinline__ void poll_own(const ChainArgs& A, const uint64_t* src, int n, uint32_t e,
+__device__ __forceinline__ bool poll_own(const ChainArgs& A, const uint64_t* src, int n, uint32_t e,
                                          uint32_t (&raw)[Q]) {
+    bool gave_up = false;
     const uint64_t t0 = wall_clock64();
     uint64_t v[Q];
 #pragma unroll
@@ -158,6 +124,7 @@ __device__ __forceinline__ void poll_own(const ChainArgs& A, const uint64_t* src
         if (!stale) break;
         if (wall_clock64() - t0 > A.spin_ticks) {
             store_coherent(A.err, 1u);
+            gave_up = true;
             break;
         }
         __builtin_amdgcn_s_sleep(1);
@@ -167,6 +134,27 @@ __device__ __forceinline__ void poll_own(const ChainArgs& A, const uint64_t* src
     }
 #pragma unroll
     for (int q = 0; q < Q; ++q) raw[q] = (uint32_t)v[q];
+    return gave_up;
+}
+
+// Reads n tagged words src[0..n) into dst (as raw 32-bit values), workgroup
+// wide, NT * 4 words per pass (poll_own per pass; passes of 8 words per
+// thread measured slower).  Returns true in a thread that gave up.
+template <int NT>
+__device__ __forceinline__ bool poll_words(const ChainArgs& A, const uint64_t* src, int n, uint32_t e,
+                                           uint32_t* dst) {
+    constexpr int Q = 4;
+    bool gave_up = false;
+    for (int base = 0; base < n; base += NT * Q) {
+        uint32_t raw[Q];
+        gave_up |= poll_own<NT, Q>(A, src + base, n - base, e, raw);
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int j = base + q * NT + (int)threadIdx.x;
+            if (j < n) dst[j] = raw[q];
+        }
+    }
+    return gave_up;
 }
 
 template <int NB>
@@ -208,14 +196,69 @@ __device__ __forceinline__ float dot_lds(const Raw8<uint16_t> (&w)[NB], const fl
     return wave_sum(acc);
 }
 
-// Scores per thread in the selection: thread t holds ids t + NT q, q < kSelQ.
+// Scores per thread in the selection: thread t holds ids kSelQ t + q.
 constexpr int kSelQ = 4;
 constexpr int kChainMaxM = kChainThreads * kSelQ;
+// Shortlist lengths stay below 2^kLenBits (the layout scan packs the member
+// count above the length in one 32-bit word).
+constexpr int kLenBits = 21;
+
+// Thread t reads the tagged words src[Q t + q], q < Q (those below n), into
+// raw[q], re-polling its stale ones together until they carry epoch e or the
+// time bound runs out.  Returns true if it gave up.
+template <int Q>
+__device__ __forceinline__ bool poll_run(const ChainArgs& A, const uint64_t* src, int n, uint32_t e,
+                                         uint32_t (&raw)[Q]) {
+    bool gave_up = false;
+    const uint64_t t0 = wall_clock64();
+    const int j0 = (int)threadIdx.x * Q;
+    uint64_t v[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) v[q] = j0 + q < n ? load_coherent(src + j0 + q) : tagged(e, 0u);
+    for (;;) {
+        bool stale = false;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) stale |= (uint32_t)(v[q] >> 32) != e;
+        if (!stale) break;
+        if (wall_clock64() - t0 > A.spin_ticks) {
+            store_coherent(A.err, 1u);
+            gave_up = true;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+            if ((uint32_t)(v[q] >> 32) != e) v[q] = load_coherent(src + j0 + q);
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) raw[q] = (uint32_t)v[q];
+    return gave_up;
+}
+
+// Minimum and maximum over the wave (on lane 63), the two reductions
+// interleaved step by step.
+__device__ __forceinline__ void wave_min_max(float& lo, float& hi) {
+    auto step = [&](auto ctrl_tag, auto rmask_tag) {
+        constexpr int CTRL = decltype(ctrl_tag)::value;
+        constexpr int RM = decltype(rmask_tag)::value;
+        const float l2 = __uint_as_float(dpp<CTRL, RM>(__float_as_uint(__builtin_inff()), __float_as_uint(lo)));
+        const float h2 = __uint_as_float(dpp<CTRL, RM>(__float_as_uint(-__builtin_inff()), __float_as_uint(hi)));
+        lo = fminf(lo, l2);
+        hi = fmaxf(hi, h2);
+    };
+    step(std::integral_constant<int, kRowShr1>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr2>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr4>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowShr8>{}, std::integral_constant<int, 0xf>{});
+    step(std::integral_constant<int, kRowBcast15>{}, std::integral_constant<int, 0xa>{});
+    step(std::integral_constant<int, kRowBcast31>{}, std::integral_constant<int, 0xc>{});
+}
 
 // The k best of the M <= NT * kSelQ scores v[] (registers; thread t holds
-// ids t + NT q) by (score desc, id asc), as the shortlist in ascending
-// cluster id: sid[0..k) the ids, rowoff[0..k] the exclusive prefix of their
-// slab sizes.  Returns the shortlist length.
+// ids kSelQ t + q) by (score desc, id asc), as the shortlist in ascending
+// cluster id: sid[0..k) the ids, mkey[0..k) their (score, id) keys,
+// rowoff[0..k] the exclusive prefix of their slab sizes.  Returns the
+// shortlist length; sets `bad` in thread 0 when the members are not k.
 //
 // Each score gets a class that is monotone in the score: 0 for -inf and
 // NaN, 255 for +inf, and for finite scores 1 + one of 254 equal-width bins
@@ -223,24 +266,27 @@ constexpr int kChainMaxM = kChainThreads * kSelQ;
 // whatever their scale).  One histogram, scanned from the top by every wave,
 // gives the class c* of the k-th best and the number `need` of places left
 // in it; classes above c* are members, and the few scores in class c* are
-// ranked exactly by their (score, id) keys.  Counts and sizes of the members
-// are then scanned in id order (q major, thread minor) to lay out the
-// shortlist.
+// ranked exactly by their (score, id) keys.  With consecutive ids in each
+// thread, thread order is id order, so one scan of (member count, slab
+// length) per thread lays out the shortlist.  The member keys reuse the
+// candidate area (cand[0..k)), which the ranking has finished reading by then.
 template <int NT>
 __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32_t* offs, int M, int k,
-                                            uint64_t* cand, int32_t* sid, int32_t* rowoff, uint32_t* err) {
+                                            uint64_t* cand, int32_t* sid, int32_t* rowoff, uint32_t* err,
+                                            bool& bad) {
     static_assert(NT == 256, "one histogram bin per thread");
     constexpr int NW = NT / kWave;
     constexpr int Q = kSelQ;
     __shared__ __attribute__((aligned(16))) int hist[256];
     __shared__ float s_lo[NW], s_hi[NW];
     __shared__ int s_nc[NW];
-    __shared__ int s_cnt[Q][NW], s_len[Q][NW];
+    __shared__ uint32_t s_tot[NW];
     const float inf = __builtin_inff();
     const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+    const int id0 = t * Q;
     bool valid[Q];
 #pragma unroll
-    for (int q = 0; q < Q; ++q) valid[q] = t + NT * q < M;
+    for (int q = 0; q < Q; ++q) valid[q] = id0 + q < M;
 
     // range of the finite scores
     float lo = inf, hi = -inf;
@@ -251,13 +297,10 @@ __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32
             hi = fmaxf(hi, v[q]);
         }
     hist[t] = 0;
-    {
-        const float wl = -readlane_f32(wave_max_f32(-lo), kWave - 1);
-        const float wh = readlane_f32(wave_max_f32(hi), kWave - 1);
-        if (lane == 0) {
-            s_lo[w] = wl;
-            s_hi[w] = wh;
-        }
+    wave_min_max(lo, hi);
+    if (lane == kWave - 1) {
+        s_lo[w] = lo;
+        s_hi[w] = hi;
     }
     __syncthreads();
     lo = s_lo[0];
@@ -320,7 +363,7 @@ __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32
     for (int q = 0; q < Q; ++q) {
         mem[q] = c[q] > cstar;
         isc[q] = c[q] == cstar;
-        key[q] = sel_key(v[q], (uint32_t)(t + NT * q));
+        key[q] = sel_key(v[q], (uint32_t)(id0 + q));
         const uint64_t bal = __ballot(isc[q]);
         if (isc[q])
             seg[nc + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
@@ -344,55 +387,93 @@ __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32
             mem[q] = rank < need;
         }
 
-    // the shortlist in ascending id: (q, thread) order
-    int sz[Q], pcnt[Q], plen[Q];
+    // the shortlist in ascending id, which is thread order: one scan of the
+    // packed (member count, slab length) of each thread
+    int sz[Q];
+    uint32_t mine = 0;
+    {
+        int o[Q + 1];
+        if ((M & 3) == 0 && id0 + Q <= M) {  // offs + id0 is 16-byte aligned
+            const int4 o4 = *reinterpret_cast<const int4*>(offs + id0);
+            o[0] = o4.x;
+            o[1] = o4.y;
+            o[2] = o4.z;
+            o[3] = o4.w;
+            o[4] = offs[id0 + Q];
+        } else {
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
-        const int j = t + NT * q;
-        sz[q] = mem[q] ? offs[j + 1] - offs[j] : 0;
-        const uint64_t bal = __ballot(mem[q]);
-        pcnt[q] = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-        const int inc = wave_inclusive_scan(sz[q]);
-        plen[q] = inc - sz[q];
-        if (lane == kWave - 1) {
-            s_cnt[q][w] = __popcll(bal);
-            s_len[q][w] = inc;
+            for (int q = 0; q <= Q; ++q) o[q] = offs[min(id0 + q, M)];
+        }
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            sz[q] = mem[q] ? o[q + 1] - o[q] : 0;
+            mine += (mem[q] ? 1u << kLenBits : 0u) + (uint32_t)sz[q];
         }
     }
+    const uint32_t inc = (uint32_t)wave_inclusive_scan((int)mine);
+    if (lane == kWave - 1) s_tot[w] = inc;
     __syncthreads();
-    int total_cnt = 0, total_len = 0;
+    uint32_t pre = inc - mine, total = 0;
+#pragma unroll
+    for (int g = 0; g < NW; ++g) {
+        const uint32_t tg = s_tot[g];
+        if (g < w) pre += tg;
+        total += tg;
+    }
+    constexpr uint32_t kLenMask = (1u << kLenBits) - 1u;
+    int pos = (int)(pre >> kLenBits), off = (int)(pre & kLenMask);
 #pragma unroll
     for (int q = 0; q < Q; ++q)
-#pragma unroll
-        for (int g = 0; g < NW; ++g) {
-            const int cq = s_cnt[q][g], lq = s_len[q][g];
-            // this (q, wave) block follows every block (q', g') before it
-#pragma unroll
-            for (int qq = 0; qq < Q; ++qq)
-                if (qq == q) {
-                    if (g < w) {
-                        pcnt[qq] += cq;
-                        plen[qq] += lq;
-                    }
-                } else if (q < qq) {
-                    pcnt[qq] += cq;
-                    plen[qq] += lq;
-                }
-            total_cnt += cq;
-            total_len += lq;
+        if (mem[q]) {
+            if (pos < k) {
+                sid[pos] = id0 + q;
+                cand[pos] = key[q];
+                rowoff[pos] = off;
+            }
+            ++pos;
+            off += sz[q];
         }
-#pragma unroll
-    for (int q = 0; q < Q; ++q)
-        if (mem[q] && pcnt[q] < k) {
-            sid[pcnt[q]] = t + NT * q;
-            rowoff[pcnt[q]] = plen[q];
-        }
+    const int total_cnt = (int)(total >> kLenBits), total_len = (int)(total & kLenMask);
     if (t == 0) {
         rowoff[k] = total_len;
-        if (total_cnt != k) store_coherent(err, 1u);
+        if (total_cnt != k) {
+            store_coherent(err, 1u);
+            bad = true;
+        }
     }
     __syncthreads();
     return total_len;
+}
+
+// The selection outputs of one workgroup: the ids and slab offsets in
+// ascending id, the shortlist length, and the k clusters in rank order
+// (score desc, id asc) with their scores.  A member's rank is the number of
+// members with a larger key; P lanes share each member's count.
+template <int NT>
+__device__ __forceinline__ void chain_outputs(const ChainArgs& A, const float* sv, const int32_t* sid,
+                                              const uint64_t* mkey, const int32_t* rowoff, int k, int L) {
+    for (int i = threadIdx.x; i <= k; i += NT) {
+        if (i < k && A.sel_sorted) A.sel_sorted[i] = sid[i];
+        if (A.sel_rowoff) A.sel_rowoff[i] = rowoff[i];
+    }
+    if (threadIdx.x == 0 && A.row_len) A.row_len[0] = L;
+    if (!A.out_clusters && !A.topk_scores) return;
+    constexpr int P = 8;
+    const int part = threadIdx.x % P;
+    for (int i0 = 0; i0 < k; i0 += NT / P) {
+        const int i = i0 + (int)threadIdx.x / P;
+        const uint64_t key = i < k ? mkey[i] : 0;
+        int rank = 0;
+        if (i < k)
+            for (int j = part; j < k; j += P) rank += mkey[j] > key;
+        rank += __shfl_xor(rank, 1);
+        rank += __shfl_xor(rank, 2);
+        rank += __shfl_xor(rank, 4);
+        if (i < k && part == 0) {
+            if (A.out_clusters) A.out_clusters[rank] = sid[i];
+            if (A.topk_scores) A.topk_scores[rank] = sv[sid[i]];
+        }
+    }
 }
 
 template <int NB, int R>
@@ -417,8 +498,8 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     const int nw = G * kChainWaves;
     const int gw = blockIdx.x * kChainWaves + wv;
 
-    // ---- loads that depend on nothing: x, h, the first W1 and W2 rows,
-    // offsets (h and the W2 row only while the registers allow: d <= 4096)
+    // ---- loads that depend on nothing: x, h, the first W1 row, offsets (h
+    // only while the registers allow: d <= 4096)
     constexpr bool kEarly = NB <= 8;
     Raw8<uint16_t> xv[NB], hv[NB], w2[NB];
     auto load_h = [&]() {
@@ -439,7 +520,13 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     const int n1 = H > 0 ? H : M;
     Raw8<uint16_t> w1[NB];
     if (gw < n1) load_bf16_row<NB>(w1, A.W1 + (int64_t)gw * A.d_r, A.d_r, lane);
-    if (kEarly && H > 0 && gw < M) load_bf16_row<NB>(w2, A.W2 + (int64_t)gw * H, H, lane);
+    // The per-lane conditions above make the compiler wait for these loads
+    // before the offsets are read, and the offsets loop waits once per pass.
+    // Issuing every load at once (unconditional loads, the offsets held in
+    // registers) made the step 2 us slower: stage 1 then ends at more
+    // spread-out times over the workgroups, and both hand-offs after it took
+    // longer, the early workgroups polling words the late ones had yet to
+    // write.
     for (int j = threadIdx.x; j <= M; j += kChainThreads) offs[j] = A.offsets[j];
 
     // ---- stage 1: layer 1 (hidden units, or the scores of a linear router)
@@ -453,10 +540,15 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
                 store_coherent(out + j, tagged(e, __float_as_uint(apply_act(s + (A.b1 ? A.b1[j] : 0.0f), act))));
         }
     }
+    // the first W2 row loads during the hand-off of the hidden layer (issued
+    // with the W1 rows it only lengthens stage 1, and the hand-offs measured
+    // slower that way)
+    if (kEarly && H > 0 && gw < M) load_bf16_row<NB>(w2, A.W2 + (int64_t)gw * H, H, lane);
 
     // ---- stage 2: layer 2 over the hidden layer, polled into LDS
+    bool bad = false;  // this thread gave up a wait, or the selection failed
     if (H > 0) {
-        poll_words<kChainThreads>(A, A.thidden, H, e, reinterpret_cast<uint32_t*>(hid));
+        bad = poll_words<kChainThreads>(A, A.thidden, H, e, reinterpret_cast<uint32_t*>(hid));
         __syncthreads();
         for (int j = gw; j < M; j += nw) {
             if (!kEarly || j != gw) load_bf16_row<NB>(w2, A.W2 + (int64_t)j * H, H, lane);
@@ -469,32 +561,14 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     float v[kSelQ];
     {
         uint32_t raw[kSelQ];
-        poll_own<kChainThreads, kSelQ>(A, A.tscores, M, e, raw);
+        bad |= poll_run<kSelQ>(A, A.tscores, M, e, raw);
 #pragma unroll
         for (int q = 0; q < kSelQ; ++q) {
             v[q] = __uint_as_float(raw[q]);
-            if ((int)threadIdx.x + kChainThreads * q < M) sv[threadIdx.x + kChainThreads * q] = v[q];
+            if ((int)threadIdx.x * kSelQ + q < M) sv[threadIdx.x * kSelQ + q] = v[q];
         }
     }
-    const int L = chain_select<kChainThreads>(v, offs, M, k, cand, sid, rowoff, A.err);
-    if (blockIdx.x == 0 && (A.out_clusters || A.topk_scores)) {
-        // rank order (score desc, id asc) by counting, for the outputs only
-        for (int i = threadIdx.x; i < k; i += kChainThreads) {
-            const int id = sid[i];
-            const uint64_t key = sel_key(sv[id], (uint32_t)id);
-            int rank = 0;
-            for (int j = 0; j < k; ++j) rank += sel_key(sv[sid[j]], (uint32_t)sid[j]) > key;
-            if (A.out_clusters) A.out_clusters[rank] = id;
-            if (A.topk_scores) A.topk_scores[rank] = sv[id];
-        }
-    }
-    if (blockIdx.x == 0) {
-        for (int i = threadIdx.x; i <= k; i += kChainThreads) {
-            if (i < k && A.sel_sorted) A.sel_sorted[i] = sid[i];
-            if (A.sel_rowoff) A.sel_rowoff[i] = rowoff[i];
-        }
-        if (threadIdx.x == 0 && A.row_len) A.row_len[0] = L;
-    }
+    const int L = chain_select<kChainThreads>(v, offs, M, k, cand, sid, rowoff, A.err, bad);
 
     // ---- stage 4: logits over the wave's contiguous range of shortlist slots
     if constexpr (!kEarly) load_h();
@@ -559,67 +633,86 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
         }
     }
 
-    // ---- stage 5: greedy partials; workgroup 0 polls and merges them
+    // ---- stage 5: greedy partials; workgroup 0 polls and merges them.  A
+    // partial whose workgroup gave up a wait (or failed the selection)
+    // carries a negative sum, which fails the step.
     {
         constexpr int NW = kChainWaves;
         __shared__ uint64_t w_best[NW];
         __shared__ float w_m[NW], w_s[NW];
+        __shared__ int w_bad[NW];
         const uint64_t wb = wave_max_u64(st.best);
         const float wm = readlane_f32(wave_max_f32(st.m), kWave - 1);
         const float wsum = wave_sum(st.m == -__builtin_inff() ? 0.0f : st.s * expf((st.m - wm) * A.inv_t));
+        const bool wbad = __ballot(bad) != 0;
         if (lane == 0) {
             w_best[wv] = wb;
             w_m[wv] = wm;
             w_s[wv] = wsum;
+            w_bad[wv] = wbad;
         }
         __syncthreads();
         if (threadIdx.x == 0) {
             uint64_t bb = w_best[0];
             float bm = w_m[0], bs = w_s[0];
+            bool any_bad = w_bad[0] != 0;
             for (int q = 1; q < NW; ++q) {
                 bb = w_best[q] > bb ? w_best[q] : bb;
                 softmax_merge(bm, bs, w_m[q], w_s[q], A.inv_t);
+                any_bad |= w_bad[q] != 0;
             }
             uint64_t* pw = A.tpart + (int64_t)blockIdx.x * kPartWords;
             store_coherent(pw + 0, tagged(e, (uint32_t)(bb >> 32)));
             store_coherent(pw + 1, tagged(e, (uint32_t)bb));
             store_coherent(pw + 2, tagged(e, __float_as_uint(bm)));
-            store_coherent(pw + 3, tagged(e, __float_as_uint(bs)));
+            store_coherent(pw + 3, tagged(e, __float_as_uint(any_bad ? -1.0f : bs)));
         }
+        // the selection outputs come from the last workgroup, after its
+        // partial is out (off the merging workgroup's path when G > 1)
+        if (blockIdx.x == G - 1) chain_outputs<kChainThreads>(A, sv, sid, cand, rowoff, k, L);
         if (blockIdx.x != 0) return;
 
         // workgroup 0: thread t merges partials t, t + NT, ... in order, then a
-        // fixed-order wave and workgroup reduction
+        // fixed-order wave and workgroup reduction.  The error word (set by a
+        // wait that gave up, possibly in a straggler of an earlier launch) is
+        // read alongside the partials.
         __syncthreads();
-        poll_words<kChainThreads>(A, A.tpart, G * kPartWords, e, pv);
+        const uint32_t err_word = threadIdx.x == 0 ? load_coherent(A.err) : 0u;
+        const bool late = poll_words<kChainThreads>(A, A.tpart, G * kPartWords, e, pv);
         __syncthreads();
         uint64_t bb = 0;
         float bm = -__builtin_inff(), bs = 0.0f;
+        bool fail = late;
         for (int g = threadIdx.x; g < G; g += kChainThreads) {
             const uint32_t* q = pv + g * kPartWords;
             const uint64_t k2 = ((uint64_t)q[0] << 32) | q[1];
+            const float s2 = __uint_as_float(q[3]);
+            fail |= s2 < 0.0f;
             bb = k2 > bb ? k2 : bb;
-            softmax_merge(bm, bs, __uint_as_float(q[2]), __uint_as_float(q[3]), A.inv_t);
+            softmax_merge(bm, bs, __uint_as_float(q[2]), s2 < 0.0f ? 0.0f : s2, A.inv_t);
         }
         const uint64_t gb = wave_max_u64(bb);
         const float gm = readlane_f32(wave_max_f32(bm), kWave - 1);
         const float gs = wave_sum(bm == -__builtin_inff() ? 0.0f : bs * expf((bm - gm) * A.inv_t));
+        const bool gfail = __ballot(fail) != 0;
         __syncthreads();
         if (lane == 0) {
             w_best[wv] = gb;
             w_m[wv] = gm;
             w_s[wv] = gs;
+            w_bad[wv] = gfail;
         }
         __syncthreads();
         if (threadIdx.x == 0) {
             uint64_t fb = w_best[0];
             float fm = w_m[0], fs = w_s[0];
+            bool err = w_bad[0] != 0 || err_word != 0u;
             for (int q = 1; q < NW; ++q) {
                 fb = w_best[q] > fb ? w_best[q] : fb;
                 softmax_merge(fm, fs, w_m[q], w_s[q], A.inv_t);
+                err |= w_bad[q] != 0;
             }
             // every workgroup has read the epoch (its partial carries it)
-            const bool err = load_coherent(A.err) != 0u;
             if (err) {
                 store_coherent(A.err, 0u);
                 fb = 0;
@@ -658,7 +751,7 @@ size_t chain_region_bytes(int32_t H, int32_t M) {
 
 bool chain_step_eligible(const ChainRequest& q) {
     const int kmax = std::max(q.d_r, std::max(q.H, q.d));
-    return q.all_bf16 && q.region != nullptr && kmax <= 8192 && q.M <= kChainMaxM &&
+    return q.all_bf16 && q.region != nullptr && kmax <= 8192 && q.M <= kChainMaxM && q.V < (1 << kLenBits) &&
            chain_lds_bytes(q.M, q.k, q.H, kChainMaxGrid) <= 160 * 1024;
 }
 
