@@ -498,8 +498,7 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     const int nw = G * kChainWaves;
     const int gw = blockIdx.x * kChainWaves + wv;
 
-    // ---- loads that depend on nothing: x, h, the first W1 row (h only
-    // while the registers allow: d <= 4096)
+    // ---- loads that depend on nothing: x and the first W1 row
     constexpr bool kEarly = NB <= 8;
     Raw8<uint16_t> xv[NB], hv[NB], w2[NB];
     auto load_h = [&]() {
@@ -516,7 +515,6 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
         if (e < A.d_r) xv[blk].template load<false>(A.x + e);
         else xv[blk].zero();
     }
-    if constexpr (kEarly) load_h();
     const int n1 = H > 0 ? H : M;
     Raw8<uint16_t> w1[NB];
     if (gw < n1) load_bf16_row<NB>(w1, A.W1 + (int64_t)gw * A.d_r, A.d_r, lane);
@@ -558,12 +556,14 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     // ---- stage 3: top-k clusters and the shortlist, in every workgroup.
     // The CSR offsets are staged first: their round trip delays the first
     // poll of the scores, which measured faster (0.9 us per step) than
-    // polling at once with the offsets in flight.
+    // polling at once with the offsets in flight.  The context h for stage 4
+    // loads with them (here only while the registers allow: d <= 4096).
     {
         constexpr int kOffQ = (kChainMaxM + 1 + kChainThreads - 1) / kChainThreads;
         int32_t ov[kOffQ];
 #pragma unroll
         for (int u = 0; u < kOffQ; ++u) ov[u] = A.offsets[min((int)threadIdx.x + kChainThreads * u, M)];
+        if constexpr (kEarly) load_h();
 #pragma unroll
         for (int u = 0; u < kOffQ; ++u)
             if ((int)threadIdx.x + kChainThreads * u <= M) offs[threadIdx.x + kChainThreads * u] = ov[u];
