@@ -50,8 +50,9 @@ constexpr int kChainThreads = kThreads;  // 4 waves per workgroup
 constexpr int kChainWaves = kChainThreads / kWave;
 
 // words of the chain region of the workspace: epoch, error, then tagged
-// hidden [H], scores [M] and partials [G][4]
-constexpr int kPartWords = 4;
+// hidden [H], scores [M] and partials [G][3] (best key high, low; sum of
+// exponentials: the partial's maximum logit is its best key's value)
+constexpr int kPartWords = 3;
 constexpr int kChainMaxGrid = 1024;  // workgroups at most (twice the compute units, capped)
 
 struct ChainArgs {
@@ -89,15 +90,14 @@ struct ChainArgs {
 };
 
 // Bytes of dynamic LDS: scores [M], offsets [M + 1], candidate keys [M],
-// shortlist ids [k] and offsets [k + 1], hidden [H], the G partials' words.
-__host__ __device__ inline size_t chain_lds_bytes(int M, int k, int H, int G) {
+// shortlist ids [k] and offsets [k + 1], hidden [H].
+__host__ __device__ inline size_t chain_lds_bytes(int M, int k, int H) {
     size_t b = (size_t)M * 4 + (size_t)(M + 1) * 4;
     b = (b + 15) / 16 * 16;
     b += (size_t)M * 8;
     b += (size_t)k * 4 + (size_t)(k + 1) * 4;
     b = (b + 15) / 16 * 16;
     b += (size_t)H * 4;
-    b += (size_t)G * kPartWords * 4;
     return b;
 }
 
@@ -252,6 +252,48 @@ __device__ __forceinline__ void wave_min_max(float& lo, float& hi) {
     step(std::integral_constant<int, kRowShr8>{}, std::integral_constant<int, 0xf>{});
     step(std::integral_constant<int, kRowBcast15>{}, std::integral_constant<int, 0xa>{});
     step(std::integral_constant<int, kRowBcast31>{}, std::integral_constant<int, 0xc>{});
+}
+
+// Lane l of one wave reads the partials g = l + 64 (u0 + u), u < U (those
+// below G; kPartWords tagged words each) into raw, re-polling its stale words
+// together until they carry epoch e or the time bound runs out.  Returns true
+// if it gave up.
+template <int U>
+__device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* src, int G, int u0, uint32_t e,
+                                           uint32_t (&raw)[U * kPartWords]) {
+    constexpr int P = kPartWords;
+    bool gave_up = false;
+    const uint64_t t0 = wall_clock64();
+    const int l = lane_id();
+    uint64_t v[U * P];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int g = l + kWave * (u0 + u);
+#pragma unroll
+        for (int w = 0; w < P; ++w) v[u * P + w] = g < G ? load_coherent(src + (int64_t)g * P + w) : tagged(e, 0u);
+    }
+    for (;;) {
+        bool stale = false;
+#pragma unroll
+        for (int q = 0; q < U * P; ++q) stale |= (uint32_t)(v[q] >> 32) != e;
+        if (!stale) break;
+        if (wall_clock64() - t0 > A.spin_ticks) {
+            store_coherent(A.err, 1u);
+            gave_up = true;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int g = l + kWave * (u0 + u);
+#pragma unroll
+            for (int w = 0; w < P; ++w)
+                if ((uint32_t)(v[u * P + w] >> 32) != e) v[u * P + w] = load_coherent(src + (int64_t)g * P + w);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < U * P; ++q) raw[q] = (uint32_t)v[q];
+    return gave_up;
 }
 
 // The k best of the M <= NT * kSelQ scores v[] (registers; thread t holds
@@ -489,7 +531,6 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     int32_t* rowoff = sid + k;                                // [k + 1]
     o = (o + (size_t)k * 4 + (size_t)(k + 1) * 4 + 15) / 16 * 16;
     float* hid = reinterpret_cast<float*>(smem + o);          // [H]
-    uint32_t* pv = reinterpret_cast<uint32_t*>(hid + H);      // [G][kPartWords]
 
     const int G = gridDim.x;
     const uint32_t e = __builtin_amdgcn_readfirstlane(load_coherent(A.epoch)) + 1u;
@@ -651,8 +692,9 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
         __shared__ uint64_t w_best[NW];
         __shared__ float w_m[NW], w_s[NW];
         __shared__ int w_bad[NW];
+        // the wave's maximum logit is the value of its best key
         const uint64_t wb = wave_max_u64(st.best);
-        const float wm = readlane_f32(wave_max_f32(st.m), kWave - 1);
+        const float wm = wb != 0 ? key_val(wb) : -__builtin_inff();
         const float wsum = wave_sum(st.m == -__builtin_inff() ? 0.0f : st.s * expf((st.m - wm) * A.inv_t));
         const bool wbad = __ballot(bad) != 0;
         if (lane == 0) {
@@ -674,54 +716,46 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
             uint64_t* pw = A.tpart + (int64_t)blockIdx.x * kPartWords;
             store_coherent(pw + 0, tagged(e, (uint32_t)(bb >> 32)));
             store_coherent(pw + 1, tagged(e, (uint32_t)bb));
-            store_coherent(pw + 2, tagged(e, __float_as_uint(bm)));
-            store_coherent(pw + 3, tagged(e, __float_as_uint(any_bad ? -1.0f : bs)));
+            store_coherent(pw + 2, tagged(e, __float_as_uint(any_bad ? -1.0f : bs)));
         }
         // the selection outputs come from the last workgroup, after its
         // partial is out (off the merging workgroup's path when G > 1)
         if (blockIdx.x == G - 1) chain_outputs<kChainThreads>(A, sv, sid, cand, rowoff, k, L);
         if (blockIdx.x != 0) return;
 
-        // workgroup 0: thread t merges partials t, t + NT, ... in order, then a
-        // fixed-order wave and workgroup reduction.  The error word (set by a
-        // wait that gave up, possibly in a straggler of an earlier launch) is
-        // read alongside the partials.
-        __syncthreads();
-        const uint32_t err_word = threadIdx.x == 0 ? load_coherent(A.err) : 0u;
-        const bool late = poll_words<kChainThreads>(A, A.tpart, G * kPartWords, e, pv);
-        __syncthreads();
+        // workgroup 0, wave 0: lane l polls and merges partials l, l + 64, ...
+        // in order, then a fixed-order wave reduction (no barrier on this
+        // path).  The error word (set by a wait that gave up, possibly in a
+        // straggler of an earlier launch) is read alongside the partials.
+        if (wv != 0) return;
+        constexpr int kLaneParts = kChainMaxGrid / kWave;
+        const uint32_t err_word = lane == 0 ? load_coherent(A.err) : 0u;
         uint64_t bb = 0;
         float bm = -__builtin_inff(), bs = 0.0f;
-        bool fail = late;
-        for (int g = threadIdx.x; g < G; g += kChainThreads) {
-            const uint32_t* q = pv + g * kPartWords;
-            const uint64_t k2 = ((uint64_t)q[0] << 32) | q[1];
-            const float s2 = __uint_as_float(q[3]);
-            fail |= s2 < 0.0f;
-            bb = k2 > bb ? k2 : bb;
-            softmax_merge(bm, bs, __uint_as_float(q[2]), s2 < 0.0f ? 0.0f : s2, A.inv_t);
+        bool fail = false;
+        for (int u0 = 0; u0 < kLaneParts; u0 += 4) {
+            if (u0 * kWave >= G) break;
+            uint32_t raw[4 * kPartWords];
+            fail |= poll_parts<4>(A, A.tpart, G, u0, e, raw);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int g = lane + kWave * (u0 + u);
+                if (g >= G) continue;
+                const uint64_t k2 = ((uint64_t)raw[u * kPartWords] << 32) | raw[u * kPartWords + 1];
+                const float s2 = __uint_as_float(raw[u * kPartWords + 2]);
+                fail |= s2 < 0.0f;
+                bb = k2 > bb ? k2 : bb;
+                softmax_merge(bm, bs, k2 != 0 ? key_val(k2) : -__builtin_inff(), s2 < 0.0f ? 0.0f : s2, A.inv_t);
+            }
         }
         const uint64_t gb = wave_max_u64(bb);
-        const float gm = readlane_f32(wave_max_f32(bm), kWave - 1);
+        const float gm = gb != 0 ? key_val(gb) : -__builtin_inff();
         const float gs = wave_sum(bm == -__builtin_inff() ? 0.0f : bs * expf((bm - gm) * A.inv_t));
         const bool gfail = __ballot(fail) != 0;
-        __syncthreads();
         if (lane == 0) {
-            w_best[wv] = gb;
-            w_m[wv] = gm;
-            w_s[wv] = gs;
-            w_bad[wv] = gfail;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            uint64_t fb = w_best[0];
-            float fm = w_m[0], fs = w_s[0];
-            bool err = w_bad[0] != 0 || err_word != 0u;
-            for (int q = 1; q < NW; ++q) {
-                fb = w_best[q] > fb ? w_best[q] : fb;
-                softmax_merge(fm, fs, w_m[q], w_s[q], A.inv_t);
-                err |= w_bad[q] != 0;
-            }
+            uint64_t fb = gb;
+            const float fm = gm, fs = gs;
+            const bool err = gfail || err_word != 0u;
             // every workgroup has read the epoch (its partial carries it)
             if (err) {
                 store_coherent(A.err, 0u);
@@ -762,7 +796,7 @@ size_t chain_region_bytes(int32_t H, int32_t M) {
 bool chain_step_eligible(const ChainRequest& q) {
     const int kmax = std::max(q.d_r, std::max(q.H, q.d));
     return q.all_bf16 && q.region != nullptr && kmax <= 8192 && q.M <= kChainMaxM && q.V < (1 << kLenBits) &&
-           chain_lds_bytes(q.M, q.k, q.H, kChainMaxGrid) <= 160 * 1024;
+           chain_lds_bytes(q.M, q.k, q.H) <= 160 * 1024;
 }
 
 dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
@@ -822,7 +856,7 @@ dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
     a.beta = q.beta;
     // every wait is bounded by 0.2 s of wall clock
     a.spin_ticks = (uint64_t)tick_khz[dev].load() * 200;
-    const size_t lds = chain_lds_bytes(q.M, q.k, q.H, grid);
+    const size_t lds = chain_lds_bytes(q.M, q.k, q.H);
     const int nb = (std::max(q.d_r, std::max(q.H, q.d)) + 511) / 512;
     if (nb <= 1) return launch_chain_nb<1, 4>(a, grid, lds, s);
     if (nb <= 2) return launch_chain_nb<2, 4>(a, grid, lds, s);
