@@ -677,6 +677,14 @@ def test_tiny_vocab_every_k():
 FUSED_CASES = [c for c in CASES if c.B == 1] + [
     case("fused_big", V=20000, d=1024, M=100, H=64, k=12, B=1),
     case("fused_f32", V=3000, d=128, M=24, H=16, k=5, B=1, dtype="f32"),
+    # one-launch step shapes: a single linear router; d above 4096 (h loaded
+    # for the gathered head, two rows per wave) with more hidden units than
+    # waves (two W1 rows per wave); k = M (the shortlist is the vocabulary);
+    # M at its one-launch maximum of 1024
+    case("chain_linear", V=6000, d=256, M=50, H=0, act="none", k=6, B=1),
+    case("chain_wide", V=9000, d=5120, M=256, H=1536, k=64, B=1),
+    case("chain_k_eq_m", V=2000, d=128, M=16, H=16, k=16, B=1),
+    case("chain_m1024", V=50000, d=256, M=1024, H=64, k=100, B=1),
 ]
 
 
