@@ -90,12 +90,12 @@ struct ChainArgs {
 };
 
 // Bytes of dynamic LDS: scores [M], offsets [M + 1], candidate keys [M],
-// shortlist ids [k] and offsets [k + 1], hidden [H].
+// shortlist ids [k], offsets [k + 1] and slab starts [k], hidden [H].
 __host__ __device__ inline size_t chain_lds_bytes(int M, int k, int H) {
     size_t b = (size_t)M * 4 + (size_t)(M + 1) * 4;
     b = (b + 15) / 16 * 16;
     b += (size_t)M * 8;
-    b += (size_t)k * 4 + (size_t)(k + 1) * 4;
+    b += (size_t)k * 4 + (size_t)(k + 1) * 4 + (size_t)k * 4;
     b = (b + 15) / 16 * 16;
     b += (size_t)H * 4;
     return b;
@@ -299,7 +299,8 @@ __device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* s
 // The k best of the M <= NT * kSelQ scores v[] (registers; thread t holds
 // ids kSelQ t + q) by (score desc, id asc), as the shortlist in ascending
 // cluster id: sid[0..k) the ids, mkey[0..k) their (score, id) keys,
-// rowoff[0..k] the exclusive prefix of their slab sizes.  Returns the
+// rowoff[0..k] the exclusive prefix of their slab sizes, sbase[0..k) their
+// slabs' first layout rows.  Returns the
 // shortlist length; sets `bad` in thread 0 when the members are not k.
 //
 // Each score gets a class that is monotone in the score: 0 for -inf and
@@ -314,8 +315,8 @@ __device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* s
 // candidate area (cand[0..k)), which the ranking has finished reading by then.
 template <int NT>
 __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32_t* offs, int M, int k,
-                                            uint64_t* cand, int32_t* sid, int32_t* rowoff, uint32_t* err,
-                                            bool& bad) {
+                                            uint64_t* cand, int32_t* sid, int32_t* rowoff, int32_t* sbase,
+                                            uint32_t* err, bool& bad) {
     static_assert(NT == 256, "one histogram bin per thread");
     constexpr int NW = NT / kWave;
     constexpr int Q = kSelQ;
@@ -431,7 +432,7 @@ __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32
 
     // the shortlist in ascending id, which is thread order: one scan of the
     // packed (member count, slab length) of each thread
-    int sz[Q];
+    int sz[Q], base[Q];
     uint32_t mine = 0;
     {
         int o[Q + 1];
@@ -448,6 +449,7 @@ __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32
         }
 #pragma unroll
         for (int q = 0; q < Q; ++q) {
+            base[q] = o[q];
             sz[q] = mem[q] ? o[q + 1] - o[q] : 0;
             mine += (mem[q] ? 1u << kLenBits : 0u) + (uint32_t)sz[q];
         }
@@ -471,6 +473,7 @@ __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32
                 sid[pos] = id0 + q;
                 cand[pos] = key[q];
                 rowoff[pos] = off;
+                sbase[pos] = base[q];
             }
             ++pos;
             off += sz[q];
@@ -529,7 +532,8 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     o += (size_t)M * 8;
     int32_t* sid = reinterpret_cast<int32_t*>(smem + o);      // [k] ids ascending
     int32_t* rowoff = sid + k;                                // [k + 1]
-    o = (o + (size_t)k * 4 + (size_t)(k + 1) * 4 + 15) / 16 * 16;
+    int32_t* sbase = rowoff + k + 1;                          // [k] slab starts (layout rows)
+    o = (o + (size_t)k * 4 + (size_t)(k + 1) * 4 + (size_t)k * 4 + 15) / 16 * 16;
     float* hid = reinterpret_cast<float*>(smem + o);          // [H]
 
     const int G = gridDim.x;
@@ -619,16 +623,23 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
             if ((int)threadIdx.x * kSelQ + q < M) sv[threadIdx.x * kSelQ + q] = v[q];
         }
     }
-    const int L = chain_select<kChainThreads>(v, offs, M, k, cand, sid, rowoff, A.err, bad);
+    const int L = chain_select<kChainThreads>(v, offs, M, k, cand, sid, rowoff, sbase, A.err, bad);
 
     // ---- stage 4: logits over the wave's contiguous range of shortlist slots
     if constexpr (!kEarly) load_h();
     GreedyState st;
     {
         const int64_t p0 = (int64_t)gw * L / nw, p1 = (int64_t)(gw + 1) * L / nw;
-        // cluster position of slot p0: the first i with rowoff[i + 1] > p0
+        // slot q's cluster position: the number of clusters whose slabs end at
+        // or before q.  With k <= 64, lane i holds cluster i's end, start
+        // offset and slab start, and a ballot counts (one LDS round trip);
+        // else a binary search for the first slot's cluster and a walk.
+        const bool lanes = k <= kWave;
+        const int my_end = lanes && lane < k ? rowoff[lane + 1] : 0x7fffffff;
+        const int my_off = lanes && lane < k ? rowoff[lane] : 0;
+        const int my_base = lanes && lane < k ? sbase[lane] : 0;
         int ci = 0;
-        if (p0 < p1) {
+        if (!lanes && p0 < p1) {
             int lo = 0, hi = k - 1;
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
@@ -643,8 +654,13 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const int q = (int)p + min(r, nrow - 1);
-                while (q >= rowoff[ci + 1]) ++ci;
-                lrow[r] = (int64_t)offs[sid[ci]] + (q - rowoff[ci]);
+                if (lanes) {
+                    const int c = __builtin_amdgcn_readfirstlane(__popcll(__ballot(my_end <= q)));
+                    lrow[r] = (int64_t)__builtin_amdgcn_readlane(my_base, c) + (q - __builtin_amdgcn_readlane(my_off, c));
+                } else {
+                    while (q >= rowoff[ci + 1]) ++ci;
+                    lrow[r] = (int64_t)sbase[ci] + (q - rowoff[ci]);
+                }
             }
             Raw8<uint16_t> w[R][NB];
 #pragma unroll
