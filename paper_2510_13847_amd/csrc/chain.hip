@@ -255,9 +255,10 @@ __device__ __forceinline__ void wave_min_max(float& lo, float& hi) {
 }
 
 // Lane l of one wave reads the partials g = l + 64 (u0 + u), u < U (those
-// below G; kPartWords tagged words each) into raw, re-polling its stale words
-// together until they carry epoch e or the time bound runs out.  Returns true
-// if it gave up.
+// below G; kPartWords tagged words each) into raw, re-reading them all
+// together until every word carries epoch e or the time bound runs out.
+// Every read is issued without a branch (lanes past G re-read partial
+// G - 1), so that one round is one round trip.  Returns true if it gave up.
 template <int U>
 __device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* src, int G, int u0, uint32_t e,
                                            uint32_t (&raw)[U * kPartWords]) {
@@ -265,17 +266,25 @@ __device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* s
     bool gave_up = false;
     const uint64_t t0 = wall_clock64();
     const int l = lane_id();
-    uint64_t v[U * P];
+    const uint64_t* ps[U];
+    bool in[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int g = l + kWave * (u0 + u);
-#pragma unroll
-        for (int w = 0; w < P; ++w) v[u * P + w] = g < G ? load_coherent(src + (int64_t)g * P + w) : tagged(e, 0u);
+        in[u] = g < G;
+        ps[u] = src + (int64_t)min(g, G - 1) * P;
     }
+    uint64_t v[U * P];
     for (;;) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int w = 0; w < P; ++w) v[u * P + w] = load_coherent(ps[u] + w);
         bool stale = false;
 #pragma unroll
-        for (int q = 0; q < U * P; ++q) stale |= (uint32_t)(v[q] >> 32) != e;
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int w = 0; w < P; ++w) stale |= in[u] && (uint32_t)(v[u * P + w] >> 32) != e;
         if (!stale) break;
         if (wall_clock64() - t0 > A.spin_ticks) {
             store_coherent(A.err, 1u);
@@ -283,13 +292,6 @@ __device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* s
             break;
         }
         __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int g = l + kWave * (u0 + u);
-#pragma unroll
-            for (int w = 0; w < P; ++w)
-                if ((uint32_t)(v[u * P + w] >> 32) != e) v[u * P + w] = load_coherent(src + (int64_t)g * P + w);
-        }
     }
 #pragma unroll
     for (int q = 0; q < U * P; ++q) raw[q] = (uint32_t)v[q];
