@@ -570,7 +570,7 @@ def main():
     k_flops = 2.0 * w.d * float(np.mean([rows[i % POOL] for i in range(n_kt)]))
 
     rec = {
-        "metric": "draft-head steps/s (dynamic vocabulary head, 1 GPU)",
+        "metric": "draft-head steps/s + achieved HBM GB/s (% peak) vs dense full-vocab head, 1 GPU",
         "value": round(steps_per_s, 2),
         "unit": "steps/s",
         "n_gpus": 1,
