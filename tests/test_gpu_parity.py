@@ -117,11 +117,14 @@ def test_layout_with_empty_clusters_and_bad_ids():
 
 
 # ---------------------------------------------------------------- router
-@pytest.mark.parametrize("path", [0, 1, 2, 3])
-@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def _paths(paths, mfma_from):
+    """(case, path) pairs; the MFMA paths (path >= mfma_from) take bf16 weights only."""
+    return [pytest.param(w, p, id=f"{w.name}-{p}") for w in CASES for p in paths
+            if p < mfma_from or w.dtype != "f32"]
+
+
+@pytest.mark.parametrize("w,path", _paths([0, 1, 2, 3], 2))
 def test_route_parity(w, path):
-    if path >= 2 and w.dtype == "f32":
-        pytest.skip("MFMA router path needs bf16 weights")
     p = Problem(w)
     D.set_option(D.OPT_ROUTER_PATH, path)
     try:
@@ -208,12 +211,10 @@ def _random_selection(p, B, k, seed):
     return np.array(rows, dtype=np.int32)
 
 
-@pytest.mark.parametrize("path", [1, 2, 3])
-@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+@pytest.mark.parametrize("w,path", _paths([1, 2, 3], 2))
 def test_logits_parity(w, path):
-    """Paths: 1 GEMV, 2 MFMA with LDS-staged slabs, 3 MFMA with direct loads."""
-    if path >= 2 and w.dtype == "f32":
-        pytest.skip("MFMA logits paths need bf16 weights")
+    """Paths: 1 GEMV, 2 MFMA with LDS-staged slabs, 3 MFMA with direct loads
+    (the MFMA paths take bf16 weights only)."""
     p = Problem(w)
     topk = _random_selection(p, w.B, w.k, 3)
     sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
@@ -412,9 +413,11 @@ UNION_VARIANTS = {**{f"dense{c}": (0, c) for c in range(15)}, "gemv": (1, 0), "l
 UNION_EXTRA = {"long_b8": case("long_b8", V=40000, d=64, M=48, H=16, k=12, B=8)}
 
 
-@pytest.mark.parametrize("variant", list(UNION_VARIANTS))
-@pytest.mark.parametrize("name", ["ragged_b3", "ragged_b37", "zipf_b9", "wide_b64", "many_b130", "f32_b5",
-                                  "long_b8"])
+# fp32 heads take the GEMV path only
+@pytest.mark.parametrize("name,variant", [
+    pytest.param(n, v, id=f"{n}-{v}")
+    for n in ["ragged_b3", "ragged_b37", "zipf_b9", "wide_b64", "many_b130", "f32_b5", "long_b8"]
+    for v in UNION_VARIANTS if n != "f32_b5" or v == "gemv"])
 def test_union_shortlist_head(name, variant):
     """Union routing (Sec. 4.2): the rows of a step share one shortlist, the
     union of their selected clusters; every row's logits, tokens and sample
@@ -423,8 +426,6 @@ def test_union_shortlist_head(name, variant):
     workgroup) and the per-chunk-list kernels on the same plan."""
     w = UNION_EXTRA[name] if name in UNION_EXTRA else next(c for c in CASES if c.name == name)
     path, cfg = UNION_VARIANTS[variant]
-    if w.dtype == "f32" and variant != "gemv":
-        pytest.skip("fp32 heads take the GEMV path")
     p = Problem(w)
     mode = D.SEL_TOPK | D.SEL_SAMPLE
     D.set_option(D.OPT_LOGITS_PATH, path)
