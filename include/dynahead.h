@@ -350,8 +350,10 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   0 automatic, else 1, 2 or 4 (capped by the register budget).
  * DYNA_OPT_FUSED_B1: how dyna_draft_head runs a one-context greedy step.
  *   0 (default): one launch (router, top-k, shortlist, gathered logits and
- *   selection with two grid-wide hand-offs) when the router, LM head and
- *   activations are all bf16, d, d_r, H <= 8192 and routing stays on
+ *   selection, the workgroups handing the hidden layer, the router scores
+ *   and their partial results to each other inside the launch) when the
+ *   router, LM head and activations are all bf16, d, d_r, H <= 8192,
+ *   M <= 1024, V < 2^21, the step's LDS fits in 160 KB and routing stays on
  *   `stream`; otherwise as 2.  2: four launches (router layer 1; router
  *   layer 2; top-k with shortlist and plan; gathered head fused with
  *   selection).  1: the separate kernels.  All give bit-identical results.
@@ -366,17 +368,25 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   ring stages, k columns per stage, context columns per pass); 10..13
  *   other shapes of the automatic kernel.
  * DYNA_OPT_GREEDY_GRID: workgroups of the fused one-context gathered head:
- *   0 automatic (256), else 1..4096.
+ *   0 automatic (256), else 1..4096; of the one-launch step: 0 automatic (one
+ *   per compute unit), else that many, at most two per compute unit and 1024.
  * DYNA_OPT_UNION_CFG: shape of the dense union-row kernel of
  *   DYNA_SEL_UNION steps: 0 automatic, 1..14 fixed (waves per workgroup,
  *   row tiles per wave, k columns per stage, ring depth); a shape whose ring does not
  *   fit in LDS for the batch's context count returns DYNA_ERR_UNSUPPORTED.
  * DYNA_OPT_KMEANS_CFG: shape of the k-means assignment kernel: 0
- *   automatic, 1..4 fixed. */
+ *   automatic, 1..4 fixed.
+ * DYNA_OPT_WAIT_BOUND_US: bound of every wait of the one-launch step, in
+ *   microseconds of wall clock: 0 (default) 200000, 1..1000000 that many,
+ *   -1 none (a wait gives up at its first read that finds a word missing;
+ *   for tests of the failure path).  A step in which a wait gave up reports
+ *   out_ids = -1 and out_logprobs = -inf; it clears the error word, and the
+ *   step after it may report the same if a late workgroup set the word
+ *   again. */
 enum { DYNA_OPT_LOGITS_PATH = 1, DYNA_OPT_ROUTER_PATH = 2, DYNA_OPT_KERNEL_TIMING = 3,
        DYNA_OPT_GEMV_ROWS = 4, DYNA_OPT_FUSED_B1 = 5, DYNA_OPT_MFMA_UNROLL = 6,
        DYNA_OPT_GATHER_CFG = 7, DYNA_OPT_GREEDY_GRID = 8, DYNA_OPT_UNION_CFG = 9,
-       DYNA_OPT_KMEANS_CFG = 10 };
+       DYNA_OPT_KMEANS_CFG = 10, DYNA_OPT_WAIT_BOUND_US = 11 };
 dyna_status dyna_set_option(int32_t option, int32_t value);
 
 /* Waits for the events recorded under DYNA_OPT_KERNEL_TIMING and returns the

@@ -28,6 +28,7 @@ std::atomic<int> g_gather_cfg{0};
 std::atomic<int> g_greedy_grid{0};
 std::atomic<int> g_union_cfg{0};
 std::atomic<int> g_kmeans_cfg{0};
+std::atomic<int> g_wait_bound_us{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -112,6 +113,7 @@ int option_gather_cfg() { return g_gather_cfg.load(); }
 int option_greedy_grid() { return g_greedy_grid.load(); }
 int option_union_cfg() { return g_union_cfg.load(); }
 int option_kmeans_cfg() { return g_kmeans_cfg.load(); }
+int option_wait_bound_us() { return g_wait_bound_us.load(); }
 
 // ------------------------------------------------------------------ workspace
 // One carving serves every hot entry point, so a single workspace can back a
@@ -394,6 +396,11 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
     if (option == DYNA_OPT_GREEDY_GRID) {
         REQUIRE(value >= 0 && value <= kGreedyMaxBlocks, "greedy grid %d outside [0, %d]", value, kGreedyMaxBlocks);
         g_greedy_grid.store(value);
+        return DYNA_OK;
+    }
+    if (option == DYNA_OPT_WAIT_BOUND_US) {
+        REQUIRE(value >= -1 && value <= 1000000, "wait bound %d us outside [-1, 1000000]", value);
+        g_wait_bound_us.store(value);
         return DYNA_OK;
     }
     if (option == DYNA_OPT_KMEANS_CFG) {

@@ -817,6 +817,8 @@ bool chain_step_eligible(const ChainRequest& q) {
            chain_lds_bytes(q.M, q.k, q.H) <= 160 * 1024;
 }
 
+int option_wait_bound_us();  // DYNA_OPT_WAIT_BOUND_US: 0 default, -1 none, else microseconds
+
 dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
     if (!chain_step_eligible(q)) return set_error(DYNA_ERR_UNSUPPORTED, "one-launch step: shape");
     static std::atomic<int> cus[kMaxDevices] = {};
@@ -872,8 +874,11 @@ dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
     a.out_logprobs = q.out_logprobs;
     a.inv_t = q.inv_t;
     a.beta = q.beta;
-    // every wait is bounded by 0.2 s of wall clock
-    a.spin_ticks = (uint64_t)tick_khz[dev].load() * 200;
+    // every wait is bounded by 0.2 s of wall clock (or the bound set by
+    // DYNA_OPT_WAIT_BOUND_US; -1: a wait gives up at its first read that
+    // finds a word missing)
+    const int bound_us = option_wait_bound_us();
+    a.spin_ticks = bound_us < 0 ? 0 : (uint64_t)tick_khz[dev].load() * (uint64_t)(bound_us > 0 ? bound_us : 200000) / 1000;
     const size_t lds = chain_lds_bytes(q.M, q.k, q.H);
     const int nb = (std::max(q.d_r, std::max(q.H, q.d)) + 511) / 512;
     if (nb <= 1) return launch_chain_nb<1, 4>(a, grid, lds, s);

@@ -766,3 +766,43 @@ def test_one_launch_step_ties(variant):
             # the tied clusters taken are the lowest ids of the tied run
             tied = sorted(c for c in got if c >= 3)
             assert tied == list(range(3, 3 + len(tied)))
+
+
+def test_one_launch_step_wait_bound():
+    """Every wait of the one-launch step is bounded.  With the bound forced
+    from the host to nothing (a wait gives up at its first read that finds a
+    word missing), a step must report the failure (id -1, log-probability
+    -inf) and never a token from half-written data; once the bound is back,
+    the steps are correct again (the step that reports an error clears it; the
+    first step after may still report one set late in the failed launch)."""
+    w = next(c for c in FUSED_CASES if c.name == "chain_wide")
+    p = Problem(w)
+    mode = D.SEL_ARGMAX
+    one = D.DraftHead(p.R, p.L, 1, w.k, mode, 1, keep_logits=True)
+    sep = D.DraftHead(p.R, p.L, 1, w.k, mode, 1, keep_logits=True)
+
+    def step(it, bound):
+        x = W.contexts(w, "cpu", salt=it).to(DEV)
+        D.set_option(D.OPT_WAIT_BOUND_US, bound)
+        try:
+            one(x, x)
+            D.set_option(D.OPT_FUSED_B1, 1)
+            sep(x, x)
+        finally:
+            D.set_option(D.OPT_FUSED_B1, 0)
+            D.set_option(D.OPT_WAIT_BOUND_US, 0)
+        torch.cuda.synchronize()
+        got, want = int(one.ids[0, 0]), int(sep.ids[0, 0])
+        if got == -1:
+            assert float(one.logprobs[0, 0]) == -np.inf
+            return False
+        assert got == want and torch.equal(one.clusters, sep.clusters)
+        return True
+
+    with pytest.raises(D.DynaError):
+        D.set_option(D.OPT_WAIT_BOUND_US, -2)
+    assert step(0, 0)
+    forced = [step(1 + i, -1) for i in range(3)]
+    assert not all(forced)  # at least one forced step found a word missing
+    step(4, 0)  # may report an error set late in the last forced step
+    assert step(5, 0) and step(6, 0)
