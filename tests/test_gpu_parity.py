@@ -434,8 +434,9 @@ def test_union_shortlist_head(name, variant):
         try:
             head = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode | D.SEL_UNION, k_t=w.k_t, uniforms=p.ud)
         except D.DynaError as e:
-            if e.status == D.ERR_UNSUPPORTED and "does not fit" in str(e):
-                pytest.skip("union shape does not fit in LDS at this context count")
+            # a fixed shape may not fit; the automatic one must always run
+            if e.status == D.ERR_UNSUPPORTED and "does not fit" in str(e) and cfg != 0:
+                pytest.skip("fixed union shape does not fit in LDS at this context count")
             raise
         torch.cuda.synchronize()
     finally:
