@@ -27,6 +27,16 @@ def test_library_loads_and_exports_every_declared_symbol():
     assert lib.dyna_abi_version() == D.ABI_VERSION == 2
 
 
+def test_header_constants_match_the_binding():
+    """Every DYNA_OPT_*, DYNA_SEL_* and DYNA_ERR_* value the header defines is
+    the value the Python binding passes."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    found = dict((n, int(v, 0)) for n, v in re.findall(r"\bDYNA_((?:OPT|SEL|ERR)_[A-Z0-9_]+)\s*=\s*(-?(?:0x[0-9a-fA-F]+|\d+))", text))
+    assert any(n.startswith("OPT_") for n in found)
+    for name, value in found.items():
+        assert getattr(D, name, None) == value, f"DYNA_{name} = {value} in the header"
+
+
 def test_status_strings():
     lib = D.lib()
     for code, name in enumerate(["DYNA_OK", "DYNA_ERR_INVALID_ARG", "DYNA_ERR_CAPACITY",
@@ -47,6 +57,10 @@ def test_set_option_validation():
     assert lib.dyna_set_option(D.OPT_UNION_CFG, 0) == D.OK
     assert lib.dyna_set_option(D.OPT_KMEANS_CFG, 5) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_KMEANS_CFG, 0) == D.OK
+    for v in (-2, 1000001):
+        assert lib.dyna_set_option(D.OPT_WAIT_BOUND_US, v) == D.ERR_INVALID_ARG
+    for v in (-1, 1, 1000000, 0):
+        assert lib.dyna_set_option(D.OPT_WAIT_BOUND_US, v) == D.OK
     assert lib.dyna_set_option(D.OPT_FUSED_B1, 3) == D.ERR_INVALID_ARG
     for v in (2, 1, 0):
         assert lib.dyna_set_option(D.OPT_FUSED_B1, v) == D.OK
