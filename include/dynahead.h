@@ -30,7 +30,9 @@
  *    then ascending vocabulary id inside each cluster (= layout order).
  *  - Results are bit-identical from run to run (no floating-point atomics).
  *  - Calls are thread-safe for distinct workspaces; dyna_last_error() is
- *    per host thread.
+ *    per host thread.  The options of dyna_set_option are process-wide
+ *    diagnostics for tests and measurement: set them while no other thread
+ *    is calling the library.
  */
 #ifndef DYNAHEAD_H
 #define DYNAHEAD_H
@@ -85,7 +87,9 @@ typedef struct dyna_layout {
 /* Router r: R^{d_r} -> R^M (Sec. 4.2, "Low-cost router").
  * H > 0: s = W2 . act(W1 . x + b1) + b2, W1 [H, d_r], W2 [M, H].
  * H = 0: s = W1 . x + b1, W1 [M, d_r] (a single linear map).
- * The hidden activation is kept in fp32 (never re-rounded to bf16). */
+ * The hidden activation is kept in fp32 between the layers.  The GEMV and
+ * one-launch paths use it as fp32; the matrix-core path for batches feeds it
+ * to the second layer as two bf16 terms, hi + lo (16 significant bits). */
 typedef struct dyna_router {
     int32_t d_r, H, M;
     int32_t wdtype;            /* dyna_dtype of W1 and W2 */
@@ -178,7 +182,9 @@ dyna_status dyna_shortlist_logits(const dyna_layout* L, const void* h, int32_t h
  *  out_logprobs [B, k_t] device output, may be NULL
  *  uniforms [B]        device, u in [0, 1), required with DYNA_SEL_SAMPLE
  *  out_sample [B]      device output (SAMPLE): first j in shortlist order whose
- *                      CDF exceeds u, else the last j with nonzero mass
+ *                      CDF exceeds u, else the last j with nonzero mass; -1
+ *                      when the shortlist is empty (only empty clusters were
+ *                      selected: no token is proposed)
  *  out_sample_logprob [B] device output, may be NULL
  *  tail_beta           weight beta in [0, 1) of the tail mixture proposal
  *                      q~ = (1 - beta) q_S + beta omega (Sec. 5), omega uniform
@@ -353,8 +359,9 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   selection, the workgroups handing the hidden layer, the router scores
  *   and their partial results to each other inside the launch) when the
  *   router, LM head and activations are all bf16, d, d_r, H <= 8192,
- *   M <= 1024, V < 2^21, the step's LDS fits in 160 KB and routing stays on
- *   `stream`; otherwise as 2.  2: four launches (router layer 1; router
+ *   M <= 1024, V < 2^21, the step's LDS fits in 160 KB, routing stays on
+ *   `stream` and the occupancy calculator finds room for the whole grid at
+ *   once (its workgroups hand words to each other); otherwise as 2.  2: four launches (router layer 1; router
  *   layer 2; top-k with shortlist and plan; gathered head fused with
  *   selection).  1: the separate kernels.  All give bit-identical results.
  *   Under kernel timing the one-launch step, or the fused gathered-head +
@@ -369,7 +376,8 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   other shapes of the automatic kernel.
  * DYNA_OPT_GREEDY_GRID: workgroups of the fused one-context gathered head:
  *   0 automatic (256), else 1..4096; of the one-launch step: 0 automatic (one
- *   per compute unit), else that many, at most two per compute unit and 1024.
+ *   per compute unit), else that many, capped at 1024 and at what the
+ *   occupancy calculator says can be resident at once.
  * DYNA_OPT_UNION_CFG: shape of the dense union-row kernel of
  *   DYNA_SEL_UNION steps: 0 automatic, 1..14 fixed (waves per workgroup,
  *   row tiles per wave, k columns per stage, ring depth); a shape whose ring does not
@@ -380,9 +388,10 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   microseconds of wall clock: 0 (default) 200000, 1..1000000 that many,
  *   -1 none (a wait gives up at its first read that finds a word missing;
  *   for tests of the failure path).  A step in which a wait gave up reports
- *   out_ids = -1 and out_logprobs = -inf; it clears the error word, and the
- *   step after it may report the same if a late workgroup set the word
- *   again. */
+ *   out_ids = -1 and out_logprobs = -inf.  The error word carries the epoch
+ *   of the launch that set it, so a later step is not failed by it; only a
+ *   workgroup of a failed launch that started after the failure was
+ *   reported fails the next step too, which may read its stale words. */
 enum { DYNA_OPT_LOGITS_PATH = 1, DYNA_OPT_ROUTER_PATH = 2, DYNA_OPT_KERNEL_TIMING = 3,
        DYNA_OPT_GEMV_ROWS = 4, DYNA_OPT_FUSED_B1 = 5, DYNA_OPT_MFMA_UNROLL = 6,
        DYNA_OPT_GATHER_CFG = 7, DYNA_OPT_GREEDY_GRID = 8, DYNA_OPT_UNION_CFG = 9,

@@ -30,12 +30,14 @@ Readings where the paper is silent (each is listed in the design notes):
     shortlist order and returns the first j with F_j > u, else the last j
     with p_j > 0;
   * the router's hidden activation is not re-rounded (fp64 here);
+  * clusters may be empty (no balance is enforced), so a context can select
+    only empty clusters: its shortlist is empty and it proposes no token (no
+    ids, no sample);
   * the partition itself comes from spherical k-means on the unit LM-head
     rows (Sec. 4.2): centroids start at caller-chosen points, each round
-    assigns every point to its most similar centroid (ties to the lower id;
-    the similarity is taken with centroids in bf16, the kernel's operand
-    precision) and then sets each centroid to the mean direction of its
-    points; an empty cluster keeps its centroid.
+    assigns every point to its most similar centroid (cosine similarity in
+    float64; ties to the lower id) and then sets each centroid to the mean
+    direction of its points; an empty cluster keeps its centroid.
 
 Every function below has a pin in tests/test_oracle_pins.py.
 """
@@ -195,8 +197,11 @@ def shortlist_logits(h, W_lm, vocab_ids) -> np.ndarray:
 # Sec. 5: the restricted, renormalised draft q_S)
 # --------------------------------------------------------------------------
 def log_softmax(z, temperature: float = 1.0) -> np.ndarray:
-    """log q_S over the shortlist: z/T - log(sum exp(z/T)), shifted by the max."""
+    """log q_S over the shortlist: z/T - log(sum exp(z/T)), shifted by the max.
+    An empty shortlist has no log-probabilities."""
     t = np.asarray(z, dtype=np.float64) / float(temperature)
+    if t.size == 0:
+        return t
     mx = np.max(t)
     return t - (mx + np.log(np.sum(np.exp(t - mx))))
 
@@ -211,9 +216,12 @@ def sample_inverse_cdf(z, u: float, temperature: float = 1.0) -> int:
     """Shortlist position drawn from softmax(z/T) by the inverse CDF at u.
 
     The CDF runs in shortlist order; the answer is the first j with F_j > u,
-    else (when rounding leaves F_n <= u) the last j with p_j > 0.
+    else (when rounding leaves F_n <= u) the last j with p_j > 0.  An empty
+    shortlist gives -1 (no token).
     """
     t = np.asarray(z, dtype=np.float64) / float(temperature)
+    if t.size == 0:
+        return -1
     p = np.exp(t - np.max(t))
     p = p / p.sum()
     F = np.cumsum(p)
@@ -246,6 +254,13 @@ def draft_select(z, vocab_ids, k_t: int = 1, temperature: float = 1.0, u=None, b
     complement leaves q~ = q_S.
     """
     vocab_ids = np.asarray(vocab_ids, dtype=np.int64)
+    if vocab_ids.size == 0 and (complement_ids is None or len(complement_ids) == 0 or beta <= 0.0):
+        # only empty clusters were selected: nothing to propose
+        e = np.zeros(0, dtype=np.int64)
+        out = dict(ids=e, logprobs=np.zeros(0), positions=e)
+        if u is not None:
+            out.update(sample_id=-1, sample_pos=-1, sample_logprob=-np.inf)
+        return out
     C = 0 if complement_ids is None else len(complement_ids)
     b = float(beta) if (beta > 0.0 and C > 0) else 0.0
     lp = log_softmax(z, temperature) + (np.log1p(-b) if b > 0.0 else 0.0)
@@ -379,19 +394,6 @@ def pa_fr_budget(t: int, k_max: int) -> int:
 # --------------------------------------------------------------------------
 # building the partition: spherical k-means (Sec. 4.2, "Vocabulary partition")
 # --------------------------------------------------------------------------
-def round_bf16(a) -> np.ndarray:
-    """Values rounded to bf16 (round to nearest, ties to even), returned as
-    float64.  Used only where a decision is taken in the kernel's operand
-    precision: a float32 value keeps its upper 16 bits after adding half an
-    ulp of bf16 plus the parity bit of the kept part."""
-    f = np.asarray(a, dtype=np.float64).astype(np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    keep = ((u >> np.uint64(16)) & np.uint64(1))
-    r = ((u + np.uint64(0x7FFF) + keep) >> np.uint64(16)) << np.uint64(16)
-    r = np.where(np.isnan(f), u, r)  # NaN stays NaN
-    return (r.astype(np.uint32)).view(np.float32).astype(np.float64)
-
-
 def unit_rows(W) -> np.ndarray:
     """The paper's points: every LM-head column (here row) divided by its
     2-norm; an all-zero row stays zero (it has no direction)."""
@@ -406,10 +408,9 @@ def unit_rows(W) -> np.ndarray:
 def kmeans_assign(W, centroids):
     """Assignment step: each point goes to the centroid of largest cosine
     similarity, x_v . mu_m for unit mu_m; ties go to the lower cluster id.
-    The centroids enter in the kernel's operand precision (bf16); the
-    similarities are formed in float64.  Returns (assign[V], S[V, M])."""
+    Everything in float64 from the exact inputs.  Returns (assign[V], S[V, M])."""
     X = unit_rows(W)
-    S = X @ round_bf16(centroids).T
+    S = X @ np.asarray(centroids, dtype=np.float64).T
     return np.argmax(_canonical(S), axis=1).astype(np.int64), S
 
 

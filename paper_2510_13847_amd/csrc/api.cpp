@@ -669,7 +669,10 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
         q.out_logprobs = want_ids ? out_logprobs : nullptr;
         q.inv_t = 1.0f / temperature;
         q.beta = tail_beta;
-        if (chain_step_eligible(q) && q.out_ids != nullptr)
+        // the one launch needs its whole grid resident at once; a shape the
+        // occupancy check rejects takes the four-launch form below
+        int64_t khz = 0;
+        if (q.out_ids != nullptr && chain_step_grid(q, &khz) > 0)
             return timed([&] { return launch_chain_step(q, stream); }, stream);
     }
 

@@ -37,6 +37,7 @@
 // workgroup's partial, the poll gives up, and the launch reports no token
 // (out_ids = -1) but still terminates.
 #include <atomic>
+#include <mutex>
 
 #include "dyna_internal.h"
 #include "gemv.h"
@@ -123,7 +124,7 @@ __device__ __forceinline__ bool poll_own(const ChainArgs& A, const uint64_t* src
         for (int q = 0; q < Q; ++q) stale |= (uint32_t)(v[q] >> 32) != e;
         if (!stale) break;
         if (wall_clock64() - t0 > A.spin_ticks) {
-            store_coherent(A.err, 1u);
+            store_coherent(A.err, e);
             gave_up = true;
             break;
         }
@@ -221,7 +222,7 @@ __device__ __forceinline__ bool poll_run(const ChainArgs& A, const uint64_t* src
         for (int q = 0; q < Q; ++q) stale |= (uint32_t)(v[q] >> 32) != e;
         if (!stale) break;
         if (wall_clock64() - t0 > A.spin_ticks) {
-            store_coherent(A.err, 1u);
+            store_coherent(A.err, e);
             gave_up = true;
             break;
         }
@@ -287,7 +288,7 @@ __device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* s
             for (int w = 0; w < P; ++w) stale |= in[u] && (uint32_t)(v[u * P + w] >> 32) != e;
         if (!stale) break;
         if (wall_clock64() - t0 > A.spin_ticks) {
-            store_coherent(A.err, 1u);
+            store_coherent(A.err, e);
             gave_up = true;
             break;
         }
@@ -318,7 +319,7 @@ __device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* s
 template <int NT>
 __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32_t* offs, int M, int k,
                                             uint64_t* cand, int32_t* sid, int32_t* rowoff, int32_t* sbase,
-                                            uint32_t* err, bool& bad) {
+                                            uint32_t* err, uint32_t e, bool& bad) {
     static_assert(NT == 256, "one histogram bin per thread");
     constexpr int NW = NT / kWave;
     constexpr int Q = kSelQ;
@@ -484,7 +485,7 @@ __device__ __forceinline__ int chain_select(const float (&v)[kSelQ], const int32
     if (t == 0) {
         rowoff[k] = total_len;
         if (total_cnt != k) {
-            store_coherent(err, 1u);
+            store_coherent(err, e);
             bad = true;
         }
     }
@@ -625,7 +626,7 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
             if ((int)threadIdx.x * kSelQ + q < M) sv[threadIdx.x * kSelQ + q] = v[q];
         }
     }
-    const int L = chain_select<kChainThreads>(v, offs, M, k, cand, sid, rowoff, sbase, A.err, bad);
+    const int L = chain_select<kChainThreads>(v, offs, M, k, cand, sid, rowoff, sbase, A.err, e, bad);
 
     // ---- stage 4: logits over the wave's contiguous range of shortlist slots
     if constexpr (!kEarly) load_h();
@@ -743,8 +744,12 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
 
         // workgroup 0, wave 0: lane l polls and merges partials l, l + 64, ...
         // in order, then a fixed-order wave reduction (no barrier on this
-        // path).  The error word (set by a wait that gave up, possibly in a
-        // straggler of an earlier launch) is read alongside the partials.
+        // path).  The error word holds the epoch of the last launch in which
+        // a wait gave up; only this launch's epoch fails this launch.  (A
+        // workgroup of a failed launch that starts after workgroup 0 has
+        // advanced the epoch computes with the next epoch, leaves words
+        // tagged with it and gives up its waits, so it marks the next launch
+        // as failed, which is right: that launch may read its stale words.)
         if (wv != 0) return;
         constexpr int kLaneParts = kChainMaxGrid / kWave;
         const uint32_t err_word = lane == 0 ? load_coherent(A.err) : 0u;
@@ -773,12 +778,9 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
         if (lane == 0) {
             uint64_t fb = gb;
             const float fm = gm, fs = gs;
-            const bool err = gfail || err_word != 0u;
+            const bool err = gfail || err_word == e;
             // every workgroup has read the epoch (its partial carries it)
-            if (err) {
-                store_coherent(A.err, 0u);
-                fb = 0;
-            }
+            if (err) fb = 0;
             store_coherent(A.epoch, e);
             A.out_ids[0] = fb != 0 ? (int32_t)key_id(fb) : -1;
             if (A.out_logprobs) {
@@ -790,20 +792,37 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
 }
 
 template <int NB, int R>
-dyna_status launch_chain_nb(const ChainArgs& a, int grid, size_t lds, hipStream_t s) {
-    static std::atomic<bool> raised[kMaxDevices] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
-        return set_error(DYNA_ERR_HIP, "one-launch step: no current device");
-    if (lds > 64 * 1024 && !raised[dev]) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(chain_step_kernel<NB, R>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-            return set_error(DYNA_ERR_UNSUPPORTED, "one-launch step needs %zu bytes of LDS", lds);
-        raised[dev] = true;
-    }
-    launch_timed_kernel(chain_step_kernel<NB, R>, dim3(grid), dim3(kChainThreads), (uint32_t)lds, s, a);
-    return check_launch("chain_step_kernel");
+const void* chain_fn() {
+    return reinterpret_cast<const void*>(chain_step_kernel<NB, R>);
 }
+
+// The kernel instance for the widest of d_r, H and d: NB blocks of 512
+// elements per row in registers, R head rows per wave in flight.
+template <typename F>
+auto with_chain_instance(int kmax, F f) {
+    const int nb = (kmax + 511) / 512;
+    if (nb <= 1) return f(std::integral_constant<int, 1>{}, std::integral_constant<int, 4>{});
+    if (nb <= 2) return f(std::integral_constant<int, 2>{}, std::integral_constant<int, 4>{});
+    if (nb <= 4) return f(std::integral_constant<int, 4>{}, std::integral_constant<int, 4>{});
+    if (nb <= 8) return f(std::integral_constant<int, 8>{}, std::integral_constant<int, 4>{});
+    if (nb <= 12) return f(std::integral_constant<int, 12>{}, std::integral_constant<int, 2>{});
+    return f(std::integral_constant<int, 16>{}, std::integral_constant<int, 2>{});
+}
+
+constexpr int kChainInstances = 6;
+int chain_instance_index(int kmax) {
+    const int nb = (kmax + 511) / 512;
+    return nb <= 1 ? 0 : nb <= 2 ? 1 : nb <= 4 ? 2 : nb <= 8 ? 3 : nb <= 12 ? 4 : 5;
+}
+
+struct ChainDevice {
+    int cus = 0;
+    int64_t tick_khz = 0;
+    bool lds_raised[kChainInstances] = {};
+};
+
+std::mutex g_chain_mu;
+ChainDevice g_chain_dev[kMaxDevices];
 
 }  // namespace
 
@@ -819,26 +838,55 @@ bool chain_step_eligible(const ChainRequest& q) {
 
 int option_wait_bound_us();  // DYNA_OPT_WAIT_BOUND_US: 0 default, -1 none, else microseconds
 
-dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
-    if (!chain_step_eligible(q)) return set_error(DYNA_ERR_UNSUPPORTED, "one-launch step: shape");
-    static std::atomic<int> cus[kMaxDevices] = {};
-    static std::atomic<int64_t> tick_khz[kMaxDevices] = {};
+// The hand-offs need every workgroup resident at once.  The grid is one
+// workgroup per compute unit (or the DYNA_OPT_GREEDY_GRID request), capped at
+// what the occupancy calculator says can be resident together for this
+// kernel instance and LDS size; 0 when no grid fits (or a query failed),
+// and the caller then takes the four-launch form.  Kernels of other streams
+// that hold compute units can still delay workgroups; the bounded waits
+// cover that case.
+int chain_step_grid(const ChainRequest& q, int64_t* tick_khz) {
+    if (!chain_step_eligible(q)) return 0;
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
-        return set_error(DYNA_ERR_HIP, "one-launch step: no current device");
-    if (cus[dev] == 0) {
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+    const int kmax = std::max(q.d_r, std::max(q.H, q.d));
+    const int inst = chain_instance_index(kmax);
+    const size_t lds = chain_lds_bytes(q.M, q.k, q.H);
+    std::lock_guard<std::mutex> g(g_chain_mu);
+    ChainDevice& cd = g_chain_dev[dev];
+    if (cd.cus == 0) {
         int n = 0, khz = 0;
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0 ||
-            hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0)
-            return set_error(DYNA_ERR_HIP, "one-launch step: device attributes");
-        tick_khz[dev].store(khz);
-        cus[dev].store(n);
+            hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0) {
+            (void)hipGetLastError();
+            return 0;
+        }
+        cd.cus = n;
+        cd.tick_khz = khz;
     }
-    // one workgroup per compute unit by default: the hand-offs need every
-    // workgroup resident at once
+    const void* fn = with_chain_instance(kmax, [](auto nb, auto r) { return chain_fn<decltype(nb)::value, decltype(r)::value>(); });
+    if (!cd.lds_raised[inst]) {
+        if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess) {
+            (void)hipGetLastError();
+            return 0;
+        }
+        cd.lds_raised[inst] = true;
+    }
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kChainThreads, lds) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    const int fit = std::min(per_cu * cd.cus, kChainMaxGrid);
     const int opt = option_greedy_grid();
-    const int n_cu = cus[dev].load();
-    const int grid = std::max(1, std::min(opt > 0 ? opt : n_cu, std::min(2 * n_cu, kChainMaxGrid)));
+    *tick_khz = cd.tick_khz;
+    return std::max(0, std::min(opt > 0 ? opt : cd.cus, fit));
+}
+
+dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
+    int64_t khz = 0;
+    const int grid = chain_step_grid(q, &khz);
+    if (grid <= 0) return set_error(DYNA_ERR_UNSUPPORTED, "one-launch step: no co-resident grid");
     ChainArgs a{};
     a.W1 = static_cast<const uint16_t*>(q.W1);
     a.b1 = q.b1;
@@ -878,15 +926,15 @@ dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
     // DYNA_OPT_WAIT_BOUND_US; -1: a wait gives up at its first read that
     // finds a word missing)
     const int bound_us = option_wait_bound_us();
-    a.spin_ticks = bound_us < 0 ? 0 : (uint64_t)tick_khz[dev].load() * (uint64_t)(bound_us > 0 ? bound_us : 200000) / 1000;
+    a.spin_ticks = bound_us < 0 ? 0 : (uint64_t)khz * (uint64_t)(bound_us > 0 ? bound_us : 200000) / 1000;
     const size_t lds = chain_lds_bytes(q.M, q.k, q.H);
-    const int nb = (std::max(q.d_r, std::max(q.H, q.d)) + 511) / 512;
-    if (nb <= 1) return launch_chain_nb<1, 4>(a, grid, lds, s);
-    if (nb <= 2) return launch_chain_nb<2, 4>(a, grid, lds, s);
-    if (nb <= 4) return launch_chain_nb<4, 4>(a, grid, lds, s);
-    if (nb <= 8) return launch_chain_nb<8, 4>(a, grid, lds, s);
-    if (nb <= 12) return launch_chain_nb<12, 2>(a, grid, lds, s);
-    return launch_chain_nb<16, 2>(a, grid, lds, s);
+    const int kmax = std::max(q.d_r, std::max(q.H, q.d));
+    with_chain_instance(kmax, [&](auto nb, auto r) {
+        launch_timed_kernel(chain_step_kernel<decltype(nb)::value, decltype(r)::value>, dim3(grid),
+                            dim3(kChainThreads), (uint32_t)lds, s, a);
+        return 0;
+    });
+    return check_launch("chain_step_kernel");
 }
 
 }  // namespace dyna

@@ -301,6 +301,10 @@ struct ChainRequest {
 };
 size_t chain_region_bytes(int32_t H, int32_t M);
 bool chain_step_eligible(const ChainRequest& q);
+// Grid the one-launch step takes on the current device (capped at what can
+// be resident at once), or 0 when it cannot run co-resident; fills the wall
+// clock rate (kHz) for the wait bounds.
+int chain_step_grid(const ChainRequest& q, int64_t* tick_khz);
 dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s);
 
 // Global options (dyna_set_option).

@@ -12,7 +12,15 @@ near-tie upstream cannot cascade:
     for fp32 inputs (fp32 accumulation on the GPU, fp64 in the oracle);
   * tokens: bit-exact on the GPU's own logits; against oracle logits, ranks may
     swap only inside groups whose adjacent gaps are below 1e-3 relative;
-  * sampled token: exact unless u lies within 1e-3 of a CDF boundary.
+  * sampled token: exact unless u lies within SAMPLE_WIN of a boundary of the
+    CDF the oracle builds from the GPU's own logits; the strict mismatches are
+    counted and bounded by the callers.
+
+A second, tight logit bound sits next to the benchmark spec's tolerance: fp32
+accumulation of d exactly representable products errs by at most
+(summation depth) * 2^-24 * sum_i |w_i h_i|, and the kernels' depth stays
+below d / 4 + 64 (per-lane runs, MFMA k-steps, wave and block reductions).
+A kernel that rounded its accumulator or its context to bf16 fails it.
 """
 from __future__ import annotations
 
@@ -27,6 +35,33 @@ TOL = {"bf16": (1e-2, 2e-2), "f32": (1e-5, 1e-5)}
 # (16 significant bits).  Both stay far inside this bound.
 SCORE_TOL = (2e-4, 2e-4)
 LOGPROB_TOL = (1e-4, 1e-5)
+# The GPU walks the CDF in fp32: each exp term carries a few ulps, a slot's
+# prefix is a per-thread run of at most 16 terms plus a block scan of depth
+# 10 (or a segment merge), and the target u * total is one more rounding.
+# That is at most about 40 * 2^-24 ~ 2.4e-6 of the total mass; the window
+# takes 1e-5.
+SAMPLE_WIN = 1e-5
+
+
+def tight_bound(d):
+    """Relative factor of the tight logit bound: (d / 4 + 64) * 2^-24."""
+    return (d / 4.0 + 64.0) * 2.0 ** -24
+
+
+def assert_tight(got, h_row, W_rows, what):
+    """|got - h.W| <= tight_bound(d) * sum_i |W_i h_i| + 1e-30, per slot, from
+    the exact fp64 values of the inputs (bf16 bit patterns or floats)."""
+    hv = O.as_f64(h_row)
+    Wv = O.as_f64(W_rows)
+    ref = Wv @ hv
+    mag = np.abs(Wv) @ np.abs(hv)
+    got = np.asarray(got, dtype=np.float64)
+    err = np.abs(got - ref)
+    bound = tight_bound(len(hv)) * mag + 1e-30
+    bad = np.nonzero(~(err <= bound))[0]
+    assert len(bad) == 0, (f"{what}: {len(bad)} of {len(got)} outside the tight bound; first at {bad[0]}: "
+                           f"got {got[bad[0]]}, ref {ref[bad[0]]}, bound {bound[bad[0]]:.3e}")
+    return float((err / np.maximum(mag, 1e-300)).max()) if len(err) else 0.0
 
 
 def rel_gap(a, b):
@@ -98,7 +133,12 @@ def tokens_check(got_ids, z_ref, vids, k_t):
 
 
 def sample_check(got_vid, z, vids, u, temperature=1.0):
+    """(strict_equal, accepted) for a sampled token against the oracle's
+    inverse-CDF draw on the same logits: accepted when u lies in the GPU
+    token's CDF interval widened by SAMPLE_WIN."""
     vids = np.asarray(vids)
+    if len(vids) == 0:
+        return int(got_vid) == -1, int(got_vid) == -1
     j = O.sample_inverse_cdf(z, u, temperature)
     if int(vids[j]) == int(got_vid):
         return True, True
@@ -108,4 +148,10 @@ def sample_check(got_vid, z, vids, u, temperature=1.0):
     jg = int(hit[0])
     F = O.sample_cdf(z, temperature)
     lo = F[jg - 1] if jg > 0 else 0.0
-    return False, bool(lo - TIE <= u < F[jg] + TIE)
+    return False, bool(lo - SAMPLE_WIN <= u < F[jg] + SAMPLE_WIN)
+
+
+def strict_limit(n):
+    """Strict mismatches allowed among n checked rows: a near-boundary u (or a
+    near-tie) is a rare event at the kernels' true fp32 error."""
+    return max(1, int(0.05 * n))

@@ -1,11 +1,14 @@
 """GPU parity of the partition builder (spherical k-means on the unit LM-head
 rows, Sec. 4.2 "Vocabulary partition") against the CPU oracle.
 
-The assignment is an argmax decided in the kernel's operand precision (bf16
-centroids, fp32 sums); the oracle takes the same decision with bf16 centroids
-and float64 sums, so an assignment may differ only where the oracle's two best
-similarities lie within 1e-5 (relative) of each other.  Centroids are fp32
-sums of unit rows; they match the oracle's float64 sums within 2e-5.
+The oracle computes the cosine similarities exactly (float64, unrounded
+centroids).  The kernel multiplies on the matrix cores with the centroids
+rounded to bf16 (relative error at most 2^-8 per coordinate) and sums in
+fp32.  Its similarity to centroid m therefore errs by at most
+e_m = (2^-8 + (d / 4 + 64) 2^-24) * sum_i |x_i mu_m,i|, so the GPU may pick
+centroid g over the oracle's r only when S[r] - S[g] <= e_r + e_g.  The rows
+where the two differ are counted and bounded.  Centroids are fp32 sums of
+unit rows; they match the oracle's float64 sums within 2e-5.
 """
 import numpy as np
 import pytest
@@ -40,13 +43,25 @@ def _unit(rng, M, d):
     return (c / np.linalg.norm(c, axis=1, keepdims=True)).astype(np.float32)
 
 
-def _check_assign(got, S, what):
-    """got[v] equals the oracle's argmax, or ties with it within 1e-5 relative."""
+def _check_assign(got, Wh, C, S, what, limit=None):
+    """got[v] equals the oracle's argmax, or the oracle's two similarities lie
+    within the bf16-rounding window e_r + e_g of each other.  Returns the
+    number of rows that differ (asserted below `limit`, default 1% of V + 1)."""
     ref = np.argmax(S, axis=1)
     bad = np.nonzero(got != ref)[0]
-    for v in bad:
-        a, b = S[v, got[v]], S[v, ref[v]]
-        assert abs(a - b) <= 1e-5 * max(abs(a), abs(b)) + 1e-7, f"{what}: row {v} -> {got[v]}, oracle {ref[v]}"
+    if len(bad):
+        X = O.unit_rows(Wh[bad])
+        d = X.shape[1]
+        eps = 2.0 ** -8 + (d / 4.0 + 64.0) * 2.0 ** -24
+        Ca = np.abs(np.asarray(C, dtype=np.float64))
+        for i, v in enumerate(bad):
+            g, r = int(got[v]), int(ref[v])
+            assert 0 <= g < S.shape[1], f"{what}: row {v} -> {g} out of range"
+            win = eps * (np.abs(X[i]) @ Ca[r] + np.abs(X[i]) @ Ca[g])
+            assert S[v, r] - S[v, g] <= win, (f"{what}: row {v} -> {g}, oracle {r}, gap {S[v, r] - S[v, g]:.3e} "
+                                              f"above the bf16 window {win:.3e}")
+    limit = max(1, S.shape[0] // 100) if limit is None else limit
+    assert len(bad) <= limit, f"{what}: {len(bad)} rows differ from the oracle's assignment (limit {limit})"
     return len(bad)
 
 
@@ -68,9 +83,10 @@ def test_assign_step(V, d, M, cfg):
     finally:
         D.set_option(D.OPT_KMEANS_CFG, 0)
     got = a.cpu().numpy().astype(np.int64)
-    ref, S = O.kmeans_assign(W.host_array(Wl), C)
-    n_tie = _check_assign(got, S, "assign")
-    assert n_tie <= max(1, V // 500)
+    Wh = W.host_array(Wl)
+    ref, S = O.kmeans_assign(Wh, C)
+    n_diff = _check_assign(got, Wh, C, S, "assign")
+    print(f"[kmeans] V={V} d={d} M={M} cfg={cfg}: {n_diff} assignments differ from the exact oracle", flush=True)
     # the reported product is the raw row's: S[v, m] * ||W[v]||
     norms = np.linalg.norm(O.as_f64(W.host_array(Wl)), axis=1)
     want = S[np.arange(V), got] * norms
@@ -90,8 +106,9 @@ def test_assign_ties_and_zero_rows():
     got = a.cpu().numpy()
     assert got[17] == 0
     assert not np.any(got == 4)
-    ref, S = O.kmeans_assign(W.host_array(Wl), C)
-    _check_assign(got.astype(np.int64), S, "ties")
+    Wh = W.host_array(Wl)
+    ref, S = O.kmeans_assign(Wh, C)
+    _check_assign(got.astype(np.int64), Wh, C, S, "ties")
 
 
 @pytest.mark.parametrize("V,d,M", [(1000, 64, 7), (3001, 200, 37), (2048, 1024, 513), (2000, 8192, 5)])
@@ -141,30 +158,46 @@ def test_planted_partition_is_recovered():
     assert L.cap_by_k[M] == V
 
 
-@pytest.mark.parametrize("iters", [1, 3])
+@pytest.mark.parametrize("iters", [1, 4])
 def test_random_head_rounds(iters):
-    # no planted structure: one round compares exactly (up to ties); later
-    # rounds are compared while the assignments still agree
+    """No planted structure.  Every GPU round is checked against the oracle's
+    round taken from the GPU's own previous centroids (so rounding in an early
+    round cannot cascade): the assignment within the bf16 window, the update
+    within 2e-5.  The whole builder (dyna_kmeans) must equal the chained
+    steps exactly."""
     w = W.scaled(W.WORKLOADS["llama3_8b_chain"], V=5000, d=256, M=40)
     Wl = W.lm_head(w)
+    Wd = Wl.to(DEV)
     init = W.kmeans_init_ids(w)
-    cl, mu = D.kmeans(Wl.to(DEV), w.M, torch.from_numpy(init).to(DEV), iters=iters)
-    torch.cuda.synchronize()
     Wh = W.host_array(Wl)
     X = O.unit_rows(Wh)
-    mu_ref = X[init]
+    ws = D.kmeans_workspace(Wd, w.M)
+    # round 1 starts from the unit points at init (the GPU normalises them in fp32)
+    cl, mu = D.kmeans(Wd, w.M, torch.from_numpy(init).to(DEV), iters=1, ws=ws)
+    torch.cuda.synchronize()
+    prev = X[init]
     got = cl.cpu().numpy().astype(np.int64)
-    for it in range(iters):
-        a_ref, S = O.kmeans_assign(Wh, mu_ref)
-        mu_ref = O.kmeans_update(Wh, a_ref, w.M, mu_ref)
-    if iters == 1:
-        _check_assign(got, S, "round 1")
-        if np.array_equal(got, a_ref):
-            np.testing.assert_allclose(mu.cpu().numpy(), mu_ref, rtol=0, atol=2e-5)
-    else:
-        # the GPU's own last round is self-consistent: its assignment is the
-        # oracle's argmax against the GPU's previous centroids
-        assert (got == a_ref).mean() > 0.99
+    _, S = O.kmeans_assign(Wh, prev)
+    diffs = [_check_assign(got, Wh, prev, S, "round 1")]
+    ref_mu = O.kmeans_update(Wh, got, w.M, prev)
+    np.testing.assert_allclose(mu.cpu().numpy(), ref_mu, rtol=0, atol=2e-5)
+    for it in range(1, iters):
+        prev = mu.cpu().numpy().astype(np.float64)   # the GPU's own centroids
+        a, _ = D.kmeans_assign(Wd, mu, ws=ws)
+        torch.cuda.synchronize()
+        got = a.cpu().numpy().astype(np.int64)
+        _, S = O.kmeans_assign(Wh, prev)
+        diffs.append(_check_assign(got, Wh, prev, S, f"round {it + 1}"))
+        D.kmeans_update(Wd, a, mu, ws=ws)
+        torch.cuda.synchronize()
+        ref_mu = O.kmeans_update(Wh, got, w.M, prev)
+        np.testing.assert_allclose(mu.cpu().numpy(), ref_mu, rtol=0, atol=2e-5)
+    print(f"[kmeans] rounds {iters}: assignments differing from the exact oracle per round {diffs}", flush=True)
+    # the builder in one call is the chained steps
+    cl_all, mu_all = D.kmeans(Wd, w.M, torch.from_numpy(init).to(DEV), iters=iters, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(cl_all, torch.from_numpy(got.astype(np.int32)).to(DEV))
+    assert torch.equal(mu_all, mu)
 
 
 def test_deterministic_and_errors():

@@ -7,6 +7,7 @@ mistakes are planted in the oracle only, on the CPU, for the duration of one
 test.
 """
 import numpy as np
+import torch
 import pytest
 
 from oracle import dynaspec_oracle as O
@@ -170,10 +171,17 @@ def kmeans_argmin(W, centroids):
     return np.argmin(S, axis=1).astype(np.int64), S
 
 
-def round_bf16_truncates(a):
-    f = np.asarray(a, dtype=np.float64).astype(np.float32)
-    u = f.view(np.uint32) & np.uint32(0xFFFF0000)
-    return u.view(np.float32).astype(np.float64)
+def kmeans_bf16_centroids(W, centroids):
+    # the kernel's operand precision leaking into the definition
+    c = torch.from_numpy(np.asarray(centroids, dtype=np.float32)).to(torch.bfloat16).double().numpy()
+    return ORIG["kmeans_assign"](W, c)
+
+
+def empty_shortlist_takes_complement_token(z, vocab_ids, k_t=1, temperature=1.0, u=None, beta=0.0,
+                                           complement_ids=None):
+    if len(vocab_ids) == 0:
+        vocab_ids, z = np.array([0]), np.array([0.0])
+    return ORIG["draft_select"](z, vocab_ids, k_t, temperature, u, beta, complement_ids)
 
 
 MUTANTS = {
@@ -226,8 +234,10 @@ MUTANTS = {
         [P.test_kmeans_ties_go_to_the_lower_cluster_and_empty_clusters_keep_their_centroid]),
     "k-means: least similar centroid": ("kmeans_assign", kmeans_argmin,
         [P.test_kmeans_assignment_is_euclidean_argmin_on_the_sphere, P.test_kmeans_planted_directions_are_recovered]),
-    "k-means: bf16 rounding truncates": ("round_bf16", round_bf16_truncates,
-        [P.test_round_bf16_matches_torch_conversion]),
+    "k-means: centroids rounded to bf16": ("kmeans_assign", kmeans_bf16_centroids,
+        [P.test_kmeans_similarity_is_exact_below_bf16_resolution]),
+    "select: an empty shortlist still proposes a token": ("draft_select", empty_shortlist_takes_complement_token,
+        [P.test_empty_shortlist_proposes_nothing]),
 }
 
 

@@ -224,6 +224,35 @@ def test_select_tie_goes_to_lower_vocab_id():
     assert O.topk_tokens(np.array(g["z"]), np.array(g["vocab_ids"]), 3).tolist() == g["top3_positions"]
 
 
+def test_sample_cdf_hand_example():
+    g = GOLD["sample_cdf"]
+    z = np.log(np.array(g["probs"])) - 1.5  # any shift gives the same q_S
+    np.testing.assert_allclose(O.sample_cdf(z), g["cdf_T1"], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(O.sample_cdf(z, temperature=0.5), np.array(g["cdf_T0.5_times_22"]) / 22.0,
+                               rtol=0, atol=1e-15)
+    # the inverse-CDF draw is the first position whose CDF exceeds u
+    F = O.sample_cdf(z, temperature=0.5)
+    for u in np.linspace(0.0, 0.999, 37):
+        assert O.sample_inverse_cdf(z, u, temperature=0.5) == int(np.searchsorted(F, u, side="right"))
+
+
+def test_empty_shortlist_proposes_nothing():
+    # clusters may be empty (no balance is enforced); a router that picks only
+    # empty clusters leaves an empty shortlist, which proposes no token
+    cluster_of = np.array([0, 0, 2, 2, 2, 0])  # cluster 1 and 3 are empty
+    W_lm = np.eye(6, 4, dtype=np.float32)
+    x = np.ones((1, 4), dtype=np.float32)
+    W1 = np.zeros((4, 4), dtype=np.float32)
+    b1 = np.array([0.0, 5.0, 0.0, 4.0])  # scores from the bias alone: clusters 1, 3 on top
+    r = O.draft_head(x, x, W1, None, "none", cluster_of, 4, W_lm, k=2, k_t=3, u=np.array([0.4]), b1=b1)[0]
+    assert r["clusters"].tolist() == [1, 3]
+    assert len(r["vocab_ids"]) == 0 and len(r["ids"]) == 0
+    assert r["sample_id"] == -1 and r["sample_logprob"] == -np.inf
+    # one more cluster brings in its tokens
+    r = O.draft_head(x, x, W1, None, "none", cluster_of, 4, W_lm, k=3, k_t=3, u=np.array([0.4]), b1=b1)[0]
+    assert sorted(r["vocab_ids"].tolist()) == [0, 1, 5]
+
+
 def test_sampling_fallback_and_zero_mass():
     z = np.array([0.0, -np.inf])
     assert O.sample_inverse_cdf(z, 0.5) == 0
@@ -424,12 +453,18 @@ def test_pa_fr_budget_hand_values():
 
 
 # ---------------------------------------------------------------- spherical k-means (Sec. 4.2, "Vocabulary partition")
-def test_round_bf16_matches_torch_conversion():
-    rng = np.random.default_rng(7)
-    v = np.concatenate([rng.standard_normal(4096) * 10.0 ** rng.integers(-30, 30, 4096),
-                        [1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -8), 0.0, -0.0, 3.0e38]])
-    ref = torch.tensor(v, dtype=torch.float32).to(torch.bfloat16).double().numpy()
-    np.testing.assert_array_equal(O.round_bf16(v), ref)
+def test_kmeans_similarity_is_exact_below_bf16_resolution():
+    # centroid 1 differs from centroid 0 = (1, 0) only below bf16 resolution in
+    # its first coordinate: mu1 = (1, 2^-12) / |.|.  For the point (1, 2^-14),
+    # exactly, x . mu1 = (1 + 2^-26) / sqrt(1 + 2^-24) < 1 = x . mu0 (times
+    # 1/|x|), so cluster 0 wins; rounding mu1 to bf16 gives (1, 2^-12) and
+    # would hand the point to cluster 1.
+    W = np.array([[1.0, 2.0 ** -14]], dtype=np.float32)
+    C = np.array([[1.0, 0.0], [1.0, 2.0 ** -12]])
+    C[1] /= np.linalg.norm(C[1])
+    assign, S = O.kmeans_assign(W, C)
+    assert assign.tolist() == [0]
+    assert S[0, 0] - S[0, 1] > 0
 
 
 def test_kmeans_mean_direction_hand_example():
@@ -464,11 +499,13 @@ def test_kmeans_planted_directions_are_recovered():
 
 def test_kmeans_assignment_is_euclidean_argmin_on_the_sphere():
     # with unit centroids, max cosine = min euclidean distance between unit
-    # vectors; centroids are rows of a normalised Hadamard matrix (exact in bf16)
+    # vectors; centroids are the rows of a normalised Hadamard matrix and of
+    # its negation, plus random unit vectors
     from sklearn.metrics import pairwise_distances_argmin
     H = 0.5 * np.array([[1, 1, 1, 1], [1, -1, 1, -1], [1, 1, -1, -1], [1, -1, -1, 1]], dtype=np.float64)
-    C = np.vstack([H, -H])
     rng = np.random.default_rng(5)
+    R = rng.standard_normal((5, 4))
+    C = np.vstack([H, -H, R / np.linalg.norm(R, axis=1, keepdims=True)])
     W = rng.standard_normal((500, 4)).astype(np.float32)
     assign, _ = O.kmeans_assign(W, C)
     X = W.astype(np.float64) / np.linalg.norm(W.astype(np.float64), axis=1, keepdims=True)
@@ -497,7 +534,7 @@ def test_kmeans_is_invariant_to_positive_row_scales():
 
 
 def test_kmeans_steps_each_maximise_the_objective_and_end_at_a_fixed_point():
-    # the assignment maximises the summed similarity to the (bf16) centroids
+    # the assignment maximises the summed similarity to the centroids
     # given them, the update maximises it over unit centroids given the
     # assignment; brute force over all centroids confirms every final choice
     rng = np.random.default_rng(2)
@@ -508,10 +545,9 @@ def test_kmeans_steps_each_maximise_the_objective_and_end_at_a_fixed_point():
     mu = X[init]
     a = np.zeros(60, dtype=np.int64)
     for it in range(30):
-        Cb = O.round_bf16(mu)
         a_new, _ = O.kmeans_assign(W, mu)
         if it:
-            assert O.kmeans_objective(W, a_new, Cb) >= O.kmeans_objective(W, a, Cb) - 1e-12
+            assert O.kmeans_objective(W, a_new, mu) >= O.kmeans_objective(W, a, mu) - 1e-12
         a = a_new
         mu_new = O.kmeans_update(W, a, M, mu)
         assert O.kmeans_objective(W, a, mu_new) >= O.kmeans_objective(W, a, mu) - 1e-12
@@ -525,7 +561,6 @@ def test_kmeans_steps_each_maximise_the_objective_and_end_at_a_fixed_point():
                 assert np.all(mem.sum(0) @ probes.T <= best + 1e-12)
         mu = mu_new
     a, _ = O.kmeans_assign(W, mu)
-    Cb = O.round_bf16(mu)
     for v in range(60):
-        sims = [float(np.dot(X[v], Cb[m])) for m in range(M)]
+        sims = [float(np.dot(X[v], mu[m])) for m in range(M)]
         assert a[v] == min(m for m in range(M) if sims[m] == max(sims))
