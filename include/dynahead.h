@@ -363,7 +363,9 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   `stream` and the occupancy calculator finds room for the whole grid at
  *   once (its workgroups hand words to each other); otherwise as 2.  2: four launches (router layer 1; router
  *   layer 2; top-k with shortlist and plan; gathered head fused with
- *   selection).  1: the separate kernels.  All give bit-identical results.
+ *   selection).  1: the separate kernels.  3: the one launch only; a step it
+ *   cannot run returns DYNA_ERR_UNSUPPORTED (for tests and measurement that
+ *   must know which form ran).  All give bit-identical results.
  *   Under kernel timing the one-launch step, or the fused gathered-head +
  *   selection launch, is what is timed.
  * DYNA_OPT_MFMA_UNROLL: k steps the direct-load MFMA kernel (path 3) loads

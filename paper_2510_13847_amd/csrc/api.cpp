@@ -424,7 +424,7 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         return DYNA_OK;
     }
     if (option == DYNA_OPT_FUSED_B1) {
-        REQUIRE(value >= 0 && value <= 2, "fused option %d not in {0, 1, 2}", value);
+        REQUIRE(value >= 0 && value <= 3, "fused option %d not in {0, 1, 2, 3}", value);
         g_fused_off.store(value);
         return DYNA_OK;
     }
@@ -639,7 +639,7 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
     // or the whole step is one launch
     const int fused_opt = g_fused_off.load();
     const bool fused = B == 1 && fused_opt != 1 && option_logits_path() <= 1 && k_t == 1 && !want_sample;
-    if (fused && fused_opt == 0 && !split && option_router_path() <= 1) {
+    if (fused && (fused_opt == 0 || fused_opt == 3) && !split && option_router_path() <= 1) {
         ChainRequest q{};
         q.all_bf16 = r->wdtype == DYNA_BF16 && L->wdtype == DYNA_BF16 && adtype == DYNA_BF16;
         q.W1 = r->W1;
@@ -675,6 +675,8 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
         if (q.out_ids != nullptr && chain_step_grid(q, &khz) > 0)
             return timed([&] { return launch_chain_step(q, stream); }, stream);
     }
+    if (fused_opt == 3)
+        return set_error(DYNA_ERR_UNSUPPORTED, "one-launch step requested (DYNA_OPT_FUSED_B1 = 3) but not possible");
 
     // routing (the router's stream); with several contexts a split-K last
     // layer leaves its partial sums to the top-k

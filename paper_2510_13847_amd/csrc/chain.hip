@@ -818,7 +818,7 @@ int chain_instance_index(int kmax) {
 struct ChainDevice {
     int cus = 0;
     int64_t tick_khz = 0;
-    bool lds_raised[kChainInstances] = {};
+    size_t lds_raised[kChainInstances] = {};  // dynamic LDS limit set per instance (0: the default 64 KB)
 };
 
 std::mutex g_chain_mu;
@@ -865,12 +865,14 @@ int chain_step_grid(const ChainRequest& q, int64_t* tick_khz) {
         cd.tick_khz = khz;
     }
     const void* fn = with_chain_instance(kmax, [](auto nb, auto r) { return chain_fn<decltype(nb)::value, decltype(r)::value>(); });
-    if (!cd.lds_raised[inst]) {
-        if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess) {
+    // dynamic LDS above the default 64 KB must be allowed per kernel first
+    // (up to what the kernel's static LDS leaves of the 160 KB)
+    if (lds > 64 * 1024 && lds > cd.lds_raised[inst]) {
+        if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
             (void)hipGetLastError();
             return 0;
         }
-        cd.lds_raised[inst] = true;
+        cd.lds_raised[inst] = lds;
     }
     int per_cu = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kChainThreads, lds) != hipSuccess) {

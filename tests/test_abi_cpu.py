@@ -61,8 +61,8 @@ def test_set_option_validation():
         assert lib.dyna_set_option(D.OPT_WAIT_BOUND_US, v) == D.ERR_INVALID_ARG
     for v in (-1, 1, 1000000, 0):
         assert lib.dyna_set_option(D.OPT_WAIT_BOUND_US, v) == D.OK
-    assert lib.dyna_set_option(D.OPT_FUSED_B1, 3) == D.ERR_INVALID_ARG
-    for v in (2, 1, 0):
+    assert lib.dyna_set_option(D.OPT_FUSED_B1, 4) == D.ERR_INVALID_ARG
+    for v in (3, 2, 1, 0):
         assert lib.dyna_set_option(D.OPT_FUSED_B1, v) == D.OK
 
 

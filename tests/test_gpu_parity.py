@@ -717,8 +717,14 @@ FUSED_CASES = [c for c in CASES if c.B == 1] + [
 ]
 
 
+def _one_launch_opt(w, route_stream=None):
+    """DYNA_OPT_FUSED_B1 value that makes a step of w run as the one launch
+    (3: the one launch or an error), where w's shape allows it; else 0."""
+    return 3 if w.dtype == "bf16" and route_stream is None else 0
+
+
 @pytest.mark.parametrize("temperature", [1.0, 0.6])
-@pytest.mark.parametrize("fused_opt", [0, 2], ids=["one_launch", "four_launches"])
+@pytest.mark.parametrize("fused_opt", [3, 2], ids=["one_launch", "four_launches"])
 @pytest.mark.parametrize("w", FUSED_CASES, ids=lambda w: w.name)
 def test_fused_greedy_matches_separate_kernels(w, temperature, fused_opt):
     """A greedy one-context step folds the selection into the gathered head
@@ -734,7 +740,7 @@ def test_fused_greedy_matches_separate_kernels(w, temperature, fused_opt):
     side = torch.cuda.Stream()
     for it, rs in enumerate([None, None, side, None, None]):
         x = W.contexts(w, "cpu", salt=it).to(DEV)
-        D.set_option(D.OPT_FUSED_B1, fused_opt)
+        D.set_option(D.OPT_FUSED_B1, _one_launch_opt(w, rs) if fused_opt == 3 else fused_opt)
         try:
             fused(x, x, route_stream=rs)
             D.set_option(D.OPT_FUSED_B1, 1)
@@ -774,7 +780,7 @@ def test_one_launch_step_ties(variant):
     sep = D.DraftHead(R, p.L, 1, w.k, mode, 1, keep_logits=True)
     for it in range(4):
         x = W.contexts(w, "cpu", salt=it).to(DEV)
-        D.set_option(D.OPT_FUSED_B1, 0)
+        D.set_option(D.OPT_FUSED_B1, 3)
         try:
             one(x, x)
             D.set_option(D.OPT_FUSED_B1, 1)
@@ -812,6 +818,7 @@ def test_one_launch_step_wait_bound():
     def step(it, bound):
         x = W.contexts(w, "cpu", salt=it).to(DEV)
         D.set_option(D.OPT_WAIT_BOUND_US, bound)
+        D.set_option(D.OPT_FUSED_B1, 3)
         try:
             one(x, x)
             D.set_option(D.OPT_FUSED_B1, 1)
@@ -851,6 +858,7 @@ def test_one_launch_step_grid_beyond_residency(grid_per_cu):
         for it in range(3):
             x = W.contexts(w, "cpu", salt=it).to(DEV)
             D.set_option(D.OPT_GREEDY_GRID, min(4096, grid_per_cu * n_cu))
+            D.set_option(D.OPT_FUSED_B1, 3)
             try:
                 one(x, x)
                 D.set_option(D.OPT_FUSED_B1, 1)
@@ -890,9 +898,10 @@ def test_one_launch_step_special_inputs(variant):
     one = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_ARGMAX, 1, keep_logits=True)
     sep = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_ARGMAX, 1, keep_logits=True)
     for _ in range(3):
-        one(x, h)
-        D.set_option(D.OPT_FUSED_B1, 1)
+        D.set_option(D.OPT_FUSED_B1, 3)
         try:
+            one(x, h)
+            D.set_option(D.OPT_FUSED_B1, 1)
             sep(x, h)
         finally:
             D.set_option(D.OPT_FUSED_B1, 0)
@@ -963,7 +972,7 @@ def test_empty_and_single_row_clusters(name, B, sel, path, union, k):
     mode = (D.SEL_ARGMAX if sel == "argmax" else D.SEL_TOPK | D.SEL_SAMPLE) | (D.SEL_UNION if union else 0)
     kt = 1 if sel == "argmax" else 4
     D.set_option(D.OPT_LOGITS_PATH, path)
-    D.set_option(D.OPT_FUSED_B1, 2 if name.startswith("four_launch") else 0)
+    D.set_option(D.OPT_FUSED_B1, 2 if name.startswith("four_launch") else 3 if name.startswith("one_launch") else 0)
     try:
         head = D.draft_head(p.R, p.L, p.hd, p.hd, k, mode=mode, k_t=kt, uniforms=p.ud)
         torch.cuda.synchronize()
@@ -1003,7 +1012,7 @@ def test_determinism_over_many_steps():
     four-launch steps and 100 batched steps."""
     chain = next(c for c in FUSED_CASES if c.name == "chain_wide")
     pc = Problem(chain)
-    for fused_opt in (0, 2):
+    for fused_opt in (3, 2):
         head = D.DraftHead(pc.R, pc.L, 1, chain.k, D.SEL_ARGMAX, 1, keep_logits=True)
         D.set_option(D.OPT_FUSED_B1, fused_opt)
         try:
