@@ -239,6 +239,38 @@ dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
                             hipEvent_t x_ready);
 
 /* ------------------------------------------------------------------ */
+/* The whole head without a workspace.                                 */
+/* ------------------------------------------------------------------ */
+
+/* Bytes of the library's static per-GPU scratch array used by
+ * dyna_draft_head_noalloc (the first 128 KiB hold the one-launch step's
+ * hand-off region, the rest is the step's workspace). */
+#define DYNA_NOALLOC_SCRATCH_BYTES (16u << 20)
+
+/* dyna_draft_head for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same step, arguments and results, with no workspace argument, no
+ * second routing stream (everything runs on `stream`) and no kernel-timing
+ * events.  It calls no allocating routine: its scratch is a static device
+ * array of DYNA_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends.
+ * The first call on a GPU looks the array up and clears its hand-off region
+ * with a small kernel on `stream` (a plain kernel, safe under capture).
+ * Every call on a GPU shares that GPU's array and may leave data in it, so
+ * calls that overlap on one GPU (other streams, other host threads) race;
+ * order them on one stream.  A step whose workspace (dyna_workspace_bytes)
+ * exceeds DYNA_NOALLOC_SCRATCH_BYTES - 128 KiB returns DYNA_ERR_WORKSPACE:
+ * one context at any shape, and batches up to the tree-batch and serving
+ * shapes of the paper's settings (B = 64, k = 32 at V = 128256; B = 16, k =
+ * 64 at V = 151936) fit. */
+dyna_status dyna_draft_head_noalloc(const dyna_router* r, const dyna_layout* L,
+                                    const void* x, const void* h, int32_t adtype,
+                                    int32_t B, int32_t k, int32_t mode, int32_t k_t,
+                                    float temperature, float tail_beta, const float* uniforms,
+                                    int32_t* out_ids, float* out_logprobs, int32_t* out_sample,
+                                    float* out_sample_logprob, int32_t* out_clusters,
+                                    float* out_logits, int32_t cap, hipStream_t stream);
+
+/* ------------------------------------------------------------------ */
 /* Baselines on the same kernels (Sec. 4.1).                           */
 /* ------------------------------------------------------------------ */
 

@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdynahead.so")
 
-SOURCES = ["api.cpp", "layout.hip", "rowdot.hip", "gather.hip", "router.hip", "select.hip", "fused.hip", "chain.hip", "kmeans.hip"]
+SOURCES = ["api.cpp", "layout.hip", "rowdot.hip", "gather.hip", "router.hip", "select.hip", "fused.hip", "chain.hip", "kmeans.hip", "noalloc.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",

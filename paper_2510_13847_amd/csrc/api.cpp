@@ -585,13 +585,24 @@ DYNA_API dyna_status dyna_draft_select(const dyna_layout* L, const float* logits
                          want_sample ? out_sample_logprob : nullptr, c.select_ws, stream);
 }
 
-DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L, const void* x, const void* h,
-                                     int32_t adtype, int32_t B, int32_t k, int32_t mode, int32_t k_t,
-                                     float temperature, float tail_beta, const float* uniforms, int32_t* out_ids,
-                                     float* out_logprobs, int32_t* out_sample, float* out_sample_logprob,
-                                     int32_t* out_clusters, float* out_logits, int32_t cap, void* ws,
-                                     size_t ws_bytes, hipStream_t stream, hipStream_t route_stream,
-                                     hipEvent_t x_ready) {
+namespace dyna {
+
+// The whole head (dyna_draft_head).  `chain_region`, when set, is the
+// one-launch step's tagged hand-off region (at a fixed address, so its
+// epoch survives calls of different shapes) in place of the workspace's own;
+// `timing` lets DYNA_OPT_KERNEL_TIMING bracket the gathered head with events.
+dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const void* x, const void* h,
+                            int32_t adtype, int32_t B, int32_t k, int32_t mode, int32_t k_t, float temperature,
+                            float tail_beta, const float* uniforms, int32_t* out_ids, float* out_logprobs,
+                            int32_t* out_sample, float* out_sample_logprob, int32_t* out_clusters,
+                            float* out_logits, int32_t cap, void* ws, size_t ws_bytes, hipStream_t stream,
+                            hipStream_t route_stream, hipEvent_t x_ready, void* chain_region, bool timing) {
+    auto timed = [&](auto launch, hipStream_t s) -> dyna_status {
+        return timing ? dyna::timed(launch, s) : launch();
+    };
+    auto timed_rowdot = [&](const RowdotArgs& a, int path, hipStream_t s) -> dyna_status {
+        return timed([&] { return launch_rowdot(a, path, s); }, s);
+    };
     TRY(check_router(r));
     TRY(check_layout(L));
     REQUIRE(r->M == L->M, "router M=%d differs from layout M=%d", r->M, L->M);
@@ -658,7 +669,7 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
         q.V = L->V;
         q.h = h;
         q.k = k;
-        q.region = c.chain;
+        q.region = chain_region ? chain_region : c.chain;
         q.out_clusters = clusters;
         q.topk_scores = c.topk_scores;
         q.sel_sorted = c.sel_sorted;
@@ -734,6 +745,20 @@ DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
                          want_sample ? out_sample_logprob : nullptr, c.select_ws, stream, c.slot_vid,
                          dense_union ? 0 : cap, union_mode);
+}
+
+}  // namespace dyna
+
+DYNA_API dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L, const void* x, const void* h,
+                                     int32_t adtype, int32_t B, int32_t k, int32_t mode, int32_t k_t,
+                                     float temperature, float tail_beta, const float* uniforms, int32_t* out_ids,
+                                     float* out_logprobs, int32_t* out_sample, float* out_sample_logprob,
+                                     int32_t* out_clusters, float* out_logits, int32_t cap, void* ws,
+                                     size_t ws_bytes, hipStream_t stream, hipStream_t route_stream,
+                                     hipEvent_t x_ready) {
+    return draft_head_core(r, L, x, h, adtype, B, k, mode, k_t, temperature, tail_beta, uniforms, out_ids,
+                           out_logprobs, out_sample, out_sample_logprob, out_clusters, out_logits, cap, ws,
+                           ws_bytes, stream, route_stream, x_ready, nullptr, true);
 }
 
 // ------------------------------------------------------------------ beam expansion

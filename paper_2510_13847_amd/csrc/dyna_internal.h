@@ -307,6 +307,16 @@ bool chain_step_eligible(const ChainRequest& q);
 int chain_step_grid(const ChainRequest& q, int64_t* tick_khz);
 dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s);
 
+// The whole head behind dyna_draft_head and its allocation-free variant:
+// `chain_region` (may be null) replaces the workspace's hand-off region of
+// the one-launch step; `timing` allows DYNA_OPT_KERNEL_TIMING's events.
+dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const void* x, const void* h,
+                            int32_t adtype, int32_t B, int32_t k, int32_t mode, int32_t k_t, float temperature,
+                            float tail_beta, const float* uniforms, int32_t* out_ids, float* out_logprobs,
+                            int32_t* out_sample, float* out_sample_logprob, int32_t* out_clusters,
+                            float* out_logits, int32_t cap, void* ws, size_t ws_bytes, hipStream_t stream,
+                            hipStream_t route_stream, hipEvent_t x_ready, void* chain_region, bool timing);
+
 // Global options (dyna_set_option).
 int option_logits_path();
 int option_router_path();

@@ -68,6 +68,8 @@ _SIGNATURES = {
                                _P, _Z, _P]),
     "dyna_draft_head": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _F, _P, _P, _P, _P, _P, _P, _P,
                              _I, _P, _Z, _P, _P, _P]),
+    "dyna_draft_head_noalloc": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _F, _P, _P, _P, _P, _P, _P, _P,
+                                     _I, _P]),
     "dyna_dense_workspace_bytes": (_Z, [_I, _I]),
     "dyna_cluster_budget": (_I, [_I, _I, _I, _I, _I]),
     "dyna_beam_expand": (_I, [_P, _P, _P, _I, _I, _I, _P, _P, _P, _P]),
@@ -342,6 +344,23 @@ class DraftHead:
                                      _ptr(self.logits), self.cap, _ptr(self.ws), self.ws.numel(),
                                      _stream(stream), rs, ev))
         return self
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # DYNA_NOALLOC_SCRATCH_BYTES
+
+
+def draft_head_noalloc(head: "DraftHead", x, h, uniforms=None, stream=None,
+                       layout: Optional[Layout] = None, router: Optional[Router] = None):
+    """dyna_draft_head_noalloc into head's preallocated outputs (its own
+    workspace is not used: the library's static scratch stands in for it)."""
+    L = layout or head.layout
+    R = router or head.router
+    _check(lib().dyna_draft_head_noalloc(R.c, L.c, _ptr(x), _ptr(h), _dtype_code(h), head.B, head.k,
+                                         head.mode, head.k_t, head.temperature, head.tail_beta,
+                                         _ptr(uniforms), _ptr(head.ids), _ptr(head.logprobs),
+                                         _ptr(head.sample), _ptr(head.sample_logprob), _ptr(head.clusters),
+                                         _ptr(head.logits), head.cap, _stream(stream)))
+    return head
 
 
 def draft_head(router: Router, layout: Layout, x, h, k: int, mode=SEL_ARGMAX, k_t=1,

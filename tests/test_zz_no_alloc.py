@@ -1,0 +1,108 @@
+"""dyna_draft_head_noalloc (the head on the library's static per-GPU scratch,
+for callers that cannot allocate) against dyna_draft_head on the same inputs.
+
+Both run the same kernels, so every output must be bit-identical: cluster
+ids, token ids, samples, logits and log-probabilities.  Calls follow each
+other with different shapes (a batch, then a smaller one, then one-context
+steps of two router shapes) because the static array keeps the previous
+call's contents; the one-launch step's hand-off region sits at a fixed place
+in it and must stay consistent."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+D = None
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    global D
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2510_13847_amd import dynahead
+    D = dynahead
+    D.lib()
+    yield
+
+
+BASE = W.WORKLOADS["llama3_8b_chain"]
+
+
+def _problem(name, **kw):
+    w = W.scaled(BASE, name=name, **kw)
+    cl = W.partition(w)
+    W_lm = W.lm_head(w, "cpu").to(DEV)
+    W1, W2 = W.router_weights(w, "cpu")
+    L = D.build_layout(torch.from_numpy(cl).to(DEV), W_lm, w.M)
+    R = D.Router(W1.to(DEV), None if W2 is None else W2.to(DEV), act=w.act)
+    h = W.contexts(w, "cpu").to(DEV)
+    u = W.uniforms(w, "cpu").to(DEV)
+    return w, L, R, h, u
+
+
+def _pair(w, L, R, mode, k_t):
+    ref = D.DraftHead(R, L, w.B, w.k, mode, k_t, keep_logits=True)
+    na = D.DraftHead(R, L, w.B, w.k, mode, k_t, keep_logits=True)
+    return ref, na
+
+
+def _same(a, b):
+    for name in ("ids", "logprobs", "sample", "sample_logprob", "clusters", "logits"):
+        x, y = getattr(a, name), getattr(b, name)
+        if x is None:
+            assert y is None
+            continue
+        assert torch.equal(torch.nan_to_num(x, nan=7.0), torch.nan_to_num(y, nan=7.0)), name
+
+
+def test_noalloc_matches_the_workspace_entry_point():
+    big = _problem("na_b37", V=3001, d=200, M=37, H=24, k=5, B=37)
+    small = _problem("na_b6", V=2500, d=264, M=30, H=48, k=4, B=6)
+    chain_a = _problem("na_chain_a", V=9000, d=1024, M=100, H=256, k=12, B=1)
+    chain_b = _problem("na_chain_b", V=6000, d=256, M=50, H=0, act="none", k=6, B=1)
+    steps = [(big, D.SEL_TOPK | D.SEL_SAMPLE, 6), (small, D.SEL_TOPK | D.SEL_SAMPLE, 3),
+             (chain_a, D.SEL_ARGMAX, 1), (chain_b, D.SEL_ARGMAX, 1), (chain_a, D.SEL_ARGMAX, 1),
+             (small, D.SEL_TOPK, 4)]
+    for i, ((w, L, R, h, u), mode, k_t) in enumerate(steps):
+        print(f"[noalloc] call {i}: {w.name} B={w.B} k={w.k} mode={mode}", flush=True)
+        ref, na = _pair(w, L, R, mode, k_t)
+        ref(h, h, u)
+        D.draft_head_noalloc(na, h, h, u)
+        torch.cuda.synchronize()
+        _same(ref, na)
+        if w.B == 1:
+            assert int(na.ids[0, 0]) >= 0, "the one-context step reported no token"
+        # twice in a row on the same inputs: still identical
+        D.draft_head_noalloc(na, h, h, u)
+        torch.cuda.synchronize()
+        _same(ref, na)
+
+
+def test_noalloc_one_launch_step_runs():
+    """The one-context greedy step takes the one-launch form on the static
+    scratch (DYNA_OPT_FUSED_B1 = 3 makes any other form an error)."""
+    w, L, R, h, u = _problem("na_chain_c", V=7000, d=512, M=64, H=128, k=8, B=1)
+    ref, na = _pair(w, L, R, D.SEL_ARGMAX, 1)
+    D.set_option(D.OPT_FUSED_B1, 3)
+    try:
+        for it in range(3):
+            x = W.contexts(w, "cpu", salt=it).to(DEV)
+            ref(x, x)
+            D.draft_head_noalloc(na, x, x)
+            torch.cuda.synchronize()
+            _same(ref, na)
+    finally:
+        D.set_option(D.OPT_FUSED_B1, 0)
+
+
+def test_noalloc_rejects_a_step_beyond_the_scratch():
+    w, L, R, h, u = _problem("na_wide", V=20000, d=64, M=40, H=16, k=40, B=200)
+    head = D.DraftHead(R, L, w.B, w.k, D.SEL_TOPK, 4, keep_logits=False)
+    need = D.workspace_bytes(L, R, w.B, w.k, head.cap)
+    assert need > D.NOALLOC_SCRATCH_BYTES - 128 * 1024
+    with pytest.raises(D.DynaError) as e:
+        D.draft_head_noalloc(head, h, h)
+    assert e.value.status == D.ERR_WORKSPACE and "scratch" in str(e.value)
