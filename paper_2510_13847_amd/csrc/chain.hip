@@ -172,9 +172,7 @@ template <int NB>
 __device__ __forceinline__ float dot_bf16(const Raw8<uint16_t> (&w)[NB], const Raw8<uint16_t> (&v)[NB]) {
     float acc = 0.0f;
 #pragma unroll
-    for (int blk = 0; blk < NB; ++blk)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc = fmaf(w[blk].at(j), v[blk].at(j), acc);
+    for (int blk = 0; blk < NB; ++blk) acc = dot8(w[blk], v[blk], acc);
     return wave_sum(acc);
 }
 
@@ -679,17 +677,14 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
                 if (lane == r) my_row = lrow[r];
             const bool own = lane < nrow;
             const int32_t vid = own ? A.perm[my_row] : 0;
+            // row by row, so each row's dot starts as soon as its loads land
             float acc[R];
 #pragma unroll
-            for (int r = 0; r < R; ++r) acc[r] = 0.0f;
+            for (int r = 0; r < R; ++r) {
+                acc[r] = 0.0f;
 #pragma unroll
-            for (int blk = 0; blk < NB; ++blk)
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const float hj = hv[blk].at(j);
-#pragma unroll
-                    for (int r = 0; r < R; ++r) acc[r] = fmaf(w[r][blk].at(j), hj, acc[r]);
-                }
+                for (int blk = 0; blk < NB; ++blk) acc[r] = dot8(w[r][blk], hv[blk], acc[r]);
+            }
             float mine = 0.0f;
 #pragma unroll
             for (int r = 0; r < R; ++r) {
@@ -723,19 +718,24 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
             w_bad[wv] = wbad;
         }
         __syncthreads();
-        if (threadIdx.x == 0) {
-            uint64_t bb = w_best[0];
-            float bm = w_m[0], bs = w_s[0];
-            bool any_bad = w_bad[0] != 0;
-            for (int q = 1; q < NW; ++q) {
-                bb = w_best[q] > bb ? w_best[q] : bb;
-                softmax_merge(bm, bs, w_m[q], w_s[q], A.inv_t);
-                any_bad |= w_bad[q] != 0;
+        if (wv == 0) {
+            // the waves' partials side by side in lanes 0..NW-1, reduced
+            // across the lanes at once (a chain of merges one after another
+            // costs an exponential per wave on the critical path)
+            const bool has = lane < NW;
+            const uint64_t bl = has ? w_best[lane] : 0;
+            const float ml = has ? w_m[lane] : -__builtin_inff();
+            const float sl = has ? w_s[lane] : 0.0f;
+            const bool any_bad = __ballot(has && w_bad[lane] != 0) != 0;
+            const uint64_t bb = wave_max_u64(bl);
+            const float bm = bb != 0 ? key_val(bb) : -__builtin_inff();
+            const float bs = wave_sum(ml == -__builtin_inff() ? 0.0f : sl * expf((ml - bm) * A.inv_t));
+            if (lane == 0) {
+                uint64_t* pw = A.tpart + (int64_t)blockIdx.x * kPartWords;
+                store_coherent(pw + 0, tagged(e, (uint32_t)(bb >> 32)));
+                store_coherent(pw + 1, tagged(e, (uint32_t)bb));
+                store_coherent(pw + 2, tagged(e, __float_as_uint(any_bad ? -1.0f : bs)));
             }
-            uint64_t* pw = A.tpart + (int64_t)blockIdx.x * kPartWords;
-            store_coherent(pw + 0, tagged(e, (uint32_t)(bb >> 32)));
-            store_coherent(pw + 1, tagged(e, (uint32_t)bb));
-            store_coherent(pw + 2, tagged(e, __float_as_uint(any_bad ? -1.0f : bs)));
         }
         // the selection outputs come from the last workgroup, after its
         // partial is out (off the merging workgroup's path when G > 1)
@@ -760,16 +760,25 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
             if (u0 * kWave >= G) break;
             uint32_t raw[4 * kPartWords];
             fail |= poll_parts<4>(A, A.tpart, G, u0, e, raw);
+            // the lane's four partials: their maximum first, then the four
+            // rescaled sums independently (no chain of exponentials)
+            float mu[4], su[4], lm = -__builtin_inff();
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int g = lane + kWave * (u0 + u);
-                if (g >= G) continue;
                 const uint64_t k2 = ((uint64_t)raw[u * kPartWords] << 32) | raw[u * kPartWords + 1];
                 const float s2 = __uint_as_float(raw[u * kPartWords + 2]);
-                fail |= s2 < 0.0f;
-                bb = k2 > bb ? k2 : bb;
-                softmax_merge(bm, bs, k2 != 0 ? key_val(k2) : -__builtin_inff(), s2 < 0.0f ? 0.0f : s2, A.inv_t);
+                const bool in = g < G;
+                fail |= in && s2 < 0.0f;
+                bb = in && k2 > bb ? k2 : bb;
+                mu[u] = in && k2 != 0 ? key_val(k2) : -__builtin_inff();
+                su[u] = in && s2 > 0.0f ? s2 : 0.0f;
+                lm = fmaxf(lm, mu[u]);
             }
+            float ls = 0.0f;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) ls += mu[u] == -__builtin_inff() ? 0.0f : su[u] * expf((mu[u] - lm) * A.inv_t);
+            softmax_merge(bm, bs, lm, ls, A.inv_t);
         }
         const uint64_t gb = wave_max_u64(bb);
         const float gm = gb != 0 ? key_val(gb) : -__builtin_inff();

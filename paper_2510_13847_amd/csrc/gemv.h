@@ -46,6 +46,32 @@ struct Raw8<float> {
     }
 };
 
+// acc + w . x over the 8 elements of two raw pieces, in element order.  Two
+// bf16 pieces use the packed bf16 dot product (two exact products and the
+// accumulator per instruction, four instructions instead of eight widenings
+// and eight FMAs); any fp32 operand takes FMAs.  Every kernel that must agree
+// bit for bit with another (the one-context paths) accumulates through this.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// A 32-bit word as two bf16 lanes.  (Through memcpy: a bit cast applied to a
+// vector element directly was compiled to read element 0 every time.)
+__device__ __forceinline__ bf16x2 as_bf16x2(uint32_t u) {
+    bf16x2 r;
+    __builtin_memcpy(&r, &u, 4);
+    return r;
+}
+__device__ __forceinline__ float dot8(const Raw8<uint16_t>& w, const Raw8<uint16_t>& x, float acc) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+        acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(w.q[p]), as_bf16x2(x.q[p]), acc, false);
+    return acc;
+}
+template <typename WT, typename VT>
+__device__ __forceinline__ float dot8(const Raw8<WT>& w, const Raw8<VT>& x, float acc) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc = fmaf(w.at(j), x.at(j), acc);
+    return acc;
+}
+
 // One wave computes R consecutive rows per iteration.  With SINGLE (one
 // context: B = 1) the context row is loaded into registers once per wave.
 // Default epilogue: store the value (and, in plan mode, the slot's vocabulary id).
@@ -153,11 +179,7 @@ __device__ __forceinline__ void gemv_rows(const RowdotArgs& a, Epi& epi) {
                     else x.zero();
                 }
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const float xj = x.at(j);
-#pragma unroll
-                    for (int r = 0; r < R; ++r) acc[r] = fmaf(w[r][blk].at(j), xj, acc[r]);
-                }
+                for (int r = 0; r < R; ++r) acc[r] = dot8(w[r][blk], x, acc[r]);
             }
             float mine = 0.0f;
 #pragma unroll
