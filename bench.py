@@ -114,33 +114,60 @@ def time_graph_steps(make_step, K, torch):
     return e0.elapsed_time(e1) / 1e3, wall
 
 
-def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20):
-    """Routing on a second stream while a stand-in draft-layer GEMM runs on the
-    main stream (Sec. 4.2/4.3: the router overlaps the drafter's layer).
+def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20, route_grid=None):
+    """Routing on a second stream while a stand-in draft layer (one GEMM of
+    the drafter's MLP) runs on the caller's stream (Sec. 4.2 and Sec. 4.3:
+    the router runs in parallel with the draft layer, so a step costs about
+    T_D = T_emb + max(T_core, T_meta) + T_index+gemm).
 
-    Times, per step: the GEMM alone, the head alone, GEMM then head on one
-    stream, and GEMM with the head's routing on a second stream.  The hidden
-    fraction is how much of the routing time the overlap removes."""
+    Times per step: the draft layer alone (T_core), routing alone (T_meta:
+    router and top-k; also with its grid capped at a quarter of the compute
+    units), both at once on two streams, and the hidden fraction
+    (T_core + T_meta - T_both) / T_meta.  Then whole steps: draft layer and
+    head on one stream, draft layer with the head's routing on the second
+    stream (the overlapped step), and the draft layer followed by the dense
+    full-vocabulary head."""
     a, b = W.overlap_gemm_operands(w, "cuda")
     side = torch.cuda.Stream()
-    main = torch.cuda.current_stream()
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
 
-    def t_of(fn):
-        for i in range(3):
-            fn(i)
+    def t_of(fn, reps=5):
+        # n steps captured into one graph (second-stream work is forked from
+        # and joined back into the capture stream with events) and replayed:
+        # eager launches pay the runtime's cross-stream synchronisation on
+        # every event (about 25 us per dependency on this system, against
+        # almost nothing inside a graph), and the headline is timed from
+        # graphs too
+        g = capture([(lambda i=i: fn(i)) for i in range(n)], torch)
+        g.replay()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        for i in range(n):
-            fn(i)
+        for _ in range(reps):
+            g.replay()
         e1.record()
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / n * 1e3  # us
+        return e0.elapsed_time(e1) / (reps * n) * 1e3  # us
 
     L = lambda i: layouts[i % len(layouts)]
     R = lambda i: routers[i % len(routers)]
+    x_of = lambda i: xs[i % len(xs)]
     gemm = lambda i: torch.matmul(a, b)
-    only_head = lambda i: head(xs[i % len(xs)], xs[i % len(xs)], us[i % len(us)], layout=L(i), router=R(i))
+    only_head = lambda i: head(x_of(i), x_of(i), us[i % len(us)], layout=L(i), router=R(i))
+    route_only = lambda i: D.route(R(i), x_of(i), w.k, ws=head.ws)
+
+    def both(i):
+        # the draft layer on the caller's stream, routing on the side stream
+        cur = torch.cuda.current_stream()
+        ev = torch.cuda.Event()
+        ev.record(cur)
+        side.wait_event(ev)
+        torch.matmul(a, b)
+        with torch.cuda.stream(side):
+            D.route(R(i), x_of(i), w.k, ws=head.ws)
+        done = torch.cuda.Event()
+        done.record(side)
+        cur.wait_event(done)
 
     def serial(i):
         torch.matmul(a, b)
@@ -148,20 +175,43 @@ def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20):
 
     def overlapped(i):
         ev = torch.cuda.Event()
-        ev.record(main)           # x is ready before the draft layer runs
+        ev.record(torch.cuda.current_stream())  # x is ready before the draft layer runs
         torch.matmul(a, b)        # the draft layer on the main stream
-        head(xs[i % len(xs)], xs[i % len(xs)], us[i % len(us)], layout=L(i), router=R(i),
-             route_stream=side, x_ready=ev)
+        head(x_of(i), x_of(i), us[i % len(us)], layout=L(i), router=R(i), route_stream=side, x_ready=ev)
 
-    def route_only(i):
-        D.route(R(i), xs[i % len(xs)], w.k, ws=head.ws)
+    dense = D.DenseHead(L(0).W_perm, w.V, w.B, D.SEL_ARGMAX if w.B == 1 else D.SEL_TOPK, 1 if w.B == 1 else w.k_t)
 
-    t_g, t_h, t_s, t_o, t_r = t_of(gemm), t_of(only_head), t_of(serial), t_of(overlapped), t_of(route_only)
+    def draft_then_dense(i):
+        torch.matmul(a, b)
+        dense(x_of(i), W=L(i).W_perm)
+
+    if route_grid is None:
+        route_grid = 0  # the library's default: routing at full width on the second stream
+    D.set_option(D.OPT_ROUTE_GRID, route_grid)
+    try:
+        t_g, t_r, t_b = t_of(gemm), t_of(route_only), t_of(both)
+    finally:
+        D.set_option(D.OPT_ROUTE_GRID, 0)
+    D.set_option(D.OPT_ROUTE_GRID, max(1, n_cu // 4))
+    try:
+        t_r_quarter = t_of(route_only)
+    finally:
+        D.set_option(D.OPT_ROUTE_GRID, 0)
+    D.set_option(D.OPT_ROUTE_GRID, route_grid)
+    try:
+        t_h, t_s, t_o, t_d = t_of(only_head), t_of(serial), t_of(overlapped), t_of(draft_then_dense)
+    finally:
+        D.set_option(D.OPT_ROUTE_GRID, 0)
     rows, K, N = w.overlap_gemm
-    return {"gemm": f"[{rows},{K}]x[{K},{N}] bf16 (torch.matmul)", "gemm_us": round(t_g, 2),
-            "head_us": round(t_h, 2), "route_us": round(t_r, 2), "serial_us": round(t_s, 2),
-            "overlapped_us": round(t_o, 2),
-            "routing_hidden_frac": round(max(0.0, t_s - t_o) / t_r, 3) if t_r > 0 else None}
+    return {"draft_layer": f"[{rows},{K}]x[{K},{N}] bf16 (torch.matmul)",
+            "route_workgroups": route_grid if route_grid > 0 else "full width",
+            "draft_us": round(t_g, 2), "route_us": round(t_r, 2),
+            "route_quarter_of_the_cus_us": round(t_r_quarter, 2),
+            "draft_and_route_us": round(t_b, 2),
+            "routing_hidden_frac": round(max(0.0, t_g + t_r - t_b) / t_r, 3) if t_r > 0 else None,
+            "head_us": round(t_h, 2), "serial_step_us": round(t_s, 2), "overlapped_step_us": round(t_o, 2),
+            "draft_plus_dense_us": round(t_d, 2),
+            "overlapped_speedup_vs_draft_plus_dense": round(t_d / t_o, 3) if t_o > 0 else None}
 
 
 KERNEL_UNITS = {"chain_step_kernel": "chain.hip", "logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip", "gather_ring_kernel": "gather.hip", "union_gemm_kernel": "gather.hip",

@@ -35,17 +35,16 @@ constexpr int max_steps(int tt) { return tt == 1 ? 16 : 8; }
 template <bool VF32>
 constexpr int stage_batch() { return VF32 ? 8 : 16; }
 
+// One k slice `sl` of a workgroup's row tile: stage the slice of every
+// context in LDS, multiply, write the slice's partial sums.
 template <int NW, int G, bool VF32, int TT>
-__global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, int ksl, float* part) {
+__device__ __forceinline__ void splitk_slice(const RowdotArgs& a, int ksl, int sl, float* part, uint16_t* xs) {
     constexpr int MAXS = max_steps(TT);
-    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [G*16][ksl] hi, then lo
     constexpr int NCOL = G * 16;
     const int K = a.K, B = a.B, n = a.n_rows;
-    const int k0 = blockIdx.y * ksl;
+    const int k0 = sl * ksl;
     const int kn = min(ksl, K - k0);
     const int npc = ksl / 8;  // 16-byte pieces per context row of the slice
-    if (a.zero_words != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && (int)threadIdx.x < a.n_zero_words)
-        a.zero_words[threadIdx.x] = 0;
 
     // the wave's 16 W rows of the slice are requested first, so that their
     // HBM latency overlaps the staging of the contexts below
@@ -111,7 +110,7 @@ __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, 
         }
     }
     __syncthreads();
-    if (r0 >= n) return;  // no barrier follows
+    if (r0 >= n) return;  // wave-uniform; no barrier follows in this slice
 
     // every context piece read from LDS feeds the TT row tiles of the wave
     f32x4 acc[TT][G];
@@ -140,7 +139,7 @@ __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, 
         }
     }
     // partial sums of this slice: part[slice][b][row]; D row 4 * kq + r, column col
-    float* pp = part + (int64_t)blockIdx.y * B * n;
+    float* pp = part + (int64_t)sl * B * n;
 #pragma unroll
     for (int t = 0; t < TT; ++t)
 #pragma unroll
@@ -155,21 +154,49 @@ __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, 
         }
 }
 
+// Workgroup (x, y) takes k slice y of row tile x.  Each slice's partial
+// sums go to their own place, so the results do not depend on the grid.
+template <int NW, int G, bool VF32, int TT>
+__global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, int ksl, float* part) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [G*16][ksl] hi, then lo
+    if (a.zero_words != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && (int)threadIdx.x < a.n_zero_words)
+        a.zero_words[threadIdx.x] = 0;
+    splitk_slice<NW, G, VF32, TT>(a, ksl, blockIdx.y, part, xs);
+}
+
+// The same with a capped grid (routing beside a draft layer): workgroup
+// (x, y) takes the slices y, y + gridDim.y, ... below nsl one after another.
+template <int NW, int G, bool VF32, int TT>
+__global__ __launch_bounds__(NW * kWave) void dense_splitk_loop_kernel(RowdotArgs a, int ksl, int nsl, float* part) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
+    if (a.zero_words != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && (int)threadIdx.x < a.n_zero_words)
+        a.zero_words[threadIdx.x] = 0;
+    for (int sl = blockIdx.y; sl < nsl; sl += gridDim.y) {
+        if (sl != (int)blockIdx.y) __syncthreads();  // the previous slice's LDS reads are done
+        splitk_slice<NW, G, VF32, TT>(a, ksl, sl, part, xs);
+    }
+}
+
 // out[b * ld + r] = act(sum over slices, in slice order, + bias[r])
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int slices, int B, int n,
                                                             float* __restrict__ out, int64_t ld,
                                                             const float* __restrict__ bias, int act) {
-    const int r = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+    const int r = blockIdx.x * 256 + threadIdx.x;
     if (r >= n) return;
-    float s = 0.0f;
+    for (int b = blockIdx.y; b < B; b += gridDim.y) {
+        float s = 0.0f;
 #pragma unroll 8
-    for (int q = 0; q < slices; ++q) s += part[((int64_t)q * B + b) * n + r];
-    out[(int64_t)b * ld + r] = apply_act(s + (bias ? bias[r] : 0.0f), act);
+        for (int q = 0; q < slices; ++q) s += part[((int64_t)q * B + b) * n + r];
+        out[(int64_t)b * ld + r] = apply_act(s + (bias ? bias[r] : 0.0f), act);
+    }
 }
 
 template <int NW, int G, bool VF32, int TT>
 dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* part, bool reduce, hipStream_t stream) {
-    const dim3 grid((unsigned)sh.row_tiles, (unsigned)sh.slices);
+    // a capped grid keeps every row tile and folds the slices onto fewer
+    // workgroups along k
+    const int gy = a.max_blocks > 0 ? std::max(1, std::min(sh.slices, a.max_blocks / sh.row_tiles)) : sh.slices;
+    const dim3 grid((unsigned)sh.row_tiles, (unsigned)gy);
     const uint32_t lds = (uint32_t)sh.lds;
     if (lds > 64 * 1024) {
         // above 64 KiB the dynamic LDS size must be allowed, once per kernel and device
@@ -178,15 +205,22 @@ dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* pa
         if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "router: device");
         if (!(allowed.load() & (1ull << dev))) {
             if (hipFuncSetAttribute((const void*)dense_splitk_kernel<NW, G, VF32, TT>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget) != hipSuccess ||
+                hipFuncSetAttribute((const void*)dense_splitk_loop_kernel<NW, G, VF32, TT>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget) != hipSuccess)
                 return set_error(DYNA_ERR_HIP, "router: LDS attribute");
             allowed.fetch_or(1ull << dev);
         }
     }
-    dense_splitk_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
+    if (gy < sh.slices)
+        dense_splitk_loop_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, sh.slices, part);
+    else
+        dense_splitk_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
     const dyna_status st = check_launch("dense_splitk_kernel");
     if (st != DYNA_OK || !reduce) return st;
-    splitk_reduce_kernel<<<dim3((unsigned)((a.n_rows + 255) / 256), (unsigned)a.B), dim3(256), 0, stream>>>(
+    const int rx = (a.n_rows + 255) / 256;
+    const int ry = a.max_blocks > 0 ? std::max(1, std::min(a.B, a.max_blocks / rx)) : a.B;
+    splitk_reduce_kernel<<<dim3((unsigned)rx, (unsigned)ry), dim3(256), 0, stream>>>(
         part, sh.slices, a.B, a.n_rows, a.out, a.ld, a.bias, a.act);
     return check_launch("splitk_reduce_kernel");
 }

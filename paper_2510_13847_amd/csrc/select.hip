@@ -114,6 +114,7 @@ __global__ __launch_bounds__(kNT) void shortlist_kernel(
 // bandwidth-bound); the layout offsets are copied to LDS once.
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanPer = 8;
+constexpr int kPlanGrid = 32;  // workgroups of a batch's plan
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int32_t* __restrict__ offsets, int M, const int32_t* __restrict__ sel_sorted,
     const int32_t* __restrict__ sel_rowoff, int B, int k, Plan plan) {
@@ -190,11 +191,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         if (cnt[m] > 0) rc += (offs[m + 1] - offs[m] + kChunkRows - 1) / kChunkRows;
     }
     __syncthreads();
-    // chunk descriptors, all threads together: thread t writes an equal range
-    // of chunk indices; one binary search finds the cluster of its first chunk
-    // (the last cluster whose first chunk is <= c), then it walks forward
-    const int per_c = (n_chunks + kPlanThreads - 1) / kPlanThreads;
-    const int c0 = min(n_chunks, t * per_c), c1 = min(n_chunks, c0 + per_c);
+    // chunk descriptors, all threads of all workgroups together: thread gt
+    // writes an equal range of chunk indices; one binary search finds the
+    // cluster of its first chunk (the last cluster whose first chunk is <= c),
+    // then it walks forward
+    const int nthr = (int)gridDim.x * kPlanThreads;
+    const int gt = (int)blockIdx.x * kPlanThreads + t;
+    const int per_c = (n_chunks + nthr - 1) / nthr;
+    const int c0 = min(n_chunks, gt * per_c), c1 = min(n_chunks, c0 + per_c);
     if (c0 < c1) {
         int lo = 0, hi = M - 1;
         while (lo < hi) {
@@ -247,12 +251,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 #pragma unroll
         for (int q = 0; q < kPlanPer; ++q) {
             const int m = mv[q];
-            if (m < 0 || m >= M) continue;
+            // the context list of cluster m is filled by workgroup m % gridDim.x
+            if (m < 0 || m >= M || m % (int)gridDim.x != (int)blockIdx.x) continue;
             const int p = atomicAdd(&cnt[m], 1);
             plan.list[loff[m] + p] = ListEntry{bq[q], ro[q] - offs[m]};
         }
     }
-    if (t == 0) {
+    if (t == 0 && blockIdx.x == 0) {
         plan.hdr->n_chunks = n_chunks;
         plan.hdr->n_entries = n_entries;
     }
@@ -675,7 +680,13 @@ dyna_status launch_plan(const int32_t* offsets, int32_t M, const int32_t* sel_so
             allowed.fetch_or(1ull << dev);
         }
     }
-    plan_kernel<<<1, kPlanThreads, lds, stream>>>(offsets, M, sel_sorted, sel_rowoff, B, k, plan);
+    // every workgroup builds the counts and offsets itself (cheap next to a
+    // hand-off between workgroups), then writes its share of the chunk table
+    // and the context lists of its clusters; with one context the plan is
+    // small and one workgroup does it
+    const int64_t n_sel = (int64_t)B * k;
+    const int grid = n_sel <= 64 ? 1 : (int)std::min<int64_t>(kPlanGrid, std::max<int64_t>(1, n_sel / 64));
+    plan_kernel<<<grid, kPlanThreads, lds, stream>>>(offsets, M, sel_sorted, sel_rowoff, B, k, plan);
     return check_launch("plan_kernel");
 }
 

@@ -60,9 +60,11 @@ WORKLOADS = {
         Workload("tiny_fp32", 0, V=8192, d=256, M=64, dtype="f32", sizes=("equal",),
                  H=0, act="none", k=4, B=4, modes=("argmax", "topk"), k_t=8,
                  static_prefix=512),
+        # the draft-layer stand-in for the chain: one [4096 x 14336] projection
+        # of the drafter's MLP at B = 1 (117 MB of bf16 weights)
         Workload("llama3_8b_chain", 1, V=128256, d=4096, M=1024, dtype="bf16",
                  sizes=("lognormal", 0.5), H=1024, act="silu", k=32, B=1,
-                 modes=("argmax",), k_t=1),
+                 modes=("argmax",), k_t=1, overlap_gemm=(1, 4096, 14336)),
         Workload("llama3_8b_tree", 2, V=128256, d=4096, M=1024, dtype="bf16",
                  sizes=("lognormal", 0.5), H=1024, act="silu", k=32, B=64,
                  modes=("topk",), k_t=10, seed_index=1),
