@@ -19,7 +19,8 @@ dense full-vocabulary head and a static fixed-shortlist head timed the same
 way on the same GPU.  The outputs of the last replayed step are checked
 against the same step run eagerly.  With the default chain workload the line
 also carries the tree batch (B = 64 on the same LM head and router) under
-"tree_batch".
+"tree_batch", and the per-position cost of one drafting cycle (Algorithm 1:
+budgets k_c(j), union head, beam expansion) under "cycle".
 """
 from __future__ import annotations
 
@@ -542,6 +543,8 @@ def main():
                          "replicas of the workload's LM head) and print it")
     ap.add_argument("--no-tree", action="store_true",
                     help="with the default chain workload, skip the tree-batch block of the line")
+    ap.add_argument("--no-cycle", action="store_true",
+                    help="with the default chain workload, skip the drafting-cycle leg (Algorithm 1 positions)")
     ap.add_argument("--counters", action="store_true",
                     help="hardware-counter pass: build the layout (a row copy of known size) "
                          "and run 20 eager steps; no timing")
@@ -584,7 +587,87 @@ def main():
                                                  "step_bytes", "step_GBps", "step_frac", "roofline", "replay_check",
                                                  "baselines", "speedup_vs_dense", "byte_ratio_dense_over_dynamic",
                                                  "speedup_target") if k in sub}
+    if args.workload == "llama3_8b_chain" and not args.no_cycle:
+        rec["cycle"] = bench_cycle(D, torch, shared)
     print(json.dumps(rec), flush=True)
+
+
+# One verification cycle of drafting at the Llama-3-8B shapes: positions
+# j = 0..5, cluster budgets k0 = 64, k1 = 32 (eq. pos_schedule; the paper
+# prints no values, these are stand-ins), k_t = 10 tokens per row and a beam
+# of 10 rows after position 0.
+CYCLE_K0, CYCLE_K1, CYCLE_KT, CYCLE_GAMMA = 64, 32, 10, 5
+
+
+def bench_cycle(D, torch, shared, K=100):
+    """Per-position cost of one drafting cycle (Algorithm 1): position j routes
+    its rows with the budget k_c(j), evaluates every row over the union of the
+    rows' clusters (top-10 each) and expands the beam (dyna_beam_expand).
+    Position 0 has one row, later ones the 10 beam rows.  No drafter runs
+    here: each position's rows are seeded stand-ins drawn from a pool, so the
+    timed work is the head's alone.  The same cycle at the fixed budget k1
+    at every position, and the dense full-vocabulary head at the same row
+    counts, are timed beside it."""
+    dev = "cuda"
+    w = W.WORKLOADS["llama3_8b_tree_union"]  # the chain's partition, router and LM head
+    layouts, routers, W_lm = shared["layouts"], shared["routers"], shared["W_lm"]
+    sizes = np.diff(shared["L0"].offsets.cpu().numpy().astype(np.int64))
+    s_w = 2
+    router_bytes = s_w * (w.d_r * w.H + w.H * w.M)
+    Ws = [W_lm] + [W_lm.clone() for _ in range(N_REPLICAS - 1)]
+    dense_us = {}
+    for B in (1, CYCLE_KT):
+        dh = D.DenseHead(W_lm, w.V, B, D.SEL_TOPK, CYCLE_KT)
+        hs = [W.contexts(w, dev, batch=B, salt=7000 + i) for i in range(POOL)]
+        g_s, _ = time_graph_steps(lambda i, dh=dh, hs=hs: (lambda: dh(hs[i % POOL], W=Ws[i % N_REPLICAS])),
+                                  K, torch)
+        dense_us[B] = g_s / K * 1e6
+    del Ws
+    out = {"workload": "llama3_8b one drafting cycle (Algorithm 1)", "k0": CYCLE_K0, "k1": CYCLE_K1,
+           "k_t": CYCLE_KT, "positions": CYCLE_GAMMA + 1, "steps_per_position": K,
+           "timing": "hip graph replay of head + beam expansion per position"}
+    for label, budget in (("position_aware", lambda j: D.cluster_budget(j, CYCLE_K0, CYCLE_K1)),
+                          ("fixed_k1", lambda j: CYCLE_K1)):
+        per = []
+        for j in range(CYCLE_GAMMA + 1):
+            B = 1 if j == 0 else CYCLE_KT
+            k = budget(j)
+            mode = D.SEL_TOPK | (D.SEL_UNION if B > 1 else 0)
+            head = D.DraftHead(routers[0], layouts[0], B, k, mode, CYCLE_KT)
+            xs = [W.contexts(w, dev, batch=B, salt=5000 + 97 * j + i) for i in range(POOL)]
+            lasts = [-5.0 * W.uniforms(w, dev, batch=B, salt=5000 + 97 * j + i) for i in range(POOL)]
+            bout = (torch.empty(CYCLE_KT, dtype=torch.float32, device=dev),
+                    torch.empty(CYCLE_KT, dtype=torch.int32, device=dev),
+                    torch.empty(CYCLE_KT, dtype=torch.int32, device=dev))
+
+            def make_step(i, head=head, xs=xs, lasts=lasts, bout=bout, j=j):
+                L, R, x = layouts[i % N_REPLICAS], routers[i % N_REPLICAS], xs[i % POOL]
+                last = None if j == 0 else lasts[i % POOL]
+
+                def step():
+                    head(x, x, layout=L, router=R)
+                    D.beam_expand(head.logprobs, head.ids, last, CYCLE_KT, out=bout)
+                return step
+            rows = []
+            for i in range(8):
+                make_step(i)()
+                rows.append(int(sizes[np.unique(head.clusters.cpu().numpy())].sum()))
+            torch.cuda.synchronize()
+            if not bool((bout[1] >= 0).all()):
+                raise SystemExit(f"bench: cycle position {j}: the beam is short")
+            g_s, _ = time_graph_steps(make_step, K, torch)
+            us = g_s / K * 1e6
+            step_bytes = router_bytes + s_w * w.d * float(np.mean(rows)) + 2 * s_w * B * w.d
+            per.append({"position": j, "k": k, "rows": B, "shortlist": int(np.mean(rows)), "us": round(us, 2),
+                        "GBps": round(step_bytes / us / 1e3, 1), "dense_us": round(dense_us[B], 2)})
+            del head, xs, lasts
+        out[label] = {"per_position": per, "cycle_us": round(sum(p["us"] for p in per), 2),
+                      "dense_cycle_us": round(sum(p["dense_us"] for p in per), 2)}
+    pa, fx = out["position_aware"]["cycle_us"], out["fixed_k1"]["cycle_us"]
+    out["position_aware_saving_vs_fixed"] = round(1.0 - pa / fx, 4)
+    out["speedup_vs_dense"] = round(out["position_aware"]["dense_cycle_us"] / pa, 3)
+    torch.cuda.empty_cache()
+    return out
 
 
 def hbm_probe(w, D, torch, K=40):

@@ -340,6 +340,62 @@ def beam_expand(logprobs, ids, last_scores, n_out: int):
             np.array([ids[c[1], c[2]] for c in cand], dtype=np.int64))
 
 
+def draft_cycle(x0, h0, next_inputs, W1, W2, act, cluster_of, M, W_lm, k_first: int, k_second: int,
+                k_t: int, gamma: int, k_min: int = 1, form: str = "equation"):
+    """One verification cycle of drafting (Algorithm 1): positions j = 0..gamma.
+
+    Position j routes each of its rows with the budget k_c(j) (k_schedule),
+    evaluates every row over the union of the rows' clusters, keeps each
+    row's k_t best log-probabilities (TopP_j, ids T~_j), adds the parent's
+    score (cu_scores = TopP_j + last_step_scores, zero at j = 0) and keeps the
+    k_t best cu_scores over the position (beam_expand): their scores are the
+    next last_step_scores, their tokens x_j and their rows the parents whose
+    hidden rows h~[TopC_j] the next position extends.
+
+    x0 [1, d_r], h0 [1, d]: the router input and the drafter's hidden row of
+    the first position.  next_inputs(h_parent_rows, tokens) -> (x, h) stands
+    in for the draft layer (outside the head): the next position's router
+    input and hidden rows from the parents' hidden rows and the new tokens.
+
+    Returns (positions, draft_list).  positions[j] holds k, the union head's
+    per-row results ("heads"), ids/logprobs [B, k_t] (-1 / -inf past a short
+    shortlist), cu_scores [B, k_t] and the beam (scores, parents, tokens).
+    draft_list re-ranks every drafted token by cu_score, descending; ties go
+    to the earlier position, then the lower row, then the better rank.
+    """
+    x, h = np.atleast_2d(np.asarray(x0)), np.atleast_2d(np.asarray(h0))
+    last = None
+    positions = []
+    for j in range(gamma + 1):
+        k = k_schedule(j, k_first, k_second, k_min, form)
+        heads = draft_head(x, h, W1, W2, act, cluster_of, M, W_lm, k, k_t=k_t, union=True)
+        B = len(heads)
+        ids = np.full((B, k_t), -1, dtype=np.int64)
+        lp = np.full((B, k_t), -np.inf)
+        for b, r in enumerate(heads):
+            n = len(r["ids"])
+            ids[b, :n] = r["ids"]
+            lp[b, :n] = r["logprobs"]
+        base = np.zeros(B) if last is None else np.asarray(last, dtype=np.float64)
+        cu = lp + base[:, None]
+        scores, parents, tokens = beam_expand(lp, ids, last, k_t)
+        positions.append(dict(k=k, heads=heads, ids=ids, logprobs=lp, cu_scores=cu, scores=scores,
+                              parents=parents, tokens=tokens))
+        last = scores
+        if j < gamma:
+            x, h = next_inputs(h[parents], tokens)
+    entries = [(positions[j]["cu_scores"][b, r], j, b, r, positions[j]["ids"][b, r])
+               for j in range(len(positions)) for b in range(positions[j]["ids"].shape[0])
+               for r in range(k_t) if positions[j]["ids"][b, r] >= 0]
+    entries.sort(key=lambda e: (-e[0], e[1], e[2], e[3]))
+    draft_list = dict(scores=np.array([e[0] for e in entries]),
+                      position=np.array([e[1] for e in entries], dtype=np.int64),
+                      row=np.array([e[2] for e in entries], dtype=np.int64),
+                      rank=np.array([e[3] for e in entries], dtype=np.int64),
+                      ids=np.array([e[4] for e in entries], dtype=np.int64))
+    return positions, draft_list
+
+
 def dense_head(h, W_lm, k_t=1, temperature=1.0, u=None, n_rows=None):
     """Full-vocabulary head O = H W_LM (Sec. 4.1), or, with n_rows, the static
     head over the first n_rows vocabulary ids (Sec. 4.1, the FR-Spec drafter,

@@ -421,15 +421,23 @@ def union_cap(layout: "Layout", B: int, k: int) -> int:
     return min(layout.V, B * layout.cap(k))
 
 
-def beam_expand(logprobs, ids, last_scores=None, n_out=None, stream=None):
-    """dyna_beam_expand -> (scores[n_out], parent[n_out], ids[n_out])."""
+def beam_expand(logprobs, ids, last_scores=None, n_out=None, stream=None, out=None):
+    """dyna_beam_expand -> (scores[n_out], parent[n_out], ids[n_out]); out: an
+    existing (scores, parent, ids) triple to write instead of fresh tensors."""
     import torch
     B, k_t = logprobs.shape
     n_out = k_t if n_out is None else n_out
     dev = logprobs.device
-    sc = torch.empty(n_out, dtype=torch.float32, device=dev)
-    par = torch.empty(n_out, dtype=torch.int32, device=dev)
-    tok = torch.empty(n_out, dtype=torch.int32, device=dev)
+    if out is not None:
+        sc, par, tok = out
+        for t, dt in zip(out, (torch.float32, torch.int32, torch.int32)):
+            _need(t, "out")
+            if t.dtype != dt or t.numel() < n_out:
+                raise ValueError("beam_expand: out tensors must be (float32, int32, int32) of n_out entries")
+    else:
+        sc = torch.empty(n_out, dtype=torch.float32, device=dev)
+        par = torch.empty(n_out, dtype=torch.int32, device=dev)
+        tok = torch.empty(n_out, dtype=torch.int32, device=dev)
     _check(lib().dyna_beam_expand(_ptr(logprobs), _ptr(ids), _ptr(last_scores), B, k_t, n_out, _ptr(sc),
                                   _ptr(par), _ptr(tok), _stream(stream)))
     return sc, par, tok

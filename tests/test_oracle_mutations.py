@@ -184,6 +184,29 @@ def empty_shortlist_takes_complement_token(z, vocab_ids, k_t=1, temperature=1.0,
     return ORIG["draft_select"](z, vocab_ids, k_t, temperature, u, beta, complement_ids)
 
 
+def beam_ignores_parent_scores(logprobs, ids, last_scores, n_out):
+    return ORIG["beam_expand"](logprobs, ids, None, n_out)
+
+
+def beam_per_row_best(logprobs, ids, last_scores, n_out):
+    # each parent keeps its own best candidates in turn instead of the global best
+    sc, par, tok = ORIG["beam_expand"](logprobs, ids, last_scores, 10 ** 6)
+    order = sorted(range(len(sc)), key=lambda i: (par[i], -sc[i]))[:n_out]
+    return sc[order], par[order], tok[order]
+
+
+def cycle_broadcasts_one_parent(x0, h0, next_inputs, *args, **kw):
+    # h~[-1] taken for every row at every position, not only after position 0
+    return ORIG["draft_cycle"](x0, h0, lambda hp, tok: next_inputs(np.repeat(hp[-1:], len(tok), axis=0), tok),
+                               *args, **kw)
+
+
+def cycle_fixed_budget(x0, h0, next_inputs, W1, W2, act, cluster_of, M, W_lm, k_first, k_second, k_t, gamma,
+                       k_min=1, form="equation"):
+    return ORIG["draft_cycle"](x0, h0, next_inputs, W1, W2, act, cluster_of, M, W_lm, k_first, k_first, k_t,
+                               gamma, k_min=max(k_min, k_first), form=form)
+
+
 MUTANTS = {
     "layout: descending ids inside a cluster": ("cluster_layout", layout_desc_within_cluster,
         [P.test_layout_hand_example, lambda: P.test_layout_is_disjoint_covering_and_contiguous(0)]),
@@ -238,6 +261,15 @@ MUTANTS = {
         [P.test_kmeans_similarity_is_exact_below_bf16_resolution]),
     "select: an empty shortlist still proposes a token": ("draft_select", empty_shortlist_takes_complement_token,
         [P.test_empty_shortlist_proposes_nothing]),
+    "beam: parent scores not added": ("beam_expand", beam_ignores_parent_scores,
+        [P.test_beam_expand_hand_example, lambda: P.test_draft_cycle_on_the_full_vocabulary_is_a_brute_force_beam(0)]),
+    "beam: best per parent instead of overall": ("beam_expand", beam_per_row_best,
+        [P.test_beam_expand_hand_example, lambda: P.test_draft_cycle_on_the_full_vocabulary_is_a_brute_force_beam(1)]),
+    "cycle: one parent row for every beam row": ("draft_cycle", cycle_broadcasts_one_parent,
+        [lambda: P.test_draft_cycle_on_the_full_vocabulary_is_a_brute_force_beam(2),
+         P.test_draft_cycle_budget_union_and_parent_rows]),
+    "cycle: the first budget at every position": ("draft_cycle", cycle_fixed_budget,
+        [P.test_draft_cycle_budget_union_and_parent_rows]),
 }
 
 

@@ -406,6 +406,87 @@ def test_beam_expand_hand_example():
     assert p2.tolist() == [0, 0, 1] and t2.tolist() == [1, 2, 3]  # the empty candidate is never chosen
 
 
+# ---------------------------------------------------------------- Algorithm 1, one cycle
+def _cycle_problem(seed, V, M, d, H=6):
+    """A tiny cycle: router over [h_parent, emb(token)] (d_r = 2d, as in
+    Algorithm 1) and a fixed map standing in for the draft layer."""
+    rng = np.random.default_rng(seed)
+    cluster_of = rng.permutation(np.arange(V) % M)
+    W = rng.standard_normal((V, d))
+    E = rng.standard_normal((V, d))
+    A = rng.standard_normal((d, 2 * d)) / np.sqrt(2 * d)
+    W1, W2 = rng.standard_normal((H, 2 * d)), rng.standard_normal((M, H))
+    h0 = rng.standard_normal((1, d))
+    x0 = np.concatenate([rng.standard_normal((1, d)), E[[3]]], axis=1)
+
+    def next_inputs(hp, tok):
+        xin = np.concatenate([hp, E[np.asarray(tok)]], axis=1)
+        return xin, np.tanh(xin @ A.T) * 2.0
+    return cluster_of, W, W1, W2, x0, h0, next_inputs
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_draft_cycle_on_the_full_vocabulary_is_a_brute_force_beam(seed):
+    """Budget M at every position (k_min = M): the shortlist is the whole
+    vocabulary, and each position's beam is the k_t best of ALL (parent,
+    token) extensions by path log-probability (the best k_t overall always
+    lie inside the parents' own k_t best, so the per-row cut loses nothing)."""
+    from scipy.special import log_softmax as ref_lsm
+    V, M, d, k_t, gamma = 12, 4, 5, 3, 3
+    cluster_of, W, W1, W2, x0, h0, nxt = _cycle_problem(seed, V, M, d)
+    pos, dl = O.draft_cycle(x0, h0, nxt, W1, W2, "silu", cluster_of, M, W, M, M, k_t, gamma, k_min=M)
+    beam = [(0.0, h0[0], ())]  # (path log-prob, hidden row, tokens so far)
+    listed = []
+    for j in range(gamma + 1):
+        assert pos[j]["k"] == M
+        ext = []
+        for b, (sc, hb, path) in enumerate(beam):
+            lp = ref_lsm(W @ hb)
+            for v in range(V):
+                ext.append((sc + lp[v], b, v))
+            listed += [sc + lp[v] for v in sorted(range(V), key=lambda v: (-lp[v], v))[:k_t]]
+        ext.sort(key=lambda e: (-e[0], e[1], e[2]))
+        best = ext[:k_t]
+        np.testing.assert_allclose(pos[j]["scores"], [e[0] for e in best], rtol=1e-12)
+        assert pos[j]["parents"].tolist() == [e[1] for e in best]
+        assert pos[j]["tokens"].tolist() == [e[2] for e in best]
+        hp = np.stack([beam[e[1]][1] for e in best])
+        _, hn = nxt(hp, [e[2] for e in best])
+        beam = [(e[0], hn[i], beam[e[1]][2] + (e[2],)) for i, e in enumerate(best)]
+    # the draft list: every row's k_t candidates of every position, by path score
+    np.testing.assert_allclose(dl["scores"], sorted(listed, reverse=True), rtol=1e-12)
+    assert len(dl["ids"]) == k_t + gamma * k_t * k_t
+
+
+def test_draft_cycle_budget_union_and_parent_rows():
+    """Position j routes every row with k_c(j) clusters, all rows share the
+    union of their clusters, and position j+1's router input row i is
+    [h~_j[parent_i], emb(token_i)] (h~[-1] for every row after position 0)."""
+    V, M, d, k_t, gamma = 40, 10, 4, 3, 4
+    cluster_of, W, W1, W2, x0, h0, nxt = _cycle_problem(7, V, M, d)
+    pos, dl = O.draft_cycle(x0, h0, nxt, W1, W2, "silu", cluster_of, M, W, 8, 6, k_t, gamma)
+    assert [p["k"] for p in pos] == [8, 6, 2, 1, 1]    # eq. pos_schedule for k0 = 8, k1 = 6
+    x, h = x0, h0
+    for j, p in enumerate(pos):
+        s = O.router_scores(x, W1, W2, act="silu")
+        chosen = {m for b in range(len(x)) for m in sorted(range(M), key=lambda m: (-s[b, m], m))[:p["k"]]}
+        union = set(np.nonzero(np.isin(cluster_of, sorted(chosen)))[0].tolist())
+        for b, r in enumerate(p["heads"]):
+            np.testing.assert_allclose(r["scores"], s[b], rtol=1e-12)
+            assert set(r["vocab_ids"].tolist()) == union
+            assert set(p["ids"][b][p["ids"][b] >= 0].tolist()) <= union
+        np.testing.assert_allclose(p["cu_scores"], p["logprobs"] + (0 if j == 0 else pos[j - 1]["scores"][:, None]),
+                                   rtol=1e-12)
+        x, h = nxt(h[p["parents"]], p["tokens"])
+        if j == 0:
+            assert np.array_equal(x[:, :d], np.repeat(h0, k_t, axis=0))
+    # draft list: sorted, every position's candidates once
+    assert np.all(np.diff(dl["scores"]) <= 0)
+    assert sorted(zip(dl["position"].tolist(), dl["row"].tolist(), dl["rank"].tolist())) == sorted(
+        (j, b, r) for j, p in enumerate(pos) for b in range(p["ids"].shape[0]) for r in range(k_t)
+        if p["ids"][b, r] >= 0)
+
+
 def test_k_equals_M_is_the_dense_head():
     V, M = 64, 8
     cluster_of, W, h, W1, W2, u = _tiny_problem(11, V=V, M=M, d=10, B=4)
