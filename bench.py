@@ -863,6 +863,16 @@ def run_workload(w, args, D, torch, shared, steps=None, with_cpu=True):
         e1.record()
         torch.cuda.synchronize()
         base["dense_torch_matmul_argmax"] = {"ms_per_step": round(e0.elapsed_time(e1) / K, 5)}
+        # the practical row-streaming ceiling: the one-context dense head (the
+        # dense baseline itself when B = 1)
+        if w.B == 1:
+            probe = base["dense"]["GBps"]
+        else:
+            ph = D.DenseHead(W_lm, w.V, 1, D.SEL_ARGMAX, 1)
+            h1 = W.contexts(w, dev, batch=1)
+            g_s, _ = time_graph_steps(lambda i: (lambda: ph(h1, W=Ws[i % N_REPLICAS])), 40, torch)
+            probe = round(s_w * w.V * w.d * 40 / g_s / 1e9, 1)
+            del ph
         del Ws
         # the faster of the two dense heads on this GPU is the one to beat
         dense_ms = min(base["dense"]["ms_per_step"], base["dense_torch_matmul_argmax"]["ms_per_step"])
@@ -872,9 +882,8 @@ def run_workload(w, args, D, torch, shared, steps=None, with_cpu=True):
         rec["speedup_vs_static"] = round(base["static"]["ms_per_step"] / rec["ms_per_step"], 3)
         rec["byte_ratio_dense_over_dynamic"] = round(dense_bytes / step_bytes, 3)
         rec["speedup_target"] = round(0.8 * dense_bytes / step_bytes, 3)
-        # the dense head's streaming rate is this GPU's practical row-streaming
-        # ceiling (the probe of --probe, measured in the same run)
-        probe = base["dense"]["GBps"]
+        # the one-context dense head's streaming rate is this GPU's practical
+        # row-streaming ceiling (the probe of --probe, measured in the same run)
         rec["roofline"]["probe_GBps"] = probe
         rec["roofline"]["frac_of_probe"] = round(achieved / probe, 4) if probe else None
         rec["step_frac_of_probe"] = round(step_bytes * steps_per_s / 1e9 / probe, 4) if probe else None

@@ -850,7 +850,7 @@ DYNA_API dyna_status dyna_kmeans(const void* W, int32_t wdtype, int32_t V, int32
 }
 
 // ------------------------------------------------------------------ baselines
-static size_t dense_bytes(int32_t n_rows, int32_t B, float** logits, void** sel, void* base) {
+static size_t dense_bytes(int32_t n_rows, int32_t B, float** logits, void** sel, void* base, Plan* plan = nullptr) {
     char* p = static_cast<char*>(base);
     size_t off = 0;
     const size_t lb = align256(sizeof(float) * (size_t)B * (size_t)n_rows);
@@ -858,6 +858,16 @@ static size_t dense_bytes(int32_t n_rows, int32_t B, float** logits, void** sel,
     off += lb;
     if (sel) *sel = p ? p + off : nullptr;
     off += align256(select_ws_bytes(B, n_rows, DYNA_MAX_KT));
+    // the full-row plan of the matrix-core path (one chunk per 16 rows)
+    const int64_t n_chunks = ((int64_t)n_rows + kChunkRows - 1) / kChunkRows;
+    if (plan && p) {
+        plan->hdr = reinterpret_cast<PlanHeader*>(p + off);
+        plan->list = reinterpret_cast<ListEntry*>(p + off + sizeof(PlanHeader));
+        plan->chunks = reinterpret_cast<Chunk*>(p + off + sizeof(PlanHeader) + align256(sizeof(ListEntry)));
+        plan->max_chunks = (int32_t)n_chunks;
+        plan->max_entries = 1;
+    }
+    off += sizeof(PlanHeader) + align256(sizeof(ListEntry)) + align256(sizeof(Chunk) * (size_t)n_chunks);
     return off;
 }
 
@@ -884,7 +894,8 @@ DYNA_API dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_ro
     if (ws_bytes < need) return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
     float* wl = nullptr;
     void* sel = nullptr;
-    dense_bytes(n_rows, B, &wl, &sel, ws);
+    Plan plan{};
+    dense_bytes(n_rows, B, &wl, &sel, ws, &plan);
     float* logits = out_logits ? out_logits : wl;
     RowdotArgs a{};
     a.W = W;
@@ -897,7 +908,16 @@ DYNA_API dyna_status dyna_dense_head(const void* W, int32_t wdtype, int32_t n_ro
     a.ld = n_rows;
     a.act = DYNA_ACT_NONE;
     a.n_rows = n_rows;
-    TRY(timed_rowdot(a, option_logits_path(), stream));
+    if (option_logits_path() == 0 && B > 4 && wdtype == DYNA_BF16 && hdtype == DYNA_BF16) {
+        // several contexts: the rows streamed once through LDS by the union
+        // kernel, every context multiplied on the matrix cores
+        a.plan = plan;
+        a.max_chunks_bound = plan.max_chunks;
+        TRY(launch_full_plan(n_rows, B, plan, stream));
+        TRY(timed([&] { return launch_union_gemm(a, stream); }, stream));
+    } else {
+        TRY(timed_rowdot(a, option_logits_path(), stream));
+    }
     const bool want_ids = (mode & (DYNA_SEL_ARGMAX | DYNA_SEL_TOPK)) != 0;
     const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     return launch_select(logits, n_rows, nullptr, n_rows, n_rows, nullptr, nullptr, nullptr, nullptr, B, 0, k_t,

@@ -144,6 +144,10 @@ dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream);
 // union rows (every plan chunk lists contexts 0..B-1 in order): dense
 // LDS-staged MFMA product; vid_out gets one shared row [slots]
 dyna_status launch_union_gemm(const RowdotArgs& a, hipStream_t stream);
+// Plan over rows [0, V): one chunk per 16 rows, every chunk shared by all B
+// contexts (one list entry, slot base 0), so the union kernel computes the
+// dense product of the rows with every context.
+dyna_status launch_full_plan(int32_t V, int32_t B, const Plan& plan, hipStream_t stream);
 // The same product with an argmax epilogue: every plan row against the B
 // contexts (centroids); vid_out[slot] = the best context (ties to the lower
 // id), out[slot] = its product (out may be null).

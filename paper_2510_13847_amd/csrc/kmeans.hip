@@ -251,14 +251,14 @@ dyna_status launch_update(const uint16_t* W, int32_t V, int32_t d, const int32_t
     return set_error(DYNA_ERR_UNSUPPORTED, "k-means: d=%d > 8192", d);
 }
 
+}  // namespace
+
 dyna_status launch_full_plan(int32_t V, int32_t M, const Plan& plan, hipStream_t stream) {
     const int64_t n = ((int64_t)V + kChunkRows - 1) / kChunkRows;
     const unsigned blocks = (unsigned)std::min<int64_t>(1024, (n + 255) / 256);
     full_plan_kernel<<<std::max(1u, blocks), 256, 0, stream>>>(V, M, plan);
     return check_launch("full_plan_kernel");
 }
-
-}  // namespace
 
 size_t kmeans_ws_bytes(int32_t V, int32_t d, int32_t M) { return km_carve(V, d, M, nullptr).bytes; }
 

@@ -617,7 +617,7 @@ def test_k_equals_M_is_the_dense_head():
         assert ok
 
 
-@pytest.mark.parametrize("B", [1, 6])
+@pytest.mark.parametrize("B", [1, 6, 37])
 def test_static_head_prefix(B):
     w = CASES[4]
     p = Problem(w)
