@@ -215,7 +215,7 @@ def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20, route_gri
             "overlapped_speedup_vs_draft_plus_dense": round(t_d / t_o, 3) if t_o > 0 else None}
 
 
-KERNEL_UNITS = {"chain_step_kernel": "chain.hip", "logits_greedy_kernel": "fused.hip", "gather_lds_kernel": "gather.hip", "gather_ring_kernel": "gather.hip", "union_gemm_kernel": "gather.hip",
+KERNEL_UNITS = {"chain_step_kernel": "chain.hip", "logits_greedy_kernel": "fused.hip", "gather_ring_kernel": "gather.hip", "union_gemm_kernel": "gather.hip",
                 "rowdot_gemv_kernel": "rowdot.hip"}
 
 

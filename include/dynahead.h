@@ -376,7 +376,7 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
 /* Kernel-path override for tests and measurement:
  * DYNA_OPT_LOGITS_PATH: 0 automatic, 1 wave-per-row GEMV, 2 MFMA tiles with
  *   the slab rows staged through LDS (bf16 weights and contexts; other types
- *   fall back to 3), 3 MFMA tiles loaded straight from HBM.
+ *   take the GEMV).
  * DYNA_OPT_ROUTER_PATH: 0 automatic, 1 GEMV, 2 split-K MFMA with the contexts
  *   staged in LDS (bf16 weights, up to 128 contexts; else 3), 3 MFMA tiles
  *   loaded straight from HBM.
@@ -400,14 +400,13 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   must know which form ran).  All give bit-identical results.
  *   Under kernel timing the one-launch step, or the fused gathered-head +
  *   selection launch, is what is timed.
- * DYNA_OPT_MFMA_UNROLL: k steps the direct-load MFMA kernel (path 3) loads
- *   ahead: 0 automatic (8), 4, 8 or 16.
+ * DYNA_OPT_MFMA_UNROLL: k steps the direct-load MFMA kernel (router path 3,
+ *   and dense heads of fp32 contexts) loads ahead: 0 automatic (8), 4, 8 or 16.
  * DYNA_OPT_GATHER_CFG: shape of the LDS-staged MFMA kernel (path 2): 0
  *   automatic (slab rows staged through LDS, contexts loaded into
- *   registers, two workgroups of two waves per compute unit); 1..9 the
- *   older kernel that stages the contexts through LDS too (waves per block,
- *   ring stages, k columns per stage, context columns per pass); 10..13
- *   other shapes of the automatic kernel.
+ *   registers, two workgroups of two waves per compute unit); 1..4 other
+ *   shapes of the same kernel (waves per workgroup, ring stages, k columns
+ *   per stage).
  * DYNA_OPT_GREEDY_GRID: workgroups of the fused one-context gathered head:
  *   0 automatic (256), else 1..4096; of the one-launch step: 0 automatic (one
  *   per compute unit), else that many, capped at 1024 and at what the

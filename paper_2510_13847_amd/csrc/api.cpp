@@ -431,12 +431,12 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         return DYNA_OK;
     }
     if (option == DYNA_OPT_GATHER_CFG) {
-        REQUIRE(value >= 0 && value <= 13, "gather shape %d outside [0, 13]", value);
+        REQUIRE(value >= 0 && value <= 4, "gather shape %d outside [0, 4]", value);
         g_gather_cfg.store(value);
         return DYNA_OK;
     }
     if (option == DYNA_OPT_LOGITS_PATH) {
-        REQUIRE(value >= 0 && value <= 3, "logits path %d outside [0, 3]", value);
+        REQUIRE(value >= 0 && value <= 2, "logits path %d outside [0, 2]", value);
         g_logits_path.store(value);
         return DYNA_OK;
     }

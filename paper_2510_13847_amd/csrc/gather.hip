@@ -14,19 +14,19 @@
 // wave instruction is a direct-to-LDS load (global_load_lds_dwordx4) of whole
 // 256- or 512-byte row pieces, and the MFMA operands are read back from LDS.
 // Each wave keeps a private ring of S stages (a stage = KB columns of the 16
-// tile rows plus the same KB columns of its context rows), so S - 1 stages of
-// loads are always in flight without holding any registers; the wave waits on
-// its own load counter only, never on a barrier.
+// tile rows), so S - 1 stages of slab loads are always in flight; the context
+// columns come straight from L2 into registers.  The wave waits on its own
+// load counter only, never on a barrier.
 //
 // Every other memory read inside the loop (chunk descriptors, context lists,
 // the vocabulary ids of the tile rows) goes through the scalar unit, so the
 // vector-memory counter only ever holds the staged loads and the output
 // stores, and waiting on it never drains the ring.
 //
-// LDS layout of a stage: A [16 rows][KB/8 pieces of 16 B], then B [NC
-// contexts][KB/8 pieces].  Piece p of row r is stored at position p ^ r (the
-// writer picks which global piece each lane fetches), so the 16 lanes that
-// read one piece index from 16 rows hit 16 different bank groups.
+// LDS layout of a stage: [16 rows][KB/8 pieces of 16 B].  Piece p of row r
+// is stored at position p ^ r (the writer picks which global piece each lane
+// fetches), so the 16 lanes that read one piece index from 16 rows hit 16
+// different bank groups.
 #include <atomic>
 
 #include "dyna_device.h"
@@ -132,165 +132,8 @@ __device__ __forceinline__ int group_entries(const Unit& u, const Plan& plan, in
     return n;
 }
 
-// NW waves per block, S ring stages per wave, KB k-columns per stage, NC context columns.
-template <int NW, int S, int KB, int NC>
-__global__ __launch_bounds__(NW * kWave) void gather_lds_kernel(RowdotArgs a) {
-    constexpr int ROWB = KB * 2;         // bytes of one row per stage
-    constexpr int PIECES = ROWB / 16;    // 16-byte pieces per row per stage
-    constexpr int RPI = kWave / PIECES;  // rows per direct-to-LDS instruction
-    constexpr int NA = kMfmaRows / RPI;  // A instructions per stage
-    constexpr int NBI = (NC + RPI - 1) / RPI;  // B instructions per stage (at most)
-    constexpr int A_BYTES = kMfmaRows * ROWB;
-    constexpr int STAGE = A_BYTES + NBI * RPI * ROWB;
-    constexpr int STEPS = KB / 32;       // MFMA k steps per stage
-    static_assert(PIECES <= kWave && kWave % PIECES == 0 && kMfmaRows % RPI == 0, "stage shape");
-    static_assert(NC <= 16 && (NC & (NC - 1)) == 0, "context columns");
-
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    const int lane = lane_id();
-    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    char* ring = smem + wv * (S * STAGE);
-    const int K = a.K;
-    const int nkb = (K + KB - 1) / KB;
-    const uint16_t* __restrict__ W = static_cast<const uint16_t*>(a.W);
-    const uint16_t* __restrict__ v = static_cast<const uint16_t*>(a.v);
-    const int64_t n_items = (int64_t)((sptr<int32_t>)a.plan.hdr)[0];
-    const int64_t stride = (int64_t)gridDim.x * NW;
-
-    // loader lanes: row (or context) RPI * i + lsub, stored piece lpc
-    const int lsub = lane / PIECES, lpc = lane % PIECES;
-    // MFMA lanes: tile row / context column `col`, k slice kq
-    const int col = lane & 15, kq = lane >> 4;
-    const int ccol = col & (NC - 1);
-
-    Unit iu;  // issue cursor
-    iu.it = (int64_t)blockIdx.x * NW + wv;
-    find_tile(iu, a.plan, n_items, stride);
-    if (!iu.valid) return;
-    Unit cu = iu;  // consume cursor
-
-    // issue-side group state: per B instruction, this lane's context row
-    const uint16_t* bsrc[NBI];
-    int nbi = 0;
-    auto issue_group = [&]() {
-        int vb, vs;
-        const int n = group_entries<NC>(iu, a.plan, vb, vs);
-        nbi = (n + RPI - 1) / RPI;
-#pragma unroll
-        for (int i = 0; i < NBI; ++i) bsrc[i] = v + (int64_t)from_lane(vb, min(RPI * i + lsub, n - 1)) * K;
-    };
-    // consume-side group state: this lane's output row base, and tile vocabulary ids
-    int ncols = 0;
-    int64_t obase = 0;
-    int32_t vid[4] = {0, 0, 0, 0};
-    auto consume_group = [&]() {
-        int vb, vs;
-        ncols = group_entries<NC>(cu, a.plan, vb, vs);
-        obase = (int64_t)from_lane(vb, ccol) * a.ld + from_lane(vs, ccol) + cu.r0;
-        if (a.vid_out != nullptr && cu.g == 0) {
-            // lane j < 16 of vp holds the vocabulary id of tile row j
-            sptr<int32_t> P = (sptr<int32_t>)a.perm + cu.r0;
-            int vp = P[0];
-            if (cu.nrows == kMfmaRows) {
-#pragma unroll
-                for (int j = 1; j < kMfmaRows; ++j) vp = set_lane(vp, P[j], j);
-            } else {
-#pragma unroll
-                for (int j = 1; j < kMfmaRows; ++j)
-                    if (j < cu.nrows) vp = set_lane(vp, P[j], j);
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) vid[r] = from_lane(vp, 4 * kq + r);
-        }
-    };
-
-    auto issue = [&](int slot) {
-        char* dst = ring + slot * STAGE;
-        const int kb = iu.kb;
-#pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            const int row = RPI * i + lsub;
-            const int piece = lpc ^ (row % PIECES);
-            int e = kb * KB + piece * 8;
-            e = e < K ? e : 0;  // k tail: any in-bounds piece; zeroed when read
-            const uint16_t* src = W + (int64_t)(iu.r0 + min(row, iu.nrows - 1)) * K + e;
-            __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + i * (RPI * ROWB)), 16, 0, kSlabPolicy);
-        }
-#pragma unroll
-        for (int i = 0; i < NBI; ++i) {
-            if (i < nbi) {
-                const int c = RPI * i + lsub;
-                const int piece = lpc ^ (c % PIECES);
-                int e = kb * KB + piece * 8;
-                e = e < K ? e : 0;
-                __builtin_amdgcn_global_load_lds((glb_ptr)(bsrc[i] + e),
-                                                 (lds_ptr)(dst + A_BYTES + i * (RPI * ROWB)), 16, 0, 0);
-            }
-        }
-    };
-
-    issue_group();
-    consume_group();
-    int issued = 0;
-#pragma unroll
-    for (int s = 0; s < S - 1; ++s) {
-        if (iu.valid) {
-            issue(issued % S);
-            ++issued;
-            if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) issue_group();
-        }
-    }
-
-    int consumed = 0;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    while (true) {
-        if (iu.valid) {
-            issue(issued % S);
-            ++issued;
-            if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) issue_group();
-            wait_vmem<(S - 1) * NA>();  // the S - 1 later stages may stay in flight
-        } else {
-            wait_vmem<0>();
-        }
-        const char* st = ring + (consumed % S) * STAGE;
-        const int k0 = cu.kb * KB;
-#pragma unroll
-        for (int s = 0; s < STEPS; ++s) {
-            const int p = s * 4 + kq;
-            u32x4 av = *reinterpret_cast<const u32x4*>(st + col * ROWB + (p ^ (col % PIECES)) * 16);
-            u32x4 bv = *reinterpret_cast<const u32x4*>(st + A_BYTES + ccol * ROWB + (p ^ (ccol % PIECES)) * 16);
-            if (col >= ncols) bv = u32x4{0u, 0u, 0u, 0u};
-            if (k0 + p * 8 >= K) {
-                av = u32x4{0u, 0u, 0u, 0u};
-                bv = u32x4{0u, 0u, 0u, 0u};
-            }
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
-                                                          __builtin_bit_cast(bf16x8, bv), acc, 0, 0, 0);
-        }
-        ++consumed;
-        if (cu.kb == nkb - 1) {
-            // D rows 4 * kq + r, column col
-            if (col < ncols) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int row = 4 * kq + r;
-                    if (row < cu.nrows) {
-                        a.out[obase + row] = acc[r];
-                        if (a.vid_out != nullptr) a.vid_out[obase + row] = vid[r];
-                    }
-                }
-            }
-            acc = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-        if (advance<NC>(cu, nkb, a.plan, n_items, stride)) {
-            if (!cu.valid) break;
-            consume_group();
-        }
-    }
-}
-
-// The same work units with only the slab rows (A) in the LDS ring and the
-// context columns (B) loaded straight into registers: the contexts of a
+// Gathered-head kernel: only the slab rows (A) go through the LDS ring; the
+// context columns (B) are loaded straight into registers.  The contexts of a
 // step stay in L2, and keeping them out of LDS leaves the whole ring to the
 // slab rows, so each wave keeps more HBM bytes in flight.  Every stage
 // issues exactly NA direct-to-LDS loads and STEPS register loads (lanes
@@ -509,32 +352,6 @@ dyna_status launch_ring_cfg(const RowdotArgs& a, hipStream_t stream) {
     const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + NW - 1) / NW, 256 * per_cu));
     launch_timed_kernel(gather_ring_kernel<NW, S, KB>, dim3((unsigned)blocks), dim3(NW * kWave), LDS, stream, a);
     return check_launch("gather_ring_kernel");
-}
-
-template <int NW, int S, int KB, int NC>
-dyna_status launch_cfg(const RowdotArgs& a, hipStream_t stream) {
-    constexpr int ROWB = KB * 2, PIECES = ROWB / 16, RPI = kWave / PIECES;
-    constexpr int NBI = (NC + RPI - 1) / RPI;
-    constexpr int STAGE = kMfmaRows * ROWB + NBI * RPI * ROWB;
-    constexpr int LDS = NW * S * STAGE;
-    static_assert(LDS <= 160 * 1024, "LDS per block");
-    // more than 64 KiB of dynamic LDS must be allowed, once per kernel and
-    // device (the first launch is eager: a captured graph never sees this call)
-    static std::atomic<uint64_t> allowed{0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "gather: device");
-    if (!(allowed.load() & (1ull << dev))) {
-        if (hipFuncSetAttribute((const void*)gather_lds_kernel<NW, S, KB, NC>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, LDS) != hipSuccess)
-            return set_error(DYNA_ERR_HIP, "gather: LDS attribute");
-        allowed.fetch_or(1ull << dev);
-    }
-    const int per_cu = (160 * 1024) / LDS;
-    const int64_t items = (int64_t)a.max_chunks_bound;
-    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + NW - 1) / NW, 256 * per_cu));
-    launch_timed_kernel(gather_lds_kernel<NW, S, KB, NC>, dim3((unsigned)blocks), dim3(NW * kWave), LDS, stream,
-                        a);
-    return check_launch("gather_lds_kernel");
 }
 
 // ------------------------------------------------------------------ union head
@@ -909,19 +726,10 @@ bool gather_lds_eligible(const RowdotArgs& a) {
 dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
     if (!gather_lds_eligible(a)) return set_error(DYNA_ERR_UNSUPPORTED, "gather: needs bf16 plan mode");
     switch (option_gather_cfg()) {
-        case 1: return launch_cfg<4, 4, 128, 16>(a, stream);
-        case 2: return launch_cfg<4, 3, 256, 8>(a, stream);
-        case 3: return launch_cfg<4, 3, 128, 8>(a, stream);
-        case 4: return launch_cfg<2, 8, 128, 16>(a, stream);
-        case 5: return launch_cfg<4, 5, 64, 16>(a, stream);
-        case 6: return launch_cfg<8, 3, 64, 16>(a, stream);
-        case 7: return launch_cfg<8, 3, 128, 8>(a, stream);
-        case 8: return launch_cfg<4, 2, 512, 4>(a, stream);
-        case 9: return launch_cfg<3, 2, 512, 8>(a, stream);
-        case 10: return launch_ring_cfg<4, 2, 512>(a, stream);
-        case 11: return launch_ring_cfg<4, 4, 256>(a, stream);
-        case 12: return launch_ring_cfg<4, 8, 128>(a, stream);
-        case 13: return launch_ring_cfg<8, 8, 64>(a, stream);
+        case 1: return launch_ring_cfg<4, 2, 512>(a, stream);
+        case 2: return launch_ring_cfg<4, 4, 256>(a, stream);
+        case 3: return launch_ring_cfg<4, 8, 128>(a, stream);
+        case 4: return launch_ring_cfg<8, 8, 64>(a, stream);
         default: return launch_ring_cfg<2, 4, 256>(a, stream);  // two workgroups of two waves per CU
     }
 }

@@ -314,10 +314,11 @@ dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream) {
     if (path >= 2 && !mfma_ok)
         return set_error(DYNA_ERR_UNSUPPORTED, "rowdot: MFMA path needs bf16 weights");
     const bool use_mfma = path >= 2 || (path == 0 && mfma_ok && a.B > 4);
-    if (!use_mfma) return plan ? launch_gemv<true>(a, stream) : launch_gemv<false>(a, stream);
-    if (plan && path != 3 && gather_lds_eligible(a)) return launch_gather_lds(a, stream);
+    // a gathered head on the matrix cores needs bf16 slabs and contexts (the
+    // LDS-staged kernel); any other gathered head takes the GEMV
+    if (plan && use_mfma && gather_lds_eligible(a)) return launch_gather_lds(a, stream);
+    if (plan || !use_mfma) return plan ? launch_gemv<true>(a, stream) : launch_gemv<false>(a, stream);
     const bool vf32 = a.vdtype == DYNA_F32;
-    if (plan) return vf32 ? launch_mfma<true, true>(a, stream) : launch_mfma<false, true>(a, stream);
     return vf32 ? launch_mfma<true, false>(a, stream) : launch_mfma<false, false>(a, stream);
 }
 

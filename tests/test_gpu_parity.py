@@ -211,10 +211,9 @@ def _random_selection(p, B, k, seed):
     return np.array(rows, dtype=np.int32)
 
 
-@pytest.mark.parametrize("w,path", _paths([1, 2, 3], 2))
+@pytest.mark.parametrize("w,path", _paths([1, 2], 2))
 def test_logits_parity(w, path):
-    """Paths: 1 GEMV, 2 MFMA with LDS-staged slabs, 3 MFMA with direct loads
-    (the MFMA paths take bf16 weights only)."""
+    """Paths: 1 GEMV, 2 MFMA with LDS-staged slabs (bf16 weights only)."""
     p = Problem(w)
     topk = _random_selection(p, w.B, w.k, 3)
     sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
@@ -234,7 +233,7 @@ def test_logits_parity(w, path):
         assert np.all(np.isnan(lg[b, n:])), "slots past row_len must stay untouched"
 
 
-@pytest.mark.parametrize("cfg", list(range(0, 14)))
+@pytest.mark.parametrize("cfg", list(range(0, 5)))
 @pytest.mark.parametrize("name", ["ragged_b37", "zipf_b9", "many_b130"])
 def test_logits_gather_shapes(name, cfg):
     """Every workgroup shape of the LDS-staged MFMA gathered head."""
