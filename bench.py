@@ -115,22 +115,20 @@ def time_graph_steps(make_step, K, torch):
     return e0.elapsed_time(e1) / 1e3, wall
 
 
-def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20, route_grid=None):
+def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20):
     """Routing on a second stream while a stand-in draft layer (one GEMM of
     the drafter's MLP) runs on the caller's stream (Sec. 4.2 and Sec. 4.3:
     the router runs in parallel with the draft layer, so a step costs about
     T_D = T_emb + max(T_core, T_meta) + T_index+gemm).
 
     Times per step: the draft layer alone (T_core), routing alone (T_meta:
-    router and top-k; also with its grid capped at a quarter of the compute
-    units), both at once on two streams, and the hidden fraction
+    router and top-k), both at once on two streams, and the hidden fraction
     (T_core + T_meta - T_both) / T_meta.  Then whole steps: draft layer and
     head on one stream, draft layer with the head's routing on the second
     stream (the overlapped step), and the draft layer followed by the dense
     full-vocabulary head."""
     a, b = W.overlap_gemm_operands(w, "cuda")
     side = torch.cuda.Stream()
-    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
 
     def t_of(fn, reps=5):
         # n steps captured into one graph (second-stream work is forked from
@@ -186,28 +184,11 @@ def measure_overlap(w, D, head, layouts, routers, xs, us, torch, n=20, route_gri
         torch.matmul(a, b)
         dense(x_of(i), W=L(i).W_perm)
 
-    if route_grid is None:
-        route_grid = 0  # the library's default: routing at full width on the second stream
-    D.set_option(D.OPT_ROUTE_GRID, route_grid)
-    try:
-        t_g, t_r, t_b = t_of(gemm), t_of(route_only), t_of(both)
-    finally:
-        D.set_option(D.OPT_ROUTE_GRID, 0)
-    D.set_option(D.OPT_ROUTE_GRID, max(1, n_cu // 4))
-    try:
-        t_r_quarter = t_of(route_only)
-    finally:
-        D.set_option(D.OPT_ROUTE_GRID, 0)
-    D.set_option(D.OPT_ROUTE_GRID, route_grid)
-    try:
-        t_h, t_s, t_o, t_d = t_of(only_head), t_of(serial), t_of(overlapped), t_of(draft_then_dense)
-    finally:
-        D.set_option(D.OPT_ROUTE_GRID, 0)
+    t_g, t_r, t_b = t_of(gemm), t_of(route_only), t_of(both)
+    t_h, t_s, t_o, t_d = t_of(only_head), t_of(serial), t_of(overlapped), t_of(draft_then_dense)
     rows, K, N = w.overlap_gemm
     return {"draft_layer": f"[{rows},{K}]x[{K},{N}] bf16 (torch.matmul)",
-            "route_workgroups": route_grid if route_grid > 0 else "full width",
             "draft_us": round(t_g, 2), "route_us": round(t_r, 2),
-            "route_quarter_of_the_cus_us": round(t_r_quarter, 2),
             "draft_and_route_us": round(t_b, 2),
             "routing_hidden_frac": round(max(0.0, t_g + t_r - t_b) / t_r, 3) if t_r > 0 else None,
             "head_us": round(t_h, 2), "serial_step_us": round(t_s, 2), "overlapped_step_us": round(t_o, 2),

@@ -424,18 +424,11 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   out_ids = -1 and out_logprobs = -inf.  The error word carries the epoch
  *   of the launch that set it, so a later step is not failed by it; only a
  *   workgroup of a failed launch that started after the failure was
- *   reported fails the next step too, which may read its stale words.
- * DYNA_OPT_ROUTE_GRID: workgroups each router layer may take while routing
- *   runs on dyna_draft_head's route_stream beside the caller's draft layer
- *   (Sec. 4.2: the router on a parallel stream): 0 (default) and -1 no cap;
- *   1..4096 that many.  The results do not depend on it (each row, and each k slice
- *   of the batched router, is computed and summed the same way).  Set
- *   explicitly (1..4096), it caps dyna_route's router layers too, so that
- *   routing can be timed as it runs beside a draft layer. */
+ *   reported fails the next step too, which may read its stale words. */
 enum { DYNA_OPT_LOGITS_PATH = 1, DYNA_OPT_ROUTER_PATH = 2, DYNA_OPT_KERNEL_TIMING = 3,
        DYNA_OPT_GEMV_ROWS = 4, DYNA_OPT_FUSED_B1 = 5, DYNA_OPT_MFMA_UNROLL = 6,
        DYNA_OPT_GATHER_CFG = 7, DYNA_OPT_GREEDY_GRID = 8, DYNA_OPT_UNION_CFG = 9,
-       DYNA_OPT_KMEANS_CFG = 10, DYNA_OPT_WAIT_BOUND_US = 11, DYNA_OPT_ROUTE_GRID = 12 };
+       DYNA_OPT_KMEANS_CFG = 10, DYNA_OPT_WAIT_BOUND_US = 11 };
 dyna_status dyna_set_option(int32_t option, int32_t value);
 
 /* Waits for the events recorded under DYNA_OPT_KERNEL_TIMING and returns the

@@ -29,7 +29,6 @@ std::atomic<int> g_greedy_grid{0};
 std::atomic<int> g_union_cfg{0};
 std::atomic<int> g_kmeans_cfg{0};
 std::atomic<int> g_wait_bound_us{0};
-std::atomic<int> g_route_grid{0};
 
 // event pairs around timed gathered-head launches
 std::mutex g_timing_mu;
@@ -292,21 +291,11 @@ static dyna_status run_layer(const RowdotArgs& a, int path, float* part, size_t 
     return launch_rowdot(a, path >= 2 ? 3 : path, s);
 }
 
-// Workgroups the router layers may take when routing runs on a second
-// stream beside the caller's draft layer (DYNA_OPT_ROUTE_GRID): no cap by
-// default (capped grids measured slower both alone and beside a draft-layer
-// GEMM, which takes the whole chip itself), else that many.
-static int side_route_blocks() {
-    const int opt = g_route_grid.load();
-    return opt > 0 ? opt : 0;
-}
-
 static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtype, int32_t B,
                               float* scores, float* hidden, float* part, size_t part_floats, hipStream_t s,
-                              int32_t* zero_words = nullptr, ScoreSlices* defer = nullptr, int max_blocks = 0) {
+                              int32_t* zero_words = nullptr, ScoreSlices* defer = nullptr) {
     const int path = option_router_path();
     RowdotArgs a{};
-    a.max_blocks = max_blocks;
     a.zero_words = zero_words;  // cleared by block 0 of the first router kernel
     a.n_zero_words = zero_words ? 4 : 0;
     a.W = r->W1;
@@ -330,7 +319,6 @@ static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtyp
     a.n_rows = r->H;
     TRY(run_layer(a, path, part, part_floats, s));
     RowdotArgs b{};
-    b.max_blocks = max_blocks;
     b.W = r->W2;
     b.wdtype = r->wdtype;
     b.K = r->H;
@@ -408,11 +396,6 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
     if (option == DYNA_OPT_GREEDY_GRID) {
         REQUIRE(value >= 0 && value <= kGreedyMaxBlocks, "greedy grid %d outside [0, %d]", value, kGreedyMaxBlocks);
         g_greedy_grid.store(value);
-        return DYNA_OK;
-    }
-    if (option == DYNA_OPT_ROUTE_GRID) {
-        REQUIRE(value >= -1 && value <= 4096, "route grid %d outside [-1, 4096]", value);
-        g_route_grid.store(value);
         return DYNA_OK;
     }
     if (option == DYNA_OPT_WAIT_BOUND_US) {
@@ -539,10 +522,7 @@ DYNA_API dyna_status dyna_route(const dyna_router* r, const void* x, int32_t xdt
     if (ws_bytes < c0.bytes) return set_error(DYNA_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, c0.bytes);
     const Carve c = carve(nullptr, r, B, k, 0, ws);
     float* sc = scores ? scores : c.scores;
-    // an explicitly set DYNA_OPT_ROUTE_GRID caps this call's router too (to
-    // time routing as it runs beside a draft layer)
-    const int cap = g_route_grid.load() > 0 ? g_route_grid.load() : 0;
-    TRY(run_router(r, x, xdtype, B, sc, c.hidden, c.rpart, c.rpart_floats, stream, nullptr, nullptr, cap));
+    TRY(run_router(r, x, xdtype, B, sc, c.hidden, c.rpart, c.rpart_floats, stream));
     return launch_topk_clusters(sc, B, r->M, k, topk_ids, topk_scores, nullptr, nullptr, nullptr,
                                 nullptr, nullptr, stream);
 }
@@ -713,7 +693,7 @@ dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const vo
     // layer leaves its partial sums to the top-k
     ScoreSlices slices;
     TRY(run_router(r, x, adtype, B, c.scores, c.hidden, c.rpart, c.rpart_floats, rs, fused ? c.counters : nullptr,
-                   B > 1 ? &slices : nullptr, split ? side_route_blocks() : 0));
+                   B > 1 ? &slices : nullptr));
     // union rows: one dense product of the union's slabs with every context
     // (it needs only one list entry per union cluster, and writes one shared
     // copy of the slots' vocabulary ids)

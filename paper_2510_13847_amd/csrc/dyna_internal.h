@@ -113,7 +113,6 @@ struct RowdotArgs {
     // dense mode, optional: at most this many workgroups (0: no cap), for
     // routing on a second stream beside the caller's draft layer; the
     // results do not depend on it
-    int32_t max_blocks;
 };
 dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);
 

@@ -154,27 +154,14 @@ __device__ __forceinline__ void splitk_slice(const RowdotArgs& a, int ksl, int s
         }
 }
 
-// Workgroup (x, y) takes k slice y of row tile x.  Each slice's partial
-// sums go to their own place, so the results do not depend on the grid.
+// Workgroup (x, y) takes k slice y of row tile x; each slice's partial sums
+// go to their own place.
 template <int NW, int G, bool VF32, int TT>
 __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, int ksl, float* part) {
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [G*16][ksl] hi, then lo
     if (a.zero_words != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && (int)threadIdx.x < a.n_zero_words)
         a.zero_words[threadIdx.x] = 0;
     splitk_slice<NW, G, VF32, TT>(a, ksl, blockIdx.y, part, xs);
-}
-
-// The same with a capped grid (routing beside a draft layer): workgroup
-// (x, y) takes the slices y, y + gridDim.y, ... below nsl one after another.
-template <int NW, int G, bool VF32, int TT>
-__global__ __launch_bounds__(NW * kWave) void dense_splitk_loop_kernel(RowdotArgs a, int ksl, int nsl, float* part) {
-    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
-    if (a.zero_words != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && (int)threadIdx.x < a.n_zero_words)
-        a.zero_words[threadIdx.x] = 0;
-    for (int sl = blockIdx.y; sl < nsl; sl += gridDim.y) {
-        if (sl != (int)blockIdx.y) __syncthreads();  // the previous slice's LDS reads are done
-        splitk_slice<NW, G, VF32, TT>(a, ksl, sl, part, xs);
-    }
 }
 
 // out[b * ld + r] = act(sum over slices, in slice order, + bias[r])
@@ -193,10 +180,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 
 template <int NW, int G, bool VF32, int TT>
 dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* part, bool reduce, hipStream_t stream) {
-    // a capped grid keeps every row tile and folds the slices onto fewer
-    // workgroups along k
-    const int gy = a.max_blocks > 0 ? std::max(1, std::min(sh.slices, a.max_blocks / sh.row_tiles)) : sh.slices;
-    const dim3 grid((unsigned)sh.row_tiles, (unsigned)gy);
+    const dim3 grid((unsigned)sh.row_tiles, (unsigned)sh.slices);
     const uint32_t lds = (uint32_t)sh.lds;
     if (lds > 64 * 1024) {
         // above 64 KiB the dynamic LDS size must be allowed, once per kernel and device
@@ -205,22 +189,16 @@ dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* pa
         if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "router: device");
         if (!(allowed.load() & (1ull << dev))) {
             if (hipFuncSetAttribute((const void*)dense_splitk_kernel<NW, G, VF32, TT>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget) != hipSuccess ||
-                hipFuncSetAttribute((const void*)dense_splitk_loop_kernel<NW, G, VF32, TT>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget) != hipSuccess)
                 return set_error(DYNA_ERR_HIP, "router: LDS attribute");
             allowed.fetch_or(1ull << dev);
         }
     }
-    if (gy < sh.slices)
-        dense_splitk_loop_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, sh.slices, part);
-    else
-        dense_splitk_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
+    dense_splitk_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
     const dyna_status st = check_launch("dense_splitk_kernel");
     if (st != DYNA_OK || !reduce) return st;
     const int rx = (a.n_rows + 255) / 256;
-    const int ry = a.max_blocks > 0 ? std::max(1, std::min(a.B, a.max_blocks / rx)) : a.B;
-    splitk_reduce_kernel<<<dim3((unsigned)rx, (unsigned)ry), dim3(256), 0, stream>>>(
+    splitk_reduce_kernel<<<dim3((unsigned)rx, (unsigned)a.B), dim3(256), 0, stream>>>(
         part, sh.slices, a.B, a.n_rows, a.out, a.ld, a.bias, a.act);
     return check_launch("splitk_reduce_kernel");
 }

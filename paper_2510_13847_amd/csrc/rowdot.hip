@@ -227,7 +227,6 @@ dyna_status launch_gemv_r(const RowdotArgs& a, bool single, hipStream_t stream) 
                                : ((int64_t)a.n_rows + R - 1) / R;
     int64_t blocks = std::max<int64_t>(
         1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock, 4096));
-    if (!PLAN && a.max_blocks > 0) blocks = std::min<int64_t>(blocks, a.max_blocks);  // grid-stride rows
     if (single)
         launch_timed_kernel(rowdot_gemv_kernel<WT, VT, NB, PLAN, R, true>, dim3((unsigned)blocks),
                             dim3(kThreads), 0, stream, a);

@@ -21,7 +21,7 @@ F32, BF16 = 0, 1
 ACT = {"none": 0, "relu": 1, "silu": 2}
 SEL_ARGMAX, SEL_TOPK, SEL_SAMPLE, SEL_UNION = 1, 2, 4, 8
 OPT_LOGITS_PATH, OPT_ROUTER_PATH, OPT_KERNEL_TIMING, OPT_GEMV_ROWS, OPT_FUSED_B1, OPT_MFMA_UNROLL = 1, 2, 3, 4, 5, 6
-OPT_GATHER_CFG, OPT_GREEDY_GRID, OPT_UNION_CFG, OPT_KMEANS_CFG, OPT_WAIT_BOUND_US, OPT_ROUTE_GRID = 7, 8, 9, 10, 11, 12
+OPT_GATHER_CFG, OPT_GREEDY_GRID, OPT_UNION_CFG, OPT_KMEANS_CFG, OPT_WAIT_BOUND_US = 7, 8, 9, 10, 11
 MAX_KT = 64
 
 

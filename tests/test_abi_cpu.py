@@ -62,10 +62,7 @@ def test_set_option_validation():
         assert lib.dyna_set_option(D.OPT_WAIT_BOUND_US, v) == D.ERR_INVALID_ARG
     for v in (-1, 1, 1000000, 0):
         assert lib.dyna_set_option(D.OPT_WAIT_BOUND_US, v) == D.OK
-    for v in (-2, 4097):
-        assert lib.dyna_set_option(D.OPT_ROUTE_GRID, v) == D.ERR_INVALID_ARG
-    for v in (-1, 1, 4096, 0):
-        assert lib.dyna_set_option(D.OPT_ROUTE_GRID, v) == D.OK
+    assert lib.dyna_set_option(12, 0) == D.ERR_INVALID_ARG  # no such option
     assert lib.dyna_set_option(D.OPT_FUSED_B1, 4) == D.ERR_INVALID_ARG
     for v in (3, 2, 1, 0):
         assert lib.dyna_set_option(D.OPT_FUSED_B1, v) == D.OK
