@@ -289,8 +289,9 @@ def summarize_trace(trace_dir, bench_json, plain_json, command):
         lines.append(f"bench.py without the profiler (same command minus rocprofv3): kernel "
                      f"{pr['avg_launch_us']} us{extra}, {pr['achieved']} {pr['unit']} = {pr['frac']} of peak; "
                      f"{plain['value']} {plain['unit']}.")
-    lines.append("rocprofv3 times a kernel from dispatch to completion signal; an empty kernel reads about "
-                 "1.5 us that way, which the event figure minus an empty bracket does not contain.")
+    lines.append("rocprofv3 times a kernel from its dispatch to its completion; bench.py's start and stop "
+                 "events are handed to the same dispatch (hipExtLaunchKernelGGL), so the two averages cover "
+                 "the same span.")
     tag = wl.split()[0] + ("_kmeans" if "k-means" in wl else "")
     out = os.path.join(ROOT, "profiles", f"{sym}_{tag}_kernel_trace.md")
     with open(out, "w") as f:
