@@ -109,9 +109,12 @@ __global__ __launch_bounds__(kNT) void shortlist_kernel(
 }
 
 // ------------------------------------------------------------------ plan
-// One workgroup.  Global reads are issued kPlanPer at a time per thread so
-// that their latencies overlap (the loops below are latency-bound, not
-// bandwidth-bound); the layout offsets are copied to LDS once.
+// Up to kPlanGrid workgroups.  Each one counts the contexts per cluster and
+// scans the counts itself (the same result in every workgroup), then writes
+// an equal share of the chunk table and the context lists of the clusters m
+// with m % gridDim.x == blockIdx.x.  Global reads are issued kPlanPer at a
+// time per thread so that their latencies overlap (the loops are
+// latency-bound, not bandwidth-bound); the layout offsets go to LDS once.
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanPer = 8;
 constexpr int kPlanGrid = 32;  // workgroups of a batch's plan
