@@ -806,8 +806,8 @@ def test_one_launch_step_wait_bound():
     from the host to nothing (a wait gives up at its first read that finds a
     word missing), a step must report the failure (id -1, log-probability
     -inf) and never a token from half-written data; once the bound is back,
-    the steps are correct again (the step that reports an error clears it; the
-    first step after may still report one set late in the failed launch)."""
+    the very next step is exact again (the error word carries the epoch of
+    the launch that set it, so a late give-up cannot fail a later step)."""
     w = next(c for c in FUSED_CASES if c.name == "chain_wide")
     p = Problem(w)
     mode = D.SEL_ARGMAX
