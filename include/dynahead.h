@@ -416,7 +416,7 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   row tiles per wave, k columns per stage, ring depth); a shape whose ring does not
  *   fit in LDS for the batch's context count returns DYNA_ERR_UNSUPPORTED.
  * DYNA_OPT_KMEANS_CFG: shape of the k-means assignment kernel: 0
- *   automatic, 1..4 fixed.
+ *   automatic, 1..7 fixed.
  * DYNA_OPT_WAIT_BOUND_US: bound of every wait of the one-launch step, in
  *   microseconds of wall clock: 0 (default) 200000, 1..1000000 that many,
  *   -1 none (a wait gives up at its first read that finds a word missing;

@@ -404,7 +404,7 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         return DYNA_OK;
     }
     if (option == DYNA_OPT_KMEANS_CFG) {
-        REQUIRE(value >= 0 && value <= 4, "k-means shape %d outside [0, 4]", value);
+        REQUIRE(value >= 0 && value <= 7, "k-means shape %d outside [0, 7]", value);
         g_kmeans_cfg.store(value);
         return DYNA_OK;
     }

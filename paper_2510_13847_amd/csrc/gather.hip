@@ -426,7 +426,10 @@ struct UnionShape {
     static constexpr int S = SREQ > 0 ? SREQ : (kUnionLds / STAGE < 8 ? kUnionLds / STAGE : 8);
     static constexpr int RPI = kWave / (ROWB / 16);  // rows per direct-to-LDS instruction
     static constexpr int NBI = 16 * NT / RPI;         // context instructions per stage
-    static constexpr bool ok = S >= 3 && S * STAGE <= kUnionLds && NBI >= NW && NBI % NW == 0;
+    // two stages only when asked for (double buffering: the barrier that
+    // starts a stage frees the other one)
+    static constexpr bool ok = (S >= 3 || (SREQ == 2 && S == 2)) && S * STAGE <= kUnionLds && NBI >= NW &&
+                               NBI % NW == 0;
 };
 
 // Max of a 64-bit key over the 16 lanes of each DPP row (lanes 16r .. 16r + 15):
@@ -752,7 +755,14 @@ dyna_status launch_union_argmax(const RowdotArgs& a, int cfg, hipStream_t stream
         case 2: return launch_union_cfg<4, 1, 128, 8, 3, 1>(a, stream);
         case 3: return launch_union_cfg<8, 1, 64, 16, 3, 1>(a, stream);
         case 4: return launch_union_cfg<4, 2, 64, 16, 3, 1>(a, stream);
-        default: return launch_union_cfg<8, 2, 64, 8, 0, 1>(a, stream);
+        case 5: return launch_union_cfg<4, 4, 64, 8, 3, 1>(a, stream);
+        case 6: return launch_union_cfg<8, 2, 64, 8, 0, 1>(a, stream);
+        case 7: return launch_union_cfg<8, 4, 64, 8, 2, 1>(a, stream);
+        // measured best: eight waves of two row tiles (256 rows) against 256
+        // centroids, double-buffered (two 64 KB stages).  The rows are
+        // re-read from HBM once per group of centroids, so wider groups cut
+        // the HBM bytes: 128-centroid groups measured 1.15-1.34x slower.
+        default: return launch_union_cfg<8, 2, 64, 16, 2, 1>(a, stream);
     }
 }
 

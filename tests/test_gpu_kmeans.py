@@ -70,7 +70,7 @@ SHAPES = [  # V (ragged vs 16-row tiles), d (ragged vs k blocks), M (one group, 
 ]
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("cfg", list(range(8)))
 @pytest.mark.parametrize("V,d,M", SHAPES)
 def test_assign_step(V, d, M, cfg):
     rng = np.random.default_rng(V + M)
