@@ -739,12 +739,18 @@ dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const vo
     if (dense_union && !gather_lds_eligible(a)) return set_error(DYNA_ERR_UNSUPPORTED, "union: kernel arguments");
     if (dense_union) TRY(timed([&] { return launch_union_gemm(a, stream); }, stream));
     else TRY(timed_rowdot(a, option_logits_path(), stream));
+    // union rows over a few thousand slots select faster in one launch (one
+    // workgroup per row); long union rows split into segments.  Measured at
+    // ten rows: 6-7 us saved per step at unions of 3.7-5.9k slots (row
+    // strides up to 26k), 3 us lost at 9.2k (stride 39k), 28 us at 32k; 77 us
+    // lost at 64 rows of 32k.
+    constexpr int32_t kUnionSplitCap = 32768;
     return launch_select(logits, cap, c.row_len, 0, cap, c.sel_sorted, c.sel_rowoff, L->offsets, L->perm, B,
                          k, k_t, temperature, tail_beta, L->V, want_sample ? uniforms : nullptr,
                          want_ids ? out_ids : nullptr,
                          want_ids ? out_logprobs : nullptr, want_sample ? out_sample : nullptr,
                          want_sample ? out_sample_logprob : nullptr, c.select_ws, stream, c.slot_vid,
-                         dense_union ? 0 : cap, union_mode);
+                         dense_union ? 0 : cap, union_mode && cap > kUnionSplitCap);
 }
 
 }  // namespace dyna
