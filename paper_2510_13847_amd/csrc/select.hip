@@ -378,6 +378,7 @@ __global__ __launch_bounds__(kPlanThreads) void union_plan_kernel(
 // cu_scores and TopK_{k_t}), ordered (cu desc, b asc, r asc) by the key
 // (ordered cu << 32) | ~(b * k_t + r).
 constexpr int kBeamPer = 8;
+constexpr int kBeamSmall = 256;  // candidates up to which one counting pass ranks them
 __global__ __launch_bounds__(kRowThreads) void beam_expand_kernel(const float* __restrict__ logprobs,
                                                                   const int32_t* __restrict__ ids,
                                                                   const float* __restrict__ last, int B, int k_t,
@@ -386,6 +387,41 @@ __global__ __launch_bounds__(kRowThreads) void beam_expand_kernel(const float* _
     __shared__ int hist[256];
     __shared__ uint64_t sel[DYNA_MAX_KT], top[DYNA_MAX_KT];
     const int n = B * k_t;
+    if (n <= kBeamSmall) {  // uniform: a beam of a few rows, ranked by counting
+        __shared__ uint64_t ks[kBeamSmall];
+        __shared__ int s_nv;
+        const int t = threadIdx.x;
+        uint64_t key = 0;
+        if (t < n && ids[t] >= 0) {
+            const float cu = canon(logprobs[t]) + (last ? last[t / k_t] : 0.0f);
+            key = sel_key(canon(cu), (uint32_t)t);
+        }
+        if (t < kBeamSmall) ks[t] = key;
+        if (t == 0) s_nv = 0;
+        __syncthreads();
+        if (t < kBeamSmall) {
+            const int nv = __popcll(__ballot(key != 0));
+            if (lane_id() == 0 && nv) atomicAdd(&s_nv, nv);
+        }
+        if (key != 0) {
+            // keys are distinct (they carry the candidate's index): the rank
+            // is the number of larger keys
+            int rank = 0;
+            for (int j = 0; j < n; ++j) rank += ks[j] > key;
+            if (rank < n_out) {
+                out_scores[rank] = key_val(key);
+                out_parent[rank] = t / k_t;
+                out_ids[rank] = ids[t];
+            }
+        }
+        __syncthreads();
+        for (int r = s_nv + t; r < n_out; r += kRowThreads) {
+            out_scores[r] = -__builtin_inff();
+            out_parent[r] = -1;
+            out_ids[r] = -1;
+        }
+        return;
+    }
     uint64_t kk[kBeamPer];
     int n_valid = 0;
 #pragma unroll

@@ -522,12 +522,13 @@ def test_union_rejects_small_cap_and_tail():
     assert e.value.status == D.ERR_UNSUPPORTED
 
 
-@pytest.mark.parametrize("B,k_t,n_out", [(1, 1, 1), (1, 8, 8), (6, 8, 8), (37, 13, 20), (130, 63, 64),
-                                         (128, 64, 64)])
+@pytest.mark.parametrize("B,k_t,n_out", [(1, 1, 1), (1, 8, 8), (6, 8, 8), (20, 12, 64), (16, 16, 16),
+                                         (257, 1, 5), (37, 13, 20), (130, 63, 64), (128, 64, 64)])
 def test_beam_expand(B, k_t, n_out):
     """EAGLE-2 expansion (Algorithm 1): the n_out best cumulative scores over the
     B x k_t candidates, ordered (score desc, row asc, rank asc); missing tokens
-    (id -1) are never chosen."""
+    (id -1) are never chosen.  Up to 256 candidates are ranked by counting,
+    more by the radix selection (both sides of the boundary are here)."""
     rng = np.random.default_rng(B * 1000 + k_t)
     lp = -rng.exponential(3.0, size=(B, k_t)).astype(np.float32)
     lp[:, ::3] = np.round(lp[:, ::3] * 4) / 4  # exact ties across rows
