@@ -697,8 +697,15 @@ dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const vo
     // union rows: one dense product of the union's slabs with every context
     // (it needs only one list entry per union cluster, and writes one shared
     // copy of the slots' vocabulary ids)
+    // A few rows over a short union take the per-chunk gathered kernel (one
+    // unit of every row per chunk, private rings per wave): measured at ten
+    // rows, 7 us faster per step than the dense union kernel at unions of
+    // 3.7-9.2k slots (row strides up to 39k) and 4 us slower at 32k.  A
+    // fixed union shape (DYNA_OPT_UNION_CFG) always takes the dense kernel.
+    constexpr int32_t kSmallUnionCap = 65536;
+    const bool small_union = option_union_cfg() == 0 && B <= 16 && cap <= kSmallUnionCap;
     const bool dense_union = union_mode && option_logits_path() == 0 && L->wdtype == DYNA_BF16 &&
-                             adtype == DYNA_BF16 && L->d % 8 == 0;
+                             adtype == DYNA_BF16 && L->d % 8 == 0 && !small_union;
     if (union_mode) {
         // per-row clusters, then one shared shortlist (its ids go to sel_sorted)
         TRY(launch_topk_clusters(c.scores, B, L->M, k, clusters, c.topk_scores, nullptr, nullptr, nullptr, nullptr,
