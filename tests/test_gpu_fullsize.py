@@ -35,15 +35,22 @@ def _host_rows(W_lm, vids):
     return W.host_array(W_lm.index_select(0, torch.from_numpy(np.asarray(vids)).to(DEV)))
 
 
+# later positions of one drafting cycle at the Llama-3-8B shapes: ten beam
+# rows over one union shortlist with a small cluster budget (the few-row
+# short-union path) and with the second position's budget
+EXTRA = {
+    "cycle_position3": W.scaled(W.WORKLOADS["llama3_8b_tree_union"], name="cycle_position3", B=10, k=5),
+    "cycle_position1": W.scaled(W.WORKLOADS["llama3_8b_tree_union"], name="cycle_position1", B=10, k=32),
+}
 CASES = [pytest.param(n, False, id=n) for n in W.WORKLOAD_ORDER] + [
     pytest.param(n, True, id=f"{n}-route_stream") for n in W.WORKLOAD_ORDER
-    if W.WORKLOADS[n].overlap_gemm is not None]
+    if W.WORKLOADS[n].overlap_gemm is not None] + [pytest.param(n, False, id=n) for n in EXTRA]
 
 
 @pytest.mark.parametrize("name,side_stream", CASES)
 def test_fullsize_workload(name, side_stream):
     from paper_2510_13847_amd import dynahead as D
-    w = W.WORKLOADS[name]
+    w = EXTRA[name] if name in EXTRA else W.WORKLOADS[name]
     print(f"[fullsize] {name}: V={w.V} d={w.d} M={w.M} B={w.B} k={w.k} side_stream={side_stream}",
           flush=True)
     cluster_of = W.partition(w)
