@@ -110,10 +110,8 @@ struct RowdotArgs {
     // next kernels of the step use)
     int32_t* zero_words;
     int32_t n_zero_words;
-    // dense mode, optional: at most this many workgroups (0: no cap), for
-    // routing on a second stream beside the caller's draft layer; the
-    // results do not depend on it
 };
+
 dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);
 
 // router.hip: dense layers for 1..128 contexts as split-K MFMA workgroups
