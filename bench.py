@@ -507,7 +507,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="llama3_8b_chain", choices=W.WORKLOAD_ORDER)
+    ap.add_argument("--workload", default="llama3_8b_chain", choices=W.WORKLOAD_ORDER + list(W.SHARD_WORKLOADS),
+                    help="a workload, or one GPU's share of a batch split by rows over eight GPUs (*_shard8)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-baselines", action="store_true", help="skip dense/static heads")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
@@ -547,7 +548,7 @@ def main():
     from paper_2510_13847_amd import dynahead as D
 
     D.lib()
-    w = W.WORKLOADS[args.workload]
+    w = W.WORKLOADS[args.workload] if args.workload in W.WORKLOADS else W.SHARD_WORKLOADS[args.workload]
     if args.kmeans:
         bench_kmeans(w, args, D, torch)
         return

@@ -41,6 +41,8 @@ def _host_rows(W_lm, vids):
 EXTRA = {
     "cycle_position3": W.scaled(W.WORKLOADS["llama3_8b_tree_union"], name="cycle_position3", B=10, k=5),
     "cycle_position1": W.scaled(W.WORKLOADS["llama3_8b_tree_union"], name="cycle_position1", B=10, k=32),
+    # one GPU's share of the large-vocabulary batch split by rows over eight GPUs
+    **W.SHARD_WORKLOADS,
 }
 CASES = [pytest.param(n, False, id=n) for n in W.WORKLOAD_ORDER] + [
     pytest.param(n, True, id=f"{n}-route_stream") for n in W.WORKLOAD_ORDER

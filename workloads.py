@@ -90,6 +90,19 @@ def scaled(w: Workload, **changes) -> Workload:
     return dataclasses.replace(w, **changes)
 
 
+# One GPU's share of a batch split by context rows over eight GPUs (the rows
+# are independent: no exchange between the GPUs).  The same partition, router
+# and LM head; B / 8 rows.
+SHARD_WORKLOADS = {
+    w.name: w
+    for w in [
+        scaled(WORKLOADS["llama3_8b_tree"], name="llama3_8b_tree_shard8", B=8),
+        scaled(WORKLOADS["gemma3_large_vocab"], name="gemma3_large_vocab_shard8", B=16, seed_index=4,
+               overlap_gemm=None),
+    ]
+}
+
+
 # --------------------------------------------------------------------------
 # seeds
 # --------------------------------------------------------------------------
