@@ -230,7 +230,7 @@ def dominant_kernel(w):
         return "logits_greedy_kernel", "gathered head fused with argmax selection (one context)"
     if w.union and w.dtype == "bf16":
         return "union_gemm_kernel", "union head: dense LDS-staged MFMA product of the union slabs with every context"
-    if w.dtype == "bf16" and w.B > 4:
+    if w.dtype == "bf16" and w.B > 32:
         return "gather_ring_kernel", "gathered head, MFMA tiles with the slab rows staged through LDS"
     return "rowdot_gemv_kernel", "gathered head, wave-per-row GEMV"
 

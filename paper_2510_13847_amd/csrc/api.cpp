@@ -333,6 +333,19 @@ static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtyp
     return run_layer(b, path, part, part_floats, s, defer);
 }
 
+// Path of a gathered head with per-row shortlists: the option when set, else
+// the wave-per-row GEMV for up to 32 contexts and the LDS-staged MFMA tiles
+// beyond.  The GEMV's 1 KiB row loads stream better when a slab row serves
+// few contexts: measured 4-12 us less per step at 8-48 contexts on the
+// Llama-3-8B head and 6-7 us at 16 contexts on the Qwen- and Gemma-shaped
+// heads; equal at 32 and 32 us more at 64 contexts on the Gemma-shaped head.
+constexpr int32_t kGemvMaxContexts = 32;
+static int gathered_path(int32_t B) {
+    const int opt = option_logits_path();
+    if (opt != 0) return opt;
+    return B <= kGemvMaxContexts ? 1 : 0;
+}
+
 static dyna_status run_logits(const dyna_layout* L, const void* h, int32_t hdtype, int32_t B, int32_t k,
                               const int32_t* sel_sorted, const int32_t* sel_rowoff, float* logits,
                               int32_t cap, const Plan& plan, hipStream_t s) {
@@ -351,7 +364,7 @@ static dyna_status run_logits(const dyna_layout* L, const void* h, int32_t hdtyp
     a.n_rows = 0;
     a.plan = plan;
     a.max_chunks_bound = chunk_bound(L, B, k);
-    return timed_rowdot(a, option_logits_path(), s);
+    return timed_rowdot(a, gathered_path(B), s);
 }
 
 static hipEvent_t lazy_event(hipEvent_t* table) {
@@ -745,7 +758,7 @@ dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const vo
     if (fused) return timed([&] { return launch_logits_greedy(a, sa, c.partials, c.counters, stream); }, stream);
     if (dense_union && !gather_lds_eligible(a)) return set_error(DYNA_ERR_UNSUPPORTED, "union: kernel arguments");
     if (dense_union) TRY(timed([&] { return launch_union_gemm(a, stream); }, stream));
-    else TRY(timed_rowdot(a, option_logits_path(), stream));
+    else TRY(timed_rowdot(a, union_mode ? option_logits_path() : gathered_path(B), stream));
     // union rows over a few thousand slots select faster in one launch (one
     // workgroup per row); long union rows split into segments.  Measured at
     // ten rows: 6-7 us saved per step at unions of 3.7-5.9k slots (row
