@@ -397,7 +397,11 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   layer 2; top-k with shortlist and plan; gathered head fused with
  *   selection).  1: the separate kernels.  3: the one launch only; a step it
  *   cannot run returns DYNA_ERR_UNSUPPORTED (for tests and measurement that
- *   must know which form ran).  All give bit-identical results.
+ *   must know which form ran).  A one-context top-k_t step without sampling
+ *   (1 < k_t <= 16) takes the gathered head fused with the selection under 0
+ *   and 2, and the separate kernels under 1 (3 rejects it).  All forms give
+ *   identical clusters, logits and ids; log-probabilities agree to rounding
+ *   (the softmax sum is taken in another order).
  *   Under kernel timing the one-launch step, or the fused gathered-head +
  *   selection launch, is what is timed.
  * DYNA_OPT_MFMA_UNROLL: k steps the direct-load MFMA kernel (router path 3,

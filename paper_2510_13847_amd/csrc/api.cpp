@@ -659,11 +659,12 @@ dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const vo
     const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     int32_t* clusters = out_clusters ? out_clusters : c.topk_ids;
     float* logits = out_logits ? out_logits : c.logits;
-    // one greedy context: the gathered head carries the selection (4 launches),
-    // or the whole step is one launch
+    // one context, argmax or top-k_t: the gathered head carries the selection
+    // (4 launches); greedy, the whole step can be one launch
     const int fused_opt = g_fused_off.load();
-    const bool fused = B == 1 && fused_opt != 1 && option_logits_path() <= 1 && k_t == 1 && !want_sample;
-    if (fused && (fused_opt == 0 || fused_opt == 3) && !split && option_router_path() <= 1) {
+    const bool fused = B == 1 && fused_opt != 1 && option_logits_path() <= 1 && k_t >= 1 &&
+                       k_t <= kFusedTopkMax && !want_sample;
+    if (fused && k_t == 1 && (fused_opt == 0 || fused_opt == 3) && !split && option_router_path() <= 1) {
         ChainRequest q{};
         q.all_bf16 = r->wdtype == DYNA_BF16 && L->wdtype == DYNA_BF16 && adtype == DYNA_BF16;
         q.W1 = r->W1;

@@ -270,9 +270,11 @@ SelectArgs make_select_args(const float* logits, int64_t ld, const int32_t* row_
 // True when the one-workgroup select handles rows of max_len slots.
 bool select_row_fits(int32_t max_len, bool fixed, int32_t k_t, int32_t k);
 
-// fused.hip (one context, greedy): gathered head + argmax selection with
-// per-workgroup online-softmax partials; `counter` is zero on entry.
+// fused.hip (one context, argmax or top-k_t up to kFusedTopkMax): gathered
+// head + selection with per-workgroup online-softmax partials; `counter` is
+// zero on entry.
 constexpr int kGreedyMaxBlocks = 4096;
+constexpr int kFusedTopkMax = 16;
 size_t greedy_partials_bytes();
 dyna_status launch_logits_greedy(const RowdotArgs& lg, const SelectArgs& sa, void* partials,
                                  int32_t* counter, hipStream_t s);

@@ -23,6 +23,7 @@ constexpr int kGreedyGrid = 256;  // default workgroups of the fused one-context
 struct GreedyEpi {
     float inv_t;
     GreedyState st;
+    __device__ __forceinline__ void idle() {}
     __device__ __forceinline__ void put(const RowdotArgs& a, int64_t o, float value, int32_t vid) {
         a.out[o] = value;
         if (a.vid_out) a.vid_out[o] = vid;
@@ -55,6 +56,221 @@ __global__ __launch_bounds__(kThreads) void logits_greedy_kernel(RowdotArgs lg, 
     }
 }
 
+// ---------------------------------------------------------------- top-k_t
+// The same fused head for TopK_{k_t} with k_t <= kTopkMax: every wave keeps
+// its kTopkMax best keys (spread over its lanes) next to the lanes' online
+// softmax pairs; a workgroup publishes its k_t best keys and its pair, and
+// the last workgroup to arrive takes the k_t best of all published keys.
+constexpr int kTopkMax = kFusedTopkMax;
+
+struct TopkPartial {
+    uint64_t key[kTopkMax];
+    float m, s;
+};
+
+// The key of each row goes into a list kept across the wave: lane l of
+// every 16-lane row holds the wave's l-th best key so far (descending, 0 =
+// empty).  A key x enters in one step, all lanes at once: place l takes
+// max(key_l, min(key_{l-1}, x)), key_{l-1} read from the lane below (row
+// shift; the row's first lane reads the all-ones identity).  Eight vector
+// instructions per key, and no per-lane list in registers.
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t row_list_insert(uint64_t mine, uint64_t x) {
+    const uint32_t plo = dpp<kRowShr1>(0xffffffffu, (uint32_t)mine);
+    const uint32_t phi = dpp<kRowShr1>(0xffffffffu, (uint32_t)(mine >> 32));
+    const uint64_t prev = ((uint64_t)phi << 32) | plo;
+    const uint64_t up = prev < x ? prev : x;
+    return mine > up ? mine : up;
+}
+
+// Epilogue of the one-context top-k head: lanes below R own the rows of a
+// group (one context: one row per lane per group); their keys are listed at
+// the next group's idle point, while its loads are in flight.
+template <int R>
+struct TopkEpi {
+    float inv_t;
+    uint64_t wk = 0;    // this lane's place of the wave's list
+    uint64_t pend = 0;  // key of the row this lane produced last (0: none)
+    float m = -__builtin_inff(), s = 0.0f;
+    __device__ __forceinline__ void idle() {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const uint64_t x = readlane_u64(pend, r);
+            if (x != 0) wk = row_list_insert(wk, x);
+        }
+        pend = 0;
+    }
+    __device__ __forceinline__ void put(const RowdotArgs& a, int64_t o, float value, int32_t vid) {
+        a.out[o] = value;
+        if (a.vid_out) a.vid_out[o] = vid;
+        const float z = value != value ? -__builtin_inff() : value;
+        pend = sel_key(z, (uint32_t)vid);
+        softmax_merge(m, s, z, 1.0f, inv_t);
+    }
+};
+
+// The workgroup's (m, s) over its lanes in a fixed order (thread 0 gets it).
+__device__ __forceinline__ void block_softmax_pair(float m, float s, float inv_t, float* w_m, float* w_s,
+                                                   float* out_m, float* out_s) {
+    constexpr int NW = kThreads / kWave;
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    const float wm = readlane_f32(wave_max_f32(m), kWave - 1);
+    const float ws = wave_sum(m == -__builtin_inff() ? 0.0f : s * expf((m - wm) * inv_t));
+    if (lane == 0) {
+        w_m[w] = wm;
+        w_s[w] = ws;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float bm = w_m[0], bs = w_s[0];
+        for (int q = 1; q < NW; ++q) softmax_merge(bm, bs, w_m[q], w_s[q], inv_t);
+        *out_m = bm;
+        *out_s = bs;
+    }
+}
+
+// The k_t (<= L) best keys held in sorted lists (descending, 0 = empty;
+// valid keys distinct and nonzero), one list per thread of NT.  The k_t-th
+// best list head T bounds the answer from below (k_t distinct heads are
+// >= T), so only entries >= T of lists whose head is >= T can be selected:
+// at most k_t lists of k_t entries, ranked by counting.  No chain of k_t
+// block-wide maxima.  out[0..k_t) gets the keys in descending order, 0 where
+// fewer exist; ends with a barrier.
+template <int L, int NT>
+__device__ void block_topk_lists(const uint64_t (&list)[L], int k_t, uint64_t* heads /* LDS [NT] */,
+                                 uint64_t* cand /* LDS [L * L] */, uint64_t* out /* LDS [k_t] */) {
+    __shared__ uint64_t sh_T;
+    __shared__ int sh_n;
+    const uint64_t head = list[0];
+    heads[threadIdx.x] = head;
+    if (threadIdx.x == 0) {
+        sh_T = 0;
+        sh_n = 0;
+    }
+    __syncthreads();
+    if (head != 0) {
+        int rank = 0;
+        for (int j = 0; j < NT; ++j) rank += heads[j] > head;
+        if (rank == k_t - 1) sh_T = head;
+    }
+    __syncthreads();
+    const uint64_t T = sh_T;
+    if (head != 0 && head >= T) {
+#pragma unroll
+        for (int r = 0; r < L; ++r)
+            if (r < k_t && list[r] != 0 && list[r] >= T) cand[atomicAdd(&sh_n, 1)] = list[r];
+    }
+    __syncthreads();
+    const int n = sh_n;
+    for (int c = threadIdx.x; c < n; c += NT) {
+        const uint64_t key = cand[c];
+        int rank = 0;
+        for (int j = 0; j < n; ++j) rank += cand[j] > key;
+        if (rank < k_t) out[rank] = key;
+    }
+    for (int r = n + threadIdx.x; r < k_t; r += NT) out[r] = 0;
+    __syncthreads();
+}
+
+template <typename WT, typename VT, int NB, int R>
+__global__ __launch_bounds__(kThreads) void logits_topk_kernel(RowdotArgs lg, SelectArgs sa, TopkPartial* part,
+                                                               int32_t* counter) {
+    constexpr int NW = kThreads / kWave;
+    __shared__ uint64_t heads[kThreads];
+    __shared__ uint64_t cand[kTopkMax * kTopkMax];
+    __shared__ uint64_t top[kTopkMax];
+    __shared__ float w_m[NW], w_s[NW], f_m, f_s;
+    __shared__ int last;
+    const int64_t n_items = (int64_t)lg.plan.hdr->n_chunks * (kChunkRows / R);
+    const int64_t n_part = std::max<int64_t>(
+        1, std::min<int64_t>(gridDim.x, (n_items + kWavesPerBlock - 1) / kWavesPerBlock));
+    if ((int64_t)blockIdx.x >= n_part) return;
+    const int k_t = sa.k_t;
+
+    TopkEpi<R> epi;
+    epi.inv_t = sa.inv_t;
+    gemv_rows<WT, VT, NB, true, R, true, TopkEpi<R>>(lg, epi);
+    epi.idle();
+
+    // the workgroup's k_t best keys (the k_t best of its waves' lists, ranked
+    // by counting) and softmax pair, published device-coherent
+    {
+        const int lane = lane_id(), w = threadIdx.x / kWave;
+        if ((int)threadIdx.x < k_t) top[threadIdx.x] = 0;
+        if (lane < k_t) cand[w * k_t + lane] = epi.wk;
+        __syncthreads();
+        if ((int)threadIdx.x < NW * k_t) {
+            const uint64_t key = cand[threadIdx.x];
+            int rank = 0;
+            for (int j = 0; j < NW * k_t; ++j) rank += cand[j] > key;
+            if (key != 0 && rank < k_t) top[rank] = key;
+        }
+        __syncthreads();
+    }
+    block_softmax_pair(epi.m, epi.s, sa.inv_t, w_m, w_s, &f_m, &f_s);
+    TopkPartial* mine = part + blockIdx.x;
+    if ((int)threadIdx.x < k_t) store_coherent(&mine->key[threadIdx.x], top[threadIdx.x]);
+    if (threadIdx.x == 0) {
+        store_coherent(&mine->m, f_m);
+        store_coherent(&mine->s, f_s);
+    }
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0)
+        last = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == n_part - 1;
+    __syncthreads();
+    if (!last) return;
+
+    // last workgroup: thread t merges the lists of partials t, t + NT, ... into
+    // its own sorted list, then the k_t best over the threads; the softmax
+    // pairs in partial order
+    if (threadIdx.x == 0) store_coherent(counter, 0);
+    uint64_t list[kTopkMax];
+#pragma unroll
+    for (int r = 0; r < kTopkMax; ++r) list[r] = 0;
+    float bm = -__builtin_inff(), bs = 0.0f;
+    for (int64_t g = threadIdx.x; g < n_part; g += kThreads) {
+        // all of the partial's loads in flight at once, then the merge
+        uint64_t pk[kTopkMax];
+#pragma unroll
+        for (int r = 0; r < kTopkMax; ++r) pk[r] = r < k_t ? load_coherent(&part[g].key[r]) : 0;
+        const float m2 = load_coherent(&part[g].m), s2 = load_coherent(&part[g].s);
+        if (g == threadIdx.x) {
+#pragma unroll
+            for (int r = 0; r < kTopkMax; ++r) list[r] = pk[r];
+        } else {
+            for (int r = 0; r < k_t; ++r) {
+                if (pk[r] <= list[kTopkMax - 1]) break;  // the partial's list is sorted
+                list[kTopkMax - 1] = pk[r];
+#pragma unroll
+                for (int q = kTopkMax - 1; q > 0; --q)
+                    if (list[q] > list[q - 1]) {
+                        const uint64_t t = list[q];
+                        list[q] = list[q - 1];
+                        list[q - 1] = t;
+                    }
+            }
+        }
+        softmax_merge(bm, bs, m2, s2, sa.inv_t);
+    }
+    block_topk_lists<kTopkMax, kThreads>(list, k_t, heads, cand, top);
+    block_softmax_pair(bm, bs, sa.inv_t, w_m, w_s, &f_m, &f_s);
+    __syncthreads();
+    const TailMix tail = tail_of(sa, sa.row_len ? sa.row_len[0] : sa.fixed_len);
+    const float log_total = logf(f_s) - tail.lshift;
+    for (int r = threadIdx.x; r < k_t; r += kThreads) {
+        const uint64_t key = top[r];
+        if (sa.out_ids) sa.out_ids[r] = key != 0 ? (int32_t)key_id(key) : -1;
+        if (sa.out_logprobs)
+            sa.out_logprobs[r] = key != 0 ? (key_val(key) - f_m) * sa.inv_t - log_total : -__builtin_inff();
+    }
+}
+
 template <typename WT, typename VT, int NB, int R>
 dyna_status launch_lg_r(const RowdotArgs& lg, const SelectArgs& sa, void* part, int32_t* counter,
                         hipStream_t s) {
@@ -62,6 +278,11 @@ dyna_status launch_lg_r(const RowdotArgs& lg, const SelectArgs& sa, void* part, 
     const int cap = option_greedy_grid() > 0 ? std::min(option_greedy_grid(), kGreedyMaxBlocks) : kGreedyGrid;
     const unsigned grid = (unsigned)std::max<int64_t>(
         1, std::min<int64_t>((items + kWavesPerBlock - 1) / kWavesPerBlock, cap));
+    if (sa.k_t > 1) {
+        launch_timed_kernel(logits_topk_kernel<WT, VT, NB, R>, dim3(grid), dim3(kThreads), 0, s, lg, sa,
+                            static_cast<TopkPartial*>(part), counter);
+        return check_launch("logits_topk_kernel");
+    }
     launch_timed_kernel(logits_greedy_kernel<WT, VT, NB, R>, dim3(grid), dim3(kThreads), 0, s, lg, sa,
                         static_cast<GreedyPartial*>(part), counter);
     return check_launch("logits_greedy_kernel");
@@ -79,13 +300,16 @@ dyna_status launch_lg(const RowdotArgs& lg, const SelectArgs& sa, void* part, in
 
 }  // namespace
 
-size_t greedy_partials_bytes() { return sizeof(GreedyPartial) * (size_t)kGreedyMaxBlocks; }
+size_t greedy_partials_bytes() {
+    return std::max(sizeof(GreedyPartial), sizeof(TopkPartial)) * (size_t)kGreedyMaxBlocks;
+}
 
 dyna_status launch_logits_greedy(const RowdotArgs& lg, const SelectArgs& sa, void* partials,
                                  int32_t* counter, hipStream_t s) {
     const int nb = (lg.K + 511) / 512;
     const int rows = option_gemv_rows();
-    if (lg.B != 1 || sa.k_t != 1) return set_error(DYNA_ERR_UNSUPPORTED, "fused head: one context, argmax");
+    if (lg.B != 1 || sa.k_t < 1 || sa.k_t > kTopkMax)
+        return set_error(DYNA_ERR_UNSUPPORTED, "fused head: one context, k_t <= %d", kTopkMax);
 #define DYNA_LG(N)                                                                                         \
     if (nb <= N) {                                                                                         \
         if (lg.wdtype == DYNA_BF16)                                                                        \

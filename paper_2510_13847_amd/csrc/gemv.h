@@ -75,8 +75,10 @@ __device__ __forceinline__ float dot8(const Raw8<WT>& w, const Raw8<VT>& x, floa
 // One wave computes R consecutive rows per iteration.  With SINGLE (one
 // context: B = 1) the context row is loaded into registers once per wave.
 // Default epilogue: store the value (and, in plan mode, the slot's vocabulary id).
+// An epilogue's idle() runs while a row group's loads are in flight.
 template <bool PLAN>
 struct StoreEpi {
+    __device__ __forceinline__ void idle() {}
     __device__ __forceinline__ void put(const RowdotArgs& a, int64_t o, float value, int32_t vid) {
         a.out[o] = value;
         if constexpr (PLAN) {
@@ -154,6 +156,7 @@ __device__ __forceinline__ void gemv_rows(const RowdotArgs& a, Epi& epi) {
         if constexpr (PLAN) {
             if (a.perm && own) vid = a.perm[row0 + lane];
         }
+        epi.idle();
 
         for (int i = 0; i < lcnt; ++i) {
             int b, base;

@@ -386,7 +386,8 @@ def test_tail_mixture(name, beta):
     p = Problem(w)
     u = torch.linspace(0.0, 0.999, w.B, dtype=torch.float32) if w.B > 1 else torch.tensor([0.9])
     ud = u.to(DEV)
-    modes = [D.SEL_TOPK | D.SEL_SAMPLE] + ([D.SEL_ARGMAX] if w.B == 1 else [])  # argmax alone: fused path
+    # one context without sampling: the fused head (argmax and top-k)
+    modes = [D.SEL_TOPK | D.SEL_SAMPLE] + ([D.SEL_ARGMAX, D.SEL_TOPK] if w.B == 1 else [])
     for mode in modes:
         kt = w.k_t if mode & D.SEL_TOPK else 1
         base = D.draft_head(p.R, p.L, p.hd, p.hd, w.k, mode=mode, k_t=kt, uniforms=ud)
@@ -759,6 +760,79 @@ def test_fused_greedy_matches_separate_kernels(w, temperature, fused_opt):
         r = O.draft_select(z, vids, 1, temperature)
         assert int(fused.ids[0, 0]) == int(r["ids"][0])
         PC.assert_close(fused.logprobs[0].cpu().numpy(), r["logprobs"], PC.LOGPROB_TOL, "lp oracle")
+
+
+TOPK_FUSED_CASES = [c for c in FUSED_CASES if c.name in
+                    ("ragged_b1", "fused_big", "fused_f32", "chain_wide", "chain_d8192", "chain_m1024")] + [
+    # a shortlist shorter than k_t = 16: the missing places are -1 / -inf
+    case("short_list", V=60, d=64, M=20, H=16, k=1, B=1),
+]
+
+
+@pytest.mark.parametrize("temperature", [1.0, 0.6])
+@pytest.mark.parametrize("k_t", [2, 7, 16])
+@pytest.mark.parametrize("w", TOPK_FUSED_CASES, ids=lambda w: w.name)
+def test_fused_topk_matches_separate_kernels(w, k_t, temperature):
+    """TopK_{k_t} of one context (k_t up to 16) folds the selection into the
+    gathered head: the ids must equal the separate kernels' exactly, in rank
+    order, and the log-probabilities within rounding, call after call (the
+    arrival counter resets itself); and both against the oracle's selection
+    on the GPU's own logits."""
+    p = Problem(w)
+    mode = D.SEL_TOPK
+    fused = D.DraftHead(p.R, p.L, 1, w.k, mode, k_t, temperature, keep_logits=True)
+    sep = D.DraftHead(p.R, p.L, 1, w.k, mode, k_t, temperature, keep_logits=True)
+    for it in range(4):
+        x = W.contexts(w, "cpu", salt=it).to(DEV)
+        D.set_option(D.OPT_FUSED_B1, 0)
+        try:
+            fused(x, x)
+            D.set_option(D.OPT_FUSED_B1, 1)
+            sep(x, x)
+        finally:
+            D.set_option(D.OPT_FUSED_B1, 0)
+        torch.cuda.synchronize()
+        assert torch.equal(fused.clusters, sep.clusters)
+        vids = O.shortlist(fused.clusters[0].cpu().numpy(), p.offsets, p.perm)[3]
+        n = len(vids)
+        assert torch.equal(fused.logits[:, :n], sep.logits[:, :n])
+        assert torch.equal(fused.ids, sep.ids)
+        lf, ls = fused.logprobs.cpu().numpy(), sep.logprobs.cpu().numpy()
+        assert np.array_equal(np.isfinite(lf), np.isfinite(ls))
+        fin = np.isfinite(ls)
+        PC.assert_close(lf[fin], ls[fin], (2e-6, 2e-6), "lp")
+        z = fused.logits[0, :n].cpu().numpy().astype(np.float64)
+        r = O.draft_select(z, vids, k_t, temperature)
+        got = fused.ids[0].cpu().numpy()
+        m = min(k_t, n)
+        assert got[:m].tolist() == [int(v) for v in r["ids"][:m]]
+        assert (got[m:] == -1).all() and np.isneginf(lf[0, m:]).all()
+        PC.assert_close(lf[0, :m], np.asarray(r["logprobs"][:m]), PC.LOGPROB_TOL, "lp oracle")
+
+
+def test_fused_topk_ties_take_lower_ids():
+    """A zero drafter state makes every shortlist logit 0: the fused top-k
+    must then take the k_t lowest vocabulary ids of the shortlist, each with
+    log-probability -log |V_S|, as the separate kernels do."""
+    w = next(c for c in FUSED_CASES if c.name == "fused_big")
+    p = Problem(w)
+    k_t = 16
+    fused = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_TOPK, k_t, keep_logits=True)
+    sep = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_TOPK, k_t, keep_logits=True)
+    x = W.contexts(w, "cpu", salt=3).to(DEV)
+    h = torch.zeros_like(x)
+    D.set_option(D.OPT_FUSED_B1, 0)
+    try:
+        fused(x, h)
+        D.set_option(D.OPT_FUSED_B1, 1)
+        sep(x, h)
+    finally:
+        D.set_option(D.OPT_FUSED_B1, 0)
+    torch.cuda.synchronize()
+    vids = O.shortlist(fused.clusters[0].cpu().numpy(), p.offsets, p.perm)[3]
+    assert fused.ids[0].cpu().tolist() == sorted(int(v) for v in vids)[:k_t]
+    assert torch.equal(fused.ids, sep.ids)
+    np.testing.assert_allclose(fused.logprobs[0].cpu().numpy(), -np.log(len(vids)), rtol=0, atol=2e-6)
 
 
 @pytest.mark.parametrize("variant", ["tied_rows", "zero_router"])
