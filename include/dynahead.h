@@ -417,7 +417,7 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   occupancy calculator says can be resident at once.
  * DYNA_OPT_UNION_CFG: shape of the dense union-row kernel of
  *   DYNA_SEL_UNION steps: 0 automatic (up to 16 rows over a row stride of at
- *   most 65536 slots take the per-chunk gathered kernel instead), 1..14
+ *   most 65536 slots take the per-chunk gathered kernel instead), 1..15
  *   fixed (waves per workgroup, row tiles per wave, k columns per stage, ring
  *   depth; always the dense kernel); a shape whose ring does not fit in LDS
  *   for the batch's context count returns DYNA_ERR_UNSUPPORTED.

@@ -422,7 +422,7 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         return DYNA_OK;
     }
     if (option == DYNA_OPT_UNION_CFG) {
-        REQUIRE(value >= 0 && value <= 14, "union shape %d outside [0, 14]", value);
+        REQUIRE(value >= 0 && value <= 15, "union shape %d outside [0, 15]", value);
         g_union_cfg.store(value);
         return DYNA_OK;
     }

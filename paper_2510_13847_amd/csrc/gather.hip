@@ -711,14 +711,18 @@ dyna_status launch_union_nt(const RowdotArgs& a, int cfg, hipStream_t stream) {
         case 12: return launch_union_cfg<4, 1, 64, NT, 3>(a, stream);
         case 13: return launch_union_cfg<4, 2, 64, NT, 3>(a, stream);
         case 14: return launch_union_cfg<2, 2, 64, NT, 3>(a, stream);
+        case 15: return launch_union_cfg<2, 1, 64, NT, 3>(a, stream);
         default:  // measured best per context count (eight waves where the context loads split)
             if constexpr (NT >= 8) return launch_union_cfg<8, 2, 64, NT>(a, stream);
             else if constexpr (NT == 4) return launch_union_cfg<8, 1, 64, NT, 3>(a, stream);
             else if constexpr (NT == 2) return launch_union_cfg<4, 1, 64, NT, 3>(a, stream);
-            // up to 16 contexts: two-wave workgroups (more workgroups for
-            // short unions: 27 us less per drafting cycle at ten rows; the
-            // 16-context dense head 233 -> 201 us)
-            else return launch_union_cfg<2, 1, 128, NT, 3>(a, stream);
+            // up to 16 contexts: two-wave workgroups of 64-column stages
+            // (many small workgroups per CU).  Measured at ten rows over a
+            // union of 31.6k slots: 52.2 us against 60.3 with 128-column
+            // stages and 54-81 us for deeper rings or more rows per wave;
+            // the 16-context dense head 186 us (128 columns: 188; four-wave
+            // workgroups: 233)
+            else return launch_union_cfg<2, 1, 64, NT, 3>(a, stream);
     }
 }
 

@@ -54,7 +54,7 @@ def test_set_option_validation():
     assert lib.dyna_set_option(D.OPT_GATHER_CFG, 5) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 3) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_GATHER_CFG, 0) == D.OK
-    assert lib.dyna_set_option(D.OPT_UNION_CFG, 15) == D.ERR_INVALID_ARG
+    assert lib.dyna_set_option(D.OPT_UNION_CFG, 16) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_UNION_CFG, 0) == D.OK
     assert lib.dyna_set_option(D.OPT_KMEANS_CFG, 8) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_KMEANS_CFG, 0) == D.OK

@@ -423,7 +423,7 @@ def test_tail_mixture(name, beta):
         assert strict <= PC.strict_limit(w.B)
 
 
-UNION_VARIANTS = {**{f"dense{c}": (0, c) for c in range(15)}, "gemv": (1, 0), "lds": (2, 0)}
+UNION_VARIANTS = {**{f"dense{c}": (0, c) for c in range(16)}, "gemv": (1, 0), "lds": (2, 0)}
 # a union longer than 16384 slots: the segmented selection
 UNION_EXTRA = {"long_b8": case("long_b8", V=40000, d=64, M=48, H=16, k=12, B=8)}
 
