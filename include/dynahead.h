@@ -410,7 +410,9 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   automatic (slab rows staged through LDS, contexts loaded into
  *   registers, two workgroups of two waves per compute unit); 1..4 other
  *   shapes of the same kernel (waves per workgroup, ring stages, k columns
- *   per stage).
+ *   per stage); 5..9 shapes whose waves split the k dimension of one chunk
+ *   (for short shortlists; a shape whose split would leave a wave without
+ *   k columns runs unsplit).
  * DYNA_OPT_GREEDY_GRID: workgroups of the fused one-context gathered head:
  *   0 automatic (256), else 1..4096; of the one-launch step: 0 automatic (one
  *   per compute unit), else that many, capped at 1024 and at what the

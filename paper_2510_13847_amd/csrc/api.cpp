@@ -427,7 +427,7 @@ DYNA_API dyna_status dyna_set_option(int32_t option, int32_t value) {
         return DYNA_OK;
     }
     if (option == DYNA_OPT_GATHER_CFG) {
-        REQUIRE(value >= 0 && value <= 4, "gather shape %d outside [0, 4]", value);
+        REQUIRE(value >= 0 && value <= 9, "gather shape %d outside [0, 9]", value);
         g_gather_cfg.store(value);
         return DYNA_OK;
     }

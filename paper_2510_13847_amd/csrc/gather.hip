@@ -68,8 +68,9 @@ struct Unit {
 
 static_assert(kChunkRows == kMfmaRows, "a plan chunk is one MFMA tile");
 
-// Move u to the first chunk at or after u.it (stride `stride`) with rows and contexts.
-__device__ __forceinline__ void find_tile(Unit& u, const Plan& plan, int64_t n_items, int64_t stride) {
+// Move u to the first chunk at or after u.it (stride `stride`) with rows and
+// contexts; its first stage is k block kb0.
+__device__ __forceinline__ void find_tile(Unit& u, const Plan& plan, int64_t n_items, int64_t stride, int kb0) {
     sptr<int32_t> ch = (sptr<int32_t>)plan.chunks;
     while (u.it < n_items) {
         const int64_t c = u.it;
@@ -80,7 +81,7 @@ __device__ __forceinline__ void find_tile(Unit& u, const Plan& plan, int64_t n_i
             u.list_off = lo;
             u.lcnt = lc;
             u.g = 0;
-            u.kb = 0;
+            u.kb = kb0;
             u.valid = true;
             return;
         }
@@ -89,14 +90,16 @@ __device__ __forceinline__ void find_tile(Unit& u, const Plan& plan, int64_t n_i
     u.valid = false;
 }
 
-// Next stage of a unit: next k block, else next context group, else next tile.
+// Next stage of a unit: next k block of [kb0, kb1), else next context group,
+// else next tile.
 template <int NC>
-__device__ __forceinline__ bool advance(Unit& u, int nkb, const Plan& plan, int64_t n_items, int64_t stride) {
-    if (++u.kb < nkb) return false;
-    u.kb = 0;
+__device__ __forceinline__ bool advance(Unit& u, int kb0, int kb1, const Plan& plan, int64_t n_items,
+                                        int64_t stride) {
+    if (++u.kb < kb1) return false;
+    u.kb = kb0;
     if (++u.g * NC < u.lcnt) return true;  // same tile, next group
     u.it += stride;
-    find_tile(u, plan, n_items, stride);
+    find_tile(u, plan, n_items, stride, kb0);
     return true;
 }
 
@@ -140,7 +143,13 @@ __device__ __forceinline__ int group_entries(const Unit& u, const Plan& plan, in
 // whose column has no context read context 0 and are zeroed when used), so
 // the wave can wait for a stage with one counter value; the loop is unrolled
 // by the ring depth so that a stage's B registers have fixed names.
-template <int NW, int S, int KB>
+//
+// KS = NW splits the k dimension instead: all waves of a workgroup take the
+// same chunk, wave w its w-th share of the k blocks, and the partial tiles
+// are added through LDS in wave order at the end of each context group.  For
+// a short shortlist (a few hundred chunks) that puts NW times more waves on
+// the slab bytes.
+template <int NW, int S, int KB, int KS = 1>
 __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
     constexpr int NC = 16;
     constexpr int ROWB = KB * 2;
@@ -152,6 +161,7 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
     constexpr int PER_STAGE = NA + STEPS;  // vector-memory instructions per stage
     static_assert(PIECES <= kWave && kWave % PIECES == 0 && kMfmaRows % RPI == 0, "stage shape");
     static_assert((S - 1) * PER_STAGE <= 63, "ring depth beyond the load counter");
+    static_assert(KS == 1 || KS == NW, "k split: every wave of the workgroup on one chunk");
 
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int lane = lane_id();
@@ -162,14 +172,18 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
     const uint16_t* __restrict__ W = static_cast<const uint16_t*>(a.W);
     const uint16_t* __restrict__ v = static_cast<const uint16_t*>(a.v);
     const int64_t n_items = (int64_t)((sptr<int32_t>)a.plan.hdr)[0];
-    const int64_t stride = (int64_t)gridDim.x * NW;
+    const int64_t stride = (int64_t)gridDim.x * (NW / KS);
+    // this wave's k blocks (all of them without a split; the host makes sure
+    // that every wave of a split gets at least one)
+    const int kb0 = KS == 1 ? 0 : wv * nkb / KS;
+    const int kb1 = KS == 1 ? nkb : (wv + 1) * nkb / KS;
 
     const int lsub = lane / PIECES, lpc = lane % PIECES;
     const int col = lane & 15, kq = lane >> 4;
 
     Unit iu;
-    iu.it = (int64_t)blockIdx.x * NW + wv;
-    find_tile(iu, a.plan, n_items, stride);
+    iu.it = (int64_t)blockIdx.x * (NW / KS) + (KS == 1 ? wv : 0);
+    find_tile(iu, a.plan, n_items, stride, kb0);
     if (!iu.valid) return;
     Unit cu = iu;
 
@@ -257,7 +271,7 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
     // next stage of the issue side: the context group (and, on a new chunk,
     // the rows) follow the cursor
     auto advance_issue = [&]() {
-        if (advance<NC>(iu, nkb, a.plan, n_items, stride) && iu.valid) {
+        if (advance<NC>(iu, kb0, kb1, a.plan, n_items, stride) && iu.valid) {
             issue_group();
             if (iu.g == 0) set_rows();
         }
@@ -309,13 +323,33 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
                     acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
                                                                    __builtin_bit_cast(bf16x8, bv), acc0, 0, 0, 0);
             }
-            if (cu.kb == nkb - 1) {
-                if (col < ncols) {
+            if (cu.kb == kb1 - 1) {
+                f32x4 tile;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) tile[r] = acc0[r] + acc1[r];
+                bool store = true;
+                if constexpr (KS > 1) {
+                    // the waves' shares of the tile, added in wave order by wave 0
+                    __shared__ f32x4 part[KS][kWave];
+                    part[wv][lane] = tile;
+                    __syncthreads();
+                    store = wv == 0;
+                    if (store) {
+#pragma unroll
+                        for (int q = 1; q < KS; ++q) {
+                            const f32x4 o = part[q][lane];
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) tile[r] += o[r];
+                        }
+                    }
+                    __syncthreads();
+                }
+                if (store && col < ncols) {
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int row = 4 * kq + r;
                         if (row < cu.nrows) {
-                            a.out[obase + row] = acc0[r] + acc1[r];
+                            a.out[obase + row] = tile[r];
                             if (a.vid_out != nullptr) a.vid_out[obase + row] = vid[r];
                         }
                     }
@@ -323,7 +357,7 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
                 acc0 = f32x4{0.f, 0.f, 0.f, 0.f};
                 acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
             }
-            if (advance<NC>(cu, nkb, a.plan, n_items, stride)) {
+            if (advance<NC>(cu, kb0, kb1, a.plan, n_items, stride)) {
                 if (!cu.valid) {
                     done = true;
                     break;
@@ -334,23 +368,27 @@ __global__ __launch_bounds__(NW * kWave) void gather_ring_kernel(RowdotArgs a) {
     }
 }
 
-template <int NW, int S, int KB>
+template <int NW, int S, int KB, int KS = 1>
 dyna_status launch_ring_cfg(const RowdotArgs& a, hipStream_t stream) {
     constexpr int LDS = NW * S * kMfmaRows * KB * 2;
+    // a split needs at least one k block per wave
+    if (KS > 1 && (a.K + KB - 1) / KB < KS) return launch_ring_cfg<NW, S, KB, 1>(a, stream);
     static_assert(LDS <= 160 * 1024, "LDS per block");
     static std::atomic<uint64_t> allowed{0};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "gather: device");
     if (!(allowed.load() & (1ull << dev))) {
-        if (hipFuncSetAttribute((const void*)gather_ring_kernel<NW, S, KB>,
+        if (hipFuncSetAttribute((const void*)gather_ring_kernel<NW, S, KB, KS>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, LDS) != hipSuccess)
             return set_error(DYNA_ERR_HIP, "gather: LDS attribute");
         allowed.fetch_or(1ull << dev);
     }
     const int per_cu = (160 * 1024) / LDS;
     const int64_t items = (int64_t)a.max_chunks_bound;
-    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + NW - 1) / NW, 256 * per_cu));
-    launch_timed_kernel(gather_ring_kernel<NW, S, KB>, dim3((unsigned)blocks), dim3(NW * kWave), LDS, stream, a);
+    constexpr int kItemsPerBlock = NW / KS;
+    const int64_t blocks =
+        std::max<int64_t>(1, std::min<int64_t>((items + kItemsPerBlock - 1) / kItemsPerBlock, 256 * per_cu));
+    launch_timed_kernel(gather_ring_kernel<NW, S, KB, KS>, dim3((unsigned)blocks), dim3(NW * kWave), LDS, stream, a);
     return check_launch("gather_ring_kernel");
 }
 
@@ -733,6 +771,8 @@ bool gather_lds_eligible(const RowdotArgs& a) {
            a.bias == nullptr && a.act == DYNA_ACT_NONE && (a.vid_out == nullptr || a.perm != nullptr);
 }
 
+constexpr int32_t kSplitChunks = 4096;
+
 dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
     if (!gather_lds_eligible(a)) return set_error(DYNA_ERR_UNSUPPORTED, "gather: needs bf16 plan mode");
     switch (option_gather_cfg()) {
@@ -740,7 +780,19 @@ dyna_status launch_gather_lds(const RowdotArgs& a, hipStream_t stream) {
         case 2: return launch_ring_cfg<4, 4, 256>(a, stream);
         case 3: return launch_ring_cfg<4, 8, 128>(a, stream);
         case 4: return launch_ring_cfg<8, 8, 64>(a, stream);
-        default: return launch_ring_cfg<2, 4, 256>(a, stream);  // two workgroups of two waves per CU
+        case 5: return launch_ring_cfg<2, 4, 256, 2>(a, stream);
+        case 6: return launch_ring_cfg<4, 4, 256, 4>(a, stream);
+        case 7: return launch_ring_cfg<4, 4, 128, 4>(a, stream);
+        case 8: return launch_ring_cfg<4, 3, 256, 4>(a, stream);
+        case 9: return launch_ring_cfg<8, 4, 128, 8>(a, stream);
+        default:
+            // a short shortlist (at most a few thousand chunks, as in the
+            // union steps of a few rows): four waves split each chunk's k
+            // dimension.  Measured at ten rows: 19.0 -> 17.2 us over a union
+            // of 5.9k rows, 26.0 -> 23.4 us over 9.2k rows; the other split
+            // shapes gained less or lost.
+            if (a.max_chunks_bound <= kSplitChunks) return launch_ring_cfg<4, 4, 128, 4>(a, stream);
+            return launch_ring_cfg<2, 4, 256>(a, stream);  // two workgroups of two waves per CU
     }
 }
 

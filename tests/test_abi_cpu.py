@@ -51,7 +51,7 @@ def test_set_option_validation():
     assert b"unknown option" in lib.dyna_last_error()
     assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 7) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 0) == D.OK
-    assert lib.dyna_set_option(D.OPT_GATHER_CFG, 5) == D.ERR_INVALID_ARG
+    assert lib.dyna_set_option(D.OPT_GATHER_CFG, 10) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_LOGITS_PATH, 3) == D.ERR_INVALID_ARG
     assert lib.dyna_set_option(D.OPT_GATHER_CFG, 0) == D.OK
     assert lib.dyna_set_option(D.OPT_UNION_CFG, 16) == D.ERR_INVALID_ARG

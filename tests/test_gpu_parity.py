@@ -233,11 +233,16 @@ def test_logits_parity(w, path):
         assert np.all(np.isnan(lg[b, n:])), "slots past row_len must stay untouched"
 
 
-@pytest.mark.parametrize("cfg", list(range(0, 5)))
-@pytest.mark.parametrize("name", ["ragged_b37", "zipf_b9", "many_b130"])
+# d = 1000: four to eight k blocks for the split shapes, the last one a tail
+GATHER_EXTRA = {"kdeep_b6": case("kdeep_b6", V=3001, d=1000, M=37, H=24, k=5, B=6)}
+
+
+@pytest.mark.parametrize("cfg", list(range(0, 10)))
+@pytest.mark.parametrize("name", ["ragged_b37", "zipf_b9", "many_b130", "kdeep_b6"])
 def test_logits_gather_shapes(name, cfg):
-    """Every workgroup shape of the LDS-staged MFMA gathered head."""
-    w = next(c for c in CASES if c.name == name)
+    """Every workgroup shape of the LDS-staged MFMA gathered head, with and
+    without the waves splitting the k dimension of a chunk."""
+    w = GATHER_EXTRA[name] if name in GATHER_EXTRA else next(c for c in CASES if c.name == name)
     p = Problem(w)
     topk = _random_selection(p, w.B, w.k, 5)
     sel, rowoff, row_len, sl = D.shortlist(p.L, torch.from_numpy(topk).to(DEV))
