@@ -145,6 +145,24 @@ static int64_t max_chunks_for(const dyna_layout* L) {
 // Chunks a step can produce: the union of the selected slabs holds at most
 // min(V, B * cap_by_k[k]) rows in at most min(M, B * k) clusters, and each
 // cluster adds at most one partial chunk.
+// 5..16 contexts: router layer 2 stages the hidden layer straight from layer
+// 1's split-K partial sums, so layer 1 needs no reduction launch (both
+// layers' partial sums then share the workspace side by side).
+constexpr int32_t kHiddenFromPartsMaxB = 16;
+// (The workspace is sized for it whatever the router-path option says.)
+static bool hidden_from_parts(const dyna_router* r, int32_t xdtype, int32_t B, size_t* f1, size_t* f2,
+                              bool sizing = false) {
+    if (r->H == 0 || B <= 4 || B > kHiddenFromPartsMaxB || r->wdtype != DYNA_BF16 ||
+        (!sizing && option_router_path() != 0))
+        return false;
+    SplitShape s1, s2;
+    if (!splitk_shape(r->H, r->d_r, B, xdtype == DYNA_F32, &s1) || !splitk_shape(r->M, r->H, B, true, &s2))
+        return false;
+    *f1 = (size_t)s1.slices * (size_t)B * (size_t)r->H;
+    *f2 = (size_t)s2.slices * (size_t)B * (size_t)r->M;
+    return true;
+}
+
 static int32_t chunk_bound(const dyna_layout* L, int32_t B, int32_t k) {
     const int64_t rows = std::min<int64_t>(L->V, (int64_t)B * L->cap_by_k[k]);
     const int64_t clusters = std::min<int64_t>(L->M, (int64_t)B * k);
@@ -169,6 +187,10 @@ static Carve carve(const dyna_layout* L, const dyna_router* r, int32_t B, int32_
         const int32_t n1 = r->H > 0 ? r->H : r->M;
         size_t f = std::max(splitk_part_floats(n1, r->d_r, B, false), splitk_part_floats(n1, r->d_r, B, true));
         if (r->H > 0) f = std::max(f, splitk_part_floats(r->M, r->H, B, true));
+        // both layers' partial sums at once (either input type of layer 1)
+        size_t f1 = 0, f2 = 0, g1 = 0, g2 = 0;
+        if (hidden_from_parts(r, DYNA_BF16, B, &f1, &f2, true)) f = std::max(f, f1 + f2);
+        if (hidden_from_parts(r, DYNA_F32, B, &g1, &g2, true)) f = std::max(f, g1 + g2);
         c.rpart_floats = f;
         if (f > 0) c.rpart = static_cast<float*>(take(sizeof(float) * f));
     }
@@ -317,6 +339,42 @@ static dyna_status run_router(const dyna_router* r, const void* x, int32_t xdtyp
     a.bias = r->b1;
     a.act = r->act;
     a.n_rows = r->H;
+    size_t f1 = 0, f2 = 0;
+    if (part != nullptr && hidden_from_parts(r, xdtype, B, &f1, &f2) && f1 + f2 <= part_floats) {
+        // layer 1's slices stay in part[0, f1); layer 2 adds them up (in slice
+        // order, then bias and activation) while staging its contexts
+        RowdotArgs a1 = a;
+        a1.act = DYNA_ACT_NONE;
+        a1.bias = nullptr;
+        int slices1 = 0;
+        TRY(launch_dense_splitk(a1, part, f1, s, &slices1));
+        RowdotArgs b{};
+        b.W = r->W2;
+        b.wdtype = r->wdtype;
+        b.K = r->H;
+        b.v = hidden;  // unused: the contexts come from the partial sums
+        b.vdtype = DYNA_F32;
+        b.vpart = part;
+        b.vslices = slices1;
+        b.vbias = r->b1;
+        b.vact = r->act;
+        b.B = B;
+        b.out = scores;
+        b.ld = r->M;
+        b.bias = r->b2;
+        b.act = DYNA_ACT_NONE;
+        b.n_rows = r->M;
+        float* part2 = part + f1;
+        if (defer != nullptr) {
+            int slices2 = 0;
+            TRY(launch_dense_splitk(b, part2, part_floats - f1, s, &slices2));
+            defer->part = part2;
+            defer->slices = slices2;
+            defer->bias = b.bias;
+            return DYNA_OK;
+        }
+        return launch_dense_splitk(b, part2, part_floats - f1, s);
+    }
     TRY(run_layer(a, path, part, part_floats, s));
     RowdotArgs b{};
     b.W = r->W2;

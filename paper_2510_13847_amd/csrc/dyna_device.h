@@ -26,16 +26,8 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
 
 // Eight consecutive elements of a row as fp32, from bf16 (one 16-byte load)
 // or fp32 (two 16-byte loads).  `nt` streams the load past the caches.
-// 8 consecutive fp32 values split into bf16 hi and lo terms.
-__device__ __forceinline__ void split8(const float* p, u32x4& hi, u32x4& lo) {
-    const u32x4* q = reinterpret_cast<const u32x4*>(p);
-    const u32x4 x0 = q[0], x1 = q[1];
-    float f[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        f[i] = __uint_as_float(x0[i]);
-        f[4 + i] = __uint_as_float(x1[i]);
-    }
+// 8 fp32 values split into bf16 hi and lo terms.
+__device__ __forceinline__ void split8_regs(const float (&f)[8], u32x4& hi, u32x4& lo) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const uint32_t h0 = f32_to_bf16_bits(f[2 * i]);
@@ -45,6 +37,18 @@ __device__ __forceinline__ void split8(const float* p, u32x4& hi, u32x4& lo) {
         hi[i] = h0 | (h1 << 16);
         lo[i] = l0 | (l1 << 16);
     }
+}
+// 8 consecutive fp32 values in memory split into bf16 hi and lo terms.
+__device__ __forceinline__ void split8(const float* p, u32x4& hi, u32x4& lo) {
+    const u32x4* q = reinterpret_cast<const u32x4*>(p);
+    const u32x4 x0 = q[0], x1 = q[1];
+    float f[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[i] = __uint_as_float(x0[i]);
+        f[4 + i] = __uint_as_float(x1[i]);
+    }
+    split8_regs(f, hi, lo);
 }
 
 template <typename T, bool NT>

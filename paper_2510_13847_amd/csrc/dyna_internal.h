@@ -110,6 +110,14 @@ struct RowdotArgs {
     // next kernels of the step use)
     int32_t* zero_words;
     int32_t n_zero_words;
+    // split-K router, optional: fp32 contexts given as the previous layer's
+    // split-K partial sums; context c's element k is act(sum over slices s,
+    // in slice order, of vpart[(s * B + c) * K + k], + vbias[k]), the value
+    // that layer's reduction would have written (v is then unused)
+    const float* vpart;
+    int32_t vslices;
+    const float* vbias;
+    int32_t vact;
 };
 
 dyna_status launch_rowdot(const RowdotArgs& a, int path, hipStream_t stream);

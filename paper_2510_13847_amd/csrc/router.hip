@@ -35,9 +35,43 @@ constexpr int max_steps(int tt) { return tt == 1 ? 16 : 8; }
 template <bool VF32>
 constexpr int stage_batch() { return VF32 ? 8 : 16; }
 
+// Eight consecutive elements (k .. k + 7) of context c given as the previous
+// layer's split-K partial sums: the slices added in order (sixteen slices'
+// loads in flight at once), then the bias and the activation, exactly as that
+// layer's reduction kernel computes them; split into bf16 hi and lo terms.
+__device__ __forceinline__ void hidden8(const RowdotArgs& a, int c, int k, u32x4& hi, u32x4& lo) {
+    constexpr int kSlicesInFlight = 16;
+    const int64_t stride = (int64_t)a.B * a.K;
+    const float* p = a.vpart + (int64_t)c * a.K + k;
+    float f[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = 0.0f;
+    for (int s0 = 0; s0 < a.vslices; s0 += kSlicesInFlight) {
+        u32x4 y[kSlicesInFlight][2];
+#pragma unroll
+        for (int u = 0; u < kSlicesInFlight; ++u)
+            if (s0 + u < a.vslices) {
+                const u32x4* q = reinterpret_cast<const u32x4*>(p + (s0 + u) * stride);
+                y[u][0] = q[0];
+                y[u][1] = q[1];
+            }
+#pragma unroll
+        for (int u = 0; u < kSlicesInFlight; ++u)
+            if (s0 + u < a.vslices)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    f[i] += __uint_as_float(y[u][0][i]);
+                    f[4 + i] += __uint_as_float(y[u][1][i]);
+                }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = apply_act(f[i] + (a.vbias ? a.vbias[k + i] : 0.0f), a.vact);
+    split8_regs(f, hi, lo);
+}
+
 // One k slice `sl` of a workgroup's row tile: stage the slice of every
 // context in LDS, multiply, write the slice's partial sums.
-template <int NW, int G, bool VF32, int TT>
+template <int NW, int G, bool VF32, int TT, bool FP = false>
 __device__ __forceinline__ void splitk_slice(const RowdotArgs& a, int ksl, int sl, float* part, uint16_t* xs) {
     constexpr int MAXS = max_steps(TT);
     constexpr int NCOL = G * 16;
@@ -76,7 +110,22 @@ __device__ __forceinline__ void splitk_slice(const RowdotArgs& a, int ksl, int s
     const int dc = T / npc, dp = T - dc * npc;
     int c = threadIdx.x / npc, p = threadIdx.x - c * npc;
     constexpr int kStageBatch = stage_batch<VF32>();
-    for (int idx0 = threadIdx.x; idx0 < npieces; idx0 += T * kStageBatch) {
+    // contexts given as the previous layer's partial sums: one piece at a
+    // time per thread, its slices' loads in flight together
+    // (FP: instances for the contexts of a few-context step only, whose
+    // registers the partial-sum loads take)
+    constexpr bool from_parts = VF32 && FP;
+    if constexpr (from_parts) {
+        for (int idx = threadIdx.x; idx < npieces; idx += T) {
+            const int cc = idx / npc, pp = idx - cc * npc;
+            u32x4 hi{0u, 0u, 0u, 0u}, lo{0u, 0u, 0u, 0u};
+            if (cc < B && pp * 8 < kn) hidden8(a, cc, k0 + pp * 8, hi, lo);
+            const int pos = cc * ksl + (pp ^ (cc & 15)) * 8;
+            *reinterpret_cast<u32x4*>(xs + pos) = hi;
+            *reinterpret_cast<u32x4*>(xs + NCOL * ksl + pos) = lo;
+        }
+    }
+    for (int idx0 = from_parts ? npieces : threadIdx.x; idx0 < npieces; idx0 += T * kStageBatch) {
         u32x4 hi[kStageBatch], lo[kStageBatch];
         int cq[kStageBatch], pq[kStageBatch];
 #pragma unroll
@@ -156,12 +205,12 @@ __device__ __forceinline__ void splitk_slice(const RowdotArgs& a, int ksl, int s
 
 // Workgroup (x, y) takes k slice y of row tile x; each slice's partial sums
 // go to their own place.
-template <int NW, int G, bool VF32, int TT>
+template <int NW, int G, bool VF32, int TT, bool FP>
 __global__ __launch_bounds__(NW * kWave) void dense_splitk_kernel(RowdotArgs a, int ksl, float* part) {
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [G*16][ksl] hi, then lo
     if (a.zero_words != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && (int)threadIdx.x < a.n_zero_words)
         a.zero_words[threadIdx.x] = 0;
-    splitk_slice<NW, G, VF32, TT>(a, ksl, blockIdx.y, part, xs);
+    splitk_slice<NW, G, VF32, TT, FP>(a, ksl, blockIdx.y, part, xs);
 }
 
 // out[b * ld + r] = act(sum over slices, in slice order, + bias[r])
@@ -178,7 +227,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     }
 }
 
-template <int NW, int G, bool VF32, int TT>
+template <int NW, int G, bool VF32, int TT, bool FP = false>
 dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* part, bool reduce, hipStream_t stream) {
     const dim3 grid((unsigned)sh.row_tiles, (unsigned)sh.slices);
     const uint32_t lds = (uint32_t)sh.lds;
@@ -188,13 +237,13 @@ dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* pa
         int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return set_error(DYNA_ERR_HIP, "router: device");
         if (!(allowed.load() & (1ull << dev))) {
-            if (hipFuncSetAttribute((const void*)dense_splitk_kernel<NW, G, VF32, TT>,
+            if (hipFuncSetAttribute((const void*)dense_splitk_kernel<NW, G, VF32, TT, FP>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget) != hipSuccess)
                 return set_error(DYNA_ERR_HIP, "router: LDS attribute");
             allowed.fetch_or(1ull << dev);
         }
     }
-    dense_splitk_kernel<NW, G, VF32, TT><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
+    dense_splitk_kernel<NW, G, VF32, TT, FP><<<grid, dim3(NW * kWave), lds, stream>>>(a, sh.ksl, part);
     const dyna_status st = check_launch("dense_splitk_kernel");
     if (st != DYNA_OK || !reduce) return st;
     const int rx = (a.n_rows + 255) / 256;
@@ -206,6 +255,13 @@ dyna_status launch_splitk_t(const RowdotArgs& a, const SplitShape& sh, float* pa
 template <int NW, bool VF32>
 dyna_status launch_splitk_g(const RowdotArgs& a, const SplitShape& sh, float* part, bool reduce, hipStream_t stream) {
     // the kernel's row tiles per wave must be the shape's (they bound the slice length)
+    if (a.vpart != nullptr) {
+        // contexts from partial sums: up to 16 contexts (one column group)
+        if constexpr (VF32) {
+            if (sh.tiles == 1 && sh.groups == 1) return launch_splitk_t<NW, 1, true, 1, true>(a, sh, part, reduce, stream);
+        }
+        return set_error(DYNA_ERR_UNSUPPORTED, "split-K router: partial-sum contexts need fp32 and <= 16 contexts");
+    }
     if (sh.tiles == 2) {
         if (sh.groups == 4) return launch_splitk_t<NW, 4, VF32, 2>(a, sh, part, reduce, stream);
         return launch_splitk_t<NW, 8, VF32, 2>(a, sh, part, reduce, stream);

@@ -148,6 +148,32 @@ def test_route_parity(w, path):
     assert strict <= PC.strict_limit(w.B)
 
 
+@pytest.mark.parametrize("B", [5, 9, 16, 17])
+@pytest.mark.parametrize("x_dtype", ["bf16", "f32"])
+def test_route_hidden_from_partial_sums(B, x_dtype):
+    """5..16 contexts: router layer 2 stages the hidden layer from layer 1's
+    split-K partial sums (added in slice order, then bias and activation)
+    instead of a reduction launch.  The scores must equal, bit for bit, those
+    of the explicit split-K path with its reduction kernel (router path 2),
+    and the oracle's within the score tolerance; 17 contexts take the
+    reduction launch on both paths."""
+    w = case(f"hid_b{B}", V=3001, d=1000, M=300, H=520, k=5, B=B)
+    p = Problem(w)
+    x = p.hd if x_dtype == "bf16" else p.hd.float()
+    out = {}
+    for path in (0, 2):
+        D.set_option(D.OPT_ROUTER_PATH, path)
+        try:
+            _, _, scores = D.route(p.R, x, w.k, want_scores=True)
+            torch.cuda.synchronize()
+        finally:
+            D.set_option(D.OPT_ROUTER_PATH, 0)
+        out[path] = scores.cpu()
+    assert torch.equal(out[0], out[2])
+    # the fp32 contexts hold the bf16 values exactly: the same reference
+    PC.assert_close(out[0].numpy().astype(np.float64), p.oracle_scores(), PC.SCORE_TOL, "router scores")
+
+
 def test_route_nan_and_ties():
     # NaN features make every score NaN: all count as -inf, ties go to lower ids
     M, d_r = 50, 64
