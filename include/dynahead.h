@@ -243,7 +243,7 @@ dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
 /* ------------------------------------------------------------------ */
 
 /* Bytes of the library's static per-GPU scratch array used by
- * dyna_draft_head_noalloc (the first 128 KiB hold the one-launch step's
+ * dyna_draft_head_noalloc (the first 384 KiB hold the one-launch step's
  * hand-off region, the rest is the step's workspace). */
 #define DYNA_NOALLOC_SCRATCH_BYTES (16u << 20)
 
@@ -258,7 +258,7 @@ dyna_status dyna_draft_head(const dyna_router* r, const dyna_layout* L,
  * Every call on a GPU shares that GPU's array and may leave data in it, so
  * calls that overlap on one GPU (other streams, other host threads) race;
  * order them on one stream.  A step whose workspace (dyna_workspace_bytes)
- * exceeds DYNA_NOALLOC_SCRATCH_BYTES - 128 KiB returns DYNA_ERR_WORKSPACE:
+ * exceeds DYNA_NOALLOC_SCRATCH_BYTES - 384 KiB returns DYNA_ERR_WORKSPACE:
  * one context at any shape, and batches up to the tree-batch and serving
  * shapes of the paper's settings (B = 64, k = 32 at V = 128256; B = 16, k =
  * 64 at V = 151936) fit. */

@@ -717,12 +717,12 @@ dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const vo
     const bool want_sample = (mode & DYNA_SEL_SAMPLE) != 0;
     int32_t* clusters = out_clusters ? out_clusters : c.topk_ids;
     float* logits = out_logits ? out_logits : c.logits;
-    // one context, argmax or top-k_t: the gathered head carries the selection
-    // (4 launches); greedy, the whole step can be one launch
+    // one context, argmax or top-k_t: the whole step in one launch, or the
+    // gathered head carrying the selection (4 launches)
     const int fused_opt = g_fused_off.load();
     const bool fused = B == 1 && fused_opt != 1 && option_logits_path() <= 1 && k_t >= 1 &&
                        k_t <= kFusedTopkMax && !want_sample;
-    if (fused && k_t == 1 && (fused_opt == 0 || fused_opt == 3) && !split && option_router_path() <= 1) {
+    if (fused && (fused_opt == 0 || fused_opt == 3) && !split && option_router_path() <= 1) {
         ChainRequest q{};
         q.all_bf16 = r->wdtype == DYNA_BF16 && L->wdtype == DYNA_BF16 && adtype == DYNA_BF16;
         q.W1 = r->W1;
@@ -750,6 +750,7 @@ dyna_status draft_head_core(const dyna_router* r, const dyna_layout* L, const vo
         q.out_logits = out_logits;
         q.out_ids = want_ids ? out_ids : nullptr;
         q.out_logprobs = want_ids ? out_logprobs : nullptr;
+        q.k_t = k_t;
         q.inv_t = 1.0f / temperature;
         q.beta = tail_beta;
         // the one launch needs its whole grid resident at once; a shape the

@@ -1,6 +1,6 @@
-// One-context greedy draft step in a single launch (B = 1): router layer 1,
-// router layer 2, top-k clusters and shortlist, gathered logits and argmax
-// selection (Sec. 4.2 and Sec. 4.3; Algorithm 1, one draft step).
+// One-context draft step in a single launch (B = 1): router layer 1, router
+// layer 2, top-k clusters and shortlist, gathered logits and the argmax or
+// top-k_t selection (Sec. 4.2 and Sec. 4.3; Algorithm 1, one draft step).
 //
 // With one context every stage is small (the chain workload moves 8 MB,
 // 2 MB, 4 KB and 33 MB), so as separate kernels the step is dominated by
@@ -22,7 +22,9 @@
 //      non-temporal 16-byte loads and dotted with h (in registers);
 //   5. each workgroup publishes its greedy partial; workgroup 0 polls them,
 //      merges them in workgroup order and writes the token, and the last
-//      workgroup writes the selection outputs.
+//      workgroup writes the selection outputs.  For top-k_t (k_t <= 16) a
+//      partial also carries the workgroup's k_t best keys, and workgroup 0
+//      takes the k_t best of all of them.
 //
 // Hand-off protocol: every handed-off word is 64 bits, a 32-bit epoch tag
 // above the 32-bit value, written with one device-coherent store; readers
@@ -52,8 +54,12 @@ constexpr int kChainWaves = kChainThreads / kWave;
 
 // words of the chain region of the workspace: epoch, error, then tagged
 // hidden [H], scores [M] and partials [G][3] (best key high, low; sum of
-// exponentials: the partial's maximum logit is its best key's value)
+// exponentials: the partial's maximum logit is its best key's value).  A
+// top-k_t partial adds the keys of places 1 .. k_t - 1 (high, low), at a
+// stride of kPartWordsTopk words.
 constexpr int kPartWords = 3;
+constexpr int kChainTopkMax = 16;
+constexpr int kPartWordsTopk = kPartWords + 2 * (kChainTopkMax - 1);
 constexpr int kChainMaxGrid = 1024;  // workgroups at most (twice the compute units, capped)
 
 struct ChainArgs {
@@ -84,8 +90,9 @@ struct ChainArgs {
     int32_t* sel_rowoff;    // [k + 1]
     int32_t* row_len;       // [1]
     float* out_logits;      // [cap], shortlist order
-    int32_t* out_ids;       // [1]
-    float* out_logprobs;    // [1]
+    int32_t* out_ids;       // [k_t]
+    float* out_logprobs;    // [k_t]
+    int32_t k_t;
     float inv_t, beta;
     uint64_t spin_ticks;  // bound of every wait, in wall-clock ticks
 };
@@ -294,6 +301,37 @@ __device__ __forceinline__ bool poll_parts(const ChainArgs& A, const uint64_t* s
     }
 #pragma unroll
     for (int q = 0; q < U * P; ++q) raw[q] = (uint32_t)v[q];
+    return gave_up;
+}
+
+// One thread reads the n <= P tagged words src[0..n) into raw, re-reading its
+// stale ones together until every word carries epoch e or the time bound
+// runs out.  Returns true if it gave up.
+template <int P>
+__device__ __forceinline__ bool poll_span(const ChainArgs& A, const uint64_t* src, int n, uint32_t e,
+                                          uint32_t (&raw)[P]) {
+    bool gave_up = false;
+    const uint64_t t0 = wall_clock64();
+    uint64_t v[P];
+#pragma unroll
+    for (int w = 0; w < P; ++w) v[w] = w < n ? load_coherent(src + w) : tagged(e, 0u);
+    for (;;) {
+        bool stale = false;
+#pragma unroll
+        for (int w = 0; w < P; ++w) stale |= (uint32_t)(v[w] >> 32) != e;
+        if (!stale) break;
+        if (wall_clock64() - t0 > A.spin_ticks) {
+            store_coherent(A.err, e);
+            gave_up = true;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int w = 0; w < P; ++w)
+            if ((uint32_t)(v[w] >> 32) != e) v[w] = load_coherent(src + w);
+    }
+#pragma unroll
+    for (int w = 0; w < P; ++w) raw[w] = (uint32_t)v[w];
     return gave_up;
 }
 
@@ -522,7 +560,122 @@ __device__ __forceinline__ void chain_outputs(const ChainArgs& A, const float* s
     }
 }
 
-template <int NB, int R>
+// Stage 5 of the top-k_t step.  Every workgroup ranks its waves' k_t best
+// keys by counting and publishes them with its softmax pair (tagged words);
+// workgroup 0 polls the partials, one per thread, takes the k_t best of all
+// of them (the k_t-th best partial head bounds the answer from below) and
+// merges the softmax pairs in a fixed order; the last workgroup writes the
+// selection outputs.
+template <int NT>
+__device__ void chain_topk_finish(const ChainArgs& A, const GreedyState& st, uint64_t wk, bool bad, uint32_t e,
+                                  int G, const float* sv, const int32_t* sid, const uint64_t* mkey,
+                                  const int32_t* rowoff, int k, int L) {
+    constexpr int NW = NT / kWave;
+    constexpr int KT = kChainTopkMax;
+    __shared__ uint64_t t_cand[KT * KT];
+    __shared__ uint64_t t_top[KT];
+    __shared__ uint64_t t_heads[NT];
+    __shared__ float w_m[NW], w_s[NW], f_m, f_s;
+    __shared__ int w_bad[NW], f_bad;
+    const int kt = A.k_t;
+    const int lane = lane_id(), wv = threadIdx.x / kWave;
+    // the wave's softmax pair (its maximum logit is its best key's value)
+    const uint64_t wb = wave_max_u64(st.best);
+    const float wm = wb != 0 ? key_val(wb) : -__builtin_inff();
+    const float wsum = wave_sum(st.m == -__builtin_inff() ? 0.0f : st.s * expf((st.m - wm) * A.inv_t));
+    const bool wbad = __ballot(bad) != 0;
+    if ((int)threadIdx.x < kt) t_top[threadIdx.x] = 0;
+    if (lane < kt) t_cand[wv * kt + lane] = wk;
+    if (lane == 0) {
+        w_m[wv] = wm;
+        w_s[wv] = wsum;
+        w_bad[wv] = wbad;
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < NW * kt) {
+        const uint64_t key = t_cand[threadIdx.x];
+        int rank = 0;
+        for (int j = 0; j < NW * kt; ++j) rank += t_cand[j] > key;
+        if (key != 0 && rank < kt) t_top[rank] = key;
+    }
+    if (threadIdx.x == 0) {
+        float bm = w_m[0], bs = w_s[0];
+        int any_bad = w_bad[0];
+        for (int q = 1; q < NW; ++q) {
+            softmax_merge(bm, bs, w_m[q], w_s[q], A.inv_t);
+            any_bad |= w_bad[q];
+        }
+        f_s = any_bad ? -1.0f : bs;
+    }
+    __syncthreads();
+    // publish: words 0, 1 the best key, 2 the sum, then places 1 .. kt - 1
+    uint64_t* pw = A.tpart + (int64_t)blockIdx.x * kPartWordsTopk;
+    if ((int)threadIdx.x < kt) {
+        const uint64_t key = t_top[threadIdx.x];
+        const int w0 = threadIdx.x == 0 ? 0 : kPartWords + 2 * ((int)threadIdx.x - 1);
+        store_coherent(pw + w0, tagged(e, (uint32_t)(key >> 32)));
+        store_coherent(pw + w0 + 1, tagged(e, (uint32_t)key));
+    }
+    if (threadIdx.x == 0) store_coherent(pw + 2, tagged(e, __float_as_uint(f_s)));
+    if (blockIdx.x == G - 1) chain_outputs<NT>(A, sv, sid, mkey, rowoff, k, L);
+    if (blockIdx.x != 0) return;
+
+    // workgroup 0: thread t polls partials t, t + NT, ... and keeps their
+    // keys as one sorted list
+    const uint32_t err_word = load_coherent(A.err);
+    const int nwords = kPartWords + 2 * (kt - 1);
+    uint64_t list[KT];
+#pragma unroll
+    for (int r = 0; r < KT; ++r) list[r] = 0;
+    float bm = -__builtin_inff(), bs = 0.0f;
+    bool fail = false;
+    for (int g = threadIdx.x; g < G; g += NT) {
+        uint32_t raw[kPartWordsTopk];
+        fail |= poll_span<kPartWordsTopk>(A, A.tpart + (int64_t)g * kPartWordsTopk, nwords, e, raw);
+        uint64_t pk[KT];
+#pragma unroll
+        for (int r = 0; r < KT; ++r) {
+            const int w0 = r == 0 ? 0 : kPartWords + 2 * (r - 1);
+            pk[r] = r < kt ? ((uint64_t)raw[w0] << 32) | raw[w0 + 1] : 0;
+        }
+        const float s2 = __uint_as_float(raw[2]);
+        fail |= s2 < 0.0f;
+        softmax_merge(bm, bs, pk[0] != 0 ? key_val(pk[0]) : -__builtin_inff(), s2 > 0.0f ? s2 : 0.0f, A.inv_t);
+        if (g == (int)threadIdx.x) {
+#pragma unroll
+            for (int r = 0; r < KT; ++r) list[r] = pk[r];
+        } else {
+            for (int r = 0; r < kt; ++r) {
+                if (pk[r] <= list[KT - 1]) break;  // the partial's keys are sorted
+                list[KT - 1] = pk[r];
+#pragma unroll
+                for (int q = KT - 1; q > 0; --q)
+                    if (list[q] > list[q - 1]) {
+                        const uint64_t t = list[q];
+                        list[q] = list[q - 1];
+                        list[q - 1] = t;
+                    }
+            }
+        }
+    }
+    if (threadIdx.x == 0) f_bad = 0;
+    block_topk_lists<KT, NT>(list, kt, t_heads, t_cand, t_top);
+    if (fail) f_bad = 1;
+    block_softmax_pair<NT>(bm, bs, A.inv_t, w_m, w_s, &f_m, &f_s);
+    __syncthreads();
+    const bool err = f_bad != 0 || err_word == e;
+    // every workgroup has read the epoch (its partial carries it)
+    if (threadIdx.x == 0) store_coherent(A.epoch, e);
+    const float lshift = (A.beta > 0.0f && (int64_t)A.V > L) ? log1pf(-A.beta) : 0.0f;
+    for (int r = threadIdx.x; r < kt; r += NT) {
+        const uint64_t key = err ? 0 : t_top[r];
+        A.out_ids[r] = key != 0 ? (int32_t)key_id(key) : -1;
+        if (A.out_logprobs)
+            A.out_logprobs[r] = key != 0 ? (key_val(key) - f_m) * A.inv_t - logf(f_s) + lshift : -__builtin_inff();
+    }
+}
+
+template <int NB, int R, bool TOPK>
 __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int M = A.M, k = A.k, H = A.H;
@@ -629,6 +782,7 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     // ---- stage 4: logits over the wave's contiguous range of shortlist slots
     if constexpr (!kEarly) load_h();
     GreedyState st;
+    uint64_t wk = 0;  // top-k_t: this lane's place of the wave's key list
     {
         const int64_t p0 = (int64_t)gw * L / nw, p1 = (int64_t)(gw + 1) * L / nw;
         // slot q's cluster position: the number of clusters whose slabs end at
@@ -695,7 +849,18 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
                 if (A.out_logits) A.out_logits[p + lane] = mine;
                 st.add(mine, vid, A.inv_t);
             }
+            if constexpr (TOPK) {
+                // the group's keys into the wave's list, one row at a time
+                // (branch-free: an empty key 0 leaves the list as it is)
+                const uint64_t mykey = own ? sel_key(mine != mine ? -__builtin_inff() : mine, (uint32_t)vid) : 0;
+#pragma unroll
+                for (int r = 0; r < R; ++r) wk = row_list_insert(wk, readlane_u64(mykey, r));
+            }
         }
+    }
+    if constexpr (TOPK) {
+        chain_topk_finish<kChainThreads>(A, st, wk, bad, e, G, sv, sid, cand, rowoff, k, L);
+        return;
     }
 
     // ---- stage 5: greedy partials; workgroup 0 polls and merges them.  A
@@ -800,9 +965,9 @@ __global__ __launch_bounds__(kChainThreads) void chain_step_kernel(ChainArgs A) 
     }
 }
 
-template <int NB, int R>
+template <int NB, int R, bool TOPK>
 const void* chain_fn() {
-    return reinterpret_cast<const void*>(chain_step_kernel<NB, R>);
+    return reinterpret_cast<const void*>(chain_step_kernel<NB, R, TOPK>);
 }
 
 // The kernel instance for the widest of d_r, H and d: NB blocks of 512
@@ -827,7 +992,7 @@ int chain_instance_index(int kmax) {
 struct ChainDevice {
     int cus = 0;
     int64_t tick_khz = 0;
-    size_t lds_raised[kChainInstances] = {};  // dynamic LDS limit set per instance (0: the default 64 KB)
+    size_t lds_raised[2 * kChainInstances] = {};  // dynamic LDS limit set per instance (0: the default 64 KB)
 };
 
 std::mutex g_chain_mu;
@@ -836,13 +1001,13 @@ ChainDevice g_chain_dev[kMaxDevices];
 }  // namespace
 
 size_t chain_region_bytes(int32_t H, int32_t M) {
-    return 256 + (size_t)8 * (H + M) + (size_t)8 * kPartWords * kChainMaxGrid;
+    return 256 + (size_t)8 * (H + M) + (size_t)8 * kPartWordsTopk * kChainMaxGrid;
 }
 
 bool chain_step_eligible(const ChainRequest& q) {
     const int kmax = std::max(q.d_r, std::max(q.H, q.d));
     return q.all_bf16 && q.region != nullptr && kmax <= 8192 && q.M <= kChainMaxM && q.V < (1 << kLenBits) &&
-           chain_lds_bytes(q.M, q.k, q.H) <= 160 * 1024;
+           q.k_t >= 1 && q.k_t <= kChainTopkMax && chain_lds_bytes(q.M, q.k, q.H) <= 160 * 1024;
 }
 
 int option_wait_bound_us();  // DYNA_OPT_WAIT_BOUND_US: 0 default, -1 none, else microseconds
@@ -859,7 +1024,7 @@ int chain_step_grid(const ChainRequest& q, int64_t* tick_khz) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
     const int kmax = std::max(q.d_r, std::max(q.H, q.d));
-    const int inst = chain_instance_index(kmax);
+    const int inst = chain_instance_index(kmax) + (q.k_t > 1 ? kChainInstances : 0);
     const size_t lds = chain_lds_bytes(q.M, q.k, q.H);
     std::lock_guard<std::mutex> g(g_chain_mu);
     ChainDevice& cd = g_chain_dev[dev];
@@ -873,7 +1038,12 @@ int chain_step_grid(const ChainRequest& q, int64_t* tick_khz) {
         cd.cus = n;
         cd.tick_khz = khz;
     }
-    const void* fn = with_chain_instance(kmax, [](auto nb, auto r) { return chain_fn<decltype(nb)::value, decltype(r)::value>(); });
+    const void* fn = q.k_t > 1 ? with_chain_instance(kmax, [](auto nb, auto r) {
+        return chain_fn<decltype(nb)::value, decltype(r)::value, true>();
+    })
+                               : with_chain_instance(kmax, [](auto nb, auto r) {
+                                     return chain_fn<decltype(nb)::value, decltype(r)::value, false>();
+                                 });
     // dynamic LDS above the default 64 KB must be allowed per kernel first
     // (up to what the kernel's static LDS leaves of the 160 KB)
     if (lds > 64 * 1024 && lds > cd.lds_raised[inst]) {
@@ -931,6 +1101,7 @@ dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
     a.out_logits = q.out_logits;
     a.out_ids = q.out_ids;
     a.out_logprobs = q.out_logprobs;
+    a.k_t = q.k_t;
     a.inv_t = q.inv_t;
     a.beta = q.beta;
     // every wait is bounded by 0.2 s of wall clock (or the bound set by
@@ -941,8 +1112,12 @@ dyna_status launch_chain_step(const ChainRequest& q, hipStream_t s) {
     const size_t lds = chain_lds_bytes(q.M, q.k, q.H);
     const int kmax = std::max(q.d_r, std::max(q.H, q.d));
     with_chain_instance(kmax, [&](auto nb, auto r) {
-        launch_timed_kernel(chain_step_kernel<decltype(nb)::value, decltype(r)::value>, dim3(grid),
-                            dim3(kChainThreads), (uint32_t)lds, s, a);
+        if (q.k_t > 1)
+            launch_timed_kernel(chain_step_kernel<decltype(nb)::value, decltype(r)::value, true>, dim3(grid),
+                                dim3(kChainThreads), (uint32_t)lds, s, a);
+        else
+            launch_timed_kernel(chain_step_kernel<decltype(nb)::value, decltype(r)::value, false>, dim3(grid),
+                                dim3(kChainThreads), (uint32_t)lds, s, a);
         return 0;
     });
     return check_launch("chain_step_kernel");

@@ -287,8 +287,9 @@ size_t greedy_partials_bytes();
 dyna_status launch_logits_greedy(const RowdotArgs& lg, const SelectArgs& sa, void* partials,
                                  int32_t* counter, hipStream_t s);
 
-// chain.hip (one context, greedy, bf16 throughout): the whole step in one
-// launch, handing words between workgroups through an epoch-tagged region.
+// chain.hip (one context, argmax or top-k_t, bf16 throughout): the whole
+// step in one launch, handing words between workgroups through an
+// epoch-tagged region.
 struct ChainRequest {
     bool all_bf16;  // router weights, LM head, x and h all bf16
     const void* W1;
@@ -310,8 +311,9 @@ struct ChainRequest {
     int32_t* sel_rowoff;
     int32_t* row_len;
     float* out_logits;
-    int32_t* out_ids;
-    float* out_logprobs;
+    int32_t* out_ids;       // [k_t]
+    float* out_logprobs;    // [k_t]
+    int32_t k_t;            // 1 (argmax) .. 16
     float inv_t, beta;
 };
 size_t chain_region_bytes(int32_t H, int32_t M);

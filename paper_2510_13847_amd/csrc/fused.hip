@@ -68,25 +68,6 @@ struct TopkPartial {
     float m, s;
 };
 
-// The key of each row goes into a list kept across the wave: lane l of
-// every 16-lane row holds the wave's l-th best key so far (descending, 0 =
-// empty).  A key x enters in one step, all lanes at once: place l takes
-// max(key_l, min(key_{l-1}, x)), key_{l-1} read from the lane below (row
-// shift; the row's first lane reads the all-ones identity).  Eight vector
-// instructions per key, and no per-lane list in registers.
-__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
-    return ((uint64_t)hi << 32) | lo;
-}
-__device__ __forceinline__ uint64_t row_list_insert(uint64_t mine, uint64_t x) {
-    const uint32_t plo = dpp<kRowShr1>(0xffffffffu, (uint32_t)mine);
-    const uint32_t phi = dpp<kRowShr1>(0xffffffffu, (uint32_t)(mine >> 32));
-    const uint64_t prev = ((uint64_t)phi << 32) | plo;
-    const uint64_t up = prev < x ? prev : x;
-    return mine > up ? mine : up;
-}
-
 // Epilogue of the one-context top-k head: lanes below R own the rows of a
 // group (one context: one row per lane per group); their keys are listed at
 // the next group's idle point, while its loads are in flight.
@@ -97,11 +78,9 @@ struct TopkEpi {
     uint64_t pend = 0;  // key of the row this lane produced last (0: none)
     float m = -__builtin_inff(), s = 0.0f;
     __device__ __forceinline__ void idle() {
+        // branch-free: an empty key 0 leaves the list as it is
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const uint64_t x = readlane_u64(pend, r);
-            if (x != 0) wk = row_list_insert(wk, x);
-        }
+        for (int r = 0; r < R; ++r) wk = row_list_insert(wk, readlane_u64(pend, r));
         pend = 0;
     }
     __device__ __forceinline__ void put(const RowdotArgs& a, int64_t o, float value, int32_t vid) {
@@ -112,69 +91,6 @@ struct TopkEpi {
         softmax_merge(m, s, z, 1.0f, inv_t);
     }
 };
-
-// The workgroup's (m, s) over its lanes in a fixed order (thread 0 gets it).
-__device__ __forceinline__ void block_softmax_pair(float m, float s, float inv_t, float* w_m, float* w_s,
-                                                   float* out_m, float* out_s) {
-    constexpr int NW = kThreads / kWave;
-    const int lane = lane_id(), w = threadIdx.x / kWave;
-    const float wm = readlane_f32(wave_max_f32(m), kWave - 1);
-    const float ws = wave_sum(m == -__builtin_inff() ? 0.0f : s * expf((m - wm) * inv_t));
-    if (lane == 0) {
-        w_m[w] = wm;
-        w_s[w] = ws;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        float bm = w_m[0], bs = w_s[0];
-        for (int q = 1; q < NW; ++q) softmax_merge(bm, bs, w_m[q], w_s[q], inv_t);
-        *out_m = bm;
-        *out_s = bs;
-    }
-}
-
-// The k_t (<= L) best keys held in sorted lists (descending, 0 = empty;
-// valid keys distinct and nonzero), one list per thread of NT.  The k_t-th
-// best list head T bounds the answer from below (k_t distinct heads are
-// >= T), so only entries >= T of lists whose head is >= T can be selected:
-// at most k_t lists of k_t entries, ranked by counting.  No chain of k_t
-// block-wide maxima.  out[0..k_t) gets the keys in descending order, 0 where
-// fewer exist; ends with a barrier.
-template <int L, int NT>
-__device__ void block_topk_lists(const uint64_t (&list)[L], int k_t, uint64_t* heads /* LDS [NT] */,
-                                 uint64_t* cand /* LDS [L * L] */, uint64_t* out /* LDS [k_t] */) {
-    __shared__ uint64_t sh_T;
-    __shared__ int sh_n;
-    const uint64_t head = list[0];
-    heads[threadIdx.x] = head;
-    if (threadIdx.x == 0) {
-        sh_T = 0;
-        sh_n = 0;
-    }
-    __syncthreads();
-    if (head != 0) {
-        int rank = 0;
-        for (int j = 0; j < NT; ++j) rank += heads[j] > head;
-        if (rank == k_t - 1) sh_T = head;
-    }
-    __syncthreads();
-    const uint64_t T = sh_T;
-    if (head != 0 && head >= T) {
-#pragma unroll
-        for (int r = 0; r < L; ++r)
-            if (r < k_t && list[r] != 0 && list[r] >= T) cand[atomicAdd(&sh_n, 1)] = list[r];
-    }
-    __syncthreads();
-    const int n = sh_n;
-    for (int c = threadIdx.x; c < n; c += NT) {
-        const uint64_t key = cand[c];
-        int rank = 0;
-        for (int j = 0; j < n; ++j) rank += cand[j] > key;
-        if (rank < k_t) out[rank] = key;
-    }
-    for (int r = n + threadIdx.x; r < k_t; r += NT) out[r] = 0;
-    __syncthreads();
-}
 
 template <typename WT, typename VT, int NB, int R>
 __global__ __launch_bounds__(kThreads) void logits_topk_kernel(RowdotArgs lg, SelectArgs sa, TopkPartial* part,
@@ -211,7 +127,7 @@ __global__ __launch_bounds__(kThreads) void logits_topk_kernel(RowdotArgs lg, Se
         }
         __syncthreads();
     }
-    block_softmax_pair(epi.m, epi.s, sa.inv_t, w_m, w_s, &f_m, &f_s);
+    block_softmax_pair<kThreads>(epi.m, epi.s, sa.inv_t, w_m, w_s, &f_m, &f_s);
     TopkPartial* mine = part + blockIdx.x;
     if ((int)threadIdx.x < k_t) store_coherent(&mine->key[threadIdx.x], top[threadIdx.x]);
     if (threadIdx.x == 0) {
@@ -259,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void logits_topk_kernel(RowdotArgs lg, Se
         softmax_merge(bm, bs, m2, s2, sa.inv_t);
     }
     block_topk_lists<kTopkMax, kThreads>(list, k_t, heads, cand, top);
-    block_softmax_pair(bm, bs, sa.inv_t, w_m, w_s, &f_m, &f_s);
+    block_softmax_pair<kThreads>(bm, bs, sa.inv_t, w_m, w_s, &f_m, &f_s);
     __syncthreads();
     const TailMix tail = tail_of(sa, sa.row_len ? sa.row_len[0] : sa.fixed_len);
     const float log_total = logf(f_s) - tail.lshift;

@@ -20,9 +20,9 @@ namespace dyna {
 namespace {
 
 constexpr size_t kScratchBytes = DYNA_NOALLOC_SCRATCH_BYTES;
-// 256 + 8 (H + M) + 24 * 1024 bytes for H <= 8192, M <= 1024 (the one-launch
-// step's limits) is below 100 KB
-constexpr size_t kChainReserve = 128 * 1024;
+// 256 + 8 (H + M) + 8 * 33 * 1024 bytes for H <= 8192, M <= 1024 (the
+// one-launch step's limits) is below 340 KB
+constexpr size_t kChainReserve = 384 * 1024;
 static_assert(kScratchBytes > kChainReserve, "scratch too small");
 
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];

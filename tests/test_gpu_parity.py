@@ -802,12 +802,14 @@ TOPK_FUSED_CASES = [c for c in FUSED_CASES if c.name in
 
 @pytest.mark.parametrize("temperature", [1.0, 0.6])
 @pytest.mark.parametrize("k_t", [2, 7, 16])
+@pytest.mark.parametrize("fused_opt", [3, 2], ids=["one_launch", "four_launches"])
 @pytest.mark.parametrize("w", TOPK_FUSED_CASES, ids=lambda w: w.name)
-def test_fused_topk_matches_separate_kernels(w, k_t, temperature):
-    """TopK_{k_t} of one context (k_t up to 16) folds the selection into the
-    gathered head: the ids must equal the separate kernels' exactly, in rank
-    order, and the log-probabilities within rounding, call after call (the
-    arrival counter resets itself); and both against the oracle's selection
+def test_fused_topk_matches_separate_kernels(w, fused_opt, k_t, temperature):
+    """TopK_{k_t} of one context (k_t up to 16) runs as the one-launch step
+    (bf16 shapes), or folds the selection into the gathered head: the ids
+    must equal the separate kernels' exactly, in rank order, and the
+    log-probabilities within rounding, call after call (the hand-off epoch
+    and the arrival counter run on); and both against the oracle's selection
     on the GPU's own logits."""
     p = Problem(w)
     mode = D.SEL_TOPK
@@ -815,7 +817,7 @@ def test_fused_topk_matches_separate_kernels(w, k_t, temperature):
     sep = D.DraftHead(p.R, p.L, 1, w.k, mode, k_t, temperature, keep_logits=True)
     for it in range(4):
         x = W.contexts(w, "cpu", salt=it).to(DEV)
-        D.set_option(D.OPT_FUSED_B1, 0)
+        D.set_option(D.OPT_FUSED_B1, _one_launch_opt(w) if fused_opt == 3 else fused_opt)
         try:
             fused(x, x)
             D.set_option(D.OPT_FUSED_B1, 1)
@@ -841,10 +843,12 @@ def test_fused_topk_matches_separate_kernels(w, k_t, temperature):
         PC.assert_close(lf[0, :m], np.asarray(r["logprobs"][:m]), PC.LOGPROB_TOL, "lp oracle")
 
 
-def test_fused_topk_ties_take_lower_ids():
-    """A zero drafter state makes every shortlist logit 0: the fused top-k
-    must then take the k_t lowest vocabulary ids of the shortlist, each with
-    log-probability -log |V_S|, as the separate kernels do."""
+@pytest.mark.parametrize("fused_opt", [3, 2], ids=["one_launch", "four_launches"])
+def test_fused_topk_ties_take_lower_ids(fused_opt):
+    """A zero drafter state makes every shortlist logit 0: the one-launch and
+    the fused top-k must then take the k_t lowest vocabulary ids of the
+    shortlist, each with log-probability -log |V_S|, as the separate kernels
+    do."""
     w = next(c for c in FUSED_CASES if c.name == "fused_big")
     p = Problem(w)
     k_t = 16
@@ -852,7 +856,7 @@ def test_fused_topk_ties_take_lower_ids():
     sep = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_TOPK, k_t, keep_logits=True)
     x = W.contexts(w, "cpu", salt=3).to(DEV)
     h = torch.zeros_like(x)
-    D.set_option(D.OPT_FUSED_B1, 0)
+    D.set_option(D.OPT_FUSED_B1, fused_opt)
     try:
         fused(x, h)
         D.set_option(D.OPT_FUSED_B1, 1)
