@@ -911,18 +911,20 @@ def test_one_launch_step_ties(variant):
             assert tied == list(range(3, 3 + len(tied)))
 
 
-def test_one_launch_step_wait_bound():
-    """Every wait of the one-launch step is bounded.  With the bound forced
-    from the host to nothing (a wait gives up at its first read that finds a
-    word missing), a step must report the failure (id -1, log-probability
-    -inf) and never a token from half-written data; once the bound is back,
-    the very next step is exact again (the error word carries the epoch of
-    the launch that set it, so a late give-up cannot fail a later step)."""
+@pytest.mark.parametrize("k_t", [1, 10])
+def test_one_launch_step_wait_bound(k_t):
+    """Every wait of the one-launch step (argmax and top-k_t) is bounded.
+    With the bound forced from the host to nothing (a wait gives up at its
+    first read that finds a word missing), a step must report the failure
+    (ids -1, log-probabilities -inf) and never a token from half-written
+    data; once the bound is back, the very next step is exact again (the
+    error word carries the epoch of the launch that set it, so a late give-up
+    cannot fail a later step)."""
     w = next(c for c in FUSED_CASES if c.name == "chain_wide")
     p = Problem(w)
-    mode = D.SEL_ARGMAX
-    one = D.DraftHead(p.R, p.L, 1, w.k, mode, 1, keep_logits=True)
-    sep = D.DraftHead(p.R, p.L, 1, w.k, mode, 1, keep_logits=True)
+    mode = D.SEL_ARGMAX if k_t == 1 else D.SEL_TOPK
+    one = D.DraftHead(p.R, p.L, 1, w.k, mode, k_t, keep_logits=True)
+    sep = D.DraftHead(p.R, p.L, 1, w.k, mode, k_t, keep_logits=True)
 
     def step(it, bound):
         x = W.contexts(w, "cpu", salt=it).to(DEV)
@@ -936,11 +938,11 @@ def test_one_launch_step_wait_bound():
             D.set_option(D.OPT_FUSED_B1, 0)
             D.set_option(D.OPT_WAIT_BOUND_US, 0)
         torch.cuda.synchronize()
-        got, want = int(one.ids[0, 0]), int(sep.ids[0, 0])
-        if got == -1:
-            assert float(one.logprobs[0, 0]) == -np.inf
+        got, want = one.ids[0].cpu(), sep.ids[0].cpu()
+        if int(got[0]) == -1:
+            assert (got == -1).all() and torch.isneginf(one.logprobs[0].cpu()).all()
             return False
-        assert got == want and torch.equal(one.clusters, sep.clusters)
+        assert torch.equal(got, want) and torch.equal(one.clusters, sep.clusters)
         return True
 
     with pytest.raises(D.DynaError):
