@@ -843,6 +843,33 @@ def test_fused_topk_matches_separate_kernels(w, fused_opt, k_t, temperature):
         PC.assert_close(lf[0, :m], np.asarray(r["logprobs"][:m]), PC.LOGPROB_TOL, "lp oracle")
 
 
+@pytest.mark.parametrize("grid", [37, 1024, 4096])
+def test_fused_topk_workgroup_counts(grid):
+    """The fused top-k head with a fixed number of workgroups (few, and more
+    than the last workgroup has threads, so that a thread merges several
+    partial lists): ids equal to the separate kernels', log-probabilities
+    within rounding."""
+    w = next(c for c in FUSED_CASES if c.name == "fused_big")
+    p = Problem(w)
+    k_t = 16
+    fused = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_TOPK, k_t, keep_logits=True)
+    sep = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_TOPK, k_t, keep_logits=True)
+    for it in range(3):
+        x = W.contexts(w, "cpu", salt=it).to(DEV)
+        D.set_option(D.OPT_GREEDY_GRID, grid)
+        D.set_option(D.OPT_FUSED_B1, 2)
+        try:
+            fused(x, x)
+            D.set_option(D.OPT_FUSED_B1, 1)
+            sep(x, x)
+        finally:
+            D.set_option(D.OPT_FUSED_B1, 0)
+            D.set_option(D.OPT_GREEDY_GRID, 0)
+        torch.cuda.synchronize()
+        assert torch.equal(fused.ids, sep.ids)
+        PC.assert_close(fused.logprobs.cpu().numpy(), sep.logprobs.cpu().numpy(), (2e-6, 2e-6), "lp")
+
+
 @pytest.mark.parametrize("fused_opt", [3, 2], ids=["one_launch", "four_launches"])
 def test_fused_topk_ties_take_lower_ids(fused_opt):
     """A zero drafter state makes every shortlist logit 0: the one-launch and
@@ -956,16 +983,19 @@ def test_one_launch_step_wait_bound(k_t):
 
 
 @pytest.mark.parametrize("grid_per_cu", [2, 3])
-def test_one_launch_step_grid_beyond_residency(grid_per_cu):
+@pytest.mark.parametrize("k_t", [1, 10])
+def test_one_launch_step_grid_beyond_residency(grid_per_cu, k_t):
     """A grid request above what can be resident at once is capped by the
     occupancy check (or the step takes the four-launch form): the results stay
-    exact against the separate kernels."""
+    exact against the separate kernels.  With more workgroups than threads in
+    workgroup 0, the top-k_t merge takes several partials per thread."""
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    mode = D.SEL_ARGMAX if k_t == 1 else D.SEL_TOPK
     for name in ["chain_wide", "chain_d8192", "ragged_b1"]:
         w = next(c for c in FUSED_CASES if c.name == name)
         p = Problem(w)
-        one = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_ARGMAX, 1, keep_logits=True)
-        sep = D.DraftHead(p.R, p.L, 1, w.k, D.SEL_ARGMAX, 1, keep_logits=True)
+        one = D.DraftHead(p.R, p.L, 1, w.k, mode, k_t, keep_logits=True)
+        sep = D.DraftHead(p.R, p.L, 1, w.k, mode, k_t, keep_logits=True)
         for it in range(3):
             x = W.contexts(w, "cpu", salt=it).to(DEV)
             D.set_option(D.OPT_GREEDY_GRID, min(4096, grid_per_cu * n_cu))
@@ -981,6 +1011,7 @@ def test_one_launch_step_grid_beyond_residency(grid_per_cu):
             assert torch.equal(one.clusters, sep.clusters) and torch.equal(one.ids, sep.ids), name
             n = len(O.shortlist(one.clusters[0].cpu().numpy(), p.offsets, p.perm)[3])
             assert torch.equal(one.logits[:, :n], sep.logits[:, :n])
+            PC.assert_close(one.logprobs.cpu().numpy(), sep.logprobs.cpu().numpy(), (2e-6, 2e-6), "lp")
 
 
 @pytest.mark.parametrize("variant", ["nan", "pos_inf", "neg_inf", "mixed_inf", "all_equal"])
