@@ -386,22 +386,22 @@ int32_t dyna_static_budget(int32_t t, int32_t k_max);
  *   0 stops.
  * DYNA_OPT_GEMV_ROWS: rows each wave of the GEMV kernel keeps in flight:
  *   0 automatic, else 1, 2 or 4 (capped by the register budget).
- * DYNA_OPT_FUSED_B1: how dyna_draft_head runs a one-context greedy step.
+ * DYNA_OPT_FUSED_B1: how dyna_draft_head runs a one-context step without
+ *   sampling (argmax, or top-k_t with k_t <= 16).
  *   0 (default): one launch (router, top-k, shortlist, gathered logits and
  *   selection, the workgroups handing the hidden layer, the router scores
  *   and their partial results to each other inside the launch) when the
  *   router, LM head and activations are all bf16, d, d_r, H <= 8192,
  *   M <= 1024, V < 2^21, the step's LDS fits in 160 KB, routing stays on
  *   `stream` and the occupancy calculator finds room for the whole grid at
- *   once (its workgroups hand words to each other); otherwise as 2.  2: four launches (router layer 1; router
- *   layer 2; top-k with shortlist and plan; gathered head fused with
- *   selection).  1: the separate kernels.  3: the one launch only; a step it
- *   cannot run returns DYNA_ERR_UNSUPPORTED (for tests and measurement that
- *   must know which form ran).  A one-context top-k_t step without sampling
- *   (1 < k_t <= 16) takes the gathered head fused with the selection under 0
- *   and 2, and the separate kernels under 1 (3 rejects it).  All forms give
- *   identical clusters, logits and ids; log-probabilities agree to rounding
- *   (the softmax sum is taken in another order).
+ *   once (its workgroups hand words to each other); otherwise as 2.
+ *   2: four launches (router layer 1; router layer 2; top-k with shortlist
+ *   and plan; gathered head fused with selection).  1: the separate
+ *   kernels.  3: the one launch only; a step it cannot run returns
+ *   DYNA_ERR_UNSUPPORTED (for tests and measurement that must know which
+ *   form ran).  All forms give identical clusters, logits and ids;
+ *   log-probabilities agree to rounding (the softmax sum is taken in
+ *   another order).
  *   Under kernel timing the one-launch step, or the fused gathered-head +
  *   selection launch, is what is timed.
  * DYNA_OPT_MFMA_UNROLL: k steps the direct-load MFMA kernel (router path 3,
