@@ -35,10 +35,13 @@ def _host_rows(W_lm, vids):
     return W.host_array(W_lm.index_select(0, torch.from_numpy(np.asarray(vids)).to(DEV)))
 
 
-# later positions of one drafting cycle at the Llama-3-8B shapes: ten beam
-# rows over one union shortlist with a small cluster budget (the few-row
+# positions of one drafting cycle at the Llama-3-8B shapes: the first (one
+# context, 64 clusters, top-10: the one-launch top-k step), and ten beam rows
+# over one union shortlist with a small cluster budget (the few-row
 # short-union path) and with the second position's budget
 EXTRA = {
+    "cycle_position0": W.scaled(W.WORKLOADS["llama3_8b_chain"], name="cycle_position0", k=64, modes=("topk",),
+                                k_t=10),
     "cycle_position3": W.scaled(W.WORKLOADS["llama3_8b_tree_union"], name="cycle_position3", B=10, k=5),
     "cycle_position1": W.scaled(W.WORKLOADS["llama3_8b_tree_union"], name="cycle_position1", B=10, k=32),
     # one GPU's share of the large-vocabulary batch split by rows over eight GPUs
