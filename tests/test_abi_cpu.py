@@ -86,6 +86,28 @@ def test_workspace_sizes_are_host_only():
     assert lib.dyna_layout_workspace_bytes(128256, 1024) >= 128256 * 4
 
 
+def test_noalloc_scratch_covers_the_stated_shapes():
+    """The allocation-free entry point's scratch (DYNA_NOALLOC_SCRATCH_BYTES
+    less the 384 KiB hand-off region) holds the workspace of one context and
+    of the tree-batch and serving steps, as the header states, and not the
+    large-vocabulary and union batches (host-only sizing)."""
+    import workloads as W
+    from oracle import dynaspec_oracle as O
+    lib = D.lib()
+    limit = D.NOALLOC_SCRATCH_BYTES - 384 * 1024
+    expect = {"llama3_8b_chain": True, "llama3_8b_tree": True, "qwen25_serving": True,
+              "gemma3_large_vocab": False, "llama3_8b_tree_union": False}
+    for name, fits in expect.items():
+        w = W.WORKLOADS[name]
+        sizes, _, _, cap = O.cluster_layout(W.partition(w), w.M)
+        cap_arr = (ctypes.c_int32 * (w.M + 1))(*[int(c) for c in cap])
+        L = D._Layout(w.V, w.d, w.M, D.BF16, 0x1000, 0x2000, 0x3000, ctypes.addressof(cap_arr), int(sizes.max()))
+        R = D._Router(w.d, w.H, w.M, D.BF16, 2, 0x1000, 0, 0x1000 if w.H else 0, 0)
+        c = min(w.V, w.B * int(cap[w.k])) if w.union else int(cap[w.k])
+        need = lib.dyna_workspace_bytes(ctypes.byref(L), ctypes.byref(R), w.B, w.k, c)
+        assert (0 < need <= limit) == fits, (name, need, limit)
+
+
 def test_shortlist_logits_argument_errors():
     lib = D.lib()
     L, keep = _layout()
