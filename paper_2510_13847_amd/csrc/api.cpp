@@ -142,14 +142,11 @@ static int64_t max_chunks_for(const dyna_layout* L) {
     return ((int64_t)L->V + kChunkRows - 1) / kChunkRows + L->M;
 }
 
-// Chunks a step can produce: the union of the selected slabs holds at most
-// min(V, B * cap_by_k[k]) rows in at most min(M, B * k) clusters, and each
-// cluster adds at most one partial chunk.
 // 5..16 contexts: router layer 2 stages the hidden layer straight from layer
 // 1's split-K partial sums, so layer 1 needs no reduction launch (both
-// layers' partial sums then share the workspace side by side).
+// layers' partial sums then share the workspace side by side; the workspace
+// is sized for it whatever the router-path option says).
 constexpr int32_t kHiddenFromPartsMaxB = 16;
-// (The workspace is sized for it whatever the router-path option says.)
 static bool hidden_from_parts(const dyna_router* r, int32_t xdtype, int32_t B, size_t* f1, size_t* f2,
                               bool sizing = false) {
     if (r->H == 0 || B <= 4 || B > kHiddenFromPartsMaxB || r->wdtype != DYNA_BF16 ||
@@ -163,6 +160,9 @@ static bool hidden_from_parts(const dyna_router* r, int32_t xdtype, int32_t B, s
     return true;
 }
 
+// Chunks a step can produce: the union of the selected slabs holds at most
+// min(V, B * cap_by_k[k]) rows in at most min(M, B * k) clusters, and each
+// cluster adds at most one partial chunk.
 static int32_t chunk_bound(const dyna_layout* L, int32_t B, int32_t k) {
     const int64_t rows = std::min<int64_t>(L->V, (int64_t)B * L->cap_by_k[k]);
     const int64_t clusters = std::min<int64_t>(L->M, (int64_t)B * k);

@@ -16,7 +16,9 @@
 // Each wave keeps a private ring of S stages (a stage = KB columns of the 16
 // tile rows), so S - 1 stages of slab loads are always in flight; the context
 // columns come straight from L2 into registers.  The wave waits on its own
-// load counter only, never on a barrier.
+// load counter only, never on a barrier (except that, for short shortlists,
+// the waves of a workgroup can split one chunk's k dimension and add their
+// partial tiles through LDS behind a barrier).
 //
 // Every other memory read inside the loop (chunk descriptors, context lists,
 // the vocabulary ids of the tile rows) goes through the scalar unit, so the

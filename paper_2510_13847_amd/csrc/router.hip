@@ -14,7 +14,11 @@
 //  * the k slices give enough workgroups to cover the chip and keep the
 //    staged slice small; every slice writes its partial sums, and a second
 //    kernel adds the slices in a fixed order and applies bias and activation,
-//    so results are bit-identical from run to run.
+//    so results are bit-identical from run to run;
+//  * for a few contexts the second layer can stage its fp32 contexts (the
+//    hidden layer) straight from the first layer's partial sums, adding the
+//    slices in the same order with the same bias and activation, which saves
+//    the reduction launch and gives the same values.
 //
 // LDS layout: context c, 16-byte piece p of the slice at position p ^ (c & 15)
 // (16 lanes reading one piece index of 16 contexts hit 16 bank groups).
