@@ -208,6 +208,7 @@ struct SelectArgs {
     float beta;               // tail weight of the mixture proposal (0: none)
     int32_t V;                // vocabulary rows (the complement is V - row length)
     int32_t P;                // segments per row
+    int32_t seg;              // slots per segment
     // partials, [B][P][...]
     uint64_t* pkeys;          // [B][P][k_t]
     float* pmax;              // [B][P]

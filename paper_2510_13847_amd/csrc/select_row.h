@@ -7,8 +7,10 @@
 namespace dyna {
 namespace {
 
-constexpr int kSeg = 2048;          // shortlist slots per partial workgroup
-constexpr int kPer = kSeg / kNT;    // 8 slots per thread
+// Segments of the long-row selection: 1024 slots (4 per thread) for rows of
+// at most 1024 * kNT slots, else 2048 (8 per thread; rows up to kSeg * kNT).
+constexpr int kSeg = 2048;
+constexpr int kSegShort = 1024;
 constexpr int kRowMax = 1 << 17;    // longest shortlist row the one-launch select takes
 constexpr int kRowSplit = 1 << 14;  // longer rows may go to the segmented select instead
 

@@ -670,17 +670,19 @@ def test_static_head_prefix(B):
         assert ok
 
 
+@pytest.mark.parametrize("V,B", [(40000, 5), (300000, 5), (65536, 64)])
 @pytest.mark.parametrize("k_t", [1, 10])
-def test_dense_head_long_rows(k_t):
+def test_dense_head_long_rows(k_t, V, B):
     """Rows longer than one selection workgroup takes (segmented selection:
     per-segment partials, then one merge and the segment-level CDF walk), with
-    ties across segments (duplicate LM-head rows give equal logits)."""
+    ties across segments (duplicate LM-head rows give equal logits); 1024-slot
+    segments, and 2048-slot ones for rows beyond 262144 slots."""
     rng = np.random.default_rng(3)
-    V, d, B = 40000, 64, 5
+    d = 64
     Wl = torch.from_numpy(rng.standard_normal((V, d)).astype(np.float32) / 8).to(torch.bfloat16)
     Wl[30000:30005] = Wl[17:22]  # equal logits in different segments
     h = torch.from_numpy(rng.standard_normal((B, d)).astype(np.float32)).to(torch.bfloat16)
-    u = torch.tensor([0.0, 0.25, 0.5, 0.999, 0.731], dtype=torch.float32)
+    u = torch.tensor([0.0, 0.25, 0.5, 0.999, 0.731] + rng.random(B - 5).tolist(), dtype=torch.float32)
     W_np, h_np = W.host_array(Wl), W.host_array(h)
     dh = D.DenseHead(Wl.to(DEV), V, B, D.SEL_TOPK | D.SEL_SAMPLE, k_t, keep_logits=True)
     dh(h.to(DEV), u.to(DEV))
