@@ -671,12 +671,13 @@ def test_static_head_prefix(B):
 
 
 @pytest.mark.parametrize("V,B", [(40000, 5), (300000, 5), (65536, 64)])
-@pytest.mark.parametrize("k_t", [1, 10])
+@pytest.mark.parametrize("k_t", [1, 10, 16, 17, 64])
 def test_dense_head_long_rows(k_t, V, B):
     """Rows longer than one selection workgroup takes (segmented selection:
     per-segment partials, then one merge and the segment-level CDF walk), with
     ties across segments (duplicate LM-head rows give equal logits); 1024-slot
-    segments, and 2048-slot ones for rows beyond 262144 slots."""
+    segments, and 2048-slot ones for rows beyond 262144 slots; k_t up to the
+    longest top-k list."""
     rng = np.random.default_rng(3)
     d = 64
     Wl = torch.from_numpy(rng.standard_normal((V, d)).astype(np.float32) / 8).to(torch.bfloat16)
